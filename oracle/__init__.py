@@ -1,0 +1,271 @@
+"""Oracle: plain CPU reference of the demand -> plan -> pack path.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import this package.  It shares no
+code with the HIP library (``paper_2609_34340_amd``) and never imports it.
+
+The C++ source ``vp_oracle.cpp`` is compiled with g++ into
+``liboracle.so`` next to it; :func:`build` (re)compiles it.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "vp_oracle.cpp")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+OK, INVALID_ARGUMENT, INVALID_DEMAND, NO_PROGRESS, CAPACITY, UNSUPPORTED = range(6)
+PIX, PXB, NIC = 0, 1, 2
+
+DEFAULT_LAMBDA_NS = 10_000
+DEFAULT_N_START = 4
+DEFAULT_I_AA = 8
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle (single-threaded, -O2, no intrinsics)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-o", tmp, _SRC])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Topo(C.Structure):
+    _fields_ = [("n_nodes", C.c_int32), ("sockets_per_node", C.c_int32),
+                ("switches_per_socket", C.c_int32), ("gpus_per_switch", C.c_int32),
+                ("nics_per_switch", C.c_int32), ("pad", C.c_int32),
+                ("pcie_bytes_per_ns", C.c_int64), ("nic_bytes_per_ns", C.c_int64)]
+
+
+class _Params(C.Structure):
+    _fields_ = [("k_target", C.c_int64), ("lambda_ns", C.c_int64), ("unit_bytes", C.c_int64),
+                ("n_start", C.c_int32), ("i_aa", C.c_int32), ("seed", C.c_uint64)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build(force=False)
+        L = C.CDLL(_LIB)
+        vp = C.c_void_p
+        L.orc_catalog_build.argtypes = [C.POINTER(_Topo), C.c_int, C.POINTER(vp)]
+        L.orc_catalog_free.argtypes = [vp]
+        L.orc_catalog_info.argtypes = [vp, vp]
+        L.orc_catalog_table.argtypes = [vp] + [vp] * 6
+        L.orc_catalog_shapes.argtypes = [vp] + [vp] * 5
+        L.orc_catalog_families.argtypes = [vp, vp, vp, vp]
+        L.orc_catalog_cluster_family.argtypes = [vp, C.c_int32, vp, vp, vp, vp]
+        L.orc_demand.argtypes = [vp, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                 C.c_int64, vp, vp, vp, vp]
+        L.orc_demand_heads.argtypes = [C.c_int64, vp, C.c_int64, C.c_int32, C.c_int32, vp]
+        L.orc_plan.argtypes = [vp, vp, C.POINTER(_Params), C.c_int32, vp, vp, vp, vp, vp, vp,
+                               vp, C.c_int64, vp]
+        L.orc_splitmix_stream.argtypes = [C.c_uint64, vp, C.c_int32, vp]
+        L.orc_utility_greater.argtypes = [C.c_int64] * 7
+        L.orc_modeled_time.argtypes = [vp, C.c_int32, C.c_int32, vp, vp, C.c_int64, vp, vp]
+        L.orc_pack_rows.argtypes = [vp, C.c_int64, C.c_int64, vp, vp, C.c_int32, C.c_int32,
+                                    C.c_int32, vp, vp, vp, vp]
+        L.orc_pack_heads.argtypes = [vp, C.c_int64, C.c_int64, vp, C.c_int64, C.c_int32,
+                                     C.c_int32, C.c_int32, vp, vp, vp, vp]
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+class OracleError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__("%s failed with status %d" % (what, status))
+        self.status = status
+
+
+class Catalog:
+    """Oracle catalog (node-circulant, or the full Alg. 1 catalog with full=True)."""
+
+    def __init__(self, topo, full: bool = False):
+        t = _Topo(*topo.as_tuple()[:5], 0, *topo.as_tuple()[5:])
+        h = C.c_void_p()
+        st = lib().orc_catalog_build(C.byref(t), 1 if full else 0, C.byref(h))
+        if st != OK:
+            raise OracleError(st, "orc_catalog_build")
+        self._h = h
+        self.topo = topo
+        self.full = full
+        info = np.zeros(8, np.int64)
+        lib().orc_catalog_info(self._h, _p(info))
+        (self.N, self.G, self.g, self.Q, self.n_nodes, self.n_shapes, self.n_families,
+         self.n_table) = (int(x) for x in info)
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and _lib is not None:
+            _lib.orc_catalog_free(h)
+            self._h = None
+
+    def table(self):
+        n = self.n_table
+        cls, src, dst, copy = (np.zeros(n, np.int32) for _ in range(4))
+        bw = np.zeros(n, np.int64)
+        res = np.zeros((n, 2), np.int32)
+        lib().orc_catalog_table(self._h, _p(cls), _p(src), _p(dst), _p(copy), _p(bw), _p(res))
+        return dict(cls=cls, src=src, dst=dst, copy=copy, bw=bw, res=res)
+
+    def shapes(self):
+        J = self.n_shapes
+        k, fb, fe = (np.zeros(J, np.int32) for _ in range(3))
+        if self.full:
+            Lm = np.zeros((J, self.G, self.G), np.int32)
+            Rm = np.zeros((J, 1), np.int32)
+        else:
+            Lm = np.zeros((J, self.Q, self.Q), np.int32)
+            Rm = np.zeros((J, self.Q, self.Q), np.int32)
+        lib().orc_catalog_shapes(self._h, _p(k), _p(fb), _p(fe), _p(Lm), _p(Rm))
+        return dict(k=k, fam_begin=fb, fam_end=fe, L=Lm, R=Rm)
+
+    def families(self):
+        F = self.n_families
+        w = self.N if self.full else self.Q * self.g
+        shape, k = np.zeros(F, np.int32), np.zeros(F, np.int32)
+        ids = np.zeros((F, w), np.int32)
+        lib().orc_catalog_families(self._h, _p(shape), _p(k), _p(ids))
+        return dict(shape=shape, k=k, ids=ids)
+
+    def cluster_family(self, f: int):
+        n = self.N
+        cls, a, d, ids = (np.zeros(n, np.int32) for _ in range(4))
+        st = lib().orc_catalog_cluster_family(self._h, f, _p(cls), _p(a), _p(d), _p(ids))
+        if st != OK:
+            raise OracleError(st, "orc_catalog_cluster_family")
+        return dict(cls=cls, a=a, d=d, id=ids)
+
+    def plan(self, D: np.ndarray, unit: int, k_target: Optional[int] = None,
+             lambda_ns: int = DEFAULT_LAMBDA_NS, n_start: int = DEFAULT_N_START,
+             i_aa: int = DEFAULT_I_AA, seed: int = 0, k_max: Optional[int] = None,
+             trace_cap: int = 0, check: bool = True):
+        """Alg. 2 on demand D (int64 [N, N] bytes).  Returns a dict schedule."""
+        N = self.N
+        D = np.ascontiguousarray(D, dtype=np.int64)
+        assert D.shape == (N, N)
+        k_target = 2 * N if k_target is None else k_target
+        k_max = 8 * N if k_max is None else k_max
+        P = _Params(k_target, lambda_ns, unit, n_start, i_aa, seed)
+        K = np.zeros(1, np.int32)
+        cap = max(k_max, 1)
+        fam = np.full(cap, -1, np.int32)
+        dst = np.full((cap, N), -1, np.int32)
+        inst = np.full((cap, N), -1, np.int32)
+        nbytes = np.zeros((cap, N), np.int64)
+        tau = np.zeros(1, np.int64)
+        trace = np.zeros((max(trace_cap, 1), 5), np.int64)
+        tn = np.zeros(1, np.int64)
+        st = lib().orc_plan(self._h, _p(D), C.byref(P), k_max, _p(K), _p(fam), _p(dst),
+                            _p(inst), _p(nbytes), _p(tau), _p(trace) if trace_cap else None,
+                            trace_cap, _p(tn))
+        if check and st != OK:
+            raise OracleError(st, "orc_plan")
+        k = int(K[0])
+        out = dict(status=st, K=k, family=fam[:k].copy(), dst=dst[:k].copy(),
+                   inst=inst[:k].copy(), bytes=nbytes[:k].copy(), tau=int(tau[0]))
+        if trace_cap:
+            out["trace"] = trace[: int(tn[0])].copy()
+        return out
+
+    def modeled_time(self, sched, lambda_ns: int = DEFAULT_LAMBDA_NS):
+        """Eq. (2) as an exact fraction (numerator, denominator) in ns."""
+        K = int(sched["K"])
+        inst = np.ascontiguousarray(sched["inst"], np.int32)
+        nb = np.ascontiguousarray(sched["bytes"], np.int64)
+        num, den = np.zeros(1, np.int64), np.zeros(1, np.int64)
+        lib().orc_modeled_time(self._h, K, self.N, _p(inst), _p(nb), lambda_ns, _p(num), _p(den))
+        return int(num[0]), int(den[0])
+
+
+def splitmix_stream(n: int, state: int = 0, key=None) -> np.ndarray:
+    """SplitMix64 outputs from a raw state, or from the keyed state of the
+    random AA starts when key = (seed, iteration, family, start, group, side)."""
+    out = np.zeros(n, np.uint64)
+    f = None if key is None else np.asarray(key, np.uint64)
+    lib().orc_splitmix_stream(state, None if f is None else _p(f), n, _p(out))
+    return out
+
+
+def utility_greater(S1, x1, b1, S2, x2, b2, lambda_ns) -> bool:
+    """The planner's exact comparison of two Eq. (10) utilities."""
+    return bool(lib().orc_utility_greater(S1, x1, b1, S2, x2, b2, lambda_ns))
+
+
+def demand(routing: np.ndarray, n_ranks: int, n_experts: int, self_rank: int, unit: int):
+    """One source rank's demand row, expert counts, (expert, token) order and offsets."""
+    r = np.ascontiguousarray(routing, dtype=np.int32)
+    T, k = r.shape
+    row = np.zeros(n_ranks, np.int64)
+    counts = np.zeros(n_experts, np.int32)
+    order = np.zeros(T * k, np.int32)
+    off = np.zeros(n_ranks + 1, np.int64)
+    st = lib().orc_demand(_p(r), T, k, n_experts, n_ranks, self_rank, unit, _p(row), _p(counts),
+                          _p(order), _p(off))
+    if st != OK:
+        raise OracleError(st, "orc_demand")
+    return dict(row=row, counts=counts, sorted_tok=order, dest_off=off)
+
+
+def demand_heads(tokens: int, head_lo: np.ndarray, head_bytes: int, self_rank: int):
+    hl = np.ascontiguousarray(head_lo, dtype=np.int64)
+    N = hl.shape[0] - 1
+    row = np.zeros(N, np.int64)
+    st = lib().orc_demand_heads(tokens, _p(hl), head_bytes, N, self_rank, _p(row))
+    if st != OK:
+        raise OracleError(st, "orc_demand_heads")
+    return row
+
+
+def demand_matrix(rows) -> np.ndarray:
+    return np.stack(list(rows)).astype(np.int64)
+
+
+def pack_rows(tokens: np.ndarray, row_bytes: int, sorted_tok, dest_off, self_rank: int, sched):
+    tok = np.ascontiguousarray(tokens).view(np.uint8).reshape(-1)
+    T = tok.size // row_bytes
+    N = sched["dst"].shape[1] if sched["K"] else len(dest_off) - 1
+    K = int(sched["K"])
+    dst = np.ascontiguousarray(sched["dst"], np.int32)
+    nb = np.ascontiguousarray(sched["bytes"], np.int64)
+    total = int(nb[:, self_rank].sum()) if K else 0
+    send = np.zeros(total, np.uint8)
+    step_off = np.zeros(K + 1, np.int64)
+    st = lib().orc_pack_rows(_p(tok), T, row_bytes, _p(np.ascontiguousarray(sorted_tok, np.int32)),
+                             _p(np.ascontiguousarray(dest_off, np.int64)), self_rank, N, K,
+                             _p(dst), _p(nb), _p(send), _p(step_off))
+    if st != OK:
+        raise OracleError(st, "orc_pack_rows")
+    return send, step_off
+
+
+def pack_heads(act: np.ndarray, token_stride: int, head_lo, head_bytes: int, self_rank: int, sched):
+    a = np.ascontiguousarray(act).view(np.uint8).reshape(-1)
+    T = a.size // token_stride
+    hl = np.ascontiguousarray(head_lo, np.int64)
+    N = hl.shape[0] - 1
+    K = int(sched["K"])
+    dst = np.ascontiguousarray(sched["dst"], np.int32)
+    nb = np.ascontiguousarray(sched["bytes"], np.int64)
+    total = int(nb[:, self_rank].sum()) if K else 0
+    send = np.zeros(total, np.uint8)
+    step_off = np.zeros(K + 1, np.int64)
+    st = lib().orc_pack_heads(_p(a), T, token_stride, _p(hl), head_bytes, self_rank, N, K,
+                              _p(dst), _p(nb), _p(send), _p(step_off))
+    if st != OK:
+        raise OracleError(st, "orc_pack_heads")
+    return send, step_off

@@ -1,0 +1,224 @@
+"""Independent Python checkers that pin the oracle.
+
+TEST INFRASTRUCTURE ONLY.  Nothing here calls the C++ oracle's internals:
+each checker restates a property the paper fixes (channel feasibility
+Eq. (1), balance Eq. (3), family compatibility Eq. (4), schedule validity,
+the modeled completion time Eq. (2)) from an independent model of the
+topology written directly in Python, or computes a reference result by
+brute force on tiny inputs.
+
+Topology model (restated independently): rank = ((node*S + socket)*W +
+switch)*g + local; a rank group is one switch.  Directed shared resources:
+UP/DN of each switch's root-complex link, TX/RX of each switch's NIC.  Paths:
+PIX (same switch, no shared resource), PXB (same socket, different switch:
+UP(src switch), DN(dst switch)), NIC (TX(src switch), RX(dst switch)).  The
+endpoint GPU<->switch links are added as ("GU", rank) / ("GD", rank) when a
+cluster-level footprint is needed.
+"""
+from __future__ import annotations
+
+import heapq
+import itertools
+from fractions import Fraction
+from typing import Dict, List, Tuple
+
+import numpy as np
+
+PIX, PXB, NIC = 0, 1, 2
+
+
+class TopoModel:
+    def __init__(self, topo):
+        self.nn = topo.n_nodes
+        self.S = topo.sockets_per_node
+        self.W = topo.switches_per_socket
+        self.g = topo.gpus_per_switch
+        self.Q = self.S * self.W
+        self.G = self.nn * self.Q
+        self.N = self.G * self.g
+        self.pcie = topo.pcie_bytes_per_ns
+        self.nic = topo.nic_bytes_per_ns
+
+    def group(self, rank: int) -> int:
+        return rank // self.g
+
+    def node(self, group: int) -> int:
+        return group // self.Q
+
+    def socket(self, group: int) -> int:
+        return (group % self.Q) // self.W
+
+    def classes(self, a: int, d: int) -> List[int]:
+        """Path classes between group a and group d, before dominance pruning."""
+        out = []
+        if a == d:
+            out.append(PIX)
+        elif self.node(a) == self.node(d) and self.socket(a) == self.socket(d):
+            out.append(PXB)
+        out.append(NIC)
+        return out
+
+    def unpruned_classes(self, a: int, d: int) -> List[int]:
+        """Classes that survive dominance: NIC inside one switch is dominated by PIX."""
+        return [c for c in self.classes(a, d) if not (a == d and c == NIC)]
+
+    def rate(self, cls: int) -> int:
+        return min(self.pcie, self.nic) if cls == NIC else self.pcie
+
+    def shared(self, cls: int, a: int, d: int) -> Tuple:
+        if cls == PIX:
+            return ()
+        if cls == PXB:
+            return (("UP", a), ("DN", d))
+        return (("TX", a), ("RX", d))
+
+    def footprint(self, cls: int, i: int, j: int) -> Tuple:
+        """Cluster-level footprint including the endpoint GPU<->switch links."""
+        a, d = self.group(i), self.group(j)
+        return self.shared(cls, a, d) + (("GU", i), ("GD", j))
+
+
+def channel_feasible(tm: TopoModel, pi: List[int], cls: List[int]) -> bool:
+    """Eq. (1) over shared resources plus the endpoint links (no repeats)."""
+    seen = set()
+    for i, (j, c) in enumerate(zip(pi, cls)):
+        if j == i:
+            return False
+        for r in tm.footprint(c, i, j):
+            if r in seen:
+                return False
+            seen.add(r)
+    return True
+
+
+def brute_force_channels(tm: TopoModel) -> set:
+    """Every feasible rank-level channel (pi, path classes) using unpruned paths."""
+    N = tm.N
+    out = set()
+    for pi in itertools.permutations(range(N)):
+        if any(pi[i] == i for i in range(N)):
+            continue
+        options = [tm.unpruned_classes(tm.group(i), tm.group(pi[i])) for i in range(N)]
+        # incremental resource check per lane
+        def rec(i, used, cls):
+            if i == N:
+                out.add((pi, tuple(cls)))
+                return
+            for c in options[i]:
+                fp = tm.shared(c, tm.group(i), tm.group(pi[i]))
+                if any(r in used for r in fp):
+                    continue
+                rec(i + 1, used | set(fp), cls + [c])
+        rec(0, frozenset(), [])
+    return out
+
+
+def instantiate(tm: TopoModel, fam: Dict[str, np.ndarray]) -> set:
+    """All endpoint bindings of one cluster-level family (self pairs excluded)."""
+    g, G = tm.g, tm.G
+    n = len(fam["cls"])
+    outs = [[t for t in range(n) if fam["a"][t] == x] for x in range(G)]
+    ins = [[t for t in range(n) if fam["d"][t] == x] for x in range(G)]
+    perms = list(itertools.permutations(range(g)))
+    res = set()
+    for sp in itertools.product(perms, repeat=G):
+        src = [0] * n
+        for x in range(G):
+            for m, t in enumerate(outs[x]):
+                src[t] = x * g + sp[x][m]
+        for dp in itertools.product(perms, repeat=G):
+            dst = [0] * n
+            for x in range(G):
+                for m, t in enumerate(ins[x]):
+                    dst[t] = x * g + dp[x][m]
+            if any(src[t] == dst[t] for t in range(n)):
+                continue
+            pi = [0] * tm.N
+            cl = [0] * tm.N
+            for t in range(n):
+                pi[src[t]] = dst[t]
+                cl[src[t]] = int(fam["cls"][t])
+            res.add((tuple(pi), tuple(cl)))
+    return res
+
+
+def schedule_valid(tm: TopoModel, D: np.ndarray, sched, cls_of_id) -> None:
+    """Raise AssertionError unless the schedule is valid (Sec. 3 'Schedule validity')."""
+    N = tm.N
+    X = np.zeros((N, N), dtype=np.int64)
+    for k in range(sched["K"]):
+        pi = [int(x) for x in sched["dst"][k]]
+        cls = [int(cls_of_id[int(x)]) for x in sched["inst"][k]]
+        assert sorted(pi) == list(range(N)), "not a permutation"
+        for i in range(N):
+            assert cls[i] in tm.unpruned_classes(tm.group(i), tm.group(pi[i])), \
+                "lane class does not match its group pair"
+        assert channel_feasible(tm, pi, cls), "activation violates Eq. (1)"
+        x = np.asarray(sched["bytes"][k], dtype=np.int64)
+        assert (x >= 0).all()
+        X[np.arange(N), pi] += x
+    assert (X == D).all(), "activations do not reconstruct D"
+
+
+def modeled_time(tm: TopoModel, sched, cls_of_id, lam: int) -> Fraction:
+    """Eq. (2) with exact rationals."""
+    total = Fraction(0)
+    for k in range(sched["K"]):
+        worst = Fraction(0)
+        for i in range(tm.N):
+            x = int(sched["bytes"][k][i])
+            b = tm.rate(int(cls_of_id[int(sched["inst"][k][i])]))
+            worst = max(worst, Fraction(x, b))
+        total += lam + worst
+    return total
+
+
+def utility(S: int, lanes: List[Tuple[int, int]], lam: int) -> Fraction:
+    """Eq. (10): S / (lambda + max_i x_i / b_i); zero when S = 0."""
+    if S == 0:
+        return Fraction(0)
+    return Fraction(S) / (lam + max(Fraction(x, b) for x, b in lanes))
+
+
+def exhaustive_makespan(tm: TopoModel, D_units: np.ndarray, unit: int, lam: int) -> Fraction:
+    """Minimum modeled completion time over all valid schedules (tiny inputs).
+
+    Dijkstra over residual-demand states; an edge is one feasible rank-level
+    channel with any integer lane volumes (0..residual, in units) costing
+    lambda + max_i x_i / bw_i.  Zero-volume activations are never useful.
+    """
+    N = tm.N
+    chans = sorted(brute_force_channels(tm))
+    start = tuple(int(v) for v in D_units.reshape(-1))
+    best = {start: Fraction(0)}
+    heap = [(Fraction(0), start)]
+    while heap:
+        cost, st = heapq.heappop(heap)
+        if best.get(st, None) != cost:
+            continue
+        if not any(st):
+            return cost
+        R = np.array(st, dtype=np.int64).reshape(N, N)
+        seen_moves = set()
+        for pi, cl in chans:
+            lanes = [(i, pi[i], cl[i]) for i in range(N) if R[i, pi[i]] > 0]
+            if not lanes:
+                continue
+            ranges = [range(0, int(R[i, j]) + 1) for i, j, _ in lanes]
+            for xs in itertools.product(*ranges):
+                if not any(xs):
+                    continue
+                key = tuple(sorted((i, j, c, x) for (i, j, c), x in zip(lanes, xs) if x))
+                if key in seen_moves:
+                    continue
+                seen_moves.add(key)
+                dur = max(Fraction(x * unit, tm.rate(c)) for (i, j, c), x in zip(lanes, xs) if x)
+                nst = list(st)
+                for (i, j, c), x in zip(lanes, xs):
+                    nst[i * N + j] -= x
+                nst = tuple(nst)
+                nc = cost + lam + dur
+                if nc < best.get(nst, None) if nst in best else True:
+                    best[nst] = nc
+                    heapq.heappush(heap, (nc, nst))
+    raise RuntimeError("unreachable")

@@ -1,0 +1,1078 @@
+// ORACLE -- TEST INFRASTRUCTURE ONLY.
+//
+// A plain, slow, single-threaded CPU implementation of the demand -> plan ->
+// pack path of VarioPath (arxiv 2609.34340), written from the paper.  Only the
+// tests, the smoke check and the benchmark's CPU-baseline leg may load it.  It
+// shares no code, header, table or helper with the HIP library; the two meet
+// only at the seeded inputs.  Every function names the passage it follows.
+//
+// Where the paper fixes a result by a plain definition (the demand matrix,
+// the send-buffer layout, the modeled completion time) the code is that
+// definition written out.  The catalog (Alg. 1) and the scheduler (Alg. 2)
+// are heuristic/enumerative: they follow the algorithms' steps in the paper's
+// order and notation, with every choice the paper leaves open fixed by the
+// readings listed in the design notes (topology model, PIX multiplicity,
+// node-circulant reduction, canonical order, integer credit, start rule,
+// counter-based randomness, exact utility comparison).
+//
+// Arithmetic: int64 bytes and nanoseconds; utilities are compared exactly by
+// cross-multiplication in unsigned 128-bit.  No floating point on the path.
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <set>
+#include <tuple>
+#include <vector>
+
+namespace {
+
+typedef int64_t i64;
+typedef unsigned __int128 u128;
+
+enum Status { OK = 0, INVALID_ARGUMENT = 1, INVALID_DEMAND = 2, NO_PROGRESS = 3,
+              CAPACITY = 4, UNSUPPORTED = 5 };
+enum Cls { PIX = 0, PXB = 1, NIC = 2 };
+
+struct Topo {
+  int n_nodes, sockets, switches, g, nics;
+  i64 pcie, nic;
+  int Q() const { return sockets * switches; }        // switch slots per node
+  int G() const { return n_nodes * Q(); }              // rank groups (one per switch)
+  int N() const { return G() * g; }                    // ranks
+};
+
+// ---------------------------------------------------------------------------
+// Group-level path instances (Sec. 4.1 "Topology abstraction"; Sec. 3 model
+// setup).  Directed resources: per switch x, the uplink UP_x and downlink DN_x
+// between the switch and its root complex; per NIC, TX_x and RX_x.  GPU<->switch
+// links are endpoint-local and not modeled.  Path classes: PIX (same switch,
+// no shared resource), PXB (same socket, other switch: UP_src, DN_dst) and NIC
+// (any pair through the source switch's NIC and the destination switch's NIC:
+// TX_src, RX_dst).  A path's rate is the minimum of its links.
+// ---------------------------------------------------------------------------
+struct Inst {
+  int id;          // canonical id (order of (cls, src, dst, copy))
+  int cls;
+  int a, d;        // source / destination group (slot for node-local sets)
+  int copy;
+  bool remote;     // NIC lane to another node (node-circulant sets only)
+  i64 bw;
+  std::vector<int> L;   // sorted resource ids
+};
+
+i64 rate_of(const Topo& t, int cls) {
+  return cls == NIC ? std::min(t.pcie, t.nic) : t.pcie;
+}
+
+// Node-local instance table shared by the k = 0 (intra-node) and k != 0
+// (remote) sets: PIX copies, PXB, and NIC for every slot pair.  Resource ids:
+// UP q -> q, DN q -> Q+q, TX q -> 2Q+q, RX q -> 3Q+q.
+std::vector<Inst> local_table(const Topo& t) {
+  const int Q = t.Q();
+  std::vector<Inst> v;
+  for (int q = 0; q < Q; ++q)
+    for (int c = 0; c < t.g; ++c)
+      v.push_back({0, PIX, q, q, c, false, rate_of(t, PIX), {}});
+  for (int q = 0; q < Q; ++q)
+    for (int q2 = 0; q2 < Q; ++q2)
+      if (q != q2 && q / t.switches == q2 / t.switches)
+        v.push_back({0, PXB, q, q2, 0, false, rate_of(t, PXB), {q, Q + q2}});
+  if (t.nics > 0)
+    for (int q = 0; q < Q; ++q)
+      for (int q2 = 0; q2 < Q; ++q2)
+        v.push_back({0, NIC, q, q2, 0, false, rate_of(t, NIC), {2 * Q + q, 3 * Q + q2}});
+  std::sort(v.begin(), v.end(), [](const Inst& x, const Inst& y) {
+    return std::make_tuple(x.cls, x.a, x.d, x.copy) < std::make_tuple(y.cls, y.a, y.d, y.copy);
+  });
+  for (size_t i = 0; i < v.size(); ++i) v[i].id = (int)i;
+  return v;
+}
+
+// Cluster-level instance set over all G groups (used for the full, unreduced
+// Alg. 1 catalog of small topologies).  Resource ids: UP a -> a, DN a -> G+a,
+// TX a -> 2G+a, RX a -> 3G+a.
+std::vector<Inst> cluster_table(const Topo& t) {
+  const int G = t.G(), Q = t.Q();
+  std::vector<Inst> v;
+  for (int a = 0; a < G; ++a)
+    for (int c = 0; c < t.g; ++c)
+      v.push_back({0, PIX, a, a, c, false, rate_of(t, PIX), {}});
+  for (int a = 0; a < G; ++a)
+    for (int d = 0; d < G; ++d) {
+      bool same_node = a / Q == d / Q;
+      bool same_socket = same_node && (a % Q) / t.switches == (d % Q) / t.switches;
+      if (a != d && same_socket)
+        v.push_back({0, PXB, a, d, 0, false, rate_of(t, PXB), {a, G + d}});
+    }
+  if (t.nics > 0)
+    for (int a = 0; a < G; ++a)
+      for (int d = 0; d < G; ++d)
+        v.push_back({0, NIC, a, d, 0, false, rate_of(t, NIC), {2 * G + a, 3 * G + d}});
+  std::sort(v.begin(), v.end(), [](const Inst& x, const Inst& y) {
+    return std::make_tuple(x.cls, x.a, x.d, x.copy) < std::make_tuple(y.cls, y.a, y.d, y.copy);
+  });
+  for (size_t i = 0; i < v.size(); ++i) v[i].id = (int)i;
+  return v;
+}
+
+bool subset_of(const std::vector<int>& x, const std::vector<int>& y) {
+  return std::includes(y.begin(), y.end(), x.begin(), x.end());
+}
+
+// PrunePaths (Sec. 4.1 "Pruning and search cost"): drop r when another r' of
+// the same ordered group pair has L(r') subset of L(r) and bw(r') >= bw(r), one
+// of them strict.
+std::vector<Inst> prune_paths(const std::vector<Inst>& R) {
+  std::vector<Inst> out;
+  for (size_t x = 0; x < R.size(); ++x) {
+    bool dominated = false;
+    for (size_t y = 0; y < R.size() && !dominated; ++y) {
+      if (x == y) continue;
+      const Inst& r = R[x];
+      const Inst& rp = R[y];
+      if (rp.a != r.a || rp.d != r.d || rp.remote != r.remote) continue;
+      bool sub = subset_of(rp.L, r.L);
+      bool strict_sub = sub && rp.L.size() < r.L.size();
+      if (sub && rp.bw >= r.bw && (strict_sub || rp.bw > r.bw)) dominated = true;
+    }
+    if (!dominated) out.push_back(R[x]);
+  }
+  return out;
+}
+
+// ---------------------------------------------------------------------------
+// Alg. 1: pruned binary DFS over the ordered instances.  Explore(t, B): if B
+// is complete, insert it into the bucket of its shape; otherwise stop when t
+// runs past the list or SuffixOK fails; explore the exclude branch first,
+// then the include branch when CanAdd holds.
+// ---------------------------------------------------------------------------
+struct Dfs {
+  const std::vector<Inst>& R;
+  int n_groups, g;
+  std::vector<int> outd, ind, used_res;
+  std::vector<std::vector<int>> suf_out, suf_in;   // remaining instances per group from t on
+  std::vector<int> B;
+  std::vector<std::vector<int>> found;
+
+  Dfs(const std::vector<Inst>& R_, int n_groups_, int g_, int n_res)
+      : R(R_), n_groups(n_groups_), g(g_), outd(n_groups_, 0), ind(n_groups_, 0),
+        used_res(n_res, 0) {
+    const size_t m = R.size();
+    suf_out.assign(m + 1, std::vector<int>(n_groups, 0));
+    suf_in.assign(m + 1, std::vector<int>(n_groups, 0));
+    for (size_t t = m; t-- > 0;) {
+      suf_out[t] = suf_out[t + 1];
+      suf_in[t] = suf_in[t + 1];
+      suf_out[t][R[t].a]++;
+      suf_in[t][R[t].d]++;
+    }
+  }
+  bool complete() const {
+    for (int x = 0; x < n_groups; ++x)
+      if (outd[x] != g || ind[x] != g) return false;
+    return true;
+  }
+  // SuffixOK: the instances not yet decided must be able to fill every
+  // group's remaining outgoing and incoming slots.
+  bool suffix_ok(size_t t) const {
+    for (int x = 0; x < n_groups; ++x)
+      if (outd[x] + suf_out[t][x] < g || ind[x] + suf_in[t][x] < g) return false;
+    return true;
+  }
+  // CanAdd: resource-disjoint and within the group-degree limits.
+  bool can_add(const Inst& r) const {
+    if (outd[r.a] >= g || ind[r.d] >= g) return false;
+    for (int l : r.L)
+      if (used_res[l]) return false;
+    return true;
+  }
+  void explore(size_t t) {
+    if (complete()) {
+      found.push_back(B);
+      return;
+    }
+    if (t >= R.size() || !suffix_ok(t)) return;
+    explore(t + 1);
+    const Inst& r = R[t];
+    if (can_add(r)) {
+      outd[r.a]++;
+      ind[r.d]++;
+      for (int l : r.L) used_res[l] = 1;
+      B.push_back((int)t);
+      explore(t + 1);
+      B.pop_back();
+      for (int l : r.L) used_res[l] = 0;
+      outd[r.a]--;
+      ind[r.d]--;
+    }
+  }
+};
+
+// A family as the canonical ids of its instances (ascending).
+typedef std::vector<int> Fam;
+
+// Shape of a family: lane counts per (src group, dst group, remote flag).
+typedef std::vector<int> ShapeKey;
+
+// PruneFamilies (Sec. 4.1): inside one shape bucket, remove exact duplicates
+// and families dominated by another (instances paired inside every group pair
+// with identical footprints and no lower rate, one strictly higher).
+std::vector<Fam> prune_families(std::vector<Fam> fams, const std::vector<Inst>& table) {
+  std::sort(fams.begin(), fams.end());
+  typedef std::tuple<int, int, bool, std::vector<int>, i64> Sig;
+  auto signature = [&](const Fam& f) {
+    std::vector<Sig> s;
+    for (int id : f) {
+      const Inst& r = table[id];
+      s.emplace_back(r.a, r.d, r.remote, r.L, r.bw);
+    }
+    std::sort(s.begin(), s.end());
+    return s;
+  };
+  std::vector<Fam> uniq;
+  std::set<std::vector<Sig>> seen;
+  for (const Fam& f : fams) {
+    auto s = signature(f);
+    if (seen.insert(s).second) uniq.push_back(f);
+  }
+  // dominance: per (group pair, footprint) the rates must be pairable with
+  // no lower rate; at least one strictly higher overall.
+  auto dominates = [&](const Fam& f1, const Fam& f2) {
+    typedef std::tuple<int, int, bool, std::vector<int>> Key;
+    std::map<Key, std::vector<i64>> r1, r2;
+    for (int id : f1) { const Inst& r = table[id]; r1[Key(r.a, r.d, r.remote, r.L)].push_back(r.bw); }
+    for (int id : f2) { const Inst& r = table[id]; r2[Key(r.a, r.d, r.remote, r.L)].push_back(r.bw); }
+    if (r1.size() != r2.size()) return false;
+    bool strict = false;
+    for (auto& kv : r1) {
+      auto it = r2.find(kv.first);
+      if (it == r2.end() || it->second.size() != kv.second.size()) return false;
+      std::vector<i64> x = kv.second, y = it->second;
+      std::sort(x.rbegin(), x.rend());
+      std::sort(y.rbegin(), y.rend());
+      for (size_t i = 0; i < x.size(); ++i) {
+        if (x[i] < y[i]) return false;
+        if (x[i] > y[i]) strict = true;
+      }
+    }
+    return strict;
+  };
+  std::vector<Fam> out;
+  for (size_t i = 0; i < uniq.size(); ++i) {
+    bool dom = false;
+    for (size_t j = 0; j < uniq.size() && !dom; ++j)
+      if (i != j && dominates(uniq[j], uniq[i])) dom = true;
+    if (!dom) out.push_back(uniq[i]);
+  }
+  return out;
+}
+
+// Run Alg. 1 on one instance set and return the buckets (shape -> families).
+std::map<ShapeKey, std::vector<Fam>> run_alg1(const std::vector<Inst>& table,
+                                               const std::vector<Inst>& candidates,
+                                               int n_groups, int g, int n_res) {
+  std::vector<Inst> R = prune_paths(candidates);
+  // fixed order r_1..r_m: ascending canonical id
+  std::sort(R.begin(), R.end(), [](const Inst& x, const Inst& y) { return x.id < y.id; });
+  Dfs dfs(R, n_groups, g, n_res);
+  dfs.explore(0);
+  std::map<ShapeKey, std::vector<Fam>> buckets;
+  for (const auto& B : dfs.found) {
+    ShapeKey M(2 * n_groups * n_groups, 0);
+    Fam f;
+    for (int t : B) {
+      const Inst& r = R[t];
+      M[(r.remote ? n_groups * n_groups : 0) + r.a * n_groups + r.d]++;
+      f.push_back(r.id);
+    }
+    std::sort(f.begin(), f.end());
+    buckets[M].push_back(f);
+  }
+  for (auto& kv : buckets) kv.second = prune_families(kv.second, table);
+  return buckets;
+}
+
+// ---------------------------------------------------------------------------
+// Catalog at cluster level: what Alg. 2 consumes.
+// ---------------------------------------------------------------------------
+struct CInst {
+  int a, d;      // source / destination group
+  int cls;
+  i64 bw;
+  int id;        // instance id recorded in the schedule
+};
+struct CFamily {
+  int shape;
+  int k;                       // node shift (node-circulant catalogs)
+  std::vector<int> local;      // node-local instance ids (node-circulant catalogs)
+  std::vector<CInst> inst;     // N instances in family order
+};
+struct CShape {
+  int k;
+  std::vector<int> Lm, Rm;                        // Q x Q block counts (circulant)
+  std::vector<std::tuple<int, int, int>> M;       // nonzero (a, d, M_ad)
+  std::vector<int> dense;                         // G x G (full catalogs only)
+  int fam_begin, fam_end;
+};
+
+struct Catalog {
+  Topo topo;
+  bool circulant;
+  std::vector<Inst> table;       // instance table (node-local or cluster)
+  std::vector<CShape> shapes;
+  std::vector<CFamily> fams;
+  i64 bw_max;
+};
+
+// Node-circulant catalog: a family is (k, B_loc): the same node-local pattern
+// in every node, NIC lanes of node n landing on node (n + k) mod n_nodes; k = 0
+// holds every family whose NIC lanes (if any) stay inside the node.  With one
+// node this is exactly Alg. 1's catalog.
+void build_circulant(Catalog& C) {
+  const Topo& t = C.topo;
+  const int Q = t.Q(), g = t.g, nn = t.n_nodes;
+  C.table = local_table(t);
+  const int n_res = 4 * Q;
+  // k = 0 set: PIX, PXB, NIC between slots of the same node (loopback).
+  std::vector<Inst> set0;
+  for (Inst r : C.table) { r.remote = false; set0.push_back(r); }
+  auto b0 = run_alg1(C.table, set0, Q, g, n_res);
+  // k != 0 set: PIX, PXB, and NIC lanes to the same slot pattern on another node.
+  std::map<ShapeKey, std::vector<Fam>> b1;
+  if (nn > 1) {
+    std::vector<Inst> set1;
+    for (Inst r : C.table) { r.remote = (r.cls == NIC); set1.push_back(r); }
+    std::vector<Inst> table1 = set1;
+    auto all1 = run_alg1(table1, set1, Q, g, n_res);
+    for (auto& kv : all1) {
+      std::vector<Fam> keep;
+      for (const Fam& f : kv.second) {
+        bool has_nic = false;
+        for (int id : f) has_nic |= C.table[id].cls == NIC;
+        if (has_nic) keep.push_back(f);       // NIC-free families live under k = 0
+      }
+      if (!keep.empty()) b1[kv.first] = keep;
+    }
+  }
+  // Canonical order: shapes by (k, diagonal-block counts, shift-block counts),
+  // families by their sorted instance ids.  std::map keys are the row-major
+  // (diagonal block, shift block) counts, so iteration order is canonical.
+  auto emit = [&](int k, const std::map<ShapeKey, std::vector<Fam>>& b) {
+    for (const auto& kv : b) {
+      CShape s;
+      s.k = k;
+      s.Lm.assign(kv.first.begin(), kv.first.begin() + Q * Q);
+      s.Rm.assign(kv.first.begin() + Q * Q, kv.first.end());
+      std::map<std::pair<int, int>, int> m;
+      for (int n = 0; n < nn; ++n)
+        for (int q = 0; q < Q; ++q)
+          for (int q2 = 0; q2 < Q; ++q2) {
+            if (s.Lm[q * Q + q2]) m[{n * Q + q, n * Q + q2}] += s.Lm[q * Q + q2];
+            if (s.Rm[q * Q + q2]) m[{n * Q + q, ((n + k) % nn) * Q + q2}] += s.Rm[q * Q + q2];
+          }
+      for (auto& e : m) s.M.emplace_back(e.first.first, e.first.second, e.second);
+      s.fam_begin = (int)C.fams.size();
+      std::vector<Fam> fs = kv.second;
+      std::sort(fs.begin(), fs.end());
+      for (const Fam& f : fs) {
+        CFamily F;
+        F.shape = (int)C.shapes.size();
+        F.k = k;
+        F.local = f;
+        for (int n = 0; n < nn; ++n)
+          for (int id : f) {
+            const Inst& r = C.table[id];
+            int dn = (r.cls == NIC && k != 0) ? (n + k) % nn : n;
+            F.inst.push_back({n * Q + r.a, dn * Q + r.d, r.cls, r.bw, id});
+          }
+        C.fams.push_back(F);
+      }
+      s.fam_end = (int)C.fams.size();
+      C.shapes.push_back(s);
+    }
+  };
+  emit(0, b0);
+  for (int k = 1; k < nn; ++k) emit(k, b1);
+}
+
+// Full Alg. 1 over the cluster-level instance set (small topologies only).
+void build_full(Catalog& C) {
+  const Topo& t = C.topo;
+  const int G = t.G();
+  C.table = cluster_table(t);
+  auto b = run_alg1(C.table, C.table, G, t.g, 4 * G);
+  for (const auto& kv : b) {
+    CShape s;
+    s.k = -1;
+    s.dense.assign(kv.first.begin(), kv.first.begin() + G * G);
+    for (int a = 0; a < G; ++a)
+      for (int d = 0; d < G; ++d)
+        if (s.dense[a * G + d]) s.M.emplace_back(a, d, s.dense[a * G + d]);
+    s.fam_begin = (int)C.fams.size();
+    for (const Fam& f : kv.second) {
+      CFamily F;
+      F.shape = (int)C.shapes.size();
+      F.k = -1;
+      F.local = f;
+      for (int id : f) {
+        const Inst& r = C.table[id];
+        F.inst.push_back({r.a, r.d, r.cls, r.bw, id});
+      }
+      C.fams.push_back(F);
+    }
+    s.fam_end = (int)C.fams.size();
+    C.shapes.push_back(s);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Counter-based randomness for the random AA starts: SplitMix64 (Steele, Lea
+// and Flood, OOPSLA 2014).  The key absorbs (seed, iteration, family, start,
+// group, side) one field at a time; the stream then steps the SplitMix64 state.
+// ---------------------------------------------------------------------------
+const uint64_t GOLDEN = 0x9E3779B97F4A7C15ULL;
+uint64_t sm_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+struct SplitMix {
+  uint64_t state;
+  uint64_t next() { state += GOLDEN; return sm_mix(state); }
+};
+SplitMix keyed_stream(uint64_t seed, uint64_t iter, uint64_t fam, uint64_t start,
+                      uint64_t group, uint64_t side) {
+  uint64_t key = seed;
+  const uint64_t fields[5] = {iter, fam, start, group, side};
+  for (uint64_t v : fields) key = sm_mix(key + GOLDEN) ^ v;
+  return SplitMix{key};
+}
+
+// ---------------------------------------------------------------------------
+// Alg. 2: online channel-guided demand decomposition.
+// ---------------------------------------------------------------------------
+struct Params {
+  i64 k_target, lambda_ns, unit;
+  int n_start, i_aa;
+  uint64_t seed;
+};
+
+struct Planner {
+  const Catalog& C;
+  const Params& P;
+  int N, G, g;
+  std::vector<i64> Drem;           // D^rem, row-major N x N bytes
+  i64 tau;
+  i64 K;                           // activations emitted so far
+  // optional trace of F after every AA half-step: (iter, family, start, half, F)
+  i64* trace;
+  i64 trace_cap, trace_n;
+
+  Planner(const Catalog& C_, const Params& P_) : C(C_), P(P_) {
+    N = C.topo.N();
+    G = C.topo.G();
+    g = C.topo.g;
+    trace = nullptr;
+    trace_cap = trace_n = 0;
+    K = 0;
+    tau = 1;
+  }
+
+  // Capacity of a path within one quantum, rounded down to whole units
+  // (at least one unit): the integer form of tau * bw(p) in Eq. (9).
+  i64 cap(i64 bw) const {
+    i64 c = (tau * bw) / P.unit * P.unit;
+    return c < P.unit ? P.unit : c;
+  }
+
+  // Binding credit, Eq. (7), scaled by tau: h' = min(D^rem_ij, tau*bw(r)).
+  // Self pairs lie outside Gamma_ad and are never bound.
+  i64 credit(const CInst& r, int i, int j) const {
+    i64 dv = Drem[(size_t)i * N + j];
+    i64 c = cap(r.bw);
+    return dv < c ? dv : c;
+  }
+
+  struct Binding { std::vector<int> src, dst; };
+
+  // Out-instances / in-instances of every group, in family order.
+  void group_lists(const CFamily& F, std::vector<std::vector<int>>& outs,
+                   std::vector<std::vector<int>>& ins) const {
+    outs.assign(G, {});
+    ins.assign(G, {});
+    for (int t = 0; t < (int)F.inst.size(); ++t) {
+      outs[F.inst[t].a].push_back(t);
+      ins[F.inst[t].d].push_back(t);
+    }
+  }
+
+  // Binding score, Eq. (8): sum of the bound credits.
+  i64 score(const CFamily& F, const Binding& b) const {
+    i64 s = 0;
+    for (int t = 0; t < (int)F.inst.size(); ++t) s += credit(F.inst[t], b.src[t], b.dst[t]);
+    return s;
+  }
+
+  // Make the binding self-transfer free (Gamma_ad excludes i == j): for every
+  // group, walk its intra-group instances in family order; a self-bound one
+  // trades destinations with the first other in-instance of the group that is
+  // not protected, or, failing that, sources with the first other unprotected
+  // out-instance.  A trade never creates a new self-binding.
+  void repair(const CFamily& F, Binding& b, int protect,
+              const std::vector<std::vector<int>>& outs,
+              const std::vector<std::vector<int>>& ins) const {
+    for (int a = 0; a < G; ++a) {
+      for (int r : outs[a]) {
+        if (F.inst[r].d != a || b.src[r] != b.dst[r]) continue;
+        int partner = -1;
+        for (int r2 : ins[a])
+          if (r2 != r && r2 != protect) { partner = r2; break; }
+        if (partner >= 0) {
+          std::swap(b.dst[r], b.dst[partner]);
+          continue;
+        }
+        for (int r3 : outs[a])
+          if (r3 != r && r3 != protect) { partner = r3; break; }
+        if (partner >= 0) std::swap(b.src[r], b.src[partner]);
+      }
+    }
+  }
+
+  // Start 0: the canonical binding (the g out-instances of group a take
+  // sources a*g+0.., the g in-instances of group d take destinations d*g+0..,
+  // both in family order) with the single highest-credit triple (t, i, j)
+  // forced in; ties go to the smallest (t, i, j).
+  Binding start_forced(const CFamily& F, const std::vector<std::vector<int>>& outs,
+                       const std::vector<std::vector<int>>& ins) const {
+    const int n = (int)F.inst.size();
+    Binding b;
+    b.src.assign(n, -1);
+    b.dst.assign(n, -1);
+    for (int a = 0; a < G; ++a)
+      for (int m = 0; m < (int)outs[a].size(); ++m) b.src[outs[a][m]] = a * g + m;
+    for (int d = 0; d < G; ++d)
+      for (int m = 0; m < (int)ins[d].size(); ++m) b.dst[ins[d][m]] = d * g + m;
+    i64 best = 0;
+    int bt = -1, bi = -1, bj = -1;
+    for (int t = 0; t < n; ++t)
+      for (int il = 0; il < g; ++il)
+        for (int jl = 0; jl < g; ++jl) {
+          int i = F.inst[t].a * g + il, j = F.inst[t].d * g + jl;
+          if (i == j) continue;
+          i64 h = credit(F.inst[t], i, j);
+          if (h > best) { best = h; bt = t; bi = i; bj = j; }
+        }
+    int protect = -1;
+    if (bt >= 0) {
+      for (int t2 : outs[F.inst[bt].a])
+        if (b.src[t2] == bi) { std::swap(b.src[t2], b.src[bt]); break; }
+      for (int t3 : ins[F.inst[bt].d])
+        if (b.dst[t3] == bj) { std::swap(b.dst[t3], b.dst[bt]); break; }
+      protect = bt;
+    }
+    repair(F, b, protect, outs, ins);
+    return b;
+  }
+
+  // Starts 1..N_start-1: an independent Fisher-Yates shuffle of every group's
+  // sources and of every group's destinations, then the self-binding repair.
+  Binding start_random(const CFamily& F, int fam_index, int s,
+                       const std::vector<std::vector<int>>& outs,
+                       const std::vector<std::vector<int>>& ins) const {
+    const int n = (int)F.inst.size();
+    Binding b;
+    b.src.assign(n, -1);
+    b.dst.assign(n, -1);
+    for (int side = 0; side < 2; ++side)
+      for (int x = 0; x < G; ++x) {
+        SplitMix rng = keyed_stream(P.seed, (uint64_t)K, (uint64_t)fam_index, (uint64_t)s,
+                                    (uint64_t)x, (uint64_t)side);
+        std::vector<int> perm(g);
+        for (int m = 0; m < g; ++m) perm[m] = m;
+        for (int m = g - 1; m >= 1; --m) {
+          int j = (int)(rng.next() % (uint64_t)(m + 1));
+          std::swap(perm[m], perm[j]);
+        }
+        const std::vector<int>& lst = side == 0 ? outs[x] : ins[x];
+        for (int m = 0; m < (int)lst.size(); ++m) {
+          if (side == 0) b.src[lst[m]] = x * g + perm[m];
+          else b.dst[lst[m]] = x * g + perm[m];
+        }
+      }
+    repair(F, b, -1, outs, ins);
+    return b;
+  }
+
+  // One half of an AA sweep for one group: with the other side fixed, try
+  // every assignment of the group's g ranks to its g instances (lexicographic
+  // order of the rank tuple), skip those that bind a rank to itself, and take
+  // the first best one if it strictly beats the current assignment.
+  bool improve_group(const CFamily& F, Binding& b, const std::vector<int>& lst, int x,
+                     bool source_side) const {
+    std::vector<int> perm(g);
+    for (int m = 0; m < g; ++m) perm[m] = m;
+    i64 cur = 0;
+    for (int t : lst) cur += credit(F.inst[t], b.src[t], b.dst[t]);
+    i64 best = -1;
+    std::vector<int> best_perm;
+    do {
+      bool ok = true;
+      i64 v = 0;
+      for (int m = 0; m < g && ok; ++m) {
+        int t = lst[m];
+        int i = source_side ? x * g + perm[m] : b.src[t];
+        int j = source_side ? b.dst[t] : x * g + perm[m];
+        if (i == j) { ok = false; break; }
+        v += credit(F.inst[t], i, j);
+      }
+      if (ok && v > best) { best = v; best_perm = perm; }
+    } while (std::next_permutation(perm.begin(), perm.end()));
+    if (best > cur) {
+      for (int m = 0; m < g; ++m) {
+        if (source_side) b.src[lst[m]] = x * g + best_perm[m];
+        else b.dst[lst[m]] = x * g + best_perm[m];
+      }
+      return true;
+    }
+    return false;
+  }
+
+  void log(int f, int s, int half, i64 F) {
+    if (!trace || trace_n >= trace_cap) return;
+    i64* e = trace + 5 * trace_n;
+    e[0] = K; e[1] = f; e[2] = s; e[3] = half; e[4] = F;
+    ++trace_n;
+  }
+
+  // Alternating Algorithm (Sec. 4.2 Step 2): source half, then destination
+  // half; each solves one g x g assignment per group without decreasing F_B.
+  // Stop after I_AA sweeps or after a sweep that changes nothing.
+  void alternating(const CFamily& F, int f, int s, Binding& b,
+                   const std::vector<std::vector<int>>& outs,
+                   const std::vector<std::vector<int>>& ins) {
+    log(f, s, 0, score(F, b));
+    for (int sweep = 0; sweep < P.i_aa; ++sweep) {
+      bool changed = false;
+      for (int a = 0; a < G; ++a) changed |= improve_group(F, b, outs[a], a, true);
+      log(f, s, 2 * sweep + 1, score(F, b));
+      for (int d = 0; d < G; ++d) changed |= improve_group(F, b, ins[d], d, false);
+      log(f, s, 2 * sweep + 2, score(F, b));
+      if (!changed) break;
+    }
+  }
+
+  // MultiStartAA: run AA from N_start feasible bindings and keep the highest
+  // F_B (ties to the earliest start).
+  Binding multistart_aa(const CFamily& F, int f) {
+    std::vector<std::vector<int>> outs, ins;
+    group_lists(F, outs, ins);
+    Binding best;
+    i64 bestF = -1;
+    for (int s = 0; s < P.n_start; ++s) {
+      Binding b = s == 0 ? start_forced(F, outs, ins) : start_random(F, f, s, outs, ins);
+      alternating(F, f, s, b, outs, ins);
+      i64 Fb = score(F, b);
+      if (Fb > bestF) { bestF = Fb; best = b; }
+    }
+    return best;
+  }
+
+  // Evaluate (Sec. 4.2 Step 3): lane volumes by Eq. (9) and the utility of
+  // Eq. (10) kept as (S, x, b) with U = S / (lambda + x / b).
+  struct Eval { std::vector<i64> x; i64 S, xm, bm; };
+  Eval evaluate(const CFamily& F, const Binding& b) const {
+    Eval e;
+    const int n = (int)F.inst.size();
+    e.x.assign(n, 0);
+    e.S = 0;
+    e.xm = 0;
+    e.bm = 1;
+    std::vector<int> by_rank(N, -1);
+    for (int t = 0; t < n; ++t) {
+      i64 c = cap(F.inst[t].bw);
+      i64 dv = Drem[(size_t)b.src[t] * N + b.dst[t]];
+      e.x[t] = c < dv ? c : dv;
+      e.S += e.x[t];
+      by_rank[b.src[t]] = t;
+    }
+    for (int i = 0; i < N; ++i) {        // slowest lane; ties to the lowest rank
+      int t = by_rank[i];
+      if ((u128)e.x[t] * (u128)e.bm > (u128)e.xm * (u128)F.inst[t].bw) {
+        e.xm = e.x[t];
+        e.bm = F.inst[t].bw;
+      }
+    }
+    return e;
+  }
+
+  // U_1 > U_2 exactly.  U = 0 when S = 0.
+  bool better(const Eval& e1, const Eval& e2) const {
+    if (e1.S == 0) return false;
+    if (e2.S == 0) return true;
+    u128 lam = (u128)P.lambda_ns;
+    u128 lhs = (u128)e1.S * (u128)e1.bm * (lam * (u128)e2.bm + (u128)e2.xm);
+    u128 rhs = (u128)e2.S * (u128)e2.bm * (lam * (u128)e1.bm + (u128)e1.xm);
+    return lhs > rhs;
+  }
+
+  int run(const i64* D, int32_t* Kout, int32_t* fam, int32_t* dst, int32_t* inst,
+          i64* bytes, int k_max, i64* tau_out) {
+    const size_t NN = (size_t)N * N;
+    Drem.assign(D, D + NN);
+    *Kout = 0;
+    for (int i = 0; i < N; ++i)
+      for (int j = 0; j < N; ++j) {
+        i64 v = Drem[(size_t)i * N + j];
+        if (v < 0 || v % P.unit != 0 || (i == j && v != 0)) return INVALID_DEMAND;
+      }
+    // Global time quantum (Sec. 5 "Global execution granularity"): the most
+    // loaded rank drains in about K_target quanta at the fastest path rate.
+    i64 Lmax = 0;
+    for (int i = 0; i < N; ++i) {
+      i64 row = 0, col = 0;
+      for (int j = 0; j < N; ++j) {
+        row += Drem[(size_t)i * N + j];
+        col += Drem[(size_t)j * N + i];
+      }
+      Lmax = std::max(Lmax, std::max(row, col));
+    }
+    i64 denom = C.bw_max * P.k_target;
+    tau = (Lmax + denom - 1) / denom;
+    if (tau < 1) tau = 1;
+    if (tau_out) *tau_out = tau;
+    K = 0;
+    auto remaining = [&]() {
+      i64 s = 0;
+      for (size_t x = 0; x < NN; ++x) s += Drem[x];
+      return s;
+    };
+    while (remaining() > 0) {
+      if (K >= k_max) return CAPACITY;
+      // Step 1: group demand, Eq. (5), and the best shape, Eq. (6).
+      std::vector<i64> Dhat((size_t)G * G, 0);
+      for (int i = 0; i < N; ++i)
+        for (int j = 0; j < N; ++j) Dhat[(size_t)(i / g) * G + j / g] += Drem[(size_t)i * N + j];
+      int Mstar = -1;
+      i64 sbest = -1;
+      for (int m = 0; m < (int)C.shapes.size(); ++m) {
+        i64 s = 0;
+        for (const auto& e : C.shapes[m].M)
+          s += Dhat[(size_t)std::get<0>(e) * G + std::get<1>(e)] * std::get<2>(e);
+        if (s > sbest) { sbest = s; Mstar = m; }
+      }
+      if (Mstar < 0 || sbest <= 0) return NO_PROGRESS;
+      // Steps 2-3: bind and evaluate every family of the chosen shape.
+      const CShape& sh = C.shapes[Mstar];
+      int fbest = -1;
+      Binding bbest;
+      Eval ebest;
+      for (int f = sh.fam_begin; f < sh.fam_end; ++f) {
+        Binding b = multistart_aa(C.fams[f], f);
+        Eval e = evaluate(C.fams[f], b);
+        if (fbest < 0 || better(e, ebest)) { fbest = f; bbest = b; ebest = e; }
+      }
+      if (fbest < 0 || ebest.S == 0) return NO_PROGRESS;
+      // Append E* and subtract X(E*) from D^rem.
+      const CFamily& F = C.fams[fbest];
+      fam[K] = fbest;
+      for (int t = 0; t < (int)F.inst.size(); ++t) {
+        int i = bbest.src[t], j = bbest.dst[t];
+        dst[(size_t)K * N + i] = j;
+        inst[(size_t)K * N + i] = F.inst[t].id;
+        bytes[(size_t)K * N + i] = ebest.x[t];
+        Drem[(size_t)i * N + j] -= ebest.x[t];
+      }
+      ++K;
+      *Kout = (int32_t)K;
+    }
+    return OK;
+  }
+};
+
+}  // namespace
+
+// ===========================================================================
+// C interface for the Python side (ctypes).
+// ===========================================================================
+extern "C" {
+
+struct orc_catalog;   // opaque: a Catalog
+
+struct orc_topology {
+  int32_t n_nodes, sockets_per_node, switches_per_socket, gpus_per_switch, nics_per_switch;
+  int32_t pad;
+  int64_t pcie_bytes_per_ns, nic_bytes_per_ns;
+};
+
+struct orc_params {
+  int64_t k_target, lambda_ns, unit_bytes;
+  int32_t n_start, i_aa;
+  uint64_t seed;
+};
+
+// mode 0: node-circulant catalog (equal to full Alg. 1 for one node)
+// mode 1: full Alg. 1 over the cluster-level instance set (small topologies)
+int orc_catalog_build(const orc_topology* tp, int mode, orc_catalog** out) {
+  if (!tp || !out) return INVALID_ARGUMENT;
+  Topo t{tp->n_nodes, tp->sockets_per_node, tp->switches_per_socket, tp->gpus_per_switch,
+         tp->nics_per_switch, tp->pcie_bytes_per_ns, tp->nic_bytes_per_ns};
+  // every ordered pair needs a path: one NIC per switch, at least two GPUs per switch
+  if (t.n_nodes < 1 || t.sockets < 1 || t.switches < 1 || t.g < 2 || t.nics != 1 ||
+      t.pcie < 1 || t.nic < 1)
+    return INVALID_ARGUMENT;
+  Catalog* C = new Catalog();
+  C->topo = t;
+  C->circulant = mode == 0;
+  if (mode == 0) build_circulant(*C);
+  else build_full(*C);
+  C->bw_max = 0;
+  for (const auto& r : C->table) C->bw_max = std::max(C->bw_max, r.bw);
+  *out = reinterpret_cast<orc_catalog*>(C);
+  return OK;
+}
+
+void orc_catalog_free(orc_catalog* c) { delete reinterpret_cast<Catalog*>(c); }
+
+// info[0..7] = N, G, g, Q, n_nodes, n_shapes, n_families, n_table_instances
+int orc_catalog_info(const orc_catalog* c, int64_t* info) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  info[0] = C->topo.N();
+  info[1] = C->topo.G();
+  info[2] = C->topo.g;
+  info[3] = C->topo.Q();
+  info[4] = C->topo.n_nodes;
+  info[5] = (int64_t)C->shapes.size();
+  info[6] = (int64_t)C->fams.size();
+  info[7] = (int64_t)C->table.size();
+  return OK;
+}
+
+// Instance table: class, src, dst, copy, rate, and up to 2 resource ids (-1 pad).
+int orc_catalog_table(const orc_catalog* c, int32_t* cls, int32_t* src, int32_t* dst,
+                      int32_t* copy, int64_t* bw, int32_t* res2) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  for (size_t i = 0; i < C->table.size(); ++i) {
+    const Inst& r = C->table[i];
+    cls[i] = r.cls; src[i] = r.a; dst[i] = r.d; copy[i] = r.copy; bw[i] = r.bw;
+    res2[2 * i] = r.L.size() > 0 ? r.L[0] : -1;
+    res2[2 * i + 1] = r.L.size() > 1 ? r.L[1] : -1;
+  }
+  return OK;
+}
+
+// Shapes: k, bucket range; circulant: Q x Q diagonal/shift blocks;
+// full: dense G x G written to Lm (Rm untouched).
+int orc_catalog_shapes(const orc_catalog* c, int32_t* k, int32_t* fam_begin, int32_t* fam_end,
+                       int32_t* Lm, int32_t* Rm) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  const int Q = C->topo.Q(), G = C->topo.G();
+  for (size_t m = 0; m < C->shapes.size(); ++m) {
+    const CShape& s = C->shapes[m];
+    k[m] = s.k;
+    fam_begin[m] = s.fam_begin;
+    fam_end[m] = s.fam_end;
+    if (C->circulant) {
+      for (int x = 0; x < Q * Q; ++x) { Lm[m * Q * Q + x] = s.Lm[x]; Rm[m * Q * Q + x] = s.Rm[x]; }
+    } else {
+      for (int x = 0; x < G * G; ++x) Lm[m * G * G + x] = s.dense[x];
+    }
+  }
+  return OK;
+}
+
+// Families: shape, k, and the instance ids (local ids for circulant
+// catalogs: Q*g per family; cluster ids for full catalogs: N per family).
+int orc_catalog_families(const orc_catalog* c, int32_t* shape, int32_t* k, int32_t* ids) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  size_t w = C->fams.empty() ? 0 : C->fams[0].local.size();
+  for (size_t f = 0; f < C->fams.size(); ++f) {
+    shape[f] = C->fams[f].shape;
+    k[f] = C->fams[f].k;
+    for (size_t x = 0; x < w; ++x) ids[f * w + x] = C->fams[f].local[x];
+  }
+  return OK;
+}
+
+// Cluster view of one family: per instance t (family order): class, source
+// group, destination group, recorded id.
+int orc_catalog_cluster_family(const orc_catalog* c, int32_t f, int32_t* cls, int32_t* a,
+                               int32_t* d, int32_t* id) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  if (f < 0 || f >= (int32_t)C->fams.size()) return INVALID_ARGUMENT;
+  const CFamily& F = C->fams[f];
+  for (size_t t = 0; t < F.inst.size(); ++t) {
+    cls[t] = F.inst[t].cls; a[t] = F.inst[t].a; d[t] = F.inst[t].d; id[t] = F.inst[t].id;
+  }
+  return OK;
+}
+
+// Demand row of one source rank (Sec. 3 model setup; Sec. 5 sparse EP):
+// counts[e] = #{(t, e)}; D_self,j = unit * sum of counts of the experts that
+// rank j hosts (experts are contiguous per rank), D_self,self = 0.  Also the
+// stable (expert, token) order of the assignments and each destination's
+// first row in it.
+int orc_demand(const int32_t* routing, int64_t T, int32_t k, int32_t E, int32_t N,
+               int32_t self, int64_t unit, int64_t* row, int32_t* counts, int32_t* sorted_tok,
+               int64_t* dest_off) {
+  if (N < 1 || E < N || E % N != 0 || self < 0 || self >= N || unit < 1) return INVALID_ARGUMENT;
+  const int eloc = E / N;
+  for (int e = 0; e < E; ++e) counts[e] = 0;
+  for (int64_t x = 0; x < T * k; ++x) {
+    int e = routing[x];
+    if (e < 0 || e >= E) return INVALID_ARGUMENT;
+    counts[e]++;
+  }
+  for (int j = 0; j < N; ++j) {
+    int64_t c = 0;
+    for (int e = j * eloc; e < (j + 1) * eloc; ++e) c += counts[e];
+    row[j] = j == self ? 0 : c * unit;
+  }
+  // stable order by expert: walk experts ascending, tokens ascending
+  std::vector<int64_t> start(E + 1, 0);
+  for (int e = 0; e < E; ++e) start[e + 1] = start[e] + counts[e];
+  std::vector<int64_t> fill(start.begin(), start.end() - 1);
+  for (int64_t x = 0; x < T * k; ++x) {
+    int e = routing[x];
+    sorted_tok[fill[e]++] = (int32_t)(x / k);
+  }
+  for (int j = 0; j <= N; ++j) dest_off[j] = start[(size_t)j * eloc];
+  return OK;
+}
+
+// Ulysses head/context re-layout demand: rank j receives its heads of every
+// local token, D_self,j = T * heads(j) * head_bytes, D_self,self = 0.
+int orc_demand_heads(int64_t T, const int64_t* head_lo, int64_t head_bytes, int32_t N,
+                     int32_t self, int64_t* row) {
+  if (N < 1 || self < 0 || self >= N) return INVALID_ARGUMENT;
+  for (int j = 0; j < N; ++j) row[j] = j == self ? 0 : T * (head_lo[j + 1] - head_lo[j]) * head_bytes;
+  return OK;
+}
+
+int orc_plan(const orc_catalog* c, const int64_t* D, const orc_params* pp, int32_t k_max,
+             int32_t* K, int32_t* fam, int32_t* dst, int32_t* inst, int64_t* bytes,
+             int64_t* tau_out, int64_t* trace, int64_t trace_cap, int64_t* trace_n) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  if (!C || !D || !pp || pp->unit_bytes < 1 || pp->k_target < 1 || pp->n_start < 1 ||
+      pp->i_aa < 0 || pp->lambda_ns < 0 || k_max < 0)
+    return INVALID_ARGUMENT;
+  Params P{pp->k_target, pp->lambda_ns, pp->unit_bytes, pp->n_start, pp->i_aa, pp->seed};
+  Planner pl(*C, P);
+  pl.trace = trace;
+  pl.trace_cap = trace ? trace_cap : 0;
+  int st = pl.run(D, K, fam, dst, inst, bytes, k_max, tau_out);
+  if (trace_n) *trace_n = pl.trace_n;
+  return st;
+}
+
+// The counter-based generator of the random AA starts, exposed for pinning:
+// n outputs of SplitMix64 from a raw state, or (when key != 0) from the state
+// keyed by (seed, iteration, family, start, group, side) = fields[0..5].
+int orc_splitmix_stream(uint64_t state, const uint64_t* fields, int32_t n, uint64_t* out) {
+  SplitMix rng{state};
+  if (fields) rng = keyed_stream(fields[0], fields[1], fields[2], fields[3], fields[4], fields[5]);
+  for (int i = 0; i < n; ++i) out[i] = rng.next();
+  return OK;
+}
+
+// The planner's exact utility order, exposed for pinning: 1 when the
+// candidate (S1, x1, b1) has a strictly larger Eq. (10) utility than
+// (S2, x2, b2), where x/b is each candidate's slowest lane.
+int orc_utility_greater(int64_t S1, int64_t x1, int64_t b1, int64_t S2, int64_t x2, int64_t b2,
+                        int64_t lambda_ns) {
+  Catalog dummy;
+  dummy.topo = Topo{1, 1, 1, 2, 1, 1, 1};
+  dummy.bw_max = 1;
+  Params P{1, lambda_ns, 1, 1, 0, 0};
+  Planner pl(dummy, P);
+  Planner::Eval e1, e2;
+  e1.S = S1; e1.xm = x1; e1.bm = b1;
+  e2.S = S2; e2.xm = x2; e2.bm = b2;
+  return pl.better(e1, e2) ? 1 : 0;
+}
+
+// Modeled completion time, Eq. (2), as an exact fraction num / den (ns).
+int orc_modeled_time(const orc_catalog* c, int32_t K, int32_t N, const int32_t* inst,
+                     const int64_t* bytes, int64_t lambda_ns, int64_t* num, int64_t* den) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  int64_t l = 1;
+  for (const auto& r : C->table) {
+    int64_t a = l, b = r.bw;
+    while (b) { int64_t t = a % b; a = b; b = t; }
+    l = l / a * r.bw;
+  }
+  int64_t total = 0;
+  for (int k = 0; k < K; ++k) {
+    int64_t worst = 0;
+    for (int i = 0; i < N; ++i) {
+      int64_t x = bytes[(size_t)k * N + i];
+      int64_t bw = C->table[inst[(size_t)k * N + i]].bw;
+      worst = std::max(worst, x * (l / bw));
+    }
+    total += lambda_ns * l + worst;
+  }
+  *num = total;
+  *den = l;
+  return OK;
+}
+
+// Send-buffer layout (Sec. 5 "Device-resident buffer layout"): for the steps
+// in which this rank's lane carries bytes, in schedule order, append the next
+// x bytes of the stream to the lane's destination.  Stream j is rank j's
+// token rows in (expert, token) order.  step_off[k] is where step k starts.
+int orc_pack_rows(const uint8_t* tokens, int64_t T, int64_t row_bytes, const int32_t* sorted_tok,
+                  const int64_t* dest_off, int32_t self, int32_t N, int32_t K,
+                  const int32_t* dst, const int64_t* bytes, uint8_t* send, int64_t* step_off) {
+  std::vector<int64_t> sent(N, 0);
+  int64_t o = 0;
+  for (int k = 0; k < K; ++k) {
+    step_off[k] = o;
+    int64_t x = bytes[(size_t)k * N + self];
+    int j = dst[(size_t)k * N + self];
+    if (x == 0) continue;
+    if (x < 0 || x % row_bytes != 0 || j < 0 || j >= N || j == self) return INVALID_ARGUMENT;
+    int64_t stream_rows = dest_off[j + 1] - dest_off[j];
+    if ((sent[j] + x) / row_bytes > stream_rows) return INVALID_ARGUMENT;
+    for (int64_t u = 0; u < x / row_bytes; ++u) {
+      int64_t p = dest_off[j] + sent[j] / row_bytes + u;
+      int64_t tok = sorted_tok[p];
+      if (tok < 0 || tok >= T) return INVALID_ARGUMENT;
+      std::memcpy(send + o + u * row_bytes, tokens + tok * row_bytes, (size_t)row_bytes);
+    }
+    sent[j] += x;
+    o += x;
+  }
+  step_off[K] = o;
+  return OK;
+}
+
+// Ulysses layout: stream j is, for every local token in order, the bytes of
+// the heads rank j owns; units are single heads.
+int orc_pack_heads(const uint8_t* act, int64_t T, int64_t token_stride, const int64_t* head_lo,
+                   int64_t head_bytes, int32_t self, int32_t N, int32_t K, const int32_t* dst,
+                   const int64_t* bytes, uint8_t* send, int64_t* step_off) {
+  std::vector<int64_t> sent(N, 0);
+  int64_t o = 0;
+  for (int k = 0; k < K; ++k) {
+    step_off[k] = o;
+    int64_t x = bytes[(size_t)k * N + self];
+    int j = dst[(size_t)k * N + self];
+    if (x == 0) continue;
+    if (x < 0 || x % head_bytes != 0 || j < 0 || j >= N || j == self) return INVALID_ARGUMENT;
+    int64_t hj = head_lo[j + 1] - head_lo[j];
+    if ((sent[j] + x) / head_bytes > T * hj) return INVALID_ARGUMENT;
+    for (int64_t u = 0; u < x / head_bytes; ++u) {
+      int64_t idx = sent[j] / head_bytes + u;
+      int64_t tok = idx / hj, head = head_lo[j] + idx % hj;
+      std::memcpy(send + o + u * head_bytes, act + tok * token_stride + head * head_bytes,
+                  (size_t)head_bytes);
+    }
+    sent[j] += x;
+    o += x;
+  }
+  step_off[K] = o;
+  return OK;
+}
+
+}  // extern "C"
