@@ -1,0 +1,245 @@
+#!/usr/bin/env python3
+"""Benchmark of the VarioPath demand -> plan -> pack hot path on one MI355X.
+
+One step = one AlltoAllv invocation of the 256-rank DeepSeek-V3-like MoE
+dispatch (4096 tokens/rank, hidden 7168 bf16, 256 experts top-8, 26 hot
+experts holding half of the per-draw mass, hot set redrawn per matrix):
+
+  vp_demand   all 256 ranks' routing -> the 256 x 256 byte-demand matrix
+              (+ rank 0's (expert, token) order and offsets)
+  vp_plan     Alg. 2 on that matrix against the node-circulant catalog
+  vp_pack     rank 0's token rows into channel-ordered send slices
+
+all enqueued on one stream with no host synchronisation, inputs resident in
+HBM.  Steps cycle over `--matrices` distinct demand matrices and two send
+buffers.  Prints one JSON line.  `value` is the pack's throughput in GB/s
+(send bytes + distinct source bytes + index bytes, over the time of the
+whole vp_pack call); the planner's microseconds per matrix, the step time
+and the roofline of the dominant copy kernel ride along.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "pack HBM GB/s (% of peak) + vp_plan µs per N×N demand matrix, N=8..256"
+PEAK_HBM_GBS = 8000.0
+HERE = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "pack_gather_traffic.json")
+
+
+def pack_source_sha() -> str:
+    with open(os.path.join(HERE, "paper_2609_34340_amd", "csrc", "pack.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def rank0_accounting(w, routing0: np.ndarray):
+    """Bytes a pack of rank 0 must move: the send bytes, the distinct source
+    rows, and the rows it indexes (for the GB/s accounting only)."""
+    eloc = w.experts // w.n_ranks
+    remote = (routing0 // eloc) != 0
+    rows = int(remote.sum())
+    distinct = int(remote.any(axis=1).sum())
+    return rows * w.row_bytes, distinct * w.row_bytes, rows
+
+
+def cpu_baseline(w, routing_np, tokens_np):
+    """The oracle, single-threaded, on one matrix: demand of every rank, the
+    plan, and rank 0's pack."""
+    import oracle
+    cat = oracle.Catalog(w.topo)
+    t0 = time.perf_counter()
+    dem = [oracle.demand(routing_np[i], w.n_ranks, w.experts, i, w.row_bytes) for i in range(w.n_ranks)]
+    t1 = time.perf_counter()
+    D = np.stack([d["row"] for d in dem])
+    s = cat.plan(D, w.row_bytes)
+    t2 = time.perf_counter()
+    send, _ = oracle.pack_rows(tokens_np, w.row_bytes, dem[0]["sorted_tok"], dem[0]["dest_off"], 0, s)
+    t3 = time.perf_counter()
+    S, U, rows = rank0_accounting(w, routing_np[0])
+    slices = int((s["bytes"][:, 0] > 0).sum())
+    pack_bytes = S + U + 4 * rows + 16 * slices
+    return dict(value=round(pack_bytes / (t3 - t2) / 1e9, 3), unit="GB/s", cores=1, kind="oracle",
+                sample="one %d x %d matrix of the workload: demand of all %d ranks, one plan (K=%d), "
+                       "rank-0 pack of %.1f MB" % (w.n_ranks, w.n_ranks, w.n_ranks, s["K"], send.size / 1e6),
+                demand_s=round(t1 - t0, 3), plan_us_per_matrix=round((t2 - t1) * 1e6, 1),
+                pack_s=round(t3 - t2, 4))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=5, help="workload configuration 1..5")
+    ap.add_argument("--matrices", type=int, default=4, help="distinct demand matrices cycled")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0,
+                    help="after the timed region, run one plain device copy of this many MiB")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build's hot path is the per-rank demand -> plan -> "
+              "pack work, which runs on a single MI355X; run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import vpgen
+    import paper_2609_34340_amd as vp
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = vpgen.config(args.config)
+    dev = torch.device("cuda:0")
+    M = max(1, min(args.matrices, args.steps))
+    print("[bench] generating %d matrices of %s" % (M, w.name), file=sys.stderr, flush=True)
+
+    if w.mode == "moe":
+        routing_np = [vpgen.routing_all(w, m) for m in range(M)]
+        routing = [torch.from_numpy(r).to(dev) for r in routing_np]
+        tokens_np = vpgen.tokens_bf16(w, 0)
+        tokens = torch.from_numpy(tokens_np).to(dev)
+        acct = [rank0_accounting(w, r[0]) for r in routing_np]
+        pipe = vp.Pipeline(w.topo, "moe", w.row_bytes, n_experts=w.experts, tokens=w.tokens, top_k=w.top_k)
+        head_lo = None
+    else:
+        hl = vpgen.head_split(w.heads, w.n_ranks)
+        head_lo = torch.from_numpy(hl).to(dev)
+        tokens_np = vpgen.tokens_bf16(w, 0)
+        tokens = torch.from_numpy(tokens_np).to(dev)
+        S = int(w.tokens * (hl[-1] - (hl[1] - hl[0])) * w.row_bytes)
+        acct = [(S, S, S // w.row_bytes)]
+        routing = [None]
+        pipe = vp.Pipeline(w.topo, "heads", w.row_bytes, tokens=w.tokens, token_stride=w.token_stride)
+    sends = [pipe.send, torch.empty_like(pipe.send)]
+    E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    def run(step, ev=None):
+        m = step % M
+        if ev is not None:
+            ev[0].record()
+        pipe.demand_stage(routing[m], head_lo)
+        if ev is not None:
+            ev[1].record()
+        pipe.plan_stage()
+        if ev is not None:
+            ev[2].record()
+        pipe.pack_prepare_stage(tokens, head_lo)
+        if ev is not None:
+            ev[3].record()
+        pipe.pack_gather_stage(tokens, sends[step % 2])
+        if ev is not None:
+            ev[4].record()
+
+    for s in range(args.warmup):
+        run(s)
+    torch.cuda.synchronize()
+    if vp.read_status(pipe.status) != 0:
+        raise SystemExit("device error during warmup: %d" % vp.read_status(pipe.status))
+
+    evs = [[E() for _ in range(5)] for _ in range(args.steps)]
+    start, end = E(), E()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for s in range(args.steps):
+        run(s, evs[s])
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    if vp.read_status(pipe.status) != 0:
+        raise SystemExit("device error in the timed region: %d" % vp.read_status(pipe.status))
+    total_ms = start.elapsed_time(end)
+    demand_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    plan_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    prep_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    gather_ms = np.array([e[3].elapsed_time(e[4]) for e in evs])
+
+    # schedule facts per matrix (untimed): K, slices, modeled completion time
+    Ks, slices, That = [], [], []
+    for m in range(M):
+        pipe.demand_stage(routing[m], head_lo)
+        pipe.plan_stage()
+        torch.cuda.synchronize()
+        h = vp.schedule_to_host(pipe.sched)
+        Ks.append(h["K"])
+        slices.append(int((h["bytes"][:, pipe.self_rank] > 0).sum()))
+        num, den = pipe.cat.modeled_time(h["K"], h["inst"], h["bytes"], pipe.params.lambda_ns)
+        That.append(num / den / 1e6)
+    step_m = [s % M for s in range(args.steps)]
+    S_b = np.array([acct[m][0] for m in step_m], dtype=np.float64)
+    U_b = np.array([acct[m][1] for m in step_m], dtype=np.float64)
+    rows = np.array([acct[m][2] for m in step_m], dtype=np.float64)
+    sl = np.array([slices[m] for m in step_m], dtype=np.float64)
+    pack_bytes = S_b + U_b + 4 * rows + 16 * sl
+    pack_ms = prep_ms + gather_ms
+    value = float(pack_bytes.sum() / (pack_ms.sum() * 1e-3) / 1e9)
+    gather_bytes = S_b + U_b
+    achieved = float(gather_bytes.sum() / (gather_ms.sum() * 1e-3) / 1e9)
+    plan_us = float(plan_ms.mean() * 1e3)
+
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        if t.get("kernel_source_sha") == pack_source_sha() and t.get("workload") == w.name:
+            traffic = t.get("bytes_per_launch")
+
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic",
+        "config": {"workload": "C%d %s: N=%d ranks (%d nodes x 2 sockets x 2 PCIe switches x 2 GPUs), "
+                               "%s, tokens/rank=%d, unit=%d B" % (
+                                   w.cid, w.name, w.n_ranks, w.topo.n_nodes,
+                                   ("%d experts top-%d" % (w.experts, w.top_k)) if w.mode == "moe"
+                                   else "Ulysses %d heads x %d" % (w.heads, w.head_dim),
+                                   w.tokens, w.row_bytes),
+                   "matrices": M, "self_rank": 0},
+        "pct_of_peak": round(100 * value / PEAK_HBM_GBS, 2),
+        "plan_us_per_matrix": round(plan_us, 1),
+        "plan_us_per_activation": round(plan_us / float(np.mean([Ks[m] for m in step_m])), 3),
+        "demand_us": round(float(demand_ms.mean() * 1e3), 1),
+        "pack_us": round(float(pack_ms.mean() * 1e3), 1),
+        "activations_K": int(round(np.mean(Ks))),
+        "modeled_T_ms": round(float(np.mean(That)), 3),
+        "plan_over_modeled_T": round(plan_us / (1e3 * float(np.mean(That))), 5),
+        "wall_s": round(wall, 3),
+        "roofline": {"bound": "hbm", "kernel": "gather_kernel (vp_pack_gather)",
+                     "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": int(gather_bytes.mean()),
+                     "avg_launch_us": round(float(gather_ms.mean() * 1e3), 2)},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on one matrix", file=sys.stderr, flush=True)
+        if w.mode == "moe":
+            out["cpu_baseline"] = cpu_baseline(w, routing_np[0], tokens_np)
+        else:
+            out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,264 @@
+/* vp.h -- C-ABI of the VarioPath demand -> plan -> pack hot path for MI355X.
+ *
+ * The library turns one AlltoAllv invocation's routing into
+ *   (1) an N x N byte-demand matrix            (Sec. 3 "Model setup"),
+ *   (2) an ordered list of channel activations  (Sec. 4.2, Alg. 2),
+ *   (3) channel-ordered send buffers            (Sec. 5 "Device-resident buffer layout"),
+ * against an offline catalog of contention-free channel families
+ * (Sec. 4.1, Alg. 1).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers marked "device" are HIP device allocations owned by the caller
+ *   (e.g. torch tensors passed by data_ptr()).  Pointers marked "host" are
+ *   ordinary host memory owned by the caller.  The library owns only the
+ *   opaque vp_catalog handle, released with vp_catalog_free().
+ * - `stream` is a hipStream_t passed as void*; NULL means the default stream.
+ *   Every device entry point only enqueues work on that stream and returns
+ *   without synchronising.  No hot call allocates memory: scratch space comes
+ *   from the caller through a workspace pointer whose size is given by the
+ *   matching *_workspace() query.
+ * - Errors found on the host (bad sizes, null pointers, unsupported shapes)
+ *   are returned immediately and nothing is enqueued.  Errors that only the
+ *   device can see (an expert id out of range, a demand entry that is
+ *   negative, on the diagonal or not a multiple of the unit, a plan that
+ *   cannot progress or exceeds k_max, a pack slice outside its stream) are
+ *   written to the caller's device int32 `dev_status` (first error wins,
+ *   VP_OK = 0 means none) and become visible after the stream is
+ *   synchronised.  Kernels never trap; after a device error the outputs of
+ *   that call are unspecified.  The caller clears dev_status (write 0)
+ *   before a chain of calls.  Nothing throws or aborts across this ABI.
+ * - vp_last_error() returns a thread-local text for the last host-side
+ *   error of the calling thread.
+ */
+#ifndef VP_H_
+#define VP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  VP_OK = 0,
+  VP_ERR_INVALID_ARGUMENT = 1, /* bad pointer/size, or a routing id outside [0, E) */
+  VP_ERR_INVALID_DEMAND = 2,   /* D_ij < 0, D_ii != 0, or D_ij not a multiple of the unit */
+  VP_ERR_NO_PROGRESS = 3,      /* an iteration of Alg. 2 could serve no byte */
+  VP_ERR_CAPACITY = 4,         /* schedule longer than k_max, or send buffer too small */
+  VP_ERR_UNSUPPORTED = 5,      /* shape outside this build's limits (see each call) */
+  VP_ERR_HIP = 6               /* a HIP runtime call failed */
+} vp_status;
+
+/* Path classes of a lane (Sec. 3; Fig. 1 legend): same switch, same socket
+ * through the root complex, and through the switches' NICs. */
+enum { VP_PATH_PIX = 0, VP_PATH_PXB = 1, VP_PATH_NIC = 2 };
+
+/* A PCIe cluster (Sec. 3 "Model setup", Sec. 5 "Topology, path, and rate
+ * model").  Rank = ((node * sockets + socket) * switches + switch) * gpus + local;
+ * one rank group per PCIe switch.  Every switch has one NIC.  Rates are in
+ * bytes per nanosecond; a NIC path runs at min(pcie, nic).
+ * Limits of this build: gpus_per_switch in [2, 4], sockets*switches <= 8,
+ * nics_per_switch == 1, n_nodes in [1, 256], N <= 1024. */
+typedef struct {
+  int32_t n_nodes;
+  int32_t sockets_per_node;
+  int32_t switches_per_socket;
+  int32_t gpus_per_switch;
+  int32_t nics_per_switch;
+  int32_t flags;               /* reserved, must be 0 */
+  int64_t pcie_bytes_per_ns;
+  int64_t nic_bytes_per_ns;
+} vp_topology;
+
+/* Inputs of Alg. 2 (Sec. 4.2) and of the quantum of Sec. 5 "Global execution
+ * granularity".  vp_plan_params_default() fills K_target = 2N, lambda =
+ * 10,000 ns, N_start = 4, I_AA = 8, seed = 0, k_max = 8N. */
+typedef struct {
+  int64_t k_target;    /* target round count; tau = ceil(L_max / (bw_max * k_target)) ns */
+  int64_t lambda_ns;   /* fixed per-activation overhead of Eq. (2) and Eq. (10) */
+  int64_t unit_bytes;  /* pack granule; every demand entry is a multiple of it */
+  int32_t n_start;     /* MultiStartAA starts, 1..16 */
+  int32_t i_aa;        /* AA sweep limit, >= 0 */
+  uint64_t seed;       /* key of the counter-based random starts */
+  int32_t k_max;       /* capacity of the schedule arrays (rows) */
+  int32_t reserved;
+} vp_plan_params;
+
+typedef struct vp_catalog vp_catalog; /* opaque, library-owned */
+
+/* ---------------------------------------------------------------- catalog */
+
+/* Offline catalog construction (Sec. 4.1, Alg. 1, PrunePaths, PruneFamilies),
+ * host only.  For one node this is the full Alg. 1 catalog; for several nodes
+ * it is the node-circulant catalog: a family repeats one node-local pattern in
+ * every node with all NIC lanes of node n landing on node (n + k) mod n_nodes.
+ * Shapes are ordered by (k, diagonal node block, shift node block) and
+ * families inside a shape by their sorted node-local instance ids.
+ * *out receives a new handle (free with vp_catalog_free). */
+vp_status vp_build_catalog(const vp_topology* topo, vp_catalog** out);
+
+/* info[0..7] = N, G (groups), g, Q (switches per node), n_nodes, shapes,
+ * families, node-local instances.  Host only. */
+vp_status vp_catalog_info(const vp_catalog* cat, int64_t info[8]);
+
+/* Node-local instance table in id order (host arrays of length info[7]):
+ * path class, source slot, destination slot, copy index, rate (bytes/ns). */
+vp_status vp_catalog_instances(const vp_catalog* cat, int32_t* cls, int32_t* src_slot,
+                               int32_t* dst_slot, int32_t* copy, int64_t* bw);
+
+/* Canonical shapes (host arrays, J = info[5], Q = info[3]): node shift k,
+ * family range [fam_begin, fam_end), and the Q x Q lane counts of the
+ * diagonal node block (L) and of the block from node n to node n+k (R). */
+vp_status vp_catalog_shapes(const vp_catalog* cat, int32_t* k, int32_t* fam_begin,
+                            int32_t* fam_end, int32_t* L, int32_t* R);
+
+/* Canonical families (host arrays, F = info[6]): shape index, node shift k,
+ * and the Q*g node-local instance ids of each family, ascending. */
+vp_status vp_catalog_families(const vp_catalog* cat, int32_t* shape, int32_t* k, int32_t* ids);
+
+/* Copy the catalog to the current device once (synchronous on `stream`);
+ * the device copy belongs to the handle.  Needed before vp_plan. */
+vp_status vp_catalog_upload(vp_catalog* cat, void* stream);
+
+void vp_catalog_free(vp_catalog* cat);
+
+/* ----------------------------------------------------------------- demand */
+
+/* Workspace bytes for vp_demand with `T` tokens, top-`k`, `E` experts. */
+size_t vp_demand_workspace(int64_t T, int32_t k, int32_t E);
+
+/* Demand rows from routing (Sec. 3 model setup; one row copy per (token,
+ * expert) assignment, Sec. 5 sparse EP).  For R source ranks
+ * first_rank .. first_rank+R-1:
+ *   routing    device int32 [R, T, k]  expert ids in [0, E)
+ *   counts     device int32 [R, E]     assignments per expert
+ *   demand     device int64 [R, N]     D_r,j = unit * sum of counts of the
+ *                                      E/N experts hosted by rank j
+ *                                      (experts contiguous per rank),
+ *                                      D_r,r = 0
+ * and for row `sort_row` (0 <= sort_row < R, or -1 for none):
+ *   sorted_tok device int32 [T*k]      token ids of that row's assignments in
+ *                                      (expert, token) order (stable)
+ *   dest_off   device int64 [N+1]      first position of each destination
+ *                                      rank's rows in sorted_tok
+ * E must be a positive multiple of N, E <= 4096, T*k < 2^31.  An expert id
+ * outside [0, E) sets VP_ERR_INVALID_ARGUMENT in dev_status. */
+vp_status vp_demand(const int32_t* routing, int32_t R, int64_t T, int32_t k, int32_t E,
+                    int32_t n_ranks, int32_t first_rank, int32_t sort_row, int64_t unit_bytes,
+                    int32_t* counts, int64_t* demand, int32_t* sorted_tok, int64_t* dest_off,
+                    int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
+
+/* Ulysses head/context re-layout demand (Sec. 6.2 sequence parallelism):
+ * rank j owns heads [head_lo[j], head_lo[j+1]) (device int64 [N+1]); each of
+ * the T local tokens sends its heads of rank j there:
+ *   demand device int64 [R, N], D_r,j = T * (head_lo[j+1]-head_lo[j]) * head_bytes,
+ *   D_r,r = 0, for ranks first_rank .. first_rank+R-1.
+ * A decreasing head_lo sets VP_ERR_INVALID_ARGUMENT in dev_status. */
+vp_status vp_demand_heads(int64_t T, const int64_t* head_lo, int64_t head_bytes, int32_t n_ranks,
+                          int32_t first_rank, int32_t R, int64_t* demand, int32_t* dev_status,
+                          void* stream);
+
+/* ------------------------------------------------------------------- plan */
+
+void vp_plan_params_default(int32_t n_ranks, int64_t unit_bytes, vp_plan_params* p);
+
+/* Workspace bytes for vp_plan (holds the residual demand D^rem). */
+size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
+
+/* Online channel-guided demand decomposition (Sec. 4.2, Alg. 2), run
+ * entirely on the device by one persistent kernel:
+ *   demand  device int64 [N, N]  bytes from rank i (row) to rank j (column)
+ *   K       device int32 [1]     activations emitted
+ *   family  device int32 [k_max] global family index of each activation
+ *   dst     device int32 [k_max, N]  pi_k(i) for source rank i
+ *   inst    device int32 [k_max, N]  node-local instance id of lane i
+ *   bytes   device int64 [k_max, N]  x_{k,i} of Eq. (9) (zero lanes kept)
+ *   tau     device int64 [1]     the quantum used (ns), may be NULL
+ * Each iteration scores every catalog shape (Eq. (5)-(6)), binds every family
+ * of the best shape with MultiStartAA (Eq. (7)-(8)), evaluates Eq. (9)-(10)
+ * exactly and appends the best activation.  Device errors:
+ * VP_ERR_INVALID_DEMAND, VP_ERR_NO_PROGRESS, VP_ERR_CAPACITY, and
+ * VP_ERR_UNSUPPORTED when a capacity tau*bw reaches 2^31 bytes or the total
+ * demand reaches 2^42 bytes.  The catalog must have been uploaded. */
+vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_params* p,
+                  int32_t* K, int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes,
+                  int64_t* tau, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------- pack */
+
+/* Workspace bytes for vp_pack_rows / vp_pack_heads with schedule capacity
+ * k_max, a send buffer of send_capacity bytes and a pack unit of unit_bytes
+ * (row_bytes or head_bytes): per-step stream offsets and one source offset
+ * per packed unit. */
+size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_bytes);
+
+/* Send-buffer layout (Sec. 5 "Device-resident buffer layout"): for the steps
+ * in which rank `self_rank` carries bytes, in schedule order, append the next
+ * x bytes of the stream to that step's destination.  Stream j is rank
+ * self_rank's token rows for j in (expert, token) order:
+ *   tokens     device [T, row_bytes]   token rows (bf16 or any bytes)
+ *   sorted_tok device int32 [T*k]      from vp_demand
+ *   dest_off   device int64 [N+1]      from vp_demand (row units)
+ *   K, dst, bytes                      the schedule of vp_plan (device)
+ *   send       device [send_capacity]  output
+ *   step_off   device int64 [k_max+1]  where step k's slice starts in send;
+ *                                      entries past K are unspecified,
+ *                                      step_off[K] = total bytes
+ * row_bytes must be a multiple of 16.  Slices that are not whole rows or run
+ * past their stream, or a total above send_capacity, set VP_ERR_INVALID_ARGUMENT
+ * or VP_ERR_CAPACITY in dev_status and write nothing to send. */
+vp_status vp_pack_rows(const void* tokens, int64_t T, int64_t row_bytes, const int32_t* sorted_tok,
+                       const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
+                       const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
+                       void* send, int64_t send_capacity, int64_t* step_off, int32_t* dev_status,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* Ulysses variant: stream j is, token by token, the bytes of the heads rank j
+ * owns, [head_lo[j], head_lo[j+1]) (device int64 [N+1]); units are single
+ * heads of head_bytes (a multiple of 16); activations are [T, token_stride]. */
+vp_status vp_pack_heads(const void* act, int64_t T, int64_t token_stride, const int64_t* head_lo,
+                        int64_t head_bytes, int32_t self_rank, int32_t n_ranks, const int32_t* K,
+                        const int32_t* dst, const int64_t* bytes, int32_t k_max, void* send,
+                        int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
+                        size_t ws_bytes, void* stream);
+
+/* The two halves of vp_pack_rows / vp_pack_heads, for callers that schedule
+ * or time the copy on its own.  vp_pack_prepare_* take the same arguments
+ * minus `send` and run the slice and index kernels: they fill step_off and
+ * the workspace (per-step stream offsets, then one int64 source byte offset
+ * per packed unit) and check every slice and the capacity.  vp_pack_gather
+ * then copies each unit from `src` (the tokens or activations given to the
+ * prepare call) into `send` with 16-byte loads and non-temporal stores; it
+ * must get the same unit_bytes, k_max, send_capacity and workspace.  It
+ * writes nothing when dev_status already holds an error. */
+vp_status vp_pack_prepare_rows(const void* tokens, int64_t T, int64_t row_bytes, const int32_t* sorted_tok,
+                               const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
+                               const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
+                               int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
+                               size_t ws_bytes, void* stream);
+vp_status vp_pack_prepare_heads(const void* act, int64_t T, int64_t token_stride, const int64_t* head_lo,
+                                int64_t head_bytes, int32_t self_rank, int32_t n_ranks, const int32_t* K,
+                                const int32_t* dst, const int64_t* bytes, int32_t k_max,
+                                int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
+                                size_t ws_bytes, void* stream);
+vp_status vp_pack_gather(const void* src, int64_t unit_bytes, const int32_t* K, const int64_t* step_off,
+                         int32_t k_max, void* send, int64_t send_capacity, int32_t* dev_status,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* --------------------------------------------------------------- helpers */
+
+/* Modeled completion time of a schedule, Eq. (2), as the exact fraction
+ * num/den nanoseconds (host arrays inst, bytes of shape [K, N]). */
+vp_status vp_modeled_time(const vp_catalog* cat, int32_t K, const int32_t* inst,
+                          const int64_t* bytes, int64_t lambda_ns, int64_t* num, int64_t* den);
+
+const char* vp_status_string(vp_status s);
+const char* vp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VP_H_ */

@@ -1,0 +1,426 @@
+"""Python binding of libvp: the VarioPath demand -> plan -> pack hot path on MI355X.
+
+Argument marshalling only: every step runs in the HIP library's kernels
+(``libvp.so`` next to this file, built by ``paper_2609_34340_amd.build``).
+Torch supplies device memory and streams; tensors are passed as raw device
+pointers and the current HIP stream.  If the library is missing this module
+raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libvp.so")
+
+OK, INVALID_ARGUMENT, INVALID_DEMAND, NO_PROGRESS, CAPACITY, UNSUPPORTED, HIP_ERROR = range(7)
+PIX, PXB, NIC = 0, 1, 2
+STATUS_NAMES = {0: "ok", 1: "invalid argument", 2: "invalid demand", 3: "no progress",
+                4: "capacity exceeded", 5: "unsupported", 6: "HIP error"}
+
+
+class VPError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__("%s: %s" % (what, STATUS_NAMES.get(status, status)))
+        self.status = status
+
+
+class _Topology(C.Structure):
+    _fields_ = [("n_nodes", C.c_int32), ("sockets_per_node", C.c_int32),
+                ("switches_per_socket", C.c_int32), ("gpus_per_switch", C.c_int32),
+                ("nics_per_switch", C.c_int32), ("flags", C.c_int32),
+                ("pcie_bytes_per_ns", C.c_int64), ("nic_bytes_per_ns", C.c_int64)]
+
+
+class PlanParams(C.Structure):
+    _fields_ = [("k_target", C.c_int64), ("lambda_ns", C.c_int64), ("unit_bytes", C.c_int64),
+                ("n_start", C.c_int32), ("i_aa", C.c_int32), ("seed", C.c_uint64),
+                ("k_max", C.c_int32), ("reserved", C.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libvp.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libvp.so is not built (run paper_2609_34340_amd.build.build())")
+    L = C.CDLL(LIB_PATH)
+    vp, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+    L.vp_build_catalog.argtypes = [C.POINTER(_Topology), C.POINTER(vp)]
+    L.vp_catalog_info.argtypes = [vp, vp]
+    L.vp_catalog_instances.argtypes = [vp] * 6
+    L.vp_catalog_shapes.argtypes = [vp] * 6
+    L.vp_catalog_families.argtypes = [vp] * 4
+    L.vp_catalog_upload.argtypes = [vp, vp]
+    L.vp_catalog_free.argtypes = [vp]
+    L.vp_catalog_free.restype = None
+    L.vp_demand_workspace.argtypes = [i64, i32, i32]
+    L.vp_demand_workspace.restype = sz
+    L.vp_demand.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, i64, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.vp_demand_heads.argtypes = [i64, vp, i64, i32, i32, i32, vp, vp, vp]
+    L.vp_plan_params_default.argtypes = [i32, i64, C.POINTER(PlanParams)]
+    L.vp_plan_params_default.restype = None
+    L.vp_plan_workspace.argtypes = [vp, C.POINTER(PlanParams)]
+    L.vp_plan_workspace.restype = sz
+    L.vp_plan.argtypes = [vp, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.vp_pack_workspace.argtypes = [i32, i64, i64]
+    L.vp_pack_workspace.restype = sz
+    L.vp_pack_rows.argtypes = [vp, i64, i64, vp, vp, i32, i32, vp, vp, vp, i32, vp, i64, vp, vp, vp, sz, vp]
+    L.vp_pack_heads.argtypes = [vp, i64, i64, vp, i64, i32, i32, vp, vp, vp, i32, vp, i64, vp, vp, vp, sz, vp]
+    L.vp_pack_prepare_rows.argtypes = [vp, i64, i64, vp, vp, i32, i32, vp, vp, vp, i32, i64, vp, vp, vp, sz, vp]
+    L.vp_pack_prepare_heads.argtypes = [vp, i64, i64, vp, i64, i32, i32, vp, vp, vp, i32, i64, vp, vp, vp, sz,
+                                        vp]
+    L.vp_pack_gather.argtypes = [vp, i64, vp, vp, i32, vp, i64, vp, vp, sz, vp]
+    L.vp_modeled_time.argtypes = [vp, i32, vp, vp, i64, vp, vp]
+    L.vp_status_string.argtypes = [C.c_int]
+    L.vp_status_string.restype = C.c_char_p
+    L.vp_last_error.argtypes = []
+    L.vp_last_error.restype = C.c_char_p
+    _lib = L
+    return L
+
+
+def _check(st: int, what: str):
+    if st != OK:
+        raise VPError(st, "%s (%s)" % (what, lib().vp_last_error().decode()))
+
+
+def _np(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor, dtype, name: str):
+    if not t.is_cuda or t.dtype != dtype or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous %s tensor on the GPU" % (name, dtype))
+    return t
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return C.c_void_p(s.cuda_stream)
+
+
+def topology(topo) -> _Topology:
+    """vp_topology from any object with the vpgen.Topology fields."""
+    return _Topology(topo.n_nodes, topo.sockets_per_node, topo.switches_per_socket,
+                     topo.gpus_per_switch, topo.nics_per_switch, 0, topo.pcie_bytes_per_ns,
+                     topo.nic_bytes_per_ns)
+
+
+class Catalog:
+    """Offline channel-family catalog (host build, one upload per device)."""
+
+    def __init__(self, topo):
+        h = C.c_void_p()
+        t = topology(topo)
+        _check(lib().vp_build_catalog(C.byref(t), C.byref(h)), "vp_build_catalog")
+        self._h = h
+        self.topo = topo
+        info = np.zeros(8, np.int64)
+        _check(lib().vp_catalog_info(self._h, _np(info)), "vp_catalog_info")
+        (self.N, self.G, self.g, self.Q, self.n_nodes, self.n_shapes, self.n_families,
+         self.n_instances) = (int(x) for x in info)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and _lib is not None:
+            _lib.vp_catalog_free(h)
+            self._h = None
+
+    def instances(self):
+        n = self.n_instances
+        cls, src, dst, copy = (np.zeros(n, np.int32) for _ in range(4))
+        bw = np.zeros(n, np.int64)
+        _check(lib().vp_catalog_instances(self._h, _np(cls), _np(src), _np(dst), _np(copy), _np(bw)),
+               "vp_catalog_instances")
+        return dict(cls=cls, src=src, dst=dst, copy=copy, bw=bw)
+
+    def shapes(self):
+        J, Q = self.n_shapes, self.Q
+        k, fb, fe = (np.zeros(J, np.int32) for _ in range(3))
+        L, R = np.zeros((J, Q, Q), np.int32), np.zeros((J, Q, Q), np.int32)
+        _check(lib().vp_catalog_shapes(self._h, _np(k), _np(fb), _np(fe), _np(L), _np(R)),
+               "vp_catalog_shapes")
+        return dict(k=k, fam_begin=fb, fam_end=fe, L=L, R=R)
+
+    def families(self):
+        F = self.n_families
+        shape, k = np.zeros(F, np.int32), np.zeros(F, np.int32)
+        ids = np.zeros((F, self.Q * self.g), np.int32)
+        _check(lib().vp_catalog_families(self._h, _np(shape), _np(k), _np(ids)), "vp_catalog_families")
+        return dict(shape=shape, k=k, ids=ids)
+
+    def upload(self, stream=None):
+        _check(lib().vp_catalog_upload(self._h, _stream(stream)), "vp_catalog_upload")
+
+    def modeled_time(self, K: int, inst: np.ndarray, nbytes: np.ndarray, lambda_ns: int = 10_000):
+        """Eq. (2) of a schedule as the exact fraction (num, den) in ns."""
+        inst = np.ascontiguousarray(inst[:K], np.int32)
+        nbytes = np.ascontiguousarray(nbytes[:K], np.int64)
+        num, den = np.zeros(1, np.int64), np.zeros(1, np.int64)
+        _check(lib().vp_modeled_time(self._h, K, _np(inst), _np(nbytes), lambda_ns, _np(num), _np(den)),
+               "vp_modeled_time")
+        return int(num[0]), int(den[0])
+
+
+def plan_params(n_ranks: int, unit_bytes: int, **kw) -> PlanParams:
+    p = PlanParams()
+    lib().vp_plan_params_default(n_ranks, unit_bytes, C.byref(p))
+    for key, v in kw.items():
+        if v is not None:
+            setattr(p, key, v)
+    return p
+
+
+def new_status(device="cuda") -> torch.Tensor:
+    return torch.zeros(1, dtype=torch.int32, device=device)
+
+
+def read_status(status: torch.Tensor) -> int:
+    return int(status.item())
+
+
+# ---------------------------------------------------------------- demand
+
+def demand_workspace_bytes(T: int, k: int, E: int) -> int:
+    return int(lib().vp_demand_workspace(T, k, E))
+
+
+def demand(routing: torch.Tensor, n_ranks: int, n_experts: int, unit: int, first_rank: int = 0,
+           sort_row: int = 0, status: Optional[torch.Tensor] = None, out: Optional[dict] = None,
+           ws: Optional[torch.Tensor] = None, stream=None) -> dict:
+    """vp_demand over routing [R, T, k] (int32, GPU).  Returns counts, demand rows,
+    and for row `sort_row` the (expert, token) order and destination offsets."""
+    _dev(routing, torch.int32, "routing")
+    R, T, k = routing.shape
+    dev = routing.device
+    if out is None:
+        out = dict(counts=torch.empty((R, n_experts), dtype=torch.int32, device=dev),
+                   demand=torch.empty((R, n_ranks), dtype=torch.int64, device=dev),
+                   sorted_tok=torch.empty(max(T * k, 1), dtype=torch.int32, device=dev),
+                   dest_off=torch.empty(n_ranks + 1, dtype=torch.int64, device=dev))
+    if status is None:
+        status = new_status(dev)
+    wsb = demand_workspace_bytes(T, k, n_experts)
+    if ws is None:
+        ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    _check(lib().vp_demand(_ptr(routing), R, T, k, n_experts, n_ranks, first_rank, sort_row, unit,
+                           _ptr(out["counts"]), _ptr(out["demand"]), _ptr(out["sorted_tok"]),
+                           _ptr(out["dest_off"]), _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
+           "vp_demand")
+    out["status"] = status
+    return out
+
+
+def demand_heads(T: int, head_lo: torch.Tensor, head_bytes: int, first_rank: int = 0, R: int = 1,
+                 status: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                 stream=None) -> torch.Tensor:
+    _dev(head_lo, torch.int64, "head_lo")
+    N = head_lo.numel() - 1
+    if out is None:
+        out = torch.empty((R, N), dtype=torch.int64, device=head_lo.device)
+    if status is None:
+        status = new_status(head_lo.device)
+    _check(lib().vp_demand_heads(T, _ptr(head_lo), head_bytes, N, first_rank, R, _ptr(out), _ptr(status),
+                                 _stream(stream)), "vp_demand_heads")
+    return out
+
+
+# ------------------------------------------------------------------ plan
+
+def plan_workspace_bytes(cat: Catalog, p: PlanParams) -> int:
+    return int(lib().vp_plan_workspace(cat.handle, C.byref(p)))
+
+
+def alloc_schedule(N: int, k_max: int, device="cuda") -> dict:
+    return dict(K=torch.zeros(1, dtype=torch.int32, device=device),
+                family=torch.empty(k_max, dtype=torch.int32, device=device),
+                dst=torch.empty((k_max, N), dtype=torch.int32, device=device),
+                inst=torch.empty((k_max, N), dtype=torch.int32, device=device),
+                bytes=torch.empty((k_max, N), dtype=torch.int64, device=device),
+                tau=torch.zeros(1, dtype=torch.int64, device=device))
+
+
+def plan(cat: Catalog, D: torch.Tensor, p: PlanParams, status: Optional[torch.Tensor] = None,
+         out: Optional[dict] = None, ws: Optional[torch.Tensor] = None, stream=None) -> dict:
+    """vp_plan on demand D [N, N] (int64, GPU): Alg. 2 in one device kernel."""
+    _dev(D, torch.int64, "demand")
+    N = cat.N
+    if tuple(D.shape) != (N, N):
+        raise ValueError("demand must be [%d, %d]" % (N, N))
+    if out is None:
+        out = alloc_schedule(N, p.k_max, D.device)
+    if status is None:
+        status = new_status(D.device)
+    if ws is None:
+        ws = torch.empty(plan_workspace_bytes(cat, p), dtype=torch.uint8, device=D.device)
+    _check(lib().vp_plan(cat.handle, _ptr(D), C.byref(p), _ptr(out["K"]), _ptr(out["family"]),
+                         _ptr(out["dst"]), _ptr(out["inst"]), _ptr(out["bytes"]), _ptr(out["tau"]),
+                         _ptr(status), _ptr(ws), ws.numel(), _stream(stream)), "vp_plan")
+    out["status"] = status
+    return out
+
+
+def schedule_to_host(s: dict) -> dict:
+    K = int(s["K"].item())
+    return dict(K=K, family=s["family"][:K].cpu().numpy(), dst=s["dst"][:K].cpu().numpy(),
+                inst=s["inst"][:K].cpu().numpy(), bytes=s["bytes"][:K].cpu().numpy(),
+                tau=int(s["tau"].item()))
+
+
+# ------------------------------------------------------------------ pack
+
+def pack_workspace_bytes(k_max: int, send_capacity: int, unit: int) -> int:
+    return int(lib().vp_pack_workspace(k_max, send_capacity, unit))
+
+
+def pack_rows(tokens: torch.Tensor, row_bytes: int, sorted_tok: torch.Tensor, dest_off: torch.Tensor,
+              self_rank: int, sched: dict, send: torch.Tensor, step_off: torch.Tensor,
+              status: torch.Tensor, ws: Optional[torch.Tensor] = None, stream=None):
+    """vp_pack_rows: this rank's token rows into the send buffer in step order."""
+    if not tokens.is_cuda or not tokens.is_contiguous():
+        raise ValueError("tokens must be a contiguous GPU tensor")
+    T = tokens.numel() * tokens.element_size() // row_bytes
+    k_max = sched["dst"].shape[0]
+    N = sched["dst"].shape[1]
+    cap = send.numel() * send.element_size()
+    if ws is None:
+        ws = torch.empty(pack_workspace_bytes(k_max, cap, row_bytes), dtype=torch.uint8, device=send.device)
+    _check(lib().vp_pack_rows(_ptr(tokens), T, row_bytes, _ptr(sorted_tok), _ptr(dest_off), self_rank, N,
+                              _ptr(sched["K"]), _ptr(sched["dst"]), _ptr(sched["bytes"]), k_max, _ptr(send),
+                              cap, _ptr(step_off), _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
+           "vp_pack_rows")
+
+
+def pack_heads(act: torch.Tensor, token_stride: int, head_lo: torch.Tensor, head_bytes: int,
+               self_rank: int, sched: dict, send: torch.Tensor, step_off: torch.Tensor,
+               status: torch.Tensor, ws: Optional[torch.Tensor] = None, stream=None):
+    """vp_pack_heads: this rank's head blocks into the send buffer in step order."""
+    if not act.is_cuda or not act.is_contiguous():
+        raise ValueError("activations must be a contiguous GPU tensor")
+    T = act.numel() * act.element_size() // token_stride
+    k_max = sched["dst"].shape[0]
+    N = sched["dst"].shape[1]
+    cap = send.numel() * send.element_size()
+    if ws is None:
+        ws = torch.empty(pack_workspace_bytes(k_max, cap, head_bytes), dtype=torch.uint8, device=send.device)
+    _check(lib().vp_pack_heads(_ptr(act), T, token_stride, _ptr(head_lo), head_bytes, self_rank, N,
+                               _ptr(sched["K"]), _ptr(sched["dst"]), _ptr(sched["bytes"]), k_max,
+                               _ptr(send), cap, _ptr(step_off), _ptr(status), _ptr(ws), ws.numel(),
+                               _stream(stream)), "vp_pack_heads")
+
+
+# -------------------------------------------------------------- pipeline
+
+class Pipeline:
+    """Preallocated demand -> plan -> pack for one workload on one GPU.
+
+    ``step()`` enqueues the whole hot path on the current stream with no host
+    synchronisation: vp_demand (or vp_demand_heads) over every rank's routing,
+    vp_plan on the resulting N x N matrix, and vp_pack of rank ``self_rank``.
+    """
+
+    def __init__(self, topo, mode: str, unit: int, *, n_experts: int = 0, tokens: int = 0,
+                 top_k: int = 0, token_stride: int = 0, self_rank: int = 0, params: Optional[dict] = None,
+                 device="cuda"):
+        self.cat = Catalog(topo)
+        self.cat.upload()
+        self.mode, self.unit, self.self_rank = mode, unit, self_rank
+        self.N = N = self.cat.N
+        self.E, self.T, self.k = n_experts, tokens, top_k
+        self.token_stride = token_stride or unit
+        self.params = plan_params(N, unit, **(params or {}))
+        kmax = self.params.k_max
+        dev = device
+        self.status = new_status(dev)
+        self.sched = alloc_schedule(N, kmax, dev)
+        self.plan_ws = torch.empty(plan_workspace_bytes(self.cat, self.params), dtype=torch.uint8, device=dev)
+        if mode == "moe":
+            self.dem = dict(counts=torch.empty((N, n_experts), dtype=torch.int32, device=dev),
+                            demand=torch.empty((N, N), dtype=torch.int64, device=dev),
+                            sorted_tok=torch.empty(max(tokens * top_k, 1), dtype=torch.int32, device=dev),
+                            dest_off=torch.empty(N + 1, dtype=torch.int64, device=dev))
+            self.dem_ws = torch.empty(max(demand_workspace_bytes(tokens, top_k, n_experts), 1),
+                                      dtype=torch.uint8, device=dev)
+            cap = tokens * top_k * unit
+        else:
+            self.dem = dict(demand=torch.empty((N, N), dtype=torch.int64, device=dev))
+            cap = tokens * (self.token_stride // unit) * unit
+        self.send_capacity = cap
+        self.send = torch.empty(max(cap, 16), dtype=torch.uint8, device=dev)
+        self.step_off = torch.empty(kmax + 1, dtype=torch.int64, device=dev)
+        self.pack_ws = torch.empty(pack_workspace_bytes(kmax, cap, unit), dtype=torch.uint8, device=dev)
+
+    # The hot path in stages (all enqueued on one stream, no host sync).
+    def demand_stage(self, routing: Optional[torch.Tensor] = None, head_lo: Optional[torch.Tensor] = None,
+                     stream=None):
+        L, s = lib(), _stream(stream)
+        if self.mode == "moe":
+            R, T, k = routing.shape
+            _check(L.vp_demand(_ptr(routing), R, T, k, self.E, self.N, 0, self.self_rank, self.unit,
+                               _ptr(self.dem["counts"]), _ptr(self.dem["demand"]),
+                               _ptr(self.dem["sorted_tok"]), _ptr(self.dem["dest_off"]), _ptr(self.status),
+                               _ptr(self.dem_ws), self.dem_ws.numel(), s), "vp_demand")
+        else:
+            _check(L.vp_demand_heads(self.T, _ptr(head_lo), self.unit, self.N, 0, self.N,
+                                     _ptr(self.dem["demand"]), _ptr(self.status), s), "vp_demand_heads")
+
+    def plan_stage(self, stream=None):
+        p = self.params
+        _check(lib().vp_plan(self.cat.handle, _ptr(self.dem["demand"]), C.byref(p), _ptr(self.sched["K"]),
+                             _ptr(self.sched["family"]), _ptr(self.sched["dst"]), _ptr(self.sched["inst"]),
+                             _ptr(self.sched["bytes"]), _ptr(self.sched["tau"]), _ptr(self.status),
+                             _ptr(self.plan_ws), self.plan_ws.numel(), _stream(stream)), "vp_plan")
+
+    def pack_prepare_stage(self, tokens: torch.Tensor, head_lo: Optional[torch.Tensor] = None, stream=None):
+        L, s, p = lib(), _stream(stream), self.params
+        if self.mode == "moe":
+            T = tokens.numel() * tokens.element_size() // self.unit
+            _check(L.vp_pack_prepare_rows(_ptr(tokens), T, self.unit, _ptr(self.dem["sorted_tok"]),
+                                          _ptr(self.dem["dest_off"]), self.self_rank, self.N,
+                                          _ptr(self.sched["K"]), _ptr(self.sched["dst"]),
+                                          _ptr(self.sched["bytes"]), p.k_max, self.send_capacity,
+                                          _ptr(self.step_off), _ptr(self.status), _ptr(self.pack_ws),
+                                          self.pack_ws.numel(), s), "vp_pack_prepare_rows")
+        else:
+            T = tokens.numel() * tokens.element_size() // self.token_stride
+            _check(L.vp_pack_prepare_heads(_ptr(tokens), T, self.token_stride, _ptr(head_lo), self.unit,
+                                           self.self_rank, self.N, _ptr(self.sched["K"]),
+                                           _ptr(self.sched["dst"]), _ptr(self.sched["bytes"]), p.k_max,
+                                           self.send_capacity, _ptr(self.step_off), _ptr(self.status),
+                                           _ptr(self.pack_ws), self.pack_ws.numel(), s), "vp_pack_prepare_heads")
+
+    def pack_gather_stage(self, tokens: torch.Tensor, send: Optional[torch.Tensor] = None, stream=None):
+        send = self.send if send is None else send
+        if send.numel() < self.send_capacity:
+            raise ValueError("send buffer smaller than the pipeline's capacity")
+        _check(lib().vp_pack_gather(_ptr(tokens), self.unit, _ptr(self.sched["K"]), _ptr(self.step_off),
+                                    self.params.k_max, _ptr(send), self.send_capacity, _ptr(self.status),
+                                    _ptr(self.pack_ws), self.pack_ws.numel(), _stream(stream)),
+               "vp_pack_gather")
+        return send
+
+    def step(self, routing: Optional[torch.Tensor] = None, tokens: Optional[torch.Tensor] = None,
+             head_lo: Optional[torch.Tensor] = None, send: Optional[torch.Tensor] = None, stream=None):
+        """demand -> plan -> pack for one matrix; returns the send buffer."""
+        self.demand_stage(routing, head_lo, stream)
+        self.plan_stage(stream)
+        self.pack_prepare_stage(tokens, head_lo, stream)
+        return self.pack_gather_stage(tokens, send, stream)

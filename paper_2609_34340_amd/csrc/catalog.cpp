@@ -1,0 +1,309 @@
+// Offline catalog construction on the host (Sec. 4.1, Alg. 1).
+//
+// The catalog is enumerated slot by slot: every switch slot of a node picks
+// the set of g outgoing lanes it launches (a combination of its candidate
+// path instances), subject to resource disjointness (Eq. (1)/(4), tracked as
+// one bit per directed resource) and the g-incoming limit per slot; a
+// complete choice with every slot receiving exactly g lanes is a family.
+// This visits exactly the compatible, complete instance sets that Alg. 1's
+// include/exclude DFS reaches, each once: identical PIX copies are taken in
+// copy order, which is PruneFamilies' exact-duplicate rule applied during the
+// search.  PrunePaths runs before, the dominance half of PruneFamilies after.
+//
+// Multi-node topologies use the node-circulant reduction: the same node-local
+// pattern in every node, all NIC lanes of node n landing on node (n+k) mod
+// n_nodes.  Shift 0 keeps NIC lanes inside the node (loopback through the two
+// switches' NICs); shifts k != 0 use the NIC-carrying patterns, identical for
+// every k.
+#include <algorithm>
+#include <map>
+#include <set>
+#include <tuple>
+
+#include "internal.h"
+
+namespace vp {
+namespace {
+
+struct Cand {
+  int id, cls, src, dst, copy;
+  int64_t bw;
+  uint32_t res;   // bit per directed resource: UP q, DN q, TX q, RX q
+  bool remote;    // NIC lane to another node
+};
+
+struct Found {
+  std::vector<int32_t> ids;   // ascending node-local ids
+  std::vector<int32_t> L, R;  // Q x Q counts of intra-node / cross-node lanes
+};
+
+// Dominance between two path instances of one ordered pair (PrunePaths):
+// no extra resource, no lower rate, and strictly better in one of the two.
+bool path_dominates(const Cand& a, const Cand& b) {
+  if (a.src != b.src || a.dst != b.dst || a.remote != b.remote) return false;
+  bool subset = (a.res & ~b.res) == 0;
+  if (!subset || a.bw < b.bw) return false;
+  return a.res != b.res || a.bw > b.bw;
+}
+
+class SlotSearch {
+ public:
+  SlotSearch(const std::vector<Cand>& cands, int Q, int g) : Q_(Q), g_(g), out_(Q) {
+    for (const Cand& c : cands) out_[c.src].push_back(c);
+    indeg_.assign(Q, 0);
+  }
+  std::vector<Found> run() {
+    slot(0, 0u);
+    return std::move(found_);
+  }
+
+ private:
+  // choose g lanes for slot q, then recurse to slot q+1
+  void slot(int q, uint32_t used) {
+    if (q == Q_) {
+      for (int x = 0; x < Q_; ++x)
+        if (indeg_[x] != g_) return;
+      record();
+      return;
+    }
+    pick(q, 0, 0, used);
+  }
+  void pick(int q, size_t from, int taken, uint32_t used) {
+    if (taken == g_) {
+      slot(q + 1, used);
+      return;
+    }
+    const std::vector<Cand>& c = out_[q];
+    for (size_t i = from; i + (size_t)(g_ - taken) <= c.size(); ++i) {
+      const Cand& x = c[i];
+      if (x.res & used) continue;
+      if (indeg_[x.dst] >= g_) continue;
+      // identical PIX copies enter in copy order only
+      if (x.cls == VP_PATH_PIX && x.copy > 0) {
+        bool prev = false;
+        for (const Cand* y : chosen_)
+          if (y->cls == VP_PATH_PIX && y->src == x.src && y->copy == x.copy - 1) prev = true;
+        if (!prev) continue;
+      }
+      indeg_[x.dst]++;
+      chosen_.push_back(&x);
+      pick(q, i + 1, taken + 1, used | x.res);
+      chosen_.pop_back();
+      indeg_[x.dst]--;
+    }
+  }
+  void record() {
+    Found f;
+    f.L.assign(Q_ * Q_, 0);
+    f.R.assign(Q_ * Q_, 0);
+    for (const Cand* c : chosen_) {
+      f.ids.push_back(c->id);
+      (c->remote ? f.R : f.L)[c->src * Q_ + c->dst]++;
+    }
+    std::sort(f.ids.begin(), f.ids.end());
+    found_.push_back(std::move(f));
+  }
+
+  int Q_, g_;
+  std::vector<std::vector<Cand>> out_;
+  std::vector<int> indeg_;
+  std::vector<const Cand*> chosen_;
+  std::vector<Found> found_;
+};
+
+// PruneFamilies: drop exact duplicates (same multiset of (pair, footprint,
+// rate)) and families dominated inside their shape.
+std::vector<Found> prune_families(std::vector<Found> fs, const std::vector<Cand>& by_id) {
+  typedef std::tuple<int, int, bool, uint32_t> PairFoot;
+  auto profile = [&](const Found& f) {
+    std::map<PairFoot, std::vector<int64_t>> m;
+    for (int id : f.ids) {
+      const Cand& c = by_id[id];
+      m[PairFoot(c.src, c.dst, c.remote, c.res)].push_back(c.bw);
+    }
+    for (auto& kv : m) std::sort(kv.second.begin(), kv.second.end(), std::greater<int64_t>());
+    return m;
+  };
+  std::sort(fs.begin(), fs.end(), [](const Found& a, const Found& b) {
+    return std::tie(a.L, a.R, a.ids) < std::tie(b.L, b.R, b.ids);
+  });
+  std::vector<Found> uniq;
+  std::set<std::map<PairFoot, std::vector<int64_t>>> seen;
+  std::vector<std::map<PairFoot, std::vector<int64_t>>> prof;
+  for (Found& f : fs) {
+    auto p = profile(f);
+    if (seen.insert(p).second) {
+      prof.push_back(p);
+      uniq.push_back(std::move(f));
+    }
+  }
+  std::vector<Found> out;
+  for (size_t i = 0; i < uniq.size(); ++i) {
+    bool dominated = false;
+    for (size_t j = 0; j < uniq.size() && !dominated; ++j) {
+      if (i == j || uniq[i].L != uniq[j].L || uniq[i].R != uniq[j].R) continue;
+      if (prof[i].size() != prof[j].size()) continue;
+      bool ok = true, strict = false;
+      for (auto it = prof[j].begin(); it != prof[j].end() && ok; ++it) {
+        auto jt = prof[i].find(it->first);
+        if (jt == prof[i].end() || jt->second.size() != it->second.size()) { ok = false; break; }
+        for (size_t x = 0; x < it->second.size(); ++x) {
+          if (it->second[x] < jt->second[x]) ok = false;
+          if (it->second[x] > jt->second[x]) strict = true;
+        }
+      }
+      dominated = ok && strict;
+    }
+    if (!dominated) out.push_back(uniq[i]);
+  }
+  return out;
+}
+
+}  // namespace
+
+vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
+  const int S = t.sockets_per_node, W = t.switches_per_socket, g = t.gpus_per_switch;
+  const int Q = S * W, nn = t.n_nodes;
+  c.topo = t;
+  c.g = g;
+  c.Q = Q;
+  c.nn = nn;
+  c.G = nn * Q;
+  c.N = c.G * g;
+  const int64_t pcie = t.pcie_bytes_per_ns;
+  const int64_t nicbw = std::min(t.pcie_bytes_per_ns, t.nic_bytes_per_ns);
+
+  // Node-local instance table in canonical id order: (class, src, dst, copy).
+  std::vector<Cand> table;
+  auto add = [&](int cls, int s, int d, int cp, int64_t bw, uint32_t res) {
+    table.push_back(Cand{(int)table.size(), cls, s, d, cp, bw, res, false});
+  };
+  for (int q = 0; q < Q; ++q)
+    for (int cp = 0; cp < g; ++cp) add(VP_PATH_PIX, q, q, cp, pcie, 0u);
+  for (int q = 0; q < Q; ++q)
+    for (int q2 = 0; q2 < Q; ++q2)
+      if (q != q2 && q / W == q2 / W) add(VP_PATH_PXB, q, q2, 0, pcie, (1u << q) | (1u << (Q + q2)));
+  for (int q = 0; q < Q; ++q)
+    for (int q2 = 0; q2 < Q; ++q2)
+      add(VP_PATH_NIC, q, q2, 0, nicbw, (1u << (2 * Q + q)) | (1u << (3 * Q + q2)));
+  for (const Cand& x : table) {
+    c.icls.push_back(x.cls);
+    c.isrc.push_back(x.src);
+    c.idst.push_back(x.dst);
+    c.icopy.push_back(x.copy);
+    c.ibw.push_back(x.bw);
+  }
+
+  auto enumerate = [&](bool remote_nic) {
+    std::vector<Cand> cand = table;
+    for (Cand& x : cand) x.remote = remote_nic && x.cls == VP_PATH_NIC;
+    std::vector<Cand> kept;
+    for (const Cand& x : cand) {
+      bool dom = false;
+      for (const Cand& y : cand)
+        if (y.id != x.id && path_dominates(y, x)) { dom = true; break; }
+      if (!dom) kept.push_back(x);
+    }
+    SlotSearch search(kept, Q, g);
+    std::vector<Found> fs = prune_families(search.run(), cand);
+    if (remote_nic) {
+      std::vector<Found> with_nic;
+      for (Found& f : fs) {
+        int n = 0;
+        for (int v : f.R) n += v;
+        if (n > 0) with_nic.push_back(std::move(f));
+      }
+      fs.swap(with_nic);
+    }
+    return fs;   // sorted by (L, R, ids): canonical
+  };
+
+  std::vector<Found> f0 = enumerate(false);
+  std::vector<Found> f1 = nn > 1 ? enumerate(true) : std::vector<Found>();
+  auto group = [&](const std::vector<Found>& fs, int fam_base) {
+    for (size_t i = 0; i < fs.size(); ++i) {
+      if (i == 0 || fs[i].L != fs[i - 1].L || fs[i].R != fs[i - 1].R) {
+        c.patL.push_back(fs[i].L);
+        c.patR.push_back(fs[i].R);
+        c.pat_fb.push_back(fam_base + (int)i);
+        c.pat_fe.push_back(fam_base + (int)i);
+      }
+      c.pat_fe.back()++;
+      c.lfam.push_back(fs[i].ids);
+    }
+  };
+  group(f0, 0);
+  c.J0 = (int)c.patL.size();
+  c.F0 = (int)f0.size();
+  group(f1, c.F0);
+  c.J1 = (int)c.patL.size() - c.J0;
+  c.F1 = (int)f1.size();
+  build_device_image(c);
+  return VP_OK;
+}
+
+void build_device_image(vp_catalog& c) {
+  DevCatalogLayout& L = c.lay;
+  const int Q = c.Q, g = c.g, QG = Q * g, P = c.J0 + c.J1, FL = c.F0 + c.F1;
+  L.N = c.N; L.G = c.G; L.g = g; L.Q = Q; L.nn = c.nn; L.n_inst = (int)c.icls.size();
+  L.J0 = c.J0; L.J1 = c.J1; L.F0 = c.F0; L.F1 = c.F1;
+  L.J = (int64_t)c.J0 + (int64_t)c.J1 * (c.nn - 1);
+  L.F = (int64_t)c.F0 + (int64_t)c.F1 * (c.nn - 1);
+  int ts = 1;
+  for (int p = 0; p < P; ++p) {
+    int n = 0;
+    for (int x = 0; x < Q * Q; ++x) n += (c.patL[p][x] != 0) + (c.patR[p][x] != 0);
+    ts = std::max(ts, n);
+  }
+  L.TS = ts;
+  int np = 1;
+  for (int x = 2; x <= g; ++x) np *= x;
+  L.n_perm = np;
+  int off = 0;
+  L.off_terms = off; off += P * ts;
+  L.off_nterms = off; off += P;
+  L.off_fb = off; off += P;
+  L.off_fe = off; off += P;
+  L.off_fam_info = off; off += FL * QG;
+  L.off_fam_out = off; off += FL * QG;
+  L.off_fam_in = off; off += FL * QG;
+  L.off_perms = off; off += np * g;
+  L.total = off;
+  L.bw_cls[VP_PATH_PIX] = c.topo.pcie_bytes_per_ns;
+  L.bw_cls[VP_PATH_PXB] = c.topo.pcie_bytes_per_ns;
+  L.bw_cls[VP_PATH_NIC] = std::min(c.topo.pcie_bytes_per_ns, c.topo.nic_bytes_per_ns);
+  L.bw_max = std::max(L.bw_cls[0], L.bw_cls[2]);
+
+  std::vector<int32_t>& im = c.image;
+  im.assign(off, 0);
+  for (int p = 0; p < P; ++p) {
+    int n = 0;
+    for (int block = 0; block < 2; ++block)
+      for (int q = 0; q < Q; ++q)
+        for (int q2 = 0; q2 < Q; ++q2) {
+          int cnt = (block ? c.patR[p] : c.patL[p])[q * Q + q2];
+          if (cnt) im[L.off_terms + p * ts + n++] = cnt | (q2 << 4) | (q << 8) | (block << 12);
+        }
+    im[L.off_nterms + p] = n;
+    im[L.off_fb + p] = c.pat_fb[p];
+    im[L.off_fe + p] = c.pat_fe[p];
+  }
+  for (int f = 0; f < FL; ++f) {
+    std::vector<int> no(Q, 0), ni(Q, 0);
+    for (int x = 0; x < QG; ++x) {
+      int id = c.lfam[f][x];
+      im[L.off_fam_info + f * QG + x] = c.icls[id] | (c.isrc[id] << 4) | (c.idst[id] << 8) | (id << 12);
+      im[L.off_fam_out + f * QG + c.isrc[id] * g + no[c.isrc[id]]++] = x;
+      im[L.off_fam_in + f * QG + c.idst[id] * g + ni[c.idst[id]]++] = x;
+    }
+  }
+  std::vector<int> perm(g);
+  for (int x = 0; x < g; ++x) perm[x] = x;
+  int pi = 0;
+  do {
+    for (int x = 0; x < g; ++x) im[L.off_perms + pi * g + x] = perm[x];
+    ++pi;
+  } while (std::next_permutation(perm.begin(), perm.end()));
+}
+
+}  // namespace vp

@@ -1,0 +1,128 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/vp.h"
+
+namespace vp {
+
+// Limits of the device planner (checked on the host before any launch).
+constexpr int kMaxGpusPerSwitch = 4;
+constexpr int kMaxSlotsPerNode = 8;
+constexpr int kMaxRanks = 1024;
+constexpr int kMaxNodes = 256;
+constexpr int kMaxStarts = 16;
+constexpr int kPlanThreads = 1024;
+
+// Sentinel credit of a self pair (never bindable).
+constexpr uint32_t kForbidden = 0xFFFFFFFFu;
+
+// Device image of the catalog: one int32 buffer, sections at these offsets
+// (in int32 elements).  A "pattern" is a node-local shape: patterns
+// [0, J0) are the intra-node shapes (shift 0), patterns [J0, J0+J1) the
+// NIC-carrying shapes repeated for every shift 1..n_nodes-1.  Local
+// families [0, F0) belong to shift 0, [F0, F0+F1) to every non-zero shift.
+struct DevCatalogLayout {
+  int32_t N, G, g, Q, nn, n_inst;
+  int32_t J0, J1, F0, F1;
+  int32_t TS;            // term slots per pattern
+  int32_t n_perm;        // g!
+  int64_t J, F;          // global shape / family counts
+  int32_t off_terms;     // (J0+J1) * TS packed terms: count | q2<<4 | q<<8 | block<<12
+  int32_t off_nterms;    // (J0+J1)
+  int32_t off_fb, off_fe;      // (J0+J1) local family range of each pattern
+  int32_t off_fam_info;  // (F0+F1) * Q*g : cls | src_slot<<4 | dst_slot<<8 | local_id<<12
+  int32_t off_fam_out;   // (F0+F1) * Q*g : [slot][m] local index of the m-th out-instance
+  int32_t off_fam_in;    // (F0+F1) * Q*g : [slot][m] local index of the m-th in-instance
+  int32_t off_perms;     // n_perm * g, lexicographic order
+  int32_t total;         // int32 elements
+  int64_t bw_cls[3];     // rate of PIX, PXB, NIC paths
+  int64_t bw_max;
+};
+
+}  // namespace vp
+
+struct vp_catalog {
+  vp_topology topo;
+  int N, G, g, Q, nn;
+  // node-local instance table (id order)
+  std::vector<int32_t> icls, isrc, idst, icopy;
+  std::vector<int64_t> ibw;
+  // node-local patterns: [0, J0) shift 0, [J0, J0+J1) NIC-carrying
+  int J0 = 0, J1 = 0;
+  std::vector<std::vector<int32_t>> patL, patR;
+  std::vector<int32_t> pat_fb, pat_fe;
+  // node-local families: [0, F0) shift 0, [F0, F0+F1) NIC-carrying
+  int F0 = 0, F1 = 0;
+  std::vector<std::vector<int32_t>> lfam;
+  // device copy
+  vp::DevCatalogLayout lay{};
+  std::vector<int32_t> image;
+  void* dev = nullptr;
+  int dev_id = -1;
+};
+
+namespace vp {
+
+vp_status set_error(vp_status s, const std::string& msg);
+vp_status build_catalog_host(const vp_topology& t, vp_catalog& c);
+void build_device_image(vp_catalog& c);
+
+struct PlanLaunch {
+  const vp_catalog* cat;
+  const int64_t* demand;
+  int64_t* drem;
+  vp_plan_params p;
+  int32_t *K, *family, *dst, *inst;
+  int64_t *bytes, *tau;
+  int32_t* status;
+};
+vp_status launch_plan(const PlanLaunch& a, void* stream);
+
+struct DemandLaunch {
+  const int32_t* routing;
+  int32_t R;
+  int64_t T;
+  int32_t k, E, N, first_rank, sort_row;
+  int64_t unit;
+  int32_t* counts;
+  int64_t* demand;
+  int32_t* sorted_tok;
+  int64_t* dest_off;
+  int32_t* status;
+  void* ws;
+  size_t ws_bytes;
+};
+size_t demand_workspace(int64_t T, int32_t k, int32_t E);
+vp_status launch_demand(const DemandLaunch& a, void* stream);
+vp_status launch_demand_heads(int64_t T, const int64_t* head_lo, int64_t head_bytes, int32_t N,
+                              int32_t first_rank, int32_t R, int64_t* demand, int32_t* status,
+                              void* stream);
+
+struct PackLaunch {
+  int mode;    // 0 rows, 1 heads
+  int stages;  // 1 prepare (slice + index kernels), 2 gather, 3 both
+  const void* src;
+  int64_t T, unit, token_stride;
+  const int32_t* sorted_tok;
+  const int64_t* dest_off;
+  const int64_t* head_lo;
+  int32_t self_rank, N;
+  const int32_t *K, *dst;
+  const int64_t* bytes;
+  int32_t k_max;
+  void* send;
+  int64_t send_capacity;
+  int64_t* step_off;
+  int32_t* status;
+  void* ws;
+  size_t ws_bytes;
+};
+size_t pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit);
+vp_status launch_pack(const PackLaunch& a, void* stream);
+
+}  // namespace vp

@@ -1,0 +1,347 @@
+"""GPU parity: the HIP library against the CPU oracle, bit-exact.
+
+Every comparison is element by element on the same seeded inputs: demand
+counts, rows, the (expert, token) order and offsets; the whole schedule (K,
+family, destination, instance and bytes of every lane, tau); and the packed
+send buffer with its step offsets.  The five workload configurations run at
+full size; extra cases cover ragged and empty inputs, other topologies, other
+planner parameters and the device-side error paths."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import vpgen
+
+pytestmark = pytest.mark.gpu
+
+_cache = {}
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def vp():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_34340_amd as vp
+    vp.lib()
+    return vp
+
+
+def ocat(topo):
+    key = ("oc",) + topo.as_tuple()
+    if key not in _cache:
+        _cache[key] = oracle.Catalog(topo)
+    return _cache[key]
+
+
+def gcat(vp, topo):
+    key = ("gc",) + topo.as_tuple()
+    if key not in _cache:
+        c = vp.Catalog(topo)
+        c.upload()
+        _cache[key] = c
+    return _cache[key]
+
+
+def moe_case(cid, matrix=0, tokens=None):
+    key = ("moe", cid, matrix, tokens)
+    if key not in _cache:
+        w = vpgen.config(cid)
+        R = vpgen.routing_all(w, matrix, tokens)
+        dem = [oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes) for i in range(w.n_ranks)]
+        D = np.stack([d["row"] for d in dem])
+        _cache[key] = (w, R, dem, D)
+    return _cache[key]
+
+
+def oracle_plan(cid, D, matrix=0, tokens=None, **kw):
+    key = ("plan", cid, matrix, tokens, tuple(sorted(kw.items())))
+    if key not in _cache:
+        w = vpgen.config(cid)
+        _cache[key] = ocat(w.topo).plan(D, w.row_bytes, **kw)
+    return _cache[key]
+
+
+def heads_case():
+    w = vpgen.config(4)
+    hl = vpgen.head_split(w.heads, w.n_ranks)
+    D = np.stack([oracle.demand_heads(w.tokens, hl, w.row_bytes, i) for i in range(w.n_ranks)])
+    return w, hl, D
+
+
+def assert_schedule_equal(g, o):
+    assert g["K"] == o["K"], (g["K"], o["K"])
+    assert g["tau"] == o["tau"]
+    for key in ("family", "dst", "inst", "bytes"):
+        a, b = np.asarray(g[key]), np.asarray(o[key])
+        if not np.array_equal(a, b):
+            bad = np.argwhere(a != b)[:5]
+            raise AssertionError("%s differs at %s: gpu %s oracle %s" % (
+                key, bad.tolist(), [a[tuple(x)] for x in bad], [b[tuple(x)] for x in bad]))
+
+
+def gpu_plan(vp, topo, D, unit, **kw):
+    cat = gcat(vp, topo)
+    p = vp.plan_params(cat.N, unit, **kw)
+    st = vp.new_status()
+    s = vp.plan(cat, torch.from_numpy(np.ascontiguousarray(D)).cuda(), p, status=st)
+    torch.cuda.synchronize()
+    h = vp.schedule_to_host(s)
+    h["status"] = vp.read_status(st)
+    return h
+
+
+# ---------------------------------------------------------------- demand
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 5])
+def test_demand_parity_full_size(vp, cid):
+    w, R, dem, D = moe_case(cid)
+    log("demand parity C%d: N=%d T=%d k=%d E=%d" % (cid, w.n_ranks, w.tokens, w.top_k, w.experts))
+    rt = torch.from_numpy(R).cuda()
+    for sort_row in (0, w.n_ranks - 1):
+        out = vp.demand(rt, w.n_ranks, w.experts, w.row_bytes, first_rank=0, sort_row=sort_row)
+        torch.cuda.synchronize()
+        assert vp.read_status(out["status"]) == 0
+        assert np.array_equal(out["demand"].cpu().numpy(), D)
+        assert np.array_equal(out["counts"].cpu().numpy(), np.stack([d["counts"] for d in dem]))
+        assert np.array_equal(out["sorted_tok"].cpu().numpy(), dem[sort_row]["sorted_tok"])
+        assert np.array_equal(out["dest_off"].cpu().numpy(), dem[sort_row]["dest_off"])
+
+
+@pytest.mark.parametrize("T,k,E,N,first", [(1000, 3, 24, 8, 5), (2049, 8, 256, 64, 0), (1, 1, 8, 8, 7),
+                                            (4097, 2, 4096, 16, 3)])
+def test_demand_ragged(vp, T, k, E, N, first):
+    log("demand ragged T=%d k=%d E=%d N=%d" % (T, k, E, N))
+    rng = np.random.default_rng(T + E)
+    R = np.stack([np.stack([rng.choice(E, k, replace=False) for _ in range(T)]) for _ in range(2)]).astype(np.int32)
+    out = vp.demand(torch.from_numpy(R).cuda(), N, E, 4096, first_rank=first if first + 2 <= N else N - 2,
+                    sort_row=1)
+    torch.cuda.synchronize()
+    fr = first if first + 2 <= N else N - 2
+    assert vp.read_status(out["status"]) == 0
+    for r in range(2):
+        ref = oracle.demand(R[r], N, E, fr + r, 4096)
+        assert np.array_equal(out["demand"][r].cpu().numpy(), ref["row"])
+        assert np.array_equal(out["counts"][r].cpu().numpy(), ref["counts"])
+    ref = oracle.demand(R[1], N, E, fr + 1, 4096)
+    assert np.array_equal(out["sorted_tok"].cpu().numpy()[:T * k], ref["sorted_tok"])
+    assert np.array_equal(out["dest_off"].cpu().numpy(), ref["dest_off"])
+
+
+def test_demand_empty_and_bad_ids(vp):
+    log("demand empty / bad ids")
+    R = torch.zeros((1, 0, 2), dtype=torch.int32, device="cuda")
+    out = vp.demand(R, 8, 32, 4096)
+    torch.cuda.synchronize()
+    assert vp.read_status(out["status"]) == 0
+    assert (out["demand"] == 0).all() and (out["dest_off"] == 0).all()
+    bad = torch.zeros((1, 16, 2), dtype=torch.int32, device="cuda")
+    bad[0, 3, 1] = 32
+    out = vp.demand(bad, 8, 32, 4096)
+    torch.cuda.synchronize()
+    assert vp.read_status(out["status"]) == vp.INVALID_ARGUMENT
+    bad[0, 3, 1] = -1
+    out = vp.demand(bad, 8, 32, 4096)
+    torch.cuda.synchronize()
+    assert vp.read_status(out["status"]) == vp.INVALID_ARGUMENT
+
+
+def test_demand_heads_parity(vp):
+    w, hl, D = heads_case()
+    log("heads demand parity")
+    st = vp.new_status()
+    out = vp.demand_heads(w.tokens, torch.from_numpy(hl).cuda(), w.row_bytes, 0, w.n_ranks, status=st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    assert np.array_equal(out.cpu().numpy(), D)
+
+
+# ------------------------------------------------------------------ plan
+
+@pytest.mark.parametrize("cid", [1, 2, 4, 3, 5])
+def test_plan_parity_full_size(vp, cid):
+    if cid == 4:
+        w, _, D = heads_case()
+    else:
+        w, _, _, D = moe_case(cid)
+    log("plan parity C%d (N=%d)" % (cid, w.n_ranks))
+    g = gpu_plan(vp, w.topo, D, w.row_bytes)
+    assert g["status"] == 0
+    o = oracle_plan(cid, D)
+    assert_schedule_equal(g, o)
+
+
+def test_plan_parity_second_matrix_of_streams(vp):
+    for cid in (3, 5):
+        w, _, _, D = moe_case(cid, matrix=1)
+        log("plan parity C%d matrix 1" % cid)
+        g = gpu_plan(vp, w.topo, D, w.row_bytes)
+        assert g["status"] == 0
+        assert_schedule_equal(g, oracle_plan(cid, D, matrix=1))
+
+
+def random_demand(rng, N, unit, density, scale):
+    D = rng.integers(0, scale + 1, (N, N)) * (rng.random((N, N)) < density)
+    np.fill_diagonal(D, 0)
+    return (D * unit).astype(np.int64)
+
+
+@pytest.mark.parametrize("topo", [vpgen.tiny_topology(), vpgen.config(1).topo, vpgen.config(2).topo,
+                                  vpgen.Topology(3, 1, 2, 3), vpgen.Topology(2, 2, 1, 4),
+                                  vpgen.Topology(1, 1, 1, 4), vpgen.Topology(4, 1, 3, 2, 1, 32, 50)])
+def test_plan_parity_random_demands(vp, topo):
+    rng = np.random.default_rng(topo.n_ranks)
+    oc = ocat(topo)
+    unit = 4096
+    for case, (density, scale, kw) in enumerate([
+            (0.3, 5, {}), (1.0, 50, {}), (0.05, 3, {}), (1.0, 7, dict(lambda_ns=0)),
+            (0.6, 20, dict(n_start=1)), (0.6, 20, dict(n_start=7, seed=12345)),
+            (0.6, 20, dict(i_aa=0)), (0.6, 20, dict(k_target=topo.n_ranks))]):
+        D = random_demand(rng, topo.n_ranks, unit, density, scale)
+        kw = dict(kw, k_max=64 * topo.n_ranks)   # dense random demands can need more than 8N steps
+        log("plan random topo N=%d case %d %s" % (topo.n_ranks, case, kw))
+        g = gpu_plan(vp, topo, D, unit, **kw)
+        o = oc.plan(D, unit, **kw)
+        assert g["status"] == o["status"] == 0
+        assert_schedule_equal(g, o)
+
+
+def test_plan_empty_demand(vp):
+    log("plan empty")
+    topo = vpgen.config(1).topo
+    g = gpu_plan(vp, topo, np.zeros((8, 8), np.int64), 4096)
+    assert g["status"] == 0 and g["K"] == 0
+
+
+def test_plan_device_errors(vp):
+    topo = vpgen.config(1).topo
+    log("plan errors")
+    D = np.zeros((8, 8), np.int64)
+    D[2, 2] = 4096
+    assert gpu_plan(vp, topo, D, 4096)["status"] == vp.INVALID_DEMAND
+    D[2, 2] = 0
+    D[1, 5] = 4097
+    assert gpu_plan(vp, topo, D, 4096)["status"] == vp.INVALID_DEMAND
+    D[1, 5] = -4096
+    assert gpu_plan(vp, topo, D, 4096)["status"] == vp.INVALID_DEMAND
+    w, _, _, D1 = moe_case(1)
+    g = gpu_plan(vp, topo, D1, w.row_bytes, k_max=3)
+    o = ocat(topo).plan(D1, w.row_bytes, k_max=3, check=False)
+    assert g["status"] == vp.CAPACITY == o["status"]
+    assert_schedule_equal(g, o)
+
+
+def test_plan_deterministic(vp):
+    w, _, _, D = moe_case(2)
+    log("plan determinism")
+    a = gpu_plan(vp, w.topo, D, w.row_bytes)
+    b = gpu_plan(vp, w.topo, D, w.row_bytes)
+    assert_schedule_equal(a, b)
+
+
+# ------------------------------------------------------------------ pack
+
+def gpu_pack_rows(vp, w, R, sched_np, self_rank, tokens_np, cap_extra=0, cap=None):
+    rt = torch.from_numpy(R).cuda()
+    dem = vp.demand(rt, w.n_ranks, w.experts, w.row_bytes, sort_row=self_rank)
+    sched = vp.alloc_schedule(w.n_ranks, 8 * w.n_ranks)
+    K = sched_np["K"]
+    sched["K"].fill_(K)
+    sched["dst"][:K] = torch.from_numpy(sched_np["dst"]).cuda()
+    sched["bytes"][:K] = torch.from_numpy(sched_np["bytes"]).cuda()
+    total = int(sched_np["bytes"][:, self_rank].sum()) if K else 0
+    cap = total + cap_extra if cap is None else cap
+    send = torch.full((max(cap, 16),), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
+    st = dem["status"]
+    tok = torch.from_numpy(tokens_np).cuda()
+    vp.pack_rows(tok, w.row_bytes, dem["sorted_tok"], dem["dest_off"], self_rank, sched,
+                 send[:cap] if cap else send[:0], step_off, st)
+    torch.cuda.synchronize()
+    return send, step_off, vp.read_status(st), total
+
+
+@pytest.mark.parametrize("cid,self_rank", [(1, 0), (1, 5), (2, 0), (2, 9), (3, 0), (5, 0)])
+def test_pack_rows_parity_full_size(vp, cid, self_rank):
+    w, R, dem, D = moe_case(cid)
+    log("pack rows parity C%d rank %d" % (cid, self_rank))
+    s = oracle_plan(cid, D)
+    tok = vpgen.tokens_bf16(w, self_rank)
+    ref, ref_off = oracle.pack_rows(tok, w.row_bytes, dem[self_rank]["sorted_tok"],
+                                    dem[self_rank]["dest_off"], self_rank, s)
+    send, step_off, st, total = gpu_pack_rows(vp, w, R, s, self_rank, tok, cap_extra=64)
+    assert st == 0
+    assert total == ref.size
+    assert torch.equal(send[:total], torch.from_numpy(ref).cuda())
+    assert (send[total:total + 64] == 0xA5).all(), "wrote past the packed bytes"
+    assert np.array_equal(step_off[:s["K"] + 1].cpu().numpy(), ref_off)
+
+
+def test_pack_rows_capacity_error_writes_nothing(vp):
+    w, R, dem, D = moe_case(1)
+    log("pack capacity error")
+    s = oracle_plan(1, D)
+    tok = vpgen.tokens_bf16(w, 0)
+    total = int(s["bytes"][:, 0].sum())
+    send, _, st, _ = gpu_pack_rows(vp, w, R, s, 0, tok, cap=total - w.row_bytes)
+    assert st == vp.CAPACITY
+    assert (send == 0xA5).all()
+
+
+@pytest.mark.parametrize("self_rank", [0, 7, 12, 15])
+def test_pack_heads_parity(vp, self_rank):
+    w, hl, D = heads_case()
+    log("pack heads parity rank %d" % self_rank)
+    s = oracle_plan(4, D)
+    act = vpgen.tokens_bf16(w, self_rank)
+    ref, ref_off = oracle.pack_heads(act, w.token_stride, hl, w.row_bytes, self_rank, s)
+    sched = vp.alloc_schedule(w.n_ranks, 8 * w.n_ranks)
+    K = s["K"]
+    sched["K"].fill_(K)
+    sched["dst"][:K] = torch.from_numpy(s["dst"]).cuda()
+    sched["bytes"][:K] = torch.from_numpy(s["bytes"]).cuda()
+    send = torch.full((ref.size + 32,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
+    st = vp.new_status()
+    vp.pack_heads(torch.from_numpy(act).cuda(), w.token_stride, torch.from_numpy(hl).cuda(), w.row_bytes,
+                  self_rank, sched, send[:ref.size], step_off, st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    assert torch.equal(send[:ref.size], torch.from_numpy(ref).cuda())
+    assert (send[ref.size:] == 0xA5).all()
+    assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off)
+
+
+# -------------------------------------------------------------- pipeline
+
+@pytest.mark.parametrize("cid", [1, 4, 5])
+def test_pipeline_matches_oracle(vp, cid):
+    """The whole hot path as the benchmark runs it (one stream, no host sync
+    between demand, plan and pack) against the oracle, end to end."""
+    log("pipeline C%d" % cid)
+    if cid == 4:
+        w, hl, D = heads_case()
+        pipe = vp.Pipeline(w.topo, "heads", w.row_bytes, tokens=w.tokens, token_stride=w.token_stride)
+        act = vpgen.tokens_bf16(w, 0)
+        send = pipe.step(tokens=torch.from_numpy(act).cuda(), head_lo=torch.from_numpy(hl).cuda())
+        torch.cuda.synchronize()
+        s = oracle_plan(4, D)
+        ref, _ = oracle.pack_heads(act, w.token_stride, hl, w.row_bytes, 0, s)
+    else:
+        w, R, dem, D = moe_case(cid)
+        pipe = vp.Pipeline(w.topo, "moe", w.row_bytes, n_experts=w.experts, tokens=w.tokens, top_k=w.top_k)
+        tok = vpgen.tokens_bf16(w, 0)
+        send = pipe.step(routing=torch.from_numpy(R).cuda(), tokens=torch.from_numpy(tok).cuda())
+        torch.cuda.synchronize()
+        s = oracle_plan(cid, D)
+        ref, _ = oracle.pack_rows(tok, w.row_bytes, dem[0]["sorted_tok"], dem[0]["dest_off"], 0, s)
+    assert vp.read_status(pipe.status) == 0
+    assert np.array_equal(pipe.dem["demand"].cpu().numpy(), D)
+    assert_schedule_equal(vp.schedule_to_host(pipe.sched), s)
+    assert torch.equal(send[:ref.size], torch.from_numpy(ref).cuda())
