@@ -6,18 +6,23 @@
 //   1. shape scores, Eq. (5)-(6), from node-block aggregates kept in LDS:
 //      A = sum over nodes of the diagonal node block of D-hat and B_k = sum of
 //      the blocks (n, n+k).  A shape (k, L, R) scores sum A.L + sum B_k.R,
-//      which equals sum D-hat.M (the aggregates are updated incrementally by
-//      each activation's lanes, so D-hat itself is never materialised);
-//      argmax with ties to the lowest shape index via one packed 64-bit key;
-//   2. for the families of the best shape: the binding credits
-//      h' = min(D^rem_ij, cap) (Eq. (7) scaled by tau) of every instance and
-//      endpoint pair are gathered into LDS once;
-//   3. MultiStartAA (Eq. (8)): one wavefront per (family, start) builds the
-//      start, runs the alternating source / destination halves (all groups of
-//      a half in parallel across lanes) and reports F and the slowest lane;
+//      which equals sum D-hat.M.  The aggregates are kept in units of the
+//      pack granule as int32 (every demand entry is a whole number of units,
+//      so scores keep their order).  One thread scores one node-local pattern
+//      over a range of node shifts: base(p) from A plus the best R(k, p) of
+//      its range; every thread's candidate carries its own shape index, so
+//      one argmax over the packed 64-bit keys (ties to the lowest index)
+//      selects the shape;
+//   2. for the families of the best shape: the cluster-level out/in lists of
+//      every group and the binding credits h' = min(D^rem_ij, cap) (Eq. (7)
+//      scaled by tau) of every instance and endpoint pair, into LDS;
+//   3. MultiStartAA (Eq. (8)): one wavefront per (family, start).  Each lane
+//      owns up to a few groups for both AA halves and keeps their source and
+//      destination assignments in registers, so a half-step is one LDS round
+//      trip (read the other side, read the credit rows, write back);
 //   4. Evaluate (Eq. (9)-(10)) and the exact utility argmax in 128-bit;
-//   5. the activation is appended and subtracted from D^rem (global, L2
-//      resident) and from the aggregates.
+//   5. the activation is appended and D^rem (global memory, touched by this
+//      one workgroup only, so its CU's L1 keeps it coherent) is updated.
 // No host round trip happens between iterations.
 #include <hip/hip_runtime.h>
 
@@ -30,29 +35,21 @@ namespace {
 
 constexpr int kWaves = kPlanThreads / 64;
 constexpr int kMaxQG = kMaxSlotsPerNode * kMaxGpusPerSwitch;   // lanes per node
-constexpr int kMaxPerm = 24;                                   // 4!
+constexpr int kMaxLTerms = 3 * kMaxSlotsPerNode;   // PIX, PXB and NIC entries of one diagonal block
 
 struct PairRes {
   int64_t F;
   int64_t xmax[3];
 };
 
-struct ChunkFam {
-  int32_t f, k;
-  int32_t info[kMaxQG];      // cls | src_slot<<4 | dst_slot<<8 | local_id<<12
-  uint8_t outl[kMaxQG];      // [slot][m] local index
-  uint8_t inl[kMaxQG];
-};
-
 struct Shared {
   uint64_t key;
-  int64_t total_rem, S, Lmax, tau;
+  int64_t total_rem, Lmax, tau, total_units;
   int64_t cap[3];
+  // best candidate so far in this iteration
   int64_t best_S, best_xm, best_bm;
-  int32_t K, err, best_valid, best_f, best_k, copy_pair;
-  int32_t fam_begin, fam_end;
-  int64_t red[kWaves + 1];
-  uint8_t perms[kMaxPerm * kMaxGpusPerSwitch];
+  int32_t best_valid, best_f, best_k, best_c, best_s, best_chunk;
+  int32_t K, err;
 };
 
 struct PlanArgs {
@@ -64,11 +61,13 @@ struct PlanArgs {
   uint64_t seed;
   uint64_t odd_inv, odd_lim;
   int32_t unit_shift;
-  int32_t n_start, i_aa, k_max, FC;
+  int32_t n_start, i_aa, k_max, FC, KC;
   int32_t *K, *family, *dst, *inst;
   int64_t *bytes, *tau;
   int32_t* status;
-  int32_t o_rinfo, o_agg, o_terms, o_nterms, o_base, o_cf, o_pair, o_best, o_sh, o_hp, o_sl, o_dl;
+  // LDS layout (byte offsets)
+  int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo, o_finl;
+  int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_hp, o_sl, o_dl, o_bsl, o_bdl, o_bx;
 };
 
 // ------------------------------------------------------------------ helpers
@@ -79,21 +78,14 @@ __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__device__ inline int64_t wave_sum(int64_t v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-__device__ inline int64_t wave_max(int64_t v) {
-  for (int o = 32; o > 0; o >>= 1) v = max(v, (int64_t)__shfl_xor(v, o));
-  return v;
-}
-__device__ inline uint64_t wave_max_u(uint64_t v) {
-  for (int o = 32; o > 0; o >>= 1) {
-    uint64_t w = __shfl_xor(v, o);
-    v = w > v ? w : v;
-  }
-  return v;
-}
+// Whole-wavefront reductions of the device library (DPP based); every lane
+// receives the result.
+extern "C" __device__ __attribute__((const)) long long __ockl_wfred_add_i64(long long);
+extern "C" __device__ __attribute__((const)) long long __ockl_wfred_max_i64(long long);
+extern "C" __device__ __attribute__((const)) unsigned long long __ockl_wfred_max_u64(unsigned long long);
+__device__ inline int64_t wave_sum(int64_t v) { return __ockl_wfred_add_i64(v); }
+__device__ inline int64_t wave_max(int64_t v) { return __ockl_wfred_max_i64(v); }
+__device__ inline uint64_t wave_max_u(uint64_t v) { return __ockl_wfred_max_u64(v); }
 
 // SplitMix64 (Steele, Lea, Flood 2014): key absorbs the fields one at a time.
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
@@ -114,220 +106,291 @@ __device__ inline bool utility_greater(int64_t S1, int64_t x1, int64_t b1, int64
   return lhs > rhs;
 }
 
-struct Fam {
-  const ChunkFam* cf;
-  const int32_t* rinfo;   // rank -> node<<8 | slot<<4 | local
-  int Q, g, QG, nn, k;
-  __device__ int node_of(int t) const { return rinfo[t] >> 8; }
-  __device__ int src_group(int t) const {
-    int n = node_of(t);
-    return n * Q + ((cf->info[t - n * QG] >> 4) & 15);
+// Lexicographic permutations of g elements.
+template <int g>
+struct Perms;
+template <>
+struct Perms<2> {
+  static constexpr int n = 2;
+  __device__ static int at(int p, int m) { return p ? 1 - m : m; }
+};
+template <>
+struct Perms<3> {
+  static constexpr int n = 6;
+  __device__ static int at(int p, int m) {
+    constexpr unsigned char t[6][3] = {{0, 1, 2}, {0, 2, 1}, {1, 0, 2}, {1, 2, 0}, {2, 0, 1}, {2, 1, 0}};
+    return t[p][m];
   }
-  __device__ int dst_group(int t) const {
-    int n = node_of(t);
-    int info = cf->info[t - n * QG];
-    int dn = ((info & 15) == VP_PATH_NIC && k) ? (n + k) % nn : n;
-    return dn * Q + ((info >> 8) & 15);
-  }
-  __device__ int cls(int t) const { return cf->info[t - node_of(t) * QG] & 15; }
-  // the m-th out-instance of group a (family order)
-  __device__ int out_t(int a, int m) const {
-    int n = a / Q, q = a - n * Q;
-    return n * QG + cf->outl[q * g + m];
-  }
-  // the in-instances of group d in family order (ascending instance index)
-  __device__ void in_list(int d, int* tl) const {
-    int n = d / Q, q = d - n * Q;
-    for (int m = 0; m < g; ++m) {
-      int idx = cf->inl[q * g + m];
-      int c = cf->info[idx] & 15;
-      int sn = (c == VP_PATH_NIC && k) ? (n - k + nn) % nn : n;
-      tl[m] = sn * QG + idx;
-    }
-    for (int m = 1; m < g; ++m)
-      for (int x = m; x > 0 && tl[x - 1] > tl[x]; --x) {
-        int t = tl[x];
-        tl[x] = tl[x - 1];
-        tl[x - 1] = t;
-      }
+};
+template <>
+struct Perms<4> {
+  static constexpr int n = 24;
+  __device__ static int at(int p, int m) {
+    constexpr unsigned char t[24][4] = {
+        {0, 1, 2, 3}, {0, 1, 3, 2}, {0, 2, 1, 3}, {0, 2, 3, 1}, {0, 3, 1, 2}, {0, 3, 2, 1},
+        {1, 0, 2, 3}, {1, 0, 3, 2}, {1, 2, 0, 3}, {1, 2, 3, 0}, {1, 3, 0, 2}, {1, 3, 2, 0},
+        {2, 0, 1, 3}, {2, 0, 3, 1}, {2, 1, 0, 3}, {2, 1, 3, 0}, {2, 3, 0, 1}, {2, 3, 1, 0},
+        {3, 0, 1, 2}, {3, 0, 2, 1}, {3, 1, 0, 2}, {3, 1, 2, 0}, {3, 2, 0, 1}, {3, 2, 1, 0}};
+    return t[p][m];
   }
 };
 
-// Self-binding repair: per group, each self-bound intra-group instance (in
-// out-list order) trades destinations with the first other unprotected
-// in-instance of the group, else sources with the first other unprotected
-// out-instance.
-__device__ void repair(const Fam& fm, uint8_t* SL, uint8_t* DL, int G, int protect, int lane) {
-  const int g = fm.g;
-  for (int a = lane; a < G; a += 64) {
-    int o[kMaxGpusPerSwitch], tl[kMaxGpusPerSwitch];
-    for (int m = 0; m < g; ++m) o[m] = fm.out_t(a, m);
-    fm.in_list(a, tl);
+// Local family descriptor word: cls | src_slot<<2 | dst_slot<<5 | out_pos<<8 | local_id<<10
+__device__ inline int d_cls(uint32_t w) { return w & 3; }
+__device__ inline int d_ss(uint32_t w) { return (w >> 2) & 7; }
+__device__ inline int d_ds(uint32_t w) { return (w >> 5) & 7; }
+__device__ inline int d_opos(uint32_t w) { return (w >> 8) & 3; }
+__device__ inline int d_id(uint32_t w) { return (int)(w >> 10); }
+
+// Per-family working set of the current chunk.
+struct FamCtx {
+  const uint16_t* outT;   // [G*g] out-instance t of (group, m)
+  const uint16_t* inT;    // [G*g] in-instance t of (group, m)
+  const int8_t* ipos;     // [G*g] position of the out-instance in its group's in-list if intra, else -1
+  const uint8_t* ocls;    // [G*g] path class of the out-instance
+  const uint32_t* H;      // [N*g*g] credits
+  int f;                  // global family index
+};
+
+// One (family, start) pair; executed by one whole wavefront.
+template <int g, int MG>
+__device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8_t* DL, int start, int iter,
+                         int lane, PairRes* out) {
+  constexpr int g2 = g * g;
+  const int G = P.L.G, N = P.L.N;
+  int o[MG][g], nn_[MG][g], ip[MG][g], sig[MG][g], del[MG][g];
+  bool own[MG];
+#pragma unroll
+  for (int r = 0; r < MG; ++r) {
+    const int a = lane + 64 * r;
+    own[r] = a < G;
+#pragma unroll
     for (int m = 0; m < g; ++m) {
-      int r = o[m];
-      if (fm.dst_group(r) != a || SL[r] != DL[r]) continue;
-      int partner = -1;
-      for (int m2 = 0; m2 < g && partner < 0; ++m2)
-        if (tl[m2] != r && tl[m2] != protect) partner = tl[m2];
-      if (partner >= 0) {
-        uint8_t x = DL[r];
-        DL[r] = DL[partner];
-        DL[partner] = x;
-        continue;
-      }
-      for (int m3 = 0; m3 < g && partner < 0; ++m3)
-        if (o[m3] != r && o[m3] != protect) partner = o[m3];
-      if (partner >= 0) {
-        uint8_t x = SL[r];
-        SL[r] = SL[partner];
-        SL[partner] = x;
-      }
+      o[r][m] = own[r] ? fc.outT[a * g + m] : 0;
+      nn_[r][m] = own[r] ? fc.inT[a * g + m] : 0;
+      ip[r][m] = own[r] ? fc.ipos[a * g + m] : -1;
+      sig[r][m] = m;
+      del[r][m] = m;
     }
   }
-  wave_sync();
-}
-
-// One (family, start) pair: build the start, run AA, report F and the
-// largest lane volume per path class.  Executed by one whole wavefront.
-__device__ void run_pair(const PlanArgs& P, const Fam& fm, const uint32_t* H, uint8_t* SL, uint8_t* DL,
-                         const Shared* sh, int start, int iter, int lane, PairRes* out) {
-  const int g = fm.g, G = P.L.G, N = P.L.N, g2 = g * g;
+  int protect = -1;
   if (start == 0) {
-    // canonical binding
-    for (int a = lane; a < G; a += 64) {
-      int tl[kMaxGpusPerSwitch];
-      for (int m = 0; m < g; ++m) SL[fm.out_t(a, m)] = (uint8_t)m;
-      fm.in_list(a, tl);
-      for (int m = 0; m < g; ++m) DL[tl[m]] = (uint8_t)m;
-    }
-    wave_sync();
-    // highest-credit triple, ties to the smallest (t, i, j)
+    // canonical binding plus the highest-credit triple, ties to the smallest (t, i, j)
     uint64_t best = 0;
-    for (int t = lane; t < N; t += 64)
+    for (int t = lane; t < N; t += 64) {
+#pragma unroll
       for (int e = 0; e < g2; ++e) {
-        uint32_t h = H[t * g2 + e];
+        const uint32_t h = fc.H[t * g2 + e];
         if (h != kForbidden && h > 0) {
-          uint64_t key = ((uint64_t)h << 24) | (uint64_t)(0xFFFFFF - (t * g2 + e));
+          const uint64_t key = ((uint64_t)h << 24) | (uint64_t)(0xFFFFFF - (t * g2 + e));
           best = key > best ? key : best;
         }
       }
+    }
     best = wave_max_u(best);
-    int protect = -1;
     if (best) {
-      int idx = 0xFFFFFF - (int)(best & 0xFFFFFF);
-      int ts = idx / g2, e = idx - ts * g2;
-      int il = e / g, jl = e - il * g;
+      const int idx = 0xFFFFFF - (int)(best & 0xFFFFFF);
+      const int ts = idx / g2, e = idx - ts * g2;
+      const int il = e / g, jl = e - il * g;
       protect = ts;
-      if (lane == 0) {
-        int a = fm.src_group(ts);
+#pragma unroll
+      for (int r = 0; r < MG; ++r) {
+        if (!own[r]) continue;
+#pragma unroll
         for (int m = 0; m < g; ++m) {
-          int t2 = fm.out_t(a, m);
-          if (SL[t2] == il) {
-            SL[t2] = SL[ts];
-            SL[ts] = (uint8_t)il;
-            break;
+          if (o[r][m] == ts) {
+#pragma unroll
+            for (int m2 = 0; m2 < g; ++m2)
+              if (sig[r][m2] == il) {
+                sig[r][m2] = sig[r][m];
+                sig[r][m] = il;
+              }
           }
-        }
-        int tl[kMaxGpusPerSwitch];
-        fm.in_list(fm.dst_group(ts), tl);
-        for (int m = 0; m < g; ++m) {
-          int t3 = tl[m];
-          if (DL[t3] == jl) {
-            DL[t3] = DL[ts];
-            DL[ts] = (uint8_t)jl;
-            break;
+          if (nn_[r][m] == ts) {
+#pragma unroll
+            for (int m2 = 0; m2 < g; ++m2)
+              if (del[r][m2] == jl) {
+                del[r][m2] = del[r][m];
+                del[r][m] = jl;
+              }
           }
         }
       }
-      wave_sync();
     }
-    repair(fm, SL, DL, G, protect, lane);
   } else {
     // independent Fisher-Yates shuffles of every group's sources and destinations
-    for (int a = lane; a < G; a += 64) {
+    uint64_t k3 = P.seed;
+    k3 = sm_mix(k3 + kGolden) ^ (uint64_t)iter;
+    k3 = sm_mix(k3 + kGolden) ^ (uint64_t)fc.f;
+    k3 = sm_mix(k3 + kGolden) ^ (uint64_t)start;
+#pragma unroll
+    for (int r = 0; r < MG; ++r) {
+      if (!own[r]) continue;
+      const int a = lane + 64 * r;
+      const uint64_t k4 = sm_mix(k3 + kGolden) ^ (uint64_t)a;
+#pragma unroll
       for (int side = 0; side < 2; ++side) {
-        uint64_t key = P.seed;
-        key = sm_mix(key + kGolden) ^ (uint64_t)iter;
-        key = sm_mix(key + kGolden) ^ (uint64_t)fm.cf->f;
-        key = sm_mix(key + kGolden) ^ (uint64_t)start;
-        key = sm_mix(key + kGolden) ^ (uint64_t)a;
-        key = sm_mix(key + kGolden) ^ (uint64_t)side;
+        const uint64_t key = sm_mix(k4 + kGolden) ^ (uint64_t)side;
         uint64_t state = key;
-        int perm[kMaxGpusPerSwitch];
+        int perm[g];
+#pragma unroll
         for (int m = 0; m < g; ++m) perm[m] = m;
+#pragma unroll
         for (int m = g - 1; m >= 1; --m) {
           state += kGolden;
-          int j = (int)(sm_mix(state) % (uint64_t)(m + 1));
-          int x = perm[m];
+          const int j = (int)(sm_mix(state) % (uint64_t)(m + 1));
+          const int x = perm[m];
           perm[m] = perm[j];
           perm[j] = x;
         }
-        if (side == 0) {
-          for (int m = 0; m < g; ++m) SL[fm.out_t(a, m)] = (uint8_t)perm[m];
-        } else {
-          int tl[kMaxGpusPerSwitch];
-          fm.in_list(a, tl);
-          for (int m = 0; m < g; ++m) DL[tl[m]] = (uint8_t)perm[m];
+#pragma unroll
+        for (int m = 0; m < g; ++m) {
+          if (side == 0) sig[r][m] = perm[m];
+          else del[r][m] = perm[m];
         }
       }
     }
-    wave_sync();
-    repair(fm, SL, DL, G, -1, lane);
   }
+  // Self-binding repair, per group in out-list order: trade destinations with
+  // the first other unprotected in-instance, else sources with the first
+  // other unprotected out-instance.
+#pragma unroll
+  for (int r = 0; r < MG; ++r) {
+    if (!own[r]) continue;
+#pragma unroll
+    for (int m = 0; m < g; ++m) {
+      const int mi = ip[r][m];
+      if (mi < 0 || sig[r][m] != del[r][mi]) continue;
+      int partner = -1;
+#pragma unroll
+      for (int m2 = 0; m2 < g; ++m2)
+        if (partner < 0 && nn_[r][m2] != o[r][m] && nn_[r][m2] != protect) partner = m2;
+      if (partner >= 0) {
+        const int x = del[r][mi];
+        del[r][mi] = del[r][partner];
+        del[r][partner] = x;
+        continue;
+      }
+#pragma unroll
+      for (int m3 = 0; m3 < g; ++m3)
+        if (partner < 0 && o[r][m3] != o[r][m] && o[r][m3] != protect) partner = m3;
+      if (partner >= 0) {
+        const int x = sig[r][m];
+        sig[r][m] = sig[r][partner];
+        sig[r][partner] = x;
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < MG; ++r) {
+    if (!own[r]) continue;
+#pragma unroll
+    for (int m = 0; m < g; ++m) {
+      SL[o[r][m]] = (uint8_t)sig[r][m];
+      DL[nn_[r][m]] = (uint8_t)del[r][m];
+    }
+  }
+  wave_sync();
 
   // Alternating Algorithm: source half, then destination half.
-  const int np = P.L.n_perm;
-  const uint8_t* perms = sh->perms;
   for (int sweep = 0; sweep < P.i_aa; ++sweep) {
     int changed = 0;
-    for (int a = lane; a < G; a += 64) {
-      int o[kMaxGpusPerSwitch], jl[kMaxGpusPerSwitch];
-      int64_t cur = 0;
+#pragma unroll
+    for (int r = 0; r < MG; ++r) {
+      if (!own[r]) continue;
+      int jl[g];
+      uint32_t row[g][g2], h[g][g];
+#pragma unroll
       for (int m = 0; m < g; ++m) {
-        o[m] = fm.out_t(a, m);
-        jl[m] = DL[o[m]];
-        cur += H[o[m] * g2 + SL[o[m]] * g + jl[m]];
+        jl[m] = DL[o[r][m]];
+#pragma unroll
+        for (int e = 0; e < g2; ++e) row[m][e] = fc.H[o[r][m] * g2 + e];
       }
+#pragma unroll
+      for (int m = 0; m < g; ++m)
+#pragma unroll
+        for (int il = 0; il < g; ++il) {
+          uint32_t v = row[m][il * g];
+#pragma unroll
+          for (int jj = 1; jj < g; ++jj) v = jl[m] == jj ? row[m][il * g + jj] : v;
+          h[m][il] = v;
+        }
+      int64_t cur = 0;
+#pragma unroll
+      for (int m = 0; m < g; ++m) cur += h[m][sig[r][m]];
       int64_t bestv = -1;
-      int bp = -1;
-      for (int p = 0; p < np; ++p) {
+      int bp = 0;
+#pragma unroll
+      for (int p = 0; p < Perms<g>::n; ++p) {
         int64_t v = 0;
         bool ok = true;
+#pragma unroll
         for (int m = 0; m < g; ++m) {
-          uint32_t h = H[o[m] * g2 + perms[p * g + m] * g + jl[m]];
-          if (h == kForbidden) { ok = false; break; }
-          v += h;
+          const uint32_t x = h[m][Perms<g>::at(p, m)];
+          ok = ok && x != kForbidden;
+          v += x;
         }
-        if (ok && v > bestv) { bestv = v; bp = p; }
+        if (ok && v > bestv) {
+          bestv = v;
+          bp = p;
+        }
       }
       if (bestv > cur) {
-        for (int m = 0; m < g; ++m) SL[o[m]] = perms[bp * g + m];
+#pragma unroll
+        for (int m = 0; m < g; ++m) {
+          sig[r][m] = Perms<g>::at(bp, m);
+          SL[o[r][m]] = (uint8_t)sig[r][m];
+        }
         changed = 1;
       }
     }
     wave_sync();
-    for (int d = lane; d < G; d += 64) {
-      int tl[kMaxGpusPerSwitch], il[kMaxGpusPerSwitch];
-      fm.in_list(d, tl);
-      int64_t cur = 0;
+#pragma unroll
+    for (int r = 0; r < MG; ++r) {
+      if (!own[r]) continue;
+      int il[g];
+      uint32_t row[g][g2], h[g][g];
+#pragma unroll
       for (int m = 0; m < g; ++m) {
-        il[m] = SL[tl[m]];
-        cur += H[tl[m] * g2 + il[m] * g + DL[tl[m]]];
+        il[m] = SL[nn_[r][m]];
+#pragma unroll
+        for (int e = 0; e < g2; ++e) row[m][e] = fc.H[nn_[r][m] * g2 + e];
       }
+#pragma unroll
+      for (int m = 0; m < g; ++m)
+#pragma unroll
+        for (int jl = 0; jl < g; ++jl) {
+          uint32_t v = row[m][jl];
+#pragma unroll
+          for (int ii = 1; ii < g; ++ii) v = il[m] == ii ? row[m][ii * g + jl] : v;
+          h[m][jl] = v;
+        }
+      int64_t cur = 0;
+#pragma unroll
+      for (int m = 0; m < g; ++m) cur += h[m][del[r][m]];
       int64_t bestv = -1;
-      int bp = -1;
-      for (int p = 0; p < np; ++p) {
+      int bp = 0;
+#pragma unroll
+      for (int p = 0; p < Perms<g>::n; ++p) {
         int64_t v = 0;
         bool ok = true;
+#pragma unroll
         for (int m = 0; m < g; ++m) {
-          uint32_t h = H[tl[m] * g2 + il[m] * g + perms[p * g + m]];
-          if (h == kForbidden) { ok = false; break; }
-          v += h;
+          const uint32_t x = h[m][Perms<g>::at(p, m)];
+          ok = ok && x != kForbidden;
+          v += x;
         }
-        if (ok && v > bestv) { bestv = v; bp = p; }
+        if (ok && v > bestv) {
+          bestv = v;
+          bp = p;
+        }
       }
       if (bestv > cur) {
-        for (int m = 0; m < g; ++m) DL[tl[m]] = perms[bp * g + m];
+#pragma unroll
+        for (int m = 0; m < g; ++m) {
+          del[r][m] = Perms<g>::at(bp, m);
+          DL[nn_[r][m]] = (uint8_t)del[r][m];
+        }
         changed = 1;
       }
     }
@@ -337,13 +400,19 @@ __device__ void run_pair(const PlanArgs& P, const Fam& fm, const uint32_t* H, ui
 
   // binding score F (Eq. (8)) and the largest lane volume per path class
   int64_t F = 0, x0 = 0, x1 = 0, x2 = 0;
-  for (int t = lane; t < N; t += 64) {
-    int64_t h = H[t * g2 + SL[t] * g + DL[t]];
-    F += h;
-    int c = fm.cls(t);
-    if (c == 0) x0 = max(x0, h);
-    else if (c == 1) x1 = max(x1, h);
-    else x2 = max(x2, h);
+#pragma unroll
+  for (int r = 0; r < MG; ++r) {
+    if (!own[r]) continue;
+    const int a = lane + 64 * r;
+#pragma unroll
+    for (int m = 0; m < g; ++m) {
+      const int64_t x = fc.H[o[r][m] * g2 + sig[r][m] * g + DL[o[r][m]]];
+      F += x;
+      const int c = fc.ocls[a * g + m];
+      if (c == 0) x0 = x > x0 ? x : x0;
+      else if (c == 1) x1 = x > x1 ? x : x1;
+      else x2 = x > x2 ? x : x2;
+    }
   }
   F = wave_sum(F);
   x0 = wave_max(x0);
@@ -359,25 +428,36 @@ __device__ void run_pair(const PlanArgs& P, const Fam& fm, const uint32_t* H, ui
 
 __device__ inline void set_err(Shared* sh, int code) { atomicCAS(&sh->err, 0, code); }
 
+template <int g, int MG>
 __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  constexpr int g2 = g * g;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const DevCatalogLayout& L = P.L;
-  const int N = L.N, g = L.g, Q = L.Q, nn = L.nn, QG = Q * g, g2 = g * g;
-  const int NP = L.J0 + L.J1, NS = P.n_start;
-  int32_t* rinfo = (int32_t*)(smem + P.o_rinfo);
-  int64_t* agg = (int64_t*)(smem + P.o_agg);
-  uint16_t* terms = (uint16_t*)(smem + P.o_terms);
-  uint8_t* nterms = smem + P.o_nterms;
-  int64_t* base = (int64_t*)(smem + P.o_base);
-  ChunkFam* cf = (ChunkFam*)(smem + P.o_cf);
-  PairRes* pr = (PairRes*)(smem + P.o_pair);
-  uint8_t* bsl = smem + P.o_best;
-  uint8_t* bdl = bsl + N;
+  const int N = L.N, Q = L.Q, nn = L.nn, QG = Q * g;
+  const int NP = L.J0 + L.J1, NS = P.n_start, FL = L.F0 + L.F1;
   Shared* sh = (Shared*)(smem + P.o_sh);
+  int32_t* rinfo = (int32_t*)(smem + P.o_rinfo);
+  int32_t* agg = (int32_t*)(smem + P.o_agg);         // [q][q2][k] units: k = 0 is A, k > 0 is B_k
+  // row stride: odd (lanes reading one shift of different rows hit distinct
+  // banks) and at least nn + 3 (zero padding for the 4-wide shift unroll)
+  const int kS = (nn + 3) | 1;
+  uint16_t* terms = (uint16_t*)(smem + P.o_terms);
+  uint16_t* nterms = (uint16_t*)(smem + P.o_nterms);  // low byte: diagonal terms, high byte: shift terms
+  int32_t* pfb = (int32_t*)(smem + P.o_pfb);           // [NP][2] local family range
+  uint32_t* finfo = (uint32_t*)(smem + P.o_finfo);
+  uint8_t* finl = smem + P.o_finl;
+  PairRes* pr = (PairRes*)(smem + P.o_pair);
+  uint16_t* outT = (uint16_t*)(smem + P.o_outT);
+  uint16_t* inT = (uint16_t*)(smem + P.o_inT);
+  int8_t* ipos = (int8_t*)(smem + P.o_ipos);
+  uint8_t* ocls = smem + P.o_ocls;
   uint32_t* hp = (uint32_t*)(smem + P.o_hp);
   uint8_t* sl = smem + P.o_sl;
   uint8_t* dl = smem + P.o_dl;
+  uint8_t* bsl = smem + P.o_bsl;
+  uint8_t* bdl = smem + P.o_bdl;
+  uint32_t* bx = (uint32_t*)(smem + P.o_bx);
   const int32_t* cat = P.cat;
 
   // ---------------------------------------------------------------- prologue
@@ -385,16 +465,36 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     sh->err = 0;
     sh->K = 0;
     sh->total_rem = 0;
+    sh->total_units = 0;
     sh->Lmax = 0;
+    sh->key = 0;
   }
-  for (int x = tid; x < L.n_perm * g; x += kPlanThreads) sh->perms[x] = (uint8_t)cat[L.off_perms + x];
   for (int r = tid; r < N; r += kPlanThreads) {
-    int grp = r / g;
+    const int grp = r / g;
     rinfo[r] = ((grp / Q) << 8) | ((grp % Q) << 4) | (r - grp * g);
   }
   for (int x = tid; x < NP * L.TS; x += kPlanThreads) terms[x] = (uint16_t)cat[L.off_terms + x];
-  for (int p = tid; p < NP; p += kPlanThreads) nterms[p] = (uint8_t)cat[L.off_nterms + p];
-  for (int x = tid; x < nn * Q * Q; x += kPlanThreads) agg[x] = 0;
+  for (int p = tid; p < NP; p += kPlanThreads) {
+    // terms are stored diagonal-block first, then shift-block
+    const int n = cat[L.off_nterms + p];
+    int nl = 0;
+    for (int m = 0; m < n; ++m) nl += (cat[L.off_terms + p * L.TS + m] >> 12) == 0;
+    nterms[p] = (uint16_t)(nl | ((n - nl) << 8));
+    pfb[2 * p] = cat[L.off_fb + p];
+    pfb[2 * p + 1] = cat[L.off_fe + p];
+  }
+  for (int x = tid; x < FL * QG; x += kPlanThreads) {
+    // descriptor word and in-list entry of local family x / QG, index x % QG
+    const int lf = x / QG, idx = x - lf * QG;
+    const int info = cat[L.off_fam_info + x];
+    const int cls = info & 15, ss = (info >> 4) & 15, ds = (info >> 8) & 15, id = info >> 12;
+    int opos = 0;
+    for (int m = 0; m < g; ++m)
+      if (cat[L.off_fam_out + lf * QG + ss * g + m] == idx) opos = m;
+    finfo[x] = (uint32_t)(cls | (ss << 2) | (ds << 5) | (opos << 8) | (id << 10));
+    finl[x] = (uint8_t)cat[L.off_fam_in + x];
+  }
+  for (int x = tid; x < kS * Q * Q; x += kPlanThreads) agg[x] = 0;
   int64_t* colsum = (int64_t*)hp;   // the credit area is free during the prologue
   for (int x = tid; x < N; x += kPlanThreads) colsum[x] = 0;
   __syncthreads();
@@ -408,9 +508,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       const int ri = rinfo[i], ni = ri >> 8, qi = (ri >> 4) & 15;
       int64_t rs = 0;
       for (int j = lane; j < N; j += 64) {
-        int64_t v = P.D[(size_t)i * N + j];
-        bool divisible = ((uint64_t)v & mask) == 0 &&
-                         ((uint64_t)v >> P.unit_shift) * P.odd_inv <= P.odd_lim;
+        const int64_t v = P.D[(size_t)i * N + j];
+        const bool divisible = ((uint64_t)v & mask) == 0 &&
+                               ((uint64_t)v >> P.unit_shift) * P.odd_inv <= P.odd_lim;
         if (v < 0 || (i == j && v != 0) || !divisible) bad = true;
         P.Drem[(size_t)i * N + j] = v;
         rs += v;
@@ -419,29 +519,33 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           int kk = nj - ni;
           if (kk < 0) kk += nn;
           atomicAdd((unsigned long long*)&colsum[j], (unsigned long long)v);
-          atomicAdd((unsigned long long*)&agg[(kk * Q + qi) * Q + qj], (unsigned long long)v);
+          // exact quotient by the unit: v >> s times the odd part's inverse
+          const int32_t vu = (int32_t)(((uint64_t)v >> P.unit_shift) * P.odd_inv);
+          atomicAdd(&agg[(qi * Q + qj) * kS + kk], vu);
         }
       }
       rs = wave_sum(rs);
       tot += rs;
-      lmax = max(lmax, rs);
+      lmax = rs > lmax ? rs : lmax;
     }
     if (bad) set_err(sh, VP_ERR_INVALID_DEMAND);
     if (lane == 0) {
       atomicAdd((unsigned long long*)&sh->total_rem, (unsigned long long)tot);
+      atomicAdd((unsigned long long*)&sh->total_units,
+                (unsigned long long)(((uint64_t)tot >> P.unit_shift) * P.odd_inv));
       atomicMax((unsigned long long*)&sh->Lmax, (unsigned long long)lmax);
     }
   }
   __syncthreads();
   {
     int64_t lmax = 0;
-    for (int j = tid; j < N; j += kPlanThreads) lmax = max(lmax, colsum[j]);
+    for (int j = tid; j < N; j += kPlanThreads) lmax = colsum[j] > lmax ? colsum[j] : lmax;
     lmax = wave_max(lmax);
     if (lane == 0) atomicMax((unsigned long long*)&sh->Lmax, (unsigned long long)lmax);
   }
   __syncthreads();
   if (tid == 0 && sh->err == 0) {
-    int64_t den = L.bw_max * P.k_target;
+    const int64_t den = L.bw_max * P.k_target;
     int64_t tau = (sh->Lmax + den - 1) / den;
     if (tau < 1) tau = 1;
     sh->tau = tau;
@@ -451,7 +555,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       sh->cap[c] = cap;
       if (cap >= (int64_t(1) << 31)) set_err(sh, VP_ERR_UNSUPPORTED);
     }
-    if (sh->total_rem >= (int64_t(1) << 42)) set_err(sh, VP_ERR_UNSUPPORTED);
+    if (sh->total_rem >= (int64_t(1) << 42) || sh->total_units >= (int64_t(1) << 28))
+      set_err(sh, VP_ERR_UNSUPPORTED);
   }
   __syncthreads();
 
@@ -465,57 +570,80 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     }
     const int K = sh->K;
 
-    // Step 1: pattern bases from A, then every shape's score; argmax.
-    for (int p = tid; p < NP; p += kPlanThreads) {
-      int64_t s = 0;
-      const int n = nterms[p];
-      for (int m = 0; m < n; ++m) {
-        int t = terms[p * L.TS + m];
-        if (!(t >> 12)) s += (int64_t)(t & 15) * agg[((t >> 8) & 15) * Q + ((t >> 4) & 15)];
-      }
-      base[p] = s;
-    }
-    if (tid == 0) sh->key = 0;
-    __syncthreads();
+    // Step 1: score every node-local pattern over every shift; argmax.
+    // Items: the J0 intra-node patterns, then (NIC-carrying pattern, shift
+    // chunk) pairs; KC chunks of KW shifts each.
     {
       uint64_t best = 0;
-      for (int j = tid; j < L.J0; j += kPlanThreads) {
-        uint64_t key = ((uint64_t)base[j] << 20) | (uint64_t)(0xFFFFF - j);
-        best = key > best ? key : best;
-      }
-      if (L.J1 > 0) {
-        const int Jr = L.J1 * (nn - 1);
-        int k = 1 + tid / L.J1, pp = tid % L.J1;
-        const int step_k = kPlanThreads / L.J1, step_p = kPlanThreads % L.J1;
-        for (int r = tid; r < Jr; r += kPlanThreads) {
-          const int p = L.J0 + pp;
-          int64_t s = base[p];
-          const int n = nterms[p];
-          const int64_t* Bk = agg + k * Q * Q;
-          for (int m = 0; m < n; ++m) {
-            int t = terms[p * L.TS + m];
-            if (t >> 12) s += (int64_t)(t & 15) * Bk[((t >> 8) & 15) * Q + ((t >> 4) & 15)];
-          }
-          uint64_t key = ((uint64_t)s << 20) | (uint64_t)(0xFFFFF - (L.J0 + r));
-          best = key > best ? key : best;
-          k += step_k;
-          pp += step_p;
-          if (pp >= L.J1) {
-            pp -= L.J1;
-            ++k;
-          }
+      const int KW = (nn - 1 + P.KC - 1) / P.KC;
+      const int items = L.J0 + L.J1 * P.KC;
+      for (int x = tid; x < items; x += kPlanThreads) {
+        int p, k0 = 0, k1 = 0;
+        if (x < L.J0) {
+          p = x;
+        } else {
+          const int y = x - L.J0;
+          p = L.J0 + y / P.KC;
+          k0 = 1 + (y - (y / P.KC) * P.KC) * KW;
+          k1 = min(nn, k0 + KW);
         }
+        const uint16_t* tp = terms + p * L.TS;
+        const int nl = nterms[p] & 255, nr = nterms[p] >> 8;
+        // fully unrolled, predicated term loops: static register indices and
+        // all LDS reads of a loop in flight together
+        int32_t s = 0;
+#pragma unroll
+        for (int m = 0; m < kMaxLTerms; ++m)
+          if (m < nl) {
+            const int t = tp[m];
+            s += (t & 15) * agg[(((t >> 8) & 15) * Q + ((t >> 4) & 15)) * kS];
+          }
+        int j = p;
+        if (p >= L.J0) {
+          if (k0 >= k1) continue;
+          // best shift of this chunk for the NIC part (counts are one lane
+          // per slot pair), ties to the lowest shift
+          int off[kMaxSlotsPerNode];
+#pragma unroll
+          for (int m = 0; m < kMaxSlotsPerNode; ++m) {
+            const int t = m < nr ? tp[nl + m] : 0;
+            off[m] = (((t >> 8) & 15) * Q + ((t >> 4) & 15)) * kS;
+          }
+          int32_t bv = -1;
+          int bk = k0;
+          for (int kb = k0; kb < k1; kb += 4) {
+            int32_t r0 = 0, r1 = 0, r2 = 0, r3 = 0;
+#pragma unroll
+            for (int m = 0; m < kMaxSlotsPerNode; ++m)
+              if (m < nr) {
+                const int32_t* row = agg + off[m] + kb;
+                r0 += row[0];
+                r1 += row[1];
+                r2 += row[2];
+                r3 += row[3];
+              }
+            if (r0 > bv) { bv = r0; bk = kb; }
+            if (kb + 1 < k1 && r1 > bv) { bv = r1; bk = kb + 1; }
+            if (kb + 2 < k1 && r2 > bv) { bv = r2; bk = kb + 2; }
+            if (kb + 3 < k1 && r3 > bv) { bv = r3; bk = kb + 3; }
+          }
+          s += bv;
+          j = L.J0 + (bk - 1) * L.J1 + (p - L.J0);
+        }
+        const uint64_t key = ((uint64_t)(uint32_t)s << 20) | (uint64_t)(0xFFFFF - j);
+        best = key > best ? key : best;
       }
       best = wave_max_u(best);
       if (lane == 0) atomicMax((unsigned long long*)&sh->key, (unsigned long long)best);
     }
     __syncthreads();
-    if ((sh->key >> 20) == 0) {
+    const uint64_t key = sh->key;
+    if ((key >> 20) == 0) {
       __syncthreads();
       if (tid == 0) set_err(sh, VP_ERR_NO_PROGRESS);
       break;
     }
-    const int jstar = 0xFFFFF - (int)(sh->key & 0xFFFFF);
+    const int jstar = 0xFFFFF - (int)(key & 0xFFFFF);
     int kstar, pstar;
     if (jstar < L.J0) {
       kstar = 0;
@@ -524,46 +652,54 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       kstar = 1 + (jstar - L.J0) / L.J1;
       pstar = L.J0 + (jstar - L.J0) % L.J1;
     }
-    const int lb = cat[L.off_fb + pstar], le = cat[L.off_fe + pstar];
-    const int fbase = kstar == 0 ? 0 : L.F0 + (kstar - 1) * L.F1 - L.F0;
+    const int lb = pfb[2 * pstar], le = pfb[2 * pstar + 1];
+    const int fbase = kstar == 0 ? 0 : (kstar - 1) * L.F1;
     const int fb = lb + fbase, fe = le + fbase;
     if (tid == 0) sh->best_valid = 0;
 
     // Steps 2-3 over the shape's bucket, FC families at a time.
+    int last_cb = fb;
     for (int cb = fb; cb < fe; cb += P.FC) {
+      last_cb = cb;
       const int nc = min(P.FC, fe - cb);
-      for (int x = tid; x < nc * QG; x += kPlanThreads) {
-        const int c = x / QG, idx = x - c * QG, f = cb + c;
-        const int lf = kstar == 0 ? f : L.F0 + (f - L.F0) % L.F1;
-        cf[c].info[idx] = cat[L.off_fam_info + lf * QG + idx];
-        cf[c].outl[idx] = (uint8_t)cat[L.off_fam_out + lf * QG + idx];
-        cf[c].inl[idx] = (uint8_t)cat[L.off_fam_in + lf * QG + idx];
-        if (idx == 0) {
-          cf[c].f = f;
-          cf[c].k = kstar;
-        }
-      }
-      __syncthreads();
-      // credits h' of every (family, instance, source slot, destination slot)
+      // group lists and credits of every (family, instance)
       {
         const int tot = nc * N;
         int c = tid / N, t = tid - (tid / N) * N;
         const int dc = kPlanThreads / N, dt = kPlanThreads % N;
         for (int x = tid; x < tot; x += kPlanThreads) {
+          const int f = cb + c;
+          const int lf = kstar == 0 ? f : L.F0 + (f - L.F0) % L.F1;
           const int n = rinfo[t] >> 8, idx = t - n * QG;
-          const int info = cf[c].info[idx], cl = info & 15;
-          const int sg = n * Q + ((info >> 4) & 15);
+          const uint32_t w = finfo[lf * QG + idx];
+          const int cl = d_cls(w), a = n * Q + d_ss(w);
           const int dn = (cl == VP_PATH_NIC && kstar) ? (n + kstar) % nn : n;
-          const int dg = dn * Q + ((info >> 8) & 15);
+          const int d = dn * Q + d_ds(w);
+          // rank of t inside the in-list of group d (family order = ascending t)
+          int mi = 0;
+          for (int m = 0; m < g; ++m) {
+            const int idx2 = finl[lf * QG + d_ds(w) * g + m];
+            const int c2 = d_cls(finfo[lf * QG + idx2]);
+            const int sn = (c2 == VP_PATH_NIC && kstar) ? (dn - kstar + nn) % nn : dn;
+            mi += (sn * QG + idx2) < t;
+          }
+          const int op = d_opos(w);
+          const size_t base = (size_t)c * N;
+          outT[base + a * g + op] = (uint16_t)t;
+          inT[base + d * g + mi] = (uint16_t)t;
+          ocls[base + a * g + op] = (uint8_t)cl;
+          ipos[base + a * g + op] = (int8_t)(d == a ? mi : -1);
           const int64_t cap = sh->cap[cl];
-          uint32_t* h = hp + ((size_t)c * N + t) * g2;
+          uint32_t* h = hp + (base + t) * g2;
+#pragma unroll
           for (int il = 0; il < g; ++il)
+#pragma unroll
             for (int jl = 0; jl < g; ++jl) {
-              const int i = sg * g + il, j = dg * g + jl;
+              const int i = a * g + il, j = d * g + jl;
               uint32_t v = kForbidden;
               if (i != j) {
-                int64_t d = P.Drem[(size_t)i * N + j];
-                v = (uint32_t)(d < cap ? d : cap);
+                const int64_t dv = P.Drem[(size_t)i * N + j];
+                v = (uint32_t)(dv < cap ? dv : cap);
               }
               h[il * g + jl] = v;
             }
@@ -578,84 +714,117 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       __syncthreads();
       for (int pi = wave; pi < nc * NS; pi += kWaves) {
         const int c = pi / NS, s = pi - c * NS;
-        Fam fm{&cf[c], rinfo, Q, g, QG, nn, kstar};
-        run_pair(P, fm, hp + (size_t)c * N * g2, sl + (size_t)pi * N, dl + (size_t)pi * N, sh, s, K,
-                 lane, &pr[pi]);
+        FamCtx fc{outT + (size_t)c * N, inT + (size_t)c * N, ipos + (size_t)c * N, ocls + (size_t)c * N,
+                  hp + (size_t)c * N * g2, cb + c};
+        run_pair<g, MG>(P, fc, sl + (size_t)pi * N, dl + (size_t)pi * N, s, K, lane, &pr[pi]);
       }
       __syncthreads();
-      // Evaluate (Eq. (9)-(10)) and keep the best family so far.
-      if (tid == 0) {
-        sh->copy_pair = -1;
-        for (int c = 0; c < nc; ++c) {
-          int bs = 0;
+      // Evaluate (Eq. (9)-(10)): best start per family, best family overall.
+      if (wave == 0) {
+        int64_t S = 0, xm = 0, bm = 1;
+        int c = -1, bs = 0;
+        for (int cc = lane; cc < nc; cc += 64) {
+          int s0 = 0;
           for (int s = 1; s < NS; ++s)
-            if (pr[c * NS + s].F > pr[c * NS + bs].F) bs = s;
-          const PairRes& r = pr[c * NS + bs];
-          int64_t xm = 0, bm = 1;
+            if (pr[cc * NS + s].F > pr[cc * NS + s0].F) s0 = s;
+          const PairRes& r = pr[cc * NS + s0];
+          int64_t xm2 = 0, bm2 = 1;
           for (int cl = 0; cl < 3; ++cl)
-            if (r.xmax[cl] * bm > xm * L.bw_cls[cl]) {
-              xm = r.xmax[cl];
-              bm = L.bw_cls[cl];
+            if (r.xmax[cl] * bm2 > xm2 * L.bw_cls[cl]) {
+              xm2 = r.xmax[cl];
+              bm2 = L.bw_cls[cl];
             }
-          if (!sh->best_valid ||
-              utility_greater(r.F, xm, bm, sh->best_S, sh->best_xm, sh->best_bm, P.lambda)) {
-            sh->best_valid = 1;
-            sh->best_S = r.F;
-            sh->best_xm = xm;
-            sh->best_bm = bm;
-            sh->best_f = cb + c;
-            sh->best_k = kstar;
-            sh->copy_pair = c * NS + bs;
+          if (c < 0 || utility_greater(r.F, xm2, bm2, S, xm, bm, P.lambda)) {
+            S = r.F;
+            xm = xm2;
+            bm = bm2;
+            c = cc;
+            bs = s0;
           }
         }
+        // wave argmax under the exact order, ties to the lower family index
+        for (int off = nc > 1 ? 32 : 0; off > 0; off >>= 1) {
+          const int64_t S2 = __shfl_xor(S, off), xm2 = __shfl_xor(xm, off), bm2 = __shfl_xor(bm, off);
+          const int c2 = __shfl_xor(c, off), bs2 = __shfl_xor(bs, off);
+          bool take = false;
+          if (c2 >= 0) {
+            if (c < 0) take = true;
+            else if (utility_greater(S2, xm2, bm2, S, xm, bm, P.lambda)) take = true;
+            else if (!utility_greater(S, xm, bm, S2, xm2, bm2, P.lambda) && c2 < c) take = true;
+          }
+          if (take) {
+            S = S2;
+            xm = xm2;
+            bm = bm2;
+            c = c2;
+            bs = bs2;
+          }
+        }
+        if (lane == 0 && (!sh->best_valid ||
+                          utility_greater(S, xm, bm, sh->best_S, sh->best_xm, sh->best_bm, P.lambda))) {
+          sh->best_valid = 1;
+          sh->best_S = S;
+          sh->best_xm = xm;
+          sh->best_bm = bm;
+          sh->best_f = cb + c;
+          sh->best_k = kstar;
+          sh->best_c = c;
+          sh->best_s = bs;
+          sh->best_chunk = cb;
+        }
       }
       __syncthreads();
-      if (sh->copy_pair >= 0)
+      if (cb + P.FC < fe && sh->best_chunk == cb) {
+        // a later chunk reuses this LDS: keep the winner's binding and volumes
+        const int pi = sh->best_c * NS + sh->best_s;
+        const uint32_t* H = hp + (size_t)sh->best_c * N * g2;
         for (int t = tid; t < N; t += kPlanThreads) {
-          bsl[t] = sl[(size_t)sh->copy_pair * N + t];
-          bdl[t] = dl[(size_t)sh->copy_pair * N + t];
+          const uint8_t s_ = sl[(size_t)pi * N + t], d_ = dl[(size_t)pi * N + t];
+          bsl[t] = s_;
+          bdl[t] = d_;
+          bx[t] = H[t * g2 + s_ * g + d_];
         }
-      __syncthreads();
+        __syncthreads();
+      }
     }
 
     // Step 4: append E* and subtract X(E*) from D^rem and the aggregates.
     {
-      if (tid == 0) sh->S = 0;
-      __syncthreads();
       const int f = sh->best_f, k = sh->best_k;
       const int lf = k == 0 ? f : L.F0 + (f - L.F0) % L.F1;
-      int64_t served = 0;
+      const bool live = sh->best_chunk == last_cb;
+      const int pi = sh->best_c * NS + sh->best_s;
+      const uint8_t* SLp = live ? sl + (size_t)pi * N : bsl;
+      const uint8_t* DLp = live ? dl + (size_t)pi * N : bdl;
+      const uint32_t* H = hp + (size_t)sh->best_c * N * g2;
       for (int t = tid; t < N; t += kPlanThreads) {
         const int n = rinfo[t] >> 8, idx = t - n * QG;
-        const int info = cat[L.off_fam_info + lf * QG + idx], cl = info & 15;
-        const int ss = (info >> 4) & 15, ds = (info >> 8) & 15;
+        const uint32_t w = finfo[lf * QG + idx];
+        const int cl = d_cls(w), ss = d_ss(w), ds = d_ds(w);
         const int dn = (cl == VP_PATH_NIC && k) ? (n + k) % nn : n;
-        const int i = (n * Q + ss) * g + bsl[t], j = (dn * Q + ds) * g + bdl[t];
-        const int64_t d = P.Drem[(size_t)i * N + j];
-        const int64_t x = d < sh->cap[cl] ? d : sh->cap[cl];
-        P.Drem[(size_t)i * N + j] = d - x;
+        const int s_ = SLp[t], d_ = DLp[t];
+        const int i = (n * Q + ss) * g + s_, j = (dn * Q + ds) * g + d_;
+        const int64_t x = live ? (int64_t)H[t * g2 + s_ * g + d_] : (int64_t)bx[t];
         const size_t o = (size_t)K * N + i;
         P.dst[o] = j;
-        P.inst[o] = info >> 12;
+        P.inst[o] = d_id(w);
         P.bytes[o] = x;
         if (x > 0) {
+          P.Drem[(size_t)i * N + j] -= x;
           int kk = dn - n;
           if (kk < 0) kk += nn;
-          atomicAdd((unsigned long long*)&agg[(kk * Q + ss) * Q + ds], (unsigned long long)(-x));
+          atomicAdd(&agg[(ss * Q + ds) * kS + kk], -(int32_t)(((uint64_t)x >> P.unit_shift) * P.odd_inv));
         }
-        served += x;
       }
-      served = wave_sum(served);
-      if (lane == 0 && served) atomicAdd((unsigned long long*)&sh->S, (unsigned long long)served);
-      __syncthreads();
       if (tid == 0) {
         P.family[K] = f;
-        if (sh->S == 0) {
+        if (sh->best_S == 0) {
           set_err(sh, VP_ERR_NO_PROGRESS);
         } else {
-          sh->total_rem -= sh->S;
+          sh->total_rem -= sh->best_S;
           sh->K = K + 1;
         }
+        sh->key = 0;
       }
       __syncthreads();
     }
@@ -670,17 +839,46 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+template <int g, int MG>
+vp_status launch_t(const PlanArgs& P, size_t lds, hipStream_t st) {
+  auto kern = plan_kernel<g, MG>;
+  if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+      hipSuccess)
+    return set_error(VP_ERR_HIP, "cannot raise the planner's LDS limit");
+  hipLaunchKernelGGL(kern, dim3(1), dim3(kPlanThreads), lds, st, P);
+  if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "planner launch failed");
+  return VP_OK;
+}
+
+template <int g>
+vp_status launch_g(const PlanArgs& P, size_t lds, hipStream_t st, int gpl) {
+  if (gpl <= 1) return launch_t<g, 1>(P, lds, st);
+  if (gpl <= 2) return launch_t<g, 2>(P, lds, st);
+  if (gpl <= 4) return launch_t<g, 4>(P, lds, st);
+  return launch_t<g, 8>(P, lds, st);
+}
+
 }  // namespace
 
 vp_status launch_plan(const PlanLaunch& a, void* stream) {
   const vp_catalog& c = *a.cat;
   const DevCatalogLayout& L = c.lay;
-  const int N = L.N, g = L.g, g2 = g * g, NS = a.p.n_start, NP = L.J0 + L.J1;
+  const int N = L.N, g = L.g, g2 = g * g, NS = a.p.n_start, NP = L.J0 + L.J1, FL = L.F0 + L.F1;
+  const int QG = L.Q * g;
   if (L.J >= (1 << 20)) return set_error(VP_ERR_UNSUPPORTED, "more than 2^20 shapes");
-  if (L.Q * g > kMaxQG) return set_error(VP_ERR_UNSUPPORTED, "too many lanes per node");
-  // largest bucket
+  if (QG > kMaxQG || L.Q > 8 || g > 4) return set_error(VP_ERR_UNSUPPORTED, "too many lanes per node");
+  if (N > 65535 || L.G > 64 * 8) return set_error(VP_ERR_UNSUPPORTED, "too many ranks for the planner");
+  for (int i = 0; i < L.n_inst; ++i)
+    if (i >= (1 << 22)) return set_error(VP_ERR_UNSUPPORTED, "too many node-local instances");
   int hmax = 1;
-  for (int p = 0; p < NP; ++p) hmax = std::max(hmax, c.pat_fe[p] - c.pat_fb[p]);
+  for (int p = 0; p < NP; ++p) {
+    hmax = std::max(hmax, c.pat_fe[p] - c.pat_fb[p]);
+    int nl = 0;
+    for (int v : c.patL[p]) nl += v != 0;
+    if (nl > kMaxLTerms) return set_error(VP_ERR_UNSUPPORTED, "too many intra-node lane classes");
+    for (int v : c.patR[p])   // one NIC per switch: at most one cross-node lane per slot pair
+      if (v > 1) return set_error(VP_ERR_UNSUPPORTED, "more than one NIC lane per slot pair");
+  }
 
   PlanArgs P{};
   P.cat = (const int32_t*)c.dev;
@@ -694,7 +892,10 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   // divisibility by unit = 2^s * odd: low s bits clear and (v >> s) * odd^-1 <= (2^64-1)/odd
   uint64_t u = (uint64_t)a.p.unit_bytes;
   int s = 0;
-  while (!(u & 1)) { u >>= 1; ++s; }
+  while (!(u & 1)) {
+    u >>= 1;
+    ++s;
+  }
   uint64_t inv = u;
   for (int it = 0; it < 6; ++it) inv *= 2 - u * inv;
   P.unit_shift = s;
@@ -703,6 +904,8 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   P.n_start = NS;
   P.i_aa = a.p.i_aa;
   P.k_max = a.p.k_max;
+  // shift chunks per NIC-carrying pattern: enough items to occupy every thread
+  P.KC = L.J1 > 0 ? std::max(1, std::min(L.nn - 1, kPlanThreads / L.J1)) : 1;
   P.K = a.K;
   P.family = a.family;
   P.dst = a.dst;
@@ -712,41 +915,52 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   P.status = a.status;
 
   size_t o = 0;
-  P.o_sh = (int32_t)o; o = align_up(o + sizeof(Shared), 16);
-  P.o_rinfo = (int32_t)o; o = align_up(o + (size_t)N * 4, 16);
-  P.o_agg = (int32_t)o; o = align_up(o + (size_t)L.nn * L.Q * L.Q * 8, 16);
-  P.o_terms = (int32_t)o; o = align_up(o + (size_t)NP * L.TS * 2, 16);
-  P.o_nterms = (int32_t)o; o = align_up(o + (size_t)NP, 16);
-  P.o_base = (int32_t)o; o = align_up(o + (size_t)NP * 8, 16);
-  P.o_best = (int32_t)o; o = align_up(o + (size_t)2 * N, 16);
+  auto take = [&](int32_t* field, size_t bytes) {
+    *field = (int32_t)o;
+    o = align_up(o + bytes, 16);
+  };
+  take(&P.o_sh, sizeof(Shared));
+  take(&P.o_rinfo, (size_t)N * 4);
+  take(&P.o_agg, (size_t)((L.nn + 3) | 1) * L.Q * L.Q * 4);
+  take(&P.o_terms, (size_t)NP * L.TS * 2);
+  take(&P.o_nterms, (size_t)NP * 2);
+  take(&P.o_pfb, (size_t)NP * 8);
+  take(&P.o_finfo, (size_t)FL * QG * 4);
+  take(&P.o_finl, (size_t)FL * QG);
+  take(&P.o_bsl, (size_t)N);
+  take(&P.o_bdl, (size_t)N);
+  take(&P.o_bx, (size_t)N * 4);
   const size_t fixed = o;
-  const size_t per_fam = align_up(sizeof(ChunkFam), 16) + align_up((size_t)NS * sizeof(PairRes), 16) +
-                         (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16);
+  const size_t per_fam = align_up((size_t)NS * sizeof(PairRes), 16) + 2 * align_up((size_t)N * 2, 16) +
+                         2 * align_up((size_t)N, 16) + (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return set_error(VP_ERR_HIP, "hipGetDevice failed");
   int lds_max = 0;
   if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
     return set_error(VP_ERR_HIP, "hipDeviceGetAttribute failed");
   const size_t budget = (size_t)lds_max;
-  size_t need_prologue = (size_t)N * 8;   // column sums alias the credit area
   if (fixed + per_fam > budget) return set_error(VP_ERR_UNSUPPORTED, "plan state does not fit in LDS");
-  int FC = (int)std::min<size_t>((size_t)hmax, (budget - fixed) / per_fam);
+  int FC = (int)std::min<size_t>((size_t)std::min(hmax, 64), (budget - fixed) / per_fam);
   FC = std::max(FC, 1);
   P.FC = FC;
-  P.o_cf = (int32_t)o; o = align_up(o + (size_t)FC * sizeof(ChunkFam), 16);
-  P.o_pair = (int32_t)o; o = align_up(o + (size_t)FC * NS * sizeof(PairRes), 16);
-  P.o_hp = (int32_t)o; o = align_up(o + std::max((size_t)FC * N * g2 * 4, need_prologue), 16);
-  P.o_sl = (int32_t)o; o = align_up(o + (size_t)FC * NS * N, 16);
-  P.o_dl = (int32_t)o; o = align_up(o + (size_t)FC * NS * N, 16);
+  take(&P.o_pair, (size_t)FC * NS * sizeof(PairRes));
+  take(&P.o_outT, (size_t)FC * N * 2);
+  take(&P.o_inT, (size_t)FC * N * 2);
+  take(&P.o_ipos, (size_t)FC * N);
+  take(&P.o_ocls, (size_t)FC * N);
+  take(&P.o_hp, std::max((size_t)FC * N * g2 * 4, (size_t)N * 8));   // also the prologue's column sums
+  take(&P.o_sl, (size_t)FC * NS * N);
+  take(&P.o_dl, (size_t)FC * NS * N);
   if (o > budget) return set_error(VP_ERR_UNSUPPORTED, "plan state does not fit in LDS");
 
   hipStream_t st = (hipStream_t)stream;
-  if (hipFuncSetAttribute((const void*)plan_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)o) !=
-      hipSuccess)
-    return set_error(VP_ERR_HIP, "cannot raise the planner's LDS limit");
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), o, st, P);
-  if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "planner launch failed");
-  return VP_OK;
+  const int gpl = (L.G + 63) / 64;
+  switch (g) {
+    case 2: return launch_g<2>(P, o, st, gpl);
+    case 3: return launch_g<3>(P, o, st, gpl);
+    case 4: return launch_g<4>(P, o, st, gpl);
+  }
+  return set_error(VP_ERR_UNSUPPORTED, "gpus_per_switch must be 2, 3 or 4");
 }
 
 }  // namespace vp
