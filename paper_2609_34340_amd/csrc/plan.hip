@@ -36,6 +36,7 @@ namespace {
 constexpr int kWaves = kPlanThreads / 64;
 constexpr int kMaxQG = kMaxSlotsPerNode * kMaxGpusPerSwitch;   // lanes per node
 constexpr int kMaxLTerms = 3 * kMaxSlotsPerNode;   // PIX, PXB and NIC entries of one diagonal block
+constexpr uint32_t kRawSaturated = 0xFFFFFFFEu;     // residual too large for 32 bits: reload it
 
 struct PairRes {
   int64_t F;
@@ -67,7 +68,7 @@ struct PlanArgs {
   int32_t* status;
   // LDS layout (byte offsets)
   int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo, o_finl;
-  int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_hp, o_sl, o_dl, o_bsl, o_bdl, o_bx;
+  int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bx, o_brw;
 };
 
 // ------------------------------------------------------------------ helpers
@@ -135,12 +136,19 @@ struct Perms<4> {
   }
 };
 
-// Local family descriptor word: cls | src_slot<<2 | dst_slot<<5 | out_pos<<8 | local_id<<10
+// Local family descriptor word: cls | src_slot<<2 | dst_slot<<5 | out_pos<<8 |
+// rank_same<<10 | n_other<<12 | local_id<<15.  rank_same is the instance's rank
+// among the in-instances of its destination slot of the same kind (same-node
+// or cross-node lane), n_other the number of the other kind: cross-node
+// in-instances precede same-node ones exactly when their source node is the
+// lower one.
 __device__ inline int d_cls(uint32_t w) { return w & 3; }
 __device__ inline int d_ss(uint32_t w) { return (w >> 2) & 7; }
 __device__ inline int d_ds(uint32_t w) { return (w >> 5) & 7; }
 __device__ inline int d_opos(uint32_t w) { return (w >> 8) & 3; }
-__device__ inline int d_id(uint32_t w) { return (int)(w >> 10); }
+__device__ inline int d_rsame(uint32_t w) { return (w >> 10) & 3; }
+__device__ inline int d_nother(uint32_t w) { return (w >> 12) & 7; }
+__device__ inline int d_id(uint32_t w) { return (int)(w >> 15); }
 
 // Per-family working set of the current chunk.
 struct FamCtx {
@@ -177,15 +185,26 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
   if (start == 0) {
     // canonical binding plus the highest-credit triple, ties to the smallest (t, i, j)
     uint64_t best = 0;
-    for (int t = lane; t < N; t += 64) {
+    for (int t0 = lane; t0 < N; t0 += 256) {
+      uint32_t hv[4][g2];
 #pragma unroll
-      for (int e = 0; e < g2; ++e) {
-        const uint32_t h = fc.H[t * g2 + e];
-        if (h != kForbidden && h > 0) {
-          const uint64_t key = ((uint64_t)h << 24) | (uint64_t)(0xFFFFFF - (t * g2 + e));
-          best = key > best ? key : best;
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < g2; ++e) {
+          const int tt = t0 + 64 * u < N ? t0 + 64 * u : N - 1;
+          const uint32_t x = fc.H[tt * g2 + e];
+          hv[u][e] = t0 + 64 * u < N ? x : 0;
         }
-      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int e = 0; e < g2; ++e) {
+          const uint32_t h = hv[u][e];
+          if (h != kForbidden && h > 0) {
+            const uint64_t key = ((uint64_t)h << 24) | (uint64_t)(0xFFFFFF - ((t0 + 64 * u) * g2 + e));
+            best = key > best ? key : best;
+          }
+        }
     }
     best = wave_max_u(best);
     if (best) {
@@ -295,103 +314,115 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
   // Alternating Algorithm: source half, then destination half.
   for (int sweep = 0; sweep < P.i_aa; ++sweep) {
     int changed = 0;
+    {
+      // every load of the half-step first (destinations and credit rows of all
+      // owned groups), then the g! comparisons
+      int jl[MG][g];
+      uint32_t row[MG][g][g2];
 #pragma unroll
-    for (int r = 0; r < MG; ++r) {
-      if (!own[r]) continue;
-      int jl[g];
-      uint32_t row[g][g2], h[g][g];
-#pragma unroll
-      for (int m = 0; m < g; ++m) {
-        jl[m] = DL[o[r][m]];
-#pragma unroll
-        for (int e = 0; e < g2; ++e) row[m][e] = fc.H[o[r][m] * g2 + e];
-      }
-#pragma unroll
-      for (int m = 0; m < g; ++m)
-#pragma unroll
-        for (int il = 0; il < g; ++il) {
-          uint32_t v = row[m][il * g];
-#pragma unroll
-          for (int jj = 1; jj < g; ++jj) v = jl[m] == jj ? row[m][il * g + jj] : v;
-          h[m][il] = v;
-        }
-      int64_t cur = 0;
-#pragma unroll
-      for (int m = 0; m < g; ++m) cur += h[m][sig[r][m]];
-      int64_t bestv = -1;
-      int bp = 0;
-#pragma unroll
-      for (int p = 0; p < Perms<g>::n; ++p) {
-        int64_t v = 0;
-        bool ok = true;
+      for (int r = 0; r < MG; ++r)
 #pragma unroll
         for (int m = 0; m < g; ++m) {
-          const uint32_t x = h[m][Perms<g>::at(p, m)];
-          ok = ok && x != kForbidden;
-          v += x;
-        }
-        if (ok && v > bestv) {
-          bestv = v;
-          bp = p;
-        }
-      }
-      if (bestv > cur) {
+          jl[r][m] = DL[o[r][m]];
 #pragma unroll
-        for (int m = 0; m < g; ++m) {
-          sig[r][m] = Perms<g>::at(bp, m);
-          SL[o[r][m]] = (uint8_t)sig[r][m];
+          for (int e = 0; e < g2; ++e) row[r][m][e] = fc.H[o[r][m] * g2 + e];
         }
-        changed = 1;
+#pragma unroll
+      for (int r = 0; r < MG; ++r) {
+        if (!own[r]) continue;
+        uint32_t h[g][g];
+#pragma unroll
+        for (int m = 0; m < g; ++m)
+#pragma unroll
+          for (int il = 0; il < g; ++il) {
+            uint32_t v = row[r][m][il * g];
+#pragma unroll
+            for (int jj = 1; jj < g; ++jj) v = jl[r][m] == jj ? row[r][m][il * g + jj] : v;
+            h[m][il] = v;
+          }
+        int64_t cur = 0;
+#pragma unroll
+        for (int m = 0; m < g; ++m) cur += h[m][sig[r][m]];
+        int64_t bestv = -1;
+        int bp = 0;
+#pragma unroll
+        for (int p = 0; p < Perms<g>::n; ++p) {
+          int64_t v = 0;
+          bool ok = true;
+#pragma unroll
+          for (int m = 0; m < g; ++m) {
+            const uint32_t x = h[m][Perms<g>::at(p, m)];
+            ok = ok && x != kForbidden;
+            v += x;
+          }
+          if (ok && v > bestv) {
+            bestv = v;
+            bp = p;
+          }
+        }
+        if (bestv > cur) {
+#pragma unroll
+          for (int m = 0; m < g; ++m) {
+            sig[r][m] = Perms<g>::at(bp, m);
+            SL[o[r][m]] = (uint8_t)sig[r][m];
+          }
+          changed = 1;
+        }
       }
     }
     wave_sync();
+    {
+      int il[MG][g];
+      uint32_t row[MG][g][g2];
 #pragma unroll
-    for (int r = 0; r < MG; ++r) {
-      if (!own[r]) continue;
-      int il[g];
-      uint32_t row[g][g2], h[g][g];
-#pragma unroll
-      for (int m = 0; m < g; ++m) {
-        il[m] = SL[nn_[r][m]];
-#pragma unroll
-        for (int e = 0; e < g2; ++e) row[m][e] = fc.H[nn_[r][m] * g2 + e];
-      }
-#pragma unroll
-      for (int m = 0; m < g; ++m)
-#pragma unroll
-        for (int jl = 0; jl < g; ++jl) {
-          uint32_t v = row[m][jl];
-#pragma unroll
-          for (int ii = 1; ii < g; ++ii) v = il[m] == ii ? row[m][ii * g + jl] : v;
-          h[m][jl] = v;
-        }
-      int64_t cur = 0;
-#pragma unroll
-      for (int m = 0; m < g; ++m) cur += h[m][del[r][m]];
-      int64_t bestv = -1;
-      int bp = 0;
-#pragma unroll
-      for (int p = 0; p < Perms<g>::n; ++p) {
-        int64_t v = 0;
-        bool ok = true;
+      for (int r = 0; r < MG; ++r)
 #pragma unroll
         for (int m = 0; m < g; ++m) {
-          const uint32_t x = h[m][Perms<g>::at(p, m)];
-          ok = ok && x != kForbidden;
-          v += x;
-        }
-        if (ok && v > bestv) {
-          bestv = v;
-          bp = p;
-        }
-      }
-      if (bestv > cur) {
+          il[r][m] = SL[nn_[r][m]];
 #pragma unroll
-        for (int m = 0; m < g; ++m) {
-          del[r][m] = Perms<g>::at(bp, m);
-          DL[nn_[r][m]] = (uint8_t)del[r][m];
+          for (int e = 0; e < g2; ++e) row[r][m][e] = fc.H[nn_[r][m] * g2 + e];
         }
-        changed = 1;
+#pragma unroll
+      for (int r = 0; r < MG; ++r) {
+        if (!own[r]) continue;
+        uint32_t h[g][g];
+#pragma unroll
+        for (int m = 0; m < g; ++m)
+#pragma unroll
+          for (int jl = 0; jl < g; ++jl) {
+            uint32_t v = row[r][m][jl];
+#pragma unroll
+            for (int ii = 1; ii < g; ++ii) v = il[r][m] == ii ? row[r][m][ii * g + jl] : v;
+            h[m][jl] = v;
+          }
+        int64_t cur = 0;
+#pragma unroll
+        for (int m = 0; m < g; ++m) cur += h[m][del[r][m]];
+        int64_t bestv = -1;
+        int bp = 0;
+#pragma unroll
+        for (int p = 0; p < Perms<g>::n; ++p) {
+          int64_t v = 0;
+          bool ok = true;
+#pragma unroll
+          for (int m = 0; m < g; ++m) {
+            const uint32_t x = h[m][Perms<g>::at(p, m)];
+            ok = ok && x != kForbidden;
+            v += x;
+          }
+          if (ok && v > bestv) {
+            bestv = v;
+            bp = p;
+          }
+        }
+        if (bestv > cur) {
+#pragma unroll
+          for (int m = 0; m < g; ++m) {
+            del[r][m] = Perms<g>::at(bp, m);
+            DL[nn_[r][m]] = (uint8_t)del[r][m];
+          }
+          changed = 1;
+        }
       }
     }
     wave_sync();
@@ -400,15 +431,28 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
 
   // binding score F (Eq. (8)) and the largest lane volume per path class
   int64_t F = 0, x0 = 0, x1 = 0, x2 = 0;
+  int jf[MG][g], cf[MG][g];
+  uint32_t rf[MG][g][g];
+#pragma unroll
+  for (int r = 0; r < MG; ++r)
+#pragma unroll
+    for (int m = 0; m < g; ++m) {
+      jf[r][m] = DL[o[r][m]];
+      cf[r][m] = own[r] ? fc.ocls[(lane + 64 * r) * g + m] : 0;
+#pragma unroll
+      for (int jl = 0; jl < g; ++jl) rf[r][m][jl] = fc.H[o[r][m] * g2 + sig[r][m] * g + jl];
+    }
 #pragma unroll
   for (int r = 0; r < MG; ++r) {
     if (!own[r]) continue;
-    const int a = lane + 64 * r;
 #pragma unroll
     for (int m = 0; m < g; ++m) {
-      const int64_t x = fc.H[o[r][m] * g2 + sig[r][m] * g + DL[o[r][m]]];
+      uint32_t xv = rf[r][m][0];
+#pragma unroll
+      for (int jj = 1; jj < g; ++jj) xv = jf[r][m] == jj ? rf[r][m][jj] : xv;
+      const int64_t x = xv;
       F += x;
-      const int c = fc.ocls[a * g + m];
+      const int c = cf[r][m];
       if (c == 0) x0 = x > x0 ? x : x0;
       else if (c == 1) x1 = x > x1 ? x : x1;
       else x2 = x > x2 ? x : x2;
@@ -453,11 +497,13 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   int8_t* ipos = (int8_t*)(smem + P.o_ipos);
   uint8_t* ocls = smem + P.o_ocls;
   uint32_t* hp = (uint32_t*)(smem + P.o_hp);
+  uint32_t* raw = (uint32_t*)(smem + P.o_raw);       // residual of every credit entry (saturating)
   uint8_t* sl = smem + P.o_sl;
   uint8_t* dl = smem + P.o_dl;
   uint8_t* bsl = smem + P.o_bsl;
   uint8_t* bdl = smem + P.o_bdl;
   uint32_t* bx = (uint32_t*)(smem + P.o_bx);
+  uint32_t* brw = (uint32_t*)(smem + P.o_brw);
   const int32_t* cat = P.cat;
 
   // ---------------------------------------------------------------- prologue
@@ -491,7 +537,16 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     int opos = 0;
     for (int m = 0; m < g; ++m)
       if (cat[L.off_fam_out + lf * QG + ss * g + m] == idx) opos = m;
-    finfo[x] = (uint32_t)(cls | (ss << 2) | (ds << 5) | (opos << 8) | (id << 10));
+    const bool remote = cls == VP_PATH_NIC && lf >= L.F0;
+    int rsame = 0, nother = 0;
+    for (int m = 0; m < g; ++m) {
+      const int idx2 = cat[L.off_fam_in + lf * QG + ds * g + m];
+      const bool r2 = (cat[L.off_fam_info + lf * QG + idx2] & 15) == VP_PATH_NIC && lf >= L.F0;
+      if (r2 != remote) ++nother;
+      else if (idx2 < idx) ++rsame;
+    }
+    finfo[x] = (uint32_t)(cls | (ss << 2) | (ds << 5) | (opos << 8) | (rsame << 10) | (nother << 12) |
+                          (id << 15));
     finl[x] = (uint8_t)cat[L.off_fam_in + x];
   }
   for (int x = tid; x < kS * Q * Q; x += kPlanThreads) agg[x] = 0;
@@ -628,7 +683,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
             if (kb + 3 < k1 && r3 > bv) { bv = r3; bk = kb + 3; }
           }
           s += bv;
-          j = L.J0 + (bk - 1) * L.J1 + (p - L.J0);
+          j = (bk << 12) | (p - L.J0);   // same order as the canonical shape index
         }
         const uint64_t key = ((uint64_t)(uint32_t)s << 20) | (uint64_t)(0xFFFFF - j);
         best = key > best ? key : best;
@@ -643,15 +698,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       if (tid == 0) set_err(sh, VP_ERR_NO_PROGRESS);
       break;
     }
-    const int jstar = 0xFFFFF - (int)(key & 0xFFFFF);
-    int kstar, pstar;
-    if (jstar < L.J0) {
-      kstar = 0;
-      pstar = jstar;
-    } else {
-      kstar = 1 + (jstar - L.J0) / L.J1;
-      pstar = L.J0 + (jstar - L.J0) % L.J1;
-    }
+    const int code = 0xFFFFF - (int)(key & 0xFFFFF);
+    const int kstar = code >> 12, pstar = kstar ? L.J0 + (code & 4095) : code;
     const int lb = pfb[2 * pstar], le = pfb[2 * pstar + 1];
     const int fbase = kstar == 0 ? 0 : (kstar - 1) * L.F1;
     const int fb = lb + fbase, fe = le + fbase;
@@ -676,13 +724,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           const int dn = (cl == VP_PATH_NIC && kstar) ? (n + kstar) % nn : n;
           const int d = dn * Q + d_ds(w);
           // rank of t inside the in-list of group d (family order = ascending t)
-          int mi = 0;
-          for (int m = 0; m < g; ++m) {
-            const int idx2 = finl[lf * QG + d_ds(w) * g + m];
-            const int c2 = d_cls(finfo[lf * QG + idx2]);
-            const int sn = (c2 == VP_PATH_NIC && kstar) ? (dn - kstar + nn) % nn : dn;
-            mi += (sn * QG + idx2) < t;
-          }
+          const bool remote = cl == VP_PATH_NIC && kstar;
+          const bool remote_first = dn >= kstar;   // cross-node sources sit on a lower node
+          const int mi = d_rsame(w) + ((remote != remote_first) ? d_nother(w) : 0);
           const int op = d_opos(w);
           const size_t base = (size_t)c * N;
           outT[base + a * g + op] = (uint16_t)t;
@@ -691,17 +735,20 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           ipos[base + a * g + op] = (int8_t)(d == a ? mi : -1);
           const int64_t cap = sh->cap[cl];
           uint32_t* h = hp + (base + t) * g2;
+          uint32_t* rw = raw + (base + t) * g2;
 #pragma unroll
           for (int il = 0; il < g; ++il)
 #pragma unroll
             for (int jl = 0; jl < g; ++jl) {
               const int i = a * g + il, j = d * g + jl;
-              uint32_t v = kForbidden;
+              uint32_t v = kForbidden, rv = kForbidden;
               if (i != j) {
                 const int64_t dv = P.Drem[(size_t)i * N + j];
                 v = (uint32_t)(dv < cap ? dv : cap);
+                rv = (uint32_t)(dv < (int64_t)kRawSaturated ? dv : (int64_t)kRawSaturated);
               }
               h[il * g + jl] = v;
+              rw[il * g + jl] = rv;
             }
           c += dc;
           t += dt;
@@ -778,11 +825,13 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         // a later chunk reuses this LDS: keep the winner's binding and volumes
         const int pi = sh->best_c * NS + sh->best_s;
         const uint32_t* H = hp + (size_t)sh->best_c * N * g2;
+        const uint32_t* RW = raw + (size_t)sh->best_c * N * g2;
         for (int t = tid; t < N; t += kPlanThreads) {
           const uint8_t s_ = sl[(size_t)pi * N + t], d_ = dl[(size_t)pi * N + t];
           bsl[t] = s_;
           bdl[t] = d_;
           bx[t] = H[t * g2 + s_ * g + d_];
+          brw[t] = RW[t * g2 + s_ * g + d_];
         }
         __syncthreads();
       }
@@ -797,6 +846,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       const uint8_t* SLp = live ? sl + (size_t)pi * N : bsl;
       const uint8_t* DLp = live ? dl + (size_t)pi * N : bdl;
       const uint32_t* H = hp + (size_t)sh->best_c * N * g2;
+      const uint32_t* RW = raw + (size_t)sh->best_c * N * g2;
       for (int t = tid; t < N; t += kPlanThreads) {
         const int n = rinfo[t] >> 8, idx = t - n * QG;
         const uint32_t w = finfo[lf * QG + idx];
@@ -805,12 +855,14 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         const int s_ = SLp[t], d_ = DLp[t];
         const int i = (n * Q + ss) * g + s_, j = (dn * Q + ds) * g + d_;
         const int64_t x = live ? (int64_t)H[t * g2 + s_ * g + d_] : (int64_t)bx[t];
+        const uint32_t rv = live ? RW[t * g2 + s_ * g + d_] : brw[t];
         const size_t o = (size_t)K * N + i;
         P.dst[o] = j;
         P.inst[o] = d_id(w);
         P.bytes[o] = x;
         if (x > 0) {
-          P.Drem[(size_t)i * N + j] -= x;
+          int64_t* dp = P.Drem + (size_t)i * N + j;
+          *dp = (rv < kRawSaturated ? (int64_t)rv : *dp) - x;
           int kk = dn - n;
           if (kk < 0) kk += nn;
           atomicAdd(&agg[(ss * Q + ds) * kS + kk], -(int32_t)(((uint64_t)x >> P.unit_shift) * P.odd_inv));
@@ -826,7 +878,13 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         }
         sh->key = 0;
       }
-      __syncthreads();
+      // LDS-only barrier: the global stores above need not land before the
+      // next scoring pass (which reads LDS only); the full barrier after it
+      // orders them before the next gather reads D^rem.
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), other counters untouched
+      __builtin_amdgcn_s_barrier();
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
     }
   }
 
@@ -865,11 +923,10 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   const DevCatalogLayout& L = c.lay;
   const int N = L.N, g = L.g, g2 = g * g, NS = a.p.n_start, NP = L.J0 + L.J1, FL = L.F0 + L.F1;
   const int QG = L.Q * g;
-  if (L.J >= (1 << 20)) return set_error(VP_ERR_UNSUPPORTED, "more than 2^20 shapes");
+  if (L.J0 > 4095 || L.J1 > 4095 || L.nn > 255) return set_error(VP_ERR_UNSUPPORTED, "catalog too large");
   if (QG > kMaxQG || L.Q > 8 || g > 4) return set_error(VP_ERR_UNSUPPORTED, "too many lanes per node");
   if (N > 65535 || L.G > 64 * 8) return set_error(VP_ERR_UNSUPPORTED, "too many ranks for the planner");
-  for (int i = 0; i < L.n_inst; ++i)
-    if (i >= (1 << 22)) return set_error(VP_ERR_UNSUPPORTED, "too many node-local instances");
+  if (L.n_inst >= (1 << 17)) return set_error(VP_ERR_UNSUPPORTED, "too many node-local instances");
   int hmax = 1;
   for (int p = 0; p < NP; ++p) {
     hmax = std::max(hmax, c.pat_fe[p] - c.pat_fb[p]);
@@ -930,9 +987,10 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_bsl, (size_t)N);
   take(&P.o_bdl, (size_t)N);
   take(&P.o_bx, (size_t)N * 4);
+  take(&P.o_brw, (size_t)N * 4);
   const size_t fixed = o;
   const size_t per_fam = align_up((size_t)NS * sizeof(PairRes), 16) + 2 * align_up((size_t)N * 2, 16) +
-                         2 * align_up((size_t)N, 16) + (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16);
+                         2 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return set_error(VP_ERR_HIP, "hipGetDevice failed");
   int lds_max = 0;
@@ -949,6 +1007,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_ipos, (size_t)FC * N);
   take(&P.o_ocls, (size_t)FC * N);
   take(&P.o_hp, std::max((size_t)FC * N * g2 * 4, (size_t)N * 8));   // also the prologue's column sums
+  take(&P.o_raw, (size_t)FC * N * g2 * 4);
   take(&P.o_sl, (size_t)FC * NS * N);
   take(&P.o_dl, (size_t)FC * NS * N);
   if (o > budget) return set_error(VP_ERR_UNSUPPORTED, "plan state does not fit in LDS");
