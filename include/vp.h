@@ -188,17 +188,21 @@ vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_pa
 
 /* ------------------------------------------------------------------- pack */
 
-/* Workspace bytes for vp_pack_rows / vp_pack_heads with schedule capacity
- * k_max, a send buffer of send_capacity bytes and a pack unit of unit_bytes
- * (row_bytes or head_bytes): per-step stream offsets and one source offset
- * per packed unit. */
-size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_bytes);
+/* Workspace bytes for vp_pack_rows (k = the routing's top-k, T tokens) or
+ * vp_pack_heads (k = 0) with schedule capacity k_max, a send buffer of
+ * send_capacity bytes and a pack unit of unit_bytes (row_bytes or
+ * head_bytes).  Rows: per-step stream offsets, a copy counter per token and
+ * up to k send-unit indices per token.  Heads: per-step stream offsets and
+ * one source offset per packed unit.  Returns 0 for negative sizes. */
+size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_bytes, int64_t T, int32_t k);
 
 /* Send-buffer layout (Sec. 5 "Device-resident buffer layout"): for the steps
  * in which rank `self_rank` carries bytes, in schedule order, append the next
  * x bytes of the stream to that step's destination.  Stream j is rank
  * self_rank's token rows for j in (expert, token) order:
  *   tokens     device [T, row_bytes]   token rows (bf16 or any bytes)
+ *   k                                  top-k of the routing (a token may
+ *                                      have at most k copies)
  *   sorted_tok device int32 [T*k]      from vp_demand
  *   dest_off   device int64 [N+1]      from vp_demand (row units)
  *   K, dst, bytes                      the schedule of vp_plan (device)
@@ -206,10 +210,13 @@ size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_byte
  *   step_off   device int64 [k_max+1]  where step k's slice starts in send;
  *                                      entries past K are unspecified,
  *                                      step_off[K] = total bytes
- * row_bytes must be a multiple of 16.  Slices that are not whole rows or run
- * past their stream, or a total above send_capacity, set VP_ERR_INVALID_ARGUMENT
- * or VP_ERR_CAPACITY in dev_status and write nothing to send. */
-vp_status vp_pack_rows(const void* tokens, int64_t T, int64_t row_bytes, const int32_t* sorted_tok,
+ * row_bytes must be a multiple of 16 and send_capacity / row_bytes below
+ * 2^31.  Each token row is read from HBM once and stored to all its copies.
+ * Slices that are not whole rows or run past their stream, a token id out of
+ * range or listed more than k times, or a total above send_capacity set
+ * VP_ERR_INVALID_ARGUMENT or VP_ERR_CAPACITY in dev_status and write nothing
+ * to send. */
+vp_status vp_pack_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes, const int32_t* sorted_tok,
                        const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
                        const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
                        void* send, int64_t send_capacity, int64_t* step_off, int32_t* dev_status,
@@ -227,13 +234,15 @@ vp_status vp_pack_heads(const void* act, int64_t T, int64_t token_stride, const 
 /* The two halves of vp_pack_rows / vp_pack_heads, for callers that schedule
  * or time the copy on its own.  vp_pack_prepare_* take the same arguments
  * minus `send` and run the slice and index kernels: they fill step_off and
- * the workspace (per-step stream offsets, then one int64 source byte offset
- * per packed unit) and check every slice and the capacity.  vp_pack_gather
- * then copies each unit from `src` (the tokens or activations given to the
- * prepare call) into `send` with 16-byte loads and non-temporal stores; it
- * must get the same unit_bytes, k_max, send_capacity and workspace.  It
- * writes nothing when dev_status already holds an error. */
-vp_status vp_pack_prepare_rows(const void* tokens, int64_t T, int64_t row_bytes, const int32_t* sorted_tok,
+ * the workspace (per-step stream offsets, then the copy lists of every token
+ * or the source offset of every unit) and check every slice and the
+ * capacity.  vp_pack_gather then copies the units from `src` (the tokens or
+ * activations given to the prepare call) into `send` with 16-byte loads and
+ * non-temporal stores; it must get the same unit_bytes, T, k (0 after
+ * vp_pack_prepare_heads), k_max, send_capacity and workspace.  It writes
+ * nothing when dev_status already holds an error. */
+vp_status vp_pack_prepare_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes,
+                               const int32_t* sorted_tok,
                                const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
                                const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
                                int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
@@ -243,9 +252,9 @@ vp_status vp_pack_prepare_heads(const void* act, int64_t T, int64_t token_stride
                                 const int32_t* dst, const int64_t* bytes, int32_t k_max,
                                 int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
                                 size_t ws_bytes, void* stream);
-vp_status vp_pack_gather(const void* src, int64_t unit_bytes, const int32_t* K, const int64_t* step_off,
-                         int32_t k_max, void* send, int64_t send_capacity, int32_t* dev_status,
-                         void* ws, size_t ws_bytes, void* stream);
+vp_status vp_pack_gather(const void* src, int64_t unit_bytes, int64_t T, int32_t k, const int32_t* K,
+                         const int64_t* step_off, int32_t k_max, void* send, int64_t send_capacity,
+                         int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
 
 /* --------------------------------------------------------------- helpers */
 

@@ -72,14 +72,15 @@ def lib():
     L.vp_plan_workspace.argtypes = [vp, C.POINTER(PlanParams)]
     L.vp_plan_workspace.restype = sz
     L.vp_plan.argtypes = [vp, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
-    L.vp_pack_workspace.argtypes = [i32, i64, i64]
+    L.vp_pack_workspace.argtypes = [i32, i64, i64, i64, i32]
     L.vp_pack_workspace.restype = sz
-    L.vp_pack_rows.argtypes = [vp, i64, i64, vp, vp, i32, i32, vp, vp, vp, i32, vp, i64, vp, vp, vp, sz, vp]
+    L.vp_pack_rows.argtypes = [vp, i64, i32, i64, vp, vp, i32, i32, vp, vp, vp, i32, vp, i64, vp, vp, vp, sz, vp]
     L.vp_pack_heads.argtypes = [vp, i64, i64, vp, i64, i32, i32, vp, vp, vp, i32, vp, i64, vp, vp, vp, sz, vp]
-    L.vp_pack_prepare_rows.argtypes = [vp, i64, i64, vp, vp, i32, i32, vp, vp, vp, i32, i64, vp, vp, vp, sz, vp]
+    L.vp_pack_prepare_rows.argtypes = [vp, i64, i32, i64, vp, vp, i32, i32, vp, vp, vp, i32, i64, vp, vp, vp, sz,
+                                       vp]
     L.vp_pack_prepare_heads.argtypes = [vp, i64, i64, vp, i64, i32, i32, vp, vp, vp, i32, i64, vp, vp, vp, sz,
                                         vp]
-    L.vp_pack_gather.argtypes = [vp, i64, vp, vp, i32, vp, i64, vp, vp, sz, vp]
+    L.vp_pack_gather.argtypes = [vp, i64, i64, i32, vp, vp, i32, vp, i64, vp, vp, sz, vp]
     L.vp_modeled_time.argtypes = [vp, i32, vp, vp, i64, vp, vp]
     L.vp_status_string.argtypes = [C.c_int]
     L.vp_status_string.restype = C.c_char_p
@@ -287,23 +288,29 @@ def schedule_to_host(s: dict) -> dict:
 
 # ------------------------------------------------------------------ pack
 
-def pack_workspace_bytes(k_max: int, send_capacity: int, unit: int) -> int:
-    return int(lib().vp_pack_workspace(k_max, send_capacity, unit))
+def pack_workspace_bytes(k_max: int, send_capacity: int, unit: int, T: int = 0, k: int = 0) -> int:
+    """Rows: T tokens, top-k k.  Heads: k = 0."""
+    return int(lib().vp_pack_workspace(k_max, send_capacity, unit, T, k))
 
 
 def pack_rows(tokens: torch.Tensor, row_bytes: int, sorted_tok: torch.Tensor, dest_off: torch.Tensor,
               self_rank: int, sched: dict, send: torch.Tensor, step_off: torch.Tensor,
               status: torch.Tensor, ws: Optional[torch.Tensor] = None, stream=None):
-    """vp_pack_rows: this rank's token rows into the send buffer in step order."""
+    """vp_pack_rows: this rank's token rows into the send buffer in step order.
+    sorted_tok holds T*k entries (T tokens, top-k k)."""
     if not tokens.is_cuda or not tokens.is_contiguous():
         raise ValueError("tokens must be a contiguous GPU tensor")
     T = tokens.numel() * tokens.element_size() // row_bytes
+    if T == 0 or sorted_tok.numel() % T != 0:
+        raise ValueError("sorted_tok must hold T*k entries")
+    k = sorted_tok.numel() // T
     k_max = sched["dst"].shape[0]
     N = sched["dst"].shape[1]
     cap = send.numel() * send.element_size()
     if ws is None:
-        ws = torch.empty(pack_workspace_bytes(k_max, cap, row_bytes), dtype=torch.uint8, device=send.device)
-    _check(lib().vp_pack_rows(_ptr(tokens), T, row_bytes, _ptr(sorted_tok), _ptr(dest_off), self_rank, N,
+        ws = torch.empty(pack_workspace_bytes(k_max, cap, row_bytes, T, k), dtype=torch.uint8,
+                         device=send.device)
+    _check(lib().vp_pack_rows(_ptr(tokens), T, k, row_bytes, _ptr(sorted_tok), _ptr(dest_off), self_rank, N,
                               _ptr(sched["K"]), _ptr(sched["dst"]), _ptr(sched["bytes"]), k_max, _ptr(send),
                               cap, _ptr(step_off), _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
            "vp_pack_rows")
@@ -360,13 +367,16 @@ class Pipeline:
             self.dem_ws = torch.empty(max(demand_workspace_bytes(tokens, top_k, n_experts), 1),
                                       dtype=torch.uint8, device=dev)
             cap = tokens * top_k * unit
+            ws_T, ws_k = tokens, top_k
         else:
             self.dem = dict(demand=torch.empty((N, N), dtype=torch.int64, device=dev))
             cap = tokens * (self.token_stride // unit) * unit
+            ws_T, ws_k = tokens, 0
         self.send_capacity = cap
         self.send = torch.empty(max(cap, 16), dtype=torch.uint8, device=dev)
         self.step_off = torch.empty(kmax + 1, dtype=torch.int64, device=dev)
-        self.pack_ws = torch.empty(pack_workspace_bytes(kmax, cap, unit), dtype=torch.uint8, device=dev)
+        self.pack_ws = torch.empty(pack_workspace_bytes(kmax, cap, unit, ws_T, ws_k), dtype=torch.uint8,
+                                   device=dev)
 
     # The hot path in stages (all enqueued on one stream, no host sync).
     def demand_stage(self, routing: Optional[torch.Tensor] = None, head_lo: Optional[torch.Tensor] = None,
@@ -393,7 +403,7 @@ class Pipeline:
         L, s, p = lib(), _stream(stream), self.params
         if self.mode == "moe":
             T = tokens.numel() * tokens.element_size() // self.unit
-            _check(L.vp_pack_prepare_rows(_ptr(tokens), T, self.unit, _ptr(self.dem["sorted_tok"]),
+            _check(L.vp_pack_prepare_rows(_ptr(tokens), T, self.k, self.unit, _ptr(self.dem["sorted_tok"]),
                                           _ptr(self.dem["dest_off"]), self.self_rank, self.N,
                                           _ptr(self.sched["K"]), _ptr(self.sched["dst"]),
                                           _ptr(self.sched["bytes"]), p.k_max, self.send_capacity,
@@ -411,7 +421,11 @@ class Pipeline:
         send = self.send if send is None else send
         if send.numel() < self.send_capacity:
             raise ValueError("send buffer smaller than the pipeline's capacity")
-        _check(lib().vp_pack_gather(_ptr(tokens), self.unit, _ptr(self.sched["K"]), _ptr(self.step_off),
+        if self.mode == "moe":
+            T, k = tokens.numel() * tokens.element_size() // self.unit, self.k
+        else:
+            T, k = tokens.numel() * tokens.element_size() // self.token_stride, 0
+        _check(lib().vp_pack_gather(_ptr(tokens), self.unit, T, k, _ptr(self.sched["K"]), _ptr(self.step_off),
                                     self.params.k_max, _ptr(send), self.send_capacity, _ptr(self.status),
                                     _ptr(self.pack_ws), self.pack_ws.numel(), _stream(stream)),
                "vp_pack_gather")

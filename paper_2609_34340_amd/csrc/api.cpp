@@ -228,27 +228,27 @@ vp_status vp_plan(const vp_catalog* c, const int64_t* demand, const vp_plan_para
   return vp::launch_plan(a, stream);
 }
 
-size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_bytes) {
-  if (k_max < 1 || send_capacity < 0 || unit_bytes < 1) return 0;
-  return vp::pack_workspace(k_max, send_capacity, unit_bytes);
+size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_bytes, int64_t T, int32_t k) {
+  if (k_max < 1 || send_capacity < 0 || unit_bytes < 1 || T < 0 || k < 0) return 0;
+  return vp::pack_workspace(k_max, send_capacity, unit_bytes, T, k);
 }
 
 namespace {
 
-vp_status pack_rows_stages(int stages, const void* tokens, int64_t T, int64_t row_bytes,
+vp_status pack_rows_stages(int stages, const void* tokens, int64_t T, int32_t k, int64_t row_bytes,
                            const int32_t* sorted_tok, const int64_t* dest_off, int32_t self_rank,
                            int32_t n_ranks, const int32_t* K, const int32_t* dst, const int64_t* bytes,
                            int32_t k_max, void* send, int64_t send_capacity, int64_t* step_off,
                            int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
-  if (T < 0 || row_bytes < 16 || row_bytes % 16 != 0 || n_ranks < 1 || n_ranks > vp::kMaxRanks ||
+  if (T < 0 || k < 1 || row_bytes < 16 || row_bytes % 16 != 0 || n_ranks < 1 || n_ranks > vp::kMaxRanks ||
       self_rank < 0 || self_rank >= n_ranks || k_max < 1 || send_capacity < 0)
     return set_error(VP_ERR_INVALID_ARGUMENT, "bad pack sizes (row_bytes must be a multiple of 16)");
   if (!dest_off || !K || !dst || !bytes || !step_off || !dev_status || (T > 0 && (!tokens || !sorted_tok)) ||
       ((stages & 2) && send_capacity > 0 && !send))
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
-  if (ws_bytes < vp::pack_workspace(k_max, send_capacity, row_bytes) || !ws)
+  if (ws_bytes < vp::pack_workspace(k_max, send_capacity, row_bytes, T, k) || !ws)
     return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
-  vp::PackLaunch a{0, stages, tokens, T, row_bytes, row_bytes, sorted_tok, dest_off, nullptr, self_rank, n_ranks,
+  vp::PackLaunch a{0, stages, tokens, T, k, row_bytes, row_bytes, sorted_tok, dest_off, nullptr, self_rank, n_ranks,
                    K, dst, bytes, k_max, send, send_capacity, step_off, dev_status, ws, ws_bytes};
   return vp::launch_pack(a, stream);
 }
@@ -265,30 +265,31 @@ vp_status pack_heads_stages(int stages, const void* act, int64_t T, int64_t toke
   if (!head_lo || !K || !dst || !bytes || !step_off || !dev_status || (T > 0 && !act) ||
       ((stages & 2) && send_capacity > 0 && !send))
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
-  if (ws_bytes < vp::pack_workspace(k_max, send_capacity, head_bytes) || !ws)
+  if (ws_bytes < vp::pack_workspace(k_max, send_capacity, head_bytes, T, 0) || !ws)
     return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
-  vp::PackLaunch a{1, stages, act, T, head_bytes, token_stride, nullptr, nullptr, head_lo, self_rank, n_ranks,
+  vp::PackLaunch a{1, stages, act, T, 0, head_bytes, token_stride, nullptr, nullptr, head_lo, self_rank, n_ranks,
                    K, dst, bytes, k_max, send, send_capacity, step_off, dev_status, ws, ws_bytes};
   return vp::launch_pack(a, stream);
 }
 
 }  // namespace
 
-vp_status vp_pack_rows(const void* tokens, int64_t T, int64_t row_bytes, const int32_t* sorted_tok,
+vp_status vp_pack_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes, const int32_t* sorted_tok,
                        const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
                        const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
                        void* send, int64_t send_capacity, int64_t* step_off, int32_t* dev_status,
                        void* ws, size_t ws_bytes, void* stream) {
-  return pack_rows_stages(3, tokens, T, row_bytes, sorted_tok, dest_off, self_rank, n_ranks, K, dst, bytes,
+  return pack_rows_stages(3, tokens, T, k, row_bytes, sorted_tok, dest_off, self_rank, n_ranks, K, dst, bytes,
                           k_max, send, send_capacity, step_off, dev_status, ws, ws_bytes, stream);
 }
 
-vp_status vp_pack_prepare_rows(const void* tokens, int64_t T, int64_t row_bytes, const int32_t* sorted_tok,
+vp_status vp_pack_prepare_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes,
+                               const int32_t* sorted_tok,
                                const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
                                const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
                                int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
                                size_t ws_bytes, void* stream) {
-  return pack_rows_stages(1, tokens, T, row_bytes, sorted_tok, dest_off, self_rank, n_ranks, K, dst, bytes,
+  return pack_rows_stages(1, tokens, T, k, row_bytes, sorted_tok, dest_off, self_rank, n_ranks, K, dst, bytes,
                           k_max, nullptr, send_capacity, step_off, dev_status, ws, ws_bytes, stream);
 }
 
@@ -310,16 +311,16 @@ vp_status vp_pack_prepare_heads(const void* act, int64_t T, int64_t token_stride
                            k_max, nullptr, send_capacity, step_off, dev_status, ws, ws_bytes, stream);
 }
 
-vp_status vp_pack_gather(const void* src, int64_t unit_bytes, const int32_t* K, const int64_t* step_off,
-                         int32_t k_max, void* send, int64_t send_capacity, int32_t* dev_status,
-                         void* ws, size_t ws_bytes, void* stream) {
-  if (unit_bytes < 16 || unit_bytes % 16 != 0 || k_max < 1 || send_capacity < 0)
+vp_status vp_pack_gather(const void* src, int64_t unit_bytes, int64_t T, int32_t k, const int32_t* K,
+                         const int64_t* step_off, int32_t k_max, void* send, int64_t send_capacity,
+                         int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
+  if (unit_bytes < 16 || unit_bytes % 16 != 0 || k_max < 1 || send_capacity < 0 || T < 0 || k < 0)
     return set_error(VP_ERR_INVALID_ARGUMENT, "bad gather sizes");
-  if (!src || !K || !step_off || !dev_status || (send_capacity > 0 && !send))
+  if ((T > 0 && !src) || !K || !step_off || !dev_status || (send_capacity > 0 && !send))
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
-  if (ws_bytes < vp::pack_workspace(k_max, send_capacity, unit_bytes) || !ws)
+  if (ws_bytes < vp::pack_workspace(k_max, send_capacity, unit_bytes, T, k) || !ws)
     return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
-  vp::PackLaunch a{0, 2, src, 0, unit_bytes, unit_bytes, nullptr, nullptr, nullptr, 0, 1,
+  vp::PackLaunch a{k > 0 ? 0 : 1, 2, src, T, k, unit_bytes, unit_bytes, nullptr, nullptr, nullptr, 0, 1,
                    K, nullptr, nullptr, k_max, send, send_capacity, const_cast<int64_t*>(step_off),
                    dev_status, ws, ws_bytes};
   return vp::launch_pack(a, stream);

@@ -107,7 +107,9 @@ struct PackLaunch {
   int mode;    // 0 rows, 1 heads
   int stages;  // 1 prepare (slice + index kernels), 2 gather, 3 both
   const void* src;
-  int64_t T, unit, token_stride;
+  int64_t T;
+  int32_t k;   // rows: routing top-k (copies per token at most); heads: 0
+  int64_t unit, token_stride;
   const int32_t* sorted_tok;
   const int64_t* dest_off;
   const int64_t* head_lo;
@@ -122,7 +124,7 @@ struct PackLaunch {
   void* ws;
   size_t ws_bytes;
 };
-size_t pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit);
+size_t pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit, int64_t T, int32_t k);
 vp_status launch_pack(const PackLaunch& a, void* stream);
 
 }  // namespace vp

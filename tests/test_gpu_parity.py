@@ -294,6 +294,62 @@ def test_pack_rows_capacity_error_writes_nothing(vp):
     assert (send == 0xA5).all()
 
 
+def test_pack_rows_empty_schedule(vp):
+    w, R, dem, D = moe_case(1)
+    log("pack rows, empty schedule")
+    s = dict(K=0, dst=np.zeros((0, w.n_ranks), np.int32), bytes=np.zeros((0, w.n_ranks), np.int64))
+    send, step_off, st, total = gpu_pack_rows(vp, w, R, s, 0, vpgen.tokens_bf16(w, 0), cap_extra=64)
+    assert st == 0 and total == 0
+    assert int(step_off[0].item()) == 0
+    assert (send == 0xA5).all()
+
+
+@pytest.mark.parametrize("bad", ["token_id", "too_many_copies"])
+def test_pack_rows_bad_token_list_writes_nothing(vp, bad):
+    """A token id out of range, or a token listed more than top-k times,
+    is reported and leaves the send buffer untouched."""
+    w, R, dem, D = moe_case(1)
+    log("pack rows, bad token list (%s)" % bad)
+    s = oracle_plan(1, D)
+    rt = torch.from_numpy(R).cuda()
+    d = vp.demand(rt, w.n_ranks, w.experts, w.row_bytes, sort_row=0)
+    lo, hi = int(d["dest_off"][1].item()), int(d["dest_off"][2].item())
+    assert hi - lo > w.top_k
+    d["sorted_tok"][lo:hi] = w.tokens if bad == "token_id" else 0
+    sched = vp.alloc_schedule(w.n_ranks, 8 * w.n_ranks)
+    sched["K"].fill_(s["K"])
+    sched["dst"][:s["K"]] = torch.from_numpy(s["dst"]).cuda()
+    sched["bytes"][:s["K"]] = torch.from_numpy(s["bytes"]).cuda()
+    total = int(s["bytes"][:, 0].sum())
+    send = torch.full((total,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
+    vp.pack_rows(torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda(), w.row_bytes, d["sorted_tok"],
+                 d["dest_off"], 0, sched, send, step_off, d["status"])
+    torch.cuda.synchronize()
+    assert vp.read_status(d["status"]) == vp.INVALID_ARGUMENT
+    assert (send == 0xA5).all()
+
+
+def test_pipeline_reuse_across_matrices(vp):
+    """One Pipeline, several matrices in a row: every call starts from its
+    own inputs (the per-token copy lists are rebuilt each time)."""
+    w = vpgen.config(2)
+    pipe = vp.Pipeline(w.topo, "moe", w.row_bytes, n_experts=w.experts, tokens=w.tokens, top_k=w.top_k)
+    tok = vpgen.tokens_bf16(w, 0)
+    tok_d = torch.from_numpy(tok).cuda()
+    for m in (1, 2, 1):
+        log("pipeline reuse C2 matrix %d" % m)
+        R = vpgen.routing_all(w, m)
+        send = pipe.step(routing=torch.from_numpy(R).cuda(), tokens=tok_d)
+        torch.cuda.synchronize()
+        assert vp.read_status(pipe.status) == 0
+        dem = [oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes) for i in range(w.n_ranks)]
+        D = np.stack([x["row"] for x in dem])
+        s = oracle.Catalog(w.topo).plan(D, w.row_bytes)
+        ref, _ = oracle.pack_rows(tok, w.row_bytes, dem[0]["sorted_tok"], dem[0]["dest_off"], 0, s)
+        assert torch.equal(send[:ref.size], torch.from_numpy(ref).cuda())
+
+
 @pytest.mark.parametrize("self_rank", [0, 7, 12, 15])
 def test_pack_heads_parity(vp, self_rank):
     w, hl, D = heads_case()
