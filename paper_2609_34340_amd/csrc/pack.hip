@@ -15,9 +15,10 @@
 //   index    one wavefront per step.  Rows: every packed unit is one copy of
 //            a token row, and its send-unit index joins that token's copy
 //            list.  Heads: the source byte offset of every packed unit.
-//   scatter  rows: one workgroup per token reads the row once into registers
-//            and stores it to each of its copies, so a source row leaves HBM
-//            once however many destinations it has.
+//   scatter  rows: one workgroup per (token, copy), XCD-aware so that all
+//            copies of a token run on one XCD: a source row leaves HBM once
+//            however many destinations it has, and each copy is stored in
+//            one sweep of the workgroup.
 //   gather   heads: grid-stride 16-byte copy of the units (each is read
 //            once) with non-temporal stores.
 #include <hip/hip_runtime.h>
@@ -31,6 +32,8 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
 __device__ inline void report(int32_t* status, int code) { atomicCAS(status, 0, code); }
 
 __device__ inline void wave_sync() {
@@ -39,26 +42,12 @@ __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Exclusive block scan of v over 1024 threads; returns the exclusive prefix
-// and writes the block total to *total.
-__device__ int64_t block_excl_scan(int64_t v, int64_t* wsum, int64_t* total) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  int64_t s = v;
-  for (int o = 1; o < 64; o <<= 1) {
-    int64_t y = __shfl_up(s, o);
-    if (lane >= o) s += y;
-  }
-  if (lane == 63) wsum[w] = s;
-  __syncthreads();
-  int64_t before = 0, all = 0;
-  for (int k = 0; k < 16; ++k) {
-    if (k < w) before += wsum[k];
-    all += wsum[k];
-  }
-  __syncthreads();
-  *total = all;
-  return before + s - v;
-}
+// Descriptor of one step in which this rank's lane carries units.
+struct StepDesc {
+  int64_t first;   // rows: index of the step's first unit in sorted_tok; heads: unit offset in the stream
+  int32_t u0, nu;  // first send unit, unit count
+  int32_t h0, h;   // heads: first head of the destination and its head count
+};
 
 struct SliceArgs {
   int mode;
@@ -66,36 +55,45 @@ struct SliceArgs {
   const int64_t* bytes;
   int32_t k_max, N, self;
   int64_t unit, T, send_capacity, token_stride;
-  const int64_t* dest_off;   // rows
-  const int64_t* head_lo;    // heads
+  const int64_t* bounds;     // rows: dest_off [N+1] (units); heads: head_lo [N+1]
   int64_t* step_off;
-  int64_t* cstream;          // per step: offset inside the destination stream (bytes)
+  StepDesc* desc;            // carrying steps (any order)
+  int32_t* n_desc;
   int32_t* tcnt;             // rows: per-token copy counters, cleared here
   int32_t* status;
 };
 
+constexpr int kSliceWaves = 16;
+
 // Dynamic LDS of the slice kernel for schedule capacity k_max and N ranks.
 size_t slice_lds_bytes(int32_t k_max, int32_t N) {
-  const size_t rw = std::max<size_t>((size_t)k_max, (size_t)8 * N);
-  return (size_t)k_max * (8 + 4 + 4) + rw * 8 + (size_t)N * (8 + 4);
+  return (size_t)(N + 1) * 8 + (size_t)(2 * k_max + 1) * 4 + (size_t)kSliceWaves * N * 4 +
+         (size_t)kSliceWaves * 64 * 4 + (size_t)k_max * 2 + 16;
+}
+
+// Inclusive scan over the 64 lanes of a wavefront.
+__device__ inline int64_t wave_incl_scan(int64_t v, int lane) {
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t y = __shfl_up(v, o);
+    if (lane >= o) v += y;
+  }
+  return v;
 }
 
 __global__ void __launch_bounds__(1024) slices_kernel(SliceArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int N = a.N;
-  const int RW = a.k_max > 8 * N ? a.k_max : 8 * N;
-  int64_t* xk = (int64_t*)smem;          // k_max: this rank's lane volume of step k (0: idle or rejected)
-  int64_t* xs = xk + a.k_max;            // RW: volumes in (destination, step) order, then their scan
-  int32_t* wcnt = (int32_t*)xs;          // [16][N]: per-wave destination counts (ranking only)
-  int64_t* len = xs + RW;                // N: stream length of each destination (bytes)
-  int32_t* jv = (int32_t*)(len + N);     // k_max: destination of step k, N when idle
-  int32_t* pos = jv + a.k_max;           // k_max: position in (destination, step) order
-  int32_t* run = pos + a.k_max;          // N: first position of each destination
-  __shared__ int64_t wsum[16];
-  __shared__ int64_t carry;
-  __shared__ int32_t Ks;
+  int64_t* bo = (int64_t*)smem;                 // N+1: stream bounds (dest_off or head_lo)
+  int32_t* so = (int32_t*)(bo + N + 1);         // k_max+1: units per step, then step offsets (units)
+  int32_t* cl = so + a.k_max + 1;               // k_max: step offset inside its wave chunk's share of the stream
+  int32_t* wv = cl + a.k_max;                   // [16][N]: per-wave units per destination, then prefixes
+  int32_t* xl = wv + kSliceWaves * N;           // [16][64]: lane staging for match-group sums
+  int16_t* jv = (int16_t*)(xl + kSliceWaves * 64);  // k_max: destination of step k, N when idle
+  __shared__ int64_t wtot[kSliceWaves];
+  __shared__ int32_t Ks, n_live;
 
+  const int64_t cap_units = a.send_capacity / a.unit;
   if (tid == 0) {
     int K = *a.Kp;
     if (K < 0 || K > a.k_max) {
@@ -103,168 +101,167 @@ __global__ void __launch_bounds__(1024) slices_kernel(SliceArgs a) {
       K = 0;
     }
     // every head a destination owns must lie inside the token row
-    if (a.mode == 1 && (a.head_lo[0] < 0 || a.head_lo[N] * a.unit > a.token_stride)) {
+    if (a.mode == 1 && (a.bounds[0] < 0 || a.bounds[N] * a.unit > a.token_stride)) {
       report(a.status, VP_ERR_INVALID_ARGUMENT);
       K = 0;
     }
     Ks = K;
-    carry = 0;
+    n_live = 0;
+    *a.n_desc = 0;
   }
-  for (int i = tid; i < 16 * N; i += 1024) wcnt[i] = 0;
+  for (int i = tid; i < kSliceWaves * N; i += 1024) wv[i] = 0;
+  for (int b = tid; b <= N; b += 1024) bo[b] = a.bounds[b];
   if (a.mode == 0)
     for (int64_t t = tid; t < a.T; t += 1024) a.tcnt[t] = 0;
   __syncthreads();
   const int K = Ks;
+  // each thread owns E consecutive steps for the loads and the step scan
+  const int E = (K + 1023) / 1024;
+  const int k_beg = tid * E < K ? tid * E : K, k_end = k_beg + E < K ? k_beg + E : K;
 
-  // 1. the only global loads: lane volumes and destinations, stream lengths
-  for (int k = tid; k < K; k += 1024) {
-    int64_t x = a.bytes[(size_t)k * N + a.self];
+  // 1. the only global loads of the schedule: this rank's lane per step
+  int64_t mine = 0;
+  for (int k = k_beg; k < k_end; ++k) {
+    const int64_t x = a.bytes[(size_t)k * N + a.self];
     const int j = a.dst[(size_t)k * N + a.self];
     int b = N;
+    int32_t u = 0;
     if (x != 0) {
       if (x < 0 || x % a.unit != 0 || j < 0 || j >= N || j == a.self) {
         report(a.status, VP_ERR_INVALID_ARGUMENT);
-        x = 0;
+      } else if (x / a.unit > cap_units) {
+        report(a.status, VP_ERR_CAPACITY);
       } else {
         b = j;
+        u = (int32_t)(x / a.unit);
       }
     }
-    xk[k] = x;
-    jv[k] = b;
+    so[k] = u;
+    jv[k] = (int16_t)b;
+    mine += u;
   }
-  for (int b = tid; b < N; b += 1024)
-    len[b] = a.mode == 0 ? (a.dest_off[b + 1] - a.dest_off[b]) * a.unit
-                         : a.T * (a.head_lo[b + 1] - a.head_lo[b]) * a.unit;
-  __syncthreads();
 
-  // 2. step offsets: exclusive scan of the lane volumes in schedule order
-  for (int k0 = 0; k0 < K; k0 += 1024) {
-    const int k = k0 + tid;
-    const int64_t x = k < K ? xk[k] : 0;
-    int64_t tot;
-    const int64_t e = block_excl_scan(x, wsum, &tot);
-    if (k < K) a.step_off[k] = carry + e;
-    __syncthreads();
-    if (tid == 0) carry += tot;
-    __syncthreads();
+  // 2. step offsets: exclusive scan of the units in schedule order
+  const int64_t incl = wave_incl_scan(mine, lane);
+  if (lane == 63) wtot[w] = incl;
+  __syncthreads();
+  int64_t run = incl - mine, total = 0;
+  for (int v = 0; v < kSliceWaves; ++v) {
+    if (v < w) run += wtot[v];
+    total += wtot[v];
+  }
+  if (total > cap_units) {
+    if (tid == 0) {
+      report(a.status, VP_ERR_CAPACITY);
+      a.step_off[K] = total * a.unit;
+    }
+    return;
+  }
+  for (int k = k_beg; k < k_end; ++k) {
+    const int32_t u = so[k];
+    so[k] = (int32_t)run;
+    a.step_off[k] = run * a.unit;
+    run += u;
   }
   if (tid == 0) {
-    a.step_off[K] = carry;
-    if (carry > a.send_capacity) report(a.status, VP_ERR_CAPACITY);
-    carry = 0;
+    so[K] = (int32_t)total;
+    a.step_off[K] = total * a.unit;
   }
+  __syncthreads();
 
-  // 3. stable rank of every carrying step among the steps to its
-  //    destination: wave v ranks the chunk [v*C, (v+1)*C) with ballot match
-  //    masks, then destinations and waves are scanned in (destination, wave)
-  //    order.
-  const int C = (((K + 15) / 16) + 63) & ~63;
+  // 3. offset of each step inside its destination's stream: the units of the
+  //    earlier steps to the same destination.  Wave v walks the chunk
+  //    [v*C, (v+1)*C) in order, keeping a running total per destination;
+  //    lanes of one 64-step slice that share a destination (ballot match
+  //    mask) add the units of the lower lanes of their group.
+  const int C = (((K + kSliceWaves - 1) / kSliceWaves) + 63) & ~63;
   {
     int bits = 0;
     while ((1 << bits) < N) ++bits;
     const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-    int32_t* mine = wcnt + w * N;
-    const int k_lo = w * C, k_hi = k_lo + C < K ? k_lo + C : K;
-    for (int k0 = k_lo; k0 < k_hi; k0 += 64) {
+    const uint64_t gt = lane == 63 ? 0ull : (~0ull << (lane + 1));
+    int32_t* acc = wv + w * N;
+    int32_t* stage = xl + w * 64;
+    const int c_lo = w * C, c_hi = c_lo + C < K ? c_lo + C : K;
+    for (int k0 = c_lo; k0 < c_hi; k0 += 64) {
       const int k = k0 + lane;
-      const int b = k < k_hi ? jv[k] : N;
+      const int b = k < c_hi ? jv[k] : N;
       const bool live = b < N;
+      const int32_t u = live ? so[k + 1] - so[k] : 0;
       uint64_t same = __ballot(live);
       for (int bt = 0; bt < bits; ++bt) {
         const uint64_t ones = __ballot(live && ((b >> bt) & 1));
         same &= ((b >> bt) & 1) ? ones : ~ones;
       }
-      int r = 0;
-      if (live) r = mine[b] + __popcll(same & lt);
+      stage[lane] = u;
       wave_sync();
-      if (live && (same & lt) == 0) mine[b] += __popcll(same);
+      int32_t pre = 0;
+      for (uint64_t m = same & lt; m; m &= m - 1) pre += stage[__builtin_ctzll(m)];
+      const int32_t r = live ? acc[b] + pre : 0;
       wave_sync();
-      if (live) pos[k] = r;
+      if (live && (same & gt) == 0) acc[b] = r + u;
+      wave_sync();
+      if (live) cl[k] = r;
     }
   }
   __syncthreads();
-  for (int b0 = 0; b0 < N; b0 += 1024) {
-    const int b = b0 + tid;
-    int64_t tb = 0;
-    if (b < N)
-      for (int v = 0; v < 16; ++v) tb += wcnt[v * N + b];
-    int64_t tot;
-    const int64_t e = block_excl_scan(tb, wsum, &tot);
-    if (b < N) {
-      int acc = (int)(carry + e);
-      run[b] = acc;
-      for (int v = 0; v < 16; ++v) {
-        const int c = wcnt[v * N + b];
-        wcnt[v * N + b] = acc;
-        acc += c;
-      }
+  for (int b = tid; b < N; b += 1024) {
+    int32_t s = 0;
+    for (int v = 0; v < kSliceWaves; ++v) {
+      const int32_t t = wv[v * N + b];
+      wv[v * N + b] = s;
+      s += t;
     }
-    __syncthreads();
-    if (tid == 0) carry += tot;
-    __syncthreads();
   }
-  const int KL = (int)carry;  // carrying steps
-  for (int k = tid; k < K; k += 1024)
-    if (jv[k] < N) pos[k] += wcnt[(k / C) * N + jv[k]];
   __syncthreads();
 
-  // 4. volumes in (destination, step) order, then one exclusive scan
-  for (int k = tid; k < K; k += 1024)
-    if (jv[k] < N) xs[pos[k]] = xk[k];
-  if (tid == 0) carry = 0;
-  __syncthreads();
-  for (int k0 = 0; k0 < KL; k0 += 1024) {
-    const int k = k0 + tid;
-    const int64_t x = k < KL ? xs[k] : 0;
-    int64_t tot;
-    const int64_t e = block_excl_scan(x, wsum, &tot);
-    if (k < KL) xs[k] = carry + e;
-    __syncthreads();
-    if (tid == 0) carry += tot;
-    __syncthreads();
-  }
-
-  // 5. offset of each step inside its destination's stream; bounds check
-  for (int k = tid; k < K; k += 1024) {
+  // 4. descriptors of the carrying steps; every slice must fit its stream
+  for (int k = k_beg; k < k_end; ++k) {
     const int b = jv[k];
-    if (b == N) {
-      a.cstream[k] = 0;
+    if (b == N) continue;
+    const int64_t c = (int64_t)cl[k] + wv[(k / C) * N + b];
+    const int32_t u = so[k + 1] - so[k];
+    const int64_t h = bo[b + 1] - bo[b];
+    const int64_t len = a.mode == 0 ? h : a.T * h;
+    if (c + u > len) {
+      report(a.status, VP_ERR_INVALID_ARGUMENT);
       continue;
     }
-    const int64_t c = xs[pos[k]] - xs[run[b]];
-    if (c + xk[k] > len[b]) report(a.status, VP_ERR_INVALID_ARGUMENT);
-    a.cstream[k] = c;
+    StepDesc d;
+    d.first = a.mode == 0 ? bo[b] + c : c;
+    d.u0 = so[k];
+    d.nu = u;
+    d.h0 = a.mode == 0 ? 0 : (int32_t)bo[b];
+    d.h = a.mode == 0 ? 0 : (int32_t)h;
+    a.desc[atomicAdd(&n_live, 1)] = d;
   }
+  __syncthreads();
+  if (tid == 0) *a.n_desc = n_live;
 }
 
 struct IndexArgs {
-  int mode;
-  const int32_t *Kp, *dst;
-  const int64_t* bytes;
-  int32_t N, self, k;
+  int mode, k;
   int64_t unit, T, token_stride;
   const int32_t* sorted_tok;
-  const int64_t* dest_off;
-  const int64_t* head_lo;
-  const int64_t* step_off;
-  const int64_t* cstream;
+  const StepDesc* desc;
+  const int32_t* n_desc;
   int32_t* tcnt;             // rows: copies recorded per token
   int32_t* lst;              // rows: [T][k] send-unit index of each copy
   int64_t* src_off;          // heads: source byte offset per send unit
   int32_t* status;
 };
 
-__global__ void __launch_bounds__(64) index_kernel(IndexArgs a) {
-  const int k = blockIdx.x, lane = threadIdx.x;
-  if (k >= *a.Kp || *a.status != 0) return;
-  const int64_t x = a.bytes[(size_t)k * a.N + a.self];
-  if (x <= 0) return;
-  const int j = a.dst[(size_t)k * a.N + a.self];
-  const int64_t nu = x / a.unit, u0 = a.step_off[k] / a.unit, p0 = a.cstream[k] / a.unit;
+constexpr int kIndexThreads = 256;
+
+// One workgroup per carrying step.
+__global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
+  const int i = blockIdx.x;
+  const int n = *a.n_desc, st = *a.status;
+  if (i >= n || st != 0) return;
+  const StepDesc d = a.desc[i];
   if (a.mode == 0) {
-    const int64_t first = a.dest_off[j] + p0;
-    for (int64_t u = lane; u < nu; u += 64) {
-      const int64_t tok = a.sorted_tok[first + u];
+    for (int u = threadIdx.x; u < d.nu; u += kIndexThreads) {
+      const int64_t tok = a.sorted_tok[d.first + u];
       if (tok < 0 || tok >= a.T) {
         report(a.status, VP_ERR_INVALID_ARGUMENT);
         continue;
@@ -274,50 +271,37 @@ __global__ void __launch_bounds__(64) index_kernel(IndexArgs a) {
         report(a.status, VP_ERR_INVALID_ARGUMENT);
         continue;
       }
-      a.lst[tok * a.k + slot] = (int32_t)(u0 + u);
+      a.lst[tok * a.k + slot] = d.u0 + u;
     }
   } else {
-    const int64_t h0 = a.head_lo[j], h = a.head_lo[j + 1] - h0;
-    for (int64_t u = lane; u < nu; u += 64) {
-      const int64_t p = p0 + u, tok = p / h, hd = h0 + (p - tok * h);
-      a.src_off[u0 + u] = tok * a.token_stride + hd * a.unit;
+    for (int u = threadIdx.x; u < d.nu; u += kIndexThreads) {
+      const int64_t p = d.first + u, tok = p / d.h, hd = d.h0 + (p - tok * d.h);
+      a.src_off[(int64_t)d.u0 + u] = tok * a.token_stride + hd * a.unit;
     }
   }
 }
 
-constexpr int kScatterThreads = 256;
-constexpr int kScatterUnroll = 4;
+constexpr int kScatterMaxThreads = 1024;
 
-// Rows: workgroup per token (grid-stride); the row is loaded once and
-// stored to every send unit on the token's copy list.
-__global__ void __launch_bounds__(kScatterThreads) scatter_rows_kernel(
+// Rows: one workgroup per (token, copy slot) with as many lanes as the row
+// has 16-byte vectors (up to 1024), so each copy is stored in one sweep.
+// Workgroups are handed to the eight XCDs round-robin; the mapping below
+// gives each XCD a contiguous run of (token, slot) pairs, so the copies of a
+// token are read on one XCD back to back and every row leaves HBM once
+// (the repeats hit that XCD's L2).
+__global__ void __launch_bounds__(kScatterMaxThreads) scatter_rows_kernel(
     const unsigned char* __restrict__ src, const int32_t* __restrict__ tcnt, const int32_t* __restrict__ lst,
     int64_t T, int k, int64_t unit, int64_t vpu, unsigned char* __restrict__ send, const int32_t* status) {
   if (*status != 0) return;
-  const int tid = threadIdx.x;
-  for (int64_t t = blockIdx.x; t < T; t += gridDim.x) {
-    int n = tcnt[t];
-    n = n < k ? n : k;
-    if (n <= 0) continue;
-    const u32x4* row = (const u32x4*)(src + t * unit);
-    const int32_t* copies = lst + t * k;
-    for (int64_t i0 = tid; i0 < vpu; i0 += kScatterThreads * kScatterUnroll) {
-      u32x4 r[kScatterUnroll];
-#pragma unroll
-      for (int m = 0; m < kScatterUnroll; ++m) {
-        const int64_t i = i0 + m * kScatterThreads;
-        if (i < vpu) r[m] = row[i];
-      }
-      for (int c = 0; c < n; ++c) {
-        u32x4* d = (u32x4*)(send + (int64_t)copies[c] * unit);
-#pragma unroll
-        for (int m = 0; m < kScatterUnroll; ++m) {
-          const int64_t i = i0 + m * kScatterThreads;
-          if (i < vpu) __builtin_nontemporal_store(r[m], d + i);
-        }
-      }
-    }
-  }
+  const int64_t Q = T * k, per = (Q + 7) / 8;
+  const int64_t q = (int64_t)(blockIdx.x & 7) * per + (blockIdx.x >> 3);
+  if (q >= Q) return;
+  const int64_t t = q / k;
+  const int c = (int)(q - t * k);
+  if (c >= tcnt[t]) return;
+  const u32x4* row = (const u32x4*)(src + t * unit);
+  u32x4* d = (u32x4*)(send + (int64_t)lst[q] * unit);
+  for (int64_t i = threadIdx.x; i < vpu; i += blockDim.x) __builtin_nontemporal_store(row[i], d + i);
 }
 
 constexpr int kGatherThreads = 256;
@@ -354,12 +338,13 @@ __global__ void __launch_bounds__(kGatherThreads) gather_kernel(const unsigned c
     __builtin_nontemporal_store(r, (u32x4*)(send + v * 16));
   }
 }
-size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+size_t desc_bytes(int32_t k_max) { return align_up((size_t)k_max * sizeof(StepDesc) + 16, 256); }
 
 }  // namespace
 
 size_t pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit, int64_t T, int32_t k) {
-  const size_t head = align_up((size_t)(k_max + 1) * sizeof(int64_t), 256);
+  const size_t head = desc_bytes(k_max);
   if (k > 0) return head + align_up((size_t)T * sizeof(int32_t), 256) + (size_t)T * (size_t)k * sizeof(int32_t);
   return head + ((size_t)(send_capacity / unit) + 1) * sizeof(int64_t);
 }
@@ -375,27 +360,27 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
   if (lds + 1024 > (size_t)lds_max) return set_error(VP_ERR_UNSUPPORTED, "k_max too large for the slice table");
   if (a.unit % 16 != 0) return set_error(VP_ERR_INVALID_ARGUMENT, "unit must be a multiple of 16");
   if ((a.mode == 0) != (a.k > 0)) return set_error(VP_ERR_INVALID_ARGUMENT, "top-k must be > 0 exactly for rows");
-  // rows record send-unit indices as int32
-  if (a.mode == 0 && a.send_capacity / a.unit >= ((int64_t)1 << 31))
-    return set_error(VP_ERR_UNSUPPORTED, "send buffer too large");
+  // unit counts and send-unit indices are held in 32 bits
+  if (a.send_capacity / a.unit >= ((int64_t)1 << 31)) return set_error(VP_ERR_UNSUPPORTED, "send buffer too large");
   char* ws = (char*)a.ws;
-  int64_t* cstream = (int64_t*)ws;
-  char* rest = ws + align_up((size_t)(a.k_max + 1) * sizeof(int64_t), 256);
+  StepDesc* desc = (StepDesc*)ws;
+  int32_t* n_desc = (int32_t*)(ws + (size_t)a.k_max * sizeof(StepDesc));
+  char* rest = ws + desc_bytes(a.k_max);
   int32_t* tcnt = (int32_t*)rest;
   int32_t* lst = (int32_t*)(rest + align_up((size_t)a.T * sizeof(int32_t), 256));
   int64_t* src_off = (int64_t*)rest;
 
   if (a.stages & 1) {
     SliceArgs sa{a.mode, a.K, a.dst, a.bytes, a.k_max, a.N, a.self_rank, a.unit, a.T, a.send_capacity,
-                 a.token_stride, a.dest_off, a.head_lo, a.step_off, cstream, tcnt, a.status};
+                 a.token_stride, a.mode == 0 ? a.dest_off : a.head_lo, a.step_off, desc, n_desc, tcnt, a.status};
     if (hipFuncSetAttribute((const void*)slices_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
         hipSuccess)
       return set_error(VP_ERR_HIP, "cannot raise the slice kernel's LDS limit");
     hipLaunchKernelGGL(slices_kernel, dim3(1), dim3(1024), lds, s, sa);
 
-    IndexArgs ia{a.mode, a.K, a.dst, a.bytes, a.N, a.self_rank, a.k, a.unit, a.T, a.token_stride, a.sorted_tok,
-                 a.dest_off, a.head_lo, a.step_off, cstream, tcnt, lst, src_off, a.status};
-    hipLaunchKernelGGL(index_kernel, dim3(a.k_max), dim3(64), 0, s, ia);
+    IndexArgs ia{a.mode, a.k, a.unit, a.T, a.token_stride, a.sorted_tok, desc, n_desc, tcnt, lst, src_off,
+                 a.status};
+    hipLaunchKernelGGL(index_kernel, dim3(a.k_max), dim3(kIndexThreads), 0, s, ia);
   }
   if (!(a.stages & 2)) {
     if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "pack launch failed");
@@ -403,9 +388,12 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
   }
   const int64_t vpu = a.unit / 16;
   if (a.mode == 0) {
-    if (a.T > 0) {
-      const int64_t blocks = std::min<int64_t>(a.T, 16384);
-      hipLaunchKernelGGL(scatter_rows_kernel, dim3((unsigned)blocks), dim3(kScatterThreads), 0, s,
+    const int64_t pairs = a.T * a.k;
+    if (pairs > 0) {
+      if (pairs + 8 > ((int64_t)1 << 31)) return set_error(VP_ERR_UNSUPPORTED, "too many token copies");
+      const int threads = (int)std::min<int64_t>(kScatterMaxThreads, (vpu + 63) / 64 * 64);
+      const int64_t blocks = (pairs + 7) / 8 * 8;
+      hipLaunchKernelGGL(scatter_rows_kernel, dim3((unsigned)blocks), dim3(threads), 0, s,
                          (const unsigned char*)a.src, tcnt, lst, a.T, a.k, a.unit, vpu, (unsigned char*)a.send,
                          a.status);
     }
