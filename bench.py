@@ -32,6 +32,8 @@ METRIC = "pack HBM GB/s (% of peak) + vp_plan µs per N×N demand matrix, N=8..2
 PEAK_HBM_GBS = 8000.0
 HERE = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "pack_gather_traffic.json")
+KERNEL_NAME = {"moe": "scatter_rows_kernel (vp_pack_gather, token rows)",
+               "heads": "gather_kernel (vp_pack_gather, heads)"}
 
 
 def pack_source_sha() -> str:
@@ -226,7 +228,7 @@ def main():
         "modeled_T_ms": round(float(np.mean(That)), 3),
         "plan_over_modeled_T": round(plan_us / (1e3 * float(np.mean(That))), 5),
         "wall_s": round(wall, 3),
-        "roofline": {"bound": "hbm", "kernel": "gather_kernel (vp_pack_gather)",
+        "roofline": {"bound": "hbm", "kernel": KERNEL_NAME[w.mode],
                      "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": int(gather_bytes.mean()),
