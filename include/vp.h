@@ -180,7 +180,7 @@ size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
  * of the best shape with MultiStartAA (Eq. (7)-(8)), evaluates Eq. (9)-(10)
  * exactly and appends the best activation.  Device errors:
  * VP_ERR_INVALID_DEMAND, VP_ERR_NO_PROGRESS, VP_ERR_CAPACITY, and
- * VP_ERR_UNSUPPORTED when a capacity tau*bw reaches 2^31 bytes or the total
+ * VP_ERR_UNSUPPORTED when a capacity tau*bw reaches 2^31 bytes or 2^27 units, or the total
  * demand reaches 2^42 bytes.  The catalog must have been uploaded. */
 vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_params* p,
                   int32_t* K, int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes,

@@ -47,6 +47,7 @@ struct Shared {
   uint64_t key;
   int64_t total_rem, Lmax, tau, total_units;
   int64_t cap[3];
+  int32_t capu[3];
   // best candidate so far in this iteration
   int64_t best_S, best_xm, best_bm;
   int32_t best_valid, best_f, best_k, best_c, best_s, best_chunk;
@@ -68,7 +69,7 @@ struct PlanArgs {
   int32_t* status;
   // LDS layout (byte offsets)
   int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo, o_finl;
-  int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bx, o_brw;
+  int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bx, o_brw, o_top;
 };
 
 // ------------------------------------------------------------------ helpers
@@ -86,7 +87,16 @@ extern "C" __device__ __attribute__((const)) long long __ockl_wfred_max_i64(long
 extern "C" __device__ __attribute__((const)) unsigned long long __ockl_wfred_max_u64(unsigned long long);
 __device__ inline int64_t wave_sum(int64_t v) { return __ockl_wfred_add_i64(v); }
 __device__ inline int64_t wave_max(int64_t v) { return __ockl_wfred_max_i64(v); }
+extern "C" __device__ __attribute__((const)) int __ockl_wfred_max_i32(int);
 __device__ inline uint64_t wave_max_u(uint64_t v) { return __ockl_wfred_max_u64(v); }
+__device__ inline int32_t wave_max32(int32_t v) { return __ockl_wfred_max_i32(v); }
+
+// Binding credits are held in pack units as int32 (every credit is a whole
+// number of units, so dividing by the unit keeps every comparison).  A self
+// pair holds kForbiddenU = -2^29: valid credits are below 2^27, so a sum of at
+// most four credits that includes a self pair is negative (it loses to every
+// assignment without one), and four self pairs still fit in 32 bits.
+constexpr int32_t kForbiddenU = -(1 << 29);
 
 // SplitMix64 (Steele, Lea, Flood 2014): key absorbs the fields one at a time.
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
@@ -156,16 +166,18 @@ struct FamCtx {
   const uint16_t* inT;    // [G*g] in-instance t of (group, m)
   const int8_t* ipos;     // [G*g] position of the out-instance in its group's in-list if intra, else -1
   const uint8_t* ocls;    // [G*g] path class of the out-instance
-  const uint32_t* H;      // [N*g*g] credits
+  const int32_t* H;       // [N*g*g] credits (units; kForbiddenU for a self pair)
   int f;                  // global family index
 };
 
-// One (family, start) pair; executed by one whole wavefront.
+// One (family, start) pair; executed by one whole wavefront.  `top` is the
+// family's highest-credit triple packed as credit << 24 | (2^24 - 1 - (t*g*g +
+// i*g + j)) (0 when no credit is positive).
 template <int g, int MG>
 __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8_t* DL, int start, int iter,
-                         int lane, PairRes* out) {
+                         int lane, uint64_t top, PairRes* out) {
   constexpr int g2 = g * g;
-  const int G = P.L.G, N = P.L.N;
+  const int G = P.L.G;
   int o[MG][g], nn_[MG][g], ip[MG][g], sig[MG][g], del[MG][g];
   bool own[MG];
 #pragma unroll
@@ -184,31 +196,8 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
   int protect = -1;
   if (start == 0) {
     // canonical binding plus the highest-credit triple, ties to the smallest (t, i, j)
-    uint64_t best = 0;
-    for (int t0 = lane; t0 < N; t0 += 256) {
-      uint32_t hv[4][g2];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int e = 0; e < g2; ++e) {
-          const int tt = t0 + 64 * u < N ? t0 + 64 * u : N - 1;
-          const uint32_t x = fc.H[tt * g2 + e];
-          hv[u][e] = t0 + 64 * u < N ? x : 0;
-        }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int e = 0; e < g2; ++e) {
-          const uint32_t h = hv[u][e];
-          if (h != kForbidden && h > 0) {
-            const uint64_t key = ((uint64_t)h << 24) | (uint64_t)(0xFFFFFF - ((t0 + 64 * u) * g2 + e));
-            best = key > best ? key : best;
-          }
-        }
-    }
-    best = wave_max_u(best);
-    if (best) {
-      const int idx = 0xFFFFFF - (int)(best & 0xFFFFFF);
+    if (top) {
+      const int idx = 0xFFFFFF - (int)(top & 0xFFFFFF);
       const int ts = idx / g2, e = idx - ts * g2;
       const int il = e / g, jl = e - il * g;
       protect = ts;
@@ -318,7 +307,7 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
       // every load of the half-step first (destinations and credit rows of all
       // owned groups), then the g! comparisons
       int jl[MG][g];
-      uint32_t row[MG][g][g2];
+      int32_t row[MG][g][g2];
 #pragma unroll
       for (int r = 0; r < MG; ++r)
 #pragma unroll
@@ -330,32 +319,32 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
 #pragma unroll
       for (int r = 0; r < MG; ++r) {
         if (!own[r]) continue;
-        uint32_t h[g][g];
+        int32_t h[g][g];
 #pragma unroll
         for (int m = 0; m < g; ++m)
 #pragma unroll
           for (int il = 0; il < g; ++il) {
-            uint32_t v = row[r][m][il * g];
+            int32_t v = row[r][m][il * g];
 #pragma unroll
             for (int jj = 1; jj < g; ++jj) v = jl[r][m] == jj ? row[r][m][il * g + jj] : v;
             h[m][il] = v;
           }
-        int64_t cur = 0;
+        int32_t cur = 0;
 #pragma unroll
-        for (int m = 0; m < g; ++m) cur += h[m][sig[r][m]];
-        int64_t bestv = -1;
+        for (int m = 0; m < g; ++m) {
+          int32_t v = h[m][0];
+#pragma unroll
+          for (int i2 = 1; i2 < g; ++i2) v = sig[r][m] == i2 ? h[m][i2] : v;
+          cur += v > 0 ? v : 0;   // a self pair counts as zero credit
+        }
+        int32_t bestv = -1;
         int bp = 0;
 #pragma unroll
         for (int p = 0; p < Perms<g>::n; ++p) {
-          int64_t v = 0;
-          bool ok = true;
+          int32_t v = 0;
 #pragma unroll
-          for (int m = 0; m < g; ++m) {
-            const uint32_t x = h[m][Perms<g>::at(p, m)];
-            ok = ok && x != kForbidden;
-            v += x;
-          }
-          if (ok && v > bestv) {
+          for (int m = 0; m < g; ++m) v += h[m][Perms<g>::at(p, m)];
+          if (v > bestv) {
             bestv = v;
             bp = p;
           }
@@ -373,7 +362,7 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
     wave_sync();
     {
       int il[MG][g];
-      uint32_t row[MG][g][g2];
+      int32_t row[MG][g][g2];
 #pragma unroll
       for (int r = 0; r < MG; ++r)
 #pragma unroll
@@ -385,32 +374,32 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
 #pragma unroll
       for (int r = 0; r < MG; ++r) {
         if (!own[r]) continue;
-        uint32_t h[g][g];
+        int32_t h[g][g];
 #pragma unroll
         for (int m = 0; m < g; ++m)
 #pragma unroll
           for (int jl = 0; jl < g; ++jl) {
-            uint32_t v = row[r][m][jl];
+            int32_t v = row[r][m][jl];
 #pragma unroll
             for (int ii = 1; ii < g; ++ii) v = il[r][m] == ii ? row[r][m][ii * g + jl] : v;
             h[m][jl] = v;
           }
-        int64_t cur = 0;
+        int32_t cur = 0;
 #pragma unroll
-        for (int m = 0; m < g; ++m) cur += h[m][del[r][m]];
-        int64_t bestv = -1;
+        for (int m = 0; m < g; ++m) {
+          int32_t v = h[m][0];
+#pragma unroll
+          for (int j2 = 1; j2 < g; ++j2) v = del[r][m] == j2 ? h[m][j2] : v;
+          cur += v > 0 ? v : 0;   // a self pair counts as zero credit
+        }
+        int32_t bestv = -1;
         int bp = 0;
 #pragma unroll
         for (int p = 0; p < Perms<g>::n; ++p) {
-          int64_t v = 0;
-          bool ok = true;
+          int32_t v = 0;
 #pragma unroll
-          for (int m = 0; m < g; ++m) {
-            const uint32_t x = h[m][Perms<g>::at(p, m)];
-            ok = ok && x != kForbidden;
-            v += x;
-          }
-          if (ok && v > bestv) {
+          for (int m = 0; m < g; ++m) v += h[m][Perms<g>::at(p, m)];
+          if (v > bestv) {
             bestv = v;
             bp = p;
           }
@@ -429,10 +418,11 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
     if (!__any(changed)) break;
   }
 
-  // binding score F (Eq. (8)) and the largest lane volume per path class
-  int64_t F = 0, x0 = 0, x1 = 0, x2 = 0;
+  // binding score F (Eq. (8)) and the largest lane volume per path class, in units
+  int64_t F = 0;
+  int32_t x0 = 0, x1 = 0, x2 = 0;
   int jf[MG][g], cf[MG][g];
-  uint32_t rf[MG][g][g];
+  int32_t rf[MG][g][g];
 #pragma unroll
   for (int r = 0; r < MG; ++r)
 #pragma unroll
@@ -447,10 +437,10 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
     if (!own[r]) continue;
 #pragma unroll
     for (int m = 0; m < g; ++m) {
-      uint32_t xv = rf[r][m][0];
+      int32_t x = rf[r][m][0];
 #pragma unroll
-      for (int jj = 1; jj < g; ++jj) xv = jf[r][m] == jj ? rf[r][m][jj] : xv;
-      const int64_t x = xv;
+      for (int jj = 1; jj < g; ++jj) x = jf[r][m] == jj ? rf[r][m][jj] : x;
+      x = x > 0 ? x : 0;   // a self pair serves nothing
       F += x;
       const int c = cf[r][m];
       if (c == 0) x0 = x > x0 ? x : x0;
@@ -459,9 +449,9 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
     }
   }
   F = wave_sum(F);
-  x0 = wave_max(x0);
-  x1 = wave_max(x1);
-  x2 = wave_max(x2);
+  x0 = wave_max32(x0);
+  x1 = wave_max32(x1);
+  x2 = wave_max32(x2);
   if (lane == 0) {
     out->F = F;
     out->xmax[0] = x0;
@@ -496,7 +486,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   uint16_t* inT = (uint16_t*)(smem + P.o_inT);
   int8_t* ipos = (int8_t*)(smem + P.o_ipos);
   uint8_t* ocls = smem + P.o_ocls;
-  uint32_t* hp = (uint32_t*)(smem + P.o_hp);
+  int32_t* hp = (int32_t*)(smem + P.o_hp);
   uint32_t* raw = (uint32_t*)(smem + P.o_raw);       // residual of every credit entry (saturating)
   uint8_t* sl = smem + P.o_sl;
   uint8_t* dl = smem + P.o_dl;
@@ -504,6 +494,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   uint8_t* bdl = smem + P.o_bdl;
   uint32_t* bx = (uint32_t*)(smem + P.o_bx);
   uint32_t* brw = (uint32_t*)(smem + P.o_brw);
+  uint64_t* topkey = (uint64_t*)(smem + P.o_top);    // [FC] best credit triple of each family in the chunk
   const int32_t* cat = P.cat;
 
   // ---------------------------------------------------------------- prologue
@@ -550,6 +541,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     finl[x] = (uint8_t)cat[L.off_fam_in + x];
   }
   for (int x = tid; x < kS * Q * Q; x += kPlanThreads) agg[x] = 0;
+  for (int x = tid; x < P.FC; x += kPlanThreads) topkey[x] = 0;
   int64_t* colsum = (int64_t*)hp;   // the credit area is free during the prologue
   for (int x = tid; x < N; x += kPlanThreads) colsum[x] = 0;
   __syncthreads();
@@ -608,7 +600,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       int64_t cap = tau * L.bw_cls[c] / P.unit * P.unit;
       if (cap < P.unit) cap = P.unit;
       sh->cap[c] = cap;
-      if (cap >= (int64_t(1) << 31)) set_err(sh, VP_ERR_UNSUPPORTED);
+      sh->capu[c] = (int32_t)(cap / P.unit);
+      // credits are int32 bytes below 2^31 and int32 units below 2^27
+      if (cap >= (int64_t(1) << 31) || cap / P.unit >= (int64_t(1) << 27)) set_err(sh, VP_ERR_UNSUPPORTED);
     }
     if (sh->total_rem >= (int64_t(1) << 42) || sh->total_units >= (int64_t(1) << 28))
       set_err(sh, VP_ERR_UNSUPPORTED);
@@ -734,22 +728,34 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           ocls[base + a * g + op] = (uint8_t)cl;
           ipos[base + a * g + op] = (int8_t)(d == a ? mi : -1);
           const int64_t cap = sh->cap[cl];
-          uint32_t* h = hp + (base + t) * g2;
+          int32_t* h = hp + (base + t) * g2;
           uint32_t* rw = raw + (base + t) * g2;
+          uint64_t kt = 0;
 #pragma unroll
           for (int il = 0; il < g; ++il)
 #pragma unroll
             for (int jl = 0; jl < g; ++jl) {
               const int i = a * g + il, j = d * g + jl;
-              uint32_t v = kForbidden, rv = kForbidden;
+              int32_t v = kForbiddenU;
+              uint32_t rv = kForbidden;
               if (i != j) {
                 const int64_t dv = P.Drem[(size_t)i * N + j];
-                v = (uint32_t)(dv < cap ? dv : cap);
+                // min(D^rem, cap) < 2^31 bytes, a multiple of the unit: exact quotient
+                const uint32_t vb = (uint32_t)(dv < cap ? dv : cap);
+                v = (int32_t)((vb >> P.unit_shift) * (uint32_t)P.odd_inv);
                 rv = (uint32_t)(dv < (int64_t)kRawSaturated ? dv : (int64_t)kRawSaturated);
+                const uint64_t key = ((uint64_t)(uint32_t)v << 24) | (uint64_t)(0xFFFFFF - (t * g2 + il * g + jl));
+                if (v > 0 && key > kt) kt = key;
               }
               h[il * g + jl] = v;
               rw[il * g + jl] = rv;
             }
+          if (N % 64 == 0) {   // one family per wavefront
+            kt = wave_max_u(kt);
+            if (lane == 0 && kt) atomicMax((unsigned long long*)&topkey[c], (unsigned long long)kt);
+          } else if (kt) {
+            atomicMax((unsigned long long*)&topkey[c], (unsigned long long)kt);
+          }
           c += dc;
           t += dt;
           if (t >= N) {
@@ -763,10 +769,12 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         const int c = pi / NS, s = pi - c * NS;
         FamCtx fc{outT + (size_t)c * N, inT + (size_t)c * N, ipos + (size_t)c * N, ocls + (size_t)c * N,
                   hp + (size_t)c * N * g2, cb + c};
-        run_pair<g, MG>(P, fc, sl + (size_t)pi * N, dl + (size_t)pi * N, s, K, lane, &pr[pi]);
+        run_pair<g, MG>(P, fc, sl + (size_t)pi * N, dl + (size_t)pi * N, s, K, lane, topkey[c], &pr[pi]);
       }
       __syncthreads();
       // Evaluate (Eq. (9)-(10)): best start per family, best family overall.
+      if (wave == 1)
+        for (int x = lane; x < P.FC; x += 64) topkey[x] = 0;   // for the next gather
       if (wave == 0) {
         int64_t S = 0, xm = 0, bm = 1;
         int c = -1, bs = 0;
@@ -781,8 +789,11 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
               xm2 = r.xmax[cl];
               bm2 = L.bw_cls[cl];
             }
-          if (c < 0 || utility_greater(r.F, xm2, bm2, S, xm, bm, P.lambda)) {
-            S = r.F;
+          // Eq. (10) in bytes: served volume and slowest lane
+          const int64_t Sb = r.F * P.unit;
+          xm2 *= P.unit;
+          if (c < 0 || utility_greater(Sb, xm2, bm2, S, xm, bm, P.lambda)) {
+            S = Sb;
             xm = xm2;
             bm = bm2;
             c = cc;
@@ -824,13 +835,14 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       if (cb + P.FC < fe && sh->best_chunk == cb) {
         // a later chunk reuses this LDS: keep the winner's binding and volumes
         const int pi = sh->best_c * NS + sh->best_s;
-        const uint32_t* H = hp + (size_t)sh->best_c * N * g2;
+        const int32_t* H = hp + (size_t)sh->best_c * N * g2;
         const uint32_t* RW = raw + (size_t)sh->best_c * N * g2;
         for (int t = tid; t < N; t += kPlanThreads) {
           const uint8_t s_ = sl[(size_t)pi * N + t], d_ = dl[(size_t)pi * N + t];
           bsl[t] = s_;
           bdl[t] = d_;
-          bx[t] = H[t * g2 + s_ * g + d_];
+          const int32_t hx = H[t * g2 + s_ * g + d_];
+          bx[t] = (uint32_t)(hx > 0 ? hx : 0);
           brw[t] = RW[t * g2 + s_ * g + d_];
         }
         __syncthreads();
@@ -845,7 +857,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       const int pi = sh->best_c * NS + sh->best_s;
       const uint8_t* SLp = live ? sl + (size_t)pi * N : bsl;
       const uint8_t* DLp = live ? dl + (size_t)pi * N : bdl;
-      const uint32_t* H = hp + (size_t)sh->best_c * N * g2;
+      const int32_t* H = hp + (size_t)sh->best_c * N * g2;
       const uint32_t* RW = raw + (size_t)sh->best_c * N * g2;
       for (int t = tid; t < N; t += kPlanThreads) {
         const int n = rinfo[t] >> 8, idx = t - n * QG;
@@ -854,18 +866,20 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         const int dn = (cl == VP_PATH_NIC && k) ? (n + k) % nn : n;
         const int s_ = SLp[t], d_ = DLp[t];
         const int i = (n * Q + ss) * g + s_, j = (dn * Q + ds) * g + d_;
-        const int64_t x = live ? (int64_t)H[t * g2 + s_ * g + d_] : (int64_t)bx[t];
+        int32_t xu = live ? H[t * g2 + s_ * g + d_] : (int32_t)bx[t];   // units
+        xu = xu > 0 ? xu : 0;   // a self pair serves nothing
+        const int64_t x = (int64_t)xu * P.unit;
         const uint32_t rv = live ? RW[t * g2 + s_ * g + d_] : brw[t];
         const size_t o = (size_t)K * N + i;
         P.dst[o] = j;
         P.inst[o] = d_id(w);
         P.bytes[o] = x;
-        if (x > 0) {
+        if (xu > 0) {
           int64_t* dp = P.Drem + (size_t)i * N + j;
           *dp = (rv < kRawSaturated ? (int64_t)rv : *dp) - x;
           int kk = dn - n;
           if (kk < 0) kk += nn;
-          atomicAdd(&agg[(ss * Q + ds) * kS + kk], -(int32_t)(((uint64_t)x >> P.unit_shift) * P.odd_inv));
+          atomicAdd(&agg[(ss * Q + ds) * kS + kk], -xu);
         }
       }
       if (tid == 0) {
@@ -990,7 +1004,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_brw, (size_t)N * 4);
   const size_t fixed = o;
   const size_t per_fam = align_up((size_t)NS * sizeof(PairRes), 16) + 2 * align_up((size_t)N * 2, 16) +
-                         2 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16);
+                         2 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16) + 16;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return set_error(VP_ERR_HIP, "hipGetDevice failed");
   int lds_max = 0;
@@ -1010,6 +1024,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_raw, (size_t)FC * N * g2 * 4);
   take(&P.o_sl, (size_t)FC * NS * N);
   take(&P.o_dl, (size_t)FC * NS * N);
+  take(&P.o_top, (size_t)FC * 8);
   if (o > budget) return set_error(VP_ERR_UNSUPPORTED, "plan state does not fit in LDS");
 
   hipStream_t st = (hipStream_t)stream;
