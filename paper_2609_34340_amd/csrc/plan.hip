@@ -300,7 +300,11 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
   }
   wave_sync();
 
-  // Alternating Algorithm: source half, then destination half.
+  // Alternating Algorithm: source half, then destination half.  A half that
+  // changes nothing, other than the very first, leaves a fixed point: the
+  // half before it made its own side optimal against this side, which has
+  // not moved.  Stopping there gives the same binding as stopping after a
+  // whole unchanged sweep, one sweep earlier.
   for (int sweep = 0; sweep < P.i_aa; ++sweep) {
     int changed = 0;
     {
@@ -360,6 +364,8 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
       }
     }
     wave_sync();
+    if (sweep > 0 && !__any(changed)) break;
+    changed = 0;
     {
       int il[MG][g];
       int32_t row[MG][g][g2];
