@@ -268,6 +268,25 @@ void build_device_image(vp_catalog& c) {
   L.off_fam_out = off; off += FL * QG;
   L.off_fam_in = off; off += FL * QG;
   L.off_perms = off; off += np * g;
+  // distinct NIC-lane sets of the NIC-carrying patterns: the shift part of a
+  // shape's score depends on its pattern only through this set
+  std::map<std::vector<int>, int> set_id;
+  std::vector<std::vector<int>> sets;
+  std::vector<int> psid(c.J1);
+  for (int p = c.J0; p < P; ++p) {
+    std::vector<int> e;
+    for (int x = 0; x < Q * Q; ++x)
+      if (c.patR[p][x]) e.push_back(x);
+    auto it = set_id.find(e);
+    if (it == set_id.end()) {
+      it = set_id.emplace(e, (int)sets.size()).first;
+      sets.push_back(e);
+    }
+    psid[p - c.J0] = it->second;
+  }
+  L.nS = (int)sets.size();
+  L.off_rset = off; off += L.nS * kMaxRTerms;
+  L.off_psid = off; off += c.J1;
   L.total = off;
   L.bw_cls[VP_PATH_PIX] = c.topo.pcie_bytes_per_ns;
   L.bw_cls[VP_PATH_PXB] = c.topo.pcie_bytes_per_ns;
@@ -297,6 +316,10 @@ void build_device_image(vp_catalog& c) {
       im[L.off_fam_in + f * QG + c.idst[id] * g + ni[c.idst[id]]++] = x;
     }
   }
+  for (int si = 0; si < L.nS; ++si)
+    for (int m = 0; m < kMaxRTerms; ++m)
+      im[L.off_rset + si * kMaxRTerms + m] = m < (int)sets[si].size() ? sets[si][m] : -1;
+  for (int p = 0; p < c.J1; ++p) im[L.off_psid + p] = psid[p];
   std::vector<int> perm(g);
   for (int x = 0; x < g; ++x) perm[x] = x;
   int pi = 0;

@@ -17,6 +17,7 @@ constexpr int kMaxRanks = 1024;
 constexpr int kMaxNodes = 256;
 constexpr int kMaxStarts = 16;
 constexpr int kPlanThreads = 1024;
+constexpr int kMaxRTerms = 8;   // NIC lanes of one node-local pattern (one per source slot)
 
 // Sentinel credit of a self pair (never bindable).
 constexpr uint32_t kForbidden = 0xFFFFFFFFu;
@@ -39,6 +40,9 @@ struct DevCatalogLayout {
   int32_t off_fam_out;   // (F0+F1) * Q*g : [slot][m] local index of the m-th out-instance
   int32_t off_fam_in;    // (F0+F1) * Q*g : [slot][m] local index of the m-th in-instance
   int32_t off_perms;     // n_perm * g, lexicographic order
+  int32_t nS;            // distinct NIC-lane sets of the NIC-carrying patterns
+  int32_t off_rset;      // nS * kMaxRTerms slot-pair indices q*Q+q2 of each set (-1 past its end)
+  int32_t off_psid;      // J1: set of each NIC-carrying pattern
   int32_t total;         // int32 elements
   int64_t bw_cls[3];     // rate of PIX, PXB, NIC paths
   int64_t bw_max;

@@ -63,13 +63,16 @@ struct PlanArgs {
   uint64_t seed;
   uint64_t odd_inv, odd_lim;
   int32_t unit_shift;
-  int32_t n_start, i_aa, k_max, FC, KC;
+  int32_t n_start, i_aa, k_max, FC;
+  int32_t LPS, SPT;   // shift scoring: lanes per NIC-lane set (a power of two) and shifts per lane
+  int32_t MLT, MRT;   // most diagonal-block terms of a pattern; largest NIC-lane set
   int32_t *K, *family, *dst, *inst;
   int64_t *bytes, *tau;
   int32_t* status;
   // LDS layout (byte offsets)
   int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo, o_finl;
   int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bx, o_brw, o_top;
+  int32_t o_rset, o_psid, o_rbest, o_pbase, o_lastj, o_lastv;
 };
 
 // ------------------------------------------------------------------ helpers
@@ -468,6 +471,15 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
 
 __device__ inline void set_err(Shared* sh, int code) { atomicCAS(&sh->err, 0, code); }
 
+// Workgroup barrier that orders LDS only: outstanding global stores of the
+// waves are not waited for.
+__device__ inline void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), other counters untouched
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 template <int g, int MG>
 __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
@@ -478,7 +490,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   const int NP = L.J0 + L.J1, NS = P.n_start, FL = L.F0 + L.F1;
   Shared* sh = (Shared*)(smem + P.o_sh);
   int32_t* rinfo = (int32_t*)(smem + P.o_rinfo);
-  int32_t* agg = (int32_t*)(smem + P.o_agg);         // [q][q2][k] units: k = 0 is A, k > 0 is B_k
+  int32_t* agg = (int32_t*)(smem + P.o_agg);         // [q][q2][k] units: k = 0 is A, k > 0 is B_k;
+                                                     // then one row of zeros
   // row stride: odd (lanes reading one shift of different rows hit distinct
   // banks) and at least nn + 3 (zero padding for the 4-wide shift unroll)
   const int kS = (nn + 3) | 1;
@@ -501,6 +514,15 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   uint32_t* bx = (uint32_t*)(smem + P.o_bx);
   uint32_t* brw = (uint32_t*)(smem + P.o_brw);
   uint64_t* topkey = (uint64_t*)(smem + P.o_top);    // [FC] best credit triple of each family in the chunk
+  uint16_t* rset = (uint16_t*)(smem + P.o_rset);     // [nS][kMaxRTerms] agg row offsets (zero row past the end)
+  uint16_t* psid = (uint16_t*)(smem + P.o_psid);     // [J1] NIC-lane set of each NIC-carrying pattern
+  uint64_t* rbest = (uint64_t*)(smem + P.o_rbest);   // [nS] best shift: units << 12 | (4095 - shift)
+  int32_t* pbase = (int32_t*)(smem + P.o_pbase);     // [NP] diagonal-block score of each pattern
+  // D^rem entry each source rank's lane changed last, and its new value: the
+  // next credit gather takes it from here, so no barrier has to wait for the
+  // global store (stores of earlier iterations are complete by then).
+  int32_t* lastj = (int32_t*)(smem + P.o_lastj);
+  int64_t* lastv = (int64_t*)(smem + P.o_lastv);
   const int32_t* cat = P.cat;
 
   // ---------------------------------------------------------------- prologue
@@ -516,7 +538,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     const int grp = r / g;
     rinfo[r] = ((grp / Q) << 8) | ((grp % Q) << 4) | (r - grp * g);
   }
-  for (int x = tid; x < NP * L.TS; x += kPlanThreads) terms[x] = (uint16_t)cat[L.off_terms + x];
+  for (int x = tid; x < NP * L.TS + 4; x += kPlanThreads)
+    terms[x] = x < NP * L.TS ? (uint16_t)cat[L.off_terms + x] : 0;
   for (int p = tid; p < NP; p += kPlanThreads) {
     // terms are stored diagonal-block first, then shift-block
     const int n = cat[L.off_nterms + p];
@@ -546,8 +569,14 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
                           (id << 15));
     finl[x] = (uint8_t)cat[L.off_fam_in + x];
   }
-  for (int x = tid; x < kS * Q * Q; x += kPlanThreads) agg[x] = 0;
+  for (int x = tid; x < kS * (Q * Q + 1); x += kPlanThreads) agg[x] = 0;
+  for (int x = tid; x < L.nS * kMaxRTerms; x += kPlanThreads) {
+    const int e = cat[L.off_rset + x];
+    rset[x] = (uint16_t)((e < 0 ? Q * Q : e) * kS);   // absent terms read the zero row
+  }
+  for (int x = tid; x < L.J1; x += kPlanThreads) psid[x] = (uint16_t)cat[L.off_psid + x];
   for (int x = tid; x < P.FC; x += kPlanThreads) topkey[x] = 0;
+  for (int x = tid; x < N; x += kPlanThreads) lastj[x] = -1;
   int64_t* colsum = (int64_t*)hp;   // the credit area is free during the prologue
   for (int x = tid; x < N; x += kPlanThreads) colsum[x] = 0;
   __syncthreads();
@@ -625,73 +654,93 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     }
     const int K = sh->K;
 
-    // Step 1: score every node-local pattern over every shift; argmax.
-    // Items: the J0 intra-node patterns, then (NIC-carrying pattern, shift
-    // chunk) pairs; KC chunks of KW shifts each.
+    // Step 1: score every shape; argmax.  A shape (k, p) scores base(p), its
+    // diagonal-block terms against A, plus, for k > 0, the sum of B_k over
+    // its NIC-lane set.  The shift part depends on p only through that set,
+    // so (a) every distinct set finds its best shift (LPS lanes per set,
+    // SPT shifts each, ties to the lowest shift) while other threads compute
+    // every base(p); (b) one thread per pattern adds its set's best and the
+    // block takes the argmax (ties to the lowest canonical shape index).
     {
-      uint64_t best = 0;
-      const int KW = (nn - 1 + P.KC - 1) / P.KC;
-      const int items = L.J0 + L.J1 * P.KC;
-      for (int x = tid; x < items; x += kPlanThreads) {
-        int p, k0 = 0, k1 = 0;
-        if (x < L.J0) {
-          p = x;
-        } else {
-          const int y = x - L.J0;
-          p = L.J0 + y / P.KC;
-          k0 = 1 + (y - (y / P.KC) * P.KC) * KW;
-          k1 = min(nn, k0 + KW);
-        }
-        const uint16_t* tp = terms + p * L.TS;
-        const int nl = nterms[p] & 255, nr = nterms[p] >> 8;
-        // fully unrolled, predicated term loops: static register indices and
-        // all LDS reads of a loop in flight together
-        int32_t s = 0;
+      const int na = L.nS * P.LPS;
+      for (int x = tid; x < na + NP; x += kPlanThreads) {
+        if (x < na) {
+          const int si = x / P.LPS, ch = x - si * P.LPS;
+          const int k0 = 1 + ch * P.SPT, k1 = min(nn, k0 + P.SPT);
+          // all loads unconditional and independent: absent terms read the zero row
+          int off[kMaxRTerms];
 #pragma unroll
-        for (int m = 0; m < kMaxLTerms; ++m)
-          if (m < nl) {
-            const int t = tp[m];
-            s += (t & 15) * agg[(((t >> 8) & 15) * Q + ((t >> 4) & 15)) * kS];
-          }
-        int j = p;
-        if (p >= L.J0) {
-          if (k0 >= k1) continue;
-          // best shift of this chunk for the NIC part (counts are one lane
-          // per slot pair), ties to the lowest shift
-          int off[kMaxSlotsPerNode];
-#pragma unroll
-          for (int m = 0; m < kMaxSlotsPerNode; ++m) {
-            const int t = m < nr ? tp[nl + m] : 0;
-            off[m] = (((t >> 8) & 15) * Q + ((t >> 4) & 15)) * kS;
-          }
-          int32_t bv = -1;
-          int bk = k0;
+          for (int m = 0; m < kMaxRTerms; ++m) off[m] = rset[si * kMaxRTerms + m];
+          uint64_t bkey = 0;
           for (int kb = k0; kb < k1; kb += 4) {
             int32_t r0 = 0, r1 = 0, r2 = 0, r3 = 0;
 #pragma unroll
-            for (int m = 0; m < kMaxSlotsPerNode; ++m)
-              if (m < nr) {
-                const int32_t* row = agg + off[m] + kb;
+            for (int m0 = 0; m0 < kMaxRTerms; m0 += 4) {
+              if (m0 >= P.MRT) break;
+#pragma unroll
+              for (int m = m0; m < m0 + 4; ++m) {
+                const int32_t* row = agg + off[m] + kb;   // rows are zero-padded past nn
                 r0 += row[0];
                 r1 += row[1];
                 r2 += row[2];
                 r3 += row[3];
               }
-            if (r0 > bv) { bv = r0; bk = kb; }
-            if (kb + 1 < k1 && r1 > bv) { bv = r1; bk = kb + 1; }
-            if (kb + 2 < k1 && r2 > bv) { bv = r2; bk = kb + 2; }
-            if (kb + 3 < k1 && r3 > bv) { bv = r3; bk = kb + 3; }
+            }
+            const uint64_t c0 = ((uint64_t)(uint32_t)r0 << 12) | (uint64_t)(4095 - kb);
+            const uint64_t c1 = kb + 1 < k1 ? ((uint64_t)(uint32_t)r1 << 12) | (uint64_t)(4094 - kb) : 0;
+            const uint64_t c2 = kb + 2 < k1 ? ((uint64_t)(uint32_t)r2 << 12) | (uint64_t)(4093 - kb) : 0;
+            const uint64_t c3 = kb + 3 < k1 ? ((uint64_t)(uint32_t)r3 << 12) | (uint64_t)(4092 - kb) : 0;
+            bkey = c0 > bkey ? c0 : bkey;
+            bkey = c1 > bkey ? c1 : bkey;
+            bkey = c2 > bkey ? c2 : bkey;
+            bkey = c3 > bkey ? c3 : bkey;
           }
-          s += bv;
-          j = (bk << 12) | (p - L.J0);   // same order as the canonical shape index
+          // the LPS lanes of a set are adjacent lanes of one wavefront
+          for (int o = 1; o < P.LPS; o <<= 1) {
+            const uint64_t y = __shfl_xor(bkey, o);
+            bkey = y > bkey ? y : bkey;
+          }
+          if (ch == 0) rbest[si] = bkey;
+        } else {
+          const int p = x - na;
+          const uint16_t* tp = terms + p * L.TS;
+          const int nl = nterms[p] & 255;
+          // term slots four at a time up to the longest diagonal part, every
+          // load of a group issued together; slots past this pattern's own
+          // count weigh zero (the term array is padded)
+          int32_t sb = 0;
+          for (int m0 = 0; m0 < P.MLT; m0 += 4) {
+            int tv[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) tv[m] = tp[m0 + m];
+            int32_t av[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) av[m] = agg[(((tv[m] >> 8) & 15) * Q + ((tv[m] >> 4) & 15)) * kS];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) sb += (m0 + m < nl ? (tv[m] & 15) : 0) * av[m];
+          }
+          pbase[p] = sb;
         }
-        const uint64_t key = ((uint64_t)(uint32_t)s << 20) | (uint64_t)(0xFFFFF - j);
+      }
+    }
+    lds_barrier();
+    {
+      uint64_t best = 0;
+      for (int p = tid; p < NP; p += kPlanThreads) {
+        int32_t sc = pbase[p];
+        int j = p;
+        if (p >= L.J0) {
+          const uint64_t rb = rbest[psid[p - L.J0]];
+          sc += (int32_t)(rb >> 12);
+          j = ((4095 - (int)(rb & 4095)) << 12) | (p - L.J0);   // same order as the canonical shape index
+        }
+        const uint64_t key = ((uint64_t)(uint32_t)sc << 20) | (uint64_t)(0xFFFFF - j);
         best = key > best ? key : best;
       }
       best = wave_max_u(best);
-      if (lane == 0) atomicMax((unsigned long long*)&sh->key, (unsigned long long)best);
+      if (lane == 0 && best) atomicMax((unsigned long long*)&sh->key, (unsigned long long)best);
     }
-    __syncthreads();
+    lds_barrier();
     const uint64_t key = sh->key;
     if ((key >> 20) == 0) {
       __syncthreads();
@@ -745,7 +794,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
               int32_t v = kForbiddenU;
               uint32_t rv = kForbidden;
               if (i != j) {
-                const int64_t dv = P.Drem[(size_t)i * N + j];
+                const int64_t dv = lastj[i] == j ? lastv[i] : P.Drem[(size_t)i * N + j];
                 // min(D^rem, cap) < 2^31 bytes, a multiple of the unit: exact quotient
                 const uint32_t vb = (uint32_t)(dv < cap ? dv : cap);
                 v = (int32_t)((vb >> P.unit_shift) * (uint32_t)P.odd_inv);
@@ -770,13 +819,15 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           }
         }
       }
-      __syncthreads();
+      lds_barrier();
       for (int pi = wave; pi < nc * NS; pi += kWaves) {
         const int c = pi / NS, s = pi - c * NS;
         FamCtx fc{outT + (size_t)c * N, inT + (size_t)c * N, ipos + (size_t)c * N, ocls + (size_t)c * N,
                   hp + (size_t)c * N * g2, cb + c};
         run_pair<g, MG>(P, fc, sl + (size_t)pi * N, dl + (size_t)pi * N, s, K, lane, topkey[c], &pr[pi]);
       }
+      // full barrier: the previous iteration's D^rem stores are complete
+      // before the next gather reads D^rem
       __syncthreads();
       // Evaluate (Eq. (9)-(10)): best start per family, best family overall.
       if (wave == 1)
@@ -882,7 +933,12 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         P.bytes[o] = x;
         if (xu > 0) {
           int64_t* dp = P.Drem + (size_t)i * N + j;
-          *dp = (rv < kRawSaturated ? (int64_t)rv : *dp) - x;
+          int64_t nv;
+          if (__builtin_expect(rv < kRawSaturated, 1)) nv = (int64_t)rv - x;
+          else nv = *dp - x;   // the residual did not fit the 32-bit copy
+          *dp = nv;
+          lastj[i] = j;
+          lastv[i] = nv;
           int kk = dn - n;
           if (kk < 0) kk += nn;
           atomicAdd(&agg[(ss * Q + ds) * kS + kk], -xu);
@@ -947,14 +1003,20 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   if (QG > kMaxQG || L.Q > 8 || g > 4) return set_error(VP_ERR_UNSUPPORTED, "too many lanes per node");
   if (N > 65535 || L.G > 64 * 8) return set_error(VP_ERR_UNSUPPORTED, "too many ranks for the planner");
   if (L.n_inst >= (1 << 17)) return set_error(VP_ERR_UNSUPPORTED, "too many node-local instances");
-  int hmax = 1;
+  int hmax = 1, mlt = 0, mrt = 0;
   for (int p = 0; p < NP; ++p) {
     hmax = std::max(hmax, c.pat_fe[p] - c.pat_fb[p]);
     int nl = 0;
     for (int v : c.patL[p]) nl += v != 0;
     if (nl > kMaxLTerms) return set_error(VP_ERR_UNSUPPORTED, "too many intra-node lane classes");
-    for (int v : c.patR[p])   // one NIC per switch: at most one cross-node lane per slot pair
+    mlt = std::max(mlt, nl);
+    int nr = 0;
+    for (int v : c.patR[p]) {   // one NIC per switch: at most one cross-node lane per slot pair
       if (v > 1) return set_error(VP_ERR_UNSUPPORTED, "more than one NIC lane per slot pair");
+      nr += v != 0;
+    }
+    if (nr > kMaxRTerms) return set_error(VP_ERR_UNSUPPORTED, "too many NIC lanes in one pattern");
+    mrt = std::max(mrt, nr);
   }
 
   PlanArgs P{};
@@ -979,10 +1041,19 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   P.odd_inv = inv;
   P.odd_lim = ~uint64_t(0) / u;
   P.n_start = NS;
+  P.MLT = mlt;
+  P.MRT = mrt;
   P.i_aa = a.p.i_aa;
   P.k_max = a.p.k_max;
   // shift chunks per NIC-carrying pattern: enough items to occupy every thread
-  P.KC = L.J1 > 0 ? std::max(1, std::min(L.nn - 1, kPlanThreads / L.J1)) : 1;
+  // shift scoring: about 8 shifts per lane, lanes per set a power of two
+  {
+    const int shifts = std::max(1, L.nn - 1);
+    int lps = 1;
+    while (lps < 64 && lps * 8 < shifts) lps <<= 1;
+    P.LPS = lps;
+    P.SPT = (shifts + lps - 1) / lps;
+  }
   P.K = a.K;
   P.family = a.family;
   P.dst = a.dst;
@@ -998,8 +1069,8 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   };
   take(&P.o_sh, sizeof(Shared));
   take(&P.o_rinfo, (size_t)N * 4);
-  take(&P.o_agg, (size_t)((L.nn + 3) | 1) * L.Q * L.Q * 4);
-  take(&P.o_terms, (size_t)NP * L.TS * 2);
+  take(&P.o_agg, (size_t)((L.nn + 3) | 1) * (L.Q * L.Q + 1) * 4);
+  take(&P.o_terms, ((size_t)NP * L.TS + 4) * 2);
   take(&P.o_nterms, (size_t)NP * 2);
   take(&P.o_pfb, (size_t)NP * 8);
   take(&P.o_finfo, (size_t)FL * QG * 4);
@@ -1008,6 +1079,12 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_bdl, (size_t)N);
   take(&P.o_bx, (size_t)N * 4);
   take(&P.o_brw, (size_t)N * 4);
+  take(&P.o_rset, (size_t)L.nS * kMaxRTerms * 2);
+  take(&P.o_psid, (size_t)L.J1 * 2);
+  take(&P.o_rbest, (size_t)L.nS * 8);
+  take(&P.o_pbase, (size_t)NP * 4);
+  take(&P.o_lastj, (size_t)N * 4);
+  take(&P.o_lastv, (size_t)N * 8);
   const size_t fixed = o;
   const size_t per_fam = align_up((size_t)NS * sizeof(PairRes), 16) + 2 * align_up((size_t)N * 2, 16) +
                          2 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16) + 16;
