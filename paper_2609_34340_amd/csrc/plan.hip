@@ -72,7 +72,7 @@ struct PlanArgs {
   // LDS layout (byte offsets)
   int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo, o_finl;
   int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bx, o_brw, o_top;
-  int32_t o_rset, o_psid, o_rbest, o_pbase, o_lastj, o_lastv;
+  int32_t o_rset, o_psid, o_rbest, o_pbase, o_lastj, o_lastv, o_rp;
 };
 
 // ------------------------------------------------------------------ helpers
@@ -175,10 +175,11 @@ struct FamCtx {
 
 // One (family, start) pair; executed by one whole wavefront.  `top` is the
 // family's highest-credit triple packed as credit << 24 | (2^24 - 1 - (t*g*g +
-// i*g + j)) (0 when no credit is positive).
+// i*g + j)) (0 when no credit is positive); `rperm` holds, for a shuffled
+// start, every group's source and destination permutation.
 template <int g, int MG>
-__device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8_t* DL, int start, int iter,
-                         int lane, uint64_t top, PairRes* out) {
+__device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8_t* DL, int start,
+                         const uint8_t* rperm, int lane, uint64_t top, PairRes* out) {
   constexpr int g2 = g * g;
   const int G = P.L.G;
   int o[MG][g], nn_[MG][g], ip[MG][g], sig[MG][g], del[MG][g];
@@ -229,36 +230,17 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
       }
     }
   } else {
-    // independent Fisher-Yates shuffles of every group's sources and destinations
-    uint64_t k3 = P.seed;
-    k3 = sm_mix(k3 + kGolden) ^ (uint64_t)iter;
-    k3 = sm_mix(k3 + kGolden) ^ (uint64_t)fc.f;
-    k3 = sm_mix(k3 + kGolden) ^ (uint64_t)start;
+    // independent Fisher-Yates shuffles of every group's sources and
+    // destinations, drawn during the credit gather (packed 2 bits per member)
 #pragma unroll
     for (int r = 0; r < MG; ++r) {
       if (!own[r]) continue;
       const int a = lane + 64 * r;
-      const uint64_t k4 = sm_mix(k3 + kGolden) ^ (uint64_t)a;
+      const int ps = rperm[2 * a], pd = rperm[2 * a + 1];
 #pragma unroll
-      for (int side = 0; side < 2; ++side) {
-        const uint64_t key = sm_mix(k4 + kGolden) ^ (uint64_t)side;
-        uint64_t state = key;
-        int perm[g];
-#pragma unroll
-        for (int m = 0; m < g; ++m) perm[m] = m;
-#pragma unroll
-        for (int m = g - 1; m >= 1; --m) {
-          state += kGolden;
-          const int j = (int)(sm_mix(state) % (uint64_t)(m + 1));
-          const int x = perm[m];
-          perm[m] = perm[j];
-          perm[j] = x;
-        }
-#pragma unroll
-        for (int m = 0; m < g; ++m) {
-          if (side == 0) sig[r][m] = perm[m];
-          else del[r][m] = perm[m];
-        }
+      for (int m = 0; m < g; ++m) {
+        sig[r][m] = (ps >> (2 * m)) & 3;
+        del[r][m] = (pd >> (2 * m)) & 3;
       }
     }
   }
@@ -521,6 +503,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   // D^rem entry each source rank's lane changed last, and its new value: the
   // next credit gather takes it from here, so no barrier has to wait for the
   // global store (stores of earlier iterations are complete by then).
+  uint8_t* rp = smem + P.o_rp;   // [FC][NS][G][2] packed permutations of the shuffled starts
   int32_t* lastj = (int32_t*)(smem + P.o_lastj);
   int64_t* lastv = (int64_t*)(smem + P.o_lastv);
   const int32_t* cat = P.cat;
@@ -818,13 +801,45 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
             ++c;
           }
         }
+        // the shuffled starts' permutations (Fisher-Yates on SplitMix64
+        // streams keyed by seed, iteration, family, start, group and side),
+        // taken from the highest thread down so that they mostly run on
+        // waves the gather leaves idle
+        const int nitems = nc * (NS - 1) * L.G * 2;
+        for (int y = kPlanThreads - 1 - tid; y < nitems; y += kPlanThreads) {
+          const int side = y & 1, z = y >> 1;
+          const int a = z % L.G, cs = z / L.G;
+          const int cc = cs / (NS - 1), st = 1 + (cs - cc * (NS - 1));
+          uint64_t k3 = P.seed;
+          k3 = sm_mix(k3 + kGolden) ^ (uint64_t)K;
+          k3 = sm_mix(k3 + kGolden) ^ (uint64_t)(cb + cc);
+          k3 = sm_mix(k3 + kGolden) ^ (uint64_t)st;
+          const uint64_t k4 = sm_mix(k3 + kGolden) ^ (uint64_t)a;
+          uint64_t state = sm_mix(k4 + kGolden) ^ (uint64_t)side;
+          int perm[g];
+#pragma unroll
+          for (int m = 0; m < g; ++m) perm[m] = m;
+#pragma unroll
+          for (int m = g - 1; m >= 1; --m) {
+            state += kGolden;
+            const int j = (int)(sm_mix(state) % (uint64_t)(m + 1));
+            const int x2 = perm[m];
+            perm[m] = perm[j];
+            perm[j] = x2;
+          }
+          int packed = 0;
+#pragma unroll
+          for (int m = 0; m < g; ++m) packed |= perm[m] << (2 * m);
+          rp[((size_t)(cc * NS + st) * L.G + a) * 2 + side] = (uint8_t)packed;
+        }
       }
       lds_barrier();
       for (int pi = wave; pi < nc * NS; pi += kWaves) {
         const int c = pi / NS, s = pi - c * NS;
         FamCtx fc{outT + (size_t)c * N, inT + (size_t)c * N, ipos + (size_t)c * N, ocls + (size_t)c * N,
                   hp + (size_t)c * N * g2, cb + c};
-        run_pair<g, MG>(P, fc, sl + (size_t)pi * N, dl + (size_t)pi * N, s, K, lane, topkey[c], &pr[pi]);
+        run_pair<g, MG>(P, fc, sl + (size_t)pi * N, dl + (size_t)pi * N, s, rp + (size_t)pi * L.G * 2, lane,
+                        topkey[c], &pr[pi]);
       }
       // full barrier: the previous iteration's D^rem stores are complete
       // before the next gather reads D^rem
@@ -1087,7 +1102,8 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_lastv, (size_t)N * 8);
   const size_t fixed = o;
   const size_t per_fam = align_up((size_t)NS * sizeof(PairRes), 16) + 2 * align_up((size_t)N * 2, 16) +
-                         2 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16) + 16;
+                         2 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16) + 16 +
+                         align_up((size_t)NS * L.G * 2, 16);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return set_error(VP_ERR_HIP, "hipGetDevice failed");
   int lds_max = 0;
@@ -1108,6 +1124,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_sl, (size_t)FC * NS * N);
   take(&P.o_dl, (size_t)FC * NS * N);
   take(&P.o_top, (size_t)FC * 8);
+  take(&P.o_rp, (size_t)FC * NS * L.G * 2);
   if (o > budget) return set_error(VP_ERR_UNSUPPORTED, "plan state does not fit in LDS");
 
   hipStream_t st = (hipStream_t)stream;
