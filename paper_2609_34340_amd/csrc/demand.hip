@@ -6,13 +6,14 @@
 // Kernels
 //   hist_rows     one block per source rank; LDS-privatised histogram of its
 //                 T*k expert ids, then the rank's demand row.
-//   sort_count    one wavefront per chunk of the sorted rank's ids: per-chunk
-//                 expert counts, written expert-major.
-//   sort_scan     one block: exclusive scan of the expert-major counts, the
-//                 destination offsets.
-//   sort_scatter  one wavefront per chunk: stable within-chunk rank of every
-//                 id from a wave-wide match mask built with one ballot per
-//                 bit of the expert id, plus a prefix popcount.
+//   sort_count    one block per 1024-id chunk of the sorted rank's ids:
+//                 per-chunk expert counts, written expert-major.
+//   sort_scan     one block: exclusive scan of the expert-major counts (one
+//                 contiguous segment per thread), the destination offsets.
+//   sort_scatter  one block per chunk: every id's stable rank inside its
+//                 wave's 256 ids from a wave-wide match mask built with one
+//                 ballot per bit of the expert id plus a prefix popcount,
+//                 then the waves' counts scanned per expert.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -20,8 +21,9 @@
 namespace vp {
 namespace {
 
-constexpr int kChunk = 2048;          // ids per wavefront chunk of the counting sort
-constexpr int kSortWaves = 4;         // wavefronts per block in sort_count / sort_scatter
+constexpr int kSortThreads = 256;     // threads per block of the counting sort
+constexpr int kPerThread = 4;         // ids per thread
+constexpr int kChunk = kSortThreads * kPerThread;   // ids per block
 
 __device__ inline void report(int32_t* status, int code) { atomicCAS(status, 0, code); }
 
@@ -68,97 +70,135 @@ __global__ void __launch_bounds__(1024) hist_rows(const int32_t* __restrict__ ro
   }
 }
 
-// per-chunk expert counts, layout ccount[e * n_chunks + chunk]
-__global__ void __launch_bounds__(64 * kSortWaves) sort_count(const int32_t* __restrict__ ids, int64_t Tk,
-                                                              int32_t E, int32_t n_chunks,
-                                                              int32_t* __restrict__ ccount) {
-  extern __shared__ int32_t whist[];   // kSortWaves * E
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int chunk = blockIdx.x * kSortWaves + w;
-  int32_t* h = whist + w * E;
-  for (int e = lane; e < E; e += 64) h[e] = 0;
-  wave_sync();
-  if (chunk < n_chunks) {
-    const int64_t b = (int64_t)chunk * kChunk, end = min(Tk, b + kChunk);
-    for (int64_t x = b + lane; x < end; x += 64) {
-      int e = ids[x];
-      if ((unsigned)e < (unsigned)E) atomicAdd(&h[e], 1);
-    }
-    wave_sync();
-    for (int e = lane; e < E; e += 64) ccount[(size_t)e * n_chunks + chunk] = h[e];
+// Counting sort of one rank's ids, chunks of kChunk ids, one block per
+// chunk.  Counts are laid out ccount[e * n_chunks + chunk].
+__global__ void __launch_bounds__(kSortThreads) sort_count(const int32_t* __restrict__ ids, int64_t Tk,
+                                                          int32_t E, int32_t n_chunks,
+                                                          int32_t* __restrict__ ccount) {
+  extern __shared__ int32_t h[];   // E
+  const int tid = threadIdx.x, chunk = blockIdx.x;
+  for (int e = tid; e < E; e += kSortThreads) h[e] = 0;
+  __syncthreads();
+  const int64_t b = (int64_t)chunk * kChunk;
+  int ev[kPerThread];
+#pragma unroll
+  for (int m = 0; m < kPerThread; ++m) {
+    const int64_t x = b + tid + m * kSortThreads;
+    ev[m] = x < Tk ? ids[x] : -1;
   }
+#pragma unroll
+  for (int m = 0; m < kPerThread; ++m)
+    if ((unsigned)ev[m] < (unsigned)E) atomicAdd(&h[ev[m]], 1);
+  __syncthreads();
+  for (int e = tid; e < E; e += kSortThreads) ccount[(size_t)e * n_chunks + chunk] = h[e];
 }
 
-// exclusive scan over E * n_chunks counts (expert-major) in one block
+// Exclusive scan of the E * n_chunks counts (expert-major) in one block:
+// tiles of 4096 counts, each thread a coalesced run of four, up to eight
+// tiles loaded ahead.  Counts and offsets fit 32 bits (at most T*k).
 __global__ void __launch_bounds__(1024) sort_scan(int32_t* __restrict__ ccount, int64_t total, int32_t E,
                                                   int32_t N, int32_t n_chunks, int64_t* __restrict__ dest_off) {
-  __shared__ int64_t wsum[16];
-  __shared__ int64_t carry;
+  constexpr int V = 4, TB = 8;
+  __shared__ int32_t wsum[16];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  if (tid == 0) carry = 0;
-  __syncthreads();
-  const int eloc = E / N;
-  for (int64_t b = 0; b < total; b += 1024) {
-    const int64_t x = b + tid;
-    int64_t v = x < total ? ccount[x] : 0;
-    // inclusive wave scan
-    int64_t s = v;
-    for (int o = 1; o < 64; o <<= 1) {
-      int64_t y = __shfl_up(s, o);
-      if (lane >= o) s += y;
-    }
-    if (lane == 63) wsum[w] = s;
-    __syncthreads();
-    int64_t before = carry;
-    for (int k = 0; k < w; ++k) before += wsum[k];
-    const int64_t excl = before + s - v;
-    if (x < total) {
-      ccount[x] = (int32_t)excl;
-      // the first chunk of expert j*eloc opens destination j
-      if (x % n_chunks == 0) {
-        const int64_t e = x / n_chunks;
-        if (e % eloc == 0) dest_off[e / eloc] = excl;
+  int32_t carry = 0;
+  const bool vec = (((uintptr_t)ccount) & 15) == 0;
+  for (int64_t b0 = 0; b0 < total; b0 += (int64_t)1024 * V * TB) {
+    int32_t v[TB][V];
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      const int64_t x = b0 + ((int64_t)tb * 1024 + tid) * V;
+      if (vec && x + V <= total) {
+        const int4 q = *(const int4*)(ccount + x);
+        v[tb][0] = q.x; v[tb][1] = q.y; v[tb][2] = q.z; v[tb][3] = q.w;
+      } else {
+#pragma unroll
+        for (int m = 0; m < V; ++m) v[tb][m] = x + m < total ? ccount[x + m] : 0;
       }
     }
-    __syncthreads();
-    if (tid == 1023) carry = excl + v;
-    __syncthreads();
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) {
+      const int64_t x = b0 + ((int64_t)tb * 1024 + tid) * V;
+      if (b0 + (int64_t)tb * 1024 * V >= total) break;   // uniform
+      const int32_t mine = v[tb][0] + v[tb][1] + v[tb][2] + v[tb][3];
+      int32_t s = mine;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int32_t y = __shfl_up(s, o);
+        if (lane >= o) s += y;
+      }
+      if (lane == 63) wsum[w] = s;
+      __syncthreads();
+      int32_t run = carry + s - mine, all = 0;
+      for (int u = 0; u < 16; ++u) {
+        if (u < w) run += wsum[u];
+        all += wsum[u];
+      }
+#pragma unroll
+      for (int m = 0; m < V; ++m) {
+        if (x + m < total) ccount[x + m] = run;
+        run += v[tb][m];
+      }
+      carry += all;
+      __syncthreads();
+    }
   }
+  __syncthreads();
+  // destination j opens at the first chunk of expert j*eloc
+  const int eloc = E / N;
+  for (int j = tid; j < N; j += 1024) dest_off[j] = ccount[(size_t)j * eloc * n_chunks];
   if (tid == 0) dest_off[N] = carry;
 }
 
-__global__ void __launch_bounds__(64 * kSortWaves) sort_scatter(const int32_t* __restrict__ ids, int64_t Tk,
-                                                                int32_t k, int32_t E, int32_t n_chunks,
-                                                                int32_t bits, const int32_t* __restrict__ coff,
-                                                                int32_t* __restrict__ sorted_tok) {
-  extern __shared__ int32_t run[];    // kSortWaves * E running positions
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int chunk = blockIdx.x * kSortWaves + w;
-  if (chunk >= n_chunks) return;
-  int32_t* pos = run + w * E;
-  for (int e = lane; e < E; e += 64) pos[e] = coff[(size_t)e * n_chunks + chunk];
+// Stable scatter of one chunk: wave v ranks the ids [v*64*kPerThread, ...)
+// of the chunk with one ballot per id bit (a match mask) and a prefix
+// popcount; the waves' counts are then scanned per expert.
+__global__ void __launch_bounds__(kSortThreads) sort_scatter(const int32_t* __restrict__ ids, int64_t Tk,
+                                                            int32_t k, int32_t E, int32_t n_chunks,
+                                                            int32_t bits, const int32_t* __restrict__ coff,
+                                                            int32_t* __restrict__ sorted_tok) {
+  extern __shared__ int32_t wc[];    // [kSortThreads / 64][E]
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, chunk = blockIdx.x;
+  constexpr int kW = kSortThreads / 64;
+  const int64_t base = (int64_t)chunk * kChunk + (int64_t)w * 64 * kPerThread;
+  int ev[kPerThread];
+#pragma unroll
+  for (int m = 0; m < kPerThread; ++m) {
+    const int64_t x = base + m * 64 + lane;
+    ev[m] = x < Tk ? ids[x] : -1;
+  }
+  int32_t* mine = wc + w * E;
+  for (int e = lane; e < E; e += 64) mine[e] = 0;
   wave_sync();
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  const int64_t b = (int64_t)chunk * kChunk, end = min(Tk, b + kChunk);
-  for (int64_t x0 = b; x0 < end; x0 += 64) {
-    const int64_t x = x0 + lane;
-    const bool live = x < end;
-    int e = live ? ids[x] : -1;
-    const bool ok = live && (unsigned)e < (unsigned)E;
-    // lanes holding the same expert id: AND of one ballot per id bit
+  int rk[kPerThread];
+#pragma unroll
+  for (int m = 0; m < kPerThread; ++m) {
+    const int e = ev[m];
+    const bool ok = (unsigned)e < (unsigned)E;
     uint64_t same = __ballot(ok);
     for (int bt = 0; bt < bits; ++bt) {
       const uint64_t ones = __ballot(ok && ((e >> bt) & 1));
       same &= ((e >> bt) & 1) ? ones : ~ones;
     }
-    int p = 0;
-    if (ok) p = pos[e] + __popcll(same & lt);
+    rk[m] = ok ? mine[e] + __popcll(same & lt) : 0;
     wave_sync();
-    if (ok) {
-      sorted_tok[p] = (int32_t)(x / k);
-      if ((same & lt) == 0) pos[e] += __popcll(same);   // lowest lane of the group advances
+    if (ok && (same & lt) == 0) mine[e] += __popcll(same);   // lowest lane of the group advances
+    wave_sync();
+  }
+  __syncthreads();
+  for (int e = tid; e < E; e += kSortThreads) {
+    int32_t acc = coff[(size_t)e * n_chunks + chunk];
+    for (int v = 0; v < kW; ++v) {
+      const int32_t c = wc[v * E + e];
+      wc[v * E + e] = acc;
+      acc += c;
     }
-    wave_sync();
+  }
+  __syncthreads();
+#pragma unroll
+  for (int m = 0; m < kPerThread; ++m) {
+    const int e = ev[m];
+    if ((unsigned)e < (unsigned)E) sorted_tok[mine[e] + rk[m]] = (int32_t)((base + m * 64 + lane) / k);
   }
 }
 
@@ -192,15 +232,14 @@ vp_status launch_demand(const DemandLaunch& a, void* stream) {
   const int32_t* ids = a.routing + (size_t)a.sort_row * Tk;
   const int nch = std::max(1, n_chunks_of(Tk));
   int32_t* ccount = (int32_t*)a.ws;
-  const int blocks = (nch + kSortWaves - 1) / kSortWaves;
-  const size_t lds = (size_t)kSortWaves * a.E * sizeof(int32_t);
-  hipLaunchKernelGGL(sort_count, dim3(blocks), dim3(64 * kSortWaves), lds, s, ids, Tk, a.E, nch, ccount);
+  hipLaunchKernelGGL(sort_count, dim3(nch), dim3(kSortThreads), (size_t)a.E * sizeof(int32_t), s, ids, Tk, a.E,
+                     nch, ccount);
   hipLaunchKernelGGL(sort_scan, dim3(1), dim3(1024), 0, s, ccount, (int64_t)a.E * nch, a.E, a.N, nch,
                      a.dest_off);
   int bits = 0;
   while ((1 << bits) < a.E) ++bits;
-  hipLaunchKernelGGL(sort_scatter, dim3(blocks), dim3(64 * kSortWaves), lds, s, ids, Tk, a.k, a.E, nch, bits,
-                     ccount, a.sorted_tok);
+  hipLaunchKernelGGL(sort_scatter, dim3(nch), dim3(kSortThreads), (size_t)(kSortThreads / 64) * a.E * sizeof(int32_t),
+                     s, ids, Tk, a.k, a.E, nch, bits, ccount, a.sorted_tok);
   if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "sort launch failed");
   return VP_OK;
 }
