@@ -17,8 +17,8 @@
 //            list.  Heads: the source byte offset of every packed unit.
 //   scatter  rows: one workgroup per (token, copy), XCD-aware so that all
 //            copies of a token run on one XCD: a source row leaves HBM once
-//            however many destinations it has, and each copy is stored in
-//            one sweep of the workgroup.
+//            however many destinations it has, and the XCDs write
+//            neighbouring tokens at any moment.
 //   gather   heads: grid-stride 16-byte copy of the units (each is read
 //            once) with non-temporal stores.
 #include <hip/hip_runtime.h>
@@ -281,26 +281,24 @@ __global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
   }
 }
 
-constexpr int kScatterMaxThreads = 1024;
+constexpr int kScatterMaxThreads = 512;
 
-// Rows: one workgroup per (token, copy slot) with as many lanes as the row
-// has 16-byte vectors (up to 1024), so each copy is stored in one sweep.
-// Workgroups are handed to the eight XCDs round-robin; the mapping below
-// gives each XCD a contiguous run of (token, slot) pairs, so the copies of a
-// token are read on one XCD back to back and every row leaves HBM once
-// (the repeats hit that XCD's L2).
+// Rows: one workgroup per (token, copy slot).  Workgroups are handed to the
+// eight XCDs round-robin; the mapping below gives XCD x the tokens t with
+// t % 8 == x, all copy slots of a token back to back, so a token's copies
+// are read on one XCD in a row (the row leaves HBM once, the repeats hit
+// that XCD's L2) while the eight XCDs work on neighbouring tokens, whose
+// copies land next to each other in every destination's stream.
 __global__ void __launch_bounds__(kScatterMaxThreads) scatter_rows_kernel(
     const unsigned char* __restrict__ src, const int32_t* __restrict__ tcnt, const int32_t* __restrict__ lst,
     int64_t T, int k, int64_t unit, int64_t vpu, unsigned char* __restrict__ send, const int32_t* status) {
   if (*status != 0) return;
-  const int64_t Q = T * k, per = (Q + 7) / 8;
-  const int64_t q = (int64_t)(blockIdx.x & 7) * per + (blockIdx.x >> 3);
-  if (q >= Q) return;
-  const int64_t t = q / k;
-  const int c = (int)(q - t * k);
-  if (c >= tcnt[t]) return;
+  const int64_t idx = blockIdx.x >> 3;
+  const int64_t t = (idx / k) * 8 + (blockIdx.x & 7);
+  const int c = (int)(idx % k);
+  if (t >= T || c >= tcnt[t]) return;
   const u32x4* row = (const u32x4*)(src + t * unit);
-  u32x4* d = (u32x4*)(send + (int64_t)lst[q] * unit);
+  u32x4* d = (u32x4*)(send + (int64_t)lst[t * k + c] * unit);
   for (int64_t i = threadIdx.x; i < vpu; i += blockDim.x) __builtin_nontemporal_store(row[i], d + i);
 }
 
@@ -388,11 +386,10 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
   }
   const int64_t vpu = a.unit / 16;
   if (a.mode == 0) {
-    const int64_t pairs = a.T * a.k;
-    if (pairs > 0) {
-      if (pairs + 8 > ((int64_t)1 << 31)) return set_error(VP_ERR_UNSUPPORTED, "too many token copies");
+    const int64_t blocks = (a.T + 7) / 8 * 8 * a.k;
+    if (blocks > 0) {
+      if (blocks >= ((int64_t)1 << 31)) return set_error(VP_ERR_UNSUPPORTED, "too many token copies");
       const int threads = (int)std::min<int64_t>(kScatterMaxThreads, (vpu + 63) / 64 * 64);
-      const int64_t blocks = (pairs + 7) / 8 * 8;
       hipLaunchKernelGGL(scatter_rows_kernel, dim3((unsigned)blocks), dim3(threads), 0, s,
                          (const unsigned char*)a.src, tcnt, lst, a.T, a.k, a.unit, vpu, (unsigned char*)a.send,
                          a.status);
