@@ -141,14 +141,16 @@ size_t vp_demand_workspace(int64_t T, int32_t k, int32_t E);
  * and for row `sort_row` (0 <= sort_row < R, or -1 for none):
  *   sorted_tok device int32 [T*k]      token ids of that row's assignments in
  *                                      (expert, token) order (stable)
+ *   sorted_slot device uint8 [T*k]     the routing slot (0..k-1) of each of
+ *                                      those assignments; may be NULL
  *   dest_off   device int64 [N+1]      first position of each destination
  *                                      rank's rows in sorted_tok
- * E must be a positive multiple of N, E <= 4096, T*k < 2^31.  An expert id
- * outside [0, E) sets VP_ERR_INVALID_ARGUMENT in dev_status. */
+ * E must be a positive multiple of N, E <= 4096, k <= 255, T*k < 2^31.  An
+ * expert id outside [0, E) sets VP_ERR_INVALID_ARGUMENT in dev_status. */
 vp_status vp_demand(const int32_t* routing, int32_t R, int64_t T, int32_t k, int32_t E,
                     int32_t n_ranks, int32_t first_rank, int32_t sort_row, int64_t unit_bytes,
-                    int32_t* counts, int64_t* demand, int32_t* sorted_tok, int64_t* dest_off,
-                    int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
+                    int32_t* counts, int64_t* demand, int32_t* sorted_tok, uint8_t* sorted_slot,
+                    int64_t* dest_off, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
 
 /* Ulysses head/context re-layout demand (Sec. 6.2 sequence parallelism):
  * rank j owns heads [head_lo[j], head_lo[j+1]) (device int64 [N+1]); each of
@@ -175,6 +177,11 @@ size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
  *   dst     device int32 [k_max, N]  pi_k(i) for source rank i
  *   inst    device int32 [k_max, N]  node-local instance id of lane i
  *   bytes   device int64 [k_max, N]  x_{k,i} of Eq. (9) (zero lanes kept)
+ *   send_off, stream_off  device int64 [k_max, N], both NULL or both given:
+ *           the buffer layout of Sec. 5 for every rank i: bytes i sent in the
+ *           steps before k (where step k's slice starts in i's send buffer),
+ *           and bytes i sent to pi_k(i) before step k (where the slice starts
+ *           in i's stream to that destination)
  *   tau     device int64 [1]     the quantum used (ns), may be NULL
  * Each iteration scores every catalog shape (Eq. (5)-(6)), binds every family
  * of the best shape with MultiStartAA (Eq. (7)-(8)), evaluates Eq. (9)-(10)
@@ -184,16 +191,19 @@ size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
  * demand reaches 2^42 bytes.  The catalog must have been uploaded. */
 vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_params* p,
                   int32_t* K, int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes,
-                  int64_t* tau, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
+                  int64_t* send_off, int64_t* stream_off, int64_t* tau, int32_t* dev_status, void* ws,
+                  size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------- pack */
 
 /* Workspace bytes for vp_pack_rows (k = the routing's top-k, T tokens) or
  * vp_pack_heads (k = 0) with schedule capacity k_max, a send buffer of
  * send_capacity bytes and a pack unit of unit_bytes (row_bytes or
- * head_bytes).  Rows: per-step stream offsets, a copy counter per token and
- * up to k send-unit indices per token.  Heads: per-step stream offsets and
- * one source offset per packed unit.  Returns 0 for negative sizes. */
+ * head_bytes).  Rows: per-step descriptors and one send-unit entry per
+ * (token, routing slot).  Heads: per-step descriptors and one source offset
+ * per packed unit.  The workspace must be zero-filled once before its first
+ * use; no later call needs it cleared (rows: the entries carry the
+ * generation of the call that wrote them).  Returns 0 for negative sizes. */
 size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_bytes, int64_t T, int32_t k);
 
 /* Send-buffer layout (Sec. 5 "Device-resident buffer layout"): for the steps
@@ -203,55 +213,63 @@ size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_byte
  *   tokens     device [T, row_bytes]   token rows (bf16 or any bytes)
  *   k                                  top-k of the routing (a token may
  *                                      have at most k copies)
- *   sorted_tok device int32 [T*k]      from vp_demand
+ *   sorted_tok, sorted_slot            from vp_demand ([T*k] each)
  *   dest_off   device int64 [N+1]      from vp_demand (row units)
  *   K, dst, bytes                      the schedule of vp_plan (device)
+ *   send_off, stream_off               vp_plan's buffer layout (device), or
+ *                                      both NULL: then a slice kernel derives
+ *                                      the same offsets from the schedule
  *   send       device [send_capacity]  output
  *   step_off   device int64 [k_max+1]  where step k's slice starts in send;
  *                                      entries past K are unspecified,
  *                                      step_off[K] = total bytes
  * row_bytes must be a multiple of 16 and send_capacity / row_bytes below
- * 2^31.  Each token row is read from HBM once and stored to all its copies.
- * Slices that are not whole rows or run past their stream, a token id out of
- * range or listed more than k times, or a total above send_capacity set
- * VP_ERR_INVALID_ARGUMENT or VP_ERR_CAPACITY in dev_status and write nothing
- * to send. */
+ * 2^31; without the planner's layout, k_max is bounded by the slice
+ * kernel's LDS table (VP_ERR_UNSUPPORTED).  Each token row is read from HBM
+ * once and stored to all its copies.  Slices that are not whole rows or run
+ * past their stream, a token id or slot out of range, or a total above
+ * send_capacity set VP_ERR_INVALID_ARGUMENT or VP_ERR_CAPACITY in dev_status
+ * and write nothing to send.  Calls that share a workspace must not
+ * overlap. */
 vp_status vp_pack_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes, const int32_t* sorted_tok,
-                       const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
-                       const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
-                       void* send, int64_t send_capacity, int64_t* step_off, int32_t* dev_status,
-                       void* ws, size_t ws_bytes, void* stream);
+                       const uint8_t* sorted_slot, const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
+                       const int32_t* K, const int32_t* dst, const int64_t* bytes, const int64_t* send_off,
+                       const int64_t* stream_off, int32_t k_max, void* send, int64_t send_capacity,
+                       int64_t* step_off, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
 
 /* Ulysses variant: stream j is, token by token, the bytes of the heads rank j
  * owns, [head_lo[j], head_lo[j+1]) (device int64 [N+1]); units are single
  * heads of head_bytes (a multiple of 16); activations are [T, token_stride]. */
 vp_status vp_pack_heads(const void* act, int64_t T, int64_t token_stride, const int64_t* head_lo,
                         int64_t head_bytes, int32_t self_rank, int32_t n_ranks, const int32_t* K,
-                        const int32_t* dst, const int64_t* bytes, int32_t k_max, void* send,
-                        int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
-                        size_t ws_bytes, void* stream);
+                        const int32_t* dst, const int64_t* bytes, const int64_t* send_off,
+                        const int64_t* stream_off, int32_t k_max, void* send, int64_t send_capacity,
+                        int64_t* step_off, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
 
 /* The two halves of vp_pack_rows / vp_pack_heads, for callers that schedule
  * or time the copy on its own.  vp_pack_prepare_* take the same arguments
- * minus `send` and run the slice and index kernels: they fill step_off and
- * the workspace (per-step stream offsets, then the copy lists of every token
- * or the source offset of every unit) and check every slice and the
+ * minus `send` and run the slice (without the planner's layout) and index
+ * kernels: they fill step_off and the workspace (the copy lists of every
+ * token or the source offset of every unit) and check every slice and the
  * capacity.  vp_pack_gather then copies the units from `src` (the tokens or
  * activations given to the prepare call) into `send` with 16-byte loads and
  * non-temporal stores; it must get the same unit_bytes, T, k (0 after
- * vp_pack_prepare_heads), k_max, send_capacity and workspace.  It writes
- * nothing when dev_status already holds an error. */
+ * vp_pack_prepare_heads), k_max, send_capacity and workspace, and no other
+ * prepare on that workspace may come between.  It writes nothing when
+ * dev_status already holds an error. */
 vp_status vp_pack_prepare_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes,
-                               const int32_t* sorted_tok,
+                               const int32_t* sorted_tok, const uint8_t* sorted_slot,
                                const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
-                               const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
+                               const int32_t* K, const int32_t* dst, const int64_t* bytes,
+                               const int64_t* send_off, const int64_t* stream_off, int32_t k_max,
                                int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
                                size_t ws_bytes, void* stream);
 vp_status vp_pack_prepare_heads(const void* act, int64_t T, int64_t token_stride, const int64_t* head_lo,
                                 int64_t head_bytes, int32_t self_rank, int32_t n_ranks, const int32_t* K,
-                                const int32_t* dst, const int64_t* bytes, int32_t k_max,
-                                int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
-                                size_t ws_bytes, void* stream);
+                                const int32_t* dst, const int64_t* bytes, const int64_t* send_off,
+                                const int64_t* stream_off, int32_t k_max, int64_t send_capacity,
+                                int64_t* step_off, int32_t* dev_status, void* ws, size_t ws_bytes,
+                                void* stream);
 vp_status vp_pack_gather(const void* src, int64_t unit_bytes, int64_t T, int32_t k, const int32_t* K,
                          const int64_t* step_off, int32_t k_max, void* send, int64_t send_capacity,
                          int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);

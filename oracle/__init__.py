@@ -66,7 +66,7 @@ def lib():
         L.orc_catalog_families.argtypes = [vp, vp, vp, vp]
         L.orc_catalog_cluster_family.argtypes = [vp, C.c_int32, vp, vp, vp, vp]
         L.orc_demand.argtypes = [vp, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
-                                 C.c_int64, vp, vp, vp, vp]
+                                 C.c_int64, vp, vp, vp, vp, vp]
         L.orc_demand_heads.argtypes = [C.c_int64, vp, C.c_int64, C.c_int32, C.c_int32, vp]
         L.orc_plan.argtypes = [vp, vp, C.POINTER(_Params), C.c_int32, vp, vp, vp, vp, vp, vp,
                                vp, C.c_int64, vp]
@@ -207,18 +207,20 @@ def utility_greater(S1, x1, b1, S2, x2, b2, lambda_ns) -> bool:
 
 
 def demand(routing: np.ndarray, n_ranks: int, n_experts: int, self_rank: int, unit: int):
-    """One source rank's demand row, expert counts, (expert, token) order and offsets."""
+    """One source rank's demand row, expert counts, (expert, token) order (the
+    token and routing slot of every assignment) and offsets."""
     r = np.ascontiguousarray(routing, dtype=np.int32)
     T, k = r.shape
     row = np.zeros(n_ranks, np.int64)
     counts = np.zeros(n_experts, np.int32)
     order = np.zeros(T * k, np.int32)
+    slot = np.zeros(T * k, np.uint8)
     off = np.zeros(n_ranks + 1, np.int64)
     st = lib().orc_demand(_p(r), T, k, n_experts, n_ranks, self_rank, unit, _p(row), _p(counts),
-                          _p(order), _p(off))
+                          _p(order), _p(slot), _p(off))
     if st != OK:
         raise OracleError(st, "orc_demand")
-    return dict(row=row, counts=counts, sorted_tok=order, dest_off=off)
+    return dict(row=row, counts=counts, sorted_tok=order, sorted_slot=slot, dest_off=off)
 
 
 def demand_heads(tokens: int, head_lo: np.ndarray, head_bytes: int, self_rank: int):

@@ -911,11 +911,11 @@ int orc_catalog_cluster_family(const orc_catalog* c, int32_t f, int32_t* cls, in
 // Demand row of one source rank (Sec. 3 model setup; Sec. 5 sparse EP):
 // counts[e] = #{(t, e)}; D_self,j = unit * sum of counts of the experts that
 // rank j hosts (experts are contiguous per rank), D_self,self = 0.  Also the
-// stable (expert, token) order of the assignments and each destination's
-// first row in it.
+// stable (expert, token) order of the assignments (token and routing slot of
+// each) and each destination's first row in it.
 int orc_demand(const int32_t* routing, int64_t T, int32_t k, int32_t E, int32_t N,
                int32_t self, int64_t unit, int64_t* row, int32_t* counts, int32_t* sorted_tok,
-               int64_t* dest_off) {
+               uint8_t* sorted_slot, int64_t* dest_off) {
   if (N < 1 || E < N || E % N != 0 || self < 0 || self >= N || unit < 1) return INVALID_ARGUMENT;
   const int eloc = E / N;
   for (int e = 0; e < E; ++e) counts[e] = 0;
@@ -933,8 +933,11 @@ int orc_demand(const int32_t* routing, int64_t T, int32_t k, int32_t E, int32_t 
   std::vector<int64_t> start(E + 1, 0);
   for (int e = 0; e < E; ++e) start[e + 1] = start[e] + counts[e];
   std::vector<int64_t> fill(start.begin(), start.end() - 1);
+  // each entry is one (token, slot) assignment: its token, and which of the
+  // token's k routing slots it is
   for (int64_t x = 0; x < T * k; ++x) {
     int e = routing[x];
+    if (sorted_slot) sorted_slot[fill[e]] = (uint8_t)(x % k);
     sorted_tok[fill[e]++] = (int32_t)(x / k);
   }
   for (int j = 0; j <= N; ++j) dest_off[j] = start[(size_t)j * eloc];

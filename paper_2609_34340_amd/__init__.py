@@ -65,21 +65,23 @@ def lib():
     L.vp_catalog_free.restype = None
     L.vp_demand_workspace.argtypes = [i64, i32, i32]
     L.vp_demand_workspace.restype = sz
-    L.vp_demand.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, i64, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.vp_demand.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.vp_demand_heads.argtypes = [i64, vp, i64, i32, i32, i32, vp, vp, vp]
     L.vp_plan_params_default.argtypes = [i32, i64, C.POINTER(PlanParams)]
     L.vp_plan_params_default.restype = None
     L.vp_plan_workspace.argtypes = [vp, C.POINTER(PlanParams)]
     L.vp_plan_workspace.restype = sz
-    L.vp_plan.argtypes = [vp, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.vp_plan.argtypes = [vp, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.vp_pack_workspace.argtypes = [i32, i64, i64, i64, i32]
     L.vp_pack_workspace.restype = sz
-    L.vp_pack_rows.argtypes = [vp, i64, i32, i64, vp, vp, i32, i32, vp, vp, vp, i32, vp, i64, vp, vp, vp, sz, vp]
-    L.vp_pack_heads.argtypes = [vp, i64, i64, vp, i64, i32, i32, vp, vp, vp, i32, vp, i64, vp, vp, vp, sz, vp]
-    L.vp_pack_prepare_rows.argtypes = [vp, i64, i32, i64, vp, vp, i32, i32, vp, vp, vp, i32, i64, vp, vp, vp, sz,
-                                       vp]
-    L.vp_pack_prepare_heads.argtypes = [vp, i64, i64, vp, i64, i32, i32, vp, vp, vp, i32, i64, vp, vp, vp, sz,
-                                        vp]
+    L.vp_pack_rows.argtypes = [vp, i64, i32, i64, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, i64, vp, vp,
+                               vp, sz, vp]
+    L.vp_pack_heads.argtypes = [vp, i64, i64, vp, i64, i32, i32, vp, vp, vp, vp, vp, i32, vp, i64, vp, vp, vp,
+                                sz, vp]
+    L.vp_pack_prepare_rows.argtypes = [vp, i64, i32, i64, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, i64, vp,
+                                       vp, vp, sz, vp]
+    L.vp_pack_prepare_heads.argtypes = [vp, i64, i64, vp, i64, i32, i32, vp, vp, vp, vp, vp, i32, i64, vp, vp,
+                                        vp, sz, vp]
     L.vp_pack_gather.argtypes = [vp, i64, i64, i32, vp, vp, i32, vp, i64, vp, vp, sz, vp]
     L.vp_modeled_time.argtypes = [vp, i32, vp, vp, i64, vp, vp]
     L.vp_status_string.argtypes = [C.c_int]
@@ -208,7 +210,8 @@ def demand(routing: torch.Tensor, n_ranks: int, n_experts: int, unit: int, first
            sort_row: int = 0, status: Optional[torch.Tensor] = None, out: Optional[dict] = None,
            ws: Optional[torch.Tensor] = None, stream=None) -> dict:
     """vp_demand over routing [R, T, k] (int32, GPU).  Returns counts, demand rows,
-    and for row `sort_row` the (expert, token) order and destination offsets."""
+    and for row `sort_row` the (expert, token) order (token and routing slot of
+    each assignment) and destination offsets."""
     _dev(routing, torch.int32, "routing")
     R, T, k = routing.shape
     dev = routing.device
@@ -216,6 +219,7 @@ def demand(routing: torch.Tensor, n_ranks: int, n_experts: int, unit: int, first
         out = dict(counts=torch.empty((R, n_experts), dtype=torch.int32, device=dev),
                    demand=torch.empty((R, n_ranks), dtype=torch.int64, device=dev),
                    sorted_tok=torch.empty(max(T * k, 1), dtype=torch.int32, device=dev),
+                   sorted_slot=torch.empty(max(T * k, 1), dtype=torch.uint8, device=dev),
                    dest_off=torch.empty(n_ranks + 1, dtype=torch.int64, device=dev))
     if status is None:
         status = new_status(dev)
@@ -224,8 +228,8 @@ def demand(routing: torch.Tensor, n_ranks: int, n_experts: int, unit: int, first
         ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
     _check(lib().vp_demand(_ptr(routing), R, T, k, n_experts, n_ranks, first_rank, sort_row, unit,
                            _ptr(out["counts"]), _ptr(out["demand"]), _ptr(out["sorted_tok"]),
-                           _ptr(out["dest_off"]), _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
-           "vp_demand")
+                           _ptr(out.get("sorted_slot")), _ptr(out["dest_off"]), _ptr(status), _ptr(ws),
+                           ws.numel(), _stream(stream)), "vp_demand")
     out["status"] = status
     return out
 
@@ -250,13 +254,19 @@ def plan_workspace_bytes(cat: Catalog, p: PlanParams) -> int:
     return int(lib().vp_plan_workspace(cat.handle, C.byref(p)))
 
 
-def alloc_schedule(N: int, k_max: int, device="cuda") -> dict:
-    return dict(K=torch.zeros(1, dtype=torch.int32, device=device),
-                family=torch.empty(k_max, dtype=torch.int32, device=device),
-                dst=torch.empty((k_max, N), dtype=torch.int32, device=device),
-                inst=torch.empty((k_max, N), dtype=torch.int32, device=device),
-                bytes=torch.empty((k_max, N), dtype=torch.int64, device=device),
-                tau=torch.zeros(1, dtype=torch.int64, device=device))
+def alloc_schedule(N: int, k_max: int, device="cuda", layout: bool = False) -> dict:
+    """Schedule buffers; with `layout` also the planner's per-rank send and
+    stream offsets (the buffer layout the pack can use directly)."""
+    s = dict(K=torch.zeros(1, dtype=torch.int32, device=device),
+             family=torch.empty(k_max, dtype=torch.int32, device=device),
+             dst=torch.empty((k_max, N), dtype=torch.int32, device=device),
+             inst=torch.empty((k_max, N), dtype=torch.int32, device=device),
+             bytes=torch.empty((k_max, N), dtype=torch.int64, device=device),
+             tau=torch.zeros(1, dtype=torch.int64, device=device))
+    if layout:
+        s["send_off"] = torch.empty((k_max, N), dtype=torch.int64, device=device)
+        s["stream_off"] = torch.empty((k_max, N), dtype=torch.int64, device=device)
+    return s
 
 
 def plan(cat: Catalog, D: torch.Tensor, p: PlanParams, status: Optional[torch.Tensor] = None,
@@ -273,8 +283,9 @@ def plan(cat: Catalog, D: torch.Tensor, p: PlanParams, status: Optional[torch.Te
     if ws is None:
         ws = torch.empty(plan_workspace_bytes(cat, p), dtype=torch.uint8, device=D.device)
     _check(lib().vp_plan(cat.handle, _ptr(D), C.byref(p), _ptr(out["K"]), _ptr(out["family"]),
-                         _ptr(out["dst"]), _ptr(out["inst"]), _ptr(out["bytes"]), _ptr(out["tau"]),
-                         _ptr(status), _ptr(ws), ws.numel(), _stream(stream)), "vp_plan")
+                         _ptr(out["dst"]), _ptr(out["inst"]), _ptr(out["bytes"]), _ptr(out.get("send_off")),
+                         _ptr(out.get("stream_off")), _ptr(out["tau"]), _ptr(status), _ptr(ws), ws.numel(),
+                         _stream(stream)), "vp_plan")
     out["status"] = status
     return out
 
@@ -293,7 +304,8 @@ def pack_workspace_bytes(k_max: int, send_capacity: int, unit: int, T: int = 0, 
     return int(lib().vp_pack_workspace(k_max, send_capacity, unit, T, k))
 
 
-def pack_rows(tokens: torch.Tensor, row_bytes: int, sorted_tok: torch.Tensor, dest_off: torch.Tensor,
+def pack_rows(tokens: torch.Tensor, row_bytes: int, sorted_tok: torch.Tensor, sorted_slot: torch.Tensor,
+              dest_off: torch.Tensor,
               self_rank: int, sched: dict, send: torch.Tensor, step_off: torch.Tensor,
               status: torch.Tensor, ws: Optional[torch.Tensor] = None, stream=None):
     """vp_pack_rows: this rank's token rows into the send buffer in step order.
@@ -308,10 +320,12 @@ def pack_rows(tokens: torch.Tensor, row_bytes: int, sorted_tok: torch.Tensor, de
     N = sched["dst"].shape[1]
     cap = send.numel() * send.element_size()
     if ws is None:
-        ws = torch.empty(pack_workspace_bytes(k_max, cap, row_bytes, T, k), dtype=torch.uint8,
+        ws = torch.zeros(pack_workspace_bytes(k_max, cap, row_bytes, T, k), dtype=torch.uint8,
                          device=send.device)
-    _check(lib().vp_pack_rows(_ptr(tokens), T, k, row_bytes, _ptr(sorted_tok), _ptr(dest_off), self_rank, N,
-                              _ptr(sched["K"]), _ptr(sched["dst"]), _ptr(sched["bytes"]), k_max, _ptr(send),
+    _check(lib().vp_pack_rows(_ptr(tokens), T, k, row_bytes, _ptr(sorted_tok), _ptr(sorted_slot), _ptr(dest_off),
+                              self_rank, N,
+                              _ptr(sched["K"]), _ptr(sched["dst"]), _ptr(sched["bytes"]),
+                              _ptr(sched.get("send_off")), _ptr(sched.get("stream_off")), k_max, _ptr(send),
                               cap, _ptr(step_off), _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
            "vp_pack_rows")
 
@@ -327,9 +341,10 @@ def pack_heads(act: torch.Tensor, token_stride: int, head_lo: torch.Tensor, head
     N = sched["dst"].shape[1]
     cap = send.numel() * send.element_size()
     if ws is None:
-        ws = torch.empty(pack_workspace_bytes(k_max, cap, head_bytes), dtype=torch.uint8, device=send.device)
+        ws = torch.zeros(pack_workspace_bytes(k_max, cap, head_bytes), dtype=torch.uint8, device=send.device)
     _check(lib().vp_pack_heads(_ptr(act), T, token_stride, _ptr(head_lo), head_bytes, self_rank, N,
-                               _ptr(sched["K"]), _ptr(sched["dst"]), _ptr(sched["bytes"]), k_max,
+                               _ptr(sched["K"]), _ptr(sched["dst"]), _ptr(sched["bytes"]),
+                               _ptr(sched.get("send_off")), _ptr(sched.get("stream_off")), k_max,
                                _ptr(send), cap, _ptr(step_off), _ptr(status), _ptr(ws), ws.numel(),
                                _stream(stream)), "vp_pack_heads")
 
@@ -357,12 +372,13 @@ class Pipeline:
         kmax = self.params.k_max
         dev = device
         self.status = new_status(dev)
-        self.sched = alloc_schedule(N, kmax, dev)
+        self.sched = alloc_schedule(N, kmax, dev, layout=True)
         self.plan_ws = torch.empty(plan_workspace_bytes(self.cat, self.params), dtype=torch.uint8, device=dev)
         if mode == "moe":
             self.dem = dict(counts=torch.empty((N, n_experts), dtype=torch.int32, device=dev),
                             demand=torch.empty((N, N), dtype=torch.int64, device=dev),
                             sorted_tok=torch.empty(max(tokens * top_k, 1), dtype=torch.int32, device=dev),
+                            sorted_slot=torch.empty(max(tokens * top_k, 1), dtype=torch.uint8, device=dev),
                             dest_off=torch.empty(N + 1, dtype=torch.int64, device=dev))
             self.dem_ws = torch.empty(max(demand_workspace_bytes(tokens, top_k, n_experts), 1),
                                       dtype=torch.uint8, device=dev)
@@ -375,7 +391,7 @@ class Pipeline:
         self.send_capacity = cap
         self.send = torch.empty(max(cap, 16), dtype=torch.uint8, device=dev)
         self.step_off = torch.empty(kmax + 1, dtype=torch.int64, device=dev)
-        self.pack_ws = torch.empty(pack_workspace_bytes(kmax, cap, unit, ws_T, ws_k), dtype=torch.uint8,
+        self.pack_ws = torch.zeros(pack_workspace_bytes(kmax, cap, unit, ws_T, ws_k), dtype=torch.uint8,
                                    device=dev)
 
     # The hot path in stages (all enqueued on one stream, no host sync).
@@ -386,7 +402,8 @@ class Pipeline:
             R, T, k = routing.shape
             _check(L.vp_demand(_ptr(routing), R, T, k, self.E, self.N, 0, self.self_rank, self.unit,
                                _ptr(self.dem["counts"]), _ptr(self.dem["demand"]),
-                               _ptr(self.dem["sorted_tok"]), _ptr(self.dem["dest_off"]), _ptr(self.status),
+                               _ptr(self.dem["sorted_tok"]), _ptr(self.dem["sorted_slot"]),
+                               _ptr(self.dem["dest_off"]), _ptr(self.status),
                                _ptr(self.dem_ws), self.dem_ws.numel(), s), "vp_demand")
         else:
             _check(L.vp_demand_heads(self.T, _ptr(head_lo), self.unit, self.N, 0, self.N,
@@ -396,7 +413,8 @@ class Pipeline:
         p = self.params
         _check(lib().vp_plan(self.cat.handle, _ptr(self.dem["demand"]), C.byref(p), _ptr(self.sched["K"]),
                              _ptr(self.sched["family"]), _ptr(self.sched["dst"]), _ptr(self.sched["inst"]),
-                             _ptr(self.sched["bytes"]), _ptr(self.sched["tau"]), _ptr(self.status),
+                             _ptr(self.sched["bytes"]), _ptr(self.sched["send_off"]),
+                             _ptr(self.sched["stream_off"]), _ptr(self.sched["tau"]), _ptr(self.status),
                              _ptr(self.plan_ws), self.plan_ws.numel(), _stream(stream)), "vp_plan")
 
     def pack_prepare_stage(self, tokens: torch.Tensor, head_lo: Optional[torch.Tensor] = None, stream=None):
@@ -404,16 +422,19 @@ class Pipeline:
         if self.mode == "moe":
             T = tokens.numel() * tokens.element_size() // self.unit
             _check(L.vp_pack_prepare_rows(_ptr(tokens), T, self.k, self.unit, _ptr(self.dem["sorted_tok"]),
-                                          _ptr(self.dem["dest_off"]), self.self_rank, self.N,
+                                          _ptr(self.dem["sorted_slot"]), _ptr(self.dem["dest_off"]),
+                                          self.self_rank, self.N,
                                           _ptr(self.sched["K"]), _ptr(self.sched["dst"]),
-                                          _ptr(self.sched["bytes"]), p.k_max, self.send_capacity,
+                                          _ptr(self.sched["bytes"]), _ptr(self.sched["send_off"]),
+                                          _ptr(self.sched["stream_off"]), p.k_max, self.send_capacity,
                                           _ptr(self.step_off), _ptr(self.status), _ptr(self.pack_ws),
                                           self.pack_ws.numel(), s), "vp_pack_prepare_rows")
         else:
             T = tokens.numel() * tokens.element_size() // self.token_stride
             _check(L.vp_pack_prepare_heads(_ptr(tokens), T, self.token_stride, _ptr(head_lo), self.unit,
                                            self.self_rank, self.N, _ptr(self.sched["K"]),
-                                           _ptr(self.sched["dst"]), _ptr(self.sched["bytes"]), p.k_max,
+                                           _ptr(self.sched["dst"]), _ptr(self.sched["bytes"]),
+                                           _ptr(self.sched["send_off"]), _ptr(self.sched["stream_off"]), p.k_max,
                                            self.send_capacity, _ptr(self.step_off), _ptr(self.status),
                                            _ptr(self.pack_ws), self.pack_ws.numel(), s), "vp_pack_prepare_heads")
 

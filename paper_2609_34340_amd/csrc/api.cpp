@@ -163,10 +163,10 @@ size_t vp_demand_workspace(int64_t T, int32_t k, int32_t E) {
 
 vp_status vp_demand(const int32_t* routing, int32_t R, int64_t T, int32_t k, int32_t E,
                     int32_t n_ranks, int32_t first_rank, int32_t sort_row, int64_t unit_bytes,
-                    int32_t* counts, int64_t* demand, int32_t* sorted_tok, int64_t* dest_off,
-                    int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
-  if (R < 1 || T < 0 || k < 1 || E < 1 || n_ranks < 1 || E % n_ranks != 0 || E > 4096)
-    return set_error(VP_ERR_INVALID_ARGUMENT, "bad demand sizes (E must be a multiple of N, <= 4096)");
+                    int32_t* counts, int64_t* demand, int32_t* sorted_tok, uint8_t* sorted_slot,
+                    int64_t* dest_off, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
+  if (R < 1 || T < 0 || k < 1 || k > 255 || E < 1 || n_ranks < 1 || E % n_ranks != 0 || E > 4096)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "bad demand sizes (E a multiple of N, <= 4096; k <= 255)");
   if (T * (int64_t)k >= (int64_t(1) << 31)) return set_error(VP_ERR_UNSUPPORTED, "T*k must be < 2^31");
   if (first_rank < 0 || first_rank + R > n_ranks) return set_error(VP_ERR_INVALID_ARGUMENT, "rank range");
   if (sort_row < -1 || sort_row >= R) return set_error(VP_ERR_INVALID_ARGUMENT, "sort_row");
@@ -178,7 +178,7 @@ vp_status vp_demand(const int32_t* routing, int32_t R, int64_t T, int32_t k, int
   if (ws_bytes < vp::demand_workspace(T, k, E) || (!ws && ws_bytes))
     return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
   vp::DemandLaunch a{routing, R, T, k, E, n_ranks, first_rank, sort_row, unit_bytes, counts, demand,
-                     sorted_tok, dest_off, dev_status, ws, ws_bytes};
+                     sorted_tok, sorted_slot, dest_off, dev_status, ws, ws_bytes};
   return vp::launch_demand(a, stream);
 }
 
@@ -210,10 +210,13 @@ size_t vp_plan_workspace(const vp_catalog* c, const vp_plan_params* p) {
 }
 
 vp_status vp_plan(const vp_catalog* c, const int64_t* demand, const vp_plan_params* p, int32_t* K,
-                  int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes, int64_t* tau,
-                  int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
+                  int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes, int64_t* send_off,
+                  int64_t* stream_off, int64_t* tau, int32_t* dev_status, void* ws, size_t ws_bytes,
+                  void* stream) {
   if (!c || !demand || !p || !K || !family || !dst || !inst || !bytes || !dev_status)
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
+  if ((send_off == nullptr) != (stream_off == nullptr))
+    return set_error(VP_ERR_INVALID_ARGUMENT, "send_off and stream_off go together");
   if (!c->dev) return set_error(VP_ERR_INVALID_ARGUMENT, "catalog not uploaded");
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev != c->dev_id)
@@ -224,7 +227,7 @@ vp_status vp_plan(const vp_catalog* c, const int64_t* demand, const vp_plan_para
   if (p->lambda_ns > (int64_t(1) << 40) || p->k_target > (int64_t(1) << 40))
     return set_error(VP_ERR_UNSUPPORTED, "lambda or k_target too large");
   if (ws_bytes < vp_plan_workspace(c, p) || !ws) return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
-  vp::PlanLaunch a{c, demand, (int64_t*)ws, *p, K, family, dst, inst, bytes, tau, dev_status};
+  vp::PlanLaunch a{c, demand, (int64_t*)ws, *p, K, family, dst, inst, bytes, tau, send_off, stream_off, dev_status};
   return vp::launch_plan(a, stream);
 }
 
@@ -236,28 +239,38 @@ size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_byte
 namespace {
 
 vp_status pack_rows_stages(int stages, const void* tokens, int64_t T, int32_t k, int64_t row_bytes,
-                           const int32_t* sorted_tok, const int64_t* dest_off, int32_t self_rank,
+                           const int32_t* sorted_tok, const uint8_t* sorted_slot, const int64_t* dest_off,
+                           int32_t self_rank,
                            int32_t n_ranks, const int32_t* K, const int32_t* dst, const int64_t* bytes,
-                           int32_t k_max, void* send, int64_t send_capacity, int64_t* step_off,
-                           int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
+                           const int64_t* send_off, const int64_t* stream_off, int32_t k_max, void* send,
+                           int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
+                           size_t ws_bytes, void* stream) {
+  if ((send_off == nullptr) != (stream_off == nullptr))
+    return set_error(VP_ERR_INVALID_ARGUMENT, "send_off and stream_off go together");
   if (T < 0 || k < 1 || row_bytes < 16 || row_bytes % 16 != 0 || n_ranks < 1 || n_ranks > vp::kMaxRanks ||
       self_rank < 0 || self_rank >= n_ranks || k_max < 1 || send_capacity < 0)
     return set_error(VP_ERR_INVALID_ARGUMENT, "bad pack sizes (row_bytes must be a multiple of 16)");
-  if (!dest_off || !K || !dst || !bytes || !step_off || !dev_status || (T > 0 && (!tokens || !sorted_tok)) ||
+  if (!dest_off || !K || !dst || !bytes || !step_off || !dev_status ||
+      (T > 0 && (!tokens || !sorted_tok || !sorted_slot)) ||
       ((stages & 2) && send_capacity > 0 && !send))
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
   if (ws_bytes < vp::pack_workspace(k_max, send_capacity, row_bytes, T, k) || !ws)
     return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
-  vp::PackLaunch a{0, stages, tokens, T, k, row_bytes, row_bytes, sorted_tok, dest_off, nullptr, self_rank, n_ranks,
-                   K, dst, bytes, k_max, send, send_capacity, step_off, dev_status, ws, ws_bytes};
+  vp::PackLaunch a{0, stages, tokens, T, k, row_bytes, row_bytes, sorted_tok, sorted_slot, dest_off, nullptr,
+                   self_rank, n_ranks,
+                   K, dst, bytes, send_off, stream_off, k_max, send, send_capacity, step_off, dev_status, ws,
+                   ws_bytes};
   return vp::launch_pack(a, stream);
 }
 
 vp_status pack_heads_stages(int stages, const void* act, int64_t T, int64_t token_stride,
                             const int64_t* head_lo, int64_t head_bytes, int32_t self_rank, int32_t n_ranks,
-                            const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
-                            void* send, int64_t send_capacity, int64_t* step_off, int32_t* dev_status,
-                            void* ws, size_t ws_bytes, void* stream) {
+                            const int32_t* K, const int32_t* dst, const int64_t* bytes,
+                            const int64_t* send_off, const int64_t* stream_off, int32_t k_max, void* send,
+                            int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
+                            size_t ws_bytes, void* stream) {
+  if ((send_off == nullptr) != (stream_off == nullptr))
+    return set_error(VP_ERR_INVALID_ARGUMENT, "send_off and stream_off go together");
   if (T < 0 || head_bytes < 16 || head_bytes % 16 != 0 || token_stride < head_bytes ||
       token_stride % 16 != 0 || n_ranks < 1 || n_ranks > vp::kMaxRanks || self_rank < 0 ||
       self_rank >= n_ranks || k_max < 1 || send_capacity < 0)
@@ -267,48 +280,58 @@ vp_status pack_heads_stages(int stages, const void* act, int64_t T, int64_t toke
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
   if (ws_bytes < vp::pack_workspace(k_max, send_capacity, head_bytes, T, 0) || !ws)
     return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
-  vp::PackLaunch a{1, stages, act, T, 0, head_bytes, token_stride, nullptr, nullptr, head_lo, self_rank, n_ranks,
-                   K, dst, bytes, k_max, send, send_capacity, step_off, dev_status, ws, ws_bytes};
+  vp::PackLaunch a{1, stages, act, T, 0, head_bytes, token_stride, nullptr, nullptr, nullptr, head_lo,
+                   self_rank, n_ranks,
+                   K, dst, bytes, send_off, stream_off, k_max, send, send_capacity, step_off, dev_status, ws,
+                   ws_bytes};
   return vp::launch_pack(a, stream);
 }
 
 }  // namespace
 
 vp_status vp_pack_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes, const int32_t* sorted_tok,
-                       const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
-                       const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
-                       void* send, int64_t send_capacity, int64_t* step_off, int32_t* dev_status,
-                       void* ws, size_t ws_bytes, void* stream) {
-  return pack_rows_stages(3, tokens, T, k, row_bytes, sorted_tok, dest_off, self_rank, n_ranks, K, dst, bytes,
-                          k_max, send, send_capacity, step_off, dev_status, ws, ws_bytes, stream);
+                       const uint8_t* sorted_slot, const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
+                       const int32_t* K, const int32_t* dst, const int64_t* bytes, const int64_t* send_off,
+                       const int64_t* stream_off, int32_t k_max, void* send, int64_t send_capacity,
+                       int64_t* step_off, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
+  return pack_rows_stages(3, tokens, T, k, row_bytes, sorted_tok, sorted_slot, dest_off, self_rank, n_ranks, K,
+                          dst, bytes,
+                          send_off, stream_off, k_max, send, send_capacity, step_off, dev_status, ws, ws_bytes,
+                          stream);
 }
 
 vp_status vp_pack_prepare_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes,
-                               const int32_t* sorted_tok,
+                               const int32_t* sorted_tok, const uint8_t* sorted_slot,
                                const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,
-                               const int32_t* K, const int32_t* dst, const int64_t* bytes, int32_t k_max,
+                               const int32_t* K, const int32_t* dst, const int64_t* bytes,
+                               const int64_t* send_off, const int64_t* stream_off, int32_t k_max,
                                int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
                                size_t ws_bytes, void* stream) {
-  return pack_rows_stages(1, tokens, T, k, row_bytes, sorted_tok, dest_off, self_rank, n_ranks, K, dst, bytes,
-                          k_max, nullptr, send_capacity, step_off, dev_status, ws, ws_bytes, stream);
+  return pack_rows_stages(1, tokens, T, k, row_bytes, sorted_tok, sorted_slot, dest_off, self_rank, n_ranks, K,
+                          dst, bytes,
+                          send_off, stream_off, k_max, nullptr, send_capacity, step_off, dev_status, ws,
+                          ws_bytes, stream);
 }
 
 vp_status vp_pack_heads(const void* act, int64_t T, int64_t token_stride, const int64_t* head_lo,
                         int64_t head_bytes, int32_t self_rank, int32_t n_ranks, const int32_t* K,
-                        const int32_t* dst, const int64_t* bytes, int32_t k_max, void* send,
-                        int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
-                        size_t ws_bytes, void* stream) {
+                        const int32_t* dst, const int64_t* bytes, const int64_t* send_off,
+                        const int64_t* stream_off, int32_t k_max, void* send, int64_t send_capacity,
+                        int64_t* step_off, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
   return pack_heads_stages(3, act, T, token_stride, head_lo, head_bytes, self_rank, n_ranks, K, dst, bytes,
-                           k_max, send, send_capacity, step_off, dev_status, ws, ws_bytes, stream);
+                           send_off, stream_off, k_max, send, send_capacity, step_off, dev_status, ws, ws_bytes,
+                           stream);
 }
 
 vp_status vp_pack_prepare_heads(const void* act, int64_t T, int64_t token_stride, const int64_t* head_lo,
                                 int64_t head_bytes, int32_t self_rank, int32_t n_ranks, const int32_t* K,
-                                const int32_t* dst, const int64_t* bytes, int32_t k_max,
-                                int64_t send_capacity, int64_t* step_off, int32_t* dev_status, void* ws,
-                                size_t ws_bytes, void* stream) {
+                                const int32_t* dst, const int64_t* bytes, const int64_t* send_off,
+                                const int64_t* stream_off, int32_t k_max, int64_t send_capacity,
+                                int64_t* step_off, int32_t* dev_status, void* ws, size_t ws_bytes,
+                                void* stream) {
   return pack_heads_stages(1, act, T, token_stride, head_lo, head_bytes, self_rank, n_ranks, K, dst, bytes,
-                           k_max, nullptr, send_capacity, step_off, dev_status, ws, ws_bytes, stream);
+                           send_off, stream_off, k_max, nullptr, send_capacity, step_off, dev_status, ws,
+                           ws_bytes, stream);
 }
 
 vp_status vp_pack_gather(const void* src, int64_t unit_bytes, int64_t T, int32_t k, const int32_t* K,
@@ -320,9 +343,9 @@ vp_status vp_pack_gather(const void* src, int64_t unit_bytes, int64_t T, int32_t
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
   if (ws_bytes < vp::pack_workspace(k_max, send_capacity, unit_bytes, T, k) || !ws)
     return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
-  vp::PackLaunch a{k > 0 ? 0 : 1, 2, src, T, k, unit_bytes, unit_bytes, nullptr, nullptr, nullptr, 0, 1,
-                   K, nullptr, nullptr, k_max, send, send_capacity, const_cast<int64_t*>(step_off),
-                   dev_status, ws, ws_bytes};
+  vp::PackLaunch a{k > 0 ? 0 : 1, 2, src, T, k, unit_bytes, unit_bytes, nullptr, nullptr, nullptr, nullptr, 0, 1,
+                   K, nullptr, nullptr, nullptr, nullptr, k_max, send, send_capacity,
+                   const_cast<int64_t*>(step_off), dev_status, ws, ws_bytes};
   return vp::launch_pack(a, stream);
 }
 

@@ -155,7 +155,8 @@ __global__ void __launch_bounds__(1024) sort_scan(int32_t* __restrict__ ccount, 
 __global__ void __launch_bounds__(kSortThreads) sort_scatter(const int32_t* __restrict__ ids, int64_t Tk,
                                                             int32_t k, int32_t E, int32_t n_chunks,
                                                             int32_t bits, const int32_t* __restrict__ coff,
-                                                            int32_t* __restrict__ sorted_tok) {
+                                                            int32_t* __restrict__ sorted_tok,
+                                                            uint8_t* __restrict__ sorted_slot) {
   extern __shared__ int32_t wc[];    // [kSortThreads / 64][E]
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, chunk = blockIdx.x;
   constexpr int kW = kSortThreads / 64;
@@ -198,7 +199,11 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter(const int32_t* __re
 #pragma unroll
   for (int m = 0; m < kPerThread; ++m) {
     const int e = ev[m];
-    if ((unsigned)e < (unsigned)E) sorted_tok[mine[e] + rk[m]] = (int32_t)((base + m * 64 + lane) / k);
+    if ((unsigned)e < (unsigned)E) {
+      const int64_t x = base + m * 64 + lane, t = x / k;
+      sorted_tok[mine[e] + rk[m]] = (int32_t)t;
+      if (sorted_slot) sorted_slot[mine[e] + rk[m]] = (uint8_t)(x - t * k);
+    }
   }
 }
 
@@ -239,7 +244,7 @@ vp_status launch_demand(const DemandLaunch& a, void* stream) {
   int bits = 0;
   while ((1 << bits) < a.E) ++bits;
   hipLaunchKernelGGL(sort_scatter, dim3(nch), dim3(kSortThreads), (size_t)(kSortThreads / 64) * a.E * sizeof(int32_t),
-                     s, ids, Tk, a.k, a.E, nch, bits, ccount, a.sorted_tok);
+                     s, ids, Tk, a.k, a.E, nch, bits, ccount, a.sorted_tok, a.sorted_slot);
   if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "sort launch failed");
   return VP_OK;
 }

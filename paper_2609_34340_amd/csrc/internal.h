@@ -83,6 +83,7 @@ struct PlanLaunch {
   vp_plan_params p;
   int32_t *K, *family, *dst, *inst;
   int64_t *bytes, *tau;
+  int64_t *send_off, *stream_off;
   int32_t* status;
 };
 vp_status launch_plan(const PlanLaunch& a, void* stream);
@@ -96,6 +97,7 @@ struct DemandLaunch {
   int32_t* counts;
   int64_t* demand;
   int32_t* sorted_tok;
+  uint8_t* sorted_slot;
   int64_t* dest_off;
   int32_t* status;
   void* ws;
@@ -115,11 +117,13 @@ struct PackLaunch {
   int32_t k;   // rows: routing top-k (copies per token at most); heads: 0
   int64_t unit, token_stride;
   const int32_t* sorted_tok;
+  const uint8_t* sorted_slot;
   const int64_t* dest_off;
   const int64_t* head_lo;
   int32_t self_rank, N;
   const int32_t *K, *dst;
   const int64_t* bytes;
+  const int64_t *send_off, *stream_off;   // the planner's buffer layout, or both null
   int32_t k_max;
   void* send;
   int64_t send_capacity;

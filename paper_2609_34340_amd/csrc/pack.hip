@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 
 #include "internal.h"
 
@@ -59,7 +60,6 @@ struct SliceArgs {
   int64_t* step_off;
   StepDesc* desc;            // carrying steps (any order)
   int32_t* n_desc;
-  int32_t* tcnt;             // rows: per-token copy counters, cleared here
   int32_t* status;
 };
 
@@ -111,8 +111,6 @@ __global__ void __launch_bounds__(1024) slices_kernel(SliceArgs a) {
   }
   for (int i = tid; i < kSliceWaves * N; i += 1024) wv[i] = 0;
   for (int b = tid; b <= N; b += 1024) bo[b] = a.bounds[b];
-  if (a.mode == 0)
-    for (int64_t t = tid; t < a.T; t += 1024) a.tcnt[t] = 0;
   __syncthreads();
   const int K = Ks;
   // each thread owns E consecutive steps for the loads and the step scan
@@ -240,41 +238,96 @@ __global__ void __launch_bounds__(1024) slices_kernel(SliceArgs a) {
 }
 
 struct IndexArgs {
-  int mode, k;
-  int64_t unit, T, token_stride;
+  int mode, k, self, N, k_max;
+  int64_t unit, T, token_stride, send_capacity;
+  uint32_t gen;                // this call's generation of the copy counters
   const int32_t* sorted_tok;
-  const StepDesc* desc;
+  const uint8_t* sorted_slot;
+  const StepDesc* desc;        // descriptors from the slice kernel, or
   const int32_t* n_desc;
-  int32_t* tcnt;             // rows: copies recorded per token
-  int32_t* lst;              // rows: [T][k] send-unit index of each copy
-  int64_t* src_off;          // heads: source byte offset per send unit
+  const int32_t *Kp, *dst;     // the schedule and the planner's buffer layout
+  const int64_t *bytes, *send_off, *stream_off;
+  const int64_t* bounds;       // rows: dest_off; heads: head_lo
+  int64_t* step_off;
+  uint32_t* hdr;               // [0]: generation, read by the scatter
+  unsigned long long* lst;     // rows: [T][k] generation << 32 | send unit of each routing slot
+  int64_t* src_off;            // heads: source byte offset per send unit
   int32_t* status;
 };
 
 constexpr int kIndexThreads = 256;
 
-// One workgroup per carrying step.
+// One workgroup per step.  With the planner's buffer layout the workgroup
+// derives its step's descriptor itself (step offsets, checks); otherwise it
+// takes the slice kernel's.  Rows: every packed unit is one (token, routing
+// slot) assignment; its send unit goes to that slot's entry, tagged with the
+// call's generation (strictly increasing), so the entries of slots this call
+// does not pack (local experts, streams not covered) are recognisably old and
+// the list is never cleared.  Heads: the source byte offset of every packed
+// unit.
 __global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
-  const int i = blockIdx.x;
-  const int n = *a.n_desc, st = *a.status;
-  if (i >= n || st != 0) return;
-  const StepDesc d = a.desc[i];
+  const int i = blockIdx.x, tid = threadIdx.x;
+  if (i == 0 && tid == 0) *a.hdr = a.gen;
+  StepDesc d;
+  if (a.send_off) {
+    const int K = *a.Kp, st = *a.status;
+    if (K < 0 || K > a.k_max) {
+      if (i == 0 && tid == 0) report(a.status, VP_ERR_INVALID_ARGUMENT);
+      return;
+    }
+    if (st != 0) return;
+    if (i == 0 && K == 0 && tid == 0) a.step_off[0] = 0;
+    if (i >= K) return;
+    const size_t o = (size_t)i * a.N + a.self;
+    const int64_t x = a.bytes[o], so = a.send_off[o], co = a.stream_off[o];
+    const int j = a.dst[o];
+    if (tid == 0) {
+      a.step_off[i] = so;
+      if (i == K - 1) {
+        a.step_off[K] = so + x;
+        if (so + x > a.send_capacity) report(a.status, VP_ERR_CAPACITY);
+      }
+    }
+    if (x == 0) return;
+    bool ok = x > 0 && x % a.unit == 0 && so >= 0 && so % a.unit == 0 && co >= 0 && co % a.unit == 0 &&
+              j >= 0 && j < a.N && j != a.self;
+    if (ok && so + x > a.send_capacity) {
+      if (tid == 0) report(a.status, VP_ERR_CAPACITY);
+      return;
+    }
+    int64_t h = 0, b0 = 0;
+    if (ok) {
+      b0 = a.bounds[j];
+      h = a.bounds[j + 1] - b0;
+      ok = co + x <= (a.mode == 0 ? h : a.T * h) * a.unit;
+    }
+    if (!ok) {
+      if (tid == 0) report(a.status, VP_ERR_INVALID_ARGUMENT);
+      return;
+    }
+    d.first = a.mode == 0 ? b0 + co / a.unit : co / a.unit;
+    d.u0 = (int32_t)(so / a.unit);
+    d.nu = (int32_t)(x / a.unit);
+    d.h0 = a.mode == 0 ? 0 : (int32_t)b0;
+    d.h = a.mode == 0 ? 0 : (int32_t)h;
+  } else {
+    const int n = *a.n_desc, st = *a.status;
+    if (i >= n || st != 0) return;
+    d = a.desc[i];
+  }
   if (a.mode == 0) {
-    for (int u = threadIdx.x; u < d.nu; u += kIndexThreads) {
+    const unsigned long long g = (unsigned long long)a.gen << 32;
+    for (int u = tid; u < d.nu; u += kIndexThreads) {
       const int64_t tok = a.sorted_tok[d.first + u];
-      if (tok < 0 || tok >= a.T) {
+      const int slot = a.sorted_slot[d.first + u];
+      if (tok < 0 || tok >= a.T || slot >= a.k) {
         report(a.status, VP_ERR_INVALID_ARGUMENT);
         continue;
       }
-      const int slot = atomicAdd(&a.tcnt[tok], 1);
-      if (slot >= a.k) {
-        report(a.status, VP_ERR_INVALID_ARGUMENT);
-        continue;
-      }
-      a.lst[tok * a.k + slot] = d.u0 + u;
+      a.lst[tok * a.k + slot] = g | (unsigned)(d.u0 + u);
     }
   } else {
-    for (int u = threadIdx.x; u < d.nu; u += kIndexThreads) {
+    for (int u = tid; u < d.nu; u += kIndexThreads) {
       const int64_t p = d.first + u, tok = p / d.h, hd = d.h0 + (p - tok * d.h);
       a.src_off[(int64_t)d.u0 + u] = tok * a.token_stride + hd * a.unit;
     }
@@ -290,15 +343,18 @@ constexpr int kScatterMaxThreads = 512;
 // that XCD's L2) while the eight XCDs work on neighbouring tokens, whose
 // copies land next to each other in every destination's stream.
 __global__ void __launch_bounds__(kScatterMaxThreads) scatter_rows_kernel(
-    const unsigned char* __restrict__ src, const int32_t* __restrict__ tcnt, const int32_t* __restrict__ lst,
-    int64_t T, int k, int64_t unit, int64_t vpu, unsigned char* __restrict__ send, const int32_t* status) {
+    const unsigned char* __restrict__ src, const unsigned long long* __restrict__ lst,
+    const uint32_t* __restrict__ hdr, int64_t T, int k, int64_t unit, int64_t vpu,
+    unsigned char* __restrict__ send, const int32_t* status) {
   if (*status != 0) return;
   const int64_t idx = blockIdx.x >> 3;
   const int64_t t = (idx / k) * 8 + (blockIdx.x & 7);
   const int c = (int)(idx % k);
-  if (t >= T || c >= tcnt[t]) return;
+  if (t >= T) return;
+  const unsigned long long e = lst[t * k + c];
+  if ((uint32_t)(e >> 32) != *hdr) return;   // this slot is not packed by this call
   const u32x4* row = (const u32x4*)(src + t * unit);
-  u32x4* d = (u32x4*)(send + (int64_t)lst[t * k + c] * unit);
+  u32x4* d = (u32x4*)(send + (int64_t)(uint32_t)e * unit);
   for (int64_t i = threadIdx.x; i < vpu; i += blockDim.x) __builtin_nontemporal_store(row[i], d + i);
 }
 
@@ -339,12 +395,18 @@ __global__ void __launch_bounds__(kGatherThreads) gather_kernel(const unsigned c
 
 size_t desc_bytes(int32_t k_max) { return align_up((size_t)k_max * sizeof(StepDesc) + 16, 256); }
 
+constexpr size_t kHeader = 256;   // [0]: the generation of the last prepare
+
 }  // namespace
 
 size_t pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit, int64_t T, int32_t k) {
-  const size_t head = desc_bytes(k_max);
-  if (k > 0) return head + align_up((size_t)T * sizeof(int32_t), 256) + (size_t)T * (size_t)k * sizeof(int32_t);
+  const size_t head = kHeader + desc_bytes(k_max);
+  if (k > 0) return head + (size_t)T * (size_t)k * 8;
   return head + ((size_t)(send_capacity / unit) + 1) * sizeof(int64_t);
+}
+
+namespace {
+std::atomic<uint32_t> g_generation{0};
 }
 
 vp_status launch_pack(const PackLaunch& a, void* stream) {
@@ -355,29 +417,35 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
   int lds_max = 0;
   if (hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
     return set_error(VP_ERR_HIP, "hipDeviceGetAttribute failed");
-  if (lds + 1024 > (size_t)lds_max) return set_error(VP_ERR_UNSUPPORTED, "k_max too large for the slice table");
+  const bool layout = a.send_off != nullptr;
+  if (!layout && lds + 1024 > (size_t)lds_max)
+    return set_error(VP_ERR_UNSUPPORTED, "k_max too large for the slice table");
   if (a.unit % 16 != 0) return set_error(VP_ERR_INVALID_ARGUMENT, "unit must be a multiple of 16");
   if ((a.mode == 0) != (a.k > 0)) return set_error(VP_ERR_INVALID_ARGUMENT, "top-k must be > 0 exactly for rows");
   // unit counts and send-unit indices are held in 32 bits
   if (a.send_capacity / a.unit >= ((int64_t)1 << 31)) return set_error(VP_ERR_UNSUPPORTED, "send buffer too large");
   char* ws = (char*)a.ws;
-  StepDesc* desc = (StepDesc*)ws;
-  int32_t* n_desc = (int32_t*)(ws + (size_t)a.k_max * sizeof(StepDesc));
-  char* rest = ws + desc_bytes(a.k_max);
-  int32_t* tcnt = (int32_t*)rest;
-  int32_t* lst = (int32_t*)(rest + align_up((size_t)a.T * sizeof(int32_t), 256));
+  uint32_t* hdr = (uint32_t*)ws;
+  StepDesc* desc = (StepDesc*)(ws + kHeader);
+  int32_t* n_desc = (int32_t*)(ws + kHeader + (size_t)a.k_max * sizeof(StepDesc));
+  char* rest = ws + kHeader + desc_bytes(a.k_max);
+  unsigned long long* lst = (unsigned long long*)rest;
   int64_t* src_off = (int64_t*)rest;
 
   if (a.stages & 1) {
-    SliceArgs sa{a.mode, a.K, a.dst, a.bytes, a.k_max, a.N, a.self_rank, a.unit, a.T, a.send_capacity,
-                 a.token_stride, a.mode == 0 ? a.dest_off : a.head_lo, a.step_off, desc, n_desc, tcnt, a.status};
-    if (hipFuncSetAttribute((const void*)slices_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
-        hipSuccess)
-      return set_error(VP_ERR_HIP, "cannot raise the slice kernel's LDS limit");
-    hipLaunchKernelGGL(slices_kernel, dim3(1), dim3(1024), lds, s, sa);
-
-    IndexArgs ia{a.mode, a.k, a.unit, a.T, a.token_stride, a.sorted_tok, desc, n_desc, tcnt, lst, src_off,
-                 a.status};
+    uint32_t gen = ++g_generation;
+    if (gen == 0) gen = ++g_generation;   // zero is the value of a cleared workspace
+    if (!layout) {
+      SliceArgs sa{a.mode, a.K, a.dst, a.bytes, a.k_max, a.N, a.self_rank, a.unit, a.T, a.send_capacity,
+                   a.token_stride, a.mode == 0 ? a.dest_off : a.head_lo, a.step_off, desc, n_desc, a.status};
+      if (hipFuncSetAttribute((const void*)slices_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds) != hipSuccess)
+        return set_error(VP_ERR_HIP, "cannot raise the slice kernel's LDS limit");
+      hipLaunchKernelGGL(slices_kernel, dim3(1), dim3(1024), lds, s, sa);
+    }
+    IndexArgs ia{a.mode, a.k, a.self_rank, a.N, a.k_max, a.unit, a.T, a.token_stride, a.send_capacity, gen,
+                 a.sorted_tok, a.sorted_slot, desc, n_desc, a.K, a.dst, a.bytes, a.send_off, a.stream_off,
+                 a.mode == 0 ? a.dest_off : a.head_lo, a.step_off, hdr, lst, src_off, a.status};
     hipLaunchKernelGGL(index_kernel, dim3(a.k_max), dim3(kIndexThreads), 0, s, ia);
   }
   if (!(a.stages & 2)) {
@@ -391,8 +459,8 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
       if (blocks >= ((int64_t)1 << 31)) return set_error(VP_ERR_UNSUPPORTED, "too many token copies");
       const int threads = (int)std::min<int64_t>(kScatterMaxThreads, (vpu + 63) / 64 * 64);
       hipLaunchKernelGGL(scatter_rows_kernel, dim3((unsigned)blocks), dim3(threads), 0, s,
-                         (const unsigned char*)a.src, tcnt, lst, a.T, a.k, a.unit, vpu, (unsigned char*)a.send,
-                         a.status);
+                         (const unsigned char*)a.src, lst, hdr, a.T, a.k, a.unit, vpu,
+                         (unsigned char*)a.send, a.status);
     }
   } else {
     // u = floor(v / vpu) = mulhi(v << 16, ceil(2^48 / vpu)) for v < 2^48 / vpu

@@ -68,11 +68,12 @@ struct PlanArgs {
   int32_t MLT, MRT;   // most diagonal-block terms of a pattern; largest NIC-lane set
   int32_t *K, *family, *dst, *inst;
   int64_t *bytes, *tau;
+  int64_t *send_off, *stream_off;   // optional [k_max][N] buffer layout per rank
   int32_t* status;
   // LDS layout (byte offsets)
   int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo, o_finl;
   int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bx, o_brw, o_top;
-  int32_t o_rset, o_psid, o_rbest, o_pbase, o_lastj, o_lastv, o_rp;
+  int32_t o_rset, o_psid, o_rbest, o_pbase, o_lastj, o_lastv, o_rp, o_sacc;
 };
 
 // ------------------------------------------------------------------ helpers
@@ -505,6 +506,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   // global store (stores of earlier iterations are complete by then).
   uint8_t* rp = smem + P.o_rp;   // [FC][NS][G][2] packed permutations of the shuffled starts
   int32_t* lastj = (int32_t*)(smem + P.o_lastj);
+  int64_t* sacc = (int64_t*)(smem + P.o_sacc);   // [N] bytes each rank has sent so far
   int64_t* lastv = (int64_t*)(smem + P.o_lastv);
   const int32_t* cat = P.cat;
 
@@ -559,7 +561,10 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   }
   for (int x = tid; x < L.J1; x += kPlanThreads) psid[x] = (uint16_t)cat[L.off_psid + x];
   for (int x = tid; x < P.FC; x += kPlanThreads) topkey[x] = 0;
-  for (int x = tid; x < N; x += kPlanThreads) lastj[x] = -1;
+  for (int x = tid; x < N; x += kPlanThreads) {
+    lastj[x] = -1;
+    sacc[x] = 0;
+  }
   int64_t* colsum = (int64_t*)hp;   // the credit area is free during the prologue
   for (int x = tid; x < N; x += kPlanThreads) colsum[x] = 0;
   __syncthreads();
@@ -946,6 +951,14 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         P.dst[o] = j;
         P.inst[o] = d_id(w);
         P.bytes[o] = x;
+        if (P.send_off) {
+          // Sec. 5 buffer layout: where this lane's slice sits in rank i's
+          // send buffer and in its stream to j (bytes sent there before)
+          const int64_t before = rv < kRawSaturated ? (int64_t)rv : P.Drem[(size_t)i * N + j];
+          P.send_off[o] = sacc[i];
+          P.stream_off[o] = P.D[(size_t)i * N + j] - before;
+          sacc[i] += x;
+        }
         if (xu > 0) {
           int64_t* dp = P.Drem + (size_t)i * N + j;
           int64_t nv;
@@ -1075,6 +1088,8 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   P.inst = a.inst;
   P.bytes = a.bytes;
   P.tau = a.tau;
+  P.send_off = a.send_off;
+  P.stream_off = a.stream_off;
   P.status = a.status;
 
   size_t o = 0;
@@ -1100,6 +1115,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_pbase, (size_t)NP * 4);
   take(&P.o_lastj, (size_t)N * 4);
   take(&P.o_lastv, (size_t)N * 8);
+  take(&P.o_sacc, (size_t)N * 8);
   const size_t fixed = o;
   const size_t per_fam = align_up((size_t)NS * sizeof(PairRes), 16) + 2 * align_up((size_t)N * 2, 16) +
                          2 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16) + 16 +

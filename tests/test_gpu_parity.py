@@ -86,15 +86,37 @@ def assert_schedule_equal(g, o):
                 key, bad.tolist(), [a[tuple(x)] for x in bad], [b[tuple(x)] for x in bad]))
 
 
-def gpu_plan(vp, topo, D, unit, **kw):
+def gpu_plan(vp, topo, D, unit, layout=False, **kw):
     cat = gcat(vp, topo)
     p = vp.plan_params(cat.N, unit, **kw)
     st = vp.new_status()
-    s = vp.plan(cat, torch.from_numpy(np.ascontiguousarray(D)).cuda(), p, status=st)
+    out = vp.alloc_schedule(cat.N, p.k_max, layout=layout)
+    s = vp.plan(cat, torch.from_numpy(np.ascontiguousarray(D)).cuda(), p, status=st, out=out)
     torch.cuda.synchronize()
     h = vp.schedule_to_host(s)
     h["status"] = vp.read_status(st)
+    if layout:
+        K = h["K"]
+        h["send_off"] = s["send_off"][:K].cpu().numpy()
+        h["stream_off"] = s["stream_off"][:K].cpu().numpy()
     return h
+
+
+def layout_np(dst, nbytes):
+    """Sec. 5 buffer layout restated from a schedule: bytes each rank sent
+    before step k, and bytes it sent to step k's destination before step k."""
+    K, N = nbytes.shape
+    send_off = np.zeros((K, N), np.int64)
+    stream_off = np.zeros((K, N), np.int64)
+    sent = np.zeros(N, np.int64)
+    to = np.zeros((N, N), np.int64)
+    rows = np.arange(N)
+    for k in range(K):
+        send_off[k] = sent
+        stream_off[k] = to[rows, dst[k]]
+        sent += nbytes[k]
+        to[rows, dst[k]] += nbytes[k]
+    return send_off, stream_off
 
 
 # ---------------------------------------------------------------- demand
@@ -111,6 +133,7 @@ def test_demand_parity_full_size(vp, cid):
         assert np.array_equal(out["demand"].cpu().numpy(), D)
         assert np.array_equal(out["counts"].cpu().numpy(), np.stack([d["counts"] for d in dem]))
         assert np.array_equal(out["sorted_tok"].cpu().numpy(), dem[sort_row]["sorted_tok"])
+        assert np.array_equal(out["sorted_slot"].cpu().numpy(), dem[sort_row]["sorted_slot"])
         assert np.array_equal(out["dest_off"].cpu().numpy(), dem[sort_row]["dest_off"])
 
 
@@ -131,6 +154,7 @@ def test_demand_ragged(vp, T, k, E, N, first):
         assert np.array_equal(out["counts"][r].cpu().numpy(), ref["counts"])
     ref = oracle.demand(R[1], N, E, fr + 1, 4096)
     assert np.array_equal(out["sorted_tok"].cpu().numpy()[:T * k], ref["sorted_tok"])
+    assert np.array_equal(out["sorted_slot"].cpu().numpy()[:T * k], ref["sorted_slot"])
     assert np.array_equal(out["dest_off"].cpu().numpy(), ref["dest_off"])
 
 
@@ -171,10 +195,14 @@ def test_plan_parity_full_size(vp, cid):
     else:
         w, _, _, D = moe_case(cid)
     log("plan parity C%d (N=%d)" % (cid, w.n_ranks))
-    g = gpu_plan(vp, w.topo, D, w.row_bytes)
+    g = gpu_plan(vp, w.topo, D, w.row_bytes, layout=cid in (2, 5))
     assert g["status"] == 0
     o = oracle_plan(cid, D)
     assert_schedule_equal(g, o)
+    if cid in (2, 5):
+        so, co = layout_np(o["dst"], o["bytes"])
+        assert np.array_equal(g["send_off"], so)
+        assert np.array_equal(g["stream_off"], co)
 
 
 def test_plan_parity_second_matrix_of_streams(vp):
@@ -247,35 +275,48 @@ def test_plan_deterministic(vp):
 
 # ------------------------------------------------------------------ pack
 
-def gpu_pack_rows(vp, w, R, sched_np, self_rank, tokens_np, cap_extra=0, cap=None):
-    rt = torch.from_numpy(R).cuda()
-    dem = vp.demand(rt, w.n_ranks, w.experts, w.row_bytes, sort_row=self_rank)
-    sched = vp.alloc_schedule(w.n_ranks, 8 * w.n_ranks)
+def upload_schedule(vp, N, sched_np, layout=False):
+    """Device schedule buffers holding sched_np (and its buffer layout)."""
+    sched = vp.alloc_schedule(N, 8 * N, layout=layout)
     K = sched_np["K"]
     sched["K"].fill_(K)
-    sched["dst"][:K] = torch.from_numpy(sched_np["dst"]).cuda()
-    sched["bytes"][:K] = torch.from_numpy(sched_np["bytes"]).cuda()
+    if K:
+        sched["dst"][:K] = torch.from_numpy(sched_np["dst"]).cuda()
+        sched["bytes"][:K] = torch.from_numpy(sched_np["bytes"]).cuda()
+        if layout:
+            so, co = layout_np(sched_np["dst"], sched_np["bytes"])
+            sched["send_off"][:K] = torch.from_numpy(so).cuda()
+            sched["stream_off"][:K] = torch.from_numpy(co).cuda()
+    return sched
+
+
+def gpu_pack_rows(vp, w, R, sched_np, self_rank, tokens_np, cap_extra=0, cap=None, layout=False):
+    rt = torch.from_numpy(R).cuda()
+    dem = vp.demand(rt, w.n_ranks, w.experts, w.row_bytes, sort_row=self_rank)
+    sched = upload_schedule(vp, w.n_ranks, sched_np, layout)
+    K = sched_np["K"]
     total = int(sched_np["bytes"][:, self_rank].sum()) if K else 0
     cap = total + cap_extra if cap is None else cap
     send = torch.full((max(cap, 16),), 0xA5, dtype=torch.uint8, device="cuda")
     step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
     st = dem["status"]
     tok = torch.from_numpy(tokens_np).cuda()
-    vp.pack_rows(tok, w.row_bytes, dem["sorted_tok"], dem["dest_off"], self_rank, sched,
+    vp.pack_rows(tok, w.row_bytes, dem["sorted_tok"], dem["sorted_slot"], dem["dest_off"], self_rank, sched,
                  send[:cap] if cap else send[:0], step_off, st)
     torch.cuda.synchronize()
     return send, step_off, vp.read_status(st), total
 
 
+@pytest.mark.parametrize("layout", [False, True])
 @pytest.mark.parametrize("cid,self_rank", [(1, 0), (1, 5), (2, 0), (2, 9), (3, 0), (5, 0)])
-def test_pack_rows_parity_full_size(vp, cid, self_rank):
+def test_pack_rows_parity_full_size(vp, cid, self_rank, layout):
     w, R, dem, D = moe_case(cid)
-    log("pack rows parity C%d rank %d" % (cid, self_rank))
+    log("pack rows parity C%d rank %d layout %s" % (cid, self_rank, layout))
     s = oracle_plan(cid, D)
     tok = vpgen.tokens_bf16(w, self_rank)
     ref, ref_off = oracle.pack_rows(tok, w.row_bytes, dem[self_rank]["sorted_tok"],
                                     dem[self_rank]["dest_off"], self_rank, s)
-    send, step_off, st, total = gpu_pack_rows(vp, w, R, s, self_rank, tok, cap_extra=64)
+    send, step_off, st, total = gpu_pack_rows(vp, w, R, s, self_rank, tok, cap_extra=64, layout=layout)
     assert st == 0
     assert total == ref.size
     assert torch.equal(send[:total], torch.from_numpy(ref).cuda())
@@ -283,31 +324,35 @@ def test_pack_rows_parity_full_size(vp, cid, self_rank):
     assert np.array_equal(step_off[:s["K"] + 1].cpu().numpy(), ref_off)
 
 
-def test_pack_rows_capacity_error_writes_nothing(vp):
+@pytest.mark.parametrize("layout", [False, True])
+def test_pack_rows_capacity_error_writes_nothing(vp, layout):
     w, R, dem, D = moe_case(1)
-    log("pack capacity error")
+    log("pack capacity error, layout %s" % layout)
     s = oracle_plan(1, D)
     tok = vpgen.tokens_bf16(w, 0)
     total = int(s["bytes"][:, 0].sum())
-    send, _, st, _ = gpu_pack_rows(vp, w, R, s, 0, tok, cap=total - w.row_bytes)
+    send, _, st, _ = gpu_pack_rows(vp, w, R, s, 0, tok, cap=total - w.row_bytes, layout=layout)
     assert st == vp.CAPACITY
     assert (send == 0xA5).all()
 
 
-def test_pack_rows_empty_schedule(vp):
+@pytest.mark.parametrize("layout", [False, True])
+def test_pack_rows_empty_schedule(vp, layout):
     w, R, dem, D = moe_case(1)
-    log("pack rows, empty schedule")
+    log("pack rows, empty schedule, layout %s" % layout)
     s = dict(K=0, dst=np.zeros((0, w.n_ranks), np.int32), bytes=np.zeros((0, w.n_ranks), np.int64))
-    send, step_off, st, total = gpu_pack_rows(vp, w, R, s, 0, vpgen.tokens_bf16(w, 0), cap_extra=64)
+    send, step_off, st, total = gpu_pack_rows(vp, w, R, s, 0, vpgen.tokens_bf16(w, 0), cap_extra=64,
+                                              layout=layout)
     assert st == 0 and total == 0
     assert int(step_off[0].item()) == 0
     assert (send == 0xA5).all()
 
 
-@pytest.mark.parametrize("bad", ["token_id", "too_many_copies"])
-def test_pack_rows_bad_token_list_writes_nothing(vp, bad):
-    """A token id out of range, or a token listed more than top-k times,
-    is reported and leaves the send buffer untouched."""
+@pytest.mark.parametrize("layout", [False, True])
+@pytest.mark.parametrize("bad", ["token_id", "slot"])
+def test_pack_rows_bad_token_list_writes_nothing(vp, bad, layout):
+    """A token id or a routing slot out of range is reported and leaves the
+    send buffer untouched."""
     w, R, dem, D = moe_case(1)
     log("pack rows, bad token list (%s)" % bad)
     s = oracle_plan(1, D)
@@ -315,16 +360,16 @@ def test_pack_rows_bad_token_list_writes_nothing(vp, bad):
     d = vp.demand(rt, w.n_ranks, w.experts, w.row_bytes, sort_row=0)
     lo, hi = int(d["dest_off"][1].item()), int(d["dest_off"][2].item())
     assert hi - lo > w.top_k
-    d["sorted_tok"][lo:hi] = w.tokens if bad == "token_id" else 0
-    sched = vp.alloc_schedule(w.n_ranks, 8 * w.n_ranks)
-    sched["K"].fill_(s["K"])
-    sched["dst"][:s["K"]] = torch.from_numpy(s["dst"]).cuda()
-    sched["bytes"][:s["K"]] = torch.from_numpy(s["bytes"]).cuda()
+    if bad == "token_id":
+        d["sorted_tok"][lo:hi] = w.tokens
+    else:
+        d["sorted_slot"][lo:hi] = w.top_k
+    sched = upload_schedule(vp, w.n_ranks, s, layout)
     total = int(s["bytes"][:, 0].sum())
     send = torch.full((total,), 0xA5, dtype=torch.uint8, device="cuda")
     step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
     vp.pack_rows(torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda(), w.row_bytes, d["sorted_tok"],
-                 d["dest_off"], 0, sched, send, step_off, d["status"])
+                 d["sorted_slot"], d["dest_off"], 0, sched, send, step_off, d["status"])
     torch.cuda.synchronize()
     assert vp.read_status(d["status"]) == vp.INVALID_ARGUMENT
     assert (send == 0xA5).all()
@@ -350,18 +395,16 @@ def test_pipeline_reuse_across_matrices(vp):
         assert torch.equal(send[:ref.size], torch.from_numpy(ref).cuda())
 
 
+@pytest.mark.parametrize("layout", [False, True])
 @pytest.mark.parametrize("self_rank", [0, 7, 12, 15])
-def test_pack_heads_parity(vp, self_rank):
+def test_pack_heads_parity(vp, self_rank, layout):
     w, hl, D = heads_case()
-    log("pack heads parity rank %d" % self_rank)
+    log("pack heads parity rank %d layout %s" % (self_rank, layout))
     s = oracle_plan(4, D)
     act = vpgen.tokens_bf16(w, self_rank)
     ref, ref_off = oracle.pack_heads(act, w.token_stride, hl, w.row_bytes, self_rank, s)
-    sched = vp.alloc_schedule(w.n_ranks, 8 * w.n_ranks)
+    sched = upload_schedule(vp, w.n_ranks, s, layout)
     K = s["K"]
-    sched["K"].fill_(K)
-    sched["dst"][:K] = torch.from_numpy(s["dst"]).cuda()
-    sched["bytes"][:K] = torch.from_numpy(s["bytes"]).cuda()
     send = torch.full((ref.size + 32,), 0xA5, dtype=torch.uint8, device="cuda")
     step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
     st = vp.new_status()

@@ -25,8 +25,11 @@ def test_demand_matches_numpy(cid, tokens):
         row[rank] = 0
         assert (out["row"] == row).all()
         assert out["row"].sum() == w.row_bytes * (T * k - per_rank[rank])
-        order = np.argsort(r.ravel(), kind="stable") // k
-        assert (out["sorted_tok"] == order).all()
+        flat = np.argsort(r.ravel(), kind="stable")
+        assert (out["sorted_tok"] == flat // k).all()
+        assert (out["sorted_slot"] == flat % k).all()
+        # every assignment appears exactly once, with the expert it was routed to
+        assert (r[out["sorted_tok"], out["sorted_slot"]] == np.sort(r.ravel(), kind="stable")).all()
         assert (out["dest_off"] == np.concatenate([[0], np.cumsum(per_rank)])).all()
 
 
