@@ -346,15 +346,34 @@ __global__ void __launch_bounds__(kScatterMaxThreads) scatter_rows_kernel(
     const unsigned char* __restrict__ src, const unsigned long long* __restrict__ lst,
     const uint32_t* __restrict__ hdr, int64_t T, int k, int64_t unit, int64_t vpu,
     unsigned char* __restrict__ send, const int32_t* status) {
-  if (*status != 0) return;
   const int64_t idx = blockIdx.x >> 3;
   const int64_t t = (idx / k) * 8 + (blockIdx.x & 7);
   const int c = (int)(idx % k);
-  if (t >= T) return;
-  const unsigned long long e = lst[t * k + c];
-  if ((uint32_t)(e >> 32) != *hdr) return;   // this slot is not packed by this call
+  if (*status != 0 || t >= T) return;
+  // this workgroup stores the token's c-th copy in send order (not routing
+  // order), so the copies the eight XCDs store at one time sit in nearby
+  // steps of the send buffer.  Every wavefront ranks the token's entries
+  // itself (one 64-lane load, k shuffles); more than 64 slots keep routing
+  // order.
+  const uint32_t gen = *hdr;
+  const int lane = threadIdx.x & 63;
+  uint32_t u;
+  if (k <= 64) {
+    const unsigned long long ei = lane < k ? lst[t * k + lane] : 0;
+    const bool ok = lane < k && (uint32_t)(ei >> 32) == gen;
+    const uint32_t ui = ok ? (uint32_t)ei : 0xFFFFFFFFu;
+    int below = 0;
+    for (int j = 0; j < k; ++j) below += (uint32_t)__shfl((int)ui, j) < ui;
+    const unsigned long long m = __ballot(ok && below == c);
+    if (m == 0) return;   // fewer than c + 1 copies of this token are packed by this call
+    u = (uint32_t)__shfl((int)ui, __builtin_ctzll(m));
+  } else {
+    const unsigned long long e = lst[t * k + c];
+    if ((uint32_t)(e >> 32) != gen) return;
+    u = (uint32_t)e;
+  }
   const u32x4* row = (const u32x4*)(src + t * unit);
-  u32x4* d = (u32x4*)(send + (int64_t)(uint32_t)e * unit);
+  u32x4* d = (u32x4*)(send + (int64_t)u * unit);
   for (int64_t i = threadIdx.x; i < vpu; i += blockDim.x) __builtin_nontemporal_store(row[i], d + i);
 }
 
