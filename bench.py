@@ -12,7 +12,9 @@ experts holding half of the per-draw mass, hot set redrawn per matrix):
 
 all enqueued on one stream with no host synchronisation, inputs resident in
 HBM.  Steps cycle over `--matrices` distinct demand matrices and two send
-buffers.  Prints one JSON line.  `value` is the pack's throughput in GB/s
+buffers.  Unless --no-sweep, the other four workloads (N = 8, 16, 64 and the
+16-rank Ulysses case) follow with six timed steps each, under "per_config".
+Prints one JSON line.  `value` is the pack's throughput in GB/s
 (send bytes + distinct source bytes + index bytes, over the time of the
 whole vp_pack call); the planner's microseconds per matrix, the step time
 and the roofline of the dominant copy kernel ride along.
@@ -74,38 +76,18 @@ def cpu_baseline(w, routing_np, tokens_np):
                 pack_s=round(t3 - t2, 4))
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=5, help="workload configuration 1..5")
-    ap.add_argument("--matrices", type=int, default=4, help="distinct demand matrices cycled")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--calibrate-copy", type=int, default=0,
-                    help="after the timed region, run one plain device copy of this many MiB")
-    args = ap.parse_args()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build's hot path is the per-rank demand -> plan -> "
-              "pack work, which runs on a single MI355X; run it with --gpus 1.", file=sys.stderr)
-        sys.exit(2)
-
+def measure(w, steps, warmup, M, dev):
+    """Time `steps` demand -> plan -> pack steps of workload `w` on one stream
+    (after `warmup` untimed ones), cycling over M matrices and two send
+    buffers.  Returns the per-stage event times and the per-matrix facts."""
     import torch
     import vpgen
     import paper_2609_34340_amd as vp
-
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    w = vpgen.config(args.config)
-    dev = torch.device("cuda:0")
-    M = max(1, min(args.matrices, args.steps))
-    print("[bench] generating %d matrices of %s" % (M, w.name), file=sys.stderr, flush=True)
 
     if w.mode == "moe":
         routing_np = [vpgen.routing_all(w, m) for m in range(M)]
         routing = [torch.from_numpy(r).to(dev) for r in routing_np]
         tokens_np = vpgen.tokens_bf16(w, 0)
-        tokens = torch.from_numpy(tokens_np).to(dev)
         acct = [rank0_accounting(w, r[0]) for r in routing_np]
         pipe = vp.Pipeline(w.topo, "moe", w.row_bytes, n_experts=w.experts, tokens=w.tokens, top_k=w.top_k)
         head_lo = None
@@ -113,11 +95,12 @@ def main():
         hl = vpgen.head_split(w.heads, w.n_ranks)
         head_lo = torch.from_numpy(hl).to(dev)
         tokens_np = vpgen.tokens_bf16(w, 0)
-        tokens = torch.from_numpy(tokens_np).to(dev)
         S = int(w.tokens * (hl[-1] - (hl[1] - hl[0])) * w.row_bytes)
         acct = [(S, S, S // w.row_bytes)]
-        routing = [None]
+        routing_np, routing = None, [None]
+        M = 1
         pipe = vp.Pipeline(w.topo, "heads", w.row_bytes, tokens=w.tokens, token_stride=w.token_stride)
+    tokens = torch.from_numpy(tokens_np).to(dev)
     sends = [pipe.send, torch.empty_like(pipe.send)]
     E = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
 
@@ -138,29 +121,29 @@ def main():
         if ev is not None:
             ev[4].record()
 
-    for s in range(args.warmup):
+    for s in range(warmup):
         run(s)
     torch.cuda.synchronize()
     if vp.read_status(pipe.status) != 0:
         raise SystemExit("device error during warmup: %d" % vp.read_status(pipe.status))
 
-    evs = [[E() for _ in range(5)] for _ in range(args.steps)]
+    evs = [[E() for _ in range(5)] for _ in range(steps)]
     start, end = E(), E()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record()
-    for s in range(args.steps):
+    for s in range(steps):
         run(s, evs[s])
     end.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     if vp.read_status(pipe.status) != 0:
         raise SystemExit("device error in the timed region: %d" % vp.read_status(pipe.status))
-    total_ms = start.elapsed_time(end)
-    demand_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
-    plan_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
-    prep_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
-    gather_ms = np.array([e[3].elapsed_time(e[4]) for e in evs])
+    r = dict(total_ms=start.elapsed_time(end), wall=wall,
+             demand_ms=np.array([e[0].elapsed_time(e[1]) for e in evs]),
+             plan_ms=np.array([e[1].elapsed_time(e[2]) for e in evs]),
+             prep_ms=np.array([e[2].elapsed_time(e[3]) for e in evs]),
+             gather_ms=np.array([e[3].elapsed_time(e[4]) for e in evs]))
 
     # schedule facts per matrix (untimed): K, slices, modeled completion time
     Ks, slices, That = [], [], []
@@ -173,17 +156,68 @@ def main():
         slices.append(int((h["bytes"][:, pipe.self_rank] > 0).sum()))
         num, den = pipe.cat.modeled_time(h["K"], h["inst"], h["bytes"], pipe.params.lambda_ns)
         That.append(num / den / 1e6)
-    step_m = [s % M for s in range(args.steps)]
+    step_m = [s % M for s in range(steps)]
     S_b = np.array([acct[m][0] for m in step_m], dtype=np.float64)
     U_b = np.array([acct[m][1] for m in step_m], dtype=np.float64)
     rows = np.array([acct[m][2] for m in step_m], dtype=np.float64)
     sl = np.array([slices[m] for m in step_m], dtype=np.float64)
-    pack_bytes = S_b + U_b + 4 * rows + 16 * sl
-    pack_ms = prep_ms + gather_ms
-    value = float(pack_bytes.sum() / (pack_ms.sum() * 1e-3) / 1e9)
-    gather_bytes = S_b + U_b
-    achieved = float(gather_bytes.sum() / (gather_ms.sum() * 1e-3) / 1e9)
-    plan_us = float(plan_ms.mean() * 1e3)
+    r["pack_bytes"] = S_b + U_b + 4 * rows + 16 * sl
+    r["pack_ms"] = r["prep_ms"] + r["gather_ms"]
+    r["gather_bytes"] = S_b + U_b
+    r["K"] = np.array([Ks[m] for m in step_m], dtype=np.float64)
+    r["That_ms"] = np.array([That[m] for m in step_m])
+    r["M"] = M
+    r["routing_np"], r["tokens_np"] = routing_np, tokens_np
+    del pipe, sends, tokens
+    torch.cuda.empty_cache()
+    return r
+
+
+def summary(w, r):
+    value = float(r["pack_bytes"].sum() / (r["pack_ms"].sum() * 1e-3) / 1e9)
+    plan_us = float(r["plan_ms"].mean() * 1e3)
+    return {"N": w.n_ranks, "plan_us_per_matrix": round(plan_us, 1),
+            "plan_us_per_activation": round(plan_us / float(r["K"].mean()), 3),
+            "activations_K": int(round(r["K"].mean())),
+            "modeled_T_ms": round(float(r["That_ms"].mean()), 3),
+            "plan_over_modeled_T": round(plan_us / (1e3 * float(r["That_ms"].mean())), 5),
+            "demand_us": round(float(r["demand_ms"].mean() * 1e3), 1),
+            "pack_us": round(float(r["pack_ms"].mean() * 1e3), 1),
+            "pack_GBps": round(value, 2), "pack_pct_of_peak": round(100 * value / PEAK_HBM_GBS, 2),
+            "pack_bytes_MB": round(float(r["pack_bytes"].mean()) / 1e6, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=5, help="workload configuration 1..5")
+    ap.add_argument("--matrices", type=int, default=4, help="distinct demand matrices cycled")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the short runs of the other configurations (plan time at every N)")
+    ap.add_argument("--calibrate-copy", type=int, default=0,
+                    help="after the timed region, run one plain device copy of this many MiB")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build's hot path is the per-rank demand -> plan -> "
+              "pack work, which runs on a single MI355X; run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import vpgen
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = vpgen.config(args.config)
+    dev = torch.device("cuda:0")
+    M = max(1, min(args.matrices, args.steps))
+    print("[bench] %s: %d matrices, %d warmup + %d timed steps" % (w.name, M, args.warmup, args.steps),
+          file=sys.stderr, flush=True)
+    r = measure(w, args.steps, args.warmup, M, dev)
+    head = summary(w, r)
+    achieved = float(r["gather_bytes"].sum() / (r["gather_ms"].sum() * 1e-3) / 1e9)
 
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
@@ -201,12 +235,12 @@ def main():
 
     out = {
         "metric": METRIC,
-        "value": round(value, 2),
+        "value": head["pack_GBps"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(total_ms / args.steps, 4),
+        "ms_per_step": round(r["total_ms"] / args.steps, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -218,26 +252,36 @@ def main():
                                    ("%d experts top-%d" % (w.experts, w.top_k)) if w.mode == "moe"
                                    else "Ulysses %d heads x %d" % (w.heads, w.head_dim),
                                    w.tokens, w.row_bytes),
-                   "matrices": M, "self_rank": 0},
-        "pct_of_peak": round(100 * value / PEAK_HBM_GBS, 2),
-        "plan_us_per_matrix": round(plan_us, 1),
-        "plan_us_per_activation": round(plan_us / float(np.mean([Ks[m] for m in step_m])), 3),
-        "demand_us": round(float(demand_ms.mean() * 1e3), 1),
-        "pack_us": round(float(pack_ms.mean() * 1e3), 1),
-        "activations_K": int(round(np.mean(Ks))),
-        "modeled_T_ms": round(float(np.mean(That)), 3),
-        "plan_over_modeled_T": round(plan_us / (1e3 * float(np.mean(That))), 5),
-        "wall_s": round(wall, 3),
+                   "matrices": r["M"], "self_rank": 0},
+        "pct_of_peak": head["pack_pct_of_peak"],
+        "plan_us_per_matrix": head["plan_us_per_matrix"],
+        "plan_us_per_activation": head["plan_us_per_activation"],
+        "demand_us": head["demand_us"],
+        "pack_us": head["pack_us"],
+        "activations_K": head["activations_K"],
+        "modeled_T_ms": head["modeled_T_ms"],
+        "plan_over_modeled_T": head["plan_over_modeled_T"],
+        "wall_s": round(r["wall"], 3),
         "roofline": {"bound": "hbm", "kernel": KERNEL_NAME[w.mode],
                      "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                     "algorithmic_bytes_per_launch": int(gather_bytes.mean()),
-                     "avg_launch_us": round(float(gather_ms.mean() * 1e3), 2)},
+                     "algorithmic_bytes_per_launch": int(r["gather_bytes"].mean()),
+                     "avg_launch_us": round(float(r["gather_ms"].mean() * 1e3), 2)},
     }
+    if not args.no_sweep:
+        # the other configurations, briefly: the planner at every N and each pack
+        per = {}
+        for cid in range(1, 6):
+            if cid == args.config:
+                continue
+            wc = vpgen.config(cid)
+            print("[bench] sweep C%d %s" % (cid, wc.name), file=sys.stderr, flush=True)
+            per["C%d" % cid] = summary(wc, measure(wc, 6, 2, 2, dev))
+        out["per_config"] = per
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on one matrix", file=sys.stderr, flush=True)
         if w.mode == "moe":
-            out["cpu_baseline"] = cpu_baseline(w, routing_np[0], tokens_np)
+            out["cpu_baseline"] = cpu_baseline(w, r["routing_np"][0], r["tokens_np"])
         else:
             out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
