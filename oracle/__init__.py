@@ -77,6 +77,14 @@ def lib():
                                     C.c_int32, vp, vp, vp, vp]
         L.orc_pack_heads.argtypes = [vp, C.c_int64, C.c_int64, vp, C.c_int64, C.c_int32,
                                      C.c_int32, C.c_int32, vp, vp, vp, vp]
+        L.orc_layout.argtypes = [C.c_int32, C.c_int32, vp, vp, vp, vp, vp]
+        L.orc_receive.argtypes = [C.c_int32, C.c_int32, C.c_int32, vp, vp, C.c_int64, C.c_int64, vp, vp, vp, vp]
+        L.orc_unpack_rows.argtypes = [vp, C.c_int32, C.c_int32, C.c_int32, vp, vp, C.c_int64, C.c_int64, vp,
+                                      C.c_int32, vp]
+        L.orc_pack_combine.argtypes = [vp, C.c_int32, C.c_int32, C.c_int32, vp, vp, C.c_int64, C.c_int64, vp,
+                                       C.c_int32, vp, vp]
+        L.orc_unpack_combine.argtypes = [vp, C.c_int32, C.c_int32, C.c_int32, vp, vp, C.c_int64, C.c_int64,
+                                         C.c_int64, C.c_int32, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -271,3 +279,97 @@ def pack_heads(act: np.ndarray, token_stride: int, head_lo, head_bytes: int, sel
     if st != OK:
         raise OracleError(st, "orc_pack_heads")
     return send, step_off
+
+
+# ------------------------------------------------------- receive / combine
+
+def slot_bytes(row_bytes: int) -> int:
+    """Receive slot of one row: rounded up to 128 bytes (Sec. 5 low-latency protocol)."""
+    return (row_bytes + 127) // 128 * 128
+
+
+def _sched(s):
+    dst = np.ascontiguousarray(s["dst"], dtype=np.int32)
+    nb = np.ascontiguousarray(s["bytes"], dtype=np.int64)
+    return int(s["K"]), dst, nb
+
+
+def layout(s, N: int):
+    """Sec. 5 buffer layout of a schedule: send, stream and receive offsets per step and lane."""
+    K, dst, nb = _sched(s)
+    so, co, ro = (np.zeros((K, N), np.int64) for _ in range(3))
+    st = lib().orc_layout(K, N, _p(dst), _p(nb), _p(so), _p(co), _p(ro))
+    if st != OK:
+        raise OracleError(st, "orc_layout")
+    return dict(send_off=so, stream_off=co, recv_off=ro)
+
+
+def received_rows(s, N: int, r: int, row_bytes: int) -> int:
+    K, dst, nb = _sched(s)
+    return int(nb[dst == r].sum()) // row_bytes
+
+
+def receive(r: int, N: int, s, row_bytes: int, sends, step_offs):
+    """Transfer emulation (test infrastructure): rank r's receive buffer from
+    every rank's send buffer and step offsets, one row per 128-B slot."""
+    K, dst, nb = _sched(s)
+    base = np.zeros(N, np.int64)
+    base[1:] = np.cumsum([x.size for x in sends])[:-1]
+    allsend = np.ascontiguousarray(np.concatenate(sends)) if sends else np.zeros(1, np.uint8)
+    offs = np.ascontiguousarray(np.stack([np.asarray(o, np.int64)[:K + 1] for o in step_offs]))
+    sb = slot_bytes(row_bytes)
+    recv = np.zeros(max(received_rows(s, N, r, row_bytes), 1) * sb, np.uint8)
+    st = lib().orc_receive(r, N, K, _p(dst), _p(nb), row_bytes, sb, _p(allsend), _p(base), _p(offs), _p(recv))
+    if st != OK:
+        raise OracleError(st, "orc_receive")
+    return recv
+
+
+def expert_rows(counts: np.ndarray, r: int, N: int) -> int:
+    E = counts.shape[1]
+    eloc = E // N
+    return int(counts[:, r * eloc:(r + 1) * eloc].sum())
+
+
+def unpack_rows(recv: np.ndarray, r: int, N: int, s, row_bytes: int, counts: np.ndarray):
+    """Dispatch receive of rank r into its expert-major output (128-B slots)."""
+    K, dst, nb = _sched(s)
+    c = np.ascontiguousarray(counts, dtype=np.int32)
+    sb = slot_bytes(row_bytes)
+    out = np.zeros(max(expert_rows(c, r, N), 1) * sb, np.uint8)
+    st = lib().orc_unpack_rows(_p(np.ascontiguousarray(recv)), r, N, K, _p(dst), _p(nb), row_bytes, sb, _p(c),
+                               c.shape[1], _p(out))
+    if st != OK:
+        raise OracleError(st, "orc_unpack_rows")
+    return out
+
+
+def pack_combine(out: np.ndarray, r: int, N: int, s, row_bytes: int, counts: np.ndarray):
+    """Combine send of rank r (schedule planned on the transposed demand)."""
+    K, dst, nb = _sched(s)
+    c = np.ascontiguousarray(counts, dtype=np.int32)
+    send = np.zeros(max(int(nb[:, r].sum()), 1), np.uint8)
+    step_off = np.zeros(K + 1, np.int64)
+    st = lib().orc_pack_combine(_p(np.ascontiguousarray(out)), r, N, K, _p(dst), _p(nb), row_bytes,
+                                slot_bytes(row_bytes), _p(c), c.shape[1], _p(send), _p(step_off))
+    if st != OK:
+        raise OracleError(st, "orc_pack_combine")
+    return send, step_off
+
+
+def unpack_combine(recv: np.ndarray, self_rank: int, N: int, s, row_bytes: int, T: int, k: int,
+                   sorted_tok: np.ndarray, sorted_slot: np.ndarray, dest_off: np.ndarray,
+                   combined: np.ndarray = None):
+    """Combine receive at its source rank: every returned row into its
+    (token, routing slot) slot of combined [T, k] (128-B slots)."""
+    K, dst, nb = _sched(s)
+    sb = slot_bytes(row_bytes)
+    if combined is None:
+        combined = np.zeros(T * k * sb, np.uint8)
+    st = lib().orc_unpack_combine(_p(np.ascontiguousarray(recv)), self_rank, N, K, _p(dst), _p(nb), row_bytes,
+                                  sb, T, k, _p(np.ascontiguousarray(sorted_tok, dtype=np.int32)),
+                                  _p(np.ascontiguousarray(sorted_slot, dtype=np.uint8)),
+                                  _p(np.ascontiguousarray(dest_off, dtype=np.int64)), _p(combined))
+    if st != OK:
+        raise OracleError(st, "orc_unpack_combine")
+    return combined

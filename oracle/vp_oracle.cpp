@@ -1,7 +1,10 @@
 // ORACLE -- TEST INFRASTRUCTURE ONLY.
 //
 // A plain, slow, single-threaded CPU implementation of the demand -> plan ->
-// pack path of VarioPath (arxiv 2609.34340), written from the paper.  Only the
+// pack path of VarioPath (arxiv 2609.34340), written from the paper, and of
+// the receive side and the combine direction that the same buffer layout
+// implies (unpack into the expert-major output; combine pack and unpack on a
+// schedule planned for the transposed demand).  Only the
 // tests, the smoke check and the benchmark's CPU-baseline leg may load it.  It
 // shares no code, header, table or helper with the HIP library; the two meet
 // only at the seeded inputs.  Every function names the passage it follows.
@@ -1075,6 +1078,174 @@ int orc_pack_heads(const uint8_t* act, int64_t T, int64_t token_stride, const in
     o += x;
   }
   step_off[K] = o;
+  return OK;
+}
+
+// Buffer layout of a schedule (Sec. 5 "Device-resident buffer layout"), per
+// step k and lane i: bytes rank i sent before step k (where the slice starts
+// in i's send buffer), bytes i sent to pi_k(i) before step k (where it starts
+// in that stream), and bytes pi_k(i) received before step k (where it lands in
+// the destination's receive stream, slices in step order).
+int orc_layout(int32_t K, int32_t N, const int32_t* dst, const int64_t* bytes, int64_t* send_off,
+               int64_t* stream_off, int64_t* recv_off) {
+  std::vector<int64_t> sent(N, 0), got(N, 0), pair((size_t)N * N, 0);
+  for (int k = 0; k < K; ++k) {
+    for (int i = 0; i < N; ++i) {
+      const size_t o = (size_t)k * N + i;
+      const int j = dst[o];
+      if (j < 0 || j >= N) return INVALID_ARGUMENT;
+      send_off[o] = sent[i];
+      stream_off[o] = pair[(size_t)i * N + j];
+      recv_off[o] = got[j];
+    }
+    for (int i = 0; i < N; ++i) {
+      const size_t o = (size_t)k * N + i;
+      const int j = dst[o];
+      sent[i] += bytes[o];
+      pair[(size_t)i * N + j] += bytes[o];
+      got[j] += bytes[o];
+    }
+  }
+  return OK;
+}
+
+// Receive slots: each token row lands at its own slot of slot_bytes (the row
+// rounded up to 128 bytes, Sec. 5 low-latency protocol).  The transfer
+// emulation below is test infrastructure: it moves every lane's slice from
+// its sender's send buffer (sends: the N buffers back to back, send_base[i]
+// where rank i's starts, step_off[i][k] where its step k starts) into rank
+// r's receive buffer, slices addressed to r in step order.
+int orc_receive(int32_t r, int32_t N, int32_t K, const int32_t* dst, const int64_t* bytes,
+                int64_t row_bytes, int64_t slot_bytes, const uint8_t* sends, const int64_t* send_base,
+                const int64_t* step_off, uint8_t* recv) {
+  int64_t got = 0;
+  for (int k = 0; k < K; ++k)
+    for (int i = 0; i < N; ++i) {
+      const size_t o = (size_t)k * N + i;
+      if (dst[o] != r || bytes[o] == 0) continue;
+      const int64_t rows = bytes[o] / row_bytes;
+      const uint8_t* src = sends + send_base[i] + step_off[(size_t)i * (K + 1) + k];
+      for (int64_t u = 0; u < rows; ++u)
+        std::memcpy(recv + (got + u) * slot_bytes, src + u * row_bytes, (size_t)row_bytes);
+      got += rows;
+    }
+  return OK;
+}
+
+namespace {
+// Expert-major output of rank r: local expert e's rows from every source in
+// (source rank, token) order.  base[i * eloc + m] is where source i's rows for
+// r's m-th local expert start; cum[i * (eloc + 1) + m] where they start in the
+// stream from i to r (rows of r's experts in (expert, token) order).
+void expert_major(int32_t r, int32_t N, const int32_t* counts, int32_t E, std::vector<int64_t>& base,
+                  std::vector<int64_t>& cum) {
+  const int eloc = E / N;
+  base.assign((size_t)N * eloc, 0);
+  cum.assign((size_t)N * (eloc + 1), 0);
+  int64_t o = 0;
+  for (int m = 0; m < eloc; ++m)
+    for (int i = 0; i < N; ++i) {
+      base[(size_t)i * eloc + m] = o;
+      o += counts[(size_t)i * E + r * eloc + m];
+    }
+  for (int i = 0; i < N; ++i)
+    for (int m = 0; m < eloc; ++m)
+      cum[(size_t)i * (eloc + 1) + m + 1] = cum[(size_t)i * (eloc + 1) + m] + counts[(size_t)i * E + r * eloc + m];
+}
+
+// Output row of stream row q from source i.
+int64_t out_row(const std::vector<int64_t>& base, const std::vector<int64_t>& cum, int eloc, int i, int64_t q) {
+  int m = 0;
+  while (m + 1 < eloc && q >= cum[(size_t)i * (eloc + 1) + m + 1]) ++m;
+  return base[(size_t)i * eloc + m] + (q - cum[(size_t)i * (eloc + 1) + m]);
+}
+}  // namespace
+
+// Dispatch receive (Sec. 5: the receive kernel unpacks straight into the
+// output layout): rank r's receive buffer, slices in step order, into the
+// expert-major output (slots of slot_bytes).  counts: [N, E] assignments per
+// (source rank, expert).
+int orc_unpack_rows(const uint8_t* recv, int32_t r, int32_t N, int32_t K, const int32_t* dst,
+                    const int64_t* bytes, int64_t row_bytes, int64_t slot_bytes, const int32_t* counts,
+                    int32_t E, uint8_t* out) {
+  if (E % N != 0) return INVALID_ARGUMENT;
+  std::vector<int64_t> base, cum;
+  expert_major(r, N, counts, E, base, cum);
+  std::vector<int64_t> sent(N, 0);
+  int64_t got = 0;
+  for (int k = 0; k < K; ++k)
+    for (int i = 0; i < N; ++i) {
+      const size_t o = (size_t)k * N + i;
+      if (dst[o] != r || bytes[o] == 0) continue;
+      const int64_t rows = bytes[o] / row_bytes;
+      for (int64_t u = 0; u < rows; ++u) {
+        const int64_t q = sent[i] + u;
+        if (q >= cum[(size_t)i * (E / N + 1) + E / N]) return INVALID_ARGUMENT;
+        std::memcpy(out + out_row(base, cum, E / N, i, q) * slot_bytes, recv + (got + u) * slot_bytes,
+                    (size_t)row_bytes);
+      }
+      sent[i] += rows;
+      got += rows;
+    }
+  return OK;
+}
+
+// Combine send (the return AlltoAllv, planned on the transposed demand):
+// stream r -> i is rank r's expert-major rows from source i in (expert,
+// token) order; lane r's steps append its next slice in schedule order.
+int orc_pack_combine(const uint8_t* out, int32_t r, int32_t N, int32_t K, const int32_t* dst,
+                     const int64_t* bytes, int64_t row_bytes, int64_t slot_bytes, const int32_t* counts,
+                     int32_t E, uint8_t* send, int64_t* step_off) {
+  if (E % N != 0) return INVALID_ARGUMENT;
+  std::vector<int64_t> base, cum;
+  expert_major(r, N, counts, E, base, cum);
+  std::vector<int64_t> sent(N, 0);
+  int64_t o = 0;
+  for (int k = 0; k < K; ++k) {
+    step_off[k] = o;
+    const size_t x = (size_t)k * N + r;
+    const int i = dst[x];
+    if (bytes[x] == 0) continue;
+    if (i < 0 || i >= N || i == r || bytes[x] % row_bytes != 0) return INVALID_ARGUMENT;
+    const int64_t rows = bytes[x] / row_bytes;
+    for (int64_t u = 0; u < rows; ++u) {
+      const int64_t q = sent[i] + u;
+      if (q >= cum[(size_t)i * (E / N + 1) + E / N]) return INVALID_ARGUMENT;
+      std::memcpy(send + o + u * row_bytes, out + out_row(base, cum, E / N, i, q) * slot_bytes, (size_t)row_bytes);
+    }
+    sent[i] += rows;
+    o += bytes[x];
+  }
+  step_off[K] = o;
+  return OK;
+}
+
+// Combine receive at source rank i: the stream from r carries the rows of
+// i's assignments to r's experts in (expert, token) order, i.e. i's sorted
+// list for destination r; each row goes to its (token, routing slot) slot of
+// combined [T, k].
+int orc_unpack_combine(const uint8_t* recv, int32_t self, int32_t N, int32_t K, const int32_t* dst,
+                       const int64_t* bytes, int64_t row_bytes, int64_t slot_bytes, int64_t T, int32_t k,
+                       const int32_t* sorted_tok, const uint8_t* sorted_slot, const int64_t* dest_off,
+                       uint8_t* combined) {
+  std::vector<int64_t> sent(N, 0);
+  int64_t got = 0;
+  for (int kk = 0; kk < K; ++kk)
+    for (int r = 0; r < N; ++r) {
+      const size_t o = (size_t)kk * N + r;
+      if (dst[o] != self || bytes[o] == 0) continue;
+      const int64_t rows = bytes[o] / row_bytes;
+      for (int64_t u = 0; u < rows; ++u) {
+        const int64_t p = dest_off[r] + sent[r] + u;
+        if (p >= dest_off[r + 1]) return INVALID_ARGUMENT;
+        const int64_t t = sorted_tok[p];
+        const int c = sorted_slot[p];
+        if (t < 0 || t >= T || c >= k) return INVALID_ARGUMENT;
+        std::memcpy(combined + (t * k + c) * slot_bytes, recv + (got + u) * slot_bytes, (size_t)row_bytes);
+      }
+      sent[r] += rows;
+      got += rows;
+    }
   return OK;
 }
 
