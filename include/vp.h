@@ -5,7 +5,8 @@
  *   (2) an ordered list of channel activations  (Sec. 4.2, Alg. 2),
  *   (3) channel-ordered send buffers            (Sec. 5 "Device-resident buffer layout"),
  * against an offline catalog of contention-free channel families
- * (Sec. 4.1, Alg. 1).
+ * (Sec. 4.1, Alg. 1), and unpacks received buffers into the output layout,
+ * for the dispatch and for the combine that returns the rows.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -182,6 +183,10 @@ size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
  *           steps before k (where step k's slice starts in i's send buffer),
  *           and bytes i sent to pi_k(i) before step k (where the slice starts
  *           in i's stream to that destination)
+ *   recv_src device int32 [k_max, N], may be NULL: the receive view of the
+ *           same steps, recv_src[k, j] = the rank i with pi_k(i) = j (every
+ *           step is a permutation, so each entry below K is written once);
+ *           the unpack calls below take it
  *   tau     device int64 [1]     the quantum used (ns), may be NULL
  * Each iteration scores every catalog shape (Eq. (5)-(6)), binds every family
  * of the best shape with MultiStartAA (Eq. (7)-(8)), evaluates Eq. (9)-(10)
@@ -191,8 +196,8 @@ size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
  * demand reaches 2^42 bytes.  The catalog must have been uploaded. */
 vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_params* p,
                   int32_t* K, int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes,
-                  int64_t* send_off, int64_t* stream_off, int64_t* tau, int32_t* dev_status, void* ws,
-                  size_t ws_bytes, void* stream);
+                  int64_t* send_off, int64_t* stream_off, int32_t* recv_src, int64_t* tau,
+                  int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------- pack */
 
@@ -273,6 +278,76 @@ vp_status vp_pack_prepare_heads(const void* act, int64_t T, int64_t token_stride
 vp_status vp_pack_gather(const void* src, int64_t unit_bytes, int64_t T, int32_t k, const int32_t* K,
                          const int64_t* step_off, int32_t k_max, void* send, int64_t send_capacity,
                          int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------ receive side, combine */
+
+/* Receive slots (Sec. 5 low-latency protocol): every received row starts at a
+ * 128-byte-aligned address; the slot stride is row_bytes rounded up to 128.
+ * Returns 0 for row_bytes < 1. */
+int64_t vp_slot_bytes(int64_t row_bytes);
+
+/* Workspace bytes of vp_unpack_rows, vp_pack_combine and vp_unpack_combine
+ * for a buffer side of `buffer_rows` rows (receive slots, or the combine's
+ * send rows): one int32 row index per row and a small header.  It needs no
+ * clearing.  Returns 0 for a negative count. */
+size_t vp_unpack_workspace(int64_t buffer_rows);
+
+/* D^T (device int64 [N, N], not in place): the demand of the return AlltoAllv
+ * of expert parallelism, whose schedule vp_plan computes like any other. */
+vp_status vp_demand_transpose(const int64_t* demand, int32_t n_ranks, int64_t* demand_t, void* stream);
+
+/* Dispatch receive (Sec. 5 "Device-resident buffer layout": the receive
+ * kernel unpacks straight into the output layout).  Rank self_rank's receive
+ * buffer holds the slices addressed to it, in step order, one row per slot of
+ * vp_slot_bytes(row_bytes); this call writes every row to the expert-major
+ * output:
+ *   recv     device [recv_capacity]    received rows
+ *   counts   device int32 [N, E]       assignments per (source rank, expert),
+ *                                      as vp_demand returns them for R = N
+ *   K, dst, bytes                      the dispatch schedule (device)
+ *   recv_src device int32 [k_max, N]   vp_plan's receive view of it
+ *   out      device [out_capacity]     expert-major output, one row per slot:
+ *                                      local expert m (expert self_rank*E/N+m)
+ *                                      takes the rows of source 0, then source
+ *                                      1, ..., each in token order; the slots
+ *                                      of this rank's own rows (never sent)
+ *                                      are left untouched
+ * row_bytes must be a multiple of 16; the schedule must deliver every source's
+ * stream to this rank whole (the rows of its assignments to this rank's
+ * experts), else VP_ERR_INVALID_ARGUMENT.  A receive buffer or output too
+ * small sets VP_ERR_CAPACITY.  On a device error nothing is copied.  Calls
+ * that share a workspace must not overlap. */
+vp_status vp_unpack_rows(const void* recv, int64_t recv_capacity, int64_t row_bytes, const int32_t* counts,
+                         int32_t E, int32_t self_rank, int32_t n_ranks, const int32_t* K, const int32_t* dst,
+                         const int64_t* bytes, const int32_t* recv_src, int32_t k_max, void* out,
+                         int64_t out_capacity, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
+
+/* Combine send: rank self_rank returns the rows in its expert-major output
+ * (layout of vp_unpack_rows, same counts) to their source ranks.  Stream
+ * self_rank -> i is source i's rows in (expert, token) order; K, dst, bytes
+ * are a schedule planned on the transposed demand.  Slices are appended in
+ * step order as by vp_pack_rows:
+ *   send     device [send_capacity]    output, rows packed at row_bytes
+ *   step_off device int64 [k_max+1]    where step k's slice starts in send;
+ *                                      step_off[K] = total bytes
+ * Errors as for vp_unpack_rows (every stream must be covered whole). */
+vp_status vp_pack_combine(const void* out, int64_t out_capacity, int64_t row_bytes, const int32_t* counts,
+                          int32_t E, int32_t self_rank, int32_t n_ranks, const int32_t* K, const int32_t* dst,
+                          const int64_t* bytes, int32_t k_max, void* send, int64_t send_capacity,
+                          int64_t* step_off, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
+
+/* Combine receive at source rank self_rank: the stream from rank r carries
+ * the rows of this rank's assignments to r's experts, in the (expert, token)
+ * order of its dispatch (sorted_tok, sorted_slot, dest_off from vp_demand);
+ * every received row goes to slot (token * k + routing slot) of
+ *   combined device [T * k, vp_slot_bytes(row_bytes)]
+ * Slots of assignments to this rank's own experts are left untouched.
+ * K, dst, bytes, recv_src: the combine schedule and its receive view. */
+vp_status vp_unpack_combine(const void* recv, int64_t recv_capacity, int64_t row_bytes, int64_t T, int32_t k,
+                            const int32_t* sorted_tok, const uint8_t* sorted_slot, const int64_t* dest_off,
+                            int32_t self_rank, int32_t n_ranks, const int32_t* K, const int32_t* dst,
+                            const int64_t* bytes, const int32_t* recv_src, int32_t k_max, void* combined,
+                            int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
 
 /* --------------------------------------------------------------- helpers */
 

@@ -71,7 +71,7 @@ def lib():
     L.vp_plan_params_default.restype = None
     L.vp_plan_workspace.argtypes = [vp, C.POINTER(PlanParams)]
     L.vp_plan_workspace.restype = sz
-    L.vp_plan.argtypes = [vp, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.vp_plan.argtypes = [vp, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.vp_pack_workspace.argtypes = [i32, i64, i64, i64, i32]
     L.vp_pack_workspace.restype = sz
     L.vp_pack_rows.argtypes = [vp, i64, i32, i64, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, i64, vp, vp,
@@ -83,6 +83,15 @@ def lib():
     L.vp_pack_prepare_heads.argtypes = [vp, i64, i64, vp, i64, i32, i32, vp, vp, vp, vp, vp, i32, i64, vp, vp,
                                         vp, sz, vp]
     L.vp_pack_gather.argtypes = [vp, i64, i64, i32, vp, vp, i32, vp, i64, vp, vp, sz, vp]
+    L.vp_slot_bytes.argtypes = [i64]
+    L.vp_slot_bytes.restype = i64
+    L.vp_unpack_workspace.argtypes = [i64]
+    L.vp_unpack_workspace.restype = sz
+    L.vp_demand_transpose.argtypes = [vp, i32, vp, vp]
+    L.vp_unpack_rows.argtypes = [vp, i64, i64, vp, i32, i32, i32, vp, vp, vp, vp, i32, vp, i64, vp, vp, sz, vp]
+    L.vp_pack_combine.argtypes = [vp, i64, i64, vp, i32, i32, i32, vp, vp, vp, i32, vp, i64, vp, vp, vp, sz, vp]
+    L.vp_unpack_combine.argtypes = [vp, i64, i64, i64, i32, vp, vp, vp, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp,
+                                    sz, vp]
     L.vp_modeled_time.argtypes = [vp, i32, vp, vp, i64, vp, vp]
     L.vp_status_string.argtypes = [C.c_int]
     L.vp_status_string.restype = C.c_char_p
@@ -256,7 +265,8 @@ def plan_workspace_bytes(cat: Catalog, p: PlanParams) -> int:
 
 def alloc_schedule(N: int, k_max: int, device="cuda", layout: bool = False) -> dict:
     """Schedule buffers; with `layout` also the planner's per-rank send and
-    stream offsets (the buffer layout the pack can use directly)."""
+    stream offsets (the buffer layout the pack can use directly) and its
+    receive view (the rank whose lane lands at each rank, for the unpack)."""
     s = dict(K=torch.zeros(1, dtype=torch.int32, device=device),
              family=torch.empty(k_max, dtype=torch.int32, device=device),
              dst=torch.empty((k_max, N), dtype=torch.int32, device=device),
@@ -266,6 +276,7 @@ def alloc_schedule(N: int, k_max: int, device="cuda", layout: bool = False) -> d
     if layout:
         s["send_off"] = torch.empty((k_max, N), dtype=torch.int64, device=device)
         s["stream_off"] = torch.empty((k_max, N), dtype=torch.int64, device=device)
+        s["recv_src"] = torch.empty((k_max, N), dtype=torch.int32, device=device)
     return s
 
 
@@ -284,7 +295,8 @@ def plan(cat: Catalog, D: torch.Tensor, p: PlanParams, status: Optional[torch.Te
         ws = torch.empty(plan_workspace_bytes(cat, p), dtype=torch.uint8, device=D.device)
     _check(lib().vp_plan(cat.handle, _ptr(D), C.byref(p), _ptr(out["K"]), _ptr(out["family"]),
                          _ptr(out["dst"]), _ptr(out["inst"]), _ptr(out["bytes"]), _ptr(out.get("send_off")),
-                         _ptr(out.get("stream_off")), _ptr(out["tau"]), _ptr(status), _ptr(ws), ws.numel(),
+                         _ptr(out.get("stream_off")), _ptr(out.get("recv_src")), _ptr(out["tau"]), _ptr(status),
+                         _ptr(ws), ws.numel(),
                          _stream(stream)), "vp_plan")
     out["status"] = status
     return out
@@ -347,6 +359,79 @@ def pack_heads(act: torch.Tensor, token_stride: int, head_lo: torch.Tensor, head
                                _ptr(sched.get("send_off")), _ptr(sched.get("stream_off")), k_max,
                                _ptr(send), cap, _ptr(step_off), _ptr(status), _ptr(ws), ws.numel(),
                                _stream(stream)), "vp_pack_heads")
+
+
+# ------------------------------------------------ receive side, combine
+
+def slot_bytes(row_bytes: int) -> int:
+    """Receive-slot stride: the row rounded up to 128 bytes."""
+    return int(lib().vp_slot_bytes(row_bytes))
+
+
+def unpack_workspace_bytes(buffer_rows: int) -> int:
+    return int(lib().vp_unpack_workspace(buffer_rows))
+
+
+def demand_transpose(D: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """vp_demand_transpose: the combine's demand D^T."""
+    _dev(D, torch.int64, "demand")
+    N = D.shape[0]
+    if out is None:
+        out = torch.empty_like(D)
+    _check(lib().vp_demand_transpose(_ptr(D), N, _ptr(out), _stream(stream)), "vp_demand_transpose")
+    return out
+
+
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
+def unpack_rows(recv: torch.Tensor, row_bytes: int, counts: torch.Tensor, self_rank: int, sched: dict,
+                out: torch.Tensor, status: torch.Tensor, ws: Optional[torch.Tensor] = None, stream=None):
+    """vp_unpack_rows: rank self_rank's receive slots into its expert-major output."""
+    _dev(counts, torch.int32, "counts")
+    N, E = counts.shape
+    k_max = sched["dst"].shape[0]
+    cap = _nbytes(recv)
+    if ws is None:
+        ws = torch.empty(unpack_workspace_bytes(cap // slot_bytes(row_bytes)), dtype=torch.uint8, device=recv.device)
+    _check(lib().vp_unpack_rows(_ptr(recv), cap, row_bytes, _ptr(counts), E, self_rank, N, _ptr(sched["K"]),
+                                _ptr(sched["dst"]), _ptr(sched["bytes"]), _ptr(sched["recv_src"]), k_max,
+                                _ptr(out), _nbytes(out), _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
+           "vp_unpack_rows")
+
+
+def pack_combine(out: torch.Tensor, row_bytes: int, counts: torch.Tensor, self_rank: int, sched: dict,
+                 send: torch.Tensor, step_off: torch.Tensor, status: torch.Tensor, ws: Optional[torch.Tensor] = None,
+                 stream=None):
+    """vp_pack_combine: expert-major rows back to their sources in the combine schedule's order."""
+    _dev(counts, torch.int32, "counts")
+    N, E = counts.shape
+    k_max = sched["dst"].shape[0]
+    cap = _nbytes(send)
+    if ws is None:
+        ws = torch.empty(unpack_workspace_bytes(cap // row_bytes), dtype=torch.uint8, device=send.device)
+    _check(lib().vp_pack_combine(_ptr(out), _nbytes(out), row_bytes, _ptr(counts), E, self_rank, N,
+                                 _ptr(sched["K"]), _ptr(sched["dst"]), _ptr(sched["bytes"]), k_max, _ptr(send), cap,
+                                 _ptr(step_off), _ptr(status), _ptr(ws), ws.numel(), _stream(stream)),
+           "vp_pack_combine")
+
+
+def unpack_combine(recv: torch.Tensor, row_bytes: int, T: int, k: int, sorted_tok: torch.Tensor,
+                   sorted_slot: torch.Tensor, dest_off: torch.Tensor, self_rank: int, sched: dict,
+                   combined: torch.Tensor, status: torch.Tensor, ws: Optional[torch.Tensor] = None, stream=None):
+    """vp_unpack_combine: returned rows into combined [T * k, slot] at (token, routing slot)."""
+    N = sched["dst"].shape[1]
+    k_max = sched["dst"].shape[0]
+    if _nbytes(combined) < T * k * slot_bytes(row_bytes):
+        raise ValueError("combined must hold T * k slots")
+    cap = _nbytes(recv)
+    if ws is None:
+        ws = torch.empty(unpack_workspace_bytes(cap // slot_bytes(row_bytes)), dtype=torch.uint8, device=recv.device)
+    _check(lib().vp_unpack_combine(_ptr(recv), cap, row_bytes, T, k, _ptr(sorted_tok), _ptr(sorted_slot),
+                                   _ptr(dest_off), self_rank, N, _ptr(sched["K"]), _ptr(sched["dst"]),
+                                   _ptr(sched["bytes"]), _ptr(sched["recv_src"]), k_max, _ptr(combined),
+                                   _ptr(status), _ptr(ws), ws.numel(), _stream(stream)), "vp_unpack_combine")
 
 
 # -------------------------------------------------------------- pipeline
@@ -414,7 +499,8 @@ class Pipeline:
         _check(lib().vp_plan(self.cat.handle, _ptr(self.dem["demand"]), C.byref(p), _ptr(self.sched["K"]),
                              _ptr(self.sched["family"]), _ptr(self.sched["dst"]), _ptr(self.sched["inst"]),
                              _ptr(self.sched["bytes"]), _ptr(self.sched["send_off"]),
-                             _ptr(self.sched["stream_off"]), _ptr(self.sched["tau"]), _ptr(self.status),
+                             _ptr(self.sched["stream_off"]), _ptr(self.sched["recv_src"]), _ptr(self.sched["tau"]),
+                             _ptr(self.status),
                              _ptr(self.plan_ws), self.plan_ws.numel(), _stream(stream)), "vp_plan")
 
     def pack_prepare_stage(self, tokens: torch.Tensor, head_lo: Optional[torch.Tensor] = None, stream=None):

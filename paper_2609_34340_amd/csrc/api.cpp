@@ -211,8 +211,8 @@ size_t vp_plan_workspace(const vp_catalog* c, const vp_plan_params* p) {
 
 vp_status vp_plan(const vp_catalog* c, const int64_t* demand, const vp_plan_params* p, int32_t* K,
                   int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes, int64_t* send_off,
-                  int64_t* stream_off, int64_t* tau, int32_t* dev_status, void* ws, size_t ws_bytes,
-                  void* stream) {
+                  int64_t* stream_off, int32_t* recv_src, int64_t* tau, int32_t* dev_status, void* ws,
+                  size_t ws_bytes, void* stream) {
   if (!c || !demand || !p || !K || !family || !dst || !inst || !bytes || !dev_status)
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
   if ((send_off == nullptr) != (stream_off == nullptr))
@@ -227,7 +227,7 @@ vp_status vp_plan(const vp_catalog* c, const int64_t* demand, const vp_plan_para
   if (p->lambda_ns > (int64_t(1) << 40) || p->k_target > (int64_t(1) << 40))
     return set_error(VP_ERR_UNSUPPORTED, "lambda or k_target too large");
   if (ws_bytes < vp_plan_workspace(c, p) || !ws) return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
-  vp::PlanLaunch a{c, demand, (int64_t*)ws, *p, K, family, dst, inst, bytes, tau, send_off, stream_off, dev_status};
+  vp::PlanLaunch a{c, demand, (int64_t*)ws, *p, K, family, dst, inst, bytes, tau, send_off, stream_off, recv_src, dev_status};
   return vp::launch_plan(a, stream);
 }
 
@@ -347,6 +347,99 @@ vp_status vp_pack_gather(const void* src, int64_t unit_bytes, int64_t T, int32_t
                    K, nullptr, nullptr, nullptr, nullptr, k_max, send, send_capacity,
                    const_cast<int64_t*>(step_off), dev_status, ws, ws_bytes};
   return vp::launch_pack(a, stream);
+}
+
+int64_t vp_slot_bytes(int64_t row_bytes) { return row_bytes < 1 ? 0 : vp::slot_bytes(row_bytes); }
+
+size_t vp_unpack_workspace(int64_t buffer_rows) {
+  if (buffer_rows < 0) return 0;
+  return vp::unpack_workspace(buffer_rows);
+}
+
+vp_status vp_demand_transpose(const int64_t* demand, int32_t n_ranks, int64_t* demand_t, void* stream) {
+  if (!demand || !demand_t || n_ranks < 1 || n_ranks > vp::kMaxRanks || demand == demand_t)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "bad transpose arguments");
+  return vp::launch_transpose(demand, n_ranks, demand_t, stream);
+}
+
+namespace {
+
+// Checks shared by the three receive-side / combine calls.
+vp_status check_unpack(int64_t row_bytes, int32_t self_rank, int32_t n_ranks, const int32_t* K, const int32_t* dst,
+                       const int64_t* bytes, int32_t k_max, int64_t rows_cap, int64_t map_cap,
+                       const int32_t* dev_status, const void* ws, size_t ws_bytes) {
+  if (row_bytes < 16 || row_bytes % 16 != 0 || n_ranks < 1 || n_ranks > vp::kMaxRanks || self_rank < 0 ||
+      self_rank >= n_ranks || k_max < 1 || rows_cap < 0 || map_cap < 0)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "bad unpack sizes (row_bytes must be a multiple of 16)");
+  if (rows_cap >= (int64_t(1) << 31) || map_cap >= (int64_t(1) << 31))
+    return set_error(VP_ERR_UNSUPPORTED, "more than 2^31 rows");
+  if (!K || !dst || !bytes || !dev_status) return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
+  if (ws_bytes < vp::unpack_workspace(rows_cap) || !ws) return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
+  return VP_OK;
+}
+
+}  // namespace
+
+vp_status vp_unpack_rows(const void* recv, int64_t recv_capacity, int64_t row_bytes, const int32_t* counts,
+                         int32_t E, int32_t self_rank, int32_t n_ranks, const int32_t* K, const int32_t* dst,
+                         const int64_t* bytes, const int32_t* recv_src, int32_t k_max, void* out,
+                         int64_t out_capacity, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
+  const int64_t sb = vp::slot_bytes(row_bytes);
+  if (recv_capacity < 0 || out_capacity < 0 || E < 1 || n_ranks < 1 || E % n_ranks != 0 || E > 4096)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "bad unpack sizes (E a multiple of N, <= 4096)");
+  const int64_t rows_cap = recv_capacity / sb, map_cap = out_capacity / sb;
+  vp_status st = check_unpack(row_bytes, self_rank, n_ranks, K, dst, bytes, k_max, rows_cap, map_cap, dev_status,
+                              ws, ws_bytes);
+  if (st != VP_OK) return st;
+  if (!counts || !recv_src || (rows_cap > 0 && (!recv || !out)))
+    return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
+  if (vp::unpack_lds_bytes(vp::kModeDispatchUnpack, n_ranks, E / n_ranks) > 64 * 1024)
+    return set_error(VP_ERR_UNSUPPORTED, "too many ranks or local experts for the row map");
+  vp::UnpackLaunch a{vp::kModeDispatchUnpack, recv, sb, out, sb, row_bytes, rows_cap, map_cap, self_rank, n_ranks,
+                     k_max, E, 0, 0, K, dst, recv_src, bytes, counts, nullptr, nullptr, nullptr, nullptr,
+                     dev_status, ws, ws_bytes};
+  return vp::launch_unpack(a, stream);
+}
+
+vp_status vp_pack_combine(const void* out, int64_t out_capacity, int64_t row_bytes, const int32_t* counts,
+                          int32_t E, int32_t self_rank, int32_t n_ranks, const int32_t* K, const int32_t* dst,
+                          const int64_t* bytes, int32_t k_max, void* send, int64_t send_capacity,
+                          int64_t* step_off, int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
+  const int64_t sb = vp::slot_bytes(row_bytes);
+  if (send_capacity < 0 || out_capacity < 0 || E < 1 || n_ranks < 1 || E % n_ranks != 0 || E > 4096)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "bad combine sizes (E a multiple of N, <= 4096)");
+  const int64_t rows_cap = send_capacity / row_bytes, map_cap = out_capacity / sb;
+  vp_status st = check_unpack(row_bytes, self_rank, n_ranks, K, dst, bytes, k_max, rows_cap, map_cap, dev_status,
+                              ws, ws_bytes);
+  if (st != VP_OK) return st;
+  if (!counts || !step_off || (rows_cap > 0 && (!out || !send)))
+    return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
+  if (vp::unpack_lds_bytes(vp::kModeCombinePack, n_ranks, E / n_ranks) > 64 * 1024)
+    return set_error(VP_ERR_UNSUPPORTED, "too many ranks or local experts for the row map");
+  vp::UnpackLaunch a{vp::kModeCombinePack, out, sb, send, row_bytes, row_bytes, rows_cap, map_cap, self_rank,
+                     n_ranks, k_max, E, 0, 0, K, dst, nullptr, bytes, counts, nullptr, nullptr, nullptr, step_off,
+                     dev_status, ws, ws_bytes};
+  return vp::launch_unpack(a, stream);
+}
+
+vp_status vp_unpack_combine(const void* recv, int64_t recv_capacity, int64_t row_bytes, int64_t T, int32_t k,
+                            const int32_t* sorted_tok, const uint8_t* sorted_slot, const int64_t* dest_off,
+                            int32_t self_rank, int32_t n_ranks, const int32_t* K, const int32_t* dst,
+                            const int64_t* bytes, const int32_t* recv_src, int32_t k_max, void* combined,
+                            int32_t* dev_status, void* ws, size_t ws_bytes, void* stream) {
+  const int64_t sb = vp::slot_bytes(row_bytes);
+  if (recv_capacity < 0 || T < 0 || k < 1 || k > 255)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "bad combine sizes (k <= 255)");
+  const int64_t rows_cap = recv_capacity / sb, map_cap = T * k;
+  vp_status st = check_unpack(row_bytes, self_rank, n_ranks, K, dst, bytes, k_max, rows_cap, map_cap, dev_status,
+                              ws, ws_bytes);
+  if (st != VP_OK) return st;
+  if (!dest_off || !recv_src || (rows_cap > 0 && !recv) || (map_cap > 0 && (!sorted_tok || !sorted_slot || !combined)))
+    return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
+  vp::UnpackLaunch a{vp::kModeCombineUnpack, recv, sb, combined, sb, row_bytes, rows_cap, map_cap, self_rank,
+                     n_ranks, k_max, n_ranks, k, T, K, dst, recv_src, bytes, nullptr, sorted_tok, sorted_slot,
+                     dest_off, nullptr, dev_status, ws, ws_bytes};
+  return vp::launch_unpack(a, stream);
 }
 
 vp_status vp_modeled_time(const vp_catalog* c, int32_t K, const int32_t* inst, const int64_t* bytes,

@@ -84,6 +84,7 @@ struct PlanLaunch {
   int32_t *K, *family, *dst, *inst;
   int64_t *bytes, *tau;
   int64_t *send_off, *stream_off;
+  int32_t* recv_src;
   int32_t* status;
 };
 vp_status launch_plan(const PlanLaunch& a, void* stream);
@@ -134,5 +135,36 @@ struct PackLaunch {
 };
 size_t pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit, int64_t T, int32_t k);
 vp_status launch_pack(const PackLaunch& a, void* stream);
+
+// Receive side and combine direction.  The buffer side holds rows in step
+// order (receive slots, or the combine's send rows); the mapped side is the
+// expert-major output or the [T, k] combine output.
+enum { kModeDispatchUnpack = 0, kModeCombinePack = 1, kModeCombineUnpack = 2 };
+struct UnpackLaunch {
+  int mode;
+  const void* src;
+  int64_t src_stride;
+  void* dst_buf;
+  int64_t dst_stride;
+  int64_t row_bytes;
+  int64_t rows_cap, map_cap;
+  int32_t self_rank, N, k_max, E, k;
+  int64_t T;
+  const int32_t *K, *dst, *recv_src;
+  const int64_t* bytes;
+  const int32_t* counts;
+  const int32_t* sorted_tok;
+  const uint8_t* sorted_slot;
+  const int64_t* dest_off;
+  int64_t* step_off;
+  int32_t* status;
+  void* ws;
+  size_t ws_bytes;
+};
+int64_t slot_bytes(int64_t row_bytes);
+size_t unpack_workspace(int64_t rows);
+size_t unpack_lds_bytes(int mode, int32_t N, int32_t eloc);
+vp_status launch_unpack(const UnpackLaunch& a, void* stream);
+vp_status launch_transpose(const int64_t* D, int32_t N, int64_t* DT, void* stream);
 
 }  // namespace vp

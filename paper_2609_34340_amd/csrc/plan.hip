@@ -69,6 +69,7 @@ struct PlanArgs {
   int32_t *K, *family, *dst, *inst;
   int64_t *bytes, *tau;
   int64_t *send_off, *stream_off;   // optional [k_max][N] buffer layout per rank
+  int32_t* recv_src;                // optional [k_max][N]: the rank whose lane lands at each rank
   int32_t* status;
   // LDS layout (byte offsets)
   int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo, o_finl;
@@ -951,6 +952,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         P.dst[o] = j;
         P.inst[o] = d_id(w);
         P.bytes[o] = x;
+        if (P.recv_src) P.recv_src[(size_t)K * N + j] = i;   // pi_k is a permutation
         if (P.send_off) {
           // Sec. 5 buffer layout: where this lane's slice sits in rank i's
           // send buffer and in its stream to j (bytes sent there before)
@@ -1090,6 +1092,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   P.tau = a.tau;
   P.send_off = a.send_off;
   P.stream_off = a.stream_off;
+  P.recv_src = a.recv_src;
   P.status = a.status;
 
   size_t o = 0;
