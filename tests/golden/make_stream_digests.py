@@ -1,0 +1,70 @@
+#!/usr/bin/env python3
+"""Write stream_digests.json: the oracle's demand, schedule and rank-0 pack
+digests for every checked matrix of the 64-rank and 256-rank demand streams.
+
+Only the oracle and the seeded input generators are called.  Runs one worker
+process per matrix batch (about 3 minutes on 8 cores).
+
+    python tests/golden/make_stream_digests.py [--jobs 8]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import multiprocessing as mp
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+import numpy as np  # noqa: E402
+
+import stream_digest as sd  # noqa: E402
+
+_tok = {}
+
+
+def oracle_job(args):
+    import oracle
+    import vpgen
+    cid, m = args
+    w = vpgen.config(cid)
+    if cid not in _tok:
+        _tok[cid] = (vpgen.tokens_bf16(w, 0), oracle.Catalog(w.topo))
+    tok, cat = _tok[cid]
+    R = vpgen.routing_all(w, m)
+    dem = [oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes) for i in range(w.n_ranks)]
+    D = np.stack([d["row"] for d in dem])
+    s = cat.plan(D, w.row_bytes)
+    send, off = oracle.pack_rows(tok, w.row_bytes, dem[0]["sorted_tok"], dem[0]["dest_off"], 0, s)
+    return dict(matrix=m, K=int(s["K"]), tau=int(s["tau"]), demand=sd.demand_digest(D),
+                schedule=sd.schedule_digest(s), send_bytes=int(send.size),
+                send=sd.send_digest(sd.send_sample(send), send.size), step_off=sd.step_off_digest(off))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--jobs", type=int, default=8)
+    args = ap.parse_args()
+    import oracle
+    import vpgen
+    oracle.build()
+    out = {"sample_stride": sd.SAMPLE_STRIDE, "streams": {}}
+    ctx = mp.get_context("spawn")
+    for cid, mats in sd.STREAMS.items():
+        t0 = time.time()
+        with ctx.Pool(args.jobs) as pool:
+            rows = pool.map(oracle_job, [(cid, m) for m in mats], chunksize=1)
+        out["streams"][str(cid)] = {"workload": vpgen.config(cid).name, "matrices": rows}
+        print("C%d: %d matrices in %.0f s" % (cid, len(rows), time.time() - t0), flush=True)
+    with open(sd.GOLDEN, "w") as f:
+        json.dump(out, f, indent=0)
+        f.write("\n")
+    print("wrote", sd.GOLDEN)
+
+
+if __name__ == "__main__":
+    main()

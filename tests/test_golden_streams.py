@@ -1,0 +1,41 @@
+"""The stored stream digests agree with the oracle as it stands: the demand
+and schedule digests of the first and last matrix of the 64-rank stream and of
+the first matrix of the 256-rank stream are recomputed here (the full streams
+and the send-buffer digests are rebuilt by golden/make_stream_digests.py)."""
+import json
+
+import numpy as np
+import pytest
+
+import oracle
+import stream_digest as sd
+import vpgen
+
+
+@pytest.fixture(scope="module")
+def golden():
+    with open(sd.GOLDEN) as f:
+        return json.load(f)
+
+
+def test_streams_cover_the_checked_matrices(golden):
+    for cid, mats in sd.STREAMS.items():
+        rows = golden["streams"][str(cid)]["matrices"]
+        assert [r["matrix"] for r in rows] == mats
+        assert golden["streams"][str(cid)]["workload"] == vpgen.config(cid).name
+        # the plan drains every matrix in at least N - 1 steps and within K_max = 8N
+        N = vpgen.config(cid).n_ranks
+        assert all(N - 1 <= r["K"] <= 8 * N for r in rows)
+
+
+@pytest.mark.parametrize("cid,m", [(3, 0), (3, 99), (5, 0)])
+def test_stream_digest_matches_oracle(golden, cid, m):
+    w = vpgen.config(cid)
+    ref = {r["matrix"]: r for r in golden["streams"][str(cid)]["matrices"]}[m]
+    R = vpgen.routing_all(w, m)
+    D = np.stack([oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes)["row"] for i in range(w.n_ranks)])
+    assert sd.demand_digest(D) == ref["demand"]
+    s = oracle.Catalog(w.topo).plan(D, w.row_bytes)
+    assert s["K"] == ref["K"] and s["tau"] == ref["tau"]
+    assert sd.schedule_digest(s) == ref["schedule"]
+    assert int(s["bytes"][:, 0].sum()) == ref["send_bytes"]

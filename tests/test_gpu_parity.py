@@ -324,6 +324,34 @@ def test_pack_rows_parity_full_size(vp, cid, self_rank, layout):
     assert np.array_equal(step_off[:s["K"] + 1].cpu().numpy(), ref_off)
 
 
+@pytest.mark.parametrize("row_bytes,cid", [(16, 1), (1040, 1), (4112, 2), (12304, 1), (36880, 1), (65536, 1)])
+def test_pack_rows_parity_row_sizes(vp, row_bytes, cid):
+    """Rows of one vector, ragged last passes, several rows per workgroup
+    (top-2 and top-8), and rows past the in-register limit of the scatter,
+    which are copied in chunks."""
+    w = vpgen.config(cid)
+    T = 512
+    R = vpgen.routing_all(w, 0, T)
+    log("pack rows parity C%d T=%d row %d" % (cid, T, row_bytes))
+    dem = [oracle.demand(R[i], w.n_ranks, w.experts, i, row_bytes) for i in range(w.n_ranks)]
+    D = np.stack([d["row"] for d in dem])
+    s = ocat(w.topo).plan(D, row_bytes)
+    tok = np.random.default_rng(row_bytes).integers(0, 256, (T, row_bytes), dtype=np.uint8)
+    ref, ref_off = oracle.pack_rows(tok, row_bytes, dem[0]["sorted_tok"], dem[0]["dest_off"], 0, s)
+    rt = torch.from_numpy(R).cuda()
+    d = vp.demand(rt, w.n_ranks, w.experts, row_bytes, sort_row=0)
+    sched = upload_schedule(vp, w.n_ranks, s, False)
+    send = torch.full((ref.size + 64,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
+    vp.pack_rows(torch.from_numpy(tok).cuda(), row_bytes, d["sorted_tok"], d["sorted_slot"], d["dest_off"], 0,
+                 sched, send[:ref.size], step_off, d["status"])
+    torch.cuda.synchronize()
+    assert vp.read_status(d["status"]) == 0
+    assert torch.equal(send[:ref.size], torch.from_numpy(ref).cuda())
+    assert (send[ref.size:] == 0xA5).all(), "wrote past the packed bytes"
+    assert np.array_equal(step_off[:s["K"] + 1].cpu().numpy(), ref_off)
+
+
 @pytest.mark.parametrize("layout", [False, True])
 def test_pack_rows_capacity_error_writes_nothing(vp, layout):
     w, R, dem, D = moe_case(1)
