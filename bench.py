@@ -7,6 +7,7 @@ experts holding half of the per-draw mass, hot set redrawn per matrix):
 
   vp_demand   all 256 ranks' routing -> the 256 x 256 byte-demand matrix
               (+ rank 0's (expert, token) order and offsets)
+  vp_control_words  the sparse expert-parallel control word of every pair
   vp_plan     Alg. 2 on that matrix against the node-circulant catalog
   vp_pack     rank 0's token rows into channel-ordered send slices
 
@@ -111,15 +112,18 @@ def measure(w, steps, warmup, M, dev):
         pipe.demand_stage(routing[m], head_lo)
         if ev is not None:
             ev[1].record()
-        pipe.plan_stage()
+        pipe.words_stage()
         if ev is not None:
             ev[2].record()
-        pipe.pack_prepare_stage(tokens, head_lo)
+        pipe.plan_stage()
         if ev is not None:
             ev[3].record()
-        pipe.pack_gather_stage(tokens, sends[step % 2])
+        pipe.pack_prepare_stage(tokens, head_lo)
         if ev is not None:
             ev[4].record()
+        pipe.pack_gather_stage(tokens, sends[step % 2])
+        if ev is not None:
+            ev[5].record()
 
     for s in range(warmup):
         run(s)
@@ -127,7 +131,7 @@ def measure(w, steps, warmup, M, dev):
     if vp.read_status(pipe.status) != 0:
         raise SystemExit("device error during warmup: %d" % vp.read_status(pipe.status))
 
-    evs = [[E() for _ in range(5)] for _ in range(steps)]
+    evs = [[E() for _ in range(6)] for _ in range(steps)]
     start, end = E(), E()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -141,9 +145,10 @@ def measure(w, steps, warmup, M, dev):
         raise SystemExit("device error in the timed region: %d" % vp.read_status(pipe.status))
     r = dict(total_ms=start.elapsed_time(end), wall=wall,
              demand_ms=np.array([e[0].elapsed_time(e[1]) for e in evs]),
-             plan_ms=np.array([e[1].elapsed_time(e[2]) for e in evs]),
-             prep_ms=np.array([e[2].elapsed_time(e[3]) for e in evs]),
-             gather_ms=np.array([e[3].elapsed_time(e[4]) for e in evs]))
+             words_ms=np.array([e[1].elapsed_time(e[2]) for e in evs]),
+             plan_ms=np.array([e[2].elapsed_time(e[3]) for e in evs]),
+             prep_ms=np.array([e[3].elapsed_time(e[4]) for e in evs]),
+             gather_ms=np.array([e[4].elapsed_time(e[5]) for e in evs]))
 
     # schedule facts per matrix (untimed): K, slices, modeled completion time
     Ks, slices, That = [], [], []
@@ -182,6 +187,7 @@ def summary(w, r):
             "modeled_T_ms": round(float(r["That_ms"].mean()), 3),
             "plan_over_modeled_T": round(plan_us / (1e3 * float(r["That_ms"].mean())), 5),
             "demand_us": round(float(r["demand_ms"].mean() * 1e3), 1),
+            "control_words_us": round(float(r["words_ms"].mean() * 1e3), 1) if w.mode == "moe" else None,
             "pack_us": round(float(r["pack_ms"].mean() * 1e3), 1),
             "pack_GBps": round(value, 2), "pack_pct_of_peak": round(100 * value / PEAK_HBM_GBS, 2),
             "pack_bytes_MB": round(float(r["pack_bytes"].mean()) / 1e6, 2)}
@@ -257,6 +263,7 @@ def main():
         "plan_us_per_matrix": head["plan_us_per_matrix"],
         "plan_us_per_activation": head["plan_us_per_activation"],
         "demand_us": head["demand_us"],
+        "control_words_us": head["control_words_us"],
         "pack_us": head["pack_us"],
         "activations_K": head["activations_K"],
         "modeled_T_ms": head["modeled_T_ms"],

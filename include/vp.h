@@ -119,6 +119,28 @@ vp_status vp_catalog_shapes(const vp_catalog* cat, int32_t* k, int32_t* fam_begi
  * and the Q*g node-local instance ids of each family, ascending. */
 vp_status vp_catalog_families(const vp_catalog* cat, int32_t* shape, int32_t* k, int32_t* ids);
 
+/* Compact serialized catalog (Table 4 sizes the catalog tree by such a
+ * payload): the topology and the node-local instance ids of every family,
+ * little-endian, with a 64-bit FNV-1a hash at the end; see vp_catalog_load.
+ * With buf == NULL, *size receives the byte count and nothing else happens;
+ * otherwise `buf` (host, `capacity` bytes, caller-owned) receives the payload
+ * and *size its length, or VP_ERR_CAPACITY when capacity is too small.  Host
+ * only. */
+vp_status vp_catalog_save(const vp_catalog* cat, void* buf, size_t capacity, size_t* size);
+
+/* A new catalog handle from a payload written by vp_catalog_save (host
+ * memory, `size` bytes), without running Alg. 1 again.  Everything Alg. 1
+ * guarantees is checked: the hash, the topology limits, and for every family
+ * that it is a complete (g lanes out of and into every switch slot),
+ * resource-disjoint set of instances that PrunePaths keeps (Eq. (1),
+ * Eq. (4)), identical PIX copies in copy order, a NIC lane in every
+ * shifted-node family, and strictly increasing canonical order.  A subset of
+ * the families Alg. 1 finds is accepted (a restricted catalog; the planner
+ * then reports VP_ERR_NO_PROGRESS for demand no family can serve).  Any
+ * failure returns VP_ERR_INVALID_ARGUMENT (VP_ERR_UNSUPPORTED for topology
+ * limits) and leaves *out NULL.  Free the handle with vp_catalog_free. */
+vp_status vp_catalog_load(const void* buf, size_t size, vp_catalog** out);
+
 /* Copy the catalog to the current device once (synchronous on `stream`);
  * the device copy belongs to the handle.  Needed before vp_plan. */
 vp_status vp_catalog_upload(vp_catalog* cat, void* stream);
@@ -162,6 +184,37 @@ vp_status vp_demand(const int32_t* routing, int32_t R, int64_t T, int32_t k, int
 vp_status vp_demand_heads(int64_t T, const int64_t* head_lo, int64_t head_bytes, int32_t n_ranks,
                           int32_t first_rank, int32_t R, int64_t* demand, int32_t* dev_status,
                           void* stream);
+
+/* Sparse expert-parallel control words (Sec. 5 "Efficient sparse data
+ * movement for expert parallelism").  Rank j hosts L = E/N local experts
+ * (experts j*L .. j*L+L-1).  For each of R source ranks
+ * first_rank .. first_rank+R-1 and every destination j:
+ *   counts device int32 [R, E]    per-expert row counts (as vp_demand writes)
+ *   words  device uint32 [R, N]   bit l (l < L) set when the source sends at
+ *                                 least one row to local expert l of rank j;
+ *                                 bits L..31 hold the exact row count of the
+ *                                 designated expert, the highest active one
+ *                                 (its payload ends the pair's expert-
+ *                                 ascending stream, the word follows it).
+ *                                 0 for the self pair and for pairs with no
+ *                                 rows: no transfer and no wait.
+ * L <= 31, else VP_ERR_UNSUPPORTED.  A designated count that does not fit in
+ * 32 - L bits sets VP_ERR_CAPACITY, a negative count VP_ERR_INVALID_ARGUMENT,
+ * in dev_status (that pair's word is then 0). */
+vp_status vp_control_words(const int32_t* counts, int32_t R, int32_t E, int32_t n_ranks, int32_t first_rank,
+                           uint32_t* words, int32_t* dev_status, void* stream);
+
+/* The receiver's decode of the same words (Sec. 5): rank r holds the word of
+ * every source i at words[i * word_stride] (device uint32; word_stride = 1
+ * for a gathered vector, N for column r of vp_control_words' output) and the
+ * per-expert signal counts signal[i][l] (device int32 [N, L]), which are read
+ * only for active experts other than the designated one.  Writes
+ *   counts device int32 [N, L]: rows from source i for local expert l
+ *   (0 where the bitmap bit is clear, the word's count for the designated
+ *   expert, the signal's otherwise).
+ * 1 <= n_local <= 31. */
+vp_status vp_receive_counts(const uint32_t* words, int64_t word_stride, const int32_t* signal, int32_t n_ranks,
+                            int32_t n_local, int32_t* counts, void* stream);
 
 /* ------------------------------------------------------------------- plan */
 

@@ -68,6 +68,8 @@ def lib():
         L.orc_demand.argtypes = [vp, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                  C.c_int64, vp, vp, vp, vp, vp]
         L.orc_demand_heads.argtypes = [C.c_int64, vp, C.c_int64, C.c_int32, C.c_int32, vp]
+        L.orc_control_words.argtypes = [vp, C.c_int32, C.c_int32, C.c_int32, vp]
+        L.orc_receive_counts.argtypes = [vp, vp, C.c_int32, C.c_int32, vp]
         L.orc_plan.argtypes = [vp, vp, C.POINTER(_Params), C.c_int32, vp, vp, vp, vp, vp, vp,
                                vp, C.c_int64, vp]
         L.orc_splitmix_stream.argtypes = [C.c_uint64, vp, C.c_int32, vp]
@@ -229,6 +231,31 @@ def demand(routing: np.ndarray, n_ranks: int, n_experts: int, self_rank: int, un
     if st != OK:
         raise OracleError(st, "orc_demand")
     return dict(row=row, counts=counts, sorted_tok=order, sorted_slot=slot, dest_off=off)
+
+
+def control_words(counts: np.ndarray, n_ranks: int, self_rank: int) -> np.ndarray:
+    """One source rank's sparse-EP control words (uint32 [N]) from its expert
+    counts (int32 [E])."""
+    c = np.ascontiguousarray(counts, dtype=np.int32)
+    words = np.zeros(n_ranks, np.uint32)
+    st = lib().orc_control_words(_p(c), c.shape[0], n_ranks, self_rank, _p(words))
+    if st != OK:
+        raise OracleError(st, "orc_control_words")
+    return words
+
+
+def receive_counts(words: np.ndarray, signal: np.ndarray, n_local: int) -> np.ndarray:
+    """A receiver's rows per (source, local expert) (int32 [N, L]) from the
+    control words it received (uint32 [N]) and the per-expert signal counts
+    (int32 [N, L]; read only for active, non-designated experts)."""
+    w = np.ascontiguousarray(words, dtype=np.uint32)
+    sg = np.ascontiguousarray(signal, dtype=np.int32)
+    N = w.shape[0]
+    out = np.zeros((N, n_local), np.int32)
+    st = lib().orc_receive_counts(_p(w), _p(sg), N, n_local, _p(out))
+    if st != OK:
+        raise OracleError(st, "orc_receive_counts")
+    return out
 
 
 def demand_heads(tokens: int, head_lo: np.ndarray, head_bytes: int, self_rank: int):

@@ -947,6 +947,64 @@ int orc_demand(const int32_t* routing, int64_t T, int32_t k, int32_t E, int32_t 
   return OK;
 }
 
+// Sparse expert-parallel control words (Sec. 5, efficient sparse data
+// movement for expert parallelism), one source rank's row.  Destination j
+// hosts L = E/N local experts (experts j*L .. j*L+L-1).  For an active pair
+// the 32-bit word has bit l set when the source sends at least one row to
+// local expert l, and the bits above the L bitmap bits hold the exact row
+// count of the designated expert.  Reading: the designated expert is the
+// highest active one, because the pair's stream runs expert-ascending and
+// the word travels right after that expert's payload.  Pairs with no rows
+// and the self pair get no word (0).
+int orc_control_words(const int32_t* counts, int32_t E, int32_t N, int32_t self, uint32_t* words) {
+  if (N < 1 || E < N || E % N != 0 || self < 0 || self >= N) return INVALID_ARGUMENT;
+  const int L = E / N;
+  if (L > 31) return UNSUPPORTED;
+  for (int j = 0; j < N; ++j) {
+    words[j] = 0;
+    if (j == self) continue;
+    uint32_t bitmap = 0;
+    int designated = -1;
+    for (int l = 0; l < L; ++l) {
+      const int32_t c = counts[j * L + l];
+      if (c < 0) return INVALID_ARGUMENT;
+      if (c > 0) {
+        bitmap |= 1u << l;
+        designated = l;
+      }
+    }
+    if (designated < 0) continue;
+    const uint64_t c = (uint64_t)counts[j * L + designated];
+    if (c >= (1ull << (32 - L))) return CAPACITY;   // the count field has 32 - L bits
+    words[j] = bitmap | (uint32_t)(c << L);
+  }
+  return OK;
+}
+
+// The receiving side of the same words: rank r rebuilds the rows it gets from
+// every source for each of its L local experts.  An expert whose bitmap bit
+// is clear gets nothing (it is skipped); the designated expert's count comes
+// from the word; the other active experts' counts come from the per-expert
+// completion signals (`signal` [N][L], read only for those entries).
+int orc_receive_counts(const uint32_t* words, const int32_t* signal, int32_t N, int32_t L,
+                       int32_t* counts) {
+  if (N < 1 || L < 1 || L > 31) return INVALID_ARGUMENT;
+  for (int i = 0; i < N; ++i) {
+    const uint32_t w = words[i];
+    const uint32_t bitmap = w & ((1u << L) - 1);
+    int designated = -1;
+    for (int l = 0; l < L; ++l)
+      if (bitmap >> l & 1) designated = l;
+    for (int l = 0; l < L; ++l) {
+      int32_t c = 0;
+      if (l == designated) c = (int32_t)(w >> L);
+      else if (bitmap >> l & 1) c = signal[i * L + l];
+      counts[i * L + l] = c;
+    }
+  }
+  return OK;
+}
+
 // Ulysses head/context re-layout demand: rank j receives its heads of every
 // local token, D_self,j = T * heads(j) * head_bytes, D_self,self = 0.
 int orc_demand_heads(int64_t T, const int64_t* head_lo, int64_t head_bytes, int32_t N,

@@ -61,12 +61,16 @@ def lib():
     L.vp_catalog_shapes.argtypes = [vp] * 6
     L.vp_catalog_families.argtypes = [vp] * 4
     L.vp_catalog_upload.argtypes = [vp, vp]
+    L.vp_catalog_save.argtypes = [vp, vp, sz, C.POINTER(sz)]
+    L.vp_catalog_load.argtypes = [vp, sz, C.POINTER(vp)]
     L.vp_catalog_free.argtypes = [vp]
     L.vp_catalog_free.restype = None
     L.vp_demand_workspace.argtypes = [i64, i32, i32]
     L.vp_demand_workspace.restype = sz
     L.vp_demand.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.vp_demand_heads.argtypes = [i64, vp, i64, i32, i32, i32, vp, vp, vp]
+    L.vp_control_words.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp]
+    L.vp_receive_counts.argtypes = [vp, i64, vp, i32, i32, vp, vp]
     L.vp_plan_params_default.argtypes = [i32, i64, C.POINTER(PlanParams)]
     L.vp_plan_params_default.restype = None
     L.vp_plan_workspace.argtypes = [vp, C.POINTER(PlanParams)]
@@ -135,10 +139,16 @@ def topology(topo) -> _Topology:
 class Catalog:
     """Offline channel-family catalog (host build, one upload per device)."""
 
-    def __init__(self, topo):
+    def __init__(self, topo=None, *, payload: Optional[bytes] = None):
+        """Build the catalog of topology `topo` (Alg. 1), or load it from a
+        payload written by save()."""
         h = C.c_void_p()
-        t = topology(topo)
-        _check(lib().vp_build_catalog(C.byref(t), C.byref(h)), "vp_build_catalog")
+        if payload is not None:
+            buf = C.create_string_buffer(bytes(payload), len(payload))
+            _check(lib().vp_catalog_load(buf, len(payload), C.byref(h)), "vp_catalog_load")
+        else:
+            t = topology(topo)
+            _check(lib().vp_build_catalog(C.byref(t), C.byref(h)), "vp_build_catalog")
         self._h = h
         self.topo = topo
         info = np.zeros(8, np.int64)
@@ -178,6 +188,18 @@ class Catalog:
         ids = np.zeros((F, self.Q * self.g), np.int32)
         _check(lib().vp_catalog_families(self._h, _np(shape), _np(k), _np(ids)), "vp_catalog_families")
         return dict(shape=shape, k=k, ids=ids)
+
+    def save(self) -> bytes:
+        """vp_catalog_save: the compact serialized catalog."""
+        n = C.c_size_t(0)
+        _check(lib().vp_catalog_save(self._h, None, 0, C.byref(n)), "vp_catalog_save")
+        buf = C.create_string_buffer(n.value)
+        _check(lib().vp_catalog_save(self._h, buf, n.value, C.byref(n)), "vp_catalog_save")
+        return buf.raw[:n.value]
+
+    @classmethod
+    def load(cls, payload: bytes) -> "Catalog":
+        return cls(payload=payload)
 
     def upload(self, stream=None):
         _check(lib().vp_catalog_upload(self._h, _stream(stream)), "vp_catalog_upload")
@@ -254,6 +276,41 @@ def demand_heads(T: int, head_lo: torch.Tensor, head_bytes: int, first_rank: int
         status = new_status(head_lo.device)
     _check(lib().vp_demand_heads(T, _ptr(head_lo), head_bytes, N, first_rank, R, _ptr(out), _ptr(status),
                                  _stream(stream)), "vp_demand_heads")
+    return out
+
+
+def control_words(counts: torch.Tensor, n_ranks: int, first_rank: int = 0,
+                  status: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                  stream=None) -> torch.Tensor:
+    """vp_control_words over counts [R, E] (int32, GPU).  Returns the words
+    [R, N] as int32 holding the uint32 bit patterns."""
+    _dev(counts, torch.int32, "counts")
+    R, E = counts.shape
+    if out is None:
+        out = torch.empty((R, n_ranks), dtype=torch.int32, device=counts.device)
+    if status is None:
+        status = new_status(counts.device)
+    _check(lib().vp_control_words(_ptr(counts), R, E, n_ranks, first_rank, _ptr(out), _ptr(status),
+                                  _stream(stream)), "vp_control_words")
+    return out
+
+
+def receive_counts(words: torch.Tensor, word_stride: int, signal: torch.Tensor, n_local: int,
+                   offset: int = 0, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """vp_receive_counts: a receiver's rows per (source, local expert), int32
+    [N, L], from the words at flat positions offset + i * word_stride of the
+    contiguous int32 tensor `words` and the signal counts [N, L]."""
+    _dev(signal, torch.int32, "signal")
+    _dev(words, torch.int32, "words")
+    N = signal.shape[0]
+    if signal.dim() != 2 or signal.shape[1] != n_local:
+        raise ValueError("signal must be [N, n_local]")
+    if offset < 0 or word_stride < 1 or offset + (N - 1) * word_stride >= words.numel():
+        raise ValueError("words too short for N sources at this offset and stride")
+    if out is None:
+        out = torch.empty((N, n_local), dtype=torch.int32, device=signal.device)
+    _check(lib().vp_receive_counts(C.c_void_p(words.data_ptr() + 4 * offset), word_stride, _ptr(signal), N,
+                                   n_local, _ptr(out), _stream(stream)), "vp_receive_counts")
     return out
 
 
@@ -440,8 +497,9 @@ class Pipeline:
     """Preallocated demand -> plan -> pack for one workload on one GPU.
 
     ``step()`` enqueues the whole hot path on the current stream with no host
-    synchronisation: vp_demand (or vp_demand_heads) over every rank's routing,
-    vp_plan on the resulting N x N matrix, and vp_pack of rank ``self_rank``.
+    synchronisation: vp_demand (or vp_demand_heads) over every rank's routing
+    and, for MoE, vp_control_words of every pair; vp_plan on the resulting
+    N x N matrix; and vp_pack of rank ``self_rank``.
     """
 
     def __init__(self, topo, mode: str, unit: int, *, n_experts: int = 0, tokens: int = 0,
@@ -467,6 +525,7 @@ class Pipeline:
                             dest_off=torch.empty(N + 1, dtype=torch.int64, device=dev))
             self.dem_ws = torch.empty(max(demand_workspace_bytes(tokens, top_k, n_experts), 1),
                                       dtype=torch.uint8, device=dev)
+            self.words = torch.empty((N, N), dtype=torch.int32, device=dev)
             cap = tokens * top_k * unit
             ws_T, ws_k = tokens, top_k
         else:
@@ -493,6 +552,12 @@ class Pipeline:
         else:
             _check(L.vp_demand_heads(self.T, _ptr(head_lo), self.unit, self.N, 0, self.N,
                                      _ptr(self.dem["demand"]), _ptr(self.status), s), "vp_demand_heads")
+
+    def words_stage(self, stream=None):
+        """vp_control_words of every rank's pairs (MoE only; uint32 bit patterns in self.words)."""
+        if self.mode == "moe":
+            _check(lib().vp_control_words(_ptr(self.dem["counts"]), self.N, self.E, self.N, 0, _ptr(self.words),
+                                          _ptr(self.status), _stream(stream)), "vp_control_words")
 
     def plan_stage(self, stream=None):
         p = self.params
@@ -540,8 +605,9 @@ class Pipeline:
 
     def step(self, routing: Optional[torch.Tensor] = None, tokens: Optional[torch.Tensor] = None,
              head_lo: Optional[torch.Tensor] = None, send: Optional[torch.Tensor] = None, stream=None):
-        """demand -> plan -> pack for one matrix; returns the send buffer."""
+        """demand (+ control words) -> plan -> pack for one matrix; returns the send buffer."""
         self.demand_stage(routing, head_lo, stream)
+        self.words_stage(stream)
         self.plan_stage(stream)
         self.pack_prepare_stage(tokens, head_lo, stream)
         return self.pack_gather_stage(tokens, send, stream)

@@ -39,25 +39,63 @@ const char* vp_status_string(vp_status s) {
 
 const char* vp_last_error(void) { return vp::g_last_error.c_str(); }
 
+}  // extern "C"
+
+namespace {
+
+vp_status check_topology(const vp_topology& t) {
+  if (t.flags != 0) return set_error(VP_ERR_UNSUPPORTED, "topology flags must be 0");
+  if (t.n_nodes < 1 || t.n_nodes > vp::kMaxNodes)
+    return set_error(VP_ERR_UNSUPPORTED, "n_nodes must be in [1, 256]");
+  if (t.sockets_per_node < 1 || t.switches_per_socket < 1 ||
+      t.sockets_per_node * t.switches_per_socket > vp::kMaxSlotsPerNode)
+    return set_error(VP_ERR_UNSUPPORTED, "sockets*switches per node must be in [1, 8]");
+  if (t.gpus_per_switch < 2 || t.gpus_per_switch > vp::kMaxGpusPerSwitch)
+    return set_error(VP_ERR_UNSUPPORTED, "gpus_per_switch must be in [2, 4]");
+  if (t.nics_per_switch != 1) return set_error(VP_ERR_UNSUPPORTED, "nics_per_switch must be 1");
+  if (t.pcie_bytes_per_ns < 1 || t.nic_bytes_per_ns < 1)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "rates must be positive");
+  int64_t N = (int64_t)t.n_nodes * t.sockets_per_node * t.switches_per_socket * t.gpus_per_switch;
+  if (N > vp::kMaxRanks) return set_error(VP_ERR_UNSUPPORTED, "more than 1024 ranks");
+  return VP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 vp_status vp_build_catalog(const vp_topology* t, vp_catalog** out) {
   if (!t || !out) return set_error(VP_ERR_INVALID_ARGUMENT, "null topology or output");
   *out = nullptr;
-  if (t->flags != 0) return set_error(VP_ERR_UNSUPPORTED, "topology flags must be 0");
-  if (t->n_nodes < 1 || t->n_nodes > vp::kMaxNodes)
-    return set_error(VP_ERR_UNSUPPORTED, "n_nodes must be in [1, 256]");
-  if (t->sockets_per_node < 1 || t->switches_per_socket < 1 ||
-      t->sockets_per_node * t->switches_per_socket > vp::kMaxSlotsPerNode)
-    return set_error(VP_ERR_UNSUPPORTED, "sockets*switches per node must be in [1, 8]");
-  if (t->gpus_per_switch < 2 || t->gpus_per_switch > vp::kMaxGpusPerSwitch)
-    return set_error(VP_ERR_UNSUPPORTED, "gpus_per_switch must be in [2, 4]");
-  if (t->nics_per_switch != 1) return set_error(VP_ERR_UNSUPPORTED, "nics_per_switch must be 1");
-  if (t->pcie_bytes_per_ns < 1 || t->nic_bytes_per_ns < 1)
-    return set_error(VP_ERR_INVALID_ARGUMENT, "rates must be positive");
-  int64_t N = (int64_t)t->n_nodes * t->sockets_per_node * t->switches_per_socket * t->gpus_per_switch;
-  if (N > vp::kMaxRanks) return set_error(VP_ERR_UNSUPPORTED, "more than 1024 ranks");
+  vp_status s = check_topology(*t);
+  if (s != VP_OK) return s;
   vp_catalog* c = new (std::nothrow) vp_catalog();
   if (!c) return set_error(VP_ERR_INVALID_ARGUMENT, "out of host memory");
-  vp_status s = vp::build_catalog_host(*t, *c);
+  s = vp::build_catalog_host(*t, *c);
+  if (s != VP_OK) {
+    delete c;
+    return s;
+  }
+  *out = c;
+  return VP_OK;
+}
+
+vp_status vp_catalog_save(const vp_catalog* c, void* buf, size_t capacity, size_t* size) {
+  if (!c || !size) return set_error(VP_ERR_INVALID_ARGUMENT, "null catalog or size");
+  const std::vector<uint8_t> b = vp::serialize_catalog(*c);
+  *size = b.size();
+  if (!buf) return VP_OK;
+  if (capacity < b.size()) return set_error(VP_ERR_CAPACITY, "buffer smaller than the serialized catalog");
+  std::memcpy(buf, b.data(), b.size());
+  return VP_OK;
+}
+
+vp_status vp_catalog_load(const void* buf, size_t size, vp_catalog** out) {
+  if (!buf || !out) return set_error(VP_ERR_INVALID_ARGUMENT, "null buffer or output");
+  *out = nullptr;
+  vp_catalog* c = new (std::nothrow) vp_catalog();
+  if (!c) return set_error(VP_ERR_INVALID_ARGUMENT, "out of host memory");
+  vp_status s = vp::deserialize_catalog((const uint8_t*)buf, size, *c, check_topology);
   if (s != VP_OK) {
     delete c;
     return s;
@@ -189,6 +227,23 @@ vp_status vp_demand_heads(int64_t T, const int64_t* head_lo, int64_t head_bytes,
       first_rank < 0 || first_rank + R > n_ranks || !demand || !dev_status)
     return set_error(VP_ERR_INVALID_ARGUMENT, "bad head-demand arguments");
   return vp::launch_demand_heads(T, head_lo, head_bytes, n_ranks, first_rank, R, demand, dev_status, stream);
+}
+
+vp_status vp_control_words(const int32_t* counts, int32_t R, int32_t E, int32_t n_ranks, int32_t first_rank,
+                           uint32_t* words, int32_t* dev_status, void* stream) {
+  if (!counts || !words || !dev_status || R < 0 || n_ranks < 1 || n_ranks > vp::kMaxRanks || E < n_ranks ||
+      E % n_ranks != 0 || first_rank < 0 || first_rank + R > n_ranks)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "bad control-word arguments");
+  if (E / n_ranks > 31) return set_error(VP_ERR_UNSUPPORTED, "more than 31 local experts per rank");
+  return vp::launch_control_words(counts, R, E, n_ranks, first_rank, words, dev_status, stream);
+}
+
+vp_status vp_receive_counts(const uint32_t* words, int64_t word_stride, const int32_t* signal, int32_t n_ranks,
+                            int32_t n_local, int32_t* counts, void* stream) {
+  if (!words || !signal || !counts || word_stride < 1 || n_ranks < 1 || n_ranks > vp::kMaxRanks || n_local < 1)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "bad receive-count arguments");
+  if (n_local > 31) return set_error(VP_ERR_UNSUPPORTED, "more than 31 local experts per rank");
+  return vp::launch_receive_counts(words, word_stride, signal, n_ranks, n_local, counts, stream);
 }
 
 void vp_plan_params_default(int32_t n_ranks, int64_t unit_bytes, vp_plan_params* p) {

@@ -16,6 +16,7 @@
 // switches' NICs); shifts k != 0 use the NIC-carrying patterns, identical for
 // every k.
 #include <algorithm>
+#include <cstring>
 #include <map>
 #include <set>
 #include <tuple>
@@ -161,19 +162,14 @@ std::vector<Found> prune_families(std::vector<Found> fs, const std::vector<Cand>
 
 }  // namespace
 
-vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
-  const int S = t.sockets_per_node, W = t.switches_per_socket, g = t.gpus_per_switch;
-  const int Q = S * W, nn = t.n_nodes;
-  c.topo = t;
-  c.g = g;
-  c.Q = Q;
-  c.nn = nn;
-  c.G = nn * Q;
-  c.N = c.G * g;
+namespace {
+
+// Node-local instance table in canonical id order: (class, src, dst, copy).
+std::vector<Cand> instance_table(const vp_topology& t) {
+  const int W = t.switches_per_socket, g = t.gpus_per_switch;
+  const int Q = t.sockets_per_node * W;
   const int64_t pcie = t.pcie_bytes_per_ns;
   const int64_t nicbw = std::min(t.pcie_bytes_per_ns, t.nic_bytes_per_ns);
-
-  // Node-local instance table in canonical id order: (class, src, dst, copy).
   std::vector<Cand> table;
   auto add = [&](int cls, int s, int d, int cp, int64_t bw, uint32_t res) {
     table.push_back(Cand{(int)table.size(), cls, s, d, cp, bw, res, false});
@@ -186,40 +182,28 @@ vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
   for (int q = 0; q < Q; ++q)
     for (int q2 = 0; q2 < Q; ++q2)
       add(VP_PATH_NIC, q, q2, 0, nicbw, (1u << (2 * Q + q)) | (1u << (3 * Q + q2)));
-  for (const Cand& x : table) {
-    c.icls.push_back(x.cls);
-    c.isrc.push_back(x.src);
-    c.idst.push_back(x.dst);
-    c.icopy.push_back(x.copy);
-    c.ibw.push_back(x.bw);
+  return table;
+}
+
+// PrunePaths over the table with NIC lanes local (remote = false) or to
+// another node (remote = true): the instances that survive.
+std::vector<Cand> prune_paths(const std::vector<Cand>& table, bool remote_nic) {
+  std::vector<Cand> cand = table;
+  for (Cand& x : cand) x.remote = remote_nic && x.cls == VP_PATH_NIC;
+  std::vector<Cand> kept;
+  for (const Cand& x : cand) {
+    bool dom = false;
+    for (const Cand& y : cand)
+      if (y.id != x.id && path_dominates(y, x)) { dom = true; break; }
+    if (!dom) kept.push_back(x);
   }
+  return kept;
+}
 
-  auto enumerate = [&](bool remote_nic) {
-    std::vector<Cand> cand = table;
-    for (Cand& x : cand) x.remote = remote_nic && x.cls == VP_PATH_NIC;
-    std::vector<Cand> kept;
-    for (const Cand& x : cand) {
-      bool dom = false;
-      for (const Cand& y : cand)
-        if (y.id != x.id && path_dominates(y, x)) { dom = true; break; }
-      if (!dom) kept.push_back(x);
-    }
-    SlotSearch search(kept, Q, g);
-    std::vector<Found> fs = prune_families(search.run(), cand);
-    if (remote_nic) {
-      std::vector<Found> with_nic;
-      for (Found& f : fs) {
-        int n = 0;
-        for (int v : f.R) n += v;
-        if (n > 0) with_nic.push_back(std::move(f));
-      }
-      fs.swap(with_nic);
-    }
-    return fs;   // sorted by (L, R, ids): canonical
-  };
-
-  std::vector<Found> f0 = enumerate(false);
-  std::vector<Found> f1 = nn > 1 ? enumerate(true) : std::vector<Found>();
+// Patterns (runs of families with one (L, R)) and the device image, from
+// the canonical shift-0 and NIC-carrying family lists.
+void fill_catalog(vp_catalog& c, const std::vector<Found>& f0, const std::vector<Found>& f1) {
+  c.patL.clear(); c.patR.clear(); c.pat_fb.clear(); c.pat_fe.clear(); c.lfam.clear();
   auto group = [&](const std::vector<Found>& fs, int fam_base) {
     for (size_t i = 0; i < fs.size(); ++i) {
       if (i == 0 || fs[i].L != fs[i - 1].L || fs[i].R != fs[i - 1].R) {
@@ -239,6 +223,168 @@ vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
   c.J1 = (int)c.patL.size() - c.J0;
   c.F1 = (int)f1.size();
   build_device_image(c);
+}
+
+void set_shape(vp_catalog& c, const vp_topology& t) {
+  c.topo = t;
+  c.g = t.gpus_per_switch;
+  c.Q = t.sockets_per_node * t.switches_per_socket;
+  c.nn = t.n_nodes;
+  c.G = c.nn * c.Q;
+  c.N = c.G * c.g;
+  const std::vector<Cand> table = instance_table(t);
+  c.icls.clear(); c.isrc.clear(); c.idst.clear(); c.icopy.clear(); c.ibw.clear();
+  for (const Cand& x : table) {
+    c.icls.push_back(x.cls);
+    c.isrc.push_back(x.src);
+    c.idst.push_back(x.dst);
+    c.icopy.push_back(x.copy);
+    c.ibw.push_back(x.bw);
+  }
+}
+
+// ------------------------------------------------------------ serialized form
+//
+// The compact serialized catalog (Table 4 sizes the catalog by such a
+// payload) holds what Alg. 1 produced and nothing the topology alone gives:
+//   magic "VPCATLG1" | topology: 6 x int32, 2 x int64 | F0, F1, Q*g: 3 x int32 |
+//   (F0 + F1) x Q*g node-local instance ids (uint8, ascending per family) |
+//   FNV-1a 64-bit hash of all preceding bytes.
+// All integers little-endian.
+constexpr char kMagic[8] = {'V', 'P', 'C', 'A', 'T', 'L', 'G', '1'};
+constexpr size_t kHead = 8 + 6 * 4 + 2 * 8 + 3 * 4;
+
+uint64_t fnv1a(const uint8_t* p, size_t n) {
+  uint64_t h = 0xcbf29ce484222325ull;
+  for (size_t i = 0; i < n; ++i) {
+    h ^= p[i];
+    h *= 0x100000001b3ull;
+  }
+  return h;
+}
+
+void put(std::vector<uint8_t>& b, uint64_t v, int bytes) {
+  for (int i = 0; i < bytes; ++i) b.push_back((uint8_t)(v >> (8 * i)));
+}
+
+uint64_t get(const uint8_t* p, int bytes) {
+  uint64_t v = 0;
+  for (int i = 0; i < bytes; ++i) v |= (uint64_t)p[i] << (8 * i);
+  return v;
+}
+
+}  // namespace
+
+vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
+  set_shape(c, t);
+  const std::vector<Cand> table = instance_table(t);
+  auto enumerate = [&](bool remote_nic) {
+    SlotSearch search(prune_paths(table, remote_nic), c.Q, c.g);
+    std::vector<Cand> cand = table;
+    for (Cand& x : cand) x.remote = remote_nic && x.cls == VP_PATH_NIC;
+    std::vector<Found> fs = prune_families(search.run(), cand);
+    if (remote_nic) {
+      std::vector<Found> with_nic;
+      for (Found& f : fs) {
+        int n = 0;
+        for (int v : f.R) n += v;
+        if (n > 0) with_nic.push_back(std::move(f));
+      }
+      fs.swap(with_nic);
+    }
+    return fs;   // sorted by (L, R, ids): canonical
+  };
+  std::vector<Found> f0 = enumerate(false);
+  std::vector<Found> f1 = c.nn > 1 ? enumerate(true) : std::vector<Found>();
+  fill_catalog(c, f0, f1);
+  return VP_OK;
+}
+
+std::vector<uint8_t> serialize_catalog(const vp_catalog& c) {
+  std::vector<uint8_t> b(kMagic, kMagic + 8);
+  const vp_topology& t = c.topo;
+  for (int32_t v : {t.n_nodes, t.sockets_per_node, t.switches_per_socket, t.gpus_per_switch, t.nics_per_switch,
+                    t.flags})
+    put(b, (uint32_t)v, 4);
+  put(b, (uint64_t)t.pcie_bytes_per_ns, 8);
+  put(b, (uint64_t)t.nic_bytes_per_ns, 8);
+  put(b, (uint32_t)c.F0, 4);
+  put(b, (uint32_t)c.F1, 4);
+  put(b, (uint32_t)(c.Q * c.g), 4);
+  for (const std::vector<int32_t>& f : c.lfam)
+    for (int32_t id : f) b.push_back((uint8_t)id);
+  put(b, fnv1a(b.data(), b.size()), 8);
+  return b;
+}
+
+// Rebuilds a catalog from its serialized form.  Everything Alg. 1 guarantees
+// is checked again: every family is a complete, resource-disjoint set of
+// surviving path instances (Eq. (1), Eq. (4)), identical PIX copies appear in
+// copy order, NIC-carrying families carry a NIC lane, and each list is in
+// strictly increasing canonical order (no duplicates).  A subset of the
+// families Alg. 1 would find is accepted (a restricted catalog).
+vp_status deserialize_catalog(const uint8_t* p, size_t n, vp_catalog& c,
+                              vp_status (*check_topology)(const vp_topology&)) {
+  if (n < kHead + 8 || std::memcmp(p, kMagic, 8) != 0)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "not a serialized catalog");
+  if (get(p + n - 8, 8) != fnv1a(p, n - 8)) return set_error(VP_ERR_INVALID_ARGUMENT, "catalog checksum mismatch");
+  vp_topology t;
+  const uint8_t* q = p + 8;
+  t.n_nodes = (int32_t)get(q, 4); t.sockets_per_node = (int32_t)get(q + 4, 4);
+  t.switches_per_socket = (int32_t)get(q + 8, 4); t.gpus_per_switch = (int32_t)get(q + 12, 4);
+  t.nics_per_switch = (int32_t)get(q + 16, 4); t.flags = (int32_t)get(q + 20, 4);
+  t.pcie_bytes_per_ns = (int64_t)get(q + 24, 8); t.nic_bytes_per_ns = (int64_t)get(q + 32, 8);
+  q += 40;
+  vp_status st = check_topology(t);
+  if (st != VP_OK) return st;
+  const int64_t F0 = (int32_t)get(q, 4), F1 = (int32_t)get(q + 4, 4), QG = (int32_t)get(q + 8, 4);
+  q += 12;
+  set_shape(c, t);
+  const int Q = c.Q, g = c.g;
+  if (QG != Q * g || F0 < 1 || F1 < 0 || (c.nn == 1) != (F1 == 0) ||
+      (size_t)((F0 + F1) * QG) != n - kHead - 8)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "catalog sizes do not match its topology");
+  const std::vector<Cand> table = instance_table(t);
+  const int n_inst = (int)table.size();
+  std::vector<Found> lists[2];
+  for (int part = 0; part < 2; ++part) {
+    const bool remote = part == 1;
+    std::vector<char> kept(n_inst, 0);
+    for (const Cand& x : prune_paths(table, remote)) kept[x.id] = 1;
+    for (int64_t f = 0; f < (part ? F1 : F0); ++f) {
+      Found fam;
+      fam.L.assign(Q * Q, 0);
+      fam.R.assign(Q * Q, 0);
+      std::vector<int> outd(Q, 0), ind(Q, 0);
+      uint32_t used = 0;
+      bool ok = true;
+      int nic = 0;
+      for (int64_t x = 0; x < QG; ++x) {
+        const int id = *q++;
+        if (id >= n_inst || !kept[id] || (!fam.ids.empty() && id <= fam.ids.back())) { ok = false; continue; }
+        const Cand& y = table[id];
+        if (y.res & used) ok = false;
+        used |= y.res;
+        if (y.cls == VP_PATH_PIX && y.copy > 0 &&
+            std::find(fam.ids.begin(), fam.ids.end(), id - 1) == fam.ids.end())
+          ok = false;
+        outd[y.src]++;
+        ind[y.dst]++;
+        const bool r = remote && y.cls == VP_PATH_NIC;
+        nic += r;
+        (r ? fam.R : fam.L)[y.src * Q + y.dst]++;
+        fam.ids.push_back(id);
+      }
+      for (int s = 0; s < Q; ++s) ok = ok && outd[s] == g && ind[s] == g;
+      if (remote && nic == 0) ok = false;
+      if (!ok) return set_error(VP_ERR_INVALID_ARGUMENT, "serialized catalog holds an infeasible family");
+      if (!lists[part].empty() && !(std::tie(lists[part].back().L, lists[part].back().R, lists[part].back().ids) <
+                                   std::tie(fam.L, fam.R, fam.ids)))
+        return set_error(VP_ERR_INVALID_ARGUMENT, "serialized families are not in canonical order");
+      lists[part].push_back(std::move(fam));
+    }
+  }
+  fill_catalog(c, lists[0], lists[1]);
   return VP_OK;
 }
 

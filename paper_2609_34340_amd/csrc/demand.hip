@@ -14,6 +14,9 @@
 //                 wave's 256 ids from a wave-wide match mask built with one
 //                 ballot per bit of the expert id plus a prefix popcount,
 //                 then the waves' counts scanned per expert.
+//   control_words / receive_counts  the sparse expert-parallel control word
+//                 of every (source, destination) pair from the counts, and
+//                 its decode at the receiver.
 #include <hip/hip_runtime.h>
 
 #include "internal.h"
@@ -218,6 +221,56 @@ __global__ void demand_heads_kernel(int64_t T, const int64_t* __restrict__ head_
   }
 }
 
+// Sparse expert-parallel control words (Sec. 5): one thread per (source row,
+// destination) pair.  The destination's L local experts are L consecutive
+// counts of the row: bit l marks an expert with rows, the bits above L carry
+// the count of the highest such expert (the last payload of the pair's
+// expert-ascending stream).  The self pair and pairs without rows get 0.
+__global__ void __launch_bounds__(256) control_words_kernel(const int32_t* __restrict__ counts, int32_t R,
+                                                            int32_t E, int32_t N, int32_t L, int32_t first_rank,
+                                                            uint32_t* __restrict__ words, int32_t* status) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= (int64_t)R * N) return;
+  const int r = (int)(p / N), j = (int)(p - (int64_t)r * N);
+  const int32_t* c = counts + (size_t)r * E + (size_t)j * L;
+  uint32_t bitmap = 0;
+  int32_t last = 0;
+  bool bad = false;
+  for (int l = 0; l < L; ++l) {
+    const int32_t v = c[l];
+    bad |= v < 0;
+    if (v > 0) {
+      bitmap |= 1u << l;
+      last = v;
+    }
+  }
+  uint32_t w = 0;
+  if (bad) {
+    report(status, VP_ERR_INVALID_ARGUMENT);
+  } else if (j != first_rank + r && bitmap != 0) {
+    if (((uint64_t)last >> (32 - L)) != 0) report(status, VP_ERR_CAPACITY);   // 32 - L count bits
+    else w = bitmap | ((uint32_t)last << L);
+  }
+  words[p] = w;
+}
+
+// The receiver's side: one thread per (source, local expert).  A clear bitmap
+// bit means no rows; the designated (highest active) expert's count is in the
+// word; the other active experts' counts come from their signals.
+__global__ void __launch_bounds__(256) receive_counts_kernel(const uint32_t* __restrict__ words,
+                                                             int64_t word_stride,
+                                                             const int32_t* __restrict__ signal, int32_t N,
+                                                             int32_t L, int32_t* __restrict__ counts) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= (int64_t)N * L) return;
+  const int i = (int)(p / L), l = (int)(p - (int64_t)i * L);
+  const uint32_t w = words[(size_t)i * word_stride];
+  const uint32_t bitmap = w & ((1u << L) - 1);
+  int32_t c = 0;
+  if (bitmap >> l & 1) c = (31 - __builtin_clz(bitmap)) == l ? (int32_t)(w >> L) : signal[p];
+  counts[p] = c;
+}
+
 int n_chunks_of(int64_t Tk) { return (int)((Tk + kChunk - 1) / kChunk); }
 
 }  // namespace
@@ -256,6 +309,25 @@ vp_status launch_demand_heads(int64_t T, const int64_t* head_lo, int64_t head_by
   hipLaunchKernelGGL(demand_heads_kernel, dim3(R), dim3(256), 0, s, T, head_lo, head_bytes, N, first_rank,
                      demand, status);
   if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "demand_heads launch failed");
+  return VP_OK;
+}
+
+vp_status launch_control_words(const int32_t* counts, int32_t R, int32_t E, int32_t N, int32_t first_rank,
+                               uint32_t* words, int32_t* status, void* stream) {
+  const int64_t n = (int64_t)R * N;
+  if (n == 0) return VP_OK;
+  hipLaunchKernelGGL(control_words_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, (hipStream_t)stream,
+                     counts, R, E, N, E / N, first_rank, words, status);
+  if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "control_words launch failed");
+  return VP_OK;
+}
+
+vp_status launch_receive_counts(const uint32_t* words, int64_t word_stride, const int32_t* signal, int32_t N,
+                                int32_t L, int32_t* counts, void* stream) {
+  const int64_t n = (int64_t)N * L;
+  hipLaunchKernelGGL(receive_counts_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                     (hipStream_t)stream, words, word_stride, signal, N, L, counts);
+  if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "receive_counts launch failed");
   return VP_OK;
 }
 

@@ -74,6 +74,9 @@ namespace vp {
 
 vp_status set_error(vp_status s, const std::string& msg);
 vp_status build_catalog_host(const vp_topology& t, vp_catalog& c);
+std::vector<uint8_t> serialize_catalog(const vp_catalog& c);
+vp_status deserialize_catalog(const uint8_t* p, size_t n, vp_catalog& c,
+                              vp_status (*check_topology)(const vp_topology&));
 void build_device_image(vp_catalog& c);
 
 struct PlanLaunch {
@@ -106,6 +109,10 @@ struct DemandLaunch {
 };
 size_t demand_workspace(int64_t T, int32_t k, int32_t E);
 vp_status launch_demand(const DemandLaunch& a, void* stream);
+vp_status launch_control_words(const int32_t* counts, int32_t R, int32_t E, int32_t N, int32_t first_rank,
+                               uint32_t* words, int32_t* status, void* stream);
+vp_status launch_receive_counts(const uint32_t* words, int64_t word_stride, const int32_t* signal, int32_t N,
+                                int32_t L, int32_t* counts, void* stream);
 vp_status launch_demand_heads(int64_t T, const int64_t* head_lo, int64_t head_bytes, int32_t N,
                               int32_t first_rank, int32_t R, int64_t* demand, int32_t* status,
                               void* stream);

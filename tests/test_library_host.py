@@ -90,3 +90,89 @@ def test_workspace_queries(vp):
     # rows: a copy counter and top-k send-unit slots per token
     assert vp.pack_workspace_bytes(2048, 468_729_856, 14336, 4096, 8) >= 4096 * 4 * 9
     assert vp.pack_workspace_bytes(2048, 468_729_856, 14336, -1, 8) == 0
+
+
+# ------------------------------------------------------- serialized catalog
+
+def fnv1a64(b: bytes) -> int:
+    h = 0xcbf29ce484222325
+    for x in b:
+        h = ((h ^ x) * 0x100000001b3) & 0xFFFFFFFFFFFFFFFF
+    return h
+
+
+def reseal(body: bytes) -> bytes:
+    return body + fnv1a64(body).to_bytes(8, "little")
+
+
+HEAD = 8 + 6 * 4 + 2 * 8 + 3 * 4
+
+
+def assert_same_catalog(a, b):
+    assert (a.N, a.G, a.g, a.Q, a.n_nodes, a.n_shapes, a.n_families, a.n_instances) == \
+        (b.N, b.G, b.g, b.Q, b.n_nodes, b.n_shapes, b.n_families, b.n_instances)
+    for x, y in [(a.instances(), b.instances()), (a.shapes(), b.shapes()), (a.families(), b.families())]:
+        for key in x:
+            assert np.array_equal(x[key], y[key]), key
+
+
+@pytest.mark.parametrize("topo", [vpgen.tiny_topology(), vpgen.config(1).topo, vpgen.config(2).topo,
+                                  vpgen.config(5).topo, vpgen.Topology(3, 1, 2, 3), vpgen.Topology(2, 2, 1, 4)])
+def test_catalog_save_load_round_trip(vp, topo):
+    c = vp.Catalog(topo)
+    p = c.save()
+    # header, one byte per node-local instance id of every local family
+    # (shift-0 ones, then the NIC-carrying ones shared by every shift), hash
+    F0 = int((c.families()["k"] == 0).sum())
+    F1 = (c.n_families - F0) // (c.n_nodes - 1) if c.n_nodes > 1 else 0
+    assert len(p) == HEAD + (F0 + F1) * c.Q * c.g + 8
+    assert p[:8] == b"VPCATLG1" and fnv1a64(p[:-8]) == int.from_bytes(p[-8:], "little")
+    d = vp.Catalog.load(p)
+    assert_same_catalog(c, d)
+    assert d.save() == p
+
+
+def test_catalog_payload_sizes(vp):
+    """One byte per node-local instance id: 152 shift-0 families for one
+    8-GPU node, 152 + 352 node-local families for every multi-node size."""
+    for cid, F in [(1, 152), (2, 504), (3, 504), (5, 504)]:
+        c = vp.Catalog(vpgen.config(cid).topo)
+        assert len(c.save()) == HEAD + F * 8 + 8
+
+
+def test_catalog_load_rejects_damaged_payloads(vp):
+    p = vp.Catalog(vpgen.config(2).topo).save()
+    body = p[:-8]
+    QG = 8
+    bad = {
+        "magic": reseal(b"XPCATLG1" + body[8:]),
+        "hash": body + bytes(8),
+        "truncated": reseal(body[:-QG]),
+        # a family with a repeated instance id (not strictly ascending)
+        "repeat": reseal(body[:HEAD] + bytes([body[HEAD]]) * 2 + body[HEAD + 2:]),
+        # two families swapped: no longer in canonical order
+        "order": reseal(body[:HEAD] + body[HEAD + QG:HEAD + 2 * QG] + body[HEAD:HEAD + QG] + body[HEAD + 2 * QG:]),
+        # an instance id past the table
+        "id": reseal(body[:HEAD + QG - 1] + bytes([250]) + body[HEAD + QG:]),
+        # gpus_per_switch 5
+        "topology": reseal(body[:20] + (5).to_bytes(4, "little") + body[24:]),
+    }
+    for name, q in bad.items():
+        with pytest.raises(vp.VPError):
+            vp.Catalog.load(q)
+        assert name
+
+
+def test_catalog_load_accepts_a_restricted_subset(vp):
+    """Dropping whole families keeps a valid (restricted) catalog."""
+    c = vp.Catalog(vpgen.config(1).topo)
+    p = c.save()
+    body = bytearray(p[:-8])
+    F0 = int.from_bytes(body[HEAD - 12:HEAD - 8], "little")
+    keep = [f for f in range(F0) if f % 3 != 1]
+    fams = b"".join(bytes(body[HEAD + f * 8:HEAD + (f + 1) * 8]) for f in keep)
+    body[HEAD - 12:HEAD - 8] = len(keep).to_bytes(4, "little")
+    d = vp.Catalog.load(reseal(bytes(body[:HEAD]) + fams))
+    assert d.n_families == len(keep)
+    ids = c.families()["ids"]
+    assert np.array_equal(d.families()["ids"], ids[keep])
