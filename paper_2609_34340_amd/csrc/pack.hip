@@ -334,15 +334,17 @@ __global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
   }
 }
 
-constexpr int kScatterMaxThreads = 512;
-
 // Rows: one workgroup per (token, copy slot).  Workgroups are handed to the
 // eight XCDs round-robin; the mapping below gives XCD x the tokens t with
 // t % 8 == x, all copy slots of a token back to back, so a token's copies
 // are read on one XCD in a row (the row leaves HBM once, the repeats hit
 // that XCD's L2) while the eight XCDs work on neighbouring tokens, whose
-// copies land next to each other in every destination's stream.
-__global__ void __launch_bounds__(kScatterMaxThreads) scatter_rows_kernel(
+// copies land next to each other in every destination's stream.  TH threads
+// move the row in passes of V 16-byte vectors per thread: all V loads of a
+// pass are issued before its first store, so a wavefront keeps V KiB in
+// flight.
+template <int TH, int V>
+__global__ void __launch_bounds__(TH) scatter_rows_kernel(
     const unsigned char* __restrict__ src, const unsigned long long* __restrict__ lst,
     const uint32_t* __restrict__ hdr, int64_t T, int k, int64_t unit, int64_t vpu,
     unsigned char* __restrict__ send, const int32_t* status) {
@@ -374,7 +376,15 @@ __global__ void __launch_bounds__(kScatterMaxThreads) scatter_rows_kernel(
   }
   const u32x4* row = (const u32x4*)(src + t * unit);
   u32x4* d = (u32x4*)(send + (int64_t)u * unit);
-  for (int64_t i = threadIdx.x; i < vpu; i += blockDim.x) __builtin_nontemporal_store(row[i], d + i);
+  for (int64_t e0 = threadIdx.x; e0 < vpu; e0 += (int64_t)V * TH) {
+    u32x4 r[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+      if (e0 + i * TH < vpu) r[i] = row[e0 + i * TH];
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+      if (e0 + i * TH < vpu) __builtin_nontemporal_store(r[i], d + e0 + i * TH);
+  }
 }
 
 constexpr int kGatherThreads = 256;
@@ -476,10 +486,25 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
     const int64_t blocks = (a.T + 7) / 8 * 8 * a.k;
     if (blocks > 0) {
       if (blocks >= ((int64_t)1 << 31)) return set_error(VP_ERR_UNSUPPORTED, "too many token copies");
-      const int threads = (int)std::min<int64_t>(kScatterMaxThreads, (vpu + 63) / 64 * 64);
-      hipLaunchKernelGGL(scatter_rows_kernel, dim3((unsigned)blocks), dim3(threads), 0, s,
-                         (const unsigned char*)a.src, lst, hdr, a.T, a.k, a.unit, vpu,
-                         (unsigned char*)a.send, a.status);
+      const unsigned char* sp = (const unsigned char*)a.src;
+      unsigned char* dp = (unsigned char*)a.send;
+      const dim3 grid((unsigned)blocks);
+      // about 2 KiB per wavefront: rows up to 2, 4 and 8 KiB take 1, 2 and 4
+      // wavefronts of two vectors per thread; longer rows take 8 wavefronts
+      // with one vector per thread per pass (measured best on 4, 8 and 14 KiB
+      // rows)
+      if (vpu <= 128)
+        hipLaunchKernelGGL((scatter_rows_kernel<64, 2>), grid, dim3(64), 0, s, sp, lst, hdr, a.T, a.k, a.unit, vpu,
+                           dp, a.status);
+      else if (vpu <= 256)
+        hipLaunchKernelGGL((scatter_rows_kernel<128, 2>), grid, dim3(128), 0, s, sp, lst, hdr, a.T, a.k, a.unit,
+                           vpu, dp, a.status);
+      else if (vpu <= 512)
+        hipLaunchKernelGGL((scatter_rows_kernel<256, 2>), grid, dim3(256), 0, s, sp, lst, hdr, a.T, a.k, a.unit,
+                           vpu, dp, a.status);
+      else
+        hipLaunchKernelGGL((scatter_rows_kernel<512, 1>), grid, dim3(512), 0, s, sp, lst, hdr, a.T, a.k, a.unit,
+                           vpu, dp, a.status);
     }
   } else {
     // u = floor(v / vpu) = mulhi(v << 16, ceil(2^48 / vpu)) for v < 2^48 / vpu
