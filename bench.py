@@ -14,7 +14,10 @@ experts holding half of the per-draw mass, hot set redrawn per matrix):
 all enqueued on one stream with no host synchronisation, inputs resident in
 HBM.  Steps cycle over `--matrices` distinct demand matrices and two send
 buffers.  Unless --no-sweep, the other four workloads (N = 8, 16, 64 and the
-16-rank Ulysses case) follow with six timed steps each, under "per_config".
+16-rank Ulysses case) follow with six timed steps each, under "per_config";
+unless --no-extra, the planner then runs on the uniform, skew and head/context
+demands with the full and the nearest-path catalog (the peer/path ablation),
+under "extra_demands".
 Prints one JSON line.  `value` is the pack's throughput in GB/s
 (send bytes + distinct source bytes + index bytes, over the time of the
 whole vp_pack call); the planner's microseconds per matrix, the step time
@@ -178,6 +181,93 @@ def measure(w, steps, warmup, M, dev):
     return r
 
 
+def extra_demand(vp, case, matrix, dev):
+    """int64 [N, N] demand of an extra case on the GPU: given matrices are
+    uploaded; a head/context layout runs vp_demand_heads per all-to-all group
+    and places each group's block on the diagonal."""
+    import torch
+    import vpgen
+    if case.kind == "uniform":
+        return torch.from_numpy(vpgen.uniform_demand(case)).to(dev)
+    if case.kind == "zipf_pairs":
+        return torch.from_numpy(vpgen.zipf_pair_demand(case, matrix)).to(dev)
+    N = case.topo.n_ranks
+    T, hl = vpgen.hc_layout(case)
+    hl_d = torch.from_numpy(hl).to(dev)
+    D = torch.zeros((N, N), dtype=torch.int64, device=dev)
+    for grp in vpgen.hc_groups(case):
+        lo, hi = int(grp[0]), int(grp[-1]) + 1
+        D[lo:hi, lo:hi] = vp.demand_heads(T, hl_d, case.unit, first_rank=0, R=case.H)
+    return D
+
+
+def extra_section(dev, reps=3):
+    """Planner on the uniform, skew (pairwise Zipf) and head/context demands,
+    with the full catalog and with the nearest-path catalog of the peer/path
+    ablation (Sec. 6.4, Table 3: demand-aware peers, fixed nearest path).
+    Per case: plan us per matrix (HIP events, mean of `reps` runs per
+    matrix), K and the modeled completion time T of Eq. (2); the ablation
+    ratios put T of the nearest-path plan and of the fixed cyclic rotation
+    (vp_rotation_time, nearest or per-stage best paths, shared links split
+    equally) over T of the full plan, averaged over the case's matrices."""
+    import torch
+    import vpgen
+    import paper_2609_34340_amd as vp
+    cats, out = {}, {}
+    for name, case in vpgen.EXTRA.items():
+        n_mat = 5 if case.kind == "zipf_pairs" else 1
+        res = {"N": case.topo.n_ranks}
+        Ts = {}
+        for variant in ("full", "nearest"):
+            key = (case.topo, variant)
+            if key not in cats:
+                c = vp.Catalog(case.topo)
+                if variant == "nearest":
+                    c = c.restrict(vp.RESTRICT_NEAREST_PATH)
+                c.upload()
+                cats[key] = c
+            cat = cats[key]
+            p = vp.plan_params(cat.N, case.unit)
+            sched = vp.alloc_schedule(cat.N, p.k_max, dev)
+            st = vp.new_status(dev)
+            ws = torch.empty(vp.plan_workspace_bytes(cat, p), dtype=torch.uint8, device=dev)
+            Ks, That, us = [], [], []
+            for m in range(n_mat):
+                D = extra_demand(vp, case, m, dev)
+                if variant == "full":
+                    Dh = D.cpu().numpy()
+                    for rule, key in [(vp.ROTATION_NEAREST_PATH, "rot_nearest"), (vp.ROTATION_DYNAMIC_PATH, "rot_dynamic")]:
+                        num, den = cat.rotation_time(Dh, rule)
+                        Ts.setdefault(key, []).append(num / den / 1e6)
+                vp.plan(cat, D, p, status=st, out=sched, ws=ws)   # warm
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                for _ in range(reps):
+                    vp.plan(cat, D, p, status=st, out=sched, ws=ws)
+                b.record()
+                torch.cuda.synchronize()
+                if vp.read_status(st) != 0:
+                    raise SystemExit("device error planning %s (%s): %d" % (name, variant, vp.read_status(st)))
+                us.append(a.elapsed_time(b) * 1e3 / reps)
+                h = vp.schedule_to_host(sched)
+                num, den = cat.modeled_time(h["K"], h["inst"], h["bytes"], p.lambda_ns)
+                Ks.append(h["K"])
+                That.append(num / den / 1e6)
+            Ts[variant] = That
+            res[variant] = {"plan_us_per_matrix": round(float(np.mean(us)), 1), "activations_K": round(float(np.mean(Ks)), 1),
+                            "modeled_T_ms": round(float(np.mean(That)), 4), "families": cat.n_families}
+        full = np.array(Ts["full"])
+        res["nearest_over_full_T"] = round(float(np.mean(np.array(Ts["nearest"]) / full)), 4)
+        # Table 3 layout: completion time over the demand-aware, dynamic-path plan's
+        res["ablation"] = {"fixed_peers_nearest_path": round(float(np.mean(np.array(Ts["rot_nearest"]) / full)), 4),
+                           "fixed_peers_dynamic_path": round(float(np.mean(np.array(Ts["rot_dynamic"]) / full)), 4),
+                           "demand_aware_nearest_path": res["nearest_over_full_T"],
+                           "demand_aware_dynamic_path": 1.0}
+        res["matrices"] = n_mat
+        out[name] = res
+    return out
+
+
 def summary(w, r):
     value = float(r["pack_bytes"].sum() / (r["pack_ms"].sum() * 1e-3) / 1e9)
     plan_us = float(r["plan_ms"].mean() * 1e3)
@@ -203,6 +293,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the short runs of the other configurations (plan time at every N)")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the planner on the extra demands and the nearest-path ablation")
     ap.add_argument("--calibrate-copy", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB")
     args = ap.parse_args()
@@ -285,6 +377,9 @@ def main():
             print("[bench] sweep C%d %s" % (cid, wc.name), file=sys.stderr, flush=True)
             per["C%d" % cid] = summary(wc, measure(wc, 6, 2, 2, dev))
         out["per_config"] = per
+    if not args.no_extra:
+        print("[bench] extra demands and nearest-path ablation", file=sys.stderr, flush=True)
+        out["extra_demands"] = extra_section(dev)
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on one matrix", file=sys.stderr, flush=True)
         if w.mode == "moe":

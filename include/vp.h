@@ -119,6 +119,17 @@ vp_status vp_catalog_shapes(const vp_catalog* cat, int32_t* k, int32_t* fam_begi
  * and the Q*g node-local instance ids of each family, ascending. */
 vp_status vp_catalog_families(const vp_catalog* cat, int32_t* shape, int32_t* k, int32_t* ids);
 
+/* Restricted catalogs for the peer/path ablation (Sec. 6.4, Table 3): a new
+ * handle holding the families of `cat` that satisfy `rule`, in the same
+ * canonical order.  VP_RESTRICT_NEAREST_PATH keeps the families in which
+ * every lane takes its group pair's nearest path (PIX inside a switch, PXB
+ * between two switches of one socket, the NICs otherwise), i.e. drops every
+ * family with a NIC lane between two switches of one socket ("fixed nearest
+ * path, demand-aware peers").  Host only; free with vp_catalog_free.  An
+ * unknown rule returns VP_ERR_INVALID_ARGUMENT. */
+enum { VP_RESTRICT_NEAREST_PATH = 1 };
+vp_status vp_catalog_restrict(const vp_catalog* cat, int32_t rule, vp_catalog** out);
+
 /* Compact serialized catalog (Table 4 sizes the catalog tree by such a
  * payload): the topology and the node-local instance ids of every family,
  * little-endian, with a 64-bit FNV-1a hash at the end; see vp_catalog_load.
@@ -408,6 +419,23 @@ vp_status vp_unpack_combine(const void* recv, int64_t recv_capacity, int64_t row
  * num/den nanoseconds (host arrays inst, bytes of shape [K, N]). */
 vp_status vp_modeled_time(const vp_catalog* cat, int32_t K, const int32_t* inst,
                           const int64_t* bytes, int64_t lambda_ns, int64_t* num, int64_t* den);
+
+/* Modeled completion time of a fixed cyclic peer rotation (Sec. 6.4, Table 3
+ * "fixed peer rotation"), the baseline the demand-aware planner is compared
+ * with, on the topology of `cat`: stage s = 1..N-1 pairs rank i with rank
+ * (i + s) mod N and moves all of D_i,(i+s) (demand: host int64 [N, N]);
+ * stages with no bytes are skipped.  path_rule VP_ROTATION_NEAREST_PATH puts
+ * each lane on its pair's nearest path; VP_ROTATION_DYNAMIC_PATH lets every
+ * stage pick, among each pair's paths (PXB or NIC between two switches of a
+ * socket), the choice that finishes the stage first.  Lanes on one directed
+ * resource share its capacity equally (a stage need not be contention-free),
+ * so a lane runs at min(path rate, capacity / sharers) over its resources;
+ * a stage takes lambda_ns plus its slowest lane.  *num / *den is the exact
+ * time in ns.  Host only.  More than 20 lanes with a path choice in one
+ * stage is VP_ERR_UNSUPPORTED; a negative entry VP_ERR_INVALID_ARGUMENT. */
+enum { VP_ROTATION_DYNAMIC_PATH = 0, VP_ROTATION_NEAREST_PATH = 1 };
+vp_status vp_rotation_time(const vp_catalog* cat, const int64_t* demand, int32_t path_rule, int64_t lambda_ns,
+                           int64_t* num, int64_t* den);
 
 const char* vp_status_string(vp_status s);
 const char* vp_last_error(void);

@@ -69,6 +69,7 @@ def lib():
                                  C.c_int64, vp, vp, vp, vp, vp]
         L.orc_demand_heads.argtypes = [C.c_int64, vp, C.c_int64, C.c_int32, C.c_int32, vp]
         L.orc_control_words.argtypes = [vp, C.c_int32, C.c_int32, C.c_int32, vp]
+        L.orc_rotation_time.argtypes = [C.POINTER(_Topo), vp, C.c_int32, C.c_int64, vp, vp]
         L.orc_receive_counts.argtypes = [vp, vp, C.c_int32, C.c_int32, vp]
         L.orc_plan.argtypes = [vp, vp, C.POINTER(_Params), C.c_int32, vp, vp, vp, vp, vp, vp,
                                vp, C.c_int64, vp]
@@ -102,17 +103,20 @@ class OracleError(RuntimeError):
 
 
 class Catalog:
-    """Oracle catalog (node-circulant, or the full Alg. 1 catalog with full=True)."""
+    """Oracle catalog (node-circulant, or the full Alg. 1 catalog with full=True);
+    nearest=True keeps only families whose lanes all take their group pair's
+    nearest path (the "fixed nearest path" ablation of Sec. 6.4)."""
 
-    def __init__(self, topo, full: bool = False):
+    def __init__(self, topo, full: bool = False, nearest: bool = False):
         t = _Topo(*topo.as_tuple()[:5], 0, *topo.as_tuple()[5:])
         h = C.c_void_p()
-        st = lib().orc_catalog_build(C.byref(t), 1 if full else 0, C.byref(h))
+        st = lib().orc_catalog_build(C.byref(t), (1 if full else 0) | (2 if nearest else 0), C.byref(h))
         if st != OK:
             raise OracleError(st, "orc_catalog_build")
         self._h = h
         self.topo = topo
         self.full = full
+        self.nearest = nearest
         info = np.zeros(8, np.int64)
         lib().orc_catalog_info(self._h, _p(info))
         (self.N, self.G, self.g, self.Q, self.n_nodes, self.n_shapes, self.n_families,
@@ -256,6 +260,17 @@ def receive_counts(words: np.ndarray, signal: np.ndarray, n_local: int) -> np.nd
     if st != OK:
         raise OracleError(st, "orc_receive_counts")
     return out
+
+
+def rotation_time(topo, D: np.ndarray, nearest: bool, lambda_ns: int = DEFAULT_LAMBDA_NS):
+    """Exact (num, den) ns of the fixed cyclic peer rotation on D (Sec. 6.4)."""
+    t = _Topo(*topo.as_tuple()[:5], 0, *topo.as_tuple()[5:])
+    Dc = np.ascontiguousarray(D, np.int64)
+    num, den = np.zeros(1, np.int64), np.zeros(1, np.int64)
+    st = lib().orc_rotation_time(C.byref(t), _p(Dc), 1 if nearest else 0, lambda_ns, _p(num), _p(den))
+    if st != OK:
+        raise OracleError(st, "orc_rotation_time")
+    return int(num[0]), int(den[0])
 
 
 def demand_heads(tokens: int, head_lo: np.ndarray, head_bytes: int, self_rank: int):

@@ -62,6 +62,11 @@ class TopoModel:
         """Classes that survive dominance: NIC inside one switch is dominated by PIX."""
         return [c for c in self.classes(a, d) if not (a == d and c == NIC)]
 
+    def nearest_class(self, a: int, d: int) -> int:
+        """The one path a pair keeps under "fixed nearest path": the switch
+        itself, else the socket's root complex, else the NICs."""
+        return self.classes(a, d)[0]
+
     def rate(self, cls: int) -> int:
         return min(self.pcie, self.nic) if cls == NIC else self.pcie
 
@@ -91,14 +96,18 @@ def channel_feasible(tm: TopoModel, pi: List[int], cls: List[int]) -> bool:
     return True
 
 
-def brute_force_channels(tm: TopoModel) -> set:
-    """Every feasible rank-level channel (pi, path classes) using unpruned paths."""
+def brute_force_channels(tm: TopoModel, nearest: bool = False) -> set:
+    """Every feasible rank-level channel (pi, path classes) using unpruned
+    paths, or with nearest=True only each pair's nearest path."""
     N = tm.N
     out = set()
     for pi in itertools.permutations(range(N)):
         if any(pi[i] == i for i in range(N)):
             continue
-        options = [tm.unpruned_classes(tm.group(i), tm.group(pi[i])) for i in range(N)]
+        if nearest:
+            options = [[tm.nearest_class(tm.group(i), tm.group(pi[i]))] for i in range(N)]
+        else:
+            options = [tm.unpruned_classes(tm.group(i), tm.group(pi[i])) for i in range(N)]
         # incremental resource check per lane
         def rec(i, used, cls):
             if i == N:

@@ -329,11 +329,36 @@ struct Catalog {
   i64 bw_max;
 };
 
+// The nearest path of an ordered group pair (Sec. 6.4 peer/path ablation,
+// "fixed nearest path"): PIX inside a switch, PXB between two switches of one
+// socket, the NICs otherwise.  A family keeps only lanes on their pair's
+// nearest path; under the topology model the only other choice is a NIC lane
+// between two switches of one socket.
+bool nearest_only(const std::vector<Inst>& table, const Fam& f, int switches, bool remote_set) {
+  for (int id : f) {
+    const Inst& r = table[id];
+    const bool same_socket = r.a != r.d && r.a / switches == r.d / switches;
+    if (r.cls == NIC && !remote_set && same_socket) return false;
+  }
+  return true;
+}
+
+void keep_nearest(std::map<ShapeKey, std::vector<Fam>>& b, const std::vector<Inst>& table, int switches,
+                  bool remote_set) {
+  for (auto it = b.begin(); it != b.end();) {
+    std::vector<Fam> keep;
+    for (const Fam& f : it->second)
+      if (nearest_only(table, f, switches, remote_set)) keep.push_back(f);
+    if (keep.empty()) it = b.erase(it);
+    else { it->second = keep; ++it; }
+  }
+}
+
 // Node-circulant catalog: a family is (k, B_loc): the same node-local pattern
 // in every node, NIC lanes of node n landing on node (n + k) mod n_nodes; k = 0
 // holds every family whose NIC lanes (if any) stay inside the node.  With one
 // node this is exactly Alg. 1's catalog.
-void build_circulant(Catalog& C) {
+void build_circulant(Catalog& C, bool nearest) {
   const Topo& t = C.topo;
   const int Q = t.Q(), g = t.g, nn = t.n_nodes;
   C.table = local_table(t);
@@ -342,6 +367,7 @@ void build_circulant(Catalog& C) {
   std::vector<Inst> set0;
   for (Inst r : C.table) { r.remote = false; set0.push_back(r); }
   auto b0 = run_alg1(C.table, set0, Q, g, n_res);
+  if (nearest) keep_nearest(b0, C.table, t.switches, false);
   // k != 0 set: PIX, PXB, and NIC lanes to the same slot pattern on another node.
   std::map<ShapeKey, std::vector<Fam>> b1;
   if (nn > 1) {
@@ -401,11 +427,14 @@ void build_circulant(Catalog& C) {
 }
 
 // Full Alg. 1 over the cluster-level instance set (small topologies only).
-void build_full(Catalog& C) {
+void build_full(Catalog& C, bool nearest) {
   const Topo& t = C.topo;
   const int G = t.G();
   C.table = cluster_table(t);
   auto b = run_alg1(C.table, C.table, G, t.g, 4 * G);
+  // cluster groups a and d share a socket when they share a node and a socket
+  // slot range; group ids are node-major, so a / switches is the socket index
+  if (nearest) keep_nearest(b, C.table, t.switches, false);
   for (const auto& kv : b) {
     CShape s;
     s.k = -1;
@@ -815,8 +844,9 @@ struct orc_params {
   uint64_t seed;
 };
 
-// mode 0: node-circulant catalog (equal to full Alg. 1 for one node)
-// mode 1: full Alg. 1 over the cluster-level instance set (small topologies)
+// mode bit 0 clear: node-circulant catalog (equal to full Alg. 1 for one node)
+// mode bit 0 set:   full Alg. 1 over the cluster-level instance set (small topologies)
+// mode bit 1 set:   only families whose lanes all take their pair's nearest path
 int orc_catalog_build(const orc_topology* tp, int mode, orc_catalog** out) {
   if (!tp || !out) return INVALID_ARGUMENT;
   Topo t{tp->n_nodes, tp->sockets_per_node, tp->switches_per_socket, tp->gpus_per_switch,
@@ -827,9 +857,10 @@ int orc_catalog_build(const orc_topology* tp, int mode, orc_catalog** out) {
     return INVALID_ARGUMENT;
   Catalog* C = new Catalog();
   C->topo = t;
-  C->circulant = mode == 0;
-  if (mode == 0) build_circulant(*C);
-  else build_full(*C);
+  C->circulant = (mode & 1) == 0;
+  if (mode & ~3) { delete C; return INVALID_ARGUMENT; }
+  if (C->circulant) build_circulant(*C, (mode & 2) != 0);
+  else build_full(*C, (mode & 2) != 0);
   C->bw_max = 0;
   for (const auto& r : C->table) C->bw_max = std::max(C->bw_max, r.bw);
   *out = reinterpret_cast<orc_catalog*>(C);
@@ -1002,6 +1033,84 @@ int orc_receive_counts(const uint32_t* words, const int32_t* signal, int32_t N, 
       counts[i * L + l] = c;
     }
   }
+  return OK;
+}
+
+// Fixed cyclic peer rotation, the baseline of the peer/path ablation
+// (Sec. 6.4, Table 3).  Stage s = 1..N-1: rank i sends all of D_i,(i+s mod N)
+// at once; empty stages are skipped.  Each lane uses its pair's nearest path
+// (nearest = 1) or, per stage, the path vector that ends the stage first
+// (nearest = 0), every vector tried.  Lanes sharing a directed resource
+// split its capacity equally: a lane's rate is the least of its path rate
+// and capacity / sharers over its resources (UP and DN links carry the PCIe
+// rate, TX and RX the NIC rate).  Stage time = lambda + max bytes / rate.
+// The result is the exact rational total in ns.
+int orc_rotation_time(const orc_topology* tp, const int64_t* D, int32_t nearest, int64_t lambda,
+                      int64_t* num, int64_t* den) {
+  Topo t{tp->n_nodes, tp->sockets_per_node, tp->switches_per_socket, tp->gpus_per_switch,
+         tp->nics_per_switch, tp->pcie_bytes_per_ns, tp->nic_bytes_per_ns};
+  const int N = t.N(), Q = t.Q();
+  auto group = [&](int r) { return r / t.g; };
+  auto node = [&](int a) { return a / Q; };
+  auto socket = [&](int a) { return (a % Q) / t.switches; };
+  // a rational p / q, q > 0
+  struct Rat { u128 p, q; };
+  auto less = [](const Rat& x, const Rat& y) { return x.p * y.q < y.p * x.q; };
+  i64 l = t.pcie;
+  { i64 a = t.pcie, b = t.nic; while (b) { i64 r = a % b; a = b; b = r; } l = t.pcie / a * t.nic; }
+  u128 total = 0;   // in units of 1 / l ns
+  for (int s = 1; s < N; ++s) {
+    std::vector<int> src, dst;
+    std::vector<std::vector<int>> opts;
+    for (int i = 0; i < N; ++i) {
+      const int j = (i + s) % N;
+      if (D[(size_t)i * N + j] < 0) return INVALID_ARGUMENT;
+      if (D[(size_t)i * N + j] == 0) continue;
+      const int a = group(i), d = group(j);
+      std::vector<int> o;
+      if (a == d) o = {PIX};
+      else if (node(a) == node(d) && socket(a) == socket(d)) o = nearest ? std::vector<int>{PXB} : std::vector<int>{PXB, NIC};
+      else o = {NIC};
+      src.push_back(i);
+      dst.push_back(j);
+      opts.push_back(o);
+    }
+    if (src.empty()) continue;
+    const size_t n = src.size();
+    std::vector<size_t> odo(n, 0);
+    bool have = false;
+    Rat best{0, 1};
+    while (true) {
+      std::map<std::pair<int, int>, int> share;   // (kind, group) -> lanes; kind 0 UP, 1 DN, 2 TX, 3 RX
+      for (size_t e = 0; e < n; ++e) {
+        const int c = opts[e][odo[e]], a = group(src[e]), d = group(dst[e]);
+        if (c == PXB) { share[{0, a}]++; share[{1, d}]++; }
+        if (c == NIC) { share[{2, a}]++; share[{3, d}]++; }
+      }
+      Rat worst{0, 1};
+      for (size_t e = 0; e < n; ++e) {
+        const int c = opts[e][odo[e]], a = group(src[e]), d = group(dst[e]);
+        const u128 x = (u128)D[(size_t)src[e] * N + dst[e]];
+        // rate as a fraction cap / sharers; start from the path rate
+        Rat rate{(u128)(c == NIC ? std::min(t.pcie, t.nic) : t.pcie), 1};
+        auto cap = [&](i64 c2, int k) { Rat r{(u128)c2, (u128)k}; if (less(r, rate)) rate = r; };
+        if (c == PXB) { cap(t.pcie, share[{0, a}]); cap(t.pcie, share[{1, d}]); }
+        if (c == NIC) { cap(t.nic, share[{2, a}]); cap(t.nic, share[{3, d}]); }
+        const Rat tm{x * rate.q, rate.p};   // bytes / rate
+        if (less(worst, tm)) worst = tm;
+      }
+      if (!have || less(worst, best)) { best = worst; have = true; }
+      size_t e = 0;
+      while (e < n && ++odo[e] == opts[e].size()) odo[e++] = 0;
+      if (e == n) break;
+    }
+    // best.p / best.q in units of 1 / l: l * p / q is whole (q divides the rates' lcm times sharers)
+    total += (u128)lambda * (u128)l + (u128)l * best.p / best.q;
+    if ((u128)l * best.p % best.q != 0) return UNSUPPORTED;   // not on the common grid
+  }
+  if (total > (u128)INT64_MAX) return UNSUPPORTED;
+  *num = (int64_t)total;
+  *den = l;
   return OK;
 }
 

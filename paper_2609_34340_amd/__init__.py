@@ -19,6 +19,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libvp.so")
 
 OK, INVALID_ARGUMENT, INVALID_DEMAND, NO_PROGRESS, CAPACITY, UNSUPPORTED, HIP_ERROR = range(7)
+RESTRICT_NEAREST_PATH = 1
+ROTATION_DYNAMIC_PATH, ROTATION_NEAREST_PATH = 0, 1
 PIX, PXB, NIC = 0, 1, 2
 STATUS_NAMES = {0: "ok", 1: "invalid argument", 2: "invalid demand", 3: "no progress",
                 4: "capacity exceeded", 5: "unsupported", 6: "HIP error"}
@@ -62,6 +64,8 @@ def lib():
     L.vp_catalog_families.argtypes = [vp] * 4
     L.vp_catalog_upload.argtypes = [vp, vp]
     L.vp_catalog_save.argtypes = [vp, vp, sz, C.POINTER(sz)]
+    L.vp_catalog_restrict.argtypes = [vp, i32, C.POINTER(vp)]
+    L.vp_rotation_time.argtypes = [vp, vp, i32, i64, vp, vp]
     L.vp_catalog_load.argtypes = [vp, sz, C.POINTER(vp)]
     L.vp_catalog_free.argtypes = [vp]
     L.vp_catalog_free.restype = None
@@ -139,11 +143,14 @@ def topology(topo) -> _Topology:
 class Catalog:
     """Offline channel-family catalog (host build, one upload per device)."""
 
-    def __init__(self, topo=None, *, payload: Optional[bytes] = None):
-        """Build the catalog of topology `topo` (Alg. 1), or load it from a
-        payload written by save()."""
+    def __init__(self, topo=None, *, payload: Optional[bytes] = None, restrict_of=None, rule: int = 0):
+        """Build the catalog of topology `topo` (Alg. 1), load it from a
+        payload written by save(), or restrict catalog `restrict_of` by `rule`."""
         h = C.c_void_p()
-        if payload is not None:
+        if restrict_of is not None:
+            _check(lib().vp_catalog_restrict(restrict_of.handle, rule, C.byref(h)), "vp_catalog_restrict")
+            topo = restrict_of.topo
+        elif payload is not None:
             buf = C.create_string_buffer(bytes(payload), len(payload))
             _check(lib().vp_catalog_load(buf, len(payload), C.byref(h)), "vp_catalog_load")
         else:
@@ -200,6 +207,20 @@ class Catalog:
     @classmethod
     def load(cls, payload: bytes) -> "Catalog":
         return cls(payload=payload)
+
+    def restrict(self, rule: int = 1) -> "Catalog":
+        """vp_catalog_restrict: 1 = families on nearest paths only."""
+        return Catalog(restrict_of=self, rule=rule)
+
+    def rotation_time(self, D: np.ndarray, path_rule: int, lambda_ns: int = 10_000):
+        """vp_rotation_time: (num, den) ns of the fixed cyclic rotation on D (host int64 [N, N])."""
+        D = np.ascontiguousarray(D, np.int64)
+        if D.shape != (self.N, self.N):
+            raise ValueError("demand must be [%d, %d]" % (self.N, self.N))
+        num, den = np.zeros(1, np.int64), np.zeros(1, np.int64)
+        _check(lib().vp_rotation_time(self._h, _np(D), path_rule, lambda_ns, _np(num), _np(den)),
+               "vp_rotation_time")
+        return int(num[0]), int(den[0])
 
     def upload(self, stream=None):
         _check(lib().vp_catalog_upload(self._h, _stream(stream)), "vp_catalog_upload")

@@ -80,6 +80,20 @@ vp_status vp_build_catalog(const vp_topology* t, vp_catalog** out) {
   return VP_OK;
 }
 
+vp_status vp_catalog_restrict(const vp_catalog* c, int32_t rule, vp_catalog** out) {
+  if (!c || !out) return set_error(VP_ERR_INVALID_ARGUMENT, "null catalog or output");
+  *out = nullptr;
+  vp_catalog* r = new (std::nothrow) vp_catalog();
+  if (!r) return set_error(VP_ERR_INVALID_ARGUMENT, "out of host memory");
+  vp_status s = vp::restrict_catalog(*c, rule, *r);
+  if (s != VP_OK) {
+    delete r;
+    return s;
+  }
+  *out = r;
+  return VP_OK;
+}
+
 vp_status vp_catalog_save(const vp_catalog* c, void* buf, size_t capacity, size_t* size) {
   if (!c || !size) return set_error(VP_ERR_INVALID_ARGUMENT, "null catalog or size");
   const std::vector<uint8_t> b = vp::serialize_catalog(*c);
@@ -523,6 +537,15 @@ vp_status vp_modeled_time(const vp_catalog* c, int32_t K, const int32_t* inst, c
   *num = (int64_t)total;
   *den = l;
   return VP_OK;
+}
+
+vp_status vp_rotation_time(const vp_catalog* c, const int64_t* demand, int32_t path_rule, int64_t lambda_ns,
+                           int64_t* num, int64_t* den) {
+  if (!c || !demand || !num || !den || lambda_ns < 0 || (path_rule != 0 && path_rule != 1))
+    return set_error(VP_ERR_INVALID_ARGUMENT, "bad rotation-time arguments");
+  for (int64_t x = 0; x < (int64_t)c->N * c->N; ++x)
+    if (demand[x] < 0) return set_error(VP_ERR_INVALID_ARGUMENT, "negative demand");
+  return vp::rotation_time(*c, demand, path_rule, lambda_ns, num, den);
 }
 
 }  // extern "C"

@@ -300,6 +300,36 @@ vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
   return VP_OK;
 }
 
+// Restricted catalogs for the peer/path ablation (Sec. 6.4): rule 1 keeps the
+// families in which every lane takes its group pair's nearest path (PIX in a
+// switch, PXB between two switches of one socket, the NICs otherwise), i.e.
+// drops every family with a NIC lane between two switches of one socket.
+// Canonical order is kept, so the result is a catalog of the same topology.
+vp_status restrict_catalog(const vp_catalog& in, int rule, vp_catalog& out) {
+  if (rule != 1) return set_error(VP_ERR_INVALID_ARGUMENT, "unknown catalog restriction");
+  set_shape(out, in.topo);
+  const std::vector<Cand> table = instance_table(in.topo);
+  const int Q = out.Q, W = in.topo.switches_per_socket;
+  std::vector<Found> lists[2];
+  for (int f = 0; f < in.F0 + in.F1; ++f) {
+    const bool remote = f >= in.F0;
+    Found fam;
+    fam.L.assign(Q * Q, 0);
+    fam.R.assign(Q * Q, 0);
+    bool keep = true;
+    for (int id : in.lfam[f]) {
+      const Cand& y = table[id];
+      const bool nic = y.cls == VP_PATH_NIC;
+      if (nic && !remote && y.src != y.dst && y.src / W == y.dst / W) keep = false;
+      ((nic && remote) ? fam.R : fam.L)[y.src * Q + y.dst]++;
+      fam.ids.push_back(id);
+    }
+    if (keep) lists[remote ? 1 : 0].push_back(std::move(fam));
+  }
+  fill_catalog(out, lists[0], lists[1]);
+  return VP_OK;
+}
+
 std::vector<uint8_t> serialize_catalog(const vp_catalog& c) {
   std::vector<uint8_t> b(kMagic, kMagic + 8);
   const vp_topology& t = c.topo;

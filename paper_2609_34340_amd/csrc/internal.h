@@ -75,6 +75,9 @@ namespace vp {
 vp_status set_error(vp_status s, const std::string& msg);
 vp_status build_catalog_host(const vp_topology& t, vp_catalog& c);
 std::vector<uint8_t> serialize_catalog(const vp_catalog& c);
+vp_status restrict_catalog(const vp_catalog& in, int rule, vp_catalog& out);
+vp_status rotation_time(const vp_catalog& c, const int64_t* D, int rule, int64_t lambda, int64_t* num,
+                        int64_t* den);
 vp_status deserialize_catalog(const uint8_t* p, size_t n, vp_catalog& c,
                               vp_status (*check_topology)(const vp_topology&));
 void build_device_image(vp_catalog& c);

@@ -1,0 +1,69 @@
+"""GPU planner on the extra demands (uniform AlltoAll, skew AlltoAllv at
+s = 0.4 / 0.6 / 0.8, Wan2.1-like head/context layouts) with the full catalog
+and with the nearest-path catalog of the peer/path ablation, against the
+oracle, bit-exact; the head/context demand itself comes from vp_demand_heads
+per all-to-all group."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import extra_cases
+import oracle
+import vpgen
+
+pytestmark = pytest.mark.gpu
+_cat = {}
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def vp():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_34340_amd as vp
+    vp.lib()
+    return vp
+
+
+def catalogs(vp, topo, nearest):
+    key = (topo.as_tuple(), nearest)
+    if key not in _cat:
+        c = vp.Catalog(topo)
+        if nearest:
+            c = c.restrict(vp.RESTRICT_NEAREST_PATH)
+        c.upload()
+        _cat[key] = (c, oracle.Catalog(topo, nearest=nearest))
+    return _cat[key]
+
+
+def check(vp, case, nearest, matrix):
+    gc, oc = catalogs(vp, case.topo, nearest)
+    D_dev = extra_cases.gpu_demand(vp, case, matrix)
+    D = extra_cases.oracle_demand(case, matrix)
+    torch.cuda.synchronize()
+    assert np.array_equal(D_dev.cpu().numpy(), D), "demand differs"
+    p = vp.plan_params(gc.N, case.unit)
+    st = vp.new_status()
+    s = vp.plan(gc, D_dev, p, status=st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    g = vp.schedule_to_host(s)
+    o = oc.plan(D, case.unit)
+    assert g["K"] == o["K"] and g["tau"] == o["tau"]
+    for key in ("family", "dst", "inst", "bytes"):
+        assert np.array_equal(g[key], o[key]), key
+
+
+@pytest.mark.parametrize("nearest", [False, True])
+@pytest.mark.parametrize("name", extra_cases.NAMES)
+def test_extra_plan_parity(vp, name, nearest):
+    case = vpgen.extra(name)
+    mats = range(extra_cases.ZIPF_MATRICES) if name == "zipf-pairs-16-s0.6" else [0]
+    for m in mats:
+        log("extra plan parity %s nearest=%s matrix %d" % (name, nearest, m))
+        check(vp, case, nearest, m)

@@ -176,3 +176,42 @@ def test_catalog_load_accepts_a_restricted_subset(vp):
     assert d.n_families == len(keep)
     ids = c.families()["ids"]
     assert np.array_equal(d.families()["ids"], ids[keep])
+
+
+@pytest.mark.parametrize("topo", [vpgen.tiny_topology(), vpgen.config(1).topo, vpgen.config(2).topo,
+                                  vpgen.config(5).topo, vpgen.Topology(3, 1, 2, 3), vpgen.Topology(2, 2, 1, 4)])
+def test_nearest_path_restriction_equals_oracle(vp, topo):
+    ours = vp.Catalog(topo).restrict(vp.RESTRICT_NEAREST_PATH)
+    ref = oracle.Catalog(topo, nearest=True)
+    assert (ours.n_shapes, ours.n_families) == (ref.n_shapes, ref.n_families)
+    sa, sb = ours.shapes(), ref.shapes()
+    for key in ("k", "fam_begin", "fam_end", "L", "R"):
+        assert np.array_equal(sa[key], sb[key]), key
+    fa, fb = ours.families(), ref.families()
+    for key in ("shape", "k", "ids"):
+        assert np.array_equal(fa[key], fb[key]), key
+    # a restricted catalog survives its own serialized form
+    assert vp.Catalog.load(ours.save()).n_families == ours.n_families
+    with pytest.raises(vp.VPError):
+        vp.Catalog(topo).restrict(7)
+
+
+@pytest.mark.parametrize("name", ["uniform-16", "zipf-pairs-16-s0.6", "wan21-H4C2", "wan21-H8C2"])
+def test_rotation_time_equals_oracle(vp, name):
+    import extra_cases
+    case = vpgen.extra(name)
+    D = extra_cases.oracle_demand(case, 1)
+    cat = vp.Catalog(case.topo)
+    for rule, near in [(vp.ROTATION_NEAREST_PATH, True), (vp.ROTATION_DYNAMIC_PATH, False)]:
+        assert cat.rotation_time(D, rule) == oracle.rotation_time(case.topo, D, near)
+
+
+def test_rotation_time_limits(vp):
+    cat = vp.Catalog(vpgen.config(3).topo)   # 64 ranks: too many path choices in one stage
+    D = np.ones((64, 64), np.int64) * 4096
+    np.fill_diagonal(D, 0)
+    with pytest.raises(vp.VPError):
+        cat.rotation_time(D, vp.ROTATION_DYNAMIC_PATH)
+    cat.rotation_time(D, vp.ROTATION_NEAREST_PATH)
+    with pytest.raises(vp.VPError):
+        cat.rotation_time(-D, vp.ROTATION_NEAREST_PATH)

@@ -246,3 +246,47 @@ def test_splitmix64_matches_published_outputs():
         k2 = list(base)
         k2[i] += 1
         assert not np.array_equal(oracle.splitmix_stream(4, key=k2), ref)
+
+
+# ------------------------------------------ "fixed nearest path" catalogs
+
+def test_nearest_path_tiny_topology_hand_count():
+    """One socket, two switches of two GPUs: of the 6 families (3 shapes),
+    the all-PIX family and the one-PXB-each-way family keep nearest paths;
+    the other three cross lanes need a NIC between the two switches."""
+    cat = oracle.Catalog(vpgen.tiny_topology(), nearest=True)
+    assert (cat.n_shapes, cat.n_families) == (2, 2)
+
+
+@pytest.mark.parametrize("topo,full", [(vpgen.tiny_topology(), False), (vpgen.config(1).topo, False),
+                                       (None, True)])
+def test_brute_force_nearest_paths_equal_restricted_catalog(topo, full):
+    """Every feasible channel whose lanes all take their pair's nearest path
+    (rank-level brute force) is exactly the instantiations of the restricted
+    catalog's families."""
+    topo = topo or two_node_one_socket()
+    tm = TopoModel(topo)
+    cat = oracle.Catalog(topo, full=full, nearest=True)
+    inst = set()
+    for f in cluster_families(cat):
+        got = instantiate(tm, f)
+        assert got and not (got & inst)
+        inst |= got
+    assert inst == brute_force_channels(tm, nearest=True)
+
+
+@pytest.mark.parametrize("cid", [2, 3, 5])
+def test_nearest_path_catalog_is_the_filtered_catalog(cid):
+    """Multi-node: the restricted catalog is the circulant catalog minus the
+    families with a NIC lane between two switches of one socket, in the same
+    order."""
+    topo = vpgen.config(cid).topo
+    tm = TopoModel(topo)
+    full, near = oracle.Catalog(topo), oracle.Catalog(topo, nearest=True)
+    keep = []
+    for f in range(full.n_families):
+        fam = full.cluster_family(f)
+        ok = all(int(c) == tm.nearest_class(int(a), int(d)) for c, a, d in zip(fam["cls"], fam["a"], fam["d"]))
+        if ok:
+            keep.append(fam_key(fam))
+    assert [fam_key(near.cluster_family(f)) for f in range(near.n_families)] == keep

@@ -268,3 +268,42 @@ def test_capacity_limit_is_reported():
     D = demand_for(1)
     s = cat.plan(D, w.row_bytes, k_max=3, check=False)
     assert s["status"] == oracle.CAPACITY and s["K"] == 3
+
+
+# ------------------------------------ extra demands and restricted catalogs
+
+import extra_cases  # noqa: E402
+
+
+@pytest.mark.parametrize("nearest", [False, True])
+@pytest.mark.parametrize("name", extra_cases.NAMES)
+def test_extra_demands_plan_valid(name, nearest):
+    """P1-P3 on the uniform, skew and head/context demands, with the full and
+    the nearest-path catalogs; with the latter every lane takes its pair's
+    nearest path."""
+    case = vpgen.extra(name)
+    tm = TopoModel(case.topo)
+    cat = oracle.Catalog(case.topo, nearest=nearest)
+    D = extra_cases.oracle_demand(case, 0)
+    s = cat.plan(D, case.unit)
+    schedule_valid(tm, D, s, cat.table()["cls"])
+    assert 0 < s["K"] <= 8 * case.topo.n_ranks
+    assert (s["bytes"].sum(axis=1) > 0).all()
+    if nearest:
+        cls = cat.table()["cls"]
+        g = case.topo.gpus_per_switch
+        for k in range(s["K"]):
+            for i in range(case.topo.n_ranks):
+                assert cls[s["inst"][k][i]] == tm.nearest_class(i // g, s["dst"][k][i] // g)
+
+
+def test_head_context_demand_is_block_diagonal():
+    """Wan2.1 H4C2: ranks exchange only inside their group of four; each
+    pair moves 9450 tokens x 10 heads x 256 B."""
+    case = vpgen.extra("wan21-H4C2")
+    D = extra_cases.oracle_demand(case)
+    want = np.zeros((8, 8), np.int64)
+    for b in (0, 4):
+        want[b:b + 4, b:b + 4] = 9450 * 10 * 256
+    np.fill_diagonal(want, 0)
+    assert np.array_equal(D, want)

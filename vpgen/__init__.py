@@ -8,6 +8,8 @@ counting, no catalog, no planning, no packing.  It produces
 * token -> expert routing tables (top-k without replacement under a stated
   expert-popularity law),
 * bf16 token rows and Ulysses-style head splits,
+* demand matrices given directly for AlltoAll / skew AlltoAllv cases and the
+  head/context layouts of a Wan2.1-like sequence-parallel model,
 
 for the five workload configurations C1..C5 that stand in for the paper's
 workloads (random top-k MoE routing over 256 experts with k = 8 and hidden
@@ -28,7 +30,8 @@ import numpy as np
 __all__ = [
     "Topology", "Workload", "CONFIGS", "config", "tiny_topology",
     "routing", "routing_all", "tokens_bf16", "head_split", "bf16_from_f32",
-    "expert_weights",
+    "expert_weights", "DemandCase", "EXTRA", "extra", "uniform_demand", "zipf_pair_demand",
+    "hc_groups", "hc_layout",
 ]
 
 
@@ -214,3 +217,94 @@ def head_split(heads: int, n_ranks: int) -> np.ndarray:
     if extra:
         counts[n_ranks - extra:] += 1
     return np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+
+
+# ---------------------------------------------------------------------------
+# Demand matrices given directly (AlltoAll / AlltoAllv microbenchmarks) and
+# the Wan2.1 head/context layouts (Sec. 6 "Workloads", skew AlltoAllv,
+# Sec. 6.2 Wan2.1, Sec. 6.4 ablation).  Only inputs: byte volumes drawn or
+# laid out here are what a caller asks the scheduler to move.
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class DemandCase:
+    name: str
+    topo: Topology
+    unit: int               # pack granule; every entry is a multiple of it
+    kind: str               # "uniform" | "zipf_pairs" | "ulysses_hc"
+    per_pair: int = 0       # uniform: bytes per ordered pair
+    per_rank: int = 0       # zipf_pairs: bytes each source sends in total (before rounding)
+    zipf_s: float = 0.0
+    seq: int = 0            # ulysses_hc: global sequence length
+    heads: int = 0
+    head_dim: int = 0
+    H: int = 0              # head-parallel degree (ranks of one all-to-all group)
+    C: int = 0              # context-parallel degree (number of groups)
+
+
+EXTRA = {
+    "uniform-16": DemandCase("uniform-16", Topology(2), 4096, "uniform", per_pair=64 << 20),
+    "zipf-pairs-16-s0.4": DemandCase("zipf-pairs-16-s0.4", Topology(2), 4096, "zipf_pairs", per_rank=1 << 30,
+                                     zipf_s=0.4),
+    "zipf-pairs-16-s0.6": DemandCase("zipf-pairs-16-s0.6", Topology(2), 4096, "zipf_pairs", per_rank=1 << 30,
+                                     zipf_s=0.6),
+    "zipf-pairs-16-s0.8": DemandCase("zipf-pairs-16-s0.8", Topology(2), 4096, "zipf_pairs", per_rank=1 << 30,
+                                     zipf_s=0.8),
+    "wan21-H8C1": DemandCase("wan21-H8C1", Topology(1), 256, "ulysses_hc", seq=75600, heads=40, head_dim=128,
+                             H=8, C=1),
+    "wan21-H4C2": DemandCase("wan21-H4C2", Topology(1), 256, "ulysses_hc", seq=75600, heads=40, head_dim=128,
+                             H=4, C=2),
+    "wan21-H8C2": DemandCase("wan21-H8C2", Topology(2), 256, "ulysses_hc", seq=75600, heads=40, head_dim=128,
+                             H=8, C=2),
+    "wan21-H4C4": DemandCase("wan21-H4C4", Topology(2), 256, "ulysses_hc", seq=75600, heads=40, head_dim=128,
+                             H=4, C=4),
+}
+
+
+def extra(name: str) -> DemandCase:
+    return EXTRA[name]
+
+
+def uniform_demand(case: DemandCase) -> np.ndarray:
+    """int64 [N, N]: every rank sends case.per_pair bytes to every other rank."""
+    N = case.topo.n_ranks
+    D = np.full((N, N), case.per_pair, dtype=np.int64)
+    np.fill_diagonal(D, 0)
+    return D
+
+
+def zipf_pair_demand(case: DemandCase, matrix: int = 0) -> np.ndarray:
+    """int64 [N, N] skew AlltoAllv demand: each source splits about
+    case.per_rank bytes over its N - 1 destinations with Zipf(s) weights
+    (1/rank^s) over a per-source random order of the destinations, each
+    volume rounded down to the unit.  Seeded by (1, s in thousandths,
+    matrix, source)."""
+    N, u = case.topo.n_ranks, case.unit
+    w = np.arange(1, N, dtype=np.float64) ** (-case.zipf_s)
+    w /= w.sum()
+    D = np.zeros((N, N), dtype=np.int64)
+    for i in range(N):
+        r = _rng(1, int(round(case.zipf_s * 1000)), matrix, i)
+        dst = np.array([j for j in range(N) if j != i])
+        order = r.permutation(N - 1)
+        units = np.floor(w * (case.per_rank // u)).astype(np.int64)
+        D[i, dst[order]] = units * u
+    return D
+
+
+def hc_groups(case: DemandCase) -> np.ndarray:
+    """int64 [C, H]: the ranks of each head-parallel all-to-all group
+    (contiguous blocks of H ranks)."""
+    N = case.topo.n_ranks
+    if case.H * case.C != N:
+        raise ValueError("H * C must equal the rank count")
+    return np.arange(N, dtype=np.int64).reshape(case.C, case.H)
+
+
+def hc_layout(case: DemandCase):
+    """(tokens per rank, head split of one group): each rank holds
+    seq / (H*C) tokens of all heads; inside its group the heads are split
+    evenly over the H ranks."""
+    if case.seq % (case.H * case.C) or case.heads % case.H:
+        raise ValueError("sequence and heads must divide evenly")
+    return case.seq // (case.H * case.C), head_split(case.heads, case.H)
