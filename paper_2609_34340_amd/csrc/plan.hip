@@ -287,6 +287,23 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
   }
   wave_sync();
 
+  // The credit rows of the owned groups' out- and in-instances do not change
+  // during the run: with few enough of them they are read once here and held
+  // in registers, and a half-step reads only the other side's assignment.
+  constexpr bool kHold = 2 * MG * g * g2 <= 64;
+  int32_t hs[kHold ? MG : 1][g][g2], hd[kHold ? MG : 1][g][g2];
+  if constexpr (kHold) {
+#pragma unroll
+    for (int r = 0; r < MG; ++r)
+#pragma unroll
+      for (int m = 0; m < g; ++m)
+#pragma unroll
+        for (int e = 0; e < g2; ++e) {
+          hs[r][m][e] = fc.H[o[r][m] * g2 + e];
+          hd[r][m][e] = fc.H[nn_[r][m] * g2 + e];
+        }
+  }
+
   // Alternating Algorithm: source half, then destination half.  A half that
   // changes nothing, other than the very first, leaves a fixed point: the
   // half before it made its own side optimal against this side, which has
@@ -305,7 +322,7 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
         for (int m = 0; m < g; ++m) {
           jl[r][m] = DL[o[r][m]];
 #pragma unroll
-          for (int e = 0; e < g2; ++e) row[r][m][e] = fc.H[o[r][m] * g2 + e];
+          for (int e = 0; e < g2; ++e) row[r][m][e] = kHold ? hs[r][m][e] : fc.H[o[r][m] * g2 + e];
         }
 #pragma unroll
       for (int r = 0; r < MG; ++r) {
@@ -362,7 +379,7 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
         for (int m = 0; m < g; ++m) {
           il[r][m] = SL[nn_[r][m]];
 #pragma unroll
-          for (int e = 0; e < g2; ++e) row[r][m][e] = fc.H[nn_[r][m] * g2 + e];
+          for (int e = 0; e < g2; ++e) row[r][m][e] = kHold ? hd[r][m][e] : fc.H[nn_[r][m] * g2 + e];
         }
 #pragma unroll
       for (int r = 0; r < MG; ++r) {
