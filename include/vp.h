@@ -53,13 +53,23 @@ typedef enum {
 } vp_status;
 
 /* Path classes of a lane (Sec. 3; Fig. 1 legend): same switch, same socket
- * through the root complex, and through the switches' NICs. */
-enum { VP_PATH_PIX = 0, VP_PATH_PXB = 1, VP_PATH_NIC = 2 };
+ * through the root complex, through the switches' NICs, and (with
+ * VP_TOPO_SYS_P2P) between sockets of one node through both root complexes
+ * and the inter-socket link. */
+enum { VP_PATH_PIX = 0, VP_PATH_PXB = 1, VP_PATH_NIC = 2, VP_PATH_SYS = 3 };
+
+/* vp_topology.flags.  VP_TOPO_SYS_P2P: GPUs under different sockets of one
+ * node reach each other peer to peer (path class SYS: the source switch's
+ * uplink, the directed link from the source socket to the destination
+ * socket, the destination switch's downlink; PCIe rate).  Without it such
+ * pairs go through the NICs only. */
+enum { VP_TOPO_SYS_P2P = 1 };
 
 /* A PCIe cluster (Sec. 3 "Model setup", Sec. 5 "Topology, path, and rate
  * model").  Rank = ((node * sockets + socket) * switches + switch) * gpus + local;
  * one rank group per PCIe switch.  Every switch has one NIC.  Rates are in
- * bytes per nanosecond; a NIC path runs at min(pcie, nic).
+ * bytes per nanosecond; a NIC path runs at min(pcie, nic), PIX, PXB and SYS
+ * paths at the PCIe rate.
  * Limits of this build: gpus_per_switch in [2, 4], sockets*switches <= 8,
  * nics_per_switch == 1, n_nodes in [1, 256], N <= 1024. */
 typedef struct {
@@ -68,7 +78,7 @@ typedef struct {
   int32_t switches_per_socket;
   int32_t gpus_per_switch;
   int32_t nics_per_switch;
-  int32_t flags;               /* reserved, must be 0 */
+  int32_t flags;               /* 0 or VP_TOPO_SYS_P2P (then sockets_per_node <= 4) */
   int64_t pcie_bytes_per_ns;
   int64_t nic_bytes_per_ns;
 } vp_topology;
@@ -123,9 +133,10 @@ vp_status vp_catalog_families(const vp_catalog* cat, int32_t* shape, int32_t* k,
  * handle holding the families of `cat` that satisfy `rule`, in the same
  * canonical order.  VP_RESTRICT_NEAREST_PATH keeps the families in which
  * every lane takes its group pair's nearest path (PIX inside a switch, PXB
- * between two switches of one socket, the NICs otherwise), i.e. drops every
- * family with a NIC lane between two switches of one socket ("fixed nearest
- * path, demand-aware peers").  Host only; free with vp_catalog_free.  An
+ * between two switches of one socket, SYS between sockets when enabled, the
+ * NICs otherwise), i.e. drops every family with a NIC lane between two
+ * switches of one node that a PCIe peer-to-peer path also joins ("fixed
+ * nearest path, demand-aware peers").  Host only; free with vp_catalog_free.  An
  * unknown rule returns VP_ERR_INVALID_ARGUMENT. */
 enum { VP_RESTRICT_NEAREST_PATH = 1 };
 vp_status vp_catalog_restrict(const vp_catalog* cat, int32_t rule, vp_catalog** out);
@@ -427,7 +438,8 @@ vp_status vp_modeled_time(const vp_catalog* cat, int32_t K, const int32_t* inst,
  * stages with no bytes are skipped.  path_rule VP_ROTATION_NEAREST_PATH puts
  * each lane on its pair's nearest path; VP_ROTATION_DYNAMIC_PATH lets every
  * stage pick, among each pair's paths (PXB or NIC between two switches of a
- * socket), the choice that finishes the stage first.  Lanes on one directed
+ * socket, SYS or NIC between sockets when enabled), the choice that
+ * finishes the stage first.  Lanes on one directed
  * resource share its capacity equally (a stage need not be contention-free),
  * so a lane runs at min(path rate, capacity / sharers) over its resources;
  * a stage takes lambda_ns plus its slowest lane.  *num / *den is the exact

@@ -21,7 +21,8 @@ _SRC = os.path.join(_HERE, "vp_oracle.cpp")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 OK, INVALID_ARGUMENT, INVALID_DEMAND, NO_PROGRESS, CAPACITY, UNSUPPORTED = range(6)
-PIX, PXB, NIC = 0, 1, 2
+PIX, PXB, NIC, SYS = 0, 1, 2, 3
+TOPO_SYS_P2P = 1
 
 DEFAULT_LAMBDA_NS = 10_000
 DEFAULT_N_START = 4
@@ -40,8 +41,13 @@ def build(force: bool = True) -> str:
 class _Topo(C.Structure):
     _fields_ = [("n_nodes", C.c_int32), ("sockets_per_node", C.c_int32),
                 ("switches_per_socket", C.c_int32), ("gpus_per_switch", C.c_int32),
-                ("nics_per_switch", C.c_int32), ("pad", C.c_int32),
+                ("nics_per_switch", C.c_int32), ("flags", C.c_int32),
                 ("pcie_bytes_per_ns", C.c_int64), ("nic_bytes_per_ns", C.c_int64)]
+
+
+def _topo(topo) -> "_Topo":
+    return _Topo(topo.n_nodes, topo.sockets_per_node, topo.switches_per_socket, topo.gpus_per_switch,
+                 topo.nics_per_switch, getattr(topo, "flags", 0), topo.pcie_bytes_per_ns, topo.nic_bytes_per_ns)
 
 
 class _Params(C.Structure):
@@ -108,7 +114,7 @@ class Catalog:
     nearest path (the "fixed nearest path" ablation of Sec. 6.4)."""
 
     def __init__(self, topo, full: bool = False, nearest: bool = False):
-        t = _Topo(*topo.as_tuple()[:5], 0, *topo.as_tuple()[5:])
+        t = _topo(topo)
         h = C.c_void_p()
         st = lib().orc_catalog_build(C.byref(t), (1 if full else 0) | (2 if nearest else 0), C.byref(h))
         if st != OK:
@@ -264,7 +270,7 @@ def receive_counts(words: np.ndarray, signal: np.ndarray, n_local: int) -> np.nd
 
 def rotation_time(topo, D: np.ndarray, nearest: bool, lambda_ns: int = DEFAULT_LAMBDA_NS):
     """Exact (num, den) ns of the fixed cyclic peer rotation on D (Sec. 6.4)."""
-    t = _Topo(*topo.as_tuple()[:5], 0, *topo.as_tuple()[5:])
+    t = _topo(topo)
     Dc = np.ascontiguousarray(D, np.int64)
     num, den = np.zeros(1, np.int64), np.zeros(1, np.int64)
     st = lib().orc_rotation_time(C.byref(t), _p(Dc), 1 if nearest else 0, lambda_ns, _p(num), _p(den))

@@ -11,9 +11,11 @@ Topology model (restated independently): rank = ((node*S + socket)*W +
 switch)*g + local; a rank group is one switch.  Directed shared resources:
 UP/DN of each switch's root-complex link, TX/RX of each switch's NIC.  Paths:
 PIX (same switch, no shared resource), PXB (same socket, different switch:
-UP(src switch), DN(dst switch)), NIC (TX(src switch), RX(dst switch)).  The
-endpoint GPU<->switch links are added as ("GU", rank) / ("GD", rank) when a
-cluster-level footprint is needed.
+UP(src switch), DN(dst switch)), NIC (TX(src switch), RX(dst switch)) and,
+when the topology enables cross-socket peer to peer, SYS (other socket of the
+same node: UP(src switch), the directed link between the two sockets,
+DN(dst switch)).  The endpoint GPU<->switch links are added as ("GU", rank) /
+("GD", rank) when a cluster-level footprint is needed.
 """
 from __future__ import annotations
 
@@ -24,7 +26,7 @@ from typing import Dict, List, Tuple
 
 import numpy as np
 
-PIX, PXB, NIC = 0, 1, 2
+PIX, PXB, NIC, SYS = 0, 1, 2, 3
 
 
 class TopoModel:
@@ -38,6 +40,7 @@ class TopoModel:
         self.N = self.G * self.g
         self.pcie = topo.pcie_bytes_per_ns
         self.nic = topo.nic_bytes_per_ns
+        self.sys = bool(getattr(topo, "flags", 0) & 1)
 
     def group(self, rank: int) -> int:
         return rank // self.g
@@ -55,6 +58,8 @@ class TopoModel:
             out.append(PIX)
         elif self.node(a) == self.node(d) and self.socket(a) == self.socket(d):
             out.append(PXB)
+        elif self.node(a) == self.node(d) and self.sys:
+            out.append(SYS)
         out.append(NIC)
         return out
 
@@ -75,6 +80,8 @@ class TopoModel:
             return ()
         if cls == PXB:
             return (("UP", a), ("DN", d))
+        if cls == SYS:
+            return (("UP", a), ("X", self.node(a), self.socket(a), self.socket(d)), ("DN", d))
         return (("TX", a), ("RX", d))
 
     def footprint(self, cls: int, i: int, j: int) -> Tuple:

@@ -36,11 +36,12 @@ typedef unsigned __int128 u128;
 
 enum Status { OK = 0, INVALID_ARGUMENT = 1, INVALID_DEMAND = 2, NO_PROGRESS = 3,
               CAPACITY = 4, UNSUPPORTED = 5 };
-enum Cls { PIX = 0, PXB = 1, NIC = 2 };
+enum Cls { PIX = 0, PXB = 1, NIC = 2, SYS = 3 };
 
 struct Topo {
   int n_nodes, sockets, switches, g, nics;
   i64 pcie, nic;
+  bool sys;   // GPUs under different sockets of a node reach each other peer to peer
   int Q() const { return sockets * switches; }        // switch slots per node
   int G() const { return n_nodes * Q(); }              // rank groups (one per switch)
   int N() const { return G() * g; }                    // ranks
@@ -53,7 +54,11 @@ struct Topo {
 // links are endpoint-local and not modeled.  Path classes: PIX (same switch,
 // no shared resource), PXB (same socket, other switch: UP_src, DN_dst) and NIC
 // (any pair through the source switch's NIC and the destination switch's NIC:
-// TX_src, RX_dst).  A path's rate is the minimum of its links.
+// TX_src, RX_dst).  A path's rate is the minimum of its links.  With
+// cross-socket peer-to-peer enabled, SYS joins two switches of different
+// sockets of one node through both root complexes and the directed
+// inter-socket link: UP_src, X(socket_src -> socket_dst), DN_dst, at the PCIe
+// rate (the inter-socket link is taken to be faster than one PCIe link).
 // ---------------------------------------------------------------------------
 struct Inst {
   int id;          // canonical id (order of (cls, src, dst, copy))
@@ -86,6 +91,13 @@ std::vector<Inst> local_table(const Topo& t) {
     for (int q = 0; q < Q; ++q)
       for (int q2 = 0; q2 < Q; ++q2)
         v.push_back({0, NIC, q, q2, 0, false, rate_of(t, NIC), {2 * Q + q, 3 * Q + q2}});
+  // socket link s -> s2: resource 4Q + s * sockets + s2
+  if (t.sys)
+    for (int q = 0; q < Q; ++q)
+      for (int q2 = 0; q2 < Q; ++q2) {
+        const int s = q / t.switches, s2 = q2 / t.switches;
+        if (s != s2) v.push_back({0, SYS, q, q2, 0, false, rate_of(t, SYS), {q, Q + q2, 4 * Q + s * t.sockets + s2}});
+      }
   std::sort(v.begin(), v.end(), [](const Inst& x, const Inst& y) {
     return std::make_tuple(x.cls, x.a, x.d, x.copy) < std::make_tuple(y.cls, y.a, y.d, y.copy);
   });
@@ -113,6 +125,14 @@ std::vector<Inst> cluster_table(const Topo& t) {
     for (int a = 0; a < G; ++a)
       for (int d = 0; d < G; ++d)
         v.push_back({0, NIC, a, d, 0, false, rate_of(t, NIC), {2 * G + a, 3 * G + d}});
+  // socket link of node n, s -> s2: resource 4G + (n * sockets + s) * sockets + s2
+  if (t.sys)
+    for (int a = 0; a < G; ++a)
+      for (int d = 0; d < G; ++d) {
+        const int n = a / Q, s = (a % Q) / t.switches, s2 = (d % Q) / t.switches;
+        if (n == d / Q && s != s2)
+          v.push_back({0, SYS, a, d, 0, false, rate_of(t, SYS), {a, G + d, 4 * G + (n * t.sockets + s) * t.sockets + s2}});
+      }
   std::sort(v.begin(), v.end(), [](const Inst& x, const Inst& y) {
     return std::make_tuple(x.cls, x.a, x.d, x.copy) < std::make_tuple(y.cls, y.a, y.d, y.copy);
   });
@@ -331,24 +351,28 @@ struct Catalog {
 
 // The nearest path of an ordered group pair (Sec. 6.4 peer/path ablation,
 // "fixed nearest path"): PIX inside a switch, PXB between two switches of one
-// socket, the NICs otherwise.  A family keeps only lanes on their pair's
-// nearest path; under the topology model the only other choice is a NIC lane
-// between two switches of one socket.
-bool nearest_only(const std::vector<Inst>& table, const Fam& f, int switches, bool remote_set) {
+// socket, SYS between sockets of one node when enabled, the NICs otherwise.
+// A family keeps only lanes on their pair's nearest path; under the topology
+// model the only other choice is a NIC lane between two switches of one node
+// that a PXB (or SYS) path also joins.  Group ids are node-major, so
+// a / Q is the node and (a % Q) / switches the socket.
+bool nearest_only(const std::vector<Inst>& table, const Fam& f, const Topo& t, bool remote_set) {
+  const int Q = t.Q();
   for (int id : f) {
     const Inst& r = table[id];
-    const bool same_socket = r.a != r.d && r.a / switches == r.d / switches;
-    if (r.cls == NIC && !remote_set && same_socket) return false;
+    if (r.cls != NIC || remote_set || r.a == r.d || r.a / Q != r.d / Q) continue;
+    const bool same_socket = (r.a % Q) / t.switches == (r.d % Q) / t.switches;
+    if (same_socket || t.sys) return false;
   }
   return true;
 }
 
-void keep_nearest(std::map<ShapeKey, std::vector<Fam>>& b, const std::vector<Inst>& table, int switches,
+void keep_nearest(std::map<ShapeKey, std::vector<Fam>>& b, const std::vector<Inst>& table, const Topo& t,
                   bool remote_set) {
   for (auto it = b.begin(); it != b.end();) {
     std::vector<Fam> keep;
     for (const Fam& f : it->second)
-      if (nearest_only(table, f, switches, remote_set)) keep.push_back(f);
+      if (nearest_only(table, f, t, remote_set)) keep.push_back(f);
     if (keep.empty()) it = b.erase(it);
     else { it->second = keep; ++it; }
   }
@@ -362,12 +386,12 @@ void build_circulant(Catalog& C, bool nearest) {
   const Topo& t = C.topo;
   const int Q = t.Q(), g = t.g, nn = t.n_nodes;
   C.table = local_table(t);
-  const int n_res = 4 * Q;
+  const int n_res = 4 * Q + t.sockets * t.sockets;
   // k = 0 set: PIX, PXB, NIC between slots of the same node (loopback).
   std::vector<Inst> set0;
   for (Inst r : C.table) { r.remote = false; set0.push_back(r); }
   auto b0 = run_alg1(C.table, set0, Q, g, n_res);
-  if (nearest) keep_nearest(b0, C.table, t.switches, false);
+  if (nearest) keep_nearest(b0, C.table, t, false);
   // k != 0 set: PIX, PXB, and NIC lanes to the same slot pattern on another node.
   std::map<ShapeKey, std::vector<Fam>> b1;
   if (nn > 1) {
@@ -431,10 +455,8 @@ void build_full(Catalog& C, bool nearest) {
   const Topo& t = C.topo;
   const int G = t.G();
   C.table = cluster_table(t);
-  auto b = run_alg1(C.table, C.table, G, t.g, 4 * G);
-  // cluster groups a and d share a socket when they share a node and a socket
-  // slot range; group ids are node-major, so a / switches is the socket index
-  if (nearest) keep_nearest(b, C.table, t.switches, false);
+  auto b = run_alg1(C.table, C.table, G, t.g, 4 * G + t.n_nodes * t.sockets * t.sockets);
+  if (nearest) keep_nearest(b, C.table, t, false);
   for (const auto& kv : b) {
     CShape s;
     s.k = -1;
@@ -834,7 +856,7 @@ struct orc_catalog;   // opaque: a Catalog
 
 struct orc_topology {
   int32_t n_nodes, sockets_per_node, switches_per_socket, gpus_per_switch, nics_per_switch;
-  int32_t pad;
+  int32_t flags;   // bit 0: peer to peer between sockets (SYS paths)
   int64_t pcie_bytes_per_ns, nic_bytes_per_ns;
 };
 
@@ -850,10 +872,10 @@ struct orc_params {
 int orc_catalog_build(const orc_topology* tp, int mode, orc_catalog** out) {
   if (!tp || !out) return INVALID_ARGUMENT;
   Topo t{tp->n_nodes, tp->sockets_per_node, tp->switches_per_socket, tp->gpus_per_switch,
-         tp->nics_per_switch, tp->pcie_bytes_per_ns, tp->nic_bytes_per_ns};
+         tp->nics_per_switch, tp->pcie_bytes_per_ns, tp->nic_bytes_per_ns, (tp->flags & 1) != 0};
   // every ordered pair needs a path: one NIC per switch, at least two GPUs per switch
   if (t.n_nodes < 1 || t.sockets < 1 || t.switches < 1 || t.g < 2 || t.nics != 1 ||
-      t.pcie < 1 || t.nic < 1)
+      t.pcie < 1 || t.nic < 1 || (tp->flags & ~1) != 0)
     return INVALID_ARGUMENT;
   Catalog* C = new Catalog();
   C->topo = t;
@@ -1042,13 +1064,13 @@ int orc_receive_counts(const uint32_t* words, const int32_t* signal, int32_t N, 
 // (nearest = 1) or, per stage, the path vector that ends the stage first
 // (nearest = 0), every vector tried.  Lanes sharing a directed resource
 // split its capacity equally: a lane's rate is the least of its path rate
-// and capacity / sharers over its resources (UP and DN links carry the PCIe
-// rate, TX and RX the NIC rate).  Stage time = lambda + max bytes / rate.
+// and capacity / sharers over its resources (UP and DN links and the socket
+// link carry the PCIe rate, TX and RX the NIC rate).  Stage time = lambda + max bytes / rate.
 // The result is the exact rational total in ns.
 int orc_rotation_time(const orc_topology* tp, const int64_t* D, int32_t nearest, int64_t lambda,
                       int64_t* num, int64_t* den) {
   Topo t{tp->n_nodes, tp->sockets_per_node, tp->switches_per_socket, tp->gpus_per_switch,
-         tp->nics_per_switch, tp->pcie_bytes_per_ns, tp->nic_bytes_per_ns};
+         tp->nics_per_switch, tp->pcie_bytes_per_ns, tp->nic_bytes_per_ns, (tp->flags & 1) != 0};
   const int N = t.N(), Q = t.Q();
   auto group = [&](int r) { return r / t.g; };
   auto node = [&](int a) { return a / Q; };
@@ -1070,6 +1092,7 @@ int orc_rotation_time(const orc_topology* tp, const int64_t* D, int32_t nearest,
       std::vector<int> o;
       if (a == d) o = {PIX};
       else if (node(a) == node(d) && socket(a) == socket(d)) o = nearest ? std::vector<int>{PXB} : std::vector<int>{PXB, NIC};
+      else if (node(a) == node(d) && t.sys) o = nearest ? std::vector<int>{SYS} : std::vector<int>{SYS, NIC};
       else o = {NIC};
       src.push_back(i);
       dst.push_back(j);
@@ -1081,10 +1104,14 @@ int orc_rotation_time(const orc_topology* tp, const int64_t* D, int32_t nearest,
     bool have = false;
     Rat best{0, 1};
     while (true) {
-      std::map<std::pair<int, int>, int> share;   // (kind, group) -> lanes; kind 0 UP, 1 DN, 2 TX, 3 RX
+      // (kind, index) -> lanes; kind 0 UP, 1 DN (switch), 2 TX, 3 RX (NIC),
+      // 4 the socket link (node, source socket, destination socket)
+      std::map<std::pair<int, int>, int> share;
+      auto xlink = [&](int a, int d) { return (node(a) * t.sockets + socket(a)) * t.sockets + socket(d); };
       for (size_t e = 0; e < n; ++e) {
         const int c = opts[e][odo[e]], a = group(src[e]), d = group(dst[e]);
-        if (c == PXB) { share[{0, a}]++; share[{1, d}]++; }
+        if (c == PXB || c == SYS) { share[{0, a}]++; share[{1, d}]++; }
+        if (c == SYS) share[{4, xlink(a, d)}]++;
         if (c == NIC) { share[{2, a}]++; share[{3, d}]++; }
       }
       Rat worst{0, 1};
@@ -1094,7 +1121,8 @@ int orc_rotation_time(const orc_topology* tp, const int64_t* D, int32_t nearest,
         // rate as a fraction cap / sharers; start from the path rate
         Rat rate{(u128)(c == NIC ? std::min(t.pcie, t.nic) : t.pcie), 1};
         auto cap = [&](i64 c2, int k) { Rat r{(u128)c2, (u128)k}; if (less(r, rate)) rate = r; };
-        if (c == PXB) { cap(t.pcie, share[{0, a}]); cap(t.pcie, share[{1, d}]); }
+        if (c == PXB || c == SYS) { cap(t.pcie, share[{0, a}]); cap(t.pcie, share[{1, d}]); }
+        if (c == SYS) cap(t.pcie, share[{4, xlink(a, d)}]);
         if (c == NIC) { cap(t.nic, share[{2, a}]); cap(t.nic, share[{3, d}]); }
         const Rat tm{x * rate.q, rate.p};   // bytes / rate
         if (less(worst, tm)) worst = tm;

@@ -20,6 +20,8 @@ LIB_PATH = os.path.join(_HERE, "libvp.so")
 
 OK, INVALID_ARGUMENT, INVALID_DEMAND, NO_PROGRESS, CAPACITY, UNSUPPORTED, HIP_ERROR = range(7)
 RESTRICT_NEAREST_PATH = 1
+PATH_PIX, PATH_PXB, PATH_NIC, PATH_SYS = 0, 1, 2, 3
+TOPO_SYS_P2P = 1
 ROTATION_DYNAMIC_PATH, ROTATION_NEAREST_PATH = 0, 1
 PIX, PXB, NIC = 0, 1, 2
 STATUS_NAMES = {0: "ok", 1: "invalid argument", 2: "invalid demand", 3: "no progress",
@@ -136,8 +138,8 @@ def _stream(stream=None):
 def topology(topo) -> _Topology:
     """vp_topology from any object with the vpgen.Topology fields."""
     return _Topology(topo.n_nodes, topo.sockets_per_node, topo.switches_per_socket,
-                     topo.gpus_per_switch, topo.nics_per_switch, 0, topo.pcie_bytes_per_ns,
-                     topo.nic_bytes_per_ns)
+                     topo.gpus_per_switch, topo.nics_per_switch, getattr(topo, "flags", 0),
+                     topo.pcie_bytes_per_ns, topo.nic_bytes_per_ns)
 
 
 class Catalog:

@@ -44,7 +44,9 @@ const char* vp_last_error(void) { return vp::g_last_error.c_str(); }
 namespace {
 
 vp_status check_topology(const vp_topology& t) {
-  if (t.flags != 0) return set_error(VP_ERR_UNSUPPORTED, "topology flags must be 0");
+  if ((t.flags & ~VP_TOPO_SYS_P2P) != 0) return set_error(VP_ERR_UNSUPPORTED, "unknown topology flags");
+  if ((t.flags & VP_TOPO_SYS_P2P) && t.sockets_per_node > 4)
+    return set_error(VP_ERR_UNSUPPORTED, "cross-socket peer to peer needs at most 4 sockets");
   if (t.n_nodes < 1 || t.n_nodes > vp::kMaxNodes)
     return set_error(VP_ERR_UNSUPPORTED, "n_nodes must be in [1, 256]");
   if (t.sockets_per_node < 1 || t.switches_per_socket < 1 ||

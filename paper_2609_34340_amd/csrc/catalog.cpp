@@ -29,7 +29,7 @@ namespace {
 struct Cand {
   int id, cls, src, dst, copy;
   int64_t bw;
-  uint32_t res;   // bit per directed resource: UP q, DN q, TX q, RX q
+  uint64_t res;   // bit per directed resource: UP q, DN q, TX q, RX q, socket link s -> s2
   bool remote;    // NIC lane to another node
 };
 
@@ -54,13 +54,13 @@ class SlotSearch {
     indeg_.assign(Q, 0);
   }
   std::vector<Found> run() {
-    slot(0, 0u);
+    slot(0, 0);
     return std::move(found_);
   }
 
  private:
   // choose g lanes for slot q, then recurse to slot q+1
-  void slot(int q, uint32_t used) {
+  void slot(int q, uint64_t used) {
     if (q == Q_) {
       for (int x = 0; x < Q_; ++x)
         if (indeg_[x] != g_) return;
@@ -69,7 +69,7 @@ class SlotSearch {
     }
     pick(q, 0, 0, used);
   }
-  void pick(int q, size_t from, int taken, uint32_t used) {
+  void pick(int q, size_t from, int taken, uint64_t used) {
     if (taken == g_) {
       slot(q + 1, used);
       return;
@@ -115,7 +115,7 @@ class SlotSearch {
 // PruneFamilies: drop exact duplicates (same multiset of (pair, footprint,
 // rate)) and families dominated inside their shape.
 std::vector<Found> prune_families(std::vector<Found> fs, const std::vector<Cand>& by_id) {
-  typedef std::tuple<int, int, bool, uint32_t> PairFoot;
+  typedef std::tuple<int, int, bool, uint64_t> PairFoot;
   auto profile = [&](const Found& f) {
     std::map<PairFoot, std::vector<int64_t>> m;
     for (int id : f.ids) {
@@ -171,17 +171,25 @@ std::vector<Cand> instance_table(const vp_topology& t) {
   const int64_t pcie = t.pcie_bytes_per_ns;
   const int64_t nicbw = std::min(t.pcie_bytes_per_ns, t.nic_bytes_per_ns);
   std::vector<Cand> table;
-  auto add = [&](int cls, int s, int d, int cp, int64_t bw, uint32_t res) {
+  const int S = t.sockets_per_node;
+  auto bit = [](int r) { return (uint64_t)1 << r; };
+  auto add = [&](int cls, int s, int d, int cp, int64_t bw, uint64_t res) {
     table.push_back(Cand{(int)table.size(), cls, s, d, cp, bw, res, false});
   };
   for (int q = 0; q < Q; ++q)
-    for (int cp = 0; cp < g; ++cp) add(VP_PATH_PIX, q, q, cp, pcie, 0u);
+    for (int cp = 0; cp < g; ++cp) add(VP_PATH_PIX, q, q, cp, pcie, 0);
   for (int q = 0; q < Q; ++q)
     for (int q2 = 0; q2 < Q; ++q2)
-      if (q != q2 && q / W == q2 / W) add(VP_PATH_PXB, q, q2, 0, pcie, (1u << q) | (1u << (Q + q2)));
+      if (q != q2 && q / W == q2 / W) add(VP_PATH_PXB, q, q2, 0, pcie, bit(q) | bit(Q + q2));
   for (int q = 0; q < Q; ++q)
-    for (int q2 = 0; q2 < Q; ++q2)
-      add(VP_PATH_NIC, q, q2, 0, nicbw, (1u << (2 * Q + q)) | (1u << (3 * Q + q2)));
+    for (int q2 = 0; q2 < Q; ++q2) add(VP_PATH_NIC, q, q2, 0, nicbw, bit(2 * Q + q) | bit(3 * Q + q2));
+  // peer to peer between sockets: both switches' root-complex links and the
+  // directed link between the two sockets, at the PCIe rate
+  if (t.flags & VP_TOPO_SYS_P2P)
+    for (int q = 0; q < Q; ++q)
+      for (int q2 = 0; q2 < Q; ++q2)
+        if (q / W != q2 / W)
+          add(VP_PATH_SYS, q, q2, 0, pcie, bit(q) | bit(Q + q2) | bit(4 * Q + (q / W) * S + q2 / W));
   return table;
 }
 
@@ -302,14 +310,16 @@ vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
 
 // Restricted catalogs for the peer/path ablation (Sec. 6.4): rule 1 keeps the
 // families in which every lane takes its group pair's nearest path (PIX in a
-// switch, PXB between two switches of one socket, the NICs otherwise), i.e.
-// drops every family with a NIC lane between two switches of one socket.
+// switch, PXB between two switches of one socket, SYS between sockets when
+// enabled, the NICs otherwise), i.e. drops every family with a NIC lane
+// between two switches of one node that a PCIe peer-to-peer path also joins.
 // Canonical order is kept, so the result is a catalog of the same topology.
 vp_status restrict_catalog(const vp_catalog& in, int rule, vp_catalog& out) {
   if (rule != 1) return set_error(VP_ERR_INVALID_ARGUMENT, "unknown catalog restriction");
   set_shape(out, in.topo);
   const std::vector<Cand> table = instance_table(in.topo);
   const int Q = out.Q, W = in.topo.switches_per_socket;
+  const bool sys = (in.topo.flags & VP_TOPO_SYS_P2P) != 0;
   std::vector<Found> lists[2];
   for (int f = 0; f < in.F0 + in.F1; ++f) {
     const bool remote = f >= in.F0;
@@ -320,7 +330,7 @@ vp_status restrict_catalog(const vp_catalog& in, int rule, vp_catalog& out) {
     for (int id : in.lfam[f]) {
       const Cand& y = table[id];
       const bool nic = y.cls == VP_PATH_NIC;
-      if (nic && !remote && y.src != y.dst && y.src / W == y.dst / W) keep = false;
+      if (nic && !remote && y.src != y.dst && (sys || y.src / W == y.dst / W)) keep = false;
       ((nic && remote) ? fam.R : fam.L)[y.src * Q + y.dst]++;
       fam.ids.push_back(id);
     }
@@ -386,7 +396,7 @@ vp_status deserialize_catalog(const uint8_t* p, size_t n, vp_catalog& c,
       fam.L.assign(Q * Q, 0);
       fam.R.assign(Q * Q, 0);
       std::vector<int> outd(Q, 0), ind(Q, 0);
-      uint32_t used = 0;
+      uint64_t used = 0;
       bool ok = true;
       int nic = 0;
       for (int64_t x = 0; x < QG; ++x) {
@@ -464,9 +474,12 @@ void build_device_image(vp_catalog& c) {
   L.off_rset = off; off += L.nS * kMaxRTerms;
   L.off_psid = off; off += c.J1;
   L.total = off;
+  // every path but NIC runs at the PCIe rate; the planner relies on it (one
+  // largest-lane maximum for the PCIe-rate classes, one for NIC)
   L.bw_cls[VP_PATH_PIX] = c.topo.pcie_bytes_per_ns;
   L.bw_cls[VP_PATH_PXB] = c.topo.pcie_bytes_per_ns;
   L.bw_cls[VP_PATH_NIC] = std::min(c.topo.pcie_bytes_per_ns, c.topo.nic_bytes_per_ns);
+  L.bw_cls[VP_PATH_SYS] = c.topo.pcie_bytes_per_ns;
   L.bw_max = std::max(L.bw_cls[0], L.bw_cls[2]);
 
   std::vector<int32_t>& im = c.image;

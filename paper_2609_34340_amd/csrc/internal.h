@@ -44,7 +44,7 @@ struct DevCatalogLayout {
   int32_t off_rset;      // nS * kMaxRTerms slot-pair indices q*Q+q2 of each set (-1 past its end)
   int32_t off_psid;      // J1: set of each NIC-carrying pattern
   int32_t total;         // int32 elements
-  int64_t bw_cls[3];     // rate of PIX, PXB, NIC paths
+  int64_t bw_cls[4];     // rate of PIX, PXB, NIC, SYS paths
   int64_t bw_max;
 };
 

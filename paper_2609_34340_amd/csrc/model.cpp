@@ -4,10 +4,11 @@
 // Stage s = 1 .. N-1 pairs rank i with rank (i + s) mod N and moves the whole
 // D_i,(i+s) at once; a stage whose lanes carry nothing is skipped.  A lane's
 // path is its pair's nearest one (PIX in a switch, PXB between two switches
-// of a socket, the NICs otherwise) or, with dynamic paths, whichever of the
-// pair's paths makes the stage finish first.  Unlike a catalog channel, a
-// rotation stage may put several lanes on one directed resource (a switch's
-// uplink or downlink, a NIC's transmit or receive side): those lanes share
+// of a socket, SYS between sockets when enabled, the NICs otherwise) or, with
+// dynamic paths, whichever of the pair's paths makes the stage finish first.
+// Unlike a catalog channel, a rotation stage may put several lanes on one
+// directed resource (a switch's uplink or downlink, a socket link, a NIC's
+// transmit or receive side): those lanes share
 // it equally, so a lane runs at min(path rate, capacity / lanes) over its
 // resources.  A stage takes lambda plus its slowest lane's bytes / rate.
 // Everything is exact: times are kept over the common denominator of the
@@ -40,13 +41,15 @@ int64_t gcd64(int64_t a, int64_t b) {
 vp_status rotation_time(const vp_catalog& c, const int64_t* D, int rule, int64_t lambda, int64_t* num,
                         int64_t* den) {
   const int N = c.N, g = c.g, Q = c.Q, G = c.G;
-  const int W = c.topo.switches_per_socket;
+  const int W = c.topo.switches_per_socket, S = c.topo.sockets_per_node;
+  const bool sys = (c.topo.flags & VP_TOPO_SYS_P2P) != 0;
   const int64_t pcie = c.topo.pcie_bytes_per_ns, nic = c.topo.nic_bytes_per_ns;
   const int64_t nic_path = std::min(pcie, nic);
   const int64_t l = pcie / gcd64(pcie, nic) * nic;   // common denominator of every rate below
   __int128 total = 0;
   std::vector<Lane> lanes;
-  std::vector<int> up(G), dn(G), tx(G), rx(G);
+  std::vector<int> up(G), dn(G), tx(G), rx(G), xs(c.nn * S * S);
+  auto xlink = [&](int a, int d) { return ((a / Q) * S + (a % Q) / W) * S + (d % Q) / W; };
   for (int s = 1; s < N; ++s) {
     lanes.clear();
     for (int i = 0; i < N; ++i) {
@@ -54,11 +57,12 @@ vp_status rotation_time(const vp_catalog& c, const int64_t* D, int rule, int64_t
       const int64_t x = D[(size_t)i * N + j];
       if (x == 0) continue;
       Lane ln{x, i / g, j / g, {VP_PATH_PIX, VP_PATH_PIX}, 1};
-      const bool same_socket = ln.a / Q == ln.d / Q && (ln.a % Q) / W == (ln.d % Q) / W;
+      const bool same_node = ln.a / Q == ln.d / Q;
+      const bool same_socket = same_node && (ln.a % Q) / W == (ln.d % Q) / W;
       if (ln.a == ln.d) {
         ln.opt[0] = VP_PATH_PIX;
-      } else if (same_socket) {
-        ln.opt[0] = VP_PATH_PXB;            // nearest
+      } else if (same_socket || (same_node && sys)) {
+        ln.opt[0] = same_socket ? VP_PATH_PXB : VP_PATH_SYS;   // nearest
         ln.opt[1] = VP_PATH_NIC;
         ln.nopt = rule == 1 ? 1 : 2;
       } else {
@@ -81,8 +85,10 @@ vp_status rotation_time(const vp_catalog& c, const int64_t* D, int rule, int64_t
       std::fill(dn.begin(), dn.end(), 0);
       std::fill(tx.begin(), tx.end(), 0);
       std::fill(rx.begin(), rx.end(), 0);
+      std::fill(xs.begin(), xs.end(), 0);
       for (size_t t = 0; t < lanes.size(); ++t) {
-        if (pick[t] == VP_PATH_PXB) { up[lanes[t].a]++; dn[lanes[t].d]++; }
+        if (pick[t] == VP_PATH_PXB || pick[t] == VP_PATH_SYS) { up[lanes[t].a]++; dn[lanes[t].d]++; }
+        if (pick[t] == VP_PATH_SYS) xs[xlink(lanes[t].a, lanes[t].d)]++;
         if (pick[t] == VP_PATH_NIC) { tx[lanes[t].a]++; rx[lanes[t].d]++; }
       }
       // slowest lane: bytes * (l / rate), the rate being the path's or a share
@@ -94,6 +100,9 @@ vp_status rotation_time(const vp_catalog& c, const int64_t* D, int rule, int64_t
           per = l / pcie;
         } else if (pick[t] == VP_PATH_PXB) {
           per = std::max<__int128>(l / pcie, (__int128)std::max(up[ln.a], dn[ln.d]) * (l / pcie));
+        } else if (pick[t] == VP_PATH_SYS) {
+          const int sh = std::max(std::max(up[ln.a], dn[ln.d]), xs[xlink(ln.a, ln.d)]);
+          per = std::max<__int128>(l / pcie, (__int128)sh * (l / pcie));
         } else {
           per = std::max<__int128>(l / nic_path, (__int128)std::max(tx[ln.a], rx[ln.d]) * (l / nic));
         }

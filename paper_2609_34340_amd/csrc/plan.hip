@@ -40,14 +40,17 @@ constexpr uint32_t kRawSaturated = 0xFFFFFFFEu;     // residual too large for 32
 
 struct PairRes {
   int64_t F;
-  int64_t xmax[3];
+  // largest lane volume on a PCIe-rate path (PIX, PXB, SYS) and on a NIC
+  // path: Eq. (10) needs only the largest volume / rate, and the classes of
+  // one rate share a maximum
+  int64_t xmax[2];
 };
 
 struct Shared {
   uint64_t key;
   int64_t total_rem, Lmax, tau, total_units;
-  int64_t cap[3];
-  int32_t capu[3];
+  int64_t cap[4];
+  int32_t capu[4];
   // best candidate so far in this iteration
   int64_t best_S, best_xm, best_bm;
   int32_t best_valid, best_f, best_k, best_c, best_s, best_chunk;
@@ -72,8 +75,9 @@ struct PlanArgs {
   int32_t* recv_src;                // optional [k_max][N]: the rank whose lane lands at each rank
   int32_t* status;
   // LDS layout (byte offsets)
-  int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo, o_finl;
-  int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bx, o_brw, o_top;
+  int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo;
+  int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_iid, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bid, o_bx, o_brw,
+      o_top;
   int32_t o_rset, o_psid, o_rbest, o_pbase, o_lastj, o_lastv, o_rp, o_sacc;
 };
 
@@ -151,8 +155,8 @@ struct Perms<4> {
   }
 };
 
-// Local family descriptor word: cls | src_slot<<2 | dst_slot<<5 | out_pos<<8 |
-// rank_same<<10 | n_other<<12 | local_id<<15.  rank_same is the instance's rank
+// Local family descriptor (16 bits): cls | src_slot<<2 | dst_slot<<5 |
+// out_pos<<8 | rank_same<<10 | n_other<<12.  rank_same is the instance's rank
 // among the in-instances of its destination slot of the same kind (same-node
 // or cross-node lane), n_other the number of the other kind: cross-node
 // in-instances precede same-node ones exactly when their source node is the
@@ -163,7 +167,6 @@ __device__ inline int d_ds(uint32_t w) { return (w >> 5) & 7; }
 __device__ inline int d_opos(uint32_t w) { return (w >> 8) & 3; }
 __device__ inline int d_rsame(uint32_t w) { return (w >> 10) & 3; }
 __device__ inline int d_nother(uint32_t w) { return (w >> 12) & 7; }
-__device__ inline int d_id(uint32_t w) { return (int)(w >> 15); }
 
 // Per-family working set of the current chunk.
 struct FamCtx {
@@ -430,7 +433,7 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
 
   // binding score F (Eq. (8)) and the largest lane volume per path class, in units
   int64_t F = 0;
-  int32_t x0 = 0, x1 = 0, x2 = 0;
+  int32_t xp = 0, xn = 0;
   int jf[MG][g], cf[MG][g];
   int32_t rf[MG][g][g];
 #pragma unroll
@@ -452,21 +455,17 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
       for (int jj = 1; jj < g; ++jj) x = jf[r][m] == jj ? rf[r][m][jj] : x;
       x = x > 0 ? x : 0;   // a self pair serves nothing
       F += x;
-      const int c = cf[r][m];
-      if (c == 0) x0 = x > x0 ? x : x0;
-      else if (c == 1) x1 = x > x1 ? x : x1;
-      else x2 = x > x2 ? x : x2;
+      if (cf[r][m] == VP_PATH_NIC) xn = x > xn ? x : xn;
+      else xp = x > xp ? x : xp;
     }
   }
   F = wave_sum(F);
-  x0 = wave_max32(x0);
-  x1 = wave_max32(x1);
-  x2 = wave_max32(x2);
+  xp = wave_max32(xp);
+  xn = wave_max32(xn);
   if (lane == 0) {
     out->F = F;
-    out->xmax[0] = x0;
-    out->xmax[1] = x1;
-    out->xmax[2] = x2;
+    out->xmax[0] = xp;
+    out->xmax[1] = xn;
   }
 }
 
@@ -499,19 +498,20 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   uint16_t* terms = (uint16_t*)(smem + P.o_terms);
   uint16_t* nterms = (uint16_t*)(smem + P.o_nterms);  // low byte: diagonal terms, high byte: shift terms
   int32_t* pfb = (int32_t*)(smem + P.o_pfb);           // [NP][2] local family range
-  uint32_t* finfo = (uint32_t*)(smem + P.o_finfo);
-  uint8_t* finl = smem + P.o_finl;
+  uint16_t* finfo = (uint16_t*)(smem + P.o_finfo);
   PairRes* pr = (PairRes*)(smem + P.o_pair);
   uint16_t* outT = (uint16_t*)(smem + P.o_outT);
   uint16_t* inT = (uint16_t*)(smem + P.o_inT);
   int8_t* ipos = (int8_t*)(smem + P.o_ipos);
   uint8_t* ocls = smem + P.o_ocls;
+  uint8_t* iid = smem + P.o_iid;     // [FC][N] node-local instance id of every instance of the chunk
   int32_t* hp = (int32_t*)(smem + P.o_hp);
   uint32_t* raw = (uint32_t*)(smem + P.o_raw);       // residual of every credit entry (saturating)
   uint8_t* sl = smem + P.o_sl;
   uint8_t* dl = smem + P.o_dl;
   uint8_t* bsl = smem + P.o_bsl;
   uint8_t* bdl = smem + P.o_bdl;
+  uint8_t* bid = smem + P.o_bid;
   uint32_t* bx = (uint32_t*)(smem + P.o_bx);
   uint32_t* brw = (uint32_t*)(smem + P.o_brw);
   uint64_t* topkey = (uint64_t*)(smem + P.o_top);    // [FC] best credit triple of each family in the chunk
@@ -556,7 +556,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     // descriptor word and in-list entry of local family x / QG, index x % QG
     const int lf = x / QG, idx = x - lf * QG;
     const int info = cat[L.off_fam_info + x];
-    const int cls = info & 15, ss = (info >> 4) & 15, ds = (info >> 8) & 15, id = info >> 12;
+    const int cls = info & 15, ss = (info >> 4) & 15, ds = (info >> 8) & 15;
     int opos = 0;
     for (int m = 0; m < g; ++m)
       if (cat[L.off_fam_out + lf * QG + ss * g + m] == idx) opos = m;
@@ -568,9 +568,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       if (r2 != remote) ++nother;
       else if (idx2 < idx) ++rsame;
     }
-    finfo[x] = (uint32_t)(cls | (ss << 2) | (ds << 5) | (opos << 8) | (rsame << 10) | (nother << 12) |
-                          (id << 15));
-    finl[x] = (uint8_t)cat[L.off_fam_in + x];
+    finfo[x] = (uint16_t)(cls | (ss << 2) | (ds << 5) | (opos << 8) | (rsame << 10) | (nother << 12));
   }
   for (int x = tid; x < kS * (Q * Q + 1); x += kPlanThreads) agg[x] = 0;
   for (int x = tid; x < L.nS * kMaxRTerms; x += kPlanThreads) {
@@ -637,7 +635,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     int64_t tau = (sh->Lmax + den - 1) / den;
     if (tau < 1) tau = 1;
     sh->tau = tau;
-    for (int c = 0; c < 3; ++c) {
+    for (int c = 0; c < 4; ++c) {
       int64_t cap = tau * L.bw_cls[c] / P.unit * P.unit;
       if (cap < P.unit) cap = P.unit;
       sh->cap[c] = cap;
@@ -787,6 +785,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           outT[base + a * g + op] = (uint16_t)t;
           inT[base + d * g + mi] = (uint16_t)t;
           ocls[base + a * g + op] = (uint8_t)cl;
+          // the instance id is only written out with the winner; its global
+          // load overlaps the residual loads below
+          iid[base + t] = (uint8_t)(cat[L.off_fam_info + lf * QG + idx] >> 12);
           ipos[base + a * g + op] = (int8_t)(d == a ? mi : -1);
           const int64_t cap = sh->cap[cl];
           int32_t* h = hp + (base + t) * g2;
@@ -879,11 +880,13 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
             if (pr[cc * NS + s].F > pr[cc * NS + s0].F) s0 = s;
           const PairRes& r = pr[cc * NS + s0];
           int64_t xm2 = 0, bm2 = 1;
-          for (int cl = 0; cl < 3; ++cl)
-            if (r.xmax[cl] * bm2 > xm2 * L.bw_cls[cl]) {
+          for (int cl = 0; cl < 2; ++cl) {
+            const int64_t b = L.bw_cls[cl ? VP_PATH_NIC : VP_PATH_PIX];
+            if (r.xmax[cl] * bm2 > xm2 * b) {
               xm2 = r.xmax[cl];
-              bm2 = L.bw_cls[cl];
+              bm2 = b;
             }
+          }
           // Eq. (10) in bytes: served volume and slowest lane
           const int64_t Sb = r.F * P.unit;
           xm2 *= P.unit;
@@ -936,6 +939,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           const uint8_t s_ = sl[(size_t)pi * N + t], d_ = dl[(size_t)pi * N + t];
           bsl[t] = s_;
           bdl[t] = d_;
+          bid[t] = iid[(size_t)sh->best_c * N + t];
           const int32_t hx = H[t * g2 + s_ * g + d_];
           bx[t] = (uint32_t)(hx > 0 ? hx : 0);
           brw[t] = RW[t * g2 + s_ * g + d_];
@@ -967,7 +971,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         const uint32_t rv = live ? RW[t * g2 + s_ * g + d_] : brw[t];
         const size_t o = (size_t)K * N + i;
         P.dst[o] = j;
-        P.inst[o] = d_id(w);
+        P.inst[o] = live ? iid[(size_t)sh->best_c * N + t] : bid[t];
         P.bytes[o] = x;
         if (P.recv_src) P.recv_src[(size_t)K * N + j] = i;   // pi_k is a permutation
         if (P.send_off) {
@@ -1049,7 +1053,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   if (L.J0 > 4095 || L.J1 > 4095 || L.nn > 255) return set_error(VP_ERR_UNSUPPORTED, "catalog too large");
   if (QG > kMaxQG || L.Q > 8 || g > 4) return set_error(VP_ERR_UNSUPPORTED, "too many lanes per node");
   if (N > 65535 || L.G > 64 * 8) return set_error(VP_ERR_UNSUPPORTED, "too many ranks for the planner");
-  if (L.n_inst >= (1 << 17)) return set_error(VP_ERR_UNSUPPORTED, "too many node-local instances");
+  if (L.n_inst > 256) return set_error(VP_ERR_UNSUPPORTED, "too many node-local instances");
   int hmax = 1, mlt = 0, mrt = 0;
   for (int p = 0; p < NP; ++p) {
     hmax = std::max(hmax, c.pat_fe[p] - c.pat_fb[p]);
@@ -1123,10 +1127,10 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_terms, ((size_t)NP * L.TS + 4) * 2);
   take(&P.o_nterms, (size_t)NP * 2);
   take(&P.o_pfb, (size_t)NP * 8);
-  take(&P.o_finfo, (size_t)FL * QG * 4);
-  take(&P.o_finl, (size_t)FL * QG);
+  take(&P.o_finfo, (size_t)FL * QG * 2);
   take(&P.o_bsl, (size_t)N);
   take(&P.o_bdl, (size_t)N);
+  take(&P.o_bid, (size_t)N);
   take(&P.o_bx, (size_t)N * 4);
   take(&P.o_brw, (size_t)N * 4);
   take(&P.o_rset, (size_t)L.nS * kMaxRTerms * 2);
@@ -1138,7 +1142,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_sacc, (size_t)N * 8);
   const size_t fixed = o;
   const size_t per_fam = align_up((size_t)NS * sizeof(PairRes), 16) + 2 * align_up((size_t)N * 2, 16) +
-                         2 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16) + 16 +
+                         3 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16) + 16 +
                          align_up((size_t)NS * L.G * 2, 16);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return set_error(VP_ERR_HIP, "hipGetDevice failed");
@@ -1155,6 +1159,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_inT, (size_t)FC * N * 2);
   take(&P.o_ipos, (size_t)FC * N);
   take(&P.o_ocls, (size_t)FC * N);
+  take(&P.o_iid, (size_t)FC * N);
   take(&P.o_hp, std::max((size_t)FC * N * g2 * 4, (size_t)N * 8));   // also the prologue's column sums
   take(&P.o_raw, (size_t)FC * N * g2 * 4);
   take(&P.o_sl, (size_t)FC * NS * N);

@@ -63,7 +63,53 @@ def check(vp, case, nearest, matrix):
 @pytest.mark.parametrize("name", extra_cases.NAMES)
 def test_extra_plan_parity(vp, name, nearest):
     case = vpgen.extra(name)
-    mats = range(extra_cases.ZIPF_MATRICES) if name == "zipf-pairs-16-s0.6" else [0]
+    mats = range(extra_cases.ZIPF_MATRICES) if name.startswith("zipf-pairs-16-s0.6") else [0]
     for m in mats:
         log("extra plan parity %s nearest=%s matrix %d" % (name, nearest, m))
         check(vp, case, nearest, m)
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3])
+def test_sys_topology_plan_parity(vp, cid):
+    """MoE demand on nodes with cross-socket peer to peer (SYS paths)."""
+    import dataclasses
+    w = vpgen.config(cid)
+    topo = dataclasses.replace(w.topo, flags=vp.TOPO_SYS_P2P)
+    log("SYS topology plan parity C%d" % cid)
+    R = vpgen.routing_all(w, 0, 2048)
+    D = np.stack([oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes)["row"] for i in range(w.n_ranks)])
+    gc, oc = catalogs(vp, topo, False)
+    p = vp.plan_params(gc.N, w.row_bytes)
+    st = vp.new_status()
+    s = vp.plan(gc, torch.from_numpy(D).cuda(), p, status=st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    g = vp.schedule_to_host(s)
+    o = oc.plan(D, w.row_bytes)
+    assert g["K"] == o["K"] and g["tau"] == o["tau"]
+    for key in ("family", "dst", "inst", "bytes"):
+        assert np.array_equal(g[key], o[key]), key
+    # some lane takes a SYS path
+    assert (gc.instances()["cls"][g["inst"]] == vp.PATH_SYS).any()
+
+
+def test_sys_topology_256_ranks_plans_validly(vp):
+    """256 ranks with SYS paths (60,104 families): the GPU plan is a valid
+    decomposition (every activation feasible, sums to D, progressing)."""
+    import dataclasses
+    from oracle.checks import TopoModel, schedule_valid
+    w = vpgen.config(5)
+    topo = dataclasses.replace(w.topo, flags=vp.TOPO_SYS_P2P)
+    log("SYS topology 256 ranks")
+    R = vpgen.routing_all(w, 0)
+    D = np.stack([oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes)["row"] for i in range(w.n_ranks)])
+    gc = vp.Catalog(topo)
+    gc.upload()
+    p = vp.plan_params(gc.N, w.row_bytes)
+    st = vp.new_status()
+    s = vp.plan(gc, torch.from_numpy(D).cuda(), p, status=st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    g = vp.schedule_to_host(s)
+    schedule_valid(TopoModel(topo), D, g, gc.instances()["cls"])
+    assert (g["bytes"].sum(axis=1) > 0).all()

@@ -215,3 +215,44 @@ def test_rotation_time_limits(vp):
     cat.rotation_time(D, vp.ROTATION_NEAREST_PATH)
     with pytest.raises(vp.VPError):
         cat.rotation_time(-D, vp.ROTATION_NEAREST_PATH)
+
+
+SYS_TOPOS = [vpgen.Topology(1, 2, 1, 2, flags=1), vpgen.Topology(1, flags=1), vpgen.Topology(2, flags=1),
+             vpgen.Topology(32, flags=1), vpgen.Topology(2, 4, 1, 2, flags=1), vpgen.Topology(3, 2, 2, 3, flags=1)]
+
+
+@pytest.mark.parametrize("nearest", [False, True])
+@pytest.mark.parametrize("topo", SYS_TOPOS)
+def test_sys_catalog_equals_oracle(vp, topo, nearest):
+    ours = vp.Catalog(topo)
+    if nearest:
+        ours = ours.restrict(vp.RESTRICT_NEAREST_PATH)
+    ref = oracle.Catalog(topo, nearest=nearest)
+    a, b = ours.instances(), ref.table()
+    for key in ("cls", "src", "dst", "copy", "bw"):
+        assert np.array_equal(a[key], b[key]), key
+    sa, sb = ours.shapes(), ref.shapes()
+    for key in ("k", "fam_begin", "fam_end", "L", "R"):
+        assert np.array_equal(sa[key], sb[key]), key
+    fa, fb = ours.families(), ref.families()
+    for key in ("shape", "k", "ids"):
+        assert np.array_equal(fa[key], fb[key]), key
+    assert vp.Catalog.load(ours.save()).n_families == ours.n_families
+
+
+def test_sys_flag_limits(vp):
+    with pytest.raises(vp.VPError):
+        vp.Catalog(vpgen.Topology(1, 8, 1, 2, flags=1))   # more than 4 sockets
+    with pytest.raises(vp.VPError):
+        vp.Catalog(vpgen.Topology(1, flags=2))            # unknown flag
+
+
+@pytest.mark.parametrize("topo", [vpgen.Topology(1, 2, 1, 2, flags=1), vpgen.Topology(2, flags=1)])
+def test_sys_rotation_time_equals_oracle(vp, topo):
+    rng = np.random.default_rng(5)
+    N = topo.n_ranks
+    D = rng.integers(0, 64, (N, N)).astype(np.int64) * 4096
+    np.fill_diagonal(D, 0)
+    cat = vp.Catalog(topo)
+    for rule, near in [(vp.ROTATION_NEAREST_PATH, True), (vp.ROTATION_DYNAMIC_PATH, False)]:
+        assert cat.rotation_time(D, rule) == oracle.rotation_time(topo, D, near)

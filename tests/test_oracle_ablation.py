@@ -67,3 +67,21 @@ def test_dynamic_paths_never_slower(cid):
     R = vpgen.routing_all(w, 0, 256)
     D = np.stack([oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes)["row"] for i in range(w.n_ranks)])
     assert T(w.topo, D, False) <= T(w.topo, D, True)
+
+
+def test_sys_rotation_by_hand():
+    """Two sockets, one switch of two GPUs each, c bytes per pair.  Shift 2
+    sends both GPUs of a switch to the other socket: on nearest (SYS) paths
+    the two lanes share the uplink, the socket link and the downlink (16 each:
+    c/16); with a path choice one lane takes the NICs (25): c/25.  Shifts 1
+    and 3 have one cross lane each way: c/32."""
+    topo = vpgen.Topology(1, 2, 1, 2, flags=oracle.TOPO_SYS_P2P)
+    c = 5 << 20
+    D = np.full((4, 4), c, np.int64)
+    np.fill_diagonal(D, 0)
+    assert T(topo, D, True) == 3 * LAM + Fraction(c, 32) * 2 + Fraction(c, 16)
+    assert T(topo, D, False) == 3 * LAM + Fraction(c, 32) * 2 + Fraction(c, 25)
+    # without peer to peer every cross lane is a NIC lane: shift 2 shares
+    # the NIC (12.5 each), shifts 1 and 3 have one NIC lane each way (25)
+    topo0 = vpgen.Topology(1, 2, 1, 2)
+    assert T(topo0, D, False) == 3 * LAM + Fraction(c, 25) * 2 + Fraction(2 * c, 25)

@@ -290,3 +290,50 @@ def test_nearest_path_catalog_is_the_filtered_catalog(cid):
         if ok:
             keep.append(fam_key(fam))
     assert [fam_key(near.cluster_family(f)) for f in range(near.n_families)] == keep
+
+
+# ------------------------------------------ cross-socket peer to peer (SYS)
+
+def two_socket_node(sys_p2p):
+    return vpgen.Topology(1, sockets_per_node=2, switches_per_socket=1, gpus_per_switch=2,
+                          flags=oracle.TOPO_SYS_P2P if sys_p2p else 0)
+
+
+def test_sys_hand_counts():
+    """Two sockets of one switch with two GPUs each.  Without peer to peer
+    the only cross path is the NIC, usable once each way: all-PIX, and one
+    PIX plus one NIC lane per switch (2 families, 2 shapes).  With SYS the
+    pair has two disjoint paths ({UP, X, DN} and {TX, RX}), as PXB and NIC
+    inside one socket: 6 families in 3 shapes, 2 of them on nearest paths."""
+    assert (oracle.Catalog(two_socket_node(False)).n_shapes, oracle.Catalog(two_socket_node(False)).n_families) == (2, 2)
+    c = oracle.Catalog(two_socket_node(True))
+    assert (c.n_shapes, c.n_families) == (3, 6)
+    assert oracle.Catalog(two_socket_node(True), nearest=True).n_families == 2
+
+
+@pytest.mark.parametrize("nearest", [False, True])
+@pytest.mark.parametrize("topo", [two_socket_node(True), vpgen.Topology(1, flags=1)])
+def test_brute_force_sys_equals_catalog(topo, nearest):
+    """Rank-level brute force with SYS paths (every derangement, every path
+    vector, Eq. (1) with the socket links) equals the catalog's
+    instantiations, with and without the nearest-path restriction."""
+    tm = TopoModel(topo)
+    cat = oracle.Catalog(topo, nearest=nearest)
+    inst = set()
+    for f in cluster_families(cat):
+        got = instantiate(tm, f)
+        assert got and not (got & inst)
+        inst |= got
+    assert inst == brute_force_channels(tm, nearest=nearest)
+
+
+def test_sys_circulant_subset_of_full_catalog():
+    topo = vpgen.Topology(2, sockets_per_node=2, switches_per_socket=1, gpus_per_switch=2, flags=1)
+    full = oracle.Catalog(topo, full=True)
+    circ = oracle.Catalog(topo)
+    assert {fam_key(f) for f in cluster_families(circ)} <= {fam_key(f) for f in cluster_families(full)}
+    tm = TopoModel(topo)
+    inst = set()
+    for f in cluster_families(full):
+        inst |= instantiate(tm, f)
+    assert inst == brute_force_channels(tm)

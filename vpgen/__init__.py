@@ -45,6 +45,7 @@ class Topology:
     nics_per_switch: int = 1
     pcie_bytes_per_ns: int = 32
     nic_bytes_per_ns: int = 25
+    flags: int = 0           # bit 0: peer-to-peer between sockets of a node (SYS paths)
 
     @property
     def n_ranks(self) -> int:
@@ -54,7 +55,7 @@ class Topology:
     def as_tuple(self):
         return (self.n_nodes, self.sockets_per_node, self.switches_per_socket,
                 self.gpus_per_switch, self.nics_per_switch,
-                self.pcie_bytes_per_ns, self.nic_bytes_per_ns)
+                self.pcie_bytes_per_ns, self.nic_bytes_per_ns, self.flags)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -250,6 +251,12 @@ EXTRA = {
                                      zipf_s=0.6),
     "zipf-pairs-16-s0.8": DemandCase("zipf-pairs-16-s0.8", Topology(2), 4096, "zipf_pairs", per_rank=1 << 30,
                                      zipf_s=0.8),
+    # the same skew and layout on nodes whose sockets reach each other peer to
+    # peer (SYS paths), where a path choice exists for every intra-node pair
+    "zipf-pairs-16-s0.6-sys": DemandCase("zipf-pairs-16-s0.6-sys", Topology(2, flags=1), 4096, "zipf_pairs",
+                                         per_rank=1 << 30, zipf_s=0.6),
+    "wan21-H8C1-sys": DemandCase("wan21-H8C1-sys", Topology(1, flags=1), 256, "ulysses_hc", seq=75600, heads=40,
+                                 head_dim=128, H=8, C=1),
     "wan21-H8C1": DemandCase("wan21-H8C1", Topology(1), 256, "ulysses_hc", seq=75600, heads=40, head_dim=128,
                              H=8, C=1),
     "wan21-H4C2": DemandCase("wan21-H4C2", Topology(1), 256, "ulysses_hc", seq=75600, heads=40, head_dim=128,
