@@ -13,7 +13,9 @@ experts holding half of the per-draw mass, hot set redrawn per matrix):
 
 all enqueued on one stream with no host synchronisation, inputs resident in
 HBM.  Steps cycle over `--matrices` distinct demand matrices and two send
-buffers.  Unless --no-sweep, the other four workloads (N = 8, 16, 64 and the
+buffers.  Unless --no-batch, vp_plan_batch then plans D with D^T, and 16 to
+256 matrices, in one launch each ("plan_batch": launch time and us per
+matrix; the headline plan time stays the one-matrix latency).  Unless --no-sweep, the other four workloads (N = 8, 16, 64 and the
 16-rank Ulysses case) follow with six timed steps each, under "per_config";
 unless --no-extra, the planner then runs on the uniform, skew and head/context
 demands with the full and the nearest-path catalog (the peer/path ablation),
@@ -181,6 +183,47 @@ def measure(w, steps, warmup, M, dev):
     return r
 
 
+def batch_section(w, routing_list, dev, sizes=(2, 16, 64, 256)):
+    """vp_plan_batch: B matrices planned side by side (one workgroup each).
+    B = 2 is a layer's dispatch matrix D and its combine matrix D^T; larger
+    batches cycle over the workload's distinct matrices.  Reports the launch
+    time and microseconds per matrix (HIP events, mean of 3 launches after
+    one warm launch)."""
+    import torch
+    import paper_2609_34340_amd as vp
+    cat = vp.Catalog(w.topo)
+    cat.upload()
+    p = vp.plan_params(w.n_ranks, w.row_bytes)
+    mats = []
+    for R in routing_list:
+        d = vp.demand(torch.from_numpy(R).to(dev), w.n_ranks, w.experts, w.row_bytes, sort_row=-1)
+        mats.append(d["demand"])
+    out = {"distinct_matrices": len(mats)}
+    for B in sizes:
+        if B == 2:
+            D = torch.stack([mats[0], mats[0].t().contiguous()])
+        else:
+            D = torch.stack([mats[b % len(mats)] for b in range(B)])
+        sched = vp.alloc_schedule_batch(B, w.n_ranks, p.k_max, dev)
+        st = torch.zeros(B, dtype=torch.int32, device=dev)
+        ws = torch.empty(vp.plan_batch_workspace_bytes(cat, p, B), dtype=torch.uint8, device=dev)
+        vp.plan_batch(cat, D, p, status=st, out=sched, ws=ws)
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(3):
+            vp.plan_batch(cat, D, p, status=st, out=sched, ws=ws)
+        b_.record()
+        torch.cuda.synchronize()
+        if (st != 0).any():
+            raise SystemExit("device error in the batched plan: %s" % st.cpu().numpy())
+        ms = a.elapsed_time(b_) / 3
+        key = "dispatch_and_combine" if B == 2 else "B%d" % B
+        out[key] = {"batch": B, "launch_ms": round(ms, 3), "us_per_matrix": round(ms * 1e3 / B, 1)}
+        del D, sched, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def extra_demand(vp, case, matrix, dev):
     """int64 [N, N] demand of an extra case on the GPU: given matrices are
     uploaded; a head/context layout runs vp_demand_heads per all-to-all group
@@ -293,6 +336,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the short runs of the other configurations (plan time at every N)")
+    ap.add_argument("--no-batch", action="store_true", help="skip the batched-planner timings")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the planner on the extra demands and the nearest-path ablation")
     ap.add_argument("--calibrate-copy", type=int, default=0,
@@ -367,6 +411,9 @@ def main():
                      "algorithmic_bytes_per_launch": int(r["gather_bytes"].mean()),
                      "avg_launch_us": round(float(r["gather_ms"].mean() * 1e3), 2)},
     }
+    if w.mode == "moe" and not args.no_batch:
+        print("[bench] batched planning", file=sys.stderr, flush=True)
+        out["plan_batch"] = batch_section(w, r["routing_np"], dev)
     if not args.no_sweep:
         # the other configurations, briefly: the planner at every N and each pack
         per = {}

@@ -274,6 +274,22 @@ vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_pa
                   int64_t* send_off, int64_t* stream_off, int32_t* recv_src, int64_t* tau,
                   int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
 
+/* Several independent matrices planned side by side, one workgroup (one
+ * compute unit) each, with the decisions vp_plan takes for each of them (the
+ * planner is latency-bound on one CU; a batch puts the others to work, e.g.
+ * a layer's dispatch matrix D and its combine matrix D^T, or a stream of
+ * matrices planned ahead).  Every buffer of vp_plan holds `batch` of its
+ * kind back to back: demand [batch, N, N]; K, tau and dev_status [batch];
+ * family [batch, k_max]; dst, inst, bytes and the optional send_off,
+ * stream_off, recv_src [batch, k_max, N].  Matrix b's device errors land in
+ * dev_status[b].  Workspace: vp_plan_batch_workspace bytes (batch * N * N *
+ * 8).  1 <= batch <= 65535. */
+size_t vp_plan_batch_workspace(const vp_catalog* cat, const vp_plan_params* p, int32_t batch);
+vp_status vp_plan_batch(const vp_catalog* cat, int32_t batch, const int64_t* demand, const vp_plan_params* p,
+                        int32_t* K, int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes,
+                        int64_t* send_off, int64_t* stream_off, int32_t* recv_src, int64_t* tau,
+                        int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------- pack */
 
 /* Workspace bytes for vp_pack_rows (k = the routing's top-k, T tokens) or

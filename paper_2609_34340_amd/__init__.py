@@ -82,6 +82,10 @@ def lib():
     L.vp_plan_workspace.argtypes = [vp, C.POINTER(PlanParams)]
     L.vp_plan_workspace.restype = sz
     L.vp_plan.argtypes = [vp, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.vp_plan_batch_workspace.argtypes = [vp, C.POINTER(PlanParams), i32]
+    L.vp_plan_batch_workspace.restype = sz
+    L.vp_plan_batch.argtypes = [vp, i32, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                vp]
     L.vp_pack_workspace.argtypes = [i32, i64, i64, i64, i32]
     L.vp_pack_workspace.restype = sz
     L.vp_pack_rows.argtypes = [vp, i64, i32, i64, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, i64, vp, vp,
@@ -378,6 +382,52 @@ def plan(cat: Catalog, D: torch.Tensor, p: PlanParams, status: Optional[torch.Te
                          _ptr(out.get("stream_off")), _ptr(out.get("recv_src")), _ptr(out["tau"]), _ptr(status),
                          _ptr(ws), ws.numel(),
                          _stream(stream)), "vp_plan")
+    out["status"] = status
+    return out
+
+
+def plan_batch_workspace_bytes(cat: Catalog, p: PlanParams, B: int) -> int:
+    return int(lib().vp_plan_batch_workspace(cat.handle, C.byref(p), B))
+
+
+def alloc_schedule_batch(B: int, N: int, k_max: int, device="cuda", layout: bool = False) -> dict:
+    """Schedule buffers of B matrices (leading dimension B)."""
+    s = dict(K=torch.zeros(B, dtype=torch.int32, device=device),
+             family=torch.empty((B, k_max), dtype=torch.int32, device=device),
+             dst=torch.empty((B, k_max, N), dtype=torch.int32, device=device),
+             inst=torch.empty((B, k_max, N), dtype=torch.int32, device=device),
+             bytes=torch.empty((B, k_max, N), dtype=torch.int64, device=device),
+             tau=torch.zeros(B, dtype=torch.int64, device=device))
+    if layout:
+        for key, dt in (("send_off", torch.int64), ("stream_off", torch.int64), ("recv_src", torch.int32)):
+            s[key] = torch.empty((B, k_max, N), dtype=dt, device=device)
+    return s
+
+
+def plan_batch(cat: Catalog, D: torch.Tensor, p: PlanParams, status: Optional[torch.Tensor] = None,
+               out: Optional[dict] = None, ws: Optional[torch.Tensor] = None, stream=None) -> dict:
+    """vp_plan_batch on demands D [B, N, N] (int64, GPU), one workgroup per matrix;
+    status is int32 [B] (matrix b's device errors)."""
+    _dev(D, torch.int64, "demand")
+    N = cat.N
+    if D.dim() != 3 or tuple(D.shape[1:]) != (N, N):
+        raise ValueError("demand must be [B, %d, %d]" % (N, N))
+    B = D.shape[0]
+    if out is None:
+        out = alloc_schedule_batch(B, N, p.k_max, D.device)
+    if out["K"].numel() != B or tuple(out["dst"].shape) != (B, p.k_max, N):
+        raise ValueError("schedule buffers do not hold B = %d schedules of k_max = %d" % (B, p.k_max))
+    if status is None:
+        status = torch.zeros(B, dtype=torch.int32, device=D.device)
+    if status.numel() != B:
+        raise ValueError("status must hold B entries")
+    need = plan_batch_workspace_bytes(cat, p, B)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=D.device)
+    _check(lib().vp_plan_batch(cat.handle, B, _ptr(D), C.byref(p), _ptr(out["K"]), _ptr(out["family"]),
+                               _ptr(out["dst"]), _ptr(out["inst"]), _ptr(out["bytes"]), _ptr(out.get("send_off")),
+                               _ptr(out.get("stream_off")), _ptr(out.get("recv_src")), _ptr(out["tau"]),
+                               _ptr(status), _ptr(ws), ws.numel(), _stream(stream)), "vp_plan_batch")
     out["status"] = status
     return out
 

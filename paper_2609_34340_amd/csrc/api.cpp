@@ -274,18 +274,21 @@ void vp_plan_params_default(int32_t n_ranks, int64_t unit_bytes, vp_plan_params*
   p->reserved = 0;
 }
 
-size_t vp_plan_workspace(const vp_catalog* c, const vp_plan_params* p) {
+size_t vp_plan_workspace(const vp_catalog* c, const vp_plan_params* p) { return vp_plan_batch_workspace(c, p, 1); }
+
+size_t vp_plan_batch_workspace(const vp_catalog* c, const vp_plan_params* p, int32_t batch) {
   (void)p;
-  if (!c) return 0;
-  return (size_t)c->N * (size_t)c->N * sizeof(int64_t);
+  if (!c || batch < 1) return 0;
+  return (size_t)batch * (size_t)c->N * (size_t)c->N * sizeof(int64_t);
 }
 
-vp_status vp_plan(const vp_catalog* c, const int64_t* demand, const vp_plan_params* p, int32_t* K,
-                  int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes, int64_t* send_off,
-                  int64_t* stream_off, int32_t* recv_src, int64_t* tau, int32_t* dev_status, void* ws,
-                  size_t ws_bytes, void* stream) {
+vp_status vp_plan_batch(const vp_catalog* c, int32_t batch, const int64_t* demand, const vp_plan_params* p,
+                        int32_t* K, int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes, int64_t* send_off,
+                        int64_t* stream_off, int32_t* recv_src, int64_t* tau, int32_t* dev_status, void* ws,
+                        size_t ws_bytes, void* stream) {
   if (!c || !demand || !p || !K || !family || !dst || !inst || !bytes || !dev_status)
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
+  if (batch < 1 || batch > 65535) return set_error(VP_ERR_INVALID_ARGUMENT, "batch must be in [1, 65535]");
   if ((send_off == nullptr) != (stream_off == nullptr))
     return set_error(VP_ERR_INVALID_ARGUMENT, "send_off and stream_off go together");
   if (!c->dev) return set_error(VP_ERR_INVALID_ARGUMENT, "catalog not uploaded");
@@ -297,9 +300,19 @@ vp_status vp_plan(const vp_catalog* c, const int64_t* demand, const vp_plan_para
     return set_error(VP_ERR_INVALID_ARGUMENT, "bad plan parameters");
   if (p->lambda_ns > (int64_t(1) << 40) || p->k_target > (int64_t(1) << 40))
     return set_error(VP_ERR_UNSUPPORTED, "lambda or k_target too large");
-  if (ws_bytes < vp_plan_workspace(c, p) || !ws) return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
-  vp::PlanLaunch a{c, demand, (int64_t*)ws, *p, K, family, dst, inst, bytes, tau, send_off, stream_off, recv_src, dev_status};
+  if (ws_bytes < vp_plan_batch_workspace(c, p, batch) || !ws)
+    return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
+  vp::PlanLaunch a{c, demand, (int64_t*)ws, *p, K, family, dst, inst, bytes, tau, send_off, stream_off, recv_src,
+                   dev_status, batch};
   return vp::launch_plan(a, stream);
+}
+
+vp_status vp_plan(const vp_catalog* c, const int64_t* demand, const vp_plan_params* p, int32_t* K,
+                  int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes, int64_t* send_off,
+                  int64_t* stream_off, int32_t* recv_src, int64_t* tau, int32_t* dev_status, void* ws,
+                  size_t ws_bytes, void* stream) {
+  return vp_plan_batch(c, 1, demand, p, K, family, dst, inst, bytes, send_off, stream_off, recv_src, tau,
+                       dev_status, ws, ws_bytes, stream);
 }
 
 size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_bytes, int64_t T, int32_t k) {

@@ -92,6 +92,7 @@ struct PlanLaunch {
   int64_t *send_off, *stream_off;
   int32_t* recv_src;
   int32_t* status;
+  int32_t batch;   // matrices planned side by side, one workgroup each
 };
 vp_status launch_plan(const PlanLaunch& a, void* stream);
 

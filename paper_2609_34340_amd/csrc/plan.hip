@@ -74,6 +74,7 @@ struct PlanArgs {
   int64_t *send_off, *stream_off;   // optional [k_max][N] buffer layout per rank
   int32_t* recv_src;                // optional [k_max][N]: the rank whose lane lands at each rank
   int32_t* status;
+  int32_t batch;                    // matrices, one workgroup each; every buffer above holds `batch` of them
   // LDS layout (byte offsets)
   int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo;
   int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_iid, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bid, o_bx, o_brw,
@@ -488,6 +489,17 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   const DevCatalogLayout& L = P.L;
   const int N = L.N, Q = L.Q, nn = L.nn, QG = Q * g;
   const int NP = L.J0 + L.J1, NS = P.n_start, FL = L.F0 + L.F1;
+  // workgroup b plans matrix b of the batch: every global buffer is offset by b
+  const size_t b = blockIdx.x, NN = (size_t)N * N, KN = (size_t)P.k_max * N;
+  const int64_t* gD = P.D + b * NN;
+  int64_t* gDrem = P.Drem + b * NN;
+  int32_t* gfamily = P.family + b * P.k_max;
+  int32_t* gdst = P.dst + b * KN;
+  int32_t* ginst = P.inst + b * KN;
+  int64_t* gbytes = P.bytes + b * KN;
+  int64_t* gsend_off = P.send_off ? P.send_off + b * KN : nullptr;
+  int64_t* gstream_off = P.stream_off ? P.stream_off + b * KN : nullptr;
+  int32_t* grecv_src = P.recv_src ? P.recv_src + b * KN : nullptr;
   Shared* sh = (Shared*)(smem + P.o_sh);
   int32_t* rinfo = (int32_t*)(smem + P.o_rinfo);
   int32_t* agg = (int32_t*)(smem + P.o_agg);         // [q][q2][k] units: k = 0 is A, k > 0 is B_k;
@@ -594,11 +606,11 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       const int ri = rinfo[i], ni = ri >> 8, qi = (ri >> 4) & 15;
       int64_t rs = 0;
       for (int j = lane; j < N; j += 64) {
-        const int64_t v = P.D[(size_t)i * N + j];
+        const int64_t v = gD[(size_t)i * N + j];
         const bool divisible = ((uint64_t)v & mask) == 0 &&
                                ((uint64_t)v >> P.unit_shift) * P.odd_inv <= P.odd_lim;
         if (v < 0 || (i == j && v != 0) || !divisible) bad = true;
-        P.Drem[(size_t)i * N + j] = v;
+        gDrem[(size_t)i * N + j] = v;
         rs += v;
         if (v > 0) {
           const int rj = rinfo[j], nj = rj >> 8, qj = (rj >> 4) & 15;
@@ -801,7 +813,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
               int32_t v = kForbiddenU;
               uint32_t rv = kForbidden;
               if (i != j) {
-                const int64_t dv = lastj[i] == j ? lastv[i] : P.Drem[(size_t)i * N + j];
+                const int64_t dv = lastj[i] == j ? lastv[i] : gDrem[(size_t)i * N + j];
                 // min(D^rem, cap) < 2^31 bytes, a multiple of the unit: exact quotient
                 const uint32_t vb = (uint32_t)(dv < cap ? dv : cap);
                 v = (int32_t)((vb >> P.unit_shift) * (uint32_t)P.odd_inv);
@@ -970,20 +982,20 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         const int64_t x = (int64_t)xu * P.unit;
         const uint32_t rv = live ? RW[t * g2 + s_ * g + d_] : brw[t];
         const size_t o = (size_t)K * N + i;
-        P.dst[o] = j;
-        P.inst[o] = live ? iid[(size_t)sh->best_c * N + t] : bid[t];
-        P.bytes[o] = x;
-        if (P.recv_src) P.recv_src[(size_t)K * N + j] = i;   // pi_k is a permutation
-        if (P.send_off) {
+        gdst[o] = j;
+        ginst[o] = live ? iid[(size_t)sh->best_c * N + t] : bid[t];
+        gbytes[o] = x;
+        if (grecv_src) grecv_src[(size_t)K * N + j] = i;   // pi_k is a permutation
+        if (gsend_off) {
           // Sec. 5 buffer layout: where this lane's slice sits in rank i's
           // send buffer and in its stream to j (bytes sent there before)
-          const int64_t before = rv < kRawSaturated ? (int64_t)rv : P.Drem[(size_t)i * N + j];
-          P.send_off[o] = sacc[i];
-          P.stream_off[o] = P.D[(size_t)i * N + j] - before;
+          const int64_t before = rv < kRawSaturated ? (int64_t)rv : gDrem[(size_t)i * N + j];
+          gsend_off[o] = sacc[i];
+          gstream_off[o] = gD[(size_t)i * N + j] - before;
           sacc[i] += x;
         }
         if (xu > 0) {
-          int64_t* dp = P.Drem + (size_t)i * N + j;
+          int64_t* dp = gDrem + (size_t)i * N + j;
           int64_t nv;
           if (__builtin_expect(rv < kRawSaturated, 1)) nv = (int64_t)rv - x;
           else nv = *dp - x;   // the residual did not fit the 32-bit copy
@@ -996,7 +1008,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         }
       }
       if (tid == 0) {
-        P.family[K] = f;
+        gfamily[K] = f;
         if (sh->best_S == 0) {
           set_err(sh, VP_ERR_NO_PROGRESS);
         } else {
@@ -1016,9 +1028,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   }
 
   if (tid == 0) {
-    *P.K = sh->K;
-    if (P.tau) *P.tau = sh->err == VP_ERR_INVALID_DEMAND ? 0 : sh->tau;
-    if (sh->err) atomicCAS(P.status, 0, sh->err);
+    P.K[b] = sh->K;
+    if (P.tau) P.tau[b] = sh->err == VP_ERR_INVALID_DEMAND ? 0 : sh->tau;
+    if (sh->err) atomicCAS(P.status + b, 0, sh->err);
   }
 }
 
@@ -1030,7 +1042,7 @@ vp_status launch_t(const PlanArgs& P, size_t lds, hipStream_t st) {
   if (hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
       hipSuccess)
     return set_error(VP_ERR_HIP, "cannot raise the planner's LDS limit");
-  hipLaunchKernelGGL(kern, dim3(1), dim3(kPlanThreads), lds, st, P);
+  hipLaunchKernelGGL(kern, dim3((unsigned)P.batch), dim3(kPlanThreads), lds, st, P);
   if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "planner launch failed");
   return VP_OK;
 }
@@ -1115,6 +1127,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   P.stream_off = a.stream_off;
   P.recv_src = a.recv_src;
   P.status = a.status;
+  P.batch = a.batch;
 
   size_t o = 0;
   auto take = [&](int32_t* field, size_t bytes) {
