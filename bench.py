@@ -15,7 +15,9 @@ all enqueued on one stream with no host synchronisation, inputs resident in
 HBM.  Steps cycle over `--matrices` distinct demand matrices and two send
 buffers.  Unless --no-batch, vp_plan_batch then plans D with D^T, and 16 to
 256 matrices, in one launch each ("plan_batch": launch time and us per
-matrix; the headline plan time stays the one-matrix latency).  Unless --no-sweep, the other four workloads (N = 8, 16, 64 and the
+matrix; the headline plan time stays the one-matrix latency).  Unless
+--no-receive, the dispatch unpack and the combine pack / unpack of the first
+matrix are timed ("receive").  Unless --no-sweep, the other four workloads (N = 8, 16, 64 and the
 16-rank Ulysses case) follow with six timed steps each, under "per_config";
 unless --no-extra, the planner then runs on the uniform, skew and head/context
 demands with the full and the nearest-path catalog (the peer/path ablation),
@@ -183,6 +185,68 @@ def measure(w, steps, warmup, M, dev):
     return r
 
 
+def receive_section(w, routing_np, dev, reps=10):
+    """Receive side and combine of the first matrix, timed with HIP events
+    (mean of `reps` calls): the dispatch unpack at the busiest receiving rank
+    r (its received rows into the expert-major output), the combine pack at r
+    (those rows back, in the order of the schedule planned on D^T) and the
+    combine unpack at rank 0 (its returned rows into (token, slot) order).
+    Buffers hold arbitrary bytes: only sizes and the schedules matter to the
+    copies.  GB/s counts every row read once and written once."""
+    import torch
+    import paper_2609_34340_amd as vp
+    N, rb = w.n_ranks, w.row_bytes
+    sb = vp.slot_bytes(rb)
+    cat = vp.Catalog(w.topo)
+    cat.upload()
+    p = vp.plan_params(N, rb)
+    st = vp.new_status(dev)
+    dem = vp.demand(torch.from_numpy(routing_np).to(dev), N, w.experts, rb, sort_row=0, status=st)
+    D = dem["demand"]
+    disp = vp.plan(cat, D, p, status=st, out=vp.alloc_schedule(N, p.k_max, dev, layout=True))
+    comb = vp.plan(cat, vp.demand_transpose(D), p, status=st, out=vp.alloc_schedule(N, p.k_max, dev, layout=True))
+    torch.cuda.synchronize()
+    Dh = D.cpu().numpy()
+    r = int(Dh.sum(axis=0).argmax())
+    rows_r = int(Dh[:, r].sum()) // rb
+    counts = dem["counts"]
+    eloc = w.experts // N
+    out_rows = int(counts[:, r * eloc:(r + 1) * eloc].sum().item())
+    recv = torch.empty(rows_r * sb, dtype=torch.uint8, device=dev)
+    outb = torch.empty(max(out_rows, 1) * sb, dtype=torch.uint8, device=dev)
+    send = torch.empty(rows_r * rb, dtype=torch.uint8, device=dev)
+    step_off = torch.empty(p.k_max + 1, dtype=torch.int64, device=dev)
+    rows_0 = int(Dh[0].sum()) // rb
+    recv0 = torch.empty(rows_0 * sb, dtype=torch.uint8, device=dev)
+    combined = torch.empty(w.tokens * w.top_k * sb, dtype=torch.uint8, device=dev)
+    ws = torch.empty(vp.unpack_workspace_bytes(max(rows_r, rows_0, out_rows)), dtype=torch.uint8, device=dev)
+
+    def timed(fn):
+        fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps
+
+    res = {"receiver": r, "rows": rows_r, "row_bytes": rb}
+    us = timed(lambda: vp.unpack_rows(recv, rb, counts, r, disp, outb, st, ws=ws))
+    res["unpack_rows"] = {"us": round(us, 2), "GBps": round(2 * rows_r * rb / us / 1e3, 1)}
+    us = timed(lambda: vp.pack_combine(outb, rb, counts, r, comb, send, step_off, st, ws=ws))
+    res["pack_combine"] = {"us": round(us, 2), "GBps": round(2 * rows_r * rb / us / 1e3, 1)}
+    us = timed(lambda: vp.unpack_combine(recv0, rb, w.tokens, w.top_k, dem["sorted_tok"], dem["sorted_slot"],
+                                         dem["dest_off"], 0, comb, combined, st, ws=ws))
+    res["unpack_combine"] = {"us": round(us, 2), "GBps": round(2 * rows_0 * rb / us / 1e3, 1), "rank": 0,
+                             "rows": rows_0}
+    if vp.read_status(st) != 0:
+        raise SystemExit("device error on the receive side: %d" % vp.read_status(st))
+    del recv, outb, send, recv0, combined, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def batch_section(w, routing_list, dev, sizes=(2, 16, 64, 256)):
     """vp_plan_batch: B matrices planned side by side (one workgroup each).
     B = 2 is a layer's dispatch matrix D and its combine matrix D^T; larger
@@ -337,6 +401,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the short runs of the other configurations (plan time at every N)")
     ap.add_argument("--no-batch", action="store_true", help="skip the batched-planner timings")
+    ap.add_argument("--no-receive", action="store_true", help="skip the receive-side and combine timings")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the planner on the extra demands and the nearest-path ablation")
     ap.add_argument("--calibrate-copy", type=int, default=0,
@@ -411,6 +476,9 @@ def main():
                      "algorithmic_bytes_per_launch": int(r["gather_bytes"].mean()),
                      "avg_launch_us": round(float(r["gather_ms"].mean() * 1e3), 2)},
     }
+    if w.mode == "moe" and not args.no_receive:
+        print("[bench] receive side and combine", file=sys.stderr, flush=True)
+        out["receive"] = receive_section(w, r["routing_np"][0], dev)
     if w.mode == "moe" and not args.no_batch:
         print("[bench] batched planning", file=sys.stderr, flush=True)
         out["plan_batch"] = batch_section(w, r["routing_np"], dev)

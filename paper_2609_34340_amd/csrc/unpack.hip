@@ -20,7 +20,8 @@
 //          the other side: an expert-major output row, or token * k + slot.
 //          The workgroup of the last step also checks that every peer's
 //          stream is covered exactly.
-//   copy   one workgroup per buffer row: 16-byte loads, non-temporal stores.
+//   copy   one workgroup per buffer row: 16-byte loads issued a pass at a
+//          time ahead of the non-temporal stores.
 //   transpose  D^T for the combine's plan, in 32 x 32 LDS tiles.
 #include <hip/hip_runtime.h>
 
@@ -270,24 +271,34 @@ __global__ void __launch_bounds__(kMapThreads) map_kernel(MapArgs a) {
   }
 }
 
-constexpr int kCopyMaxThreads = 512;
-constexpr int64_t kCopyMaxGrid = 1 << 16;
-
 // Buffer row g <-> mapped row map[g]: read from the mapped side (map_src) or
-// write to it.  Rows are whole 16-byte vectors.
-__global__ void __launch_bounds__(kCopyMaxThreads) copy_rows_kernel(
-    const unsigned char* __restrict__ src, int64_t src_stride, unsigned char* __restrict__ dst,
-    int64_t dst_stride, int64_t vpr, const int32_t* __restrict__ map, int map_src, const int64_t* total,
-    int64_t rows_cap, const int32_t* status) {
+// write to it.  Rows are whole 16-byte vectors.  One workgroup per row; TH
+// threads move it in passes of V vectors per thread, every load of a pass
+// issued before its stores (about 2 KiB in flight per wavefront, as for the
+// dispatch scatter).
+template <int TH, int V>
+__global__ void __launch_bounds__(TH) copy_rows_kernel(const unsigned char* __restrict__ src, int64_t src_stride,
+                                                       unsigned char* __restrict__ dst, int64_t dst_stride,
+                                                       int64_t vpr, const int32_t* __restrict__ map, int map_src,
+                                                       const int64_t* total, int64_t rows_cap,
+                                                       const int32_t* status) {
   if (*status != 0) return;
   int64_t U = *total;
   U = U < rows_cap ? U : rows_cap;
-  for (int64_t g = blockIdx.x; g < U; g += gridDim.x) {
-    const int64_t m = map[g];
-    const int64_t sr = map_src ? m : g, dr = map_src ? g : m;
-    const u32x4* s = (const u32x4*)(src + sr * src_stride);
-    u32x4* d = (u32x4*)(dst + dr * dst_stride);
-    for (int64_t v = threadIdx.x; v < vpr; v += blockDim.x) __builtin_nontemporal_store(s[v], d + v);
+  const int64_t g = blockIdx.x;
+  if (g >= U) return;
+  const int64_t m = map[g];
+  const int64_t sr = map_src ? m : g, dr = map_src ? g : m;
+  const u32x4* s = (const u32x4*)(src + sr * src_stride);
+  u32x4* d = (u32x4*)(dst + dr * dst_stride);
+  for (int64_t e0 = threadIdx.x; e0 < vpr; e0 += (int64_t)V * TH) {
+    u32x4 r[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+      if (e0 + i * TH < vpr) r[i] = s[e0 + i * TH];
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+      if (e0 + i * TH < vpr) __builtin_nontemporal_store(r[i], d + e0 + i * TH);
   }
 }
 
@@ -334,12 +345,26 @@ vp_status launch_unpack(const UnpackLaunch& a, void* stream) {
             map, total, a.status};
   hipLaunchKernelGGL(map_kernel, dim3(a.k_max), dim3(kMapThreads), lds, s, m);
   if (a.rows_cap > 0) {
+    if (a.rows_cap >= ((int64_t)1 << 31)) return set_error(VP_ERR_UNSUPPORTED, "too many buffer rows");
     const int64_t vpr = a.row_bytes / 16;
-    const int threads = (int)std::min<int64_t>(kCopyMaxThreads, (vpr + 63) / 64 * 64);
-    const int64_t grid = std::min<int64_t>(a.rows_cap, kCopyMaxGrid);
-    hipLaunchKernelGGL(copy_rows_kernel, dim3((unsigned)grid), dim3(threads), 0, s,
-                       (const unsigned char*)a.src, a.src_stride, (unsigned char*)a.dst_buf, a.dst_stride, vpr,
-                       map, a.mode == kModeCombinePack ? 1 : 0, total, a.rows_cap, a.status);
+    const dim3 grid((unsigned)a.rows_cap);   // rows past the buffer's count exit at once
+    const unsigned char* sp = (const unsigned char*)a.src;
+    unsigned char* dp = (unsigned char*)a.dst_buf;
+    const int ms = a.mode == kModeCombinePack ? 1 : 0;
+    // about 2 KiB per wavefront: rows up to 2, 4 and 8 KiB take 1, 2 and 4
+    // wavefronts of two vectors per thread, longer rows 8 wavefronts of one
+    if (vpr <= 128)
+      hipLaunchKernelGGL((copy_rows_kernel<64, 2>), grid, dim3(64), 0, s, sp, a.src_stride, dp, a.dst_stride, vpr,
+                         map, ms, total, a.rows_cap, a.status);
+    else if (vpr <= 256)
+      hipLaunchKernelGGL((copy_rows_kernel<128, 2>), grid, dim3(128), 0, s, sp, a.src_stride, dp, a.dst_stride, vpr,
+                         map, ms, total, a.rows_cap, a.status);
+    else if (vpr <= 512)
+      hipLaunchKernelGGL((copy_rows_kernel<256, 2>), grid, dim3(256), 0, s, sp, a.src_stride, dp, a.dst_stride, vpr,
+                         map, ms, total, a.rows_cap, a.status);
+    else
+      hipLaunchKernelGGL((copy_rows_kernel<512, 1>), grid, dim3(512), 0, s, sp, a.src_stride, dp, a.dst_stride, vpr,
+                         map, ms, total, a.rows_cap, a.status);
   }
   if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "unpack launch failed");
   return VP_OK;
