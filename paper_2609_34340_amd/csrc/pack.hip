@@ -4,21 +4,23 @@
 // are appended to the send buffer.
 //
 // Kernels
-//   slices   one block; after one round of global loads everything runs in
-//            LDS: step offsets (exclusive scan of this rank's lane volumes)
-//            and each step's offset inside its destination's stream (a
-//            stable counting sort of the steps by destination -- per-wave
-//            ballot ranks over contiguous chunks, one scan over destinations
-//            and waves -- then a scan of the volumes in (destination, step)
-//            order).  For token rows it also clears the per-token copy
-//            counters.
-//   index    one wavefront per step.  Rows: every packed unit is one copy of
-//            a token row, and its send-unit index joins that token's copy
-//            list.  Heads: the source byte offset of every packed unit.
+//   slices   only when the planner's buffer layout is not passed: one block;
+//            after one round of global loads everything runs in LDS: step
+//            offsets (exclusive scan of this rank's lane volumes) and each
+//            step's offset inside its destination's stream (a stable
+//            counting sort of the steps by destination -- per-wave ballot
+//            ranks over contiguous chunks, one scan over destinations and
+//            waves -- then a scan of the volumes in (destination, step)
+//            order).
+//   index    one workgroup per step.  Rows: every packed unit is one copy of
+//            a token row; its send unit goes to the entry of that (token,
+//            routing slot), tagged with the call's generation, so the list is
+//            never cleared.  Heads: the source byte offset of every packed
+//            unit.
 //   scatter  rows: one workgroup per (token, copy), XCD-aware so that all
 //            copies of a token run on one XCD: a source row leaves HBM once
 //            however many destinations it has, and the XCDs write
-//            neighbouring tokens at any moment.
+//            neighbouring tokens at any moment; launch shape by row size.
 //   gather   heads: grid-stride 16-byte copy of the units (each is read
 //            once) with non-temporal stores.
 #include <hip/hip_runtime.h>

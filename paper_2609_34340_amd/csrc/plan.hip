@@ -1,6 +1,6 @@
 // vp_plan: online channel-guided demand decomposition (Sec. 4.2, Alg. 2) as
 // one persistent workgroup of 1024 threads that runs the whole iteration
-// loop on the device.
+// loop on the device (vp_plan_batch: one such workgroup per matrix).
 //
 // Per iteration:
 //   1. shape scores, Eq. (5)-(6), from node-block aggregates kept in LDS:
