@@ -472,3 +472,47 @@ def test_pipeline_matches_oracle(vp, cid):
     assert np.array_equal(pipe.dem["demand"].cpu().numpy(), D)
     assert_schedule_equal(vp.schedule_to_host(pipe.sched), s)
     assert torch.equal(send[:ref.size], torch.from_numpy(ref).cuda())
+
+
+def test_plan_largest_topology_is_a_valid_decomposition(vp):
+    """1,024 ranks (128 nodes), the planner's largest shape: too big for the
+    oracle to plan in test time, so the properties any valid schedule has are
+    checked instead -- the activations sum to D exactly, every step is a
+    derangement whose lanes use path classes of their group pairs, every
+    step serves bytes, and K stays within k_max (raised to 32N)."""
+    topo = vpgen.Topology(128)
+    N = topo.n_ranks
+    rng = np.random.default_rng(1024)
+    unit = 4096
+    # MoE-like skew: light traffic between every pair plus a global set of
+    # hot destinations (a tenth of the ranks), as in the 256-rank workload
+    D = rng.integers(0, 8, (N, N)).astype(np.int64)
+    hot = rng.choice(N, N // 10, replace=False)
+    D[:, hot] += rng.integers(20, 60, (N, hot.size))
+    np.fill_diagonal(D, 0)
+    # volumes of tens of thousands of units per rank, so that a quantum
+    # (tau at K_target = 2N) holds tens of units
+    D *= 32 * unit
+    log("plan on 1024 ranks")
+    # every pair carries bytes: the caller gives room beyond the default 8N
+    g = gpu_plan(vp, topo, D, unit, k_max=32 * N)
+    assert g["status"] == 0
+    K = g["K"]
+    log("1024 ranks: K = %d" % K)
+    assert N - 1 <= K <= 32 * N
+    dst, nb, inst = g["dst"], g["bytes"], g["inst"]
+    rows = np.arange(N)
+    for k in range(K):
+        assert np.array_equal(np.sort(dst[k]), rows) and not (dst[k] == rows).any()
+    X = np.zeros((N, N), np.int64)
+    np.add.at(X, (np.broadcast_to(rows, (K, N)), dst), nb)
+    assert np.array_equal(X, D)
+    assert (nb.sum(axis=1) > 0).all()
+    cls = gcat(vp, topo).instances()["cls"][inst]
+    gs, gd = rows[None, :] // topo.gpus_per_switch, dst // topo.gpus_per_switch
+    Q = topo.sockets_per_node * topo.switches_per_socket
+    same_switch = gs == gd
+    same_socket = (gs // Q == gd // Q) & ((gs % Q) // topo.switches_per_socket == (gd % Q) // topo.switches_per_socket)
+    assert (cls[same_switch] == vp.PATH_PIX).all()
+    assert np.isin(cls[same_socket & ~same_switch], [vp.PATH_PXB, vp.PATH_NIC]).all()
+    assert (cls[~same_socket] == vp.PATH_NIC).all()
