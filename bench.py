@@ -47,8 +47,14 @@ KERNEL_NAME = {"moe": "scatter_rows_kernel (vp_pack_gather, token rows)",
 
 
 def pack_source_sha() -> str:
-    with open(os.path.join(HERE, "paper_2609_34340_amd", "csrc", "pack.hip"), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of pack.hip's code with comments and blank lines left out: the
+    committed HBM-traffic profile applies while the code it measured is
+    unchanged."""
+    import re
+    with open(os.path.join(HERE, "paper_2609_34340_amd", "csrc", "pack.hip")) as f:
+        text = f.read()
+    code = [ln.rstrip() for ln in re.sub(r"//[^\n]*", "", text).split("\n")]
+    return hashlib.sha256("\n".join(ln for ln in code if ln.strip()).encode()).hexdigest()[:16]
 
 
 def rank0_accounting(w, routing0: np.ndarray):
