@@ -12,7 +12,8 @@
 //            ranks over contiguous chunks, one scan over destinations and
 //            waves -- then a scan of the volumes in (destination, step)
 //            order).
-//   index    one workgroup per step.  Rows: every packed unit is one copy of
+//   index    one workgroup per step (split over a few when steps are long).
+//            Rows: every packed unit is one copy of
 //            a token row; its send unit goes to the entry of that (token,
 //            routing slot), tagged with the call's generation, so the list is
 //            never cleared.  Heads: the source byte offset of every packed
@@ -268,22 +269,24 @@ constexpr int kIndexThreads = 256;
 // the list is never cleared.  Heads: the source byte offset of every packed
 // unit.
 __global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
-  const int i = blockIdx.x, tid = threadIdx.x;
-  if (i == 0 && tid == 0) *a.hdr = a.gen;
+  // workgroup (i, y) handles part y of step i's units (gridDim.y parts)
+  const int i = blockIdx.x, tid = threadIdx.x, y = blockIdx.y, ny = gridDim.y;
+  const bool lead = y == 0 && tid == 0;   // the one thread that writes a step's offsets
+  if (i == 0 && lead) *a.hdr = a.gen;
   StepDesc d;
   if (a.send_off) {
     const int K = *a.Kp, st = *a.status;
     if (K < 0 || K > a.k_max) {
-      if (i == 0 && tid == 0) report(a.status, VP_ERR_INVALID_ARGUMENT);
+      if (i == 0 && lead) report(a.status, VP_ERR_INVALID_ARGUMENT);
       return;
     }
     if (st != 0) return;
-    if (i == 0 && K == 0 && tid == 0) a.step_off[0] = 0;
+    if (i == 0 && K == 0 && lead) a.step_off[0] = 0;
     if (i >= K) return;
     const size_t o = (size_t)i * a.N + a.self;
     const int64_t x = a.bytes[o], so = a.send_off[o], co = a.stream_off[o];
     const int j = a.dst[o];
-    if (tid == 0) {
+    if (lead) {
       a.step_off[i] = so;
       if (i == K - 1) {
         a.step_off[K] = so + x;
@@ -294,7 +297,7 @@ __global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
     bool ok = x > 0 && x % a.unit == 0 && so >= 0 && so % a.unit == 0 && co >= 0 && co % a.unit == 0 &&
               j >= 0 && j < a.N && j != a.self;
     if (ok && so + x > a.send_capacity) {
-      if (tid == 0) report(a.status, VP_ERR_CAPACITY);
+      if (lead) report(a.status, VP_ERR_CAPACITY);
       return;
     }
     int64_t h = 0, b0 = 0;
@@ -304,7 +307,7 @@ __global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
       ok = co + x <= (a.mode == 0 ? h : a.T * h) * a.unit;
     }
     if (!ok) {
-      if (tid == 0) report(a.status, VP_ERR_INVALID_ARGUMENT);
+      if (lead) report(a.status, VP_ERR_INVALID_ARGUMENT);
       return;
     }
     d.first = a.mode == 0 ? b0 + co / a.unit : co / a.unit;
@@ -319,7 +322,7 @@ __global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
   }
   if (a.mode == 0) {
     const unsigned long long g = (unsigned long long)a.gen << 32;
-    for (int u = tid; u < d.nu; u += kIndexThreads) {
+    for (int u = tid + y * kIndexThreads; u < d.nu; u += kIndexThreads * ny) {
       const int64_t tok = a.sorted_tok[d.first + u];
       const int slot = a.sorted_slot[d.first + u];
       if (tok < 0 || tok >= a.T || slot >= a.k) {
@@ -329,7 +332,7 @@ __global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
       a.lst[tok * a.k + slot] = g | (unsigned)(d.u0 + u);
     }
   } else {
-    for (int u = tid; u < d.nu; u += kIndexThreads) {
+    for (int u = tid + y * kIndexThreads; u < d.nu; u += kIndexThreads * ny) {
       const int64_t p = d.first + u, tok = p / d.h, hd = d.h0 + (p - tok * d.h);
       a.src_off[(int64_t)d.u0 + u] = tok * a.token_stride + hd * a.unit;
     }
@@ -477,7 +480,13 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
     IndexArgs ia{a.mode, a.k, a.self_rank, a.N, a.k_max, a.unit, a.T, a.token_stride, a.send_capacity, gen,
                  a.sorted_tok, a.sorted_slot, desc, n_desc, a.K, a.dst, a.bytes, a.send_off, a.stream_off,
                  a.mode == 0 ? a.dest_off : a.head_lo, a.step_off, hdr, lst, src_off, a.status};
-    hipLaunchKernelGGL(index_kernel, dim3(a.k_max), dim3(kIndexThreads), 0, s, ia);
+    // a step holds up to one destination's whole stream: split it over up to
+    // 16 workgroups so that a thread handles about two of its units
+    const int64_t units = a.mode == 0 ? a.T * a.k : a.send_capacity / a.unit;
+    const int64_t per_step = (units + a.N - 1) / std::max(1, a.N);
+    const int ny = (int)std::min<int64_t>(16, std::max<int64_t>(1, (per_step + 2 * kIndexThreads - 1) /
+                                                                      (2 * kIndexThreads)));
+    hipLaunchKernelGGL(index_kernel, dim3(a.k_max, ny), dim3(kIndexThreads), 0, s, ia);
   }
   if (!(a.stages & 2)) {
     if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "pack launch failed");
