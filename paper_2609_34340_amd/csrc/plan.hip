@@ -186,7 +186,7 @@ struct FamCtx {
 template <int g, int MG>
 __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8_t* DL, int start,
                          const uint8_t* rperm, int lane, uint64_t top, PairRes* out) {
-  constexpr int g2 = g * g;
+  constexpr int g2 = g * g, kRow = g2 | 1;   // credit rows padded to an odd word count
   const int G = P.L.G;
   int o[MG][g], nn_[MG][g], ip[MG][g], sig[MG][g], del[MG][g];
   bool own[MG];
@@ -303,8 +303,8 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
       for (int m = 0; m < g; ++m)
 #pragma unroll
         for (int e = 0; e < g2; ++e) {
-          hs[r][m][e] = fc.H[o[r][m] * g2 + e];
-          hd[r][m][e] = fc.H[nn_[r][m] * g2 + e];
+          hs[r][m][e] = fc.H[o[r][m] * kRow + e];
+          hd[r][m][e] = fc.H[nn_[r][m] * kRow + e];
         }
   }
 
@@ -326,7 +326,7 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
         for (int m = 0; m < g; ++m) {
           jl[r][m] = DL[o[r][m]];
 #pragma unroll
-          for (int e = 0; e < g2; ++e) row[r][m][e] = kHold ? hs[r][m][e] : fc.H[o[r][m] * g2 + e];
+          for (int e = 0; e < g2; ++e) row[r][m][e] = kHold ? hs[r][m][e] : fc.H[o[r][m] * kRow + e];
         }
 #pragma unroll
       for (int r = 0; r < MG; ++r) {
@@ -383,7 +383,7 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
         for (int m = 0; m < g; ++m) {
           il[r][m] = SL[nn_[r][m]];
 #pragma unroll
-          for (int e = 0; e < g2; ++e) row[r][m][e] = kHold ? hd[r][m][e] : fc.H[nn_[r][m] * g2 + e];
+          for (int e = 0; e < g2; ++e) row[r][m][e] = kHold ? hd[r][m][e] : fc.H[nn_[r][m] * kRow + e];
         }
 #pragma unroll
       for (int r = 0; r < MG; ++r) {
@@ -444,7 +444,7 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
       jf[r][m] = DL[o[r][m]];
       cf[r][m] = own[r] ? fc.ocls[(lane + 64 * r) * g + m] : 0;
 #pragma unroll
-      for (int jl = 0; jl < g; ++jl) rf[r][m][jl] = fc.H[o[r][m] * g2 + sig[r][m] * g + jl];
+      for (int jl = 0; jl < g; ++jl) rf[r][m][jl] = fc.H[o[r][m] * kRow + sig[r][m] * g + jl];
     }
 #pragma unroll
   for (int r = 0; r < MG; ++r) {
@@ -484,7 +484,10 @@ __device__ inline void lds_barrier() {
 template <int g, int MG>
 __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  constexpr int g2 = g * g;
+  // credit rows of the g x g endpoint pairs of an instance, padded to an odd
+  // number of words so that the lanes of a wavefront reading consecutive
+  // instances' rows fall in different LDS banks
+  constexpr int g2 = g * g, kRow = g2 | 1;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const DevCatalogLayout& L = P.L;
   const int N = L.N, Q = L.Q, nn = L.nn, QG = Q * g;
@@ -802,8 +805,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           iid[base + t] = (uint8_t)(cat[L.off_fam_info + lf * QG + idx] >> 12);
           ipos[base + a * g + op] = (int8_t)(d == a ? mi : -1);
           const int64_t cap = sh->cap[cl];
-          int32_t* h = hp + (base + t) * g2;
-          uint32_t* rw = raw + (base + t) * g2;
+          int32_t* h = hp + (base + t) * kRow;
+          uint32_t* rw = raw + (base + t) * kRow;
           uint64_t kt = 0;
 #pragma unroll
           for (int il = 0; il < g; ++il)
@@ -873,7 +876,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       for (int pi = wave; pi < nc * NS; pi += kWaves) {
         const int c = pi / NS, s = pi - c * NS;
         FamCtx fc{outT + (size_t)c * N, inT + (size_t)c * N, ipos + (size_t)c * N, ocls + (size_t)c * N,
-                  hp + (size_t)c * N * g2, cb + c};
+                  hp + (size_t)c * N * kRow, cb + c};
         run_pair<g, MG>(P, fc, sl + (size_t)pi * N, dl + (size_t)pi * N, s, rp + (size_t)pi * L.G * 2, lane,
                         topkey[c], &pr[pi]);
       }
@@ -945,16 +948,16 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       if (cb + P.FC < fe && sh->best_chunk == cb) {
         // a later chunk reuses this LDS: keep the winner's binding and volumes
         const int pi = sh->best_c * NS + sh->best_s;
-        const int32_t* H = hp + (size_t)sh->best_c * N * g2;
-        const uint32_t* RW = raw + (size_t)sh->best_c * N * g2;
+        const int32_t* H = hp + (size_t)sh->best_c * N * kRow;
+        const uint32_t* RW = raw + (size_t)sh->best_c * N * kRow;
         for (int t = tid; t < N; t += kPlanThreads) {
           const uint8_t s_ = sl[(size_t)pi * N + t], d_ = dl[(size_t)pi * N + t];
           bsl[t] = s_;
           bdl[t] = d_;
           bid[t] = iid[(size_t)sh->best_c * N + t];
-          const int32_t hx = H[t * g2 + s_ * g + d_];
+          const int32_t hx = H[t * kRow + s_ * g + d_];
           bx[t] = (uint32_t)(hx > 0 ? hx : 0);
-          brw[t] = RW[t * g2 + s_ * g + d_];
+          brw[t] = RW[t * kRow + s_ * g + d_];
         }
         __syncthreads();
       }
@@ -968,8 +971,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       const int pi = sh->best_c * NS + sh->best_s;
       const uint8_t* SLp = live ? sl + (size_t)pi * N : bsl;
       const uint8_t* DLp = live ? dl + (size_t)pi * N : bdl;
-      const int32_t* H = hp + (size_t)sh->best_c * N * g2;
-      const uint32_t* RW = raw + (size_t)sh->best_c * N * g2;
+      const int32_t* H = hp + (size_t)sh->best_c * N * kRow;
+      const uint32_t* RW = raw + (size_t)sh->best_c * N * kRow;
       for (int t = tid; t < N; t += kPlanThreads) {
         const int n = rinfo[t] >> 8, idx = t - n * QG;
         const uint32_t w = finfo[lf * QG + idx];
@@ -977,10 +980,10 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         const int dn = (cl == VP_PATH_NIC && k) ? (n + k) % nn : n;
         const int s_ = SLp[t], d_ = DLp[t];
         const int i = (n * Q + ss) * g + s_, j = (dn * Q + ds) * g + d_;
-        int32_t xu = live ? H[t * g2 + s_ * g + d_] : (int32_t)bx[t];   // units
+        int32_t xu = live ? H[t * kRow + s_ * g + d_] : (int32_t)bx[t];   // units
         xu = xu > 0 ? xu : 0;   // a self pair serves nothing
         const int64_t x = (int64_t)xu * P.unit;
-        const uint32_t rv = live ? RW[t * g2 + s_ * g + d_] : brw[t];
+        const uint32_t rv = live ? RW[t * kRow + s_ * g + d_] : brw[t];
         const size_t o = (size_t)K * N + i;
         gdst[o] = j;
         ginst[o] = live ? iid[(size_t)sh->best_c * N + t] : bid[t];
@@ -1155,7 +1158,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_sacc, (size_t)N * 8);
   const size_t fixed = o;
   const size_t per_fam = align_up((size_t)NS * sizeof(PairRes), 16) + 2 * align_up((size_t)N * 2, 16) +
-                         3 * align_up((size_t)N, 16) + 2 * (size_t)N * g2 * 4 + 2 * align_up((size_t)NS * N, 16) + 16 +
+                         3 * align_up((size_t)N, 16) + 2 * (size_t)N * (g2 | 1) * 4 + 2 * align_up((size_t)NS * N, 16) + 16 +
                          align_up((size_t)NS * L.G * 2, 16);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return set_error(VP_ERR_HIP, "hipGetDevice failed");
@@ -1173,8 +1176,8 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_ipos, (size_t)FC * N);
   take(&P.o_ocls, (size_t)FC * N);
   take(&P.o_iid, (size_t)FC * N);
-  take(&P.o_hp, std::max((size_t)FC * N * g2 * 4, (size_t)N * 8));   // also the prologue's column sums
-  take(&P.o_raw, (size_t)FC * N * g2 * 4);
+  take(&P.o_hp, std::max((size_t)FC * N * (g2 | 1) * 4, (size_t)N * 8));   // also the prologue's column sums
+  take(&P.o_raw, (size_t)FC * N * (g2 | 1) * 4);
   take(&P.o_sl, (size_t)FC * NS * N);
   take(&P.o_dl, (size_t)FC * NS * N);
   take(&P.o_top, (size_t)FC * 8);
