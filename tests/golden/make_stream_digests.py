@@ -6,6 +6,7 @@ Only the oracle and the seeded input generators are called.  Runs one worker
 process per matrix batch (about 3 minutes on 8 cores).
 
     python tests/golden/make_stream_digests.py [--jobs 8]
+    python tests/golden/make_stream_digests.py --all-256 [--jobs 8]   # every matrix of the 256-rank stream
 """
 from __future__ import annotations
 
@@ -48,22 +49,26 @@ def oracle_job(args):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=8)
+    ap.add_argument("--all-256", action="store_true",
+                    help="digest all 1000 matrices of the 256-rank stream into %s" % os.path.basename(sd.GOLDEN_ALL5))
     args = ap.parse_args()
     import oracle
     import vpgen
     oracle.build()
     out = {"sample_stride": sd.SAMPLE_STRIDE, "streams": {}}
     ctx = mp.get_context("spawn")
-    for cid, mats in sd.STREAMS.items():
+    streams = {5: list(range(1000))} if args.all_256 else sd.STREAMS
+    target = sd.GOLDEN_ALL5 if args.all_256 else sd.GOLDEN
+    for cid, mats in streams.items():
         t0 = time.time()
         with ctx.Pool(args.jobs) as pool:
             rows = pool.map(oracle_job, [(cid, m) for m in mats], chunksize=1)
         out["streams"][str(cid)] = {"workload": vpgen.config(cid).name, "matrices": rows}
         print("C%d: %d matrices in %.0f s" % (cid, len(rows), time.time() - t0), flush=True)
-    with open(sd.GOLDEN, "w") as f:
+    with open(target, "w") as f:
         json.dump(out, f, indent=0)
         f.write("\n")
-    print("wrote", sd.GOLDEN)
+    print("wrote", target)
 
 
 if __name__ == "__main__":

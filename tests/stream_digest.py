@@ -29,6 +29,8 @@ SAMPLE_STRIDE = 4099
 # stream, every 10th of the 256-rank stream
 STREAMS = {3: list(range(100)), 5: list(range(0, 1000, 10))}
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "stream_digests.json")
+# every matrix of the 256-rank stream (an opt-in GPU check)
+GOLDEN_ALL5 = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "stream_digests_256_all.json")
 
 
 def _sha(*arrays) -> str:

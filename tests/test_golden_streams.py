@@ -39,3 +39,16 @@ def test_stream_digest_matches_oracle(golden, cid, m):
     assert s["K"] == ref["K"] and s["tau"] == ref["tau"]
     assert sd.schedule_digest(s) == ref["schedule"]
     assert int(s["bytes"][:, 0].sum()) == ref["send_bytes"]
+
+
+def test_full_256_stream_digests_agree_with_the_subset(golden):
+    """The digests of all 1000 matrices of the 256-rank stream (written by
+    the same script from the oracle) repeat the subset's digests exactly."""
+    import os
+    if not os.path.exists(sd.GOLDEN_ALL5):
+        pytest.skip("no full-stream digests")
+    with open(sd.GOLDEN_ALL5) as f:
+        full = {r["matrix"]: r for r in json.load(f)["streams"]["5"]["matrices"]}
+    assert sorted(full) == list(range(1000))
+    for r in golden["streams"]["5"]["matrices"]:
+        assert full[r["matrix"]] == r

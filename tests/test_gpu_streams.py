@@ -10,6 +10,7 @@ Routing for the next matrices is generated in worker processes while the GPU
 works."""
 import json
 import multiprocessing as mp
+import os
 import sys
 import time
 
@@ -36,13 +37,10 @@ def golden():
     return g
 
 
-@pytest.mark.parametrize("cid", [3, 5])
-def test_stream_parity(golden, cid):
+def check_stream(cid, rows):
     assert torch.cuda.is_available(), "GPU tests need a GPU"
     import paper_2609_34340_amd as vp
     w = vpgen.config(cid)
-    rows = golden["streams"][str(cid)]["matrices"]
-    assert [r["matrix"] for r in rows] == sd.STREAMS[cid]
     log("stream parity C%d: %d matrices (N=%d)" % (cid, len(rows), w.n_ranks))
     pipe = vp.Pipeline(w.topo, "moe", w.row_bytes, n_experts=w.experts, tokens=w.tokens, top_k=w.top_k)
     tok = torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda()
@@ -70,3 +68,20 @@ def test_stream_parity(golden, cid):
             if n % 10 == 9:
                 log("  C%d: %d matrices checked, %d differ (%.0f s)" % (cid, n + 1, len(bad), time.time() - t0))
     assert not bad, "matrices differing from the oracle: %s" % bad[:10]
+
+
+@pytest.mark.parametrize("cid", [3, 5])
+def test_stream_parity(golden, cid):
+    rows = golden["streams"][str(cid)]["matrices"]
+    assert [r["matrix"] for r in rows] == sd.STREAMS[cid]
+    check_stream(cid, rows)
+
+
+@pytest.mark.skipif(os.environ.get("VP_ALL_STREAMS") != "1" or not os.path.exists(sd.GOLDEN_ALL5),
+                    reason="all 1000 matrices of the 256-rank stream: opt in with VP_ALL_STREAMS=1 (several minutes)")
+def test_stream_parity_all_256():
+    with open(sd.GOLDEN_ALL5) as f:
+        g = json.load(f)
+    rows = g["streams"]["5"]["matrices"]
+    assert [r["matrix"] for r in rows] == list(range(1000))
+    check_stream(5, rows)
