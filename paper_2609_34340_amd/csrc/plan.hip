@@ -51,9 +51,6 @@ struct Shared {
   int64_t total_rem, Lmax, tau, total_units;
   int64_t cap[4];
   int32_t capu[4];
-  // best candidate so far in this iteration
-  int64_t best_S, best_xm, best_bm;
-  int32_t best_valid, best_f, best_k, best_c, best_s, best_chunk;
   int32_t K, err;
 };
 
@@ -68,6 +65,7 @@ struct PlanArgs {
   int32_t unit_shift;
   int32_t n_start, i_aa, k_max, FC;
   int32_t LPS, SPT;   // shift scoring: lanes per NIC-lane set (a power of two) and shifts per lane
+  int32_t LPS_log2;
   int32_t MLT, MRT;   // most diagonal-block terms of a pattern; largest NIC-lane set
   int32_t *K, *family, *dst, *inst;
   int64_t *bytes, *tau;
@@ -100,6 +98,13 @@ __device__ inline int64_t wave_max(int64_t v) { return __ockl_wfred_max_i64(v); 
 extern "C" __device__ __attribute__((const)) int __ockl_wfred_max_i32(int);
 __device__ inline uint64_t wave_max_u(uint64_t v) { return __ockl_wfred_max_u64(v); }
 __device__ inline int32_t wave_max32(int32_t v) { return __ockl_wfred_max_i32(v); }
+// lane 0's value in every lane (the whole wavefront active)
+__device__ inline int32_t lane0(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ inline int64_t lane0(int64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)v);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int32_t)(v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
 
 // Binding credits are held in pack units as int32 (every credit is a whole
 // number of units, so dividing by the unit keeps every comparison).  A self
@@ -556,8 +561,12 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     const int grp = r / g;
     rinfo[r] = ((grp / Q) << 8) | ((grp % Q) << 4) | (r - grp * g);
   }
-  for (int x = tid; x < NP * L.TS + 4; x += kPlanThreads)
-    terms[x] = x < NP * L.TS ? (uint16_t)cat[L.off_terms + x] : 0;
+  // a diagonal-block term is kept as its count | (q * Q + q2) << 4, the
+  // index of its slot pair's A row (the scoring loop reads nothing else)
+  for (int x = tid; x < NP * L.TS + 4; x += kPlanThreads) {
+    const int tv = x < NP * L.TS ? cat[L.off_terms + x] : 0;
+    terms[x] = (uint16_t)((tv & 15) | ((((tv >> 8) & 15) * Q + ((tv >> 4) & 15)) << 4));
+  }
   for (int p = tid; p < NP; p += kPlanThreads) {
     // terms are stored diagonal-block first, then shift-block
     const int n = cat[L.off_nterms + p];
@@ -671,7 +680,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       if (tid == 0) set_err(sh, VP_ERR_CAPACITY);
       break;
     }
-    const int K = sh->K;
+    // iteration-wide values read from LDS are made wavefront-uniform, so
+    // that what is derived from them runs on the scalar unit
+    const int K = lane0((int32_t)sh->K);
 
     // Step 1: score every shape; argmax.  A shape (k, p) scores base(p), its
     // diagonal-block terms against A, plus, for k > 0, the sum of B_k over
@@ -684,13 +695,16 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       const int na = L.nS * P.LPS;
       for (int x = tid; x < na + NP; x += kPlanThreads) {
         if (x < na) {
-          const int si = x / P.LPS, ch = x - si * P.LPS;
+          const int si = x >> P.LPS_log2, ch = x & (P.LPS - 1);
           const int k0 = 1 + ch * P.SPT, k1 = min(nn, k0 + P.SPT);
           // all loads unconditional and independent: absent terms read the zero row
           int off[kMaxRTerms];
 #pragma unroll
           for (int m = 0; m < kMaxRTerms; ++m) off[m] = rset[si * kMaxRTerms + m];
-          uint64_t bkey = 0;
+          // sums are never negative: the first shift always takes the lead,
+          // and a strict gain keeps the lowest of equal shifts
+          int32_t br = -1;
+          int bk = 0;
           for (int kb = k0; kb < k1; kb += 4) {
             int32_t r0 = 0, r1 = 0, r2 = 0, r3 = 0;
 #pragma unroll
@@ -705,15 +719,24 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
                 r3 += row[3];
               }
             }
-            const uint64_t c0 = ((uint64_t)(uint32_t)r0 << 12) | (uint64_t)(4095 - kb);
-            const uint64_t c1 = kb + 1 < k1 ? ((uint64_t)(uint32_t)r1 << 12) | (uint64_t)(4094 - kb) : 0;
-            const uint64_t c2 = kb + 2 < k1 ? ((uint64_t)(uint32_t)r2 << 12) | (uint64_t)(4093 - kb) : 0;
-            const uint64_t c3 = kb + 3 < k1 ? ((uint64_t)(uint32_t)r3 << 12) | (uint64_t)(4092 - kb) : 0;
-            bkey = c0 > bkey ? c0 : bkey;
-            bkey = c1 > bkey ? c1 : bkey;
-            bkey = c2 > bkey ? c2 : bkey;
-            bkey = c3 > bkey ? c3 : bkey;
+            if (r0 > br) {
+              br = r0;
+              bk = kb;
+            }
+            if (kb + 1 < k1 && r1 > br) {
+              br = r1;
+              bk = kb + 1;
+            }
+            if (kb + 2 < k1 && r2 > br) {
+              br = r2;
+              bk = kb + 2;
+            }
+            if (kb + 3 < k1 && r3 > br) {
+              br = r3;
+              bk = kb + 3;
+            }
           }
+          uint64_t bkey = br >= 0 ? ((uint64_t)(uint32_t)br << 12) | (uint64_t)(4095 - bk) : 0;
           // the LPS lanes of a set are adjacent lanes of one wavefront
           for (int o = 1; o < P.LPS; o <<= 1) {
             const uint64_t y = __shfl_xor(bkey, o);
@@ -734,7 +757,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
             for (int m = 0; m < 4; ++m) tv[m] = tp[m0 + m];
             int32_t av[4];
 #pragma unroll
-            for (int m = 0; m < 4; ++m) av[m] = agg[(((tv[m] >> 8) & 15) * Q + ((tv[m] >> 4) & 15)) * kS];
+            for (int m = 0; m < 4; ++m) av[m] = agg[__umul24((unsigned)(tv[m] >> 4), (unsigned)kS)];
 #pragma unroll
             for (int m = 0; m < 4; ++m) sb += (m0 + m < nl ? (tv[m] & 15) : 0) * av[m];
           }
@@ -760,7 +783,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       if (lane == 0 && best) atomicMax((unsigned long long*)&sh->key, (unsigned long long)best);
     }
     lds_barrier();
-    const uint64_t key = sh->key;
+    const uint64_t key = (uint64_t)lane0((int64_t)sh->key);
     if ((key >> 20) == 0) {
       __syncthreads();
       if (tid == 0) set_err(sh, VP_ERR_NO_PROGRESS);
@@ -768,10 +791,16 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     }
     const int code = 0xFFFFF - (int)(key & 0xFFFFF);
     const int kstar = code >> 12, pstar = kstar ? L.J0 + (code & 4095) : code;
-    const int lb = pfb[2 * pstar], le = pfb[2 * pstar + 1];
+    const int lb = lane0(pfb[2 * pstar]), le = lane0(pfb[2 * pstar + 1]);
     const int fbase = kstar == 0 ? 0 : (kstar - 1) * L.F1;
     const int fb = lb + fbase, fe = le + fbase;
-    if (tid == 0) sh->best_valid = 0;
+    // best candidate of the iteration so far: each wavefront that writes the
+    // winner evaluates the candidates itself (the same reads in the same
+    // order), so each holds it in registers and no barrier separates the
+    // evaluation from the update
+    bool best_valid = false;
+    int64_t best_S = 0, best_xm = 0, best_bm = 1;
+    int best_f = 0, best_c = 0, best_s = 0, best_chunk = 0;
 
     // Steps 2-3 over the shape's bucket, FC families at a time.
     int last_cb = fb;
@@ -841,35 +870,46 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           }
         }
         // the shuffled starts' permutations (Fisher-Yates on SplitMix64
-        // streams keyed by seed, iteration, family, start, group and side),
-        // taken from the highest thread down so that they mostly run on
-        // waves the gather leaves idle
-        const int nitems = nc * (NS - 1) * L.G * 2;
-        for (int y = kPlanThreads - 1 - tid; y < nitems; y += kPlanThreads) {
-          const int side = y & 1, z = y >> 1;
-          const int a = z % L.G, cs = z / L.G;
-          const int cc = cs / (NS - 1), st = 1 + (cs - cc * (NS - 1));
-          uint64_t k3 = P.seed;
-          k3 = sm_mix(k3 + kGolden) ^ (uint64_t)K;
-          k3 = sm_mix(k3 + kGolden) ^ (uint64_t)(cb + cc);
-          k3 = sm_mix(k3 + kGolden) ^ (uint64_t)st;
-          const uint64_t k4 = sm_mix(k3 + kGolden) ^ (uint64_t)a;
-          uint64_t state = sm_mix(k4 + kGolden) ^ (uint64_t)side;
-          int perm[g];
+        // streams keyed by seed, iteration, family, start, group and side):
+        // one (family, start) pair and 64 of its groups per wavefront, on the
+        // wavefronts the gather leaves idle (on all of them when it leaves
+        // none).  The pair's key prefix is uniform over the wavefront and a
+        // group's two sides share their key, so a lane draws one group.
+        {
+          const int pairs = nc * (NS - 1), gb = (L.G + 63) >> 6;
+          const int busy = (nc * N + 63) >> 6;
+          const int w0 = busy < kWaves ? busy : 0, nw = kWaves - w0;
+          for (int blk = lane0(wave) - w0; blk >= 0 && blk < pairs * gb; blk += nw) {
+            const int cs = blk / gb, a = (blk - cs * gb) * 64 + lane;
+            const int cc = cs / (NS - 1), st = 1 + (cs - cc * (NS - 1));
+            uint64_t k3 = P.seed;
+            k3 = sm_mix(k3 + kGolden) ^ (uint64_t)K;
+            k3 = sm_mix(k3 + kGolden) ^ (uint64_t)(cb + cc);
+            k3 = sm_mix(k3 + kGolden) ^ (uint64_t)st;
+            if (a < L.G) {
+              const uint64_t k5 = sm_mix((sm_mix(k3 + kGolden) ^ (uint64_t)a) + kGolden);
+              int packed = 0;
 #pragma unroll
-          for (int m = 0; m < g; ++m) perm[m] = m;
+              for (int side = 0; side < 2; ++side) {
+                uint64_t state = k5 ^ (uint64_t)side;
+                int perm[g];
 #pragma unroll
-          for (int m = g - 1; m >= 1; --m) {
-            state += kGolden;
-            const int j = (int)(sm_mix(state) % (uint64_t)(m + 1));
-            const int x2 = perm[m];
-            perm[m] = perm[j];
-            perm[j] = x2;
+                for (int m = 0; m < g; ++m) perm[m] = m;
+#pragma unroll
+                for (int m = g - 1; m >= 1; --m) {
+                  state += kGolden;
+                  const int j = (int)(sm_mix(state) % (uint64_t)(m + 1));
+                  const int x2 = perm[m];
+                  perm[m] = perm[j];
+                  perm[j] = x2;
+                }
+#pragma unroll
+                for (int m = 0; m < g; ++m) packed |= perm[m] << (2 * m + 8 * side);
+              }
+              // byte 2a + side of the pair's entry (little-endian halfword)
+              *(uint16_t*)(rp + ((size_t)(cc * NS + st) * L.G + a) * 2) = (uint16_t)packed;
+            }
           }
-          int packed = 0;
-#pragma unroll
-          for (int m = 0; m < g; ++m) packed |= perm[m] << (2 * m);
-          rp[((size_t)(cc * NS + st) * L.G + a) * 2 + side] = (uint8_t)packed;
         }
       }
       lds_barrier();
@@ -884,15 +924,22 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       // before the next gather reads D^rem
       __syncthreads();
       // Evaluate (Eq. (9)-(10)): best start per family, best family overall.
+      // Only the wavefronts that write the winner (threads t < N) evaluate.
       if (wave == 1)
         for (int x = lane; x < P.FC; x += 64) topkey[x] = 0;   // for the next gather
-      if (wave == 0) {
+      if (wave * 64 < N) {
         int64_t S = 0, xm = 0, bm = 1;
         int c = -1, bs = 0;
         for (int cc = lane; cc < nc; cc += 64) {
           int s0 = 0;
-          for (int s = 1; s < NS; ++s)
-            if (pr[cc * NS + s].F > pr[cc * NS + s0].F) s0 = s;
+          int64_t F0 = pr[cc * NS].F;
+          for (int s = 1; s < NS; ++s) {
+            const int64_t Fs = pr[cc * NS + s].F;
+            if (Fs > F0) {
+              F0 = Fs;
+              s0 = s;
+            }
+          }
           const PairRes& r = pr[cc * NS + s0];
           int64_t xm2 = 0, bm2 = 1;
           for (int cl = 0; cl < 2; ++cl) {
@@ -931,33 +978,40 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
             bs = bs2;
           }
         }
-        if (lane == 0 && (!sh->best_valid ||
-                          utility_greater(S, xm, bm, sh->best_S, sh->best_xm, sh->best_bm, P.lambda))) {
-          sh->best_valid = 1;
-          sh->best_S = S;
-          sh->best_xm = xm;
-          sh->best_bm = bm;
-          sh->best_f = cb + c;
-          sh->best_k = kstar;
-          sh->best_c = c;
-          sh->best_s = bs;
-          sh->best_chunk = cb;
+        // lane 0 holds the chunk's winner (every lane does after the
+        // reduction above): make it uniform
+        S = lane0(S);
+        xm = lane0(xm);
+        bm = lane0(bm);
+        c = lane0(c);
+        bs = lane0(bs);
+        if (!best_valid || utility_greater(S, xm, bm, best_S, best_xm, best_bm, P.lambda)) {
+          best_valid = true;
+          best_S = S;
+          best_xm = xm;
+          best_bm = bm;
+          best_f = cb + c;
+          best_c = c;
+          best_s = bs;
+          best_chunk = cb;
         }
       }
-      __syncthreads();
-      if (cb + P.FC < fe && sh->best_chunk == cb) {
-        // a later chunk reuses this LDS: keep the winner's binding and volumes
-        const int pi = sh->best_c * NS + sh->best_s;
-        const int32_t* H = hp + (size_t)sh->best_c * N * kRow;
-        const uint32_t* RW = raw + (size_t)sh->best_c * N * kRow;
-        for (int t = tid; t < N; t += kPlanThreads) {
-          const uint8_t s_ = sl[(size_t)pi * N + t], d_ = dl[(size_t)pi * N + t];
-          bsl[t] = s_;
-          bdl[t] = d_;
-          bid[t] = iid[(size_t)sh->best_c * N + t];
-          const int32_t hx = H[t * kRow + s_ * g + d_];
-          bx[t] = (uint32_t)(hx > 0 ? hx : 0);
-          brw[t] = RW[t * kRow + s_ * g + d_];
+      if (cb + P.FC < fe) {
+        // a later chunk reuses this LDS (and the top keys just cleared): keep
+        // the winner's binding and volumes, and wait for every wavefront
+        if (best_chunk == cb) {
+          const int pi = best_c * NS + best_s;
+          const int32_t* H = hp + (size_t)best_c * N * kRow;
+          const uint32_t* RW = raw + (size_t)best_c * N * kRow;
+          for (int t = tid; t < N; t += kPlanThreads) {
+            const uint8_t s_ = sl[(size_t)pi * N + t], d_ = dl[(size_t)pi * N + t];
+            bsl[t] = s_;
+            bdl[t] = d_;
+            bid[t] = iid[(size_t)best_c * N + t];
+            const int32_t hx = H[t * kRow + s_ * g + d_];
+            bx[t] = (uint32_t)(hx > 0 ? hx : 0);
+            brw[t] = RW[t * kRow + s_ * g + d_];
+          }
         }
         __syncthreads();
       }
@@ -965,14 +1019,14 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
 
     // Step 4: append E* and subtract X(E*) from D^rem and the aggregates.
     {
-      const int f = sh->best_f, k = sh->best_k;
+      const int f = best_f, k = kstar;
       const int lf = k == 0 ? f : L.F0 + (f - L.F0) % L.F1;
-      const bool live = sh->best_chunk == last_cb;
-      const int pi = sh->best_c * NS + sh->best_s;
+      const bool live = best_chunk == last_cb;
+      const int pi = best_c * NS + best_s;
       const uint8_t* SLp = live ? sl + (size_t)pi * N : bsl;
       const uint8_t* DLp = live ? dl + (size_t)pi * N : bdl;
-      const int32_t* H = hp + (size_t)sh->best_c * N * kRow;
-      const uint32_t* RW = raw + (size_t)sh->best_c * N * kRow;
+      const int32_t* H = hp + (size_t)best_c * N * kRow;
+      const uint32_t* RW = raw + (size_t)best_c * N * kRow;
       for (int t = tid; t < N; t += kPlanThreads) {
         const int n = rinfo[t] >> 8, idx = t - n * QG;
         const uint32_t w = finfo[lf * QG + idx];
@@ -986,15 +1040,18 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         const uint32_t rv = live ? RW[t * kRow + s_ * g + d_] : brw[t];
         const size_t o = (size_t)K * N + i;
         gdst[o] = j;
-        ginst[o] = live ? iid[(size_t)sh->best_c * N + t] : bid[t];
+        ginst[o] = live ? iid[(size_t)best_c * N + t] : bid[t];
         gbytes[o] = x;
         if (grecv_src) grecv_src[(size_t)K * N + j] = i;   // pi_k is a permutation
         if (gsend_off) {
           // Sec. 5 buffer layout: where this lane's slice sits in rank i's
-          // send buffer and in its stream to j (bytes sent there before)
+          // send buffer and in its stream to j (bytes sent there before:
+          // D[i][j] minus the residual before this step; D[i][j] is added by
+          // stream_off_kernel after the plan, which keeps its load off this
+          // loop's critical path)
           const int64_t before = rv < kRawSaturated ? (int64_t)rv : gDrem[(size_t)i * N + j];
           gsend_off[o] = sacc[i];
-          gstream_off[o] = gD[(size_t)i * N + j] - before;
+          gstream_off[o] = -before;
           sacc[i] += x;
         }
         if (xu > 0) {
@@ -1012,10 +1069,10 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       }
       if (tid == 0) {
         gfamily[K] = f;
-        if (sh->best_S == 0) {
+        if (best_S == 0) {
           set_err(sh, VP_ERR_NO_PROGRESS);
         } else {
-          sh->total_rem -= sh->best_S;
+          sh->total_rem -= best_S;
           sh->K = K + 1;
         }
         sh->key = 0;
@@ -1037,6 +1094,25 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   }
 }
 
+// Stream offsets, completed after the plan: the planner stored minus the
+// pair's residual before each step, and the bytes of the pair sent before it
+// are D[i][j] plus that (Sec. 5 buffer layout).  Block row b of the grid
+// handles matrix b of the batch; its steps k < K[b] only.
+__global__ void __launch_bounds__(256) stream_off_kernel(const int64_t* __restrict__ D, const int32_t* __restrict__ K,
+                                                         const int32_t* __restrict__ dst, int64_t* stream_off, int N,
+                                                         int k_max) {
+  const size_t b = blockIdx.y, NN = (size_t)N * N, KN = (size_t)k_max * N;
+  const int64_t* Db = D + b * NN;
+  const int32_t* db = dst + b * KN;
+  int64_t* sb = stream_off + b * KN;
+  const size_t n = (size_t)K[b] * N;
+  for (size_t x = (size_t)blockIdx.x * 256 + threadIdx.x; x < n; x += (size_t)gridDim.x * 256) {
+    const size_t i = x % (size_t)N;
+    const int j = db[x];   // every lane of a step is written; checked all the same
+    if ((unsigned)j < (unsigned)N) sb[x] += Db[i * N + j];
+  }
+}
+
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 template <int g, int MG>
@@ -1047,6 +1123,13 @@ vp_status launch_t(const PlanArgs& P, size_t lds, hipStream_t st) {
     return set_error(VP_ERR_HIP, "cannot raise the planner's LDS limit");
   hipLaunchKernelGGL(kern, dim3((unsigned)P.batch), dim3(kPlanThreads), lds, st, P);
   if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "planner launch failed");
+  if (P.stream_off) {
+    const size_t KN = (size_t)P.k_max * P.L.N;
+    const unsigned bx = (unsigned)std::max<size_t>(1, std::min<size_t>((KN + 255) / 256, 2048 / (size_t)P.batch));
+    hipLaunchKernelGGL(stream_off_kernel, dim3(bx, (unsigned)P.batch), dim3(256), 0, st, P.D, P.K, P.dst,
+                       P.stream_off, P.L.N, P.k_max);
+    if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "stream offset launch failed");
+  }
   return VP_OK;
 }
 
@@ -1119,6 +1202,8 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
     while (lps < 64 && lps * 8 < shifts) lps <<= 1;
     P.LPS = lps;
     P.SPT = (shifts + lps - 1) / lps;
+    P.LPS_log2 = 0;
+    while ((1 << P.LPS_log2) < lps) ++P.LPS_log2;
   }
   P.K = a.K;
   P.family = a.family;
