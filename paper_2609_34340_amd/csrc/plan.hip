@@ -66,6 +66,7 @@ struct PlanArgs {
   int32_t n_start, i_aa, k_max, FC;
   int32_t LPS, SPT;   // shift scoring: lanes per NIC-lane set (a power of two) and shifts per lane
   int32_t LPS_log2;
+  uint32_t qg_magic;  // ceil(2^32 / (Q g)): t / (Q g) = umulhi(t, qg_magic) for t < 2^16
   int32_t MLT, MRT;   // most diagonal-block terms of a pattern; largest NIC-lane set
   int32_t *K, *family, *dst, *inst;
   int64_t *bytes, *tau;
@@ -672,6 +673,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   }
   __syncthreads();
 
+  // the per-class caps are plan constants: held in registers
+  const int64_t cap_c0 = lane0(sh->cap[0]), cap_c1 = lane0(sh->cap[1]), cap_c2 = lane0(sh->cap[2]),
+                cap_c3 = lane0(sh->cap[3]);
   // ---------------------------------------------------------------- loop
   while (true) {
     if (sh->err || sh->total_rem == 0) break;
@@ -813,12 +817,16 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         int c = tid / N, t = tid - (tid / N) * N;
         const int dc = kPlanThreads / N, dt = kPlanThreads % N;
         for (int x = tid; x < tot; x += kPlanThreads) {
-          const int f = cb + c;
-          const int lf = kstar == 0 ? f : L.F0 + (f - L.F0) % L.F1;
-          const int n = rinfo[t] >> 8, idx = t - n * QG;
+          // local family: f - fbase stays inside the pattern's local range
+          const int lf = cb - fbase + c;
+          const int n = (int)__umulhi((unsigned)t, P.qg_magic), idx = t - n * QG;   // t / QG
           const uint32_t w = finfo[lf * QG + idx];
           const int cl = d_cls(w), a = n * Q + d_ss(w);
-          const int dn = (cl == VP_PATH_NIC && kstar) ? (n + kstar) % nn : n;
+          int dn = n;
+          if (cl == VP_PATH_NIC && kstar) {
+            dn = n + kstar;
+            if (dn >= nn) dn -= nn;
+          }
           const int d = dn * Q + d_ds(w);
           // rank of t inside the in-list of group d (family order = ascending t)
           const bool remote = cl == VP_PATH_NIC && kstar;
@@ -833,7 +841,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           // load overlaps the residual loads below
           iid[base + t] = (uint8_t)(cat[L.off_fam_info + lf * QG + idx] >> 12);
           ipos[base + a * g + op] = (int8_t)(d == a ? mi : -1);
-          const int64_t cap = sh->cap[cl];
+          const int64_t cap = cl == 0 ? cap_c0 : cl == 1 ? cap_c1 : cl == 2 ? cap_c2 : cap_c3;
           int32_t* h = hp + (base + t) * kRow;
           uint32_t* rw = raw + (base + t) * kRow;
           uint64_t kt = 0;
@@ -927,7 +935,25 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       // Only the wavefronts that write the winner (threads t < N) evaluate.
       if (wave == 1)
         for (int x = lane; x < P.FC; x += 64) topkey[x] = 0;   // for the next gather
-      if (wave * 64 < N) {
+      if (wave * 64 < N && fe - fb == 1) {
+        // a one-family shape: its best start wins, no utility to compare
+        // (every lane reads the same scores)
+        int s0 = 0;
+        int64_t F0 = pr[0].F;
+        for (int s = 1; s < NS; ++s) {
+          const int64_t Fs = pr[s].F;
+          if (Fs > F0) {
+            F0 = Fs;
+            s0 = s;
+          }
+        }
+        best_valid = true;
+        best_S = F0 * P.unit;
+        best_f = cb;
+        best_c = 0;
+        best_s = s0;
+        best_chunk = cb;
+      } else if (wave * 64 < N) {
         int64_t S = 0, xm = 0, bm = 1;
         int c = -1, bs = 0;
         for (int cc = lane; cc < nc; cc += 64) {
@@ -1020,7 +1046,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     // Step 4: append E* and subtract X(E*) from D^rem and the aggregates.
     {
       const int f = best_f, k = kstar;
-      const int lf = k == 0 ? f : L.F0 + (f - L.F0) % L.F1;
+      const int lf = f - fbase;
       const bool live = best_chunk == last_cb;
       const int pi = best_c * NS + best_s;
       const uint8_t* SLp = live ? sl + (size_t)pi * N : bsl;
@@ -1028,15 +1054,20 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       const int32_t* H = hp + (size_t)best_c * N * kRow;
       const uint32_t* RW = raw + (size_t)best_c * N * kRow;
       for (int t = tid; t < N; t += kPlanThreads) {
-        const int n = rinfo[t] >> 8, idx = t - n * QG;
+        const int n = (int)__umulhi((unsigned)t, P.qg_magic), idx = t - n * QG;   // t / QG
         const uint32_t w = finfo[lf * QG + idx];
         const int cl = d_cls(w), ss = d_ss(w), ds = d_ds(w);
-        const int dn = (cl == VP_PATH_NIC && k) ? (n + k) % nn : n;
+        int dn = n;
+        if (cl == VP_PATH_NIC && k) {
+          dn = n + k;
+          if (dn >= nn) dn -= nn;
+        }
         const int s_ = SLp[t], d_ = DLp[t];
         const int i = (n * Q + ss) * g + s_, j = (dn * Q + ds) * g + d_;
         int32_t xu = live ? H[t * kRow + s_ * g + d_] : (int32_t)bx[t];   // units
         xu = xu > 0 ? xu : 0;   // a self pair serves nothing
-        const int64_t x = (int64_t)xu * P.unit;
+        // the unit is below 2^31 (a cap of at least one unit fits 31 bits)
+        const int64_t x = (int64_t)((uint64_t)(uint32_t)xu * (uint32_t)P.unit);
         const uint32_t rv = live ? RW[t * kRow + s_ * g + d_] : brw[t];
         const size_t o = (size_t)K * N + i;
         gdst[o] = j;
@@ -1202,6 +1233,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
     while (lps < 64 && lps * 8 < shifts) lps <<= 1;
     P.LPS = lps;
     P.SPT = (shifts + lps - 1) / lps;
+    P.qg_magic = (uint32_t)(((uint64_t(1) << 32) + (uint64_t)QG - 1) / (uint64_t)QG);
     P.LPS_log2 = 0;
     while ((1 << P.LPS_log2) < lps) ++P.LPS_log2;
   }
