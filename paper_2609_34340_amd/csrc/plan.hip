@@ -673,6 +673,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   }
   __syncthreads();
 
+  // this thread's first (family, instance) item of a gather and the step
+  // between its items, fixed for the plan
+  const int g_c0 = tid / N, g_t0 = tid - (tid / N) * N, g_dc = kPlanThreads / N, g_dt = kPlanThreads % N;
   // the per-class caps are plan constants: held in registers
   const int64_t cap_c0 = lane0(sh->cap[0]), cap_c1 = lane0(sh->cap[1]), cap_c2 = lane0(sh->cap[2]),
                 cap_c3 = lane0(sh->cap[3]);
@@ -814,8 +817,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       // group lists and credits of every (family, instance)
       {
         const int tot = nc * N;
-        int c = tid / N, t = tid - (tid / N) * N;
-        const int dc = kPlanThreads / N, dt = kPlanThreads % N;
+        int c = g_c0, t = g_t0;
         for (int x = tid; x < tot; x += kPlanThreads) {
           // local family: f - fbase stays inside the pattern's local range
           const int lf = cb - fbase + c;
@@ -833,13 +835,28 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           const bool remote_first = dn >= kstar;   // cross-node sources sit on a lower node
           const int mi = d_rsame(w) + ((remote != remote_first) ? d_nother(w) : 0);
           const int op = d_opos(w);
+          // Every global load of the item is issued first, unconditionally:
+          // the residuals of its g x g pairs (a self pair's zero entry is
+          // read and not used; the value is stale only for the entry the
+          // last update changed, which LDS holds) and the instance id, which
+          // is only written out with the winner.
+          int64_t gv[g][g];
+#pragma unroll
+          for (int il = 0; il < g; ++il)
+#pragma unroll
+            for (int jl = 0; jl < g; ++jl) gv[il][jl] = gDrem[(size_t)(a * g + il) * N + d * g + jl];
+          const int idv = cat[L.off_fam_info + lf * QG + idx];
+          int lj[g];
+          int64_t lv[g];
+#pragma unroll
+          for (int il = 0; il < g; ++il) {
+            lj[il] = lastj[a * g + il];
+            lv[il] = lastv[a * g + il];
+          }
           const size_t base = (size_t)c * N;
           outT[base + a * g + op] = (uint16_t)t;
           inT[base + d * g + mi] = (uint16_t)t;
           ocls[base + a * g + op] = (uint8_t)cl;
-          // the instance id is only written out with the winner; its global
-          // load overlaps the residual loads below
-          iid[base + t] = (uint8_t)(cat[L.off_fam_info + lf * QG + idx] >> 12);
           ipos[base + a * g + op] = (int8_t)(d == a ? mi : -1);
           const int64_t cap = cl == 0 ? cap_c0 : cl == 1 ? cap_c1 : cl == 2 ? cap_c2 : cap_c3;
           int32_t* h = hp + (base + t) * kRow;
@@ -850,28 +867,30 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
 #pragma unroll
             for (int jl = 0; jl < g; ++jl) {
               const int i = a * g + il, j = d * g + jl;
-              int32_t v = kForbiddenU;
-              uint32_t rv = kForbidden;
-              if (i != j) {
-                const int64_t dv = lastj[i] == j ? lastv[i] : gDrem[(size_t)i * N + j];
-                // min(D^rem, cap) < 2^31 bytes, a multiple of the unit: exact quotient
-                const uint32_t vb = (uint32_t)(dv < cap ? dv : cap);
-                v = (int32_t)((vb >> P.unit_shift) * (uint32_t)P.odd_inv);
-                rv = (uint32_t)(dv < (int64_t)kRawSaturated ? dv : (int64_t)kRawSaturated);
-                const uint64_t key = ((uint64_t)(uint32_t)v << 24) | (uint64_t)(0xFFFFFF - (t * g2 + il * g + jl));
-                if (v > 0 && key > kt) kt = key;
+              const int64_t dv = lj[il] == j ? lv[il] : gv[il][jl];
+              // min(D^rem, cap) < 2^31 bytes, a multiple of the unit: exact quotient
+              const uint32_t vb = (uint32_t)(dv < cap ? dv : cap);
+              int32_t v = (int32_t)((vb >> P.unit_shift) * (uint32_t)P.odd_inv);
+              uint32_t rv = (uint32_t)(dv < (int64_t)kRawSaturated ? dv : (int64_t)kRawSaturated);
+              const uint64_t key = ((uint64_t)(uint32_t)v << 24) | (uint64_t)(0xFFFFFF - (t * g2 + il * g + jl));
+              if (i == j) {
+                v = kForbiddenU;
+                rv = kForbidden;
+              } else if (v > 0 && key > kt) {
+                kt = key;
               }
               h[il * g + jl] = v;
               rw[il * g + jl] = rv;
             }
+          iid[base + t] = (uint8_t)(idv >> 12);
           if (N % 64 == 0) {   // one family per wavefront
             kt = wave_max_u(kt);
             if (lane == 0 && kt) atomicMax((unsigned long long*)&topkey[c], (unsigned long long)kt);
           } else if (kt) {
             atomicMax((unsigned long long*)&topkey[c], (unsigned long long)kt);
           }
-          c += dc;
-          t += dt;
+          c += g_dc;
+          t += g_dt;
           if (t >= N) {
             t -= N;
             ++c;
