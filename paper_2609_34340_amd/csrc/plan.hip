@@ -75,7 +75,7 @@ struct PlanArgs {
   int32_t* status;
   int32_t batch;                    // matrices, one workgroup each; every buffer above holds `batch` of them
   // LDS layout (byte offsets)
-  int32_t o_sh, o_rinfo, o_agg, o_terms, o_nterms, o_pfb, o_finfo;
+  int32_t o_sh, o_rinfo, o_agg, o_terms, o_pfb, o_finfo;
   int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_iid, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bid, o_bx, o_brw,
       o_top;
   int32_t o_rset, o_psid, o_rbest, o_pbase, o_lastj, o_lastv, o_rp, o_sacc;
@@ -478,6 +478,27 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
 
 __device__ inline void set_err(Shared* sh, int code) { atomicCAS(&sh->err, 0, code); }
 
+// The first start with the highest binding score F among a family's ns runs
+// (F >= 0; enter with F0 = -1).  Four scores are read per round; indices past
+// the last read the last again, which never wins a strict comparison.
+__device__ inline void best_start(const PairRes* r, int ns, int& s0, int64_t& F0) {
+  for (int b = 0; b < ns; b += 4) {
+    int64_t f[4];
+    int q[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      q[u] = b + u < ns ? b + u : ns - 1;
+      f[u] = r[q[u]].F;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (f[u] > F0) {
+        F0 = f[u];
+        s0 = q[u];
+      }
+  }
+}
+
 // Workgroup barrier that orders LDS only: outstanding global stores of the
 // waves are not waited for.
 __device__ inline void lds_barrier() {
@@ -517,7 +538,6 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   // banks) and at least nn + 3 (zero padding for the 4-wide shift unroll)
   const int kS = (nn + 3) | 1;
   uint16_t* terms = (uint16_t*)(smem + P.o_terms);
-  uint16_t* nterms = (uint16_t*)(smem + P.o_nterms);  // low byte: diagonal terms, high byte: shift terms
   int32_t* pfb = (int32_t*)(smem + P.o_pfb);           // [NP][2] local family range
   uint16_t* finfo = (uint16_t*)(smem + P.o_finfo);
   PairRes* pr = (PairRes*)(smem + P.o_pair);
@@ -563,17 +583,17 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     rinfo[r] = ((grp / Q) << 8) | ((grp % Q) << 4) | (r - grp * g);
   }
   // a diagonal-block term is kept as its count | (q * Q + q2) << 4, the
-  // index of its slot pair's A row (the scoring loop reads nothing else)
-  for (int x = tid; x < NP * L.TS + 4; x += kPlanThreads) {
-    const int tv = x < NP * L.TS ? cat[L.off_terms + x] : 0;
-    terms[x] = (uint16_t)((tv & 15) | ((((tv >> 8) & 15) * Q + ((tv >> 4) & 15)) << 4));
+  // index of its slot pair's A row (the scoring loop reads nothing else); a
+  // shift-block term's count is zeroed and each pattern's slots are padded
+  // with zeros to a multiple of 8, so no slot needs a bound check
+  const int TS8 = (L.TS + 7) & ~7;
+  for (int x = tid; x < NP * TS8; x += kPlanThreads) {
+    const int p = x / TS8, m = x - p * TS8;
+    const int tv = m < L.TS ? cat[L.off_terms + p * L.TS + m] : 0;
+    const int cnt = (tv >> 12) == 0 ? (tv & 15) : 0;
+    terms[x] = (uint16_t)(cnt | ((((tv >> 8) & 15) * Q + ((tv >> 4) & 15)) << 4));
   }
   for (int p = tid; p < NP; p += kPlanThreads) {
-    // terms are stored diagonal-block first, then shift-block
-    const int n = cat[L.off_nterms + p];
-    int nl = 0;
-    for (int m = 0; m < n; ++m) nl += (cat[L.off_terms + p * L.TS + m] >> 12) == 0;
-    nterms[p] = (uint16_t)(nl | ((n - nl) << 8));
     pfb[2 * p] = cat[L.off_fb + p];
     pfb[2 * p + 1] = cat[L.off_fe + p];
   }
@@ -752,21 +772,20 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
           if (ch == 0) rbest[si] = bkey;
         } else {
           const int p = x - na;
-          const uint16_t* tp = terms + p * L.TS;
-          const int nl = nterms[p] & 255;
-          // term slots four at a time up to the longest diagonal part, every
-          // load of a group issued together; slots past this pattern's own
-          // count weigh zero (the term array is padded)
+          const uint16_t* tp = terms + p * TS8;
+          // term slots eight at a time up to the longest diagonal part, the
+          // slot loads of a group issued together and then their A loads;
+          // shift-block and padding slots weigh zero
           int32_t sb = 0;
-          for (int m0 = 0; m0 < P.MLT; m0 += 4) {
-            int tv[4];
+          for (int m0 = 0; m0 < P.MLT; m0 += 8) {
+            int tv[8];
 #pragma unroll
-            for (int m = 0; m < 4; ++m) tv[m] = tp[m0 + m];
-            int32_t av[4];
+            for (int m = 0; m < 8; ++m) tv[m] = tp[m0 + m];
+            int32_t av[8];
 #pragma unroll
-            for (int m = 0; m < 4; ++m) av[m] = agg[__umul24((unsigned)(tv[m] >> 4), (unsigned)kS)];
+            for (int m = 0; m < 8; ++m) av[m] = agg[__umul24((unsigned)(tv[m] >> 4), (unsigned)kS)];
 #pragma unroll
-            for (int m = 0; m < 4; ++m) sb += (m0 + m < nl ? (tv[m] & 15) : 0) * av[m];
+            for (int m = 0; m < 8; ++m) sb += (tv[m] & 15) * av[m];
           }
           pbase[p] = sb;
         }
@@ -958,14 +977,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         // a one-family shape: its best start wins, no utility to compare
         // (every lane reads the same scores)
         int s0 = 0;
-        int64_t F0 = pr[0].F;
-        for (int s = 1; s < NS; ++s) {
-          const int64_t Fs = pr[s].F;
-          if (Fs > F0) {
-            F0 = Fs;
-            s0 = s;
-          }
-        }
+        int64_t F0 = -1;
+        best_start(pr, NS, s0, F0);
         best_valid = true;
         best_S = F0 * P.unit;
         best_f = cb;
@@ -977,14 +990,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         int c = -1, bs = 0;
         for (int cc = lane; cc < nc; cc += 64) {
           int s0 = 0;
-          int64_t F0 = pr[cc * NS].F;
-          for (int s = 1; s < NS; ++s) {
-            const int64_t Fs = pr[cc * NS + s].F;
-            if (Fs > F0) {
-              F0 = Fs;
-              s0 = s;
-            }
-          }
+          int64_t F0 = -1;
+          best_start(pr + cc * NS, NS, s0, F0);
           const PairRes& r = pr[cc * NS + s0];
           int64_t xm2 = 0, bm2 = 1;
           for (int cl = 0; cl < 2; ++cl) {
@@ -1276,8 +1283,7 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   take(&P.o_sh, sizeof(Shared));
   take(&P.o_rinfo, (size_t)N * 4);
   take(&P.o_agg, (size_t)((L.nn + 3) | 1) * (L.Q * L.Q + 1) * 4);
-  take(&P.o_terms, ((size_t)NP * L.TS + 4) * 2);
-  take(&P.o_nterms, (size_t)NP * 2);
+  take(&P.o_terms, (size_t)NP * ((L.TS + 7) & ~7) * 2);
   take(&P.o_pfb, (size_t)NP * 8);
   take(&P.o_finfo, (size_t)FL * QG * 2);
   take(&P.o_bsl, (size_t)N);
