@@ -334,9 +334,10 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
 #pragma unroll
           for (int e = 0; e < g2; ++e) row[r][m][e] = kHold ? hs[r][m][e] : fc.H[o[r][m] * kRow + e];
         }
+      // computed for every lane (a lane past the last group reads instance
+      // 0's rows and changes nothing): no branch but the guarded writes
 #pragma unroll
       for (int r = 0; r < MG; ++r) {
-        if (!own[r]) continue;
         int32_t h[g][g];
 #pragma unroll
         for (int m = 0; m < g; ++m)
@@ -367,14 +368,14 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
             bp = p;
           }
         }
-        if (bestv > cur) {
+        const bool up = own[r] && bestv > cur;
 #pragma unroll
-          for (int m = 0; m < g; ++m) {
-            sig[r][m] = Perms<g>::at(bp, m);
-            SL[o[r][m]] = (uint8_t)sig[r][m];
-          }
-          changed = 1;
+        for (int m = 0; m < g; ++m) sig[r][m] = up ? Perms<g>::at(bp, m) : sig[r][m];
+        if (up) {
+#pragma unroll
+          for (int m = 0; m < g; ++m) SL[o[r][m]] = (uint8_t)sig[r][m];
         }
+        changed |= up;
       }
     }
     wave_sync();
@@ -393,7 +394,6 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
         }
 #pragma unroll
       for (int r = 0; r < MG; ++r) {
-        if (!own[r]) continue;
         int32_t h[g][g];
 #pragma unroll
         for (int m = 0; m < g; ++m)
@@ -424,14 +424,14 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
             bp = p;
           }
         }
-        if (bestv > cur) {
+        const bool up = own[r] && bestv > cur;
 #pragma unroll
-          for (int m = 0; m < g; ++m) {
-            del[r][m] = Perms<g>::at(bp, m);
-            DL[nn_[r][m]] = (uint8_t)del[r][m];
-          }
-          changed = 1;
+        for (int m = 0; m < g; ++m) del[r][m] = up ? Perms<g>::at(bp, m) : del[r][m];
+        if (up) {
+#pragma unroll
+          for (int m = 0; m < g; ++m) DL[nn_[r][m]] = (uint8_t)del[r][m];
         }
+        changed |= up;
       }
     }
     wave_sync();
@@ -450,20 +450,29 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
       jf[r][m] = DL[o[r][m]];
       cf[r][m] = own[r] ? fc.ocls[(lane + 64 * r) * g + m] : 0;
 #pragma unroll
-      for (int jl = 0; jl < g; ++jl) rf[r][m][jl] = fc.H[o[r][m] * kRow + sig[r][m] * g + jl];
+      for (int jl = 0; jl < g; ++jl) {
+        if constexpr (kHold) {   // the row is in registers: select the source's part
+          int32_t v = hs[r][m][jl];
+#pragma unroll
+          for (int i2 = 1; i2 < g; ++i2) v = sig[r][m] == i2 ? hs[r][m][i2 * g + jl] : v;
+          rf[r][m][jl] = v;
+        } else {
+          rf[r][m][jl] = fc.H[o[r][m] * kRow + sig[r][m] * g + jl];
+        }
+      }
     }
 #pragma unroll
   for (int r = 0; r < MG; ++r) {
-    if (!own[r]) continue;
 #pragma unroll
     for (int m = 0; m < g; ++m) {
       int32_t x = rf[r][m][0];
 #pragma unroll
       for (int jj = 1; jj < g; ++jj) x = jf[r][m] == jj ? rf[r][m][jj] : x;
-      x = x > 0 ? x : 0;   // a self pair serves nothing
+      x = own[r] && x > 0 ? x : 0;   // a self pair serves nothing
       F += x;
-      if (cf[r][m] == VP_PATH_NIC) xn = x > xn ? x : xn;
-      else xp = x > xp ? x : xp;
+      const bool nic = cf[r][m] == VP_PATH_NIC;
+      xn = nic && x > xn ? x : xn;
+      xp = !nic && x > xp ? x : xp;
     }
   }
   F = wave_sum(F);
