@@ -191,7 +191,7 @@ struct FamCtx {
 // start, every group's source and destination permutation.
 template <int g, int MG>
 __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8_t* DL, int start,
-                         const uint8_t* rperm, int lane, uint64_t top, PairRes* out) {
+                         const uint8_t* rperm, int lane, uint64_t top, bool need_x, PairRes* out) {
   constexpr int g2 = g * g, kRow = g2 | 1;   // credit rows padded to an odd word count
   const int G = P.L.G;
   int o[MG][g], nn_[MG][g], ip[MG][g], sig[MG][g], del[MG][g];
@@ -476,8 +476,10 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
     }
   }
   F = wave_sum(F);
-  xp = wave_max32(xp);
-  xn = wave_max32(xn);
+  if (need_x) {   // the lane maxima only serve comparisons between families
+    xp = wave_max32(xp);
+    xn = wave_max32(xn);
+  }
   if (lane == 0) {
     out->F = F;
     out->xmax[0] = xp;
@@ -973,7 +975,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         FamCtx fc{outT + (size_t)c * N, inT + (size_t)c * N, ipos + (size_t)c * N, ocls + (size_t)c * N,
                   hp + (size_t)c * N * kRow, cb + c};
         run_pair<g, MG>(P, fc, sl + (size_t)pi * N, dl + (size_t)pi * N, s, rp + (size_t)pi * L.G * 2, lane,
-                        topkey[c], &pr[pi]);
+                        topkey[c], fe - fb > 1, &pr[pi]);
       }
       // full barrier: the previous iteration's D^rem stores are complete
       // before the next gather reads D^rem
