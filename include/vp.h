@@ -268,7 +268,9 @@ size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
  * exactly and appends the best activation.  Device errors:
  * VP_ERR_INVALID_DEMAND, VP_ERR_NO_PROGRESS, VP_ERR_CAPACITY, and
  * VP_ERR_UNSUPPORTED when a capacity tau*bw reaches 2^31 bytes or 2^27 units, or the total
- * demand reaches 2^42 bytes.  The catalog must have been uploaded. */
+ * demand reaches 2^42 bytes.  The catalog must have been uploaded.  Host
+ * errors: VP_ERR_UNSUPPORTED when k_max * N * 8 reaches 2^32 (one matrix's
+ * schedule arrays are addressed with 32-bit byte offsets). */
 vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_params* p,
                   int32_t* K, int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes,
                   int64_t* send_off, int64_t* stream_off, int32_t* recv_src, int64_t* tau,

@@ -489,6 +489,14 @@ __device__ void run_pair(const PlanArgs& P, const FamCtx& fc, uint8_t* SL, uint8
 
 __device__ inline void set_err(Shared* sh, int code) { atomicCAS(&sh->err, 0, code); }
 
+// Element idx of a global array whose byte offsets stay below 2^32 (checked
+// on the host): a 32-bit offset from a wavefront-uniform base, which the
+// compiler addresses as scalar base + vector offset.
+template <typename T>
+__device__ inline T& at32(T* base, uint32_t idx) {
+  return *(T*)((char*)base + (uint32_t)(idx * (uint32_t)sizeof(T)));
+}
+
 // The first start with the highest binding score F among a family's ns runs
 // (F >= 0; enter with F0 = -1).  Four scores are read per round; indices past
 // the last read the last again, which never wins a strict comparison.
@@ -874,7 +882,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
 #pragma unroll
           for (int il = 0; il < g; ++il)
 #pragma unroll
-            for (int jl = 0; jl < g; ++jl) gv[il][jl] = gDrem[(size_t)(a * g + il) * N + d * g + jl];
+            for (int jl = 0; jl < g; ++jl) gv[il][jl] = at32(gDrem, (uint32_t)((a * g + il) * N + d * g + jl));
           const int idv = cat[L.off_fam_info + lf * QG + idx];
           int lj[g];
           int64_t lv[g];
@@ -1106,24 +1114,24 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         // the unit is below 2^31 (a cap of at least one unit fits 31 bits)
         const int64_t x = (int64_t)((uint64_t)(uint32_t)xu * (uint32_t)P.unit);
         const uint32_t rv = live ? RW[t * kRow + s_ * g + d_] : brw[t];
-        const size_t o = (size_t)K * N + i;
-        gdst[o] = j;
-        ginst[o] = live ? iid[(size_t)best_c * N + t] : bid[t];
-        gbytes[o] = x;
-        if (grecv_src) grecv_src[(size_t)K * N + j] = i;   // pi_k is a permutation
+        const uint32_t o = (uint32_t)(K * N + i);
+        at32(gdst, o) = j;
+        at32(ginst, o) = live ? iid[(size_t)best_c * N + t] : bid[t];
+        at32(gbytes, o) = x;
+        if (grecv_src) at32(grecv_src, (uint32_t)(K * N + j)) = i;   // pi_k is a permutation
         if (gsend_off) {
           // Sec. 5 buffer layout: where this lane's slice sits in rank i's
           // send buffer and in its stream to j (bytes sent there before:
           // D[i][j] minus the residual before this step; D[i][j] is added by
           // stream_off_kernel after the plan, which keeps its load off this
           // loop's critical path)
-          const int64_t before = rv < kRawSaturated ? (int64_t)rv : gDrem[(size_t)i * N + j];
-          gsend_off[o] = sacc[i];
-          gstream_off[o] = -before;
+          const int64_t before = rv < kRawSaturated ? (int64_t)rv : at32(gDrem, (uint32_t)(i * N + j));
+          at32(gsend_off, o) = sacc[i];
+          at32(gstream_off, o) = -before;
           sacc[i] += x;
         }
         if (xu > 0) {
-          int64_t* dp = gDrem + (size_t)i * N + j;
+          int64_t* dp = &at32(gDrem, (uint32_t)(i * N + j));
           int64_t nv;
           if (__builtin_expect(rv < kRawSaturated, 1)) nv = (int64_t)rv - x;
           else nv = *dp - x;   // the residual did not fit the 32-bit copy
@@ -1220,6 +1228,9 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   if (QG > kMaxQG || L.Q > 8 || g > 4) return set_error(VP_ERR_UNSUPPORTED, "too many lanes per node");
   if (N > 65535 || L.G > 64 * 8) return set_error(VP_ERR_UNSUPPORTED, "too many ranks for the planner");
   if (L.n_inst > 256) return set_error(VP_ERR_UNSUPPORTED, "too many node-local instances");
+  // the kernel addresses one matrix's schedule and residual with 32-bit byte offsets
+  if ((uint64_t)a.p.k_max * (uint64_t)N * 8 >= (uint64_t(1) << 32))
+    return set_error(VP_ERR_UNSUPPORTED, "k_max * N too large for the planner");
   int hmax = 1, mlt = 0, mrt = 0;
   for (int p = 0; p < NP; ++p) {
     hmax = std::max(hmax, c.pat_fe[p] - c.pat_fb[p]);
