@@ -265,6 +265,22 @@ def test_plan_device_errors(vp):
     assert_schedule_equal(g, o)
 
 
+def test_plan_rejects_schedule_too_large_for_32_bit_offsets(vp):
+    """k_max * N * 8 >= 2^32 is refused on the host before anything is
+    enqueued (the planner addresses a matrix's schedule with 32-bit byte
+    offsets); the buffers passed are small and never touched."""
+    topo = vpgen.config(1).topo
+    log("plan k_max limit")
+    cat = gcat(vp, topo)
+    p = vp.plan_params(cat.N, 4096, k_max=(1 << 29) // cat.N)
+    out = vp.alloc_schedule(cat.N, 1, layout=True)
+    D = torch.zeros((cat.N, cat.N), dtype=torch.int64, device="cuda")
+    with pytest.raises(vp.VPError) as e:
+        vp.plan(cat, D, p, out=out)
+    assert e.value.status == vp.UNSUPPORTED and "k_max" in str(e.value)
+    torch.cuda.synchronize()
+
+
 def test_plan_deterministic(vp):
     w, _, _, D = moe_case(2)
     log("plan determinism")
