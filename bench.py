@@ -182,6 +182,7 @@ def measure(w, steps, warmup, M, dev):
     r["pack_bytes"] = S_b + U_b + 4 * rows + 16 * sl
     r["pack_ms"] = r["prep_ms"] + r["gather_ms"]
     r["gather_bytes"] = S_b + U_b
+    r["send_bytes"] = S_b
     r["K"] = np.array([Ks[m] for m in step_m], dtype=np.float64)
     r["That_ms"] = np.array([That[m] for m in step_m])
     r["M"] = M
@@ -393,7 +394,12 @@ def summary(w, r):
             "control_words_us": round(float(r["words_ms"].mean() * 1e3), 1) if w.mode == "moe" else None,
             "pack_us": round(float(r["pack_ms"].mean() * 1e3), 1),
             "pack_GBps": round(value, 2), "pack_pct_of_peak": round(100 * value / PEAK_HBM_GBS, 2),
-            "pack_bytes_MB": round(float(r["pack_bytes"].mean()) / 1e6, 2)}
+            "pack_bytes_MB": round(float(r["pack_bytes"].mean()) / 1e6, 2),
+            # median over the timed steps, and the logical rate 2S/t (every send
+            # byte read and written once; cache-served duplicate rows can make
+            # it exceed what HBM carried)
+            "pack_us_median": round(float(np.median(r["pack_ms"]) * 1e3), 1),
+            "pack_logical_2S_GBps": round(float(2 * r["send_bytes"].sum() / (r["pack_ms"].sum() * 1e-3) / 1e9), 2)}
 
 
 def main():
@@ -472,6 +478,8 @@ def main():
         "demand_us": head["demand_us"],
         "control_words_us": head["control_words_us"],
         "pack_us": head["pack_us"],
+        "pack_us_median": head["pack_us_median"],
+        "pack_logical_2S_GBps": head["pack_logical_2S_GBps"],
         "activations_K": head["activations_K"],
         "modeled_T_ms": head["modeled_T_ms"],
         "plan_over_modeled_T": head["plan_over_modeled_T"],
