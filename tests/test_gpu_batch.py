@@ -89,6 +89,11 @@ def test_dispatch_and_combine_in_one_launch(vp, cid):
     K = int(one["K"].item())
     for key in ("dst", "bytes", "send_off", "stream_off", "recv_src"):
         assert torch.equal(s[key][1, :K], one[key][:K]), key
+    zero = vp.plan(cat, D[0].contiguous(), p, out=vp.alloc_schedule(w.n_ranks, p.k_max, layout=True))
+    torch.cuda.synchronize()
+    K0 = int(zero["K"].item())
+    for key in ("dst", "bytes", "send_off", "stream_off", "recv_src"):
+        assert torch.equal(s[key][0, :K0], zero[key][:K0]), key
 
 
 def test_bad_matrix_fails_alone(vp):
