@@ -75,11 +75,33 @@ struct PlanArgs {
   int32_t* status;
   int32_t batch;                    // matrices, one workgroup each; every buffer above holds `batch` of them
   // LDS layout (byte offsets)
-  int32_t o_sh, o_rinfo, o_agg, o_terms, o_pfb, o_finfo;
-  int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_iid, o_hp, o_raw, o_sl, o_dl, o_bsl, o_bdl, o_bid, o_bx, o_brw,
-      o_top;
-  int32_t o_rset, o_psid, o_rbest, o_pbase, o_lastj, o_lastv, o_rp, o_sacc;
+  int32_t o_agg, o_terms, o_pfb, o_finfo;
+  int32_t o_pair, o_outT, o_inT, o_ipos, o_ocls, o_iid, o_hp, o_raw, o_sl, o_dl, o_top;
+  int32_t o_rset, o_psid, o_rbest, o_pbase, o_rp;
 };
+
+// Per-rank arrays of plan_kernel<g, MG> sit at compile-time offsets from the
+// start of the dynamic LDS, sized for the most ranks the instantiation
+// takes (64 MG groups of g): they are addressed with immediate offsets and
+// hold no scalar register.  Everything else follows at host-computed offsets.
+struct FixedLds {
+  size_t rinfo, lastj, lastv, sacc, bx, brw, bsl, bdl, bid, end;
+};
+__host__ __device__ constexpr size_t a16(size_t x) { return (x + 15) / 16 * 16; }
+__host__ __device__ constexpr FixedLds fixed_lds(size_t n) {
+  FixedLds f{};
+  f.rinfo = a16(sizeof(Shared));
+  f.lastj = f.rinfo + 4 * n;
+  f.lastv = a16(f.lastj + 4 * n);
+  f.sacc = f.lastv + 8 * n;
+  f.bx = f.sacc + 8 * n;
+  f.brw = f.bx + 4 * n;
+  f.bsl = f.brw + 4 * n;
+  f.bdl = f.bsl + n;
+  f.bid = f.bdl + n;
+  f.end = a16(f.bid + n);
+  return f;
+}
 
 // ------------------------------------------------------------------ helpers
 
@@ -549,8 +571,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   int64_t* gsend_off = P.send_off ? P.send_off + b * KN : nullptr;
   int64_t* gstream_off = P.stream_off ? P.stream_off + b * KN : nullptr;
   int32_t* grecv_src = P.recv_src ? P.recv_src + b * KN : nullptr;
-  Shared* sh = (Shared*)(smem + P.o_sh);
-  int32_t* rinfo = (int32_t*)(smem + P.o_rinfo);
+  constexpr FixedLds FX = fixed_lds((size_t)64 * MG * g);
+  Shared* sh = (Shared*)smem;
+  int32_t* rinfo = (int32_t*)(smem + FX.rinfo);
   int32_t* agg = (int32_t*)(smem + P.o_agg);         // [q][q2][k] units: k = 0 is A, k > 0 is B_k;
                                                      // then one row of zeros
   // row stride: odd (lanes reading one shift of different rows hit distinct
@@ -569,11 +592,11 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   uint32_t* raw = (uint32_t*)(smem + P.o_raw);       // residual of every credit entry (saturating)
   uint8_t* sl = smem + P.o_sl;
   uint8_t* dl = smem + P.o_dl;
-  uint8_t* bsl = smem + P.o_bsl;
-  uint8_t* bdl = smem + P.o_bdl;
-  uint8_t* bid = smem + P.o_bid;
-  uint32_t* bx = (uint32_t*)(smem + P.o_bx);
-  uint32_t* brw = (uint32_t*)(smem + P.o_brw);
+  uint8_t* bsl = smem + FX.bsl;
+  uint8_t* bdl = smem + FX.bdl;
+  uint8_t* bid = smem + FX.bid;
+  uint32_t* bx = (uint32_t*)(smem + FX.bx);
+  uint32_t* brw = (uint32_t*)(smem + FX.brw);
   uint64_t* topkey = (uint64_t*)(smem + P.o_top);    // [FC] best credit triple of each family in the chunk
   uint16_t* rset = (uint16_t*)(smem + P.o_rset);     // [nS][kMaxRTerms] agg row offsets (zero row past the end)
   uint16_t* psid = (uint16_t*)(smem + P.o_psid);     // [J1] NIC-lane set of each NIC-carrying pattern
@@ -583,9 +606,9 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   // next credit gather takes it from here, so no barrier has to wait for the
   // global store (stores of earlier iterations are complete by then).
   uint8_t* rp = smem + P.o_rp;   // [FC][NS][G][2] packed permutations of the shuffled starts
-  int32_t* lastj = (int32_t*)(smem + P.o_lastj);
-  int64_t* sacc = (int64_t*)(smem + P.o_sacc);   // [N] bytes each rank has sent so far
-  int64_t* lastv = (int64_t*)(smem + P.o_lastv);
+  int32_t* lastj = (int32_t*)(smem + FX.lastj);
+  int64_t* sacc = (int64_t*)(smem + FX.sacc);   // [N] bytes each rank has sent so far
+  int64_t* lastv = (int64_t*)(smem + FX.lastv);
   const int32_t* cat = P.cat;
 
   // ---------------------------------------------------------------- prologue
@@ -1297,29 +1320,22 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   P.status = a.status;
   P.batch = a.batch;
 
-  size_t o = 0;
+  // the per-rank arrays at the instantiation's fixed offsets first
+  const int gpl = (L.G + 63) / 64;
+  const int MG = gpl <= 1 ? 1 : gpl <= 2 ? 2 : gpl <= 4 ? 4 : 8;
+  size_t o = fixed_lds((size_t)64 * MG * g).end;
   auto take = [&](int32_t* field, size_t bytes) {
     *field = (int32_t)o;
     o = align_up(o + bytes, 16);
   };
-  take(&P.o_sh, sizeof(Shared));
-  take(&P.o_rinfo, (size_t)N * 4);
   take(&P.o_agg, (size_t)((L.nn + 3) | 1) * (L.Q * L.Q + 1) * 4);
   take(&P.o_terms, (size_t)NP * ((L.TS + 7) & ~7) * 2);
   take(&P.o_pfb, (size_t)NP * 8);
   take(&P.o_finfo, (size_t)FL * QG * 2);
-  take(&P.o_bsl, (size_t)N);
-  take(&P.o_bdl, (size_t)N);
-  take(&P.o_bid, (size_t)N);
-  take(&P.o_bx, (size_t)N * 4);
-  take(&P.o_brw, (size_t)N * 4);
   take(&P.o_rset, (size_t)L.nS * kMaxRTerms * 2);
   take(&P.o_psid, (size_t)L.J1 * 2);
   take(&P.o_rbest, (size_t)L.nS * 8);
   take(&P.o_pbase, (size_t)NP * 4);
-  take(&P.o_lastj, (size_t)N * 4);
-  take(&P.o_lastv, (size_t)N * 8);
-  take(&P.o_sacc, (size_t)N * 8);
   const size_t fixed = o;
   const size_t per_fam = align_up((size_t)NS * sizeof(PairRes), 16) + 2 * align_up((size_t)N * 2, 16) +
                          3 * align_up((size_t)N, 16) + 2 * (size_t)N * (g2 | 1) * 4 + 2 * align_up((size_t)NS * N, 16) + 16 +
@@ -1349,7 +1365,6 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
   if (o > budget) return set_error(VP_ERR_UNSUPPORTED, "plan state does not fit in LDS");
 
   hipStream_t st = (hipStream_t)stream;
-  const int gpl = (L.G + 63) / 64;
   switch (g) {
     case 2: return launch_g<2>(P, o, st, gpl);
     case 3: return launch_g<3>(P, o, st, gpl);
