@@ -8,21 +8,25 @@
 //      the blocks (n, n+k).  A shape (k, L, R) scores sum A.L + sum B_k.R,
 //      which equals sum D-hat.M.  The aggregates are kept in units of the
 //      pack granule as int32 (every demand entry is a whole number of units,
-//      so scores keep their order).  One thread scores one node-local pattern
-//      over a range of node shifts: base(p) from A plus the best R(k, p) of
-//      its range; every thread's candidate carries its own shape index, so
-//      one argmax over the packed 64-bit keys (ties to the lowest index)
-//      selects the shape;
+//      so scores keep their order).  The B part depends on a pattern only
+//      through its set of NIC lanes: a few lanes per distinct set find the
+//      set's best shift while other threads compute every pattern's A part;
+//      one thread per pattern then adds the two and the block takes the
+//      argmax of packed 64-bit keys (ties to the lowest canonical shape);
 //   2. for the families of the best shape: the cluster-level out/in lists of
 //      every group and the binding credits h' = min(D^rem_ij, cap) (Eq. (7)
-//      scaled by tau) of every instance and endpoint pair, into LDS;
+//      scaled by tau) of every instance and endpoint pair, into LDS, with
+//      the shuffled starts' permutations drawn on the idle wavefronts;
 //   3. MultiStartAA (Eq. (8)): one wavefront per (family, start).  Each lane
 //      owns up to a few groups for both AA halves and keeps their source and
-//      destination assignments in registers, so a half-step is one LDS round
-//      trip (read the other side, read the credit rows, write back);
-//   4. Evaluate (Eq. (9)-(10)) and the exact utility argmax in 128-bit;
+//      destination assignments and credit rows in registers, so a half-step
+//      is one LDS round trip (read the other side, write back);
+//   4. Evaluate (Eq. (9)-(10)), the exact utility argmax in 128-bit, by each
+//      wavefront that writes the winner (a one-family shape needs only its
+//      best start);
 //   5. the activation is appended and D^rem (global memory, touched by this
-//      one workgroup only, so its CU's L1 keeps it coherent) is updated.
+//      one workgroup only) is updated; the per-rank stream offsets are
+//      completed by stream_off_kernel after the loop.
 // No host round trip happens between iterations.
 #include <hip/hip_runtime.h>
 
