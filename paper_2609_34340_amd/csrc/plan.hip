@@ -747,15 +747,11 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
                 cap_c3 = lane0(sh->cap[3]);
   // ---------------------------------------------------------------- loop
   while (true) {
-    if (sh->err || sh->total_rem == 0) break;
-    if (sh->K >= P.k_max) {
-      __syncthreads();
-      if (tid == 0) set_err(sh, VP_ERR_CAPACITY);
-      break;
-    }
-    // iteration-wide values read from LDS are made wavefront-uniform, so
-    // that what is derived from them runs on the scalar unit
-    const int K = lane0((int32_t)sh->K);
+    // The loop's exit conditions are read here and tested after the scoring
+    // work, which does not depend on them (on the last pass it is wasted),
+    // so the read's latency hides behind it.
+    const int err_ = sh->err, K_ = sh->K;
+    const int64_t rem_ = sh->total_rem;
 
     // Step 1: score every shape; argmax.  A shape (k, p) scores base(p), its
     // diagonal-block terms against A, plus, for k > 0, the sum of B_k over
@@ -837,6 +833,15 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         }
       }
     }
+    if (err_ || rem_ == 0) break;   // the same LDS words for every thread
+    if (K_ >= P.k_max) {
+      __syncthreads();
+      if (tid == 0) set_err(sh, VP_ERR_CAPACITY);
+      break;
+    }
+    // iteration-wide values read from LDS are made wavefront-uniform, so
+    // that what is derived from them runs on the scalar unit
+    const int K = lane0(K_);
     lds_barrier();
     {
       uint64_t best = 0;
