@@ -267,8 +267,11 @@ size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
  * of the best shape with MultiStartAA (Eq. (7)-(8)), evaluates Eq. (9)-(10)
  * exactly and appends the best activation.  Device errors:
  * VP_ERR_INVALID_DEMAND, VP_ERR_NO_PROGRESS, VP_ERR_CAPACITY, and
- * VP_ERR_UNSUPPORTED when a capacity tau*bw reaches 2^31 bytes or 2^27 units, or the total
- * demand reaches 2^42 bytes.  The catalog must have been uploaded.  Host
+ * VP_ERR_UNSUPPORTED when a demand entry reaches 2^42 bytes, a capacity
+ * tau*bw reaches 2^31 bytes or 2^27 units, or the total demand reaches 2^42
+ * bytes or 2^28 units (the planner keeps unit counts in 32 bits: 4 GiB of
+ * demand at a 16-byte unit, 64 GiB at a 256-byte unit).  An invalid entry
+ * takes precedence over these limits.  The catalog must have been uploaded.  Host
  * errors: VP_ERR_UNSUPPORTED when k_max * N * 8 reaches 2^32 (one matrix's
  * schedule arrays are addressed with 32-bit byte offsets). */
 vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_params* p,
@@ -298,10 +301,10 @@ vp_status vp_plan_batch(const vp_catalog* cat, int32_t batch, const int64_t* dem
  * vp_pack_heads (k = 0) with schedule capacity k_max, a send buffer of
  * send_capacity bytes and a pack unit of unit_bytes (row_bytes or
  * head_bytes).  Rows: per-step descriptors and one send-unit entry per
- * (token, routing slot).  Heads: per-step descriptors and one source offset
- * per packed unit.  The workspace must be zero-filled once before its first
- * use; no later call needs it cleared (rows: the entries carry the
- * generation of the call that wrote them).  Returns 0 for negative sizes. */
+ * (token, routing slot).  Heads: per-step descriptors only.  The workspace
+ * must be zero-filled once before its first use; no later call needs it
+ * cleared (rows: the entries carry the generation of the call that wrote
+ * them).  Returns 0 for negative sizes. */
 size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_bytes, int64_t T, int32_t k);
 
 /* Send-buffer layout (Sec. 5 "Device-resident buffer layout"): for the steps
@@ -316,7 +319,11 @@ size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_byte
  *   K, dst, bytes                      the schedule of vp_plan (device)
  *   send_off, stream_off               vp_plan's buffer layout (device), or
  *                                      both NULL: then a slice kernel derives
- *                                      the same offsets from the schedule
+ *                                      the same offsets from the schedule.
+ *                                      The layout must be this schedule's:
+ *                                      each step's send offset equal to the
+ *                                      previous step's plus its bytes (0 for
+ *                                      step 0), else VP_ERR_INVALID_ARGUMENT
  *   send       device [send_capacity]  output
  *   step_off   device int64 [k_max+1]  where step k's slice starts in send;
  *                                      entries past K are unspecified,
@@ -337,7 +344,11 @@ vp_status vp_pack_rows(const void* tokens, int64_t T, int32_t k, int64_t row_byt
 
 /* Ulysses variant: stream j is, token by token, the bytes of the heads rank j
  * owns, [head_lo[j], head_lo[j+1]) (device int64 [N+1]); units are single
- * heads of head_bytes (a multiple of 16); activations are [T, token_stride]. */
+ * heads of head_bytes (a multiple of 16); activations are [T, token_stride].
+ * Every head a destination owns must lie inside the token row, else
+ * VP_ERR_INVALID_ARGUMENT.  T * (token_stride / head_bytes)^2 must stay
+ * below 2^47 and token_stride / head_bytes at or below 2^15
+ * (VP_ERR_UNSUPPORTED). */
 vp_status vp_pack_heads(const void* act, int64_t T, int64_t token_stride, const int64_t* head_lo,
                         int64_t head_bytes, int32_t self_rank, int32_t n_ranks, const int32_t* K,
                         const int32_t* dst, const int64_t* bytes, const int64_t* send_off,
@@ -354,7 +365,9 @@ vp_status vp_pack_heads(const void* act, int64_t T, int64_t token_stride, const 
  * non-temporal stores; it must get the same unit_bytes, T, k (0 after
  * vp_pack_prepare_heads), k_max, send_capacity and workspace, and no other
  * prepare on that workspace may come between.  It writes nothing when
- * dev_status already holds an error. */
+ * dev_status already holds an error.  Heads: every unit's source address is
+ * derived from its step's checked descriptor and checked against the
+ * activations again before the load. */
 vp_status vp_pack_prepare_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes,
                                const int32_t* sorted_tok, const uint8_t* sorted_slot,
                                const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,

@@ -176,6 +176,51 @@ def schedule_valid(tm: TopoModel, D: np.ndarray, sched, cls_of_id) -> None:
     assert (X == D).all(), "activations do not reconstruct D"
 
 
+def schedule_valid_np(tm: TopoModel, D: np.ndarray, dst: np.ndarray, cls: np.ndarray, nbytes: np.ndarray,
+                      chunk: int = 256) -> None:
+    """The checks of schedule_valid, vectorised for large schedules: every
+    step is a derangement, every lane's path class is one its group pair
+    has (before dominance pruning, NIC inside a switch excluded), no two
+    lanes of a step share a modeled resource (Eq. (1); the endpoint links are
+    distinct in any permutation), volumes are non-negative and the steps sum
+    to D.  dst, cls, nbytes: [K, N] destination, path class, bytes."""
+    dst = np.asarray(dst, np.int64)
+    cls = np.asarray(cls, np.int64)
+    nb = np.asarray(nbytes, np.int64)
+    K, N = dst.shape
+    assert N == tm.N
+    rows = np.arange(N)
+    assert (np.sort(dst, axis=1) == rows[None, :]).all(), "not a permutation"
+    assert not (dst == rows[None, :]).any(), "a rank sends to itself"
+    assert (nb >= 0).all()
+    a = np.broadcast_to(rows // tm.g, (K, N))
+    d = dst // tm.g
+    same_group = a == d
+    same_node = a // tm.Q == d // tm.Q
+    sa, sd = (a % tm.Q) // tm.W, (d % tm.Q) // tm.W
+    same_socket = same_node & (sa == sd)
+    ok = np.where(same_group, cls == PIX,
+                  np.where(same_socket, (cls == PXB) | (cls == NIC),
+                           np.where(same_node & tm.sys, (cls == SYS) | (cls == NIC), cls == NIC)))
+    assert ok.all(), "lane class does not match its group pair"
+    G = tm.G
+    xid = (a // tm.Q * tm.S + sa) * tm.S + sd
+    res = np.full((K, N, 3), -1, np.int64)
+    pxb_like = (cls == PXB) | (cls == SYS)
+    res[..., 0] = np.where(pxb_like, a, np.where(cls == NIC, 2 * G + a, -1))
+    res[..., 1] = np.where(pxb_like, G + d, np.where(cls == NIC, 3 * G + d, -1))
+    res[..., 2] = np.where(cls == SYS, 4 * G + xid, -1)
+    # unused slots get distinct negative ids so that they never collide
+    filler = -1 - np.arange(N * 3, dtype=np.int64).reshape(N, 3)
+    res = np.where(res < 0, filler[None], res).reshape(K, N * 3)
+    for k0 in range(0, K, chunk):
+        r = np.sort(res[k0:k0 + chunk], axis=1)
+        assert not (r[:, 1:] == r[:, :-1]).any(), "activation violates Eq. (1)"
+    X = np.zeros((N, N), np.int64)
+    np.add.at(X, (np.broadcast_to(rows, (K, N)), dst), nb)
+    assert (X == np.asarray(D, np.int64)).all(), "activations do not reconstruct D"
+
+
 def modeled_time(tm: TopoModel, sched, cls_of_id, lam: int) -> Fraction:
     """Eq. (2) with exact rationals."""
     total = Fraction(0)

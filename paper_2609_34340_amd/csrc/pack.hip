@@ -13,17 +13,20 @@
 //            waves -- then a scan of the volumes in (destination, step)
 //            order).
 //   index    one workgroup per step (split over a few when steps are long).
-//            Rows: every packed unit is one copy of
-//            a token row; its send unit goes to the entry of that (token,
-//            routing slot), tagged with the call's generation, so the list is
-//            never cleared.  Heads: the source byte offset of every packed
-//            unit.
+//            With the planner's layout every step checks that its slice
+//            starts where the previous step's ended, so the slices tile the
+//            send buffer.  Rows: every packed unit is one copy of a token
+//            row; its send unit goes to the entry of that (token, routing
+//            slot), tagged with the call's generation, so the list is never
+//            cleared.  Heads: one checked descriptor per step.
 //   scatter  rows: one workgroup per (token, copy), XCD-aware so that all
 //            copies of a token run on one XCD: a source row leaves HBM once
 //            however many destinations it has, and the XCDs write
 //            neighbouring tokens at any moment; launch shape by row size.
-//   gather   heads: grid-stride 16-byte copy of the units (each is read
-//            once) with non-temporal stores.
+//   gather   heads: workgroups per (step, part); every 16-byte vector's
+//            source address follows from the step's stream position (token
+//            and head by multiply-high division), so no per-unit table is
+//            written or read; non-temporal stores.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -247,14 +250,14 @@ struct IndexArgs {
   const int32_t* sorted_tok;
   const uint8_t* sorted_slot;
   const StepDesc* desc;        // descriptors from the slice kernel, or
-  const int32_t* n_desc;
+  int32_t* n_desc;
   const int32_t *Kp, *dst;     // the schedule and the planner's buffer layout
   const int64_t *bytes, *send_off, *stream_off;
   const int64_t* bounds;       // rows: dest_off; heads: head_lo
   int64_t* step_off;
-  uint32_t* hdr;               // [0]: generation, read by the scatter
+  uint32_t* hdr;               // [0]: generation, read by the scatter; bytes 8..15: token stride
   unsigned long long* lst;     // rows: [T][k] generation << 32 | send unit of each routing slot
-  int64_t* src_off;            // heads: source byte offset per send unit
+  StepDesc* hdesc;             // heads with the planner's layout: one descriptor per step
   int32_t* status;
 };
 
@@ -262,80 +265,100 @@ constexpr int kIndexThreads = 256;
 
 // One workgroup per step.  With the planner's buffer layout the workgroup
 // derives its step's descriptor itself (step offsets, checks); otherwise it
-// takes the slice kernel's.  Rows: every packed unit is one (token, routing
-// slot) assignment; its send unit goes to that slot's entry, tagged with the
-// call's generation (strictly increasing), so the entries of slots this call
-// does not pack (local experts, streams not covered) are recognisably old and
-// the list is never cleared.  Heads: the source byte offset of every packed
-// unit.
+// takes the slice kernel's.  The layout must tile the send buffer: step k's
+// slice starts where step k-1's ended (step 0's at 0), which each workgroup
+// checks against its predecessor, so by induction the send offsets are the
+// running sum of this rank's lane volumes.  Rows: every packed unit is one
+// (token, routing slot) assignment; its send unit goes to that slot's entry,
+// tagged with the call's generation (strictly increasing), so the entries of
+// slots this call does not pack (local experts, streams not covered) are
+// recognisably old and the list is never cleared.  Heads: the step's checked
+// descriptor (no units when the lane is idle); the gather reads only
+// descriptors of this call, and none when a step failed its checks.
 __global__ void __launch_bounds__(kIndexThreads) index_kernel(IndexArgs a) {
   // workgroup (i, y) handles part y of step i's units (gridDim.y parts)
   const int i = blockIdx.x, tid = threadIdx.x, y = blockIdx.y, ny = gridDim.y;
   const bool lead = y == 0 && tid == 0;   // the one thread that writes a step's offsets
-  if (i == 0 && lead) *a.hdr = a.gen;
+  if (i == 0 && lead) {
+    *a.hdr = a.gen;
+    *(int64_t*)(a.hdr + 2) = a.token_stride;
+  }
   StepDesc d;
   if (a.send_off) {
     const int K = *a.Kp, st = *a.status;
     if (K < 0 || K > a.k_max) {
-      if (i == 0 && lead) report(a.status, VP_ERR_INVALID_ARGUMENT);
+      if (i == 0 && lead) {
+        report(a.status, VP_ERR_INVALID_ARGUMENT);
+        if (a.mode == 1) *a.n_desc = 0;
+      }
       return;
     }
-    if (st != 0) return;
-    if (i == 0 && K == 0 && lead) a.step_off[0] = 0;
-    if (i >= K) return;
+    if (i == 0 && lead) {
+      if (a.mode == 1) *a.n_desc = K;
+      if (K == 0) a.step_off[0] = 0;
+    }
+    if (st != 0 || i >= K) return;
     const size_t o = (size_t)i * a.N + a.self;
     const int64_t x = a.bytes[o], so = a.send_off[o], co = a.stream_off[o];
     const int j = a.dst[o];
+    const int64_t prev_end = i == 0 ? 0 : a.send_off[o - a.N] + a.bytes[o - a.N];
+    d.first = 0;
+    d.u0 = 0;
+    d.nu = 0;
+    d.h0 = 0;
+    d.h = 1;
+    bool ok = so == prev_end;
     if (lead) {
       a.step_off[i] = so;
-      if (i == K - 1) {
-        a.step_off[K] = so + x;
-        if (so + x > a.send_capacity) report(a.status, VP_ERR_CAPACITY);
+      if (i == K - 1) a.step_off[K] = so + x;
+    }
+    if (ok && x != 0) {
+      ok = x > 0 && x % a.unit == 0 && so >= 0 && so % a.unit == 0 && co >= 0 && co % a.unit == 0 &&
+           j >= 0 && j < a.N && j != a.self;
+      if (ok && so + x > a.send_capacity) {
+        if (lead) report(a.status, VP_ERR_CAPACITY);
+        return;
       }
-    }
-    if (x == 0) return;
-    bool ok = x > 0 && x % a.unit == 0 && so >= 0 && so % a.unit == 0 && co >= 0 && co % a.unit == 0 &&
-              j >= 0 && j < a.N && j != a.self;
-    if (ok && so + x > a.send_capacity) {
-      if (lead) report(a.status, VP_ERR_CAPACITY);
-      return;
-    }
-    int64_t h = 0, b0 = 0;
-    if (ok) {
-      b0 = a.bounds[j];
-      h = a.bounds[j + 1] - b0;
-      ok = co + x <= (a.mode == 0 ? h : a.T * h) * a.unit;
+      int64_t h = 0, b0 = 0;
+      if (ok) {
+        b0 = a.bounds[j];
+        h = a.bounds[j + 1] - b0;
+        // heads: every head of the destination lies inside the token row
+        if (a.mode == 1) ok = b0 >= 0 && h >= 1 && (b0 + h) * a.unit <= a.token_stride;
+        ok = ok && co + x <= (a.mode == 0 ? h : a.T * h) * a.unit;
+      }
+      if (ok) {
+        d.first = a.mode == 0 ? b0 + co / a.unit : co / a.unit;
+        d.u0 = (int32_t)(so / a.unit);
+        d.nu = (int32_t)(x / a.unit);
+        d.h0 = a.mode == 0 ? 0 : (int32_t)b0;
+        d.h = a.mode == 0 ? 0 : (int32_t)h;
+      }
     }
     if (!ok) {
       if (lead) report(a.status, VP_ERR_INVALID_ARGUMENT);
       return;
     }
-    d.first = a.mode == 0 ? b0 + co / a.unit : co / a.unit;
-    d.u0 = (int32_t)(so / a.unit);
-    d.nu = (int32_t)(x / a.unit);
-    d.h0 = a.mode == 0 ? 0 : (int32_t)b0;
-    d.h = a.mode == 0 ? 0 : (int32_t)h;
+    if (a.mode == 1) {
+      if (lead) a.hdesc[i] = d;
+      return;
+    }
+    if (d.nu == 0) return;
   } else {
+    if (a.mode == 1) return;   // the slice kernel wrote the descriptors
     const int n = *a.n_desc, st = *a.status;
     if (i >= n || st != 0) return;
     d = a.desc[i];
   }
-  if (a.mode == 0) {
-    const unsigned long long g = (unsigned long long)a.gen << 32;
-    for (int u = tid + y * kIndexThreads; u < d.nu; u += kIndexThreads * ny) {
-      const int64_t tok = a.sorted_tok[d.first + u];
-      const int slot = a.sorted_slot[d.first + u];
-      if (tok < 0 || tok >= a.T || slot >= a.k) {
-        report(a.status, VP_ERR_INVALID_ARGUMENT);
-        continue;
-      }
-      a.lst[tok * a.k + slot] = g | (unsigned)(d.u0 + u);
+  const unsigned long long g = (unsigned long long)a.gen << 32;
+  for (int u = tid + y * kIndexThreads; u < d.nu; u += kIndexThreads * ny) {
+    const int64_t tok = a.sorted_tok[d.first + u];
+    const int slot = a.sorted_slot[d.first + u];
+    if (tok < 0 || tok >= a.T || slot >= a.k) {
+      report(a.status, VP_ERR_INVALID_ARGUMENT);
+      continue;
     }
-  } else {
-    for (int u = tid + y * kIndexThreads; u < d.nu; u += kIndexThreads * ny) {
-      const int64_t p = d.first + u, tok = p / d.h, hd = d.h0 + (p - tok * d.h);
-      a.src_off[(int64_t)d.u0 + u] = tok * a.token_stride + hd * a.unit;
-    }
+    a.lst[tok * a.k + slot] = g | (unsigned)(d.u0 + u);
   }
 }
 
@@ -395,35 +418,51 @@ __global__ void __launch_bounds__(TH) scatter_rows_kernel(
 constexpr int kGatherThreads = 256;
 constexpr int kGatherUnroll = 4;
 
-// Heads: grid-stride over the 16-byte vectors of the send buffer.
-__global__ void __launch_bounds__(kGatherThreads) gather_kernel(const unsigned char* __restrict__ src,
-                                                                const int64_t* __restrict__ src_off,
-                                                                const int32_t* Kp, const int64_t* step_off,
-                                                                int64_t unit, int64_t vpu, uint64_t magic,
-                                                                unsigned char* __restrict__ send,
-                                                                const int32_t* status) {
-  if (*status != 0) return;
-  const int64_t total_vec = step_off[*Kp] / 16;
-  const int64_t stride = (int64_t)gridDim.x * kGatherThreads;
-  int64_t v = (int64_t)blockIdx.x * kGatherThreads + threadIdx.x;
-  for (; v + (kGatherUnroll - 1) * stride < total_vec; v += kGatherUnroll * stride) {
+// Heads: workgroup (i, y) copies part y of descriptor i's units.  A step's
+// slice is stream positions first .. first+nu-1 of its destination, which
+// owns heads h0 .. h0+h-1 of every token: position p is token p / h, head
+// h0 + p % h.  Divisions are multiply-high by ceil(2^48 / divisor), exact
+// for dividends below 2^48 / divisor (the host bounds T * heads^2 and the
+// send vectors).  Every vector's source is checked against the activations
+// before it is loaded.  All loads of a pass are issued before its stores.
+__global__ void __launch_bounds__(kGatherThreads) gather_heads_kernel(
+    const unsigned char* __restrict__ src, const StepDesc* __restrict__ desc, const int32_t* n_desc,
+    const uint32_t* hdr, int64_t T, int64_t unit, int64_t vpu, uint64_t vpu_magic, int64_t cap_units,
+    unsigned char* __restrict__ send, int32_t* status) {
+  const int i = blockIdx.x;
+  if (*status != 0 || i >= *n_desc) return;
+  const StepDesc d = desc[i];
+  if (d.nu <= 0) return;
+  const int64_t token_stride = *(const int64_t*)(hdr + 2);
+  if (d.h < 1 || d.h0 < 0 || ((int64_t)d.h0 + d.h) * unit > token_stride || d.u0 < 0 ||
+      (int64_t)d.u0 + d.nu > cap_units || d.first < 0 || d.first + d.nu > T * d.h) {
+    if (threadIdx.x == 0 && blockIdx.y == 0) report(status, VP_ERR_INVALID_ARGUMENT);
+    return;
+  }
+  const uint64_t h_magic = ((uint64_t(1) << 48) + (uint64_t)d.h - 1) / (uint64_t)d.h;
+  const int64_t nvec = (int64_t)d.nu * vpu;
+  const int64_t stride = (int64_t)gridDim.y * kGatherThreads;
+  unsigned char* out = send + (int64_t)d.u0 * unit;
+  const unsigned char* base = src + (int64_t)d.h0 * unit;
+  for (int64_t v = (int64_t)blockIdx.y * kGatherThreads + threadIdx.x; v < nvec; v += kGatherUnroll * stride) {
     u32x4 r[kGatherUnroll];
 #pragma unroll
     for (int m = 0; m < kGatherUnroll; ++m) {
-      const uint64_t vv = (uint64_t)(v + m * stride);
-      const int64_t u = (int64_t)__umul64hi(vv << 16, magic);
-      const int64_t in = (int64_t)vv - u * vpu;
-      r[m] = *(const u32x4*)(src + src_off[u] + in * 16);
+      const int64_t vv = v + m * stride;
+      if (vv < nvec) {
+        const int64_t u = (int64_t)__umul64hi((uint64_t)vv << 16, vpu_magic);
+        const int64_t in = vv - u * vpu;
+        const int64_t p = d.first + u;
+        const int64_t tok = (int64_t)__umul64hi((uint64_t)p << 16, h_magic);
+        const int64_t hd = p - tok * d.h;
+        r[m] = *(const u32x4*)(base + tok * token_stride + hd * unit + in * 16);
+      }
     }
 #pragma unroll
-    for (int m = 0; m < kGatherUnroll; ++m)
-      __builtin_nontemporal_store(r[m], (u32x4*)(send + (v + m * stride) * 16));
-  }
-  for (; v < total_vec; v += stride) {
-    const int64_t u = (int64_t)__umul64hi((uint64_t)v << 16, magic);
-    const int64_t in = v - u * vpu;
-    u32x4 r = *(const u32x4*)(src + src_off[u] + in * 16);
-    __builtin_nontemporal_store(r, (u32x4*)(send + v * 16));
+    for (int m = 0; m < kGatherUnroll; ++m) {
+      const int64_t vv = v + m * stride;
+      if (vv < nvec) __builtin_nontemporal_store(r[m], (u32x4*)(out + vv * 16));
+    }
   }
 }
 
@@ -434,9 +473,11 @@ constexpr size_t kHeader = 256;   // [0]: the generation of the last prepare
 }  // namespace
 
 size_t pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit, int64_t T, int32_t k) {
+  (void)send_capacity;
+  (void)unit;
   const size_t head = kHeader + desc_bytes(k_max);
   if (k > 0) return head + (size_t)T * (size_t)k * 8;
-  return head + ((size_t)(send_capacity / unit) + 1) * sizeof(int64_t);
+  return head;
 }
 
 namespace {
@@ -464,7 +505,13 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
   int32_t* n_desc = (int32_t*)(ws + kHeader + (size_t)a.k_max * sizeof(StepDesc));
   char* rest = ws + kHeader + desc_bytes(a.k_max);
   unsigned long long* lst = (unsigned long long*)rest;
-  int64_t* src_off = (int64_t*)rest;
+  // heads: positions are below T * heads per token and are divided by at
+  // most that many heads in the gather; both stay within the division's range
+  if (a.mode == 1) {
+    const int64_t hmax = a.token_stride / a.unit;
+    if (a.T > 0 && (hmax > ((int64_t)1 << 15) || a.T > (((int64_t)1 << 47) / hmax) / hmax))
+      return set_error(VP_ERR_UNSUPPORTED, "too many heads per token for this many tokens");
+  }
 
   if (a.stages & 1) {
     uint32_t gen = ++g_generation;
@@ -479,10 +526,11 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
     }
     IndexArgs ia{a.mode, a.k, a.self_rank, a.N, a.k_max, a.unit, a.T, a.token_stride, a.send_capacity, gen,
                  a.sorted_tok, a.sorted_slot, desc, n_desc, a.K, a.dst, a.bytes, a.send_off, a.stream_off,
-                 a.mode == 0 ? a.dest_off : a.head_lo, a.step_off, hdr, lst, src_off, a.status};
-    // a step holds up to one destination's whole stream: split it over up to
-    // 16 workgroups so that a thread handles about two of its units
-    const int64_t units = a.mode == 0 ? a.T * a.k : a.send_capacity / a.unit;
+                 a.mode == 0 ? a.dest_off : a.head_lo, a.step_off, hdr, lst, desc, a.status};
+    // rows: a step holds up to one destination's whole stream: split it over
+    // up to 16 workgroups so that a thread handles about two of its units;
+    // heads: one thread per step does all the work
+    const int64_t units = a.mode == 0 ? a.T * a.k : 0;
     const int64_t per_step = (units + a.N - 1) / std::max(1, a.N);
     const int ny = (int)std::min<int64_t>(16, std::max<int64_t>(1, (per_step + 2 * kIndexThreads - 1) /
                                                                       (2 * kIndexThreads)));
@@ -523,11 +571,12 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
     const uint64_t magic = (uint64_t)((two48 + (unsigned __int128)vpu - 1) / (unsigned __int128)vpu);
     const int64_t max_vec = a.send_capacity / 16;
     if (max_vec >= ((int64_t)1 << 48) / vpu) return set_error(VP_ERR_UNSUPPORTED, "send buffer too large");
-    int64_t blocks = (max_vec + kGatherThreads * kGatherUnroll - 1) / (kGatherThreads * kGatherUnroll);
-    blocks = std::max<int64_t>(1, std::min<int64_t>(blocks, 8192));
-    hipLaunchKernelGGL(gather_kernel, dim3((unsigned)blocks), dim3(kGatherThreads), 0, s,
-                       (const unsigned char*)a.src, src_off, a.K, a.step_off, a.unit, vpu, magic,
-                       (unsigned char*)a.send, a.status);
+    // parts per step: about 16 KiB each for an average step of k_max
+    const int64_t per_step = a.send_capacity / std::max(1, a.k_max);
+    const int ny = (int)std::min<int64_t>(64, std::max<int64_t>(1, (per_step + 16383) / 16384));
+    hipLaunchKernelGGL(gather_heads_kernel, dim3((unsigned)a.k_max, (unsigned)ny), dim3(kGatherThreads), 0, s,
+                       (const unsigned char*)a.src, desc, n_desc, hdr, a.T, a.unit, vpu, magic,
+                       a.send_capacity / a.unit, (unsigned char*)a.send, a.status);
   }
   if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "pack launch failed");
   return VP_OK;

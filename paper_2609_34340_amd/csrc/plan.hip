@@ -56,6 +56,7 @@ struct Shared {
   int64_t cap[4];
   int32_t capu[4];
   int32_t K, err;
+  int32_t huge;   // some demand entry reaches 2^42 bytes
 };
 
 struct PlanArgs {
@@ -623,6 +624,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     sh->total_units = 0;
     sh->Lmax = 0;
     sh->key = 0;
+    sh->huge = 0;
   }
   for (int r = tid; r < N; r += kPlanThreads) {
     const int grp = r / g;
@@ -676,9 +678,12 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   for (int x = tid; x < N; x += kPlanThreads) colsum[x] = 0;
   __syncthreads();
 
-  // one pass over D: validate, copy to D^rem, row / column sums, aggregates
+  // one pass over D: validate, copy to D^rem, row / column sums, aggregates.
+  // An entry of 2^42 bytes or more is refused before anything is summed: at
+  // most 2^20 entries below 2^42 keep every row, column and total sum below
+  // 2^62.
   {
-    bool bad = false;
+    bool bad = false, huge = false;
     int64_t tot = 0, lmax = 0;
     const uint64_t mask = (uint64_t(1) << P.unit_shift) - 1;
     for (int i = wave; i < N; i += kWaves) {
@@ -689,6 +694,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         const bool divisible = ((uint64_t)v & mask) == 0 &&
                                ((uint64_t)v >> P.unit_shift) * P.odd_inv <= P.odd_lim;
         if (v < 0 || (i == j && v != 0) || !divisible) bad = true;
+        if (v >= (int64_t(1) << 42)) huge = true;
         gDrem[(size_t)i * N + j] = v;
         rs += v;
         if (v > 0) {
@@ -706,6 +712,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       lmax = rs > lmax ? rs : lmax;
     }
     if (bad) set_err(sh, VP_ERR_INVALID_DEMAND);
+    if (huge) sh->huge = 1;
     if (lane == 0) {
       atomicAdd((unsigned long long*)&sh->total_rem, (unsigned long long)tot);
       atomicAdd((unsigned long long*)&sh->total_units,
@@ -734,7 +741,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       // credits are int32 bytes below 2^31 and int32 units below 2^27
       if (cap >= (int64_t(1) << 31) || cap / P.unit >= (int64_t(1) << 27)) set_err(sh, VP_ERR_UNSUPPORTED);
     }
-    if (sh->total_rem >= (int64_t(1) << 42) || sh->total_units >= (int64_t(1) << 28))
+    if (sh->huge || sh->total_rem >= (int64_t(1) << 42) || sh->total_units >= (int64_t(1) << 28))
       set_err(sh, VP_ERR_UNSUPPORTED);
   }
   __syncthreads();

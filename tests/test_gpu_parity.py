@@ -265,6 +265,39 @@ def test_plan_device_errors(vp):
     assert_schedule_equal(g, o)
 
 
+@pytest.mark.parametrize("case", ["entry_2p62_block", "entry_2p42", "cap_2p31_bytes", "cap_2p27_units",
+                                  "total_2p42_bytes", "total_2p28_units", "invalid_first"])
+def test_plan_device_limits(vp, case):
+    """Each device-side refusal of the planner on a small 8-rank input: the
+    kernel reports a status, emits nothing and returns.  Expected statuses
+    follow from the documented limits by hand: tau = ceil(L_max / (32 *
+    k_target)) and cap = tau * 32 at the PCIe rate."""
+    topo = vpgen.config(1).topo
+    log("plan device limit %s" % case)
+    D = np.zeros((8, 8), np.int64)
+    unit, kt, want = 1 << 20, 4096, vp.UNSUPPORTED
+    if case == "entry_2p62_block":
+        # every row, column and total sum of this block wraps to 0 in int64
+        D[0:4, 4:8] = 1 << 62
+    elif case == "entry_2p42":
+        D[0, 1] = 1 << 42
+    elif case == "cap_2p31_bytes":
+        D[0, 1], kt = 1 << 31, 1          # tau = 2^26 ns, cap = 2^31 B
+    elif case == "cap_2p27_units":
+        D[0, 1], kt, unit = 1 << 30, 1, 8  # cap = 2^30 B = 2^27 units
+    elif case == "total_2p42_bytes":
+        D[0, 1] = D[2, 3] = 1 << 41        # caps 2^29 B, 2^22 units in all
+    elif case == "total_2p28_units":
+        D[0, 1] = D[2, 3] = 1 << 31
+        unit = 16                          # 2^28 units; caps 2^19 B
+    else:
+        D[0, 1] = 1 << 42
+        D[2, 2] = unit                     # an invalid entry wins over a limit
+        want = vp.INVALID_DEMAND
+    g = gpu_plan(vp, topo, D, unit, k_target=kt)
+    assert g["status"] == want and g["K"] == 0
+
+
 def test_plan_rejects_schedule_too_large_for_32_bit_offsets(vp):
     """k_max * N * 8 >= 2^32 is refused on the host before anything is
     enqueued (the planner addresses a matrix's schedule with 32-bit byte
@@ -461,6 +494,56 @@ def test_pack_heads_parity(vp, self_rank, layout):
     assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off)
 
 
+@pytest.mark.parametrize("where", ["first", "middle", "last"])
+def test_pack_rejects_a_layout_that_does_not_tile(vp, where):
+    """A send-offset layout that leaves a gap (here one unit) is refused by
+    both packs before anything is copied: the rows pack on the 8-rank
+    workload and the heads pack on the Ulysses workload, the latter on a
+    workspace that a valid call filled just before."""
+    log("pack gapped layout %s" % where)
+    # rows
+    w, R, dem, D = moe_case(1)
+    s = oracle_plan(1, D)
+    carrying = np.flatnonzero(s["bytes"][:, 0] > 0)
+    k = {"first": 0, "middle": int(carrying[len(carrying) // 2]), "last": int(carrying[-1])}[where]
+    rt = torch.from_numpy(R).cuda()
+    gd = vp.demand(rt, w.n_ranks, w.experts, w.row_bytes, sort_row=0)
+    sched = upload_schedule(vp, w.n_ranks, s, layout=True)
+    sched["send_off"][k:, 0] += w.row_bytes
+    total = int(s["bytes"][:, 0].sum())
+    send = torch.full((total + 2 * w.row_bytes,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
+    st = gd["status"]
+    vp.pack_rows(torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda(), w.row_bytes, gd["sorted_tok"],
+                 gd["sorted_slot"], gd["dest_off"], 0, sched, send, step_off, st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == vp.INVALID_ARGUMENT
+    assert (send == 0xA5).all()
+    # heads: one valid call, then the gapped layout on the same workspace
+    w, hl, D = heads_case()
+    s = oracle_plan(4, D)
+    act = torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda()
+    hl_d = torch.from_numpy(hl).cuda()
+    ref, _ = oracle.pack_heads(vpgen.tokens_bf16(w, 0), w.token_stride, hl, w.row_bytes, 0, s)
+    sched = upload_schedule(vp, w.n_ranks, s, layout=True)
+    cap = ref.size + 2 * w.row_bytes
+    send = torch.full((cap,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
+    ws = torch.zeros(vp.pack_workspace_bytes(8 * w.n_ranks, cap, w.row_bytes), dtype=torch.uint8, device="cuda")
+    st = vp.new_status()
+    vp.pack_heads(act, w.token_stride, hl_d, w.row_bytes, 0, sched, send, step_off, st, ws=ws)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0 and torch.equal(send[:ref.size], torch.from_numpy(ref).cuda())
+    carrying = np.flatnonzero(s["bytes"][:, 0] > 0)
+    k = {"first": 0, "middle": int(carrying[len(carrying) // 2]), "last": int(carrying[-1])}[where]
+    sched["send_off"][k:, 0] += w.row_bytes
+    send.fill_(0xA5)
+    vp.pack_heads(act, w.token_stride, hl_d, w.row_bytes, 0, sched, send, step_off, st, ws=ws)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == vp.INVALID_ARGUMENT
+    assert (send == 0xA5).all()
+
+
 # -------------------------------------------------------------- pipeline
 
 @pytest.mark.parametrize("cid", [1, 4, 5])
@@ -494,8 +577,9 @@ def test_plan_largest_topology_is_a_valid_decomposition(vp):
     """1,024 ranks (128 nodes), the planner's largest shape: too big for the
     oracle to plan in test time, so the properties any valid schedule has are
     checked instead -- the activations sum to D exactly, every step is a
-    derangement whose lanes use path classes of their group pairs, every
-    step serves bytes, and K stays within k_max (raised to 32N)."""
+    derangement whose lanes use path classes of their group pairs and share
+    no modeled resource (Eq. (1)), every step serves bytes, and K stays
+    within k_max (raised to 32N)."""
     topo = vpgen.Topology(128)
     N = topo.n_ranks
     rng = np.random.default_rng(1024)
@@ -525,6 +609,9 @@ def test_plan_largest_topology_is_a_valid_decomposition(vp):
     assert np.array_equal(X, D)
     assert (nb.sum(axis=1) > 0).all()
     cls = gcat(vp, topo).instances()["cls"][inst]
+    # every step's lanes are resource-disjoint (Eq. (1)) on the topology model
+    from oracle.checks import TopoModel, schedule_valid_np
+    schedule_valid_np(TopoModel(topo), D, dst, cls, nb)
     gs, gd = rows[None, :] // topo.gpus_per_switch, dst // topo.gpus_per_switch
     Q = topo.sockets_per_node * topo.switches_per_socket
     same_switch = gs == gd

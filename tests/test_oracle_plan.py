@@ -13,7 +13,7 @@ from scipy.optimize import linear_sum_assignment
 import oracle
 import vpgen
 from oracle.checks import (NIC, PIX, PXB, TopoModel, exhaustive_makespan, modeled_time,
-                           schedule_valid, utility)
+                           schedule_valid, schedule_valid_np, utility)
 
 _cat_cache = {}
 
@@ -268,6 +268,68 @@ def test_capacity_limit_is_reported():
     D = demand_for(1)
     s = cat.plan(D, w.row_bytes, k_max=3, check=False)
     assert s["status"] == oracle.CAPACITY and s["K"] == 3
+
+
+def _both_validators(tm, D, dst, cls, nb):
+    """(lane checker verdict, vectorised checker verdict): True when valid."""
+    res = []
+    sched = {"K": dst.shape[0], "dst": dst, "inst": cls, "bytes": nb}
+    for f in (lambda: schedule_valid(tm, D, sched, np.arange(4)),
+              lambda: schedule_valid_np(tm, D, dst, cls, nb)):
+        try:
+            f()
+            res.append(True)
+        except AssertionError:
+            res.append(False)
+    return tuple(res)
+
+
+@pytest.mark.parametrize("cid", [1, 2, 4])
+def test_vectorised_validity_agrees_with_the_lane_checker(cid):
+    """The vectorised validity check used at 1,024 ranks accepts what the
+    per-lane checker accepts and rejects the same planted faults: a lane
+    class foreign to its group pair, two NIC lanes out of one switch in one
+    step (Eq. (1)), a rank that sends to itself, a byte moved between pairs."""
+    w = vpgen.config(cid)
+    cat = catalog(w.topo)
+    tm = TopoModel(w.topo)
+    D = demand_for(cid)
+    s = cat.plan(D, w.row_bytes)
+    dst, nb = s["dst"].copy(), s["bytes"].copy()
+    cls = cls_table(cat)[s["inst"]].astype(np.int64)
+    assert _both_validators(tm, D, dst, cls, nb) == (True, True)
+    g = w.topo.gpus_per_switch
+    rows = np.arange(w.n_ranks)
+    # a lane inside one switch labelled NIC
+    k, i = np.argwhere(cls == PIX)[0]
+    c2 = cls.copy()
+    c2[k, i] = NIC
+    assert _both_validators(tm, D, dst, c2, nb) == (False, False)
+    # two lanes leaving one switch for other switches, both on the NIC
+    for k in range(s["K"]):
+        out = np.flatnonzero(dst[k] // g != rows // g)
+        grp = out // g
+        dup = [x for x in out if (grp == x // g).sum() >= 2]
+        if len(dup) >= 2:
+            c3 = cls.copy()
+            c3[k, dup[:2]] = NIC
+            pair_ok = all(tm.classes(int(x) // g, int(dst[k, x]) // g).count(NIC) for x in dup[:2])
+            if pair_ok:
+                assert _both_validators(tm, D, dst, c3, nb) == (False, False)
+                break
+    else:
+        pytest.fail("no step with two lanes leaving one switch")
+    # rank 0 and rank j = pi(0) swap destinations: rank j now sends to itself
+    d4 = dst.copy()
+    j = int(dst[0, 0])
+    d4[0, 0], d4[0, j] = dst[0, j], j
+    assert _both_validators(tm, D, d4, cls, nb) == (False, False)
+    # one byte moved from one lane to another
+    n5 = nb.copy()
+    k, i = np.argwhere(n5 > 0)[0]
+    n5[k, i] -= 1
+    n5[k, (i + 1) % w.n_ranks] += 1
+    assert _both_validators(tm, D, dst, cls, n5) == (False, False)
 
 
 # ------------------------------------ extra demands and restricted catalogs
