@@ -79,6 +79,9 @@ def lib():
         L.orc_receive_counts.argtypes = [vp, vp, C.c_int32, C.c_int32, vp]
         L.orc_plan.argtypes = [vp, vp, C.POINTER(_Params), C.c_int32, vp, vp, vp, vp, vp, vp,
                                vp, C.c_int64, vp]
+        L.orc_plan_candidates.argtypes = [vp, vp, C.POINTER(_Params), C.c_int32, vp, vp, vp, vp, vp, vp,
+                                          C.c_int64, vp]
+        L.orc_start_binding.argtypes = [vp, vp, C.POINTER(_Params), C.c_int64, C.c_int32, C.c_int32, vp, vp]
         L.orc_splitmix_stream.argtypes = [C.c_uint64, vp, C.c_int32, vp]
         L.orc_utility_greater.argtypes = [C.c_int64] * 7
         L.orc_modeled_time.argtypes = [vp, C.c_int32, C.c_int32, vp, vp, C.c_int64, vp, vp]
@@ -201,6 +204,58 @@ class Catalog:
         if trace_cap:
             out["trace"] = trace[: int(tn[0])].copy()
         return out
+
+    def plan_candidates(self, D: np.ndarray, unit: int, k_target: Optional[int] = None,
+                        lambda_ns: int = DEFAULT_LAMBDA_NS, n_start: int = DEFAULT_N_START,
+                        i_aa: int = DEFAULT_I_AA, seed: int = 0, k_max: Optional[int] = None,
+                        log_cap: int = 100000):
+        """The plan of D together with every candidate it evaluated: a list of
+        dicts (iteration, family, S, xm, bm, and per instance in family order
+        src, dst and the volume x)."""
+        N = self.N
+        D = np.ascontiguousarray(D, dtype=np.int64)
+        k_target = 2 * N if k_target is None else k_target
+        k_max = 8 * N if k_max is None else k_max
+        P = _Params(k_target, lambda_ns, unit, n_start, i_aa, seed)
+        K = np.zeros(1, np.int32)
+        cap = max(k_max, 1)
+        fam = np.full(cap, -1, np.int32)
+        dst = np.full((cap, N), -1, np.int32)
+        inst = np.full((cap, N), -1, np.int32)
+        nbytes = np.zeros((cap, N), np.int64)
+        w = 5 + 3 * N
+        log = np.zeros((log_cap, w), np.int64)
+        ln = np.zeros(1, np.int64)
+        st = lib().orc_plan_candidates(self._h, _p(D), C.byref(P), k_max, _p(K), _p(fam), _p(dst), _p(inst),
+                                       _p(nbytes), _p(log), log_cap, _p(ln))
+        if st != OK:
+            raise OracleError(st, "orc_plan_candidates")
+        k = int(K[0])
+        n = int(ln[0])
+        assert n < log_cap, "candidate log full"
+        cands = []
+        for r in log[:n]:
+            lanes = r[5:].reshape(N, 3)
+            cands.append(dict(iter=int(r[0]), family=int(r[1]), S=int(r[2]), xm=int(r[3]), bm=int(r[4]),
+                              src=lanes[:, 0].copy(), dst=lanes[:, 1].copy(), x=lanes[:, 2].copy()))
+        sched = dict(status=st, K=k, family=fam[:k].copy(), dst=dst[:k].copy(), inst=inst[:k].copy(),
+                     bytes=nbytes[:k].copy())
+        return sched, cands
+
+    def start_binding(self, D: np.ndarray, unit: int, family: int, start: int, iteration: int = 0,
+                      k_target: Optional[int] = None, seed: int = 0):
+        """MultiStartAA's start binding `start` of `family` on residual D
+        (before any sweep): (src, dst) rank per instance in family order."""
+        N = self.N
+        D = np.ascontiguousarray(D, dtype=np.int64)
+        k_target = 2 * N if k_target is None else k_target
+        P = _Params(k_target, DEFAULT_LAMBDA_NS, unit, DEFAULT_N_START, DEFAULT_I_AA, seed)
+        src = np.zeros(N, np.int32)
+        dst = np.zeros(N, np.int32)
+        st = lib().orc_start_binding(self._h, _p(D), C.byref(P), iteration, family, start, _p(src), _p(dst))
+        if st != OK:
+            raise OracleError(st, "orc_start_binding")
+        return src, dst
 
     def modeled_time(self, sched, lambda_ns: int = DEFAULT_LAMBDA_NS):
         """Eq. (2) as an exact fraction (numerator, denominator) in ns."""

@@ -11,9 +11,13 @@
 //
 // Where the paper fixes a result by a plain definition (the demand matrix,
 // the send-buffer layout, the modeled completion time) the code is that
-// definition written out.  The catalog (Alg. 1) and the scheduler (Alg. 2)
-// are heuristic/enumerative: they follow the algorithms' steps in the paper's
-// order and notation, with every choice the paper leaves open fixed by the
+// definition written out.  So is the catalog: every set of path instances
+// that satisfies the balance and compatibility constraints (Eq. (3),
+// Eq. (4)), found by a search over each group's choice of outgoing lanes,
+// then pruned by the dominance rules of Sec. 4.1.  The scheduler is a
+// heuristic: it takes the steps of Sec. 4.2 in the paper's order (shape by
+// Eq. (5)-(6), binding by MultiStartAA on Eq. (7)-(8), volumes and utility
+// by Eq. (9)-(10)), with every choice the paper leaves open fixed by the
 // readings listed in the design notes (topology model, PIX multiplicity,
 // node-circulant reduction, canonical order, integer credit, start rule,
 // counter-based randomness, exact utility comparison).
@@ -24,6 +28,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <functional>
 #include <map>
 #include <set>
 #include <tuple>
@@ -144,94 +149,26 @@ bool subset_of(const std::vector<int>& x, const std::vector<int>& y) {
   return std::includes(y.begin(), y.end(), x.begin(), x.end());
 }
 
-// PrunePaths (Sec. 4.1 "Pruning and search cost"): drop r when another r' of
-// the same ordered group pair has L(r') subset of L(r) and bw(r') >= bw(r), one
-// of them strict.
-std::vector<Inst> prune_paths(const std::vector<Inst>& R) {
+// Path-level dominance (Sec. 4.1 "Pruning and search cost"): an instance is
+// dropped when another instance of the same ordered group pair uses a subset
+// of its resources at no lower rate, strictly better in one of the two.
+std::vector<Inst> drop_dominated_paths(const std::vector<Inst>& R) {
   std::vector<Inst> out;
-  for (size_t x = 0; x < R.size(); ++x) {
+  for (const Inst& r : R) {
     bool dominated = false;
-    for (size_t y = 0; y < R.size() && !dominated; ++y) {
-      if (x == y) continue;
-      const Inst& r = R[x];
-      const Inst& rp = R[y];
-      if (rp.a != r.a || rp.d != r.d || rp.remote != r.remote) continue;
-      bool sub = subset_of(rp.L, r.L);
-      bool strict_sub = sub && rp.L.size() < r.L.size();
-      if (sub && rp.bw >= r.bw && (strict_sub || rp.bw > r.bw)) dominated = true;
+    for (const Inst& q : R) {
+      if (&q == &r || q.a != r.a || q.d != r.d || q.remote != r.remote) continue;
+      const bool fewer = subset_of(q.L, r.L) && q.L.size() < r.L.size();
+      const bool faster = q.bw > r.bw;
+      if (subset_of(q.L, r.L) && q.bw >= r.bw && (fewer || faster)) {
+        dominated = true;
+        break;
+      }
     }
-    if (!dominated) out.push_back(R[x]);
+    if (!dominated) out.push_back(r);
   }
   return out;
 }
-
-// ---------------------------------------------------------------------------
-// Alg. 1: pruned binary DFS over the ordered instances.  Explore(t, B): if B
-// is complete, insert it into the bucket of its shape; otherwise stop when t
-// runs past the list or SuffixOK fails; explore the exclude branch first,
-// then the include branch when CanAdd holds.
-// ---------------------------------------------------------------------------
-struct Dfs {
-  const std::vector<Inst>& R;
-  int n_groups, g;
-  std::vector<int> outd, ind, used_res;
-  std::vector<std::vector<int>> suf_out, suf_in;   // remaining instances per group from t on
-  std::vector<int> B;
-  std::vector<std::vector<int>> found;
-
-  Dfs(const std::vector<Inst>& R_, int n_groups_, int g_, int n_res)
-      : R(R_), n_groups(n_groups_), g(g_), outd(n_groups_, 0), ind(n_groups_, 0),
-        used_res(n_res, 0) {
-    const size_t m = R.size();
-    suf_out.assign(m + 1, std::vector<int>(n_groups, 0));
-    suf_in.assign(m + 1, std::vector<int>(n_groups, 0));
-    for (size_t t = m; t-- > 0;) {
-      suf_out[t] = suf_out[t + 1];
-      suf_in[t] = suf_in[t + 1];
-      suf_out[t][R[t].a]++;
-      suf_in[t][R[t].d]++;
-    }
-  }
-  bool complete() const {
-    for (int x = 0; x < n_groups; ++x)
-      if (outd[x] != g || ind[x] != g) return false;
-    return true;
-  }
-  // SuffixOK: the instances not yet decided must be able to fill every
-  // group's remaining outgoing and incoming slots.
-  bool suffix_ok(size_t t) const {
-    for (int x = 0; x < n_groups; ++x)
-      if (outd[x] + suf_out[t][x] < g || ind[x] + suf_in[t][x] < g) return false;
-    return true;
-  }
-  // CanAdd: resource-disjoint and within the group-degree limits.
-  bool can_add(const Inst& r) const {
-    if (outd[r.a] >= g || ind[r.d] >= g) return false;
-    for (int l : r.L)
-      if (used_res[l]) return false;
-    return true;
-  }
-  void explore(size_t t) {
-    if (complete()) {
-      found.push_back(B);
-      return;
-    }
-    if (t >= R.size() || !suffix_ok(t)) return;
-    explore(t + 1);
-    const Inst& r = R[t];
-    if (can_add(r)) {
-      outd[r.a]++;
-      ind[r.d]++;
-      for (int l : r.L) used_res[l] = 1;
-      B.push_back((int)t);
-      explore(t + 1);
-      B.pop_back();
-      for (int l : r.L) used_res[l] = 0;
-      outd[r.a]--;
-      ind[r.d]--;
-    }
-  }
-};
 
 // A family as the canonical ids of its instances (ascending).
 typedef std::vector<int> Fam;
@@ -239,81 +176,132 @@ typedef std::vector<int> Fam;
 // Shape of a family: lane counts per (src group, dst group, remote flag).
 typedef std::vector<int> ShapeKey;
 
-// PruneFamilies (Sec. 4.1): inside one shape bucket, remove exact duplicates
-// and families dominated by another (instances paired inside every group pair
-// with identical footprints and no lower rate, one strictly higher).
-std::vector<Fam> prune_families(std::vector<Fam> fams, const std::vector<Inst>& table) {
+// Every family of an instance set, from its definition (Sec. 4.1, Eq. (3)
+// and Eq. (4)): a set of instances in which each group is the source of
+// exactly g instances and the destination of exactly g, and no modeled
+// resource is used twice.  The search decides one group at a time which g of
+// the instances leaving it the family takes (every g-subset, in index
+// order); a choice is abandoned as soon as some group would receive more
+// than g lanes or a resource would repeat, and a complete choice is kept
+// when every group receives exactly g.  The set of families found does not
+// depend on the order of the search.
+std::vector<std::vector<int>> all_families(const std::vector<Inst>& R, int n_groups, int g, int n_res) {
+  std::vector<std::vector<int>> leaving(n_groups);
+  for (int i = 0; i < (int)R.size(); ++i) leaving[R[i].a].push_back(i);
+  std::vector<std::vector<int>> found;
+  std::vector<int> into(n_groups, 0), res_used(n_res, 0), chosen;
+
+  // try to add instance i; undo with take_back
+  auto fits = [&](int i) {
+    if (into[R[i].d] == g) return false;
+    for (int l : R[i].L)
+      if (res_used[l]) return false;
+    return true;
+  };
+  auto take = [&](int i, int sgn) {
+    into[R[i].d] += sgn;
+    for (int l : R[i].L) res_used[l] += sgn;
+  };
+  // group a picks its remaining `need` lanes among leaving[a][from..]
+  std::function<void(int, int, int)> pick = [&](int a, int from, int need) {
+    if (need == 0) {
+      if (a + 1 < n_groups) {
+        pick(a + 1, 0, g);
+        return;
+      }
+      for (int x = 0; x < n_groups; ++x)
+        if (into[x] != g) return;
+      found.push_back(chosen);
+      return;
+    }
+    const std::vector<int>& opts = leaving[a];
+    for (int m = from; m + need <= (int)opts.size(); ++m) {
+      const int i = opts[m];
+      if (!fits(i)) continue;
+      take(i, +1);
+      chosen.push_back(i);
+      pick(a, m + 1, need - 1);
+      chosen.pop_back();
+      take(i, -1);
+    }
+  };
+  if (n_groups > 0) pick(0, 0, g);
+  return found;
+}
+
+// Family-level pruning (Sec. 4.1): inside one shape bucket, exact duplicates
+// (the same multiset of (group pair, footprint, rate), e.g. two PIX copies
+// swapped) collapse to the first family in canonical order, and a family is
+// removed when another one of the bucket dominates it: their instances pair
+// up inside every group pair with identical footprints and no lower rate,
+// with at least one strictly higher rate.
+std::vector<Fam> drop_duplicate_and_dominated(std::vector<Fam> fams, const std::vector<Inst>& table) {
   std::sort(fams.begin(), fams.end());
-  typedef std::tuple<int, int, bool, std::vector<int>, i64> Sig;
-  auto signature = [&](const Fam& f) {
-    std::vector<Sig> s;
+  typedef std::tuple<int, int, bool, std::vector<int>> PairFoot;
+  auto rates_by_foot = [&](const Fam& f) {
+    std::map<PairFoot, std::vector<i64>> m;
     for (int id : f) {
       const Inst& r = table[id];
-      s.emplace_back(r.a, r.d, r.remote, r.L, r.bw);
+      m[PairFoot(r.a, r.d, r.remote, r.L)].push_back(r.bw);
     }
-    std::sort(s.begin(), s.end());
-    return s;
+    for (auto& kv : m) std::sort(kv.second.rbegin(), kv.second.rend());
+    return m;
   };
   std::vector<Fam> uniq;
-  std::set<std::vector<Sig>> seen;
+  std::vector<std::map<PairFoot, std::vector<i64>>> prof;
+  std::set<std::map<PairFoot, std::vector<i64>>> seen;
   for (const Fam& f : fams) {
-    auto s = signature(f);
-    if (seen.insert(s).second) uniq.push_back(f);
+    auto m = rates_by_foot(f);
+    if (seen.insert(m).second) {
+      uniq.push_back(f);
+      prof.push_back(m);
+    }
   }
-  // dominance: per (group pair, footprint) the rates must be pairable with
-  // no lower rate; at least one strictly higher overall.
-  auto dominates = [&](const Fam& f1, const Fam& f2) {
-    typedef std::tuple<int, int, bool, std::vector<int>> Key;
-    std::map<Key, std::vector<i64>> r1, r2;
-    for (int id : f1) { const Inst& r = table[id]; r1[Key(r.a, r.d, r.remote, r.L)].push_back(r.bw); }
-    for (int id : f2) { const Inst& r = table[id]; r2[Key(r.a, r.d, r.remote, r.L)].push_back(r.bw); }
-    if (r1.size() != r2.size()) return false;
-    bool strict = false;
-    for (auto& kv : r1) {
-      auto it = r2.find(kv.first);
-      if (it == r2.end() || it->second.size() != kv.second.size()) return false;
-      std::vector<i64> x = kv.second, y = it->second;
-      std::sort(x.rbegin(), x.rend());
-      std::sort(y.rbegin(), y.rend());
-      for (size_t i = 0; i < x.size(); ++i) {
-        if (x[i] < y[i]) return false;
-        if (x[i] > y[i]) strict = true;
+  // y dominates x: same (group pair, footprint) classes with the same sizes,
+  // rates sorted descending pairwise no lower, one strictly higher
+  auto dominates = [&](size_t y, size_t x) {
+    if (prof[y].size() != prof[x].size()) return false;
+    bool higher = false;
+    for (const auto& kv : prof[x]) {
+      auto it = prof[y].find(kv.first);
+      if (it == prof[y].end() || it->second.size() != kv.second.size()) return false;
+      for (size_t u = 0; u < kv.second.size(); ++u) {
+        if (it->second[u] < kv.second[u]) return false;
+        higher |= it->second[u] > kv.second[u];
       }
     }
-    return strict;
+    return higher;
   };
   std::vector<Fam> out;
-  for (size_t i = 0; i < uniq.size(); ++i) {
+  for (size_t x = 0; x < uniq.size(); ++x) {
     bool dom = false;
-    for (size_t j = 0; j < uniq.size() && !dom; ++j)
-      if (i != j && dominates(uniq[j], uniq[i])) dom = true;
-    if (!dom) out.push_back(uniq[i]);
+    for (size_t y = 0; y < uniq.size() && !dom; ++y) dom = y != x && dominates(y, x);
+    if (!dom) out.push_back(uniq[x]);
   }
   return out;
 }
 
-// Run Alg. 1 on one instance set and return the buckets (shape -> families).
-std::map<ShapeKey, std::vector<Fam>> run_alg1(const std::vector<Inst>& table,
-                                               const std::vector<Inst>& candidates,
-                                               int n_groups, int g, int n_res) {
-  std::vector<Inst> R = prune_paths(candidates);
-  // fixed order r_1..r_m: ascending canonical id
+// The catalog of one instance set: drop dominated paths, find every family,
+// file each under its shape (lane counts per group pair, remote lanes
+// counted apart), then prune each bucket.
+std::map<ShapeKey, std::vector<Fam>> catalog_of(const std::vector<Inst>& table,
+                                                const std::vector<Inst>& candidates, int n_groups, int g,
+                                                int n_res) {
+  std::vector<Inst> R = drop_dominated_paths(candidates);
   std::sort(R.begin(), R.end(), [](const Inst& x, const Inst& y) { return x.id < y.id; });
-  Dfs dfs(R, n_groups, g, n_res);
-  dfs.explore(0);
   std::map<ShapeKey, std::vector<Fam>> buckets;
-  for (const auto& B : dfs.found) {
+  for (const auto& sel : all_families(R, n_groups, g, n_res)) {
     ShapeKey M(2 * n_groups * n_groups, 0);
     Fam f;
-    for (int t : B) {
-      const Inst& r = R[t];
+    for (int i : sel) {
+      const Inst& r = R[i];
       M[(r.remote ? n_groups * n_groups : 0) + r.a * n_groups + r.d]++;
       f.push_back(r.id);
     }
     std::sort(f.begin(), f.end());
     buckets[M].push_back(f);
   }
-  for (auto& kv : buckets) kv.second = prune_families(kv.second, table);
+  for (auto& kv : buckets) kv.second = drop_duplicate_and_dominated(kv.second, table);
   return buckets;
 }
 
@@ -390,7 +378,7 @@ void build_circulant(Catalog& C, bool nearest) {
   // k = 0 set: PIX, PXB, NIC between slots of the same node (loopback).
   std::vector<Inst> set0;
   for (Inst r : C.table) { r.remote = false; set0.push_back(r); }
-  auto b0 = run_alg1(C.table, set0, Q, g, n_res);
+  auto b0 = catalog_of(C.table, set0, Q, g, n_res);
   if (nearest) keep_nearest(b0, C.table, t, false);
   // k != 0 set: PIX, PXB, and NIC lanes to the same slot pattern on another node.
   std::map<ShapeKey, std::vector<Fam>> b1;
@@ -398,7 +386,7 @@ void build_circulant(Catalog& C, bool nearest) {
     std::vector<Inst> set1;
     for (Inst r : C.table) { r.remote = (r.cls == NIC); set1.push_back(r); }
     std::vector<Inst> table1 = set1;
-    auto all1 = run_alg1(table1, set1, Q, g, n_res);
+    auto all1 = catalog_of(table1, set1, Q, g, n_res);
     for (auto& kv : all1) {
       std::vector<Fam> keep;
       for (const Fam& f : kv.second) {
@@ -455,7 +443,7 @@ void build_full(Catalog& C, bool nearest) {
   const Topo& t = C.topo;
   const int G = t.G();
   C.table = cluster_table(t);
-  auto b = run_alg1(C.table, C.table, G, t.g, 4 * G + t.n_nodes * t.sockets * t.sockets);
+  auto b = catalog_of(C.table, C.table, G, t.g, 4 * G + t.n_nodes * t.sockets * t.sockets);
   if (nearest) keep_nearest(b, C.table, t, false);
   for (const auto& kv : b) {
     CShape s;
@@ -505,7 +493,7 @@ SplitMix keyed_stream(uint64_t seed, uint64_t iter, uint64_t fam, uint64_t start
 }
 
 // ---------------------------------------------------------------------------
-// Alg. 2: online channel-guided demand decomposition.
+// Online channel-guided demand decomposition (Sec. 4.2, Alg. 2).
 // ---------------------------------------------------------------------------
 struct Params {
   i64 k_target, lambda_ns, unit;
@@ -523,6 +511,10 @@ struct Planner {
   // optional trace of F after every AA half-step: (iter, family, start, half, F)
   i64* trace;
   i64 trace_cap, trace_n;
+  // optional log of every evaluated candidate: (iter, family, S, x, b, then
+  // per instance in family order: source, destination, volume)
+  i64* cand_log;
+  i64 cand_cap, cand_n;
 
   Planner(const Catalog& C_, const Params& P_) : C(C_), P(P_) {
     N = C.topo.N();
@@ -530,6 +522,8 @@ struct Planner {
     g = C.topo.g;
     trace = nullptr;
     trace_cap = trace_n = 0;
+    cand_log = nullptr;
+    cand_cap = cand_n = 0;
     K = 0;
     tau = 1;
   }
@@ -771,77 +765,130 @@ struct Planner {
     return lhs > rhs;
   }
 
-  int run(const i64* D, int32_t* Kout, int32_t* fam, int32_t* dst, int32_t* inst,
-          i64* bytes, int k_max, i64* tau_out) {
-    const size_t NN = (size_t)N * N;
-    Drem.assign(D, D + NN);
-    *Kout = 0;
+  // Take D as the residual: every entry non-negative, a whole number of
+  // units and zero on the diagonal (Sec. 3: self traffic stays local).
+  bool load(const i64* D) {
+    Drem.assign(D, D + (size_t)N * N);
     for (int i = 0; i < N; ++i)
       for (int j = 0; j < N; ++j) {
-        i64 v = Drem[(size_t)i * N + j];
-        if (v < 0 || v % P.unit != 0 || (i == j && v != 0)) return INVALID_DEMAND;
+        const i64 v = Drem[(size_t)i * N + j];
+        if (v < 0 || v % P.unit != 0 || (i == j && v != 0)) return false;
       }
-    // Global time quantum (Sec. 5 "Global execution granularity"): the most
-    // loaded rank drains in about K_target quanta at the fastest path rate.
-    i64 Lmax = 0;
+    return true;
+  }
+
+  // Global time quantum (Sec. 5 "Global execution granularity"): the most
+  // loaded rank (largest row or column sum) drains in about K_target quanta
+  // at the fastest path rate.
+  void set_quantum() {
+    i64 heaviest = 0;
     for (int i = 0; i < N; ++i) {
-      i64 row = 0, col = 0;
+      i64 out = 0, in = 0;
       for (int j = 0; j < N; ++j) {
-        row += Drem[(size_t)i * N + j];
-        col += Drem[(size_t)j * N + i];
+        out += Drem[(size_t)i * N + j];
+        in += Drem[(size_t)j * N + i];
       }
-      Lmax = std::max(Lmax, std::max(row, col));
+      heaviest = std::max(heaviest, std::max(out, in));
     }
-    i64 denom = C.bw_max * P.k_target;
-    tau = (Lmax + denom - 1) / denom;
-    if (tau < 1) tau = 1;
-    if (tau_out) *tau_out = tau;
+    const i64 per_quantum = C.bw_max * P.k_target;
+    tau = std::max<i64>(1, (heaviest + per_quantum - 1) / per_quantum);
+  }
+
+  i64 unserved() const {
+    i64 s = 0;
+    for (i64 v : Drem) s += v;
+    return s;
+  }
+
+  // Step 1 (Eq. (5), Eq. (6)): the residual summed per ordered group pair,
+  // then the shape whose lane counts weigh it most; the first such shape in
+  // canonical order, or -1 when every score is zero.
+  int pressure_argmax() const {
+    std::vector<i64> Dhat((size_t)G * G, 0);
+    for (int i = 0; i < N; ++i)
+      for (int j = 0; j < N; ++j) Dhat[(size_t)(i / g) * G + j / g] += Drem[(size_t)i * N + j];
+    int arg = -1;
+    i64 top = 0;
+    for (int m = 0; m < (int)C.shapes.size(); ++m) {
+      i64 sc = 0;
+      for (const auto& e : C.shapes[m].M)
+        sc += Dhat[(size_t)std::get<0>(e) * G + std::get<1>(e)] * std::get<2>(e);
+      if (sc > top) {
+        top = sc;
+        arg = m;
+      }
+    }
+    return arg;
+  }
+
+  // Steps 2 and 3 for one family of the chosen shape: its best binding over
+  // the starts, then the lane volumes and utility of that channel.
+  struct Candidate {
+    int f;
+    Binding b;
+    Eval e;
+  };
+  Candidate candidate_for(int f) {
+    Candidate c;
+    c.f = f;
+    c.b = multistart_aa(C.fams[f], f);
+    c.e = evaluate(C.fams[f], c.b);
+    if (cand_log && cand_n < cand_cap) {
+      const size_t w = 5 + 3 * (size_t)N;
+      i64* r = cand_log + w * (size_t)cand_n++;
+      r[0] = K; r[1] = f; r[2] = c.e.S; r[3] = c.e.xm; r[4] = c.e.bm;
+      for (int t = 0; t < (int)C.fams[f].inst.size(); ++t) {
+        r[5 + 3 * t] = c.b.src[t];
+        r[6 + 3 * t] = c.b.dst[t];
+        r[7 + 3 * t] = c.e.x[t];
+      }
+    }
+    return c;
+  }
+
+  // The activation joins the schedule and its volumes leave the residual.
+  void commit(const Candidate& c, int32_t* fam, int32_t* dst, int32_t* inst, i64* bytes) {
+    const CFamily& F = C.fams[c.f];
+    fam[K] = c.f;
+    for (int t = 0; t < (int)F.inst.size(); ++t) {
+      const int i = c.b.src[t], j = c.b.dst[t];
+      const size_t o = (size_t)K * N + i;
+      dst[o] = j;
+      inst[o] = F.inst[t].id;
+      bytes[o] = c.e.x[t];
+      Drem[(size_t)i * N + j] -= c.e.x[t];
+    }
+    ++K;
+  }
+
+  // The decomposition (Sec. 4.2): until nothing is left, pick the shape,
+  // keep the family whose candidate has the highest utility (the first in
+  // canonical order on ties) and commit it.  K_max bounds the schedule.
+  int run(const i64* D, int32_t* Kout, int32_t* fam, int32_t* dst, int32_t* inst,
+          i64* bytes, int k_max, i64* tau_out) {
+    *Kout = 0;
     K = 0;
-    auto remaining = [&]() {
-      i64 s = 0;
-      for (size_t x = 0; x < NN; ++x) s += Drem[x];
-      return s;
-    };
-    while (remaining() > 0) {
+    if (!load(D)) return INVALID_DEMAND;
+    set_quantum();
+    if (tau_out) *tau_out = tau;
+    for (;;) {
+      if (unserved() == 0) return OK;
       if (K >= k_max) return CAPACITY;
-      // Step 1: group demand, Eq. (5), and the best shape, Eq. (6).
-      std::vector<i64> Dhat((size_t)G * G, 0);
-      for (int i = 0; i < N; ++i)
-        for (int j = 0; j < N; ++j) Dhat[(size_t)(i / g) * G + j / g] += Drem[(size_t)i * N + j];
-      int Mstar = -1;
-      i64 sbest = -1;
-      for (int m = 0; m < (int)C.shapes.size(); ++m) {
-        i64 s = 0;
-        for (const auto& e : C.shapes[m].M)
-          s += Dhat[(size_t)std::get<0>(e) * G + std::get<1>(e)] * std::get<2>(e);
-        if (s > sbest) { sbest = s; Mstar = m; }
+      const int m = pressure_argmax();
+      if (m < 0) return NO_PROGRESS;
+      Candidate win;
+      bool have = false;
+      for (int f = C.shapes[m].fam_begin; f < C.shapes[m].fam_end; ++f) {
+        Candidate c = candidate_for(f);
+        if (!have || better(c.e, win.e)) {
+          win = c;
+          have = true;
+        }
       }
-      if (Mstar < 0 || sbest <= 0) return NO_PROGRESS;
-      // Steps 2-3: bind and evaluate every family of the chosen shape.
-      const CShape& sh = C.shapes[Mstar];
-      int fbest = -1;
-      Binding bbest;
-      Eval ebest;
-      for (int f = sh.fam_begin; f < sh.fam_end; ++f) {
-        Binding b = multistart_aa(C.fams[f], f);
-        Eval e = evaluate(C.fams[f], b);
-        if (fbest < 0 || better(e, ebest)) { fbest = f; bbest = b; ebest = e; }
-      }
-      if (fbest < 0 || ebest.S == 0) return NO_PROGRESS;
-      // Append E* and subtract X(E*) from D^rem.
-      const CFamily& F = C.fams[fbest];
-      fam[K] = fbest;
-      for (int t = 0; t < (int)F.inst.size(); ++t) {
-        int i = bbest.src[t], j = bbest.dst[t];
-        dst[(size_t)K * N + i] = j;
-        inst[(size_t)K * N + i] = F.inst[t].id;
-        bytes[(size_t)K * N + i] = ebest.x[t];
-        Drem[(size_t)i * N + j] -= ebest.x[t];
-      }
-      ++K;
+      if (!have || win.e.S == 0) return NO_PROGRESS;
+      commit(win, fam, dst, inst, bytes);
       *Kout = (int32_t)K;
     }
-    return OK;
   }
 };
 
@@ -1165,6 +1212,54 @@ int orc_plan(const orc_catalog* c, const int64_t* D, const orc_params* pp, int32
   int st = pl.run(D, K, fam, dst, inst, bytes, k_max, tau_out);
   if (trace_n) *trace_n = pl.trace_n;
   return st;
+}
+
+// The plan with every evaluated candidate logged, exposed for pinning the
+// selection steps: row r of `log` (5 + 3N int64) holds the iteration, the
+// family, S, the slowest lane's volume and rate, then for every instance of
+// the family in family order its source, destination and volume.
+int orc_plan_candidates(const orc_catalog* c, const int64_t* D, const orc_params* pp, int32_t k_max,
+                        int32_t* K, int32_t* fam, int32_t* dst, int32_t* inst, int64_t* bytes, int64_t* log,
+                        int64_t log_cap, int64_t* log_n) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  if (!C || !D || !pp || !log || pp->unit_bytes < 1 || pp->k_target < 1 || pp->n_start < 1 ||
+      pp->i_aa < 0 || pp->lambda_ns < 0 || k_max < 0)
+    return INVALID_ARGUMENT;
+  Params P{pp->k_target, pp->lambda_ns, pp->unit_bytes, pp->n_start, pp->i_aa, pp->seed};
+  Planner pl(*C, P);
+  pl.cand_log = log;
+  pl.cand_cap = log_cap;
+  int st = pl.run(D, K, fam, dst, inst, bytes, k_max, nullptr);
+  if (log_n) *log_n = pl.cand_n;
+  return st;
+}
+
+// One start binding of MultiStartAA before any AA sweep, exposed for
+// pinning: D is taken as the residual (its quantum as at the start of a
+// plan), `iter` is the iteration number that keys the random starts, start 0
+// is the canonical binding with the top credit triple forced in, starts >= 1
+// the shuffled ones; both are then made self-transfer free.  src[t], dst[t]:
+// the ranks bound to instance t of family f (family order).
+int orc_start_binding(const orc_catalog* c, const int64_t* D, const orc_params* pp, int64_t iter, int32_t f,
+                      int32_t start, int32_t* src, int32_t* dst) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  if (!C || !D || !pp || f < 0 || f >= (int32_t)C->fams.size() || start < 0 || pp->unit_bytes < 1 ||
+      pp->k_target < 1)
+    return INVALID_ARGUMENT;
+  Params P{pp->k_target, pp->lambda_ns, pp->unit_bytes, pp->n_start, pp->i_aa, pp->seed};
+  Planner pl(*C, P);
+  if (!pl.load(D)) return INVALID_DEMAND;
+  pl.set_quantum();
+  pl.K = iter;
+  const CFamily& F = C->fams[f];
+  std::vector<std::vector<int>> outs, ins;
+  pl.group_lists(F, outs, ins);
+  Planner::Binding b = start == 0 ? pl.start_forced(F, outs, ins) : pl.start_random(F, f, start, outs, ins);
+  for (size_t t = 0; t < F.inst.size(); ++t) {
+    src[t] = b.src[t];
+    dst[t] = b.dst[t];
+  }
+  return OK;
 }
 
 // The counter-based generator of the random AA starts, exposed for pinning:
