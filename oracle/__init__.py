@@ -82,6 +82,8 @@ def lib():
         L.orc_plan_candidates.argtypes = [vp, vp, C.POINTER(_Params), C.c_int32, vp, vp, vp, vp, vp, vp,
                                           C.c_int64, vp]
         L.orc_start_binding.argtypes = [vp, vp, C.POINTER(_Params), C.c_int64, C.c_int32, C.c_int32, vp, vp]
+        L.orc_shape_candidates.argtypes = [vp, vp, C.POINTER(_Params), C.c_int64, C.c_int32, vp, C.c_int64, vp,
+                                           vp]
         L.orc_splitmix_stream.argtypes = [C.c_uint64, vp, C.c_int32, vp]
         L.orc_utility_greater.argtypes = [C.c_int64] * 7
         L.orc_modeled_time.argtypes = [vp, C.c_int32, C.c_int32, vp, vp, C.c_int64, vp, vp]
@@ -241,6 +243,33 @@ class Catalog:
         sched = dict(status=st, K=k, family=fam[:k].copy(), dst=dst[:k].copy(), inst=inst[:k].copy(),
                      bytes=nbytes[:k].copy())
         return sched, cands
+
+    def shape_candidates(self, D: np.ndarray, unit: int, shape: int, iteration: int = 0,
+                         k_target: Optional[int] = None, lambda_ns: int = DEFAULT_LAMBDA_NS,
+                         n_start: int = DEFAULT_N_START, i_aa: int = DEFAULT_I_AA, seed: int = 0):
+        """Steps 2-3 of the planner on `shape` with D as the residual: the
+        candidates of every family of the bucket (as plan_candidates lists
+        them) and the family the planner keeps."""
+        N = self.N
+        D = np.ascontiguousarray(D, dtype=np.int64)
+        k_target = 2 * N if k_target is None else k_target
+        P = _Params(k_target, lambda_ns, unit, n_start, i_aa, seed)
+        cap = 4096
+        log = np.zeros((cap, 5 + 3 * N), np.int64)
+        ln = np.zeros(1, np.int64)
+        chosen = np.zeros(1, np.int32)
+        st = lib().orc_shape_candidates(self._h, _p(D), C.byref(P), iteration, shape, _p(log), cap, _p(ln),
+                                        _p(chosen))
+        if st != OK:
+            raise OracleError(st, "orc_shape_candidates")
+        n = int(ln[0])
+        assert n < cap
+        cands = []
+        for r in log[:n]:
+            lanes = r[5:].reshape(N, 3)
+            cands.append(dict(iter=int(r[0]), family=int(r[1]), S=int(r[2]), xm=int(r[3]), bm=int(r[4]),
+                              src=lanes[:, 0].copy(), dst=lanes[:, 1].copy(), x=lanes[:, 2].copy()))
+        return cands, int(chosen[0])
 
     def start_binding(self, D: np.ndarray, unit: int, family: int, start: int, iteration: int = 0,
                       k_target: Optional[int] = None, seed: int = 0):

@@ -861,9 +861,21 @@ struct Planner {
     ++K;
   }
 
+  // The activation a shape yields: every family's candidate, the one with
+  // the highest utility kept (the first in canonical order on ties).
+  Candidate best_candidate(int m) {
+    Candidate win;
+    win.f = -1;
+    for (int f = C.shapes[m].fam_begin; f < C.shapes[m].fam_end; ++f) {
+      Candidate c = candidate_for(f);
+      if (win.f < 0 || better(c.e, win.e)) win = c;
+    }
+    return win;
+  }
+
   // The decomposition (Sec. 4.2): until nothing is left, pick the shape,
-  // keep the family whose candidate has the highest utility (the first in
-  // canonical order on ties) and commit it.  K_max bounds the schedule.
+  // take the best activation it yields and commit it.  K_max bounds the
+  // schedule.
   int run(const i64* D, int32_t* Kout, int32_t* fam, int32_t* dst, int32_t* inst,
           i64* bytes, int k_max, i64* tau_out) {
     *Kout = 0;
@@ -876,16 +888,8 @@ struct Planner {
       if (K >= k_max) return CAPACITY;
       const int m = pressure_argmax();
       if (m < 0) return NO_PROGRESS;
-      Candidate win;
-      bool have = false;
-      for (int f = C.shapes[m].fam_begin; f < C.shapes[m].fam_end; ++f) {
-        Candidate c = candidate_for(f);
-        if (!have || better(c.e, win.e)) {
-          win = c;
-          have = true;
-        }
-      }
-      if (!have || win.e.S == 0) return NO_PROGRESS;
+      const Candidate win = best_candidate(m);
+      if (win.f < 0 || win.e.S == 0) return NO_PROGRESS;
       commit(win, fam, dst, inst, bytes);
       *Kout = (int32_t)K;
     }
@@ -1232,6 +1236,28 @@ int orc_plan_candidates(const orc_catalog* c, const int64_t* D, const orc_params
   int st = pl.run(D, K, fam, dst, inst, bytes, k_max, nullptr);
   if (log_n) *log_n = pl.cand_n;
   return st;
+}
+
+// Steps 2 and 3 on a given shape m with D as the residual (its quantum as
+// at the start of a plan; `iter` keys the random starts), exposed for
+// pinning the family choice on any bucket: every candidate is logged as by
+// orc_plan_candidates and *chosen receives the family kept.
+int orc_shape_candidates(const orc_catalog* c, const int64_t* D, const orc_params* pp, int64_t iter, int32_t m,
+                         int64_t* log, int64_t log_cap, int64_t* log_n, int32_t* chosen) {
+  const Catalog* C = reinterpret_cast<const Catalog*>(c);
+  if (!C || !D || !pp || !log || !chosen || m < 0 || m >= (int32_t)C->shapes.size() || pp->unit_bytes < 1 ||
+      pp->k_target < 1 || pp->n_start < 1 || pp->i_aa < 0 || pp->lambda_ns < 0)
+    return INVALID_ARGUMENT;
+  Params P{pp->k_target, pp->lambda_ns, pp->unit_bytes, pp->n_start, pp->i_aa, pp->seed};
+  Planner pl(*C, P);
+  if (!pl.load(D)) return INVALID_DEMAND;
+  pl.set_quantum();
+  pl.K = iter;
+  pl.cand_log = log;
+  pl.cand_cap = log_cap;
+  *chosen = pl.best_candidate(m).f;
+  if (log_n) *log_n = pl.cand_n;
+  return OK;
 }
 
 // One start binding of MultiStartAA before any AA sweep, exposed for
