@@ -279,6 +279,23 @@ vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_pa
                   int64_t* send_off, int64_t* stream_off, int32_t* recv_src, int64_t* tau,
                   int32_t* dev_status, void* ws, size_t ws_bytes, void* stream);
 
+/* vp_plan without a workspace, for callers that cannot allocate device
+ * memory around the call (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): the same arguments, decisions
+ * and outputs as vp_plan, with the residual D^rem kept in a device array
+ * that the library owns (8 * 256 * 256 bytes, one copy per device, held
+ * until the process ends).  The first call on a device looks the array up
+ * (do it once outside any capture); no call allocates.  Catalogs of more
+ * than 256 ranks return VP_ERR_UNSUPPORTED before anything is enqueued.
+ * Every call on a device shares the one array: calls that overlap on one
+ * device (other streams, other threads) race and must be serialised by the
+ * caller.  Nothing in the array needs clearing (the residual is rewritten
+ * from the demand at the start of every call). */
+vp_status vp_plan_noalloc(const vp_catalog* cat, const int64_t* demand, const vp_plan_params* p,
+                          int32_t* K, int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes,
+                          int64_t* send_off, int64_t* stream_off, int32_t* recv_src, int64_t* tau,
+                          int32_t* dev_status, void* stream);
+
 /* Several independent matrices planned side by side, one workgroup (one
  * compute unit) each, with the decisions vp_plan takes for each of them (the
  * planner is latency-bound on one CU; a batch puts the others to work, e.g.

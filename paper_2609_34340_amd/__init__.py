@@ -82,6 +82,7 @@ def lib():
     L.vp_plan_workspace.argtypes = [vp, C.POINTER(PlanParams)]
     L.vp_plan_workspace.restype = sz
     L.vp_plan.argtypes = [vp, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.vp_plan_noalloc.argtypes = [vp, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.vp_plan_batch_workspace.argtypes = [vp, C.POINTER(PlanParams), i32]
     L.vp_plan_batch_workspace.restype = sz
     L.vp_plan_batch.argtypes = [vp, i32, vp, C.POINTER(PlanParams), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
@@ -382,6 +383,26 @@ def plan(cat: Catalog, D: torch.Tensor, p: PlanParams, status: Optional[torch.Te
                          _ptr(out.get("stream_off")), _ptr(out.get("recv_src")), _ptr(out["tau"]), _ptr(status),
                          _ptr(ws), ws.numel(),
                          _stream(stream)), "vp_plan")
+    out["status"] = status
+    return out
+
+
+def plan_noalloc(cat: Catalog, D: torch.Tensor, p: PlanParams, status: Optional[torch.Tensor] = None,
+                 out: Optional[dict] = None, stream=None) -> dict:
+    """vp_plan_noalloc: vp_plan with the residual in the library's own device
+    array (no workspace; at most 256 ranks)."""
+    _dev(D, torch.int64, "demand")
+    N = cat.N
+    if tuple(D.shape) != (N, N):
+        raise ValueError("demand must be [%d, %d]" % (N, N))
+    if out is None:
+        out = alloc_schedule(N, p.k_max, D.device)
+    if status is None:
+        status = new_status(D.device)
+    _check(lib().vp_plan_noalloc(cat.handle, _ptr(D), C.byref(p), _ptr(out["K"]), _ptr(out["family"]),
+                                 _ptr(out["dst"]), _ptr(out["inst"]), _ptr(out["bytes"]), _ptr(out.get("send_off")),
+                                 _ptr(out.get("stream_off")), _ptr(out.get("recv_src")), _ptr(out["tau"]),
+                                 _ptr(status), _stream(stream)), "vp_plan_noalloc")
     out["status"] = status
     return out
 

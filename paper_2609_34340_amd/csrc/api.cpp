@@ -315,6 +315,17 @@ vp_status vp_plan(const vp_catalog* c, const int64_t* demand, const vp_plan_para
                        dev_status, ws, ws_bytes, stream);
 }
 
+vp_status vp_plan_noalloc(const vp_catalog* c, const int64_t* demand, const vp_plan_params* p, int32_t* K,
+                          int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes, int64_t* send_off,
+                          int64_t* stream_off, int32_t* recv_src, int64_t* tau, int32_t* dev_status, void* stream) {
+  if (!c) return set_error(VP_ERR_INVALID_ARGUMENT, "null catalog");
+  void* residual = nullptr;
+  const vp_status st = vp::static_residual(c->N, &residual);
+  if (st != VP_OK) return st;
+  return vp_plan_batch(c, 1, demand, p, K, family, dst, inst, bytes, send_off, stream_off, recv_src, tau,
+                       dev_status, residual, (size_t)c->N * (size_t)c->N * sizeof(int64_t), stream);
+}
+
 size_t vp_pack_workspace(int32_t k_max, int64_t send_capacity, int64_t unit_bytes, int64_t T, int32_t k) {
   if (k_max < 1 || send_capacity < 0 || unit_bytes < 1 || T < 0 || k < 0) return 0;
   return vp::pack_workspace(k_max, send_capacity, unit_bytes, T, k);

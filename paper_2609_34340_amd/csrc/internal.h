@@ -95,6 +95,10 @@ struct PlanLaunch {
   int32_t batch;   // matrices planned side by side, one workgroup each
 };
 vp_status launch_plan(const PlanLaunch& a, void* stream);
+// Ranks the library-owned residual of vp_plan_noalloc holds, and its device
+// address on the current device (looked up on the first call per device).
+constexpr int kStaticRanks = 256;
+vp_status static_residual(int32_t n_ranks, void** out);
 
 struct DemandLaunch {
   const int32_t* routing;

@@ -31,6 +31,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
+#include <string>
 
 #include "internal.h"
 
@@ -1257,6 +1259,41 @@ vp_status launch_g(const PlanArgs& P, size_t lds, hipStream_t st, int gpl) {
 }
 
 }  // namespace
+
+// ------------------------------------------------- library-owned residual
+
+// vp_plan_noalloc keeps the residual D^rem in this array instead of a
+// caller's workspace: one copy per device, held until the process ends,
+// room for kStaticRanks ranks.  Host code never passes the array's name to
+// a kernel: it passes the device address looked up below.
+static __device__ __align__(256) int64_t scratch[(size_t)kStaticRanks * kStaticRanks];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+}  // namespace
+
+vp_status static_residual(int32_t n_ranks, void** out) {
+  if (n_ranks < 1 || n_ranks > kStaticRanks)
+    return set_error(VP_ERR_UNSUPPORTED, "vp_plan_noalloc plans at most " + std::to_string(kStaticRanks) +
+                                             " ranks (its residual is a fixed device array)");
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return set_error(VP_ERR_HIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kMaxDevices) return set_error(VP_ERR_UNSUPPORTED, "device index too large");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    // once per device, with that device current: its copy's address
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return set_error(VP_ERR_HIP, std::string("hipGetSymbolAddress of the static residual failed: ") +
+                                       hipGetErrorString(e));
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return VP_OK;
+}
 
 vp_status launch_plan(const PlanLaunch& a, void* stream) {
   const vp_catalog& c = *a.cat;

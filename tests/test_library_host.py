@@ -258,3 +258,15 @@ def test_sys_rotation_time_equals_oracle(vp, topo):
     cat = vp.Catalog(topo)
     for rule, near in [(vp.ROTATION_NEAREST_PATH, True), (vp.ROTATION_DYNAMIC_PATH, False)]:
         assert cat.rotation_time(D, rule) == oracle.rotation_time(topo, D, near)
+
+
+def test_plan_noalloc_refuses_more_than_256_ranks(vp):
+    """The library-owned residual holds 256 ranks: a 1,024-rank catalog is
+    refused on the host before any device call (no GPU needed)."""
+    import ctypes as C
+    cat = vp.Catalog(vpgen.Topology(128))
+    p = vp.plan_params(cat.N, 4096)
+    st = vp.lib().vp_plan_noalloc(cat.handle, None, C.byref(p), None, None, None, None, None, None, None, None,
+                                  None, None, None)
+    assert st == vp.UNSUPPORTED
+    assert b"256" in vp.lib().vp_last_error()
