@@ -318,7 +318,7 @@ def extra_demand(vp, case, matrix, dev):
 def extra_section(dev, reps=3):
     """Planner on the uniform, skew (pairwise Zipf) and head/context demands,
     with the full catalog and with the nearest-path catalog of the peer/path
-    ablation (Sec. 6.4, Table 3: demand-aware peers, fixed nearest path).
+    ablation (Sec. 6.3, Table 3: demand-aware peers, fixed nearest path).
     Per case: plan us per matrix (HIP events, mean of `reps` runs per
     matrix), K and the modeled completion time T of Eq. (2); the ablation
     ratios put T of the nearest-path plan and of the fixed cyclic rotation

@@ -129,7 +129,7 @@ vp_status vp_catalog_shapes(const vp_catalog* cat, int32_t* k, int32_t* fam_begi
  * and the Q*g node-local instance ids of each family, ascending. */
 vp_status vp_catalog_families(const vp_catalog* cat, int32_t* shape, int32_t* k, int32_t* ids);
 
-/* Restricted catalogs for the peer/path ablation (Sec. 6.4, Table 3): a new
+/* Restricted catalogs for the peer/path ablation (Sec. 6.3, Table 3): a new
  * handle holding the families of `cat` that satisfy `rule`, in the same
  * canonical order.  VP_RESTRICT_NEAREST_PATH keeps the families in which
  * every lane takes its group pair's nearest path (PIX inside a switch, PXB
@@ -479,7 +479,7 @@ vp_status vp_unpack_combine(const void* recv, int64_t recv_capacity, int64_t row
 vp_status vp_modeled_time(const vp_catalog* cat, int32_t K, const int32_t* inst,
                           const int64_t* bytes, int64_t lambda_ns, int64_t* num, int64_t* den);
 
-/* Modeled completion time of a fixed cyclic peer rotation (Sec. 6.4, Table 3
+/* Modeled completion time of a fixed cyclic peer rotation (Sec. 6.3, Table 3
  * "fixed peer rotation"), the baseline the demand-aware planner is compared
  * with, on the topology of `cat`: stage s = 1..N-1 pairs rank i with rank
  * (i + s) mod N and moves all of D_i,(i+s) (demand: host int64 [N, N]);

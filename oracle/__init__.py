@@ -116,7 +116,7 @@ class OracleError(RuntimeError):
 class Catalog:
     """Oracle catalog (node-circulant, or the full Alg. 1 catalog with full=True);
     nearest=True keeps only families whose lanes all take their group pair's
-    nearest path (the "fixed nearest path" ablation of Sec. 6.4)."""
+    nearest path (the "fixed nearest path" ablation of Sec. 6.3)."""
 
     def __init__(self, topo, full: bool = False, nearest: bool = False):
         t = _topo(topo)
@@ -353,7 +353,7 @@ def receive_counts(words: np.ndarray, signal: np.ndarray, n_local: int) -> np.nd
 
 
 def rotation_time(topo, D: np.ndarray, nearest: bool, lambda_ns: int = DEFAULT_LAMBDA_NS):
-    """Exact (num, den) ns of the fixed cyclic peer rotation on D (Sec. 6.4)."""
+    """Exact (num, den) ns of the fixed cyclic peer rotation on D (Sec. 6.3)."""
     t = _topo(topo)
     Dc = np.ascontiguousarray(D, np.int64)
     num, den = np.zeros(1, np.int64), np.zeros(1, np.int64)

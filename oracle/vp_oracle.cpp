@@ -337,7 +337,7 @@ struct Catalog {
   i64 bw_max;
 };
 
-// The nearest path of an ordered group pair (Sec. 6.4 peer/path ablation,
+// The nearest path of an ordered group pair (Sec. 6.3 peer/path ablation,
 // "fixed nearest path"): PIX inside a switch, PXB between two switches of one
 // socket, SYS between sockets of one node when enabled, the NICs otherwise.
 // A family keeps only lanes on their pair's nearest path; under the topology
@@ -1110,7 +1110,7 @@ int orc_receive_counts(const uint32_t* words, const int32_t* signal, int32_t N, 
 }
 
 // Fixed cyclic peer rotation, the baseline of the peer/path ablation
-// (Sec. 6.4, Table 3).  Stage s = 1..N-1: rank i sends all of D_i,(i+s mod N)
+// (Sec. 6.3, Table 3).  Stage s = 1..N-1: rank i sends all of D_i,(i+s mod N)
 // at once; empty stages are skipped.  Each lane uses its pair's nearest path
 // (nearest = 1) or, per stage, the path vector that ends the stage first
 // (nearest = 0), every vector tried.  Lanes sharing a directed resource

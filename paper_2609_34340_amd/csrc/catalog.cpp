@@ -308,7 +308,7 @@ vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
   return VP_OK;
 }
 
-// Restricted catalogs for the peer/path ablation (Sec. 6.4): rule 1 keeps the
+// Restricted catalogs for the peer/path ablation (Sec. 6.3): rule 1 keeps the
 // families in which every lane takes its group pair's nearest path (PIX in a
 // switch, PXB between two switches of one socket, SYS between sockets when
 // enabled, the NICs otherwise), i.e. drops every family with a NIC lane

@@ -1,5 +1,5 @@
 // Modeled completion time of a fixed cyclic peer rotation, the baseline of
-// the peer/path ablation (Sec. 6.4, Table 3: "fixed peer rotation").
+// the peer/path ablation (Sec. 6.3, Table 3: "fixed peer rotation").
 //
 // Stage s = 1 .. N-1 pairs rank i with rank (i + s) mod N and moves the whole
 // D_i,(i+s) at once; a stage whose lanes carry nothing is skipped.  A lane's

@@ -1,4 +1,4 @@
-"""Pins of the oracle's fixed-rotation model (Sec. 6.4 peer/path ablation,
+"""Pins of the oracle's fixed-rotation model (Sec. 6.3 peer/path ablation,
 Table 3 "fixed peer rotation"): hand-worked stage times with shared links,
 the contention-free single-switch closed form, and the order of the two path
 rules."""

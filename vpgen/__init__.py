@@ -223,7 +223,7 @@ def head_split(heads: int, n_ranks: int) -> np.ndarray:
 # ---------------------------------------------------------------------------
 # Demand matrices given directly (AlltoAll / AlltoAllv microbenchmarks) and
 # the Wan2.1 head/context layouts (Sec. 6 "Workloads", skew AlltoAllv,
-# Sec. 6.2 Wan2.1, Sec. 6.4 ablation).  Only inputs: byte volumes drawn or
+# Sec. 6.2 Wan2.1, Sec. 6.3 ablation).  Only inputs: byte volumes drawn or
 # laid out here are what a caller asks the scheduler to move.
 # ---------------------------------------------------------------------------
 
