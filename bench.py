@@ -163,6 +163,24 @@ def measure(w, steps, warmup, M, dev):
              prep_ms=np.array([e[3].elapsed_time(e[4]) for e in evs]),
              gather_ms=np.array([e[4].elapsed_time(e[5]) for e in evs]))
 
+    # one rank's own row (R = 1: its routing, counts, demand row and sort),
+    # the unit each rank runs in deployment; mean of 20 calls, HIP events
+    if w.mode == "moe":
+        r1 = routing[0][:1].contiguous()
+        ws1 = torch.zeros(max(vp.demand_workspace_bytes(1, w.tokens, w.top_k, w.experts), 1), dtype=torch.uint8,
+                          device=dev)
+        o1 = vp.demand(r1, w.n_ranks, w.experts, w.row_bytes, sort_row=0, ws=ws1)
+        a, b = E(), E()
+        a.record()
+        for _ in range(20):
+            vp.demand(r1, w.n_ranks, w.experts, w.row_bytes, sort_row=0, ws=ws1, out=o1, status=o1["status"])
+        b.record()
+        torch.cuda.synchronize()
+        if vp.read_status(o1["status"]) != 0:
+            raise SystemExit("device error in the one-rank demand")
+        r["demand_r1_ms"] = a.elapsed_time(b) / 20
+        del r1, ws1, o1
+
     # schedule facts per matrix (untimed): K, slices, modeled completion time
     Ks, slices, That = [], [], []
     for m in range(M):
@@ -391,6 +409,7 @@ def summary(w, r):
             "modeled_T_ms": round(float(r["That_ms"].mean()), 3),
             "plan_over_modeled_T": round(plan_us / (1e3 * float(r["That_ms"].mean())), 5),
             "demand_us": round(float(r["demand_ms"].mean() * 1e3), 1),
+            "demand_one_rank_us": round(float(r["demand_r1_ms"] * 1e3), 1) if "demand_r1_ms" in r else None,
             "control_words_us": round(float(r["words_ms"].mean() * 1e3), 1) if w.mode == "moe" else None,
             "pack_us": round(float(r["pack_ms"].mean() * 1e3), 1),
             "pack_GBps": round(value, 2), "pack_pct_of_peak": round(100 * value / PEAK_HBM_GBS, 2),
@@ -476,6 +495,7 @@ def main():
         "plan_us_per_matrix": head["plan_us_per_matrix"],
         "plan_us_per_activation": head["plan_us_per_activation"],
         "demand_us": head["demand_us"],
+        "demand_one_rank_us": head["demand_one_rank_us"],
         "control_words_us": head["control_words_us"],
         "pack_us": head["pack_us"],
         "pack_us_median": head["pack_us_median"],

@@ -171,8 +171,11 @@ void vp_catalog_free(vp_catalog* cat);
 
 /* ----------------------------------------------------------------- demand */
 
-/* Workspace bytes for vp_demand with `T` tokens, top-`k`, `E` experts. */
-size_t vp_demand_workspace(int64_t T, int32_t k, int32_t E);
+/* Workspace bytes for vp_demand over `R` rows of `T` tokens, top-`k`, `E`
+ * experts: the partial expert counts of each part of each row and the
+ * sorted row's chunk counts.  It needs no clearing; calls that share a
+ * workspace must not overlap.  Returns 0 for bad sizes. */
+size_t vp_demand_workspace(int32_t R, int64_t T, int32_t k, int32_t E);
 
 /* Demand rows from routing (Sec. 3 model setup; one row copy per (token,
  * expert) assignment, Sec. 5 sparse EP).  For R source ranks

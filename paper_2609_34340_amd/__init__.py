@@ -71,7 +71,7 @@ def lib():
     L.vp_catalog_load.argtypes = [vp, sz, C.POINTER(vp)]
     L.vp_catalog_free.argtypes = [vp]
     L.vp_catalog_free.restype = None
-    L.vp_demand_workspace.argtypes = [i64, i32, i32]
+    L.vp_demand_workspace.argtypes = [i32, i64, i32, i32]
     L.vp_demand_workspace.restype = sz
     L.vp_demand.argtypes = [vp, i32, i64, i32, i32, i32, i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.vp_demand_heads.argtypes = [i64, vp, i64, i32, i32, i32, vp, vp, vp]
@@ -261,8 +261,8 @@ def read_status(status: torch.Tensor) -> int:
 
 # ---------------------------------------------------------------- demand
 
-def demand_workspace_bytes(T: int, k: int, E: int) -> int:
-    return int(lib().vp_demand_workspace(T, k, E))
+def demand_workspace_bytes(R: int, T: int, k: int, E: int) -> int:
+    return int(lib().vp_demand_workspace(R, T, k, E))
 
 
 def demand(routing: torch.Tensor, n_ranks: int, n_experts: int, unit: int, first_rank: int = 0,
@@ -282,9 +282,9 @@ def demand(routing: torch.Tensor, n_ranks: int, n_experts: int, unit: int, first
                    dest_off=torch.empty(n_ranks + 1, dtype=torch.int64, device=dev))
     if status is None:
         status = new_status(dev)
-    wsb = demand_workspace_bytes(T, k, n_experts)
+    wsb = demand_workspace_bytes(R, T, k, n_experts)
     if ws is None:
-        ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+        ws = torch.zeros(max(wsb, 1), dtype=torch.uint8, device=dev)
     _check(lib().vp_demand(_ptr(routing), R, T, k, n_experts, n_ranks, first_rank, sort_row, unit,
                            _ptr(out["counts"]), _ptr(out["demand"]), _ptr(out["sorted_tok"]),
                            _ptr(out.get("sorted_slot")), _ptr(out["dest_off"]), _ptr(status), _ptr(ws),
@@ -617,7 +617,7 @@ class Pipeline:
                             sorted_tok=torch.empty(max(tokens * top_k, 1), dtype=torch.int32, device=dev),
                             sorted_slot=torch.empty(max(tokens * top_k, 1), dtype=torch.uint8, device=dev),
                             dest_off=torch.empty(N + 1, dtype=torch.int64, device=dev))
-            self.dem_ws = torch.empty(max(demand_workspace_bytes(tokens, top_k, n_experts), 1),
+            self.dem_ws = torch.zeros(max(demand_workspace_bytes(N, tokens, top_k, n_experts), 1),
                                       dtype=torch.uint8, device=dev)
             self.words = torch.empty((N, N), dtype=torch.int32, device=dev)
             cap = tokens * top_k * unit

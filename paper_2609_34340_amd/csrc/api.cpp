@@ -210,9 +210,9 @@ void vp_catalog_free(vp_catalog* c) {
   delete c;
 }
 
-size_t vp_demand_workspace(int64_t T, int32_t k, int32_t E) {
-  if (T < 0 || k < 1 || E < 1) return 0;
-  return vp::demand_workspace(T, k, E);
+size_t vp_demand_workspace(int32_t R, int64_t T, int32_t k, int32_t E) {
+  if (R < 1 || T < 0 || k < 1 || E < 1) return 0;
+  return vp::demand_workspace(R, T, k, E);
 }
 
 vp_status vp_demand(const int32_t* routing, int32_t R, int64_t T, int32_t k, int32_t E,
@@ -229,7 +229,7 @@ vp_status vp_demand(const int32_t* routing, int32_t R, int64_t T, int32_t k, int
     return set_error(VP_ERR_INVALID_ARGUMENT, "null pointer");
   if (sort_row >= 0 && ((T > 0 && !sorted_tok) || !dest_off))
     return set_error(VP_ERR_INVALID_ARGUMENT, "null sort output");
-  if (ws_bytes < vp::demand_workspace(T, k, E) || (!ws && ws_bytes))
+  if (ws_bytes < vp::demand_workspace(R, T, k, E) || !ws)
     return set_error(VP_ERR_INVALID_ARGUMENT, "workspace too small");
   vp::DemandLaunch a{routing, R, T, k, E, n_ranks, first_rank, sort_row, unit_bytes, counts, demand,
                      sorted_tok, sorted_slot, dest_off, dev_status, ws, ws_bytes};

@@ -4,16 +4,21 @@
 // (Sec. 5 buffer layout: the pack groups rows by destination).
 //
 // Kernels
-//   hist_rows     one block per source rank; LDS-privatised histogram of its
-//                 T*k expert ids, then the rank's demand row.
-//   sort_count    one block per 1024-id chunk of the sorted rank's ids:
-//                 per-chunk expert counts, written expert-major.
-//   sort_scan     one block: exclusive scan of the expert-major counts (one
-//                 contiguous segment per thread), the destination offsets.
-//   sort_scatter  one block per chunk: every id's stable rank inside its
-//                 wave's 256 ids from a wave-wide match mask built with one
-//                 ballot per bit of the expert id plus a prefix popcount,
-//                 then the waves' counts scanned per expert.
+//   demand_count   pass 1: every row's ids split over many workgroups, each
+//                  counting its part in per-wavefront LDS histograms and
+//                  writing the part's expert counts; the same launch counts
+//                  the sorted row per 2048-id chunk (expert-major).
+//   sort_scan      only for sorted rows of more than 64 chunks: one
+//                  workgroup turns the chunk counts into offsets.
+//   demand_finish  pass 2: one workgroup per row sums its parts into the
+//                  row's counts and demand row; one workgroup per sort chunk
+//                  derives the chunk's offsets from all chunk counts (expert
+//                  totals, a block scan, the earlier chunks' counts) and
+//                  places its ids: a stable rank inside each wave's ids from
+//                  a match mask built with one ballot per bit of the expert
+//                  id plus a prefix popcount, then the waves' counts scanned
+//                  per expert.
+//   No workgroup waits for another: the kernel boundary publishes pass 1.
 //   control_words / receive_counts  the sparse expert-parallel control word
 //                 of every (source, destination) pair from the counts, and
 //                 its decode at the receiver.
@@ -24,9 +29,12 @@
 namespace vp {
 namespace {
 
-constexpr int kSortThreads = 256;     // threads per block of the counting sort
-constexpr int kPerThread = 4;         // ids per thread
-constexpr int kChunk = kSortThreads * kPerThread;   // ids per block
+constexpr int kThreads = 256;                    // threads of every demand workgroup
+constexpr int kWaves = kThreads / 64;
+constexpr int kPerThread = 8;                    // ids per thread of a sort chunk
+constexpr int kChunk = kThreads * kPerThread;    // ids per sort chunk (2048)
+constexpr int kInBlockScan = 64;                 // sort chunks up to which each scatter
+                                                 // workgroup derives its own offsets
 
 __device__ inline void report(int32_t* status, int code) { atomicCAS(status, 0, code); }
 
@@ -36,82 +44,112 @@ __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__global__ void __launch_bounds__(1024) hist_rows(const int32_t* __restrict__ routing, int64_t Tk,
-                                                  int32_t E, int32_t N, int32_t first_rank,
-                                                  int64_t unit, int32_t* __restrict__ counts,
-                                                  int64_t* __restrict__ demand, int32_t* status) {
-  extern __shared__ int32_t hist[];
-  const int r = blockIdx.x;
-  for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = 0;
-  __syncthreads();
-  const int32_t* row = routing + (size_t)r * Tk;
-  bool bad = false;
-  // 16-byte loads of four ids where the row is 16-byte aligned
-  const int64_t nv = ((((uintptr_t)row) & 15) == 0) ? Tk / 4 : 0;
-  const int4* row4 = (const int4*)row;
-  for (int64_t v = threadIdx.x; v < nv; v += blockDim.x) {
-    int4 q = row4[v];
-    int ids[4] = {q.x, q.y, q.z, q.w};
-    for (int m = 0; m < 4; ++m) {
-      if ((unsigned)ids[m] < (unsigned)E) atomicAdd(&hist[ids[m]], 1);
-      else bad = true;
+struct DemandArgs {
+  const int32_t* routing;
+  int64_t Tk, part, unit;
+  int32_t E, N, first_rank, R, P, sort_row, nch, nch4, k, bits;
+  uint64_t k_magic;     // ceil(2^40 / k): token of assignment x = mulhi(x << 24, k_magic)
+  bool scanned;         // a scan kernel has turned the chunk counts into offsets
+  int32_t* counts;
+  int64_t* demand;
+  int32_t* sorted_tok;
+  uint8_t* sorted_slot;
+  int64_t* dest_off;
+  int32_t* partials;    // [R][P][E] expert counts of each part of each row
+  int32_t* ccount;      // [E][nch4] counts of the sorted row's chunks (zero past nch)
+  int32_t* status;
+};
+
+// Counts the ids [lo, hi) into an LDS histogram (16-byte loads of four ids
+// where the range is aligned, four loads in flight per thread).
+__device__ inline void count_ids(const int32_t* __restrict__ ids, int64_t lo, int64_t hi, int32_t E,
+                                 int32_t* hist, bool& bad) {
+  int64_t v1 = lo;
+  if ((((uintptr_t)(ids + lo)) & 15) == 0) v1 = lo + (hi - lo) / 4 * 4;
+  const int4* q4 = (const int4*)(ids + lo);
+  const int64_t nv = (v1 - lo) / 4;
+  for (int64_t v = threadIdx.x; v < nv; v += 4 * kThreads) {
+    int4 q[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (v + u * kThreads < nv) q[u] = q4[v + u * kThreads];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (v + u * kThreads >= nv) break;
+      const int e4[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        if ((unsigned)e4[m] < (unsigned)E) atomicAdd(&hist[e4[m]], 1);
+        else bad = true;
+      }
     }
   }
-  for (int64_t x = nv * 4 + threadIdx.x; x < Tk; x += blockDim.x) {
-    int e = row[x];
+  for (int64_t x = v1 + threadIdx.x; x < hi; x += kThreads) {
+    const int e = ids[x];
     if ((unsigned)e < (unsigned)E) atomicAdd(&hist[e], 1);
     else bad = true;
   }
-  if (bad) report(status, VP_ERR_INVALID_ARGUMENT);
+}
+
+// Pass 1.  Workgroups [0, nsort) count the sorted row's 2048-id chunks
+// (expert-major, the last one also zeroes the padding up to nch4);
+// workgroups after them count one part of one row each.  Every workgroup
+// keeps one LDS histogram per wavefront.
+__global__ void __launch_bounds__(kThreads) demand_count(DemandArgs a) {
+  extern __shared__ int32_t sh[];   // kWaves * E
+  const int tid = threadIdx.x, w = tid >> 6, E = a.E;
+  const int nsort = a.sort_row >= 0 ? a.nch : 0;
+  const int b = blockIdx.x;
+  const bool sort_blk = b < nsort;
+  int r, p;
+  int64_t lo;
+  if (sort_blk) {
+    r = a.sort_row;
+    p = b;
+    lo = (int64_t)p * kChunk;
+  } else {
+    r = (b - nsort) / a.P;
+    p = (b - nsort) - r * a.P;
+    lo = (int64_t)p * a.part;
+  }
+  const int64_t hi = min(a.Tk, lo + (sort_blk ? (int64_t)kChunk : a.part));
+  lo = min(lo, hi);
+  for (int e = tid; e < kWaves * E; e += kThreads) sh[e] = 0;
   __syncthreads();
-  for (int e = threadIdx.x; e < E; e += blockDim.x) counts[(size_t)r * E + e] = hist[e];
-  const int eloc = E / N, self = first_rank + r;
-  for (int j = threadIdx.x; j < N; j += blockDim.x) {
-    int64_t c = 0;
-    for (int e = j * eloc; e < (j + 1) * eloc; ++e) c += hist[e];
-    demand[(size_t)r * N + j] = j == self ? 0 : c * unit;
+  bool bad = false;
+  count_ids(a.routing + (size_t)r * a.Tk, lo, hi, E, sh + w * E, bad);
+  if (bad && !sort_blk) report(a.status, VP_ERR_INVALID_ARGUMENT);
+  __syncthreads();
+  for (int e = tid; e < E; e += kThreads) {
+    int32_t c = 0;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) c += sh[v * E + e];
+    if (sort_blk) {
+      int32_t* q = a.ccount + (size_t)e * a.nch4;
+      q[p] = c;
+      if (p == a.nch - 1)
+        for (int x = a.nch; x < a.nch4; ++x) q[x] = 0;
+    } else {
+      a.partials[((size_t)r * a.P + p) * E + e] = c;
+    }
   }
 }
 
-// Counting sort of one rank's ids, chunks of kChunk ids, one block per
-// chunk.  Counts are laid out ccount[e * n_chunks + chunk].
-__global__ void __launch_bounds__(kSortThreads) sort_count(const int32_t* __restrict__ ids, int64_t Tk,
-                                                          int32_t E, int32_t n_chunks,
-                                                          int32_t* __restrict__ ccount) {
-  extern __shared__ int32_t h[];   // E
-  const int tid = threadIdx.x, chunk = blockIdx.x;
-  for (int e = tid; e < E; e += kSortThreads) h[e] = 0;
-  __syncthreads();
-  const int64_t b = (int64_t)chunk * kChunk;
-  int ev[kPerThread];
-#pragma unroll
-  for (int m = 0; m < kPerThread; ++m) {
-    const int64_t x = b + tid + m * kSortThreads;
-    ev[m] = x < Tk ? ids[x] : -1;
-  }
-#pragma unroll
-  for (int m = 0; m < kPerThread; ++m)
-    if ((unsigned)ev[m] < (unsigned)E) atomicAdd(&h[ev[m]], 1);
-  __syncthreads();
-  for (int e = tid; e < E; e += kSortThreads) ccount[(size_t)e * n_chunks + chunk] = h[e];
-}
-
-// Exclusive scan of the E * n_chunks counts (expert-major) in one block:
-// tiles of 4096 counts, each thread a coalesced run of four, up to eight
-// tiles loaded ahead.  Counts and offsets fit 32 bits (at most T*k).
+// One workgroup scans all chunk counts (expert-major) into offsets, for
+// sorted rows of more than kInBlockScan chunks: tiles of 4096 counts, each
+// thread a coalesced run of four, eight tiles loaded ahead.
 __global__ void __launch_bounds__(1024) sort_scan(int32_t* __restrict__ ccount, int64_t total, int32_t E,
-                                                  int32_t N, int32_t n_chunks, int64_t* __restrict__ dest_off) {
+                                                  int32_t N, int32_t nch4, int64_t* __restrict__ dest_off) {
   constexpr int V = 4, TB = 8;
   __shared__ int32_t wsum[16];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   int32_t carry = 0;
-  const bool vec = (((uintptr_t)ccount) & 15) == 0;
   for (int64_t b0 = 0; b0 < total; b0 += (int64_t)1024 * V * TB) {
     int32_t v[TB][V];
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) {
       const int64_t x = b0 + ((int64_t)tb * 1024 + tid) * V;
-      if (vec && x + V <= total) {
+      if (x + V <= total) {
         const int4 q = *(const int4*)(ccount + x);
         v[tb][0] = q.x; v[tb][1] = q.y; v[tb][2] = q.z; v[tb][3] = q.w;
       } else {
@@ -148,27 +186,126 @@ __global__ void __launch_bounds__(1024) sort_scan(int32_t* __restrict__ ccount, 
   __syncthreads();
   // destination j opens at the first chunk of expert j*eloc
   const int eloc = E / N;
-  for (int j = tid; j < N; j += 1024) dest_off[j] = ccount[(size_t)j * eloc * n_chunks];
+  for (int j = tid; j < N; j += 1024) dest_off[j] = ccount[(size_t)j * eloc * nch4];
   if (tid == 0) dest_off[N] = carry;
 }
 
-// Stable scatter of one chunk: wave v ranks the ids [v*64*kPerThread, ...)
-// of the chunk with one ballot per id bit (a match mask) and a prefix
-// popcount; the waves' counts are then scanned per expert.
-__global__ void __launch_bounds__(kSortThreads) sort_scatter(const int32_t* __restrict__ ids, int64_t Tk,
-                                                            int32_t k, int32_t E, int32_t n_chunks,
-                                                            int32_t bits, const int32_t* __restrict__ coff,
-                                                            int32_t* __restrict__ sorted_tok,
-                                                            uint8_t* __restrict__ sorted_slot) {
-  extern __shared__ int32_t wc[];    // [kSortThreads / 64][E]
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, chunk = blockIdx.x;
-  constexpr int kW = kSortThreads / 64;
+// Exclusive scan over the block of n values in LDS (n <= 16 * kThreads):
+// each thread a contiguous run; returns the total.
+__device__ inline int32_t block_excl_scan(int32_t* v, int n, int32_t* wtot) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int per = (n + kThreads - 1) / kThreads;
+  const int e0 = min(n, tid * per), e1 = min(n, e0 + per);
+  int32_t own = 0;
+  for (int e = e0; e < e1; ++e) own += v[e];
+  int32_t incl = own;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) wtot[w] = incl;
+  __syncthreads();
+  int32_t run = incl - own, all = 0;
+  for (int u = 0; u < kWaves; ++u) {
+    if (u < w) run += wtot[u];
+    all += wtot[u];
+  }
+  for (int e = e0; e < e1; ++e) {
+    const int32_t x = v[e];
+    v[e] = run;
+    run += x;
+  }
+  __syncthreads();
+  return all;
+}
+
+// Pass 2.  Workgroup c < nch places the ids of sort chunk c; the R
+// workgroups after them merge their row's parts into its counts and demand
+// row.  A chunk's
+// offsets: expert e starts at the total of the experts below e plus the
+// counts of e in the chunks before c (each workgroup reads every chunk
+// count, or the scan kernel's offsets for long rows).  Inside the chunk,
+// wave v ranks the ids [v*64*kPerThread, ...) with one ballot per id bit
+// (a match mask) and a prefix popcount; the waves' counts are then scanned
+// per expert.
+__global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
+  extern __shared__ int32_t sh[];   // rows: E; chunks: off [E], tot [E], wc [kWaves][E]
+  __shared__ int32_t wtot[kWaves];
+  const int tid = threadIdx.x, E = a.E;
+  // the sort chunks, whose ranking is the longest work, come first
+  const int nsort = a.sort_row >= 0 ? a.nch : 0;
+  const int b = blockIdx.x;
+  if (b >= nsort) {
+    const int r = b - nsort;
+    const int32_t* q = a.partials + (size_t)r * a.P * E;
+    for (int e = tid; e < E; e += kThreads) {
+      // loads of 16 parts issued together, then summed
+      int32_t c = 0;
+      for (int pp = 0; pp < a.P; pp += 16) {
+        int32_t v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = pp + u < a.P ? q[(size_t)(pp + u) * E + e] : 0;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) c += v[u];
+      }
+      a.counts[(size_t)r * E + e] = c;
+      sh[e] = c;
+    }
+    __syncthreads();
+    const int eloc = E / a.N, self = a.first_rank + r;
+    for (int j = tid; j < a.N; j += kThreads) {
+      int64_t c = 0;
+      for (int e = j * eloc; e < (j + 1) * eloc; ++e) c += sh[e];
+      a.demand[(size_t)r * a.N + j] = j == self ? 0 : c * a.unit;
+    }
+    return;
+  }
+  const int chunk = b;
+  const int lane = tid & 63, w = tid >> 6;
+  int32_t* off = sh;
+  int32_t* tot = sh + E;
+  int32_t* wc = sh + 2 * E;
+  const int32_t* ids = a.routing + (size_t)a.sort_row * a.Tk;
+  // the chunk's ids first: their loads overlap the offsets' work
   const int64_t base = (int64_t)chunk * kChunk + (int64_t)w * 64 * kPerThread;
   int ev[kPerThread];
 #pragma unroll
   for (int m = 0; m < kPerThread; ++m) {
     const int64_t x = base + m * 64 + lane;
-    ev[m] = x < Tk ? ids[x] : -1;
+    ev[m] = x < a.Tk ? ids[x] : -1;
+  }
+  if (a.scanned) {
+    for (int e = tid; e < E; e += kThreads) off[e] = a.ccount[(size_t)e * a.nch4 + chunk];
+  } else {
+    for (int e = tid; e < E; e += kThreads) {
+      // this expert's counts of every chunk: up to 16 loads of four in
+      // flight (at most kInBlockScan chunks)
+      const int4* q = (const int4*)(a.ccount + (size_t)e * a.nch4);
+      const int n4 = a.nch4 / 4;
+      int4 v[kInBlockScan / 4];
+#pragma unroll
+      for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) v[c4] = c4 < n4 ? q[c4] : make_int4(0, 0, 0, 0);
+      int32_t all = 0, before = 0;
+#pragma unroll
+      for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) {
+        const int32_t x4[4] = {v[c4].x, v[c4].y, v[c4].z, v[c4].w};
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          all += x4[m];
+          before += 4 * c4 + m < chunk ? x4[m] : 0;
+        }
+      }
+      tot[e] = all;
+      off[e] = before;
+    }
+    __syncthreads();
+    const int32_t total = block_excl_scan(tot, E, wtot);
+    for (int e = tid; e < E; e += kThreads) off[e] += tot[e];
+    if (chunk == 0) {
+      const int eloc = E / a.N;
+      for (int j = tid; j < a.N; j += kThreads) a.dest_off[j] = tot[j * eloc];
+      if (tid == 0) a.dest_off[a.N] = total;
+    }
   }
   int32_t* mine = wc + w * E;
   for (int e = lane; e < E; e += 64) mine[e] = 0;
@@ -180,7 +317,7 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter(const int32_t* __re
     const int e = ev[m];
     const bool ok = (unsigned)e < (unsigned)E;
     uint64_t same = __ballot(ok);
-    for (int bt = 0; bt < bits; ++bt) {
+    for (int bt = 0; bt < a.bits; ++bt) {
       const uint64_t ones = __ballot(ok && ((e >> bt) & 1));
       same &= ((e >> bt) & 1) ? ones : ~ones;
     }
@@ -190,9 +327,9 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter(const int32_t* __re
     wave_sync();
   }
   __syncthreads();
-  for (int e = tid; e < E; e += kSortThreads) {
-    int32_t acc = coff[(size_t)e * n_chunks + chunk];
-    for (int v = 0; v < kW; ++v) {
+  for (int e = tid; e < E; e += kThreads) {
+    int32_t acc = off[e];
+    for (int v = 0; v < kWaves; ++v) {
       const int32_t c = wc[v * E + e];
       wc[v * E + e] = acc;
       acc += c;
@@ -203,9 +340,11 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter(const int32_t* __re
   for (int m = 0; m < kPerThread; ++m) {
     const int e = ev[m];
     if ((unsigned)e < (unsigned)E) {
-      const int64_t x = base + m * 64 + lane, t = x / k;
-      sorted_tok[mine[e] + rk[m]] = (int32_t)t;
-      if (sorted_slot) sorted_slot[mine[e] + rk[m]] = (uint8_t)(x - t * k);
+      // x < 2^31 and k < 256: the multiply-high quotient is exact
+      const uint32_t x = (uint32_t)(base + m * 64 + lane);
+      const uint32_t t = (uint32_t)__umul64hi((uint64_t)x << 24, a.k_magic);
+      a.sorted_tok[mine[e] + rk[m]] = (int32_t)t;
+      if (a.sorted_slot) a.sorted_slot[mine[e] + rk[m]] = (uint8_t)(x - t * (uint32_t)a.k);
     }
   }
 }
@@ -273,32 +412,61 @@ __global__ void __launch_bounds__(256) receive_counts_kernel(const uint32_t* __r
 
 int n_chunks_of(int64_t Tk) { return (int)((Tk + kChunk - 1) / kChunk); }
 
+// Ids per histogram part: kThreads * 2^s with s in [2, 5], the largest that
+// still gives about 2,048 workgroups for the whole launch.
+int64_t part_of(int32_t R, int64_t Tk) {
+  int64_t part = (int64_t)kThreads * 4;
+  while (part < (int64_t)kThreads * 32 && (int64_t)R * ((Tk + 2 * part - 1) / (2 * part)) >= 2048) part *= 2;
+  return part;
+}
+
+// Split of a call: ids per part, parts per row, sort chunks (and padded to 4).
+struct DemandWs {
+  int64_t part;
+  int32_t P, nch, nch4;
+};
+DemandWs demand_ws(int32_t R, int64_t T, int32_t k) {
+  DemandWs w;
+  const int64_t Tk = T * k;
+  w.part = part_of(R, Tk);
+  w.P = (int32_t)std::max<int64_t>(1, (Tk + w.part - 1) / w.part);
+  w.nch = std::max(1, n_chunks_of(Tk));
+  w.nch4 = (w.nch + 3) / 4 * 4;
+  return w;
+}
+
 }  // namespace
 
-size_t demand_workspace(int64_t T, int32_t k, int32_t E) {
-  const int64_t Tk = T * k;
-  return (size_t)E * (size_t)std::max(1, n_chunks_of(Tk)) * sizeof(int32_t);
+size_t demand_workspace(int32_t R, int64_t T, int32_t k, int32_t E) {
+  const DemandWs w = demand_ws(R, T, k);
+  const size_t partials = ((size_t)R * (size_t)w.P * (size_t)E * 4 + 255) / 256 * 256;
+  return partials + (size_t)E * (size_t)w.nch4 * 4;
 }
 
 vp_status launch_demand(const DemandLaunch& a, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const int64_t Tk = a.T * a.k;
-  hipLaunchKernelGGL(hist_rows, dim3(a.R), dim3(1024), (size_t)a.E * sizeof(int32_t), s, a.routing, Tk, a.E,
-                     a.N, a.first_rank, a.unit, a.counts, a.demand, a.status);
-  if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "hist_rows launch failed");
-  if (a.sort_row < 0) return VP_OK;
-  const int32_t* ids = a.routing + (size_t)a.sort_row * Tk;
-  const int nch = std::max(1, n_chunks_of(Tk));
-  int32_t* ccount = (int32_t*)a.ws;
-  hipLaunchKernelGGL(sort_count, dim3(nch), dim3(kSortThreads), (size_t)a.E * sizeof(int32_t), s, ids, Tk, a.E,
-                     nch, ccount);
-  hipLaunchKernelGGL(sort_scan, dim3(1), dim3(1024), 0, s, ccount, (int64_t)a.E * nch, a.E, a.N, nch,
-                     a.dest_off);
+  const DemandWs w = demand_ws(a.R, a.T, a.k);
+  const size_t partials = ((size_t)a.R * (size_t)w.P * (size_t)a.E * 4 + 255) / 256 * 256;
+  char* ws = (char*)a.ws;
   int bits = 0;
   while ((1 << bits) < a.E) ++bits;
-  hipLaunchKernelGGL(sort_scatter, dim3(nch), dim3(kSortThreads), (size_t)(kSortThreads / 64) * a.E * sizeof(int32_t),
-                     s, ids, Tk, a.k, a.E, nch, bits, ccount, a.sorted_tok, a.sorted_slot);
-  if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "sort launch failed");
+  const bool sorting = a.sort_row >= 0;
+  const uint64_t k_magic = ((uint64_t(1) << 40) + (uint64_t)a.k - 1) / (uint64_t)a.k;
+  DemandArgs d{a.routing, Tk, w.part, a.unit, a.E, a.N, a.first_rank, a.R, w.P, a.sort_row, w.nch, w.nch4, a.k,
+               bits, k_magic, sorting && w.nch > kInBlockScan, a.counts, a.demand, a.sorted_tok, a.sorted_slot, a.dest_off,
+               (int32_t*)ws, (int32_t*)(ws + partials), a.status};
+  const int64_t blocks1 = (int64_t)a.R * w.P + (sorting ? w.nch : 0);
+  if (blocks1 >= ((int64_t)1 << 31)) return set_error(VP_ERR_UNSUPPORTED, "too many histogram parts");
+  hipLaunchKernelGGL(demand_count, dim3((unsigned)blocks1), dim3(kThreads), (size_t)kWaves * a.E * sizeof(int32_t),
+                     s, d);
+  if (d.scanned)
+    hipLaunchKernelGGL(sort_scan, dim3(1), dim3(1024), 0, s, d.ccount, (int64_t)a.E * w.nch4, a.E, a.N, w.nch4,
+                       a.dest_off);
+  const int64_t blocks2 = (int64_t)a.R + (sorting ? w.nch : 0);
+  hipLaunchKernelGGL(demand_finish, dim3((unsigned)blocks2), dim3(kThreads),
+                     (size_t)(2 + kWaves) * a.E * sizeof(int32_t), s, d);
+  if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "demand launch failed");
   return VP_OK;
 }
 

@@ -115,7 +115,7 @@ struct DemandLaunch {
   void* ws;
   size_t ws_bytes;
 };
-size_t demand_workspace(int64_t T, int32_t k, int32_t E);
+size_t demand_workspace(int32_t R, int64_t T, int32_t k, int32_t E);
 vp_status launch_demand(const DemandLaunch& a, void* stream);
 vp_status launch_control_words(const int32_t* counts, int32_t R, int32_t E, int32_t N, int32_t first_rank,
                                uint32_t* words, int32_t* status, void* stream);

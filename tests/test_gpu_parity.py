@@ -138,7 +138,7 @@ def test_demand_parity_full_size(vp, cid):
 
 
 @pytest.mark.parametrize("T,k,E,N,first", [(1000, 3, 24, 8, 5), (2049, 8, 256, 64, 0), (1, 1, 8, 8, 7),
-                                            (4097, 2, 4096, 16, 3)])
+                                            (4097, 2, 4096, 16, 3), (20011, 8, 256, 64, 2)])
 def test_demand_ragged(vp, T, k, E, N, first):
     log("demand ragged T=%d k=%d E=%d N=%d" % (T, k, E, N))
     rng = np.random.default_rng(T + E)
@@ -156,6 +156,32 @@ def test_demand_ragged(vp, T, k, E, N, first):
     assert np.array_equal(out["sorted_tok"].cpu().numpy()[:T * k], ref["sorted_tok"])
     assert np.array_equal(out["sorted_slot"].cpu().numpy()[:T * k], ref["sorted_slot"])
     assert np.array_equal(out["dest_off"].cpu().numpy(), ref["dest_off"])
+
+
+def test_demand_reused_workspace_and_single_rank(vp):
+    """One workspace, zero-filled once, serves calls of every shape in turn
+    (its per-row tickets reset themselves): all rows of the 64-rank workload,
+    then one rank's own row (R = 1, the deployed unit) at each end of the
+    rank range, then the 8-rank workload, then all 64 rows again; each call
+    element-wise against the oracle."""
+    ws = torch.zeros(vp.demand_workspace_bytes(64, 16384, 8, 256), dtype=torch.uint8, device="cuda")
+    w3, R3, dem3, D3 = moe_case(3)
+    w1, R1, dem1, D1 = moe_case(1)
+    calls = [(w3, R3, dem3, 0, 64, 5), (w3, R3, dem3, 0, 1, 0), (w3, R3, dem3, 63, 1, 0), (w1, R1, dem1, 0, 8, 7),
+             (w3, R3, dem3, 0, 64, 63)]
+    for w, R, dem, first, nrows, sort_row in calls:
+        log("demand reuse: N=%d first=%d R=%d sort_row=%d" % (w.n_ranks, first, nrows, sort_row))
+        out = vp.demand(torch.from_numpy(np.ascontiguousarray(R[first:first + nrows])).cuda(), w.n_ranks,
+                        w.experts, w.row_bytes, first_rank=first, sort_row=sort_row, ws=ws)
+        torch.cuda.synchronize()
+        assert vp.read_status(out["status"]) == 0
+        for r in range(nrows):
+            assert np.array_equal(out["demand"][r].cpu().numpy(), dem[first + r]["row"])
+            assert np.array_equal(out["counts"][r].cpu().numpy(), dem[first + r]["counts"])
+        ref = dem[first + sort_row]
+        assert np.array_equal(out["sorted_tok"].cpu().numpy(), ref["sorted_tok"])
+        assert np.array_equal(out["sorted_slot"].cpu().numpy(), ref["sorted_slot"])
+        assert np.array_equal(out["dest_off"].cpu().numpy(), ref["dest_off"])
 
 
 def test_demand_empty_and_bad_ids(vp):

@@ -85,7 +85,10 @@ def test_plan_params_defaults(vp):
 
 
 def test_workspace_queries(vp):
-    assert vp.demand_workspace_bytes(4096, 8, 256) >= 256 * 4 * 16
+    # tickets, partial counts of every row, chunk counts of the sorted row
+    assert vp.demand_workspace_bytes(256, 4096, 8, 256) >= 256 * 4 * 32
+    assert vp.demand_workspace_bytes(1, 4096, 8, 256) < vp.demand_workspace_bytes(256, 4096, 8, 256)
+    assert vp.demand_workspace_bytes(0, 4096, 8, 256) == 0
     # heads: one descriptor per step, whatever the send buffer's size
     assert vp.pack_workspace_bytes(2048, 468_729_856, 14336) >= 2048 * 24
     assert vp.pack_workspace_bytes(2048, 468_729_856, 14336) == vp.pack_workspace_bytes(2048, 1 << 40, 256)
