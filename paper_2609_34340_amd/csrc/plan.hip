@@ -44,6 +44,20 @@ constexpr int kMaxQG = kMaxSlotsPerNode * kMaxGpusPerSwitch;   // lanes per node
 constexpr int kMaxLTerms = 3 * kMaxSlotsPerNode;   // PIX, PXB and NIC entries of one diagonal block
 constexpr uint32_t kRawSaturated = 0xFFFFFFFEu;     // residual too large for 32 bits: reload it
 
+// Phase timing, compiled only with -DVP_PHASE_STAMPS (phase_stamps.py builds
+// such a copy): thread 0 of workgroup 0 stores the cycle counter at each
+// phase boundary of every iteration, row = iteration (4096 rows of 16).
+#ifdef VP_PHASE_STAMPS
+__device__ unsigned long long g_phase_stamps[4096 * 16];
+#define VP_STAMP(k)                                                                                  \
+  do {                                                                                               \
+    if (threadIdx.x == 0 && blockIdx.x == 0)                                                         \
+      g_phase_stamps[(stamp_it < 4095 ? stamp_it : 4095) * 16 + (k)] = __builtin_readcyclecounter(); \
+  } while (0)
+#else
+#define VP_STAMP(k) ((void)0)
+#endif
+
 struct PairRes {
   int64_t F;
   // largest lane volume on a PCIe-rate path (PIX, PXB, SYS) and on a NIC
@@ -755,11 +769,15 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
   const int64_t cap_c0 = lane0(sh->cap[0]), cap_c1 = lane0(sh->cap[1]), cap_c2 = lane0(sh->cap[2]),
                 cap_c3 = lane0(sh->cap[3]);
   // ---------------------------------------------------------------- loop
+  int stamp_it = 0;
+  (void)stamp_it;
   while (true) {
     // The loop's exit conditions are read here and tested after the scoring
     // work, which does not depend on them (on the last pass it is wasted),
     // so the read's latency hides behind it.
     const int err_ = sh->err, K_ = sh->K;
+    stamp_it = K_;
+    VP_STAMP(0);
     const int64_t rem_ = sh->total_rem;
 
     // Step 1: score every shape; argmax.  A shape (k, p) scores base(p), its
@@ -842,6 +860,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         }
       }
     }
+    VP_STAMP(1);
     if (err_ || rem_ == 0) break;   // the same LDS words for every thread
     if (K_ >= P.k_max) {
       __syncthreads();
@@ -852,6 +871,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     // that what is derived from them runs on the scalar unit
     const int K = lane0(K_);
     lds_barrier();
+    VP_STAMP(2);
     {
       uint64_t best = 0;
       for (int p = tid; p < NP; p += kPlanThreads) {
@@ -870,6 +890,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
     }
     lds_barrier();
     const uint64_t key = (uint64_t)lane0((int64_t)sh->key);
+    VP_STAMP(3);
     if ((key >> 20) == 0) {
       __syncthreads();
       if (tid == 0) set_err(sh, VP_ERR_NO_PROGRESS);
@@ -1019,6 +1040,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         }
       }
       lds_barrier();
+      VP_STAMP(4);
       for (int pi = wave; pi < nc * NS; pi += kWaves) {
         const int c = pi / NS, s = pi - c * NS;
         FamCtx fc{outT + (size_t)c * N, inT + (size_t)c * N, ipos + (size_t)c * N, ocls + (size_t)c * N,
@@ -1026,9 +1048,11 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         run_pair<g, MG>(P, fc, sl + (size_t)pi * N, dl + (size_t)pi * N, s, rp + (size_t)pi * L.G * 2, lane,
                         topkey[c], fe - fb > 1, &pr[pi]);
       }
+      VP_STAMP(5);
       // full barrier: the previous iteration's D^rem stores are complete
       // before the next gather reads D^rem
       __syncthreads();
+      VP_STAMP(6);
       // Evaluate (Eq. (9)-(10)): best start per family, best family overall.
       // Only the wavefronts that write the winner (threads t < N) evaluate.
       if (wave == 1)
@@ -1129,6 +1153,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       }
     }
 
+    VP_STAMP(7);
     // Step 4: append E* and subtract X(E*) from D^rem and the aggregates.
     {
       const int f = best_f, k = kstar;
@@ -1201,6 +1226,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
       __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), other counters untouched
       __builtin_amdgcn_s_barrier();
       __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      VP_STAMP(8);
     }
   }
 
@@ -1427,3 +1453,10 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
 }
 
 }  // namespace vp
+
+#ifdef VP_PHASE_STAMPS
+// Reader of the phase stamps of the last plan (stamped builds only).
+extern "C" int vp_phase_stamps_read(unsigned long long* out) {
+  return (int)hipMemcpyFromSymbol(out, HIP_SYMBOL(vp::g_phase_stamps), sizeof(unsigned long long) * 4096 * 16);
+}
+#endif
