@@ -67,11 +67,18 @@ enum { VP_TOPO_SYS_P2P = 1 };
 
 /* A PCIe cluster (Sec. 3 "Model setup", Sec. 5 "Topology, path, and rate
  * model").  Rank = ((node * sockets + socket) * switches + switch) * gpus + local;
- * one rank group per PCIe switch.  Every switch has one NIC.  Rates are in
- * bytes per nanosecond; a NIC path runs at min(pcie, nic), PIX, PXB and SYS
- * paths at the PCIe rate.
+ * one rank group per PCIe switch.  Each switch has nics_per_switch NICs, all
+ * reachable from every GPU of the switch: a NIC path leaves through one NIC
+ * of the source switch (its transmit side) and arrives through one NIC of
+ * the destination switch (its receive side).  Families that differ only by
+ * which of a switch's NICs their lanes use are one family (the catalog
+ * keeps the one with the smallest instance ids).  Rates are in bytes per
+ * nanosecond; a NIC path runs at min(pcie, nic), PIX, PXB and SYS paths at
+ * the PCIe rate.
  * Limits of this build: gpus_per_switch in [2, 4], sockets*switches <= 8,
- * nics_per_switch == 1, n_nodes in [1, 256], N <= 1024. */
+ * nics_per_switch in [1, 4] with 2*Q*(1 + nics) (+ sockets^2 with SYS) <= 64
+ * for Q = sockets*switches, at most 256 node-local path instances, n_nodes
+ * in [1, 256], N <= 1024.  vp_rotation_time takes one NIC per switch. */
 typedef struct {
   int32_t n_nodes;
   int32_t sockets_per_node;

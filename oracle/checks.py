@@ -41,6 +41,7 @@ class TopoModel:
         self.pcie = topo.pcie_bytes_per_ns
         self.nic = topo.nic_bytes_per_ns
         self.sys = bool(getattr(topo, "flags", 0) & 1)
+        self.m = getattr(topo, "nics_per_switch", 1)   # NICs per switch, every GPU of it reaches each
 
     def group(self, rank: int) -> int:
         return rank // self.g
@@ -155,6 +156,104 @@ def instantiate(tm: TopoModel, fam: Dict[str, np.ndarray]) -> set:
                 pi[src[t]] = dst[t]
                 cl[src[t]] = int(fam["cls"][t])
             res.add((tuple(pi), tuple(cl)))
+    return res
+
+
+# ----------------------------------------------- several NICs per switch
+#
+# With m NICs per switch a NIC path is labelled by the NIC it leaves through
+# and the NIC it arrives at: footprint TX of (source group, x) and RX of
+# (destination group, y).  A path label is (class, x, y), x = y = -1 for the
+# other classes.  Renaming the NICs of a group (a permutation per group,
+# applied to the source NIC of lanes leaving it and to the destination NIC
+# of lanes entering it) maps valid channels to valid channels.
+
+def path_labels(tm: TopoModel, a: int, d: int) -> List[Tuple[int, int, int]]:
+    out = []
+    for c in tm.unpruned_classes(a, d):
+        if c == NIC:
+            out += [(NIC, x, y) for x in range(tm.m) for y in range(tm.m)]
+        else:
+            out.append((c, -1, -1))
+    return out
+
+
+def shared_labeled(tm: TopoModel, lab, a: int, d: int) -> Tuple:
+    c, x, y = lab
+    if c == NIC:
+        return (("TX", a, x), ("RX", d, y))
+    return tm.shared(c, a, d)
+
+
+def brute_force_labeled(tm: TopoModel) -> set:
+    """Every feasible rank-level channel (pi, path label per rank) by brute
+    force over derangements and labelled path vectors (Eq. (1))."""
+    N = tm.N
+    out = set()
+    for pi in itertools.permutations(range(N)):
+        if any(pi[i] == i for i in range(N)):
+            continue
+        options = [path_labels(tm, tm.group(i), tm.group(pi[i])) for i in range(N)]
+
+        def rec(i, used, labs):
+            if i == N:
+                out.add((pi, tuple(labs)))
+                return
+            for lab in options[i]:
+                fp = shared_labeled(tm, lab, tm.group(i), tm.group(pi[i]))
+                if any(r in used for r in fp):
+                    continue
+                rec(i + 1, used | set(fp), labs + [lab])
+        rec(0, frozenset(), [])
+    return out
+
+
+def canonical_labeled(tm: TopoModel, ch) -> Tuple:
+    """The smallest renaming of a labelled channel over all per-group NIC
+    permutations."""
+    pi, labs = ch
+    best = None
+    perms = list(itertools.permutations(range(tm.m)))
+    for sig in itertools.product(perms, repeat=tm.G):
+        img = []
+        for i, (c, x, y) in enumerate(labs):
+            if c == NIC:
+                img.append((c, sig[tm.group(i)][x], sig[tm.group(pi[i])][y]))
+            else:
+                img.append((c, x, y))
+        img = (pi, tuple(img))
+        if best is None or img < best:
+            best = img
+    return best
+
+
+def instantiate_labeled(tm: TopoModel, fam: Dict[str, np.ndarray], labels) -> set:
+    """All endpoint bindings of one cluster-level family whose instance t has
+    path label labels[t] (self pairs excluded): (pi, label per rank)."""
+    g, G = tm.g, tm.G
+    n = len(fam["cls"])
+    outs = [[t for t in range(n) if fam["a"][t] == x] for x in range(G)]
+    ins = [[t for t in range(n) if fam["d"][t] == x] for x in range(G)]
+    perms = list(itertools.permutations(range(g)))
+    res = set()
+    for sp in itertools.product(perms, repeat=G):
+        src = [0] * n
+        for x in range(G):
+            for m, t in enumerate(outs[x]):
+                src[t] = x * g + sp[x][m]
+        for dp in itertools.product(perms, repeat=G):
+            dst = [0] * n
+            for x in range(G):
+                for m, t in enumerate(ins[x]):
+                    dst[t] = x * g + dp[x][m]
+            if any(src[t] == dst[t] for t in range(n)):
+                continue
+            pi = [0] * tm.N
+            lab = [None] * tm.N
+            for t in range(n):
+                pi[src[t]] = dst[t]
+                lab[src[t]] = labels[t]
+            res.add((tuple(pi), tuple(lab)))
     return res
 
 

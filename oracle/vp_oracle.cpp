@@ -55,11 +55,14 @@ struct Topo {
 // ---------------------------------------------------------------------------
 // Group-level path instances (Sec. 4.1 "Topology abstraction"; Sec. 3 model
 // setup).  Directed resources: per switch x, the uplink UP_x and downlink DN_x
-// between the switch and its root complex; per NIC, TX_x and RX_x.  GPU<->switch
+// between the switch and its root complex; per NIC, TX and RX.  GPU<->switch
 // links are endpoint-local and not modeled.  Path classes: PIX (same switch,
 // no shared resource), PXB (same socket, other switch: UP_src, DN_dst) and NIC
-// (any pair through the source switch's NIC and the destination switch's NIC:
-// TX_src, RX_dst).  A path's rate is the minimum of its links.  With
+// (any pair through one NIC of the source switch and one NIC of the
+// destination switch: TX of the first, RX of the second; every GPU of a switch
+// reaches every NIC of that switch inside the switch, so a switch with m NICs
+// offers m x m NIC instances to each switch, `copy` = source NIC * m +
+// destination NIC).  A path's rate is the minimum of its links.  With
 // cross-socket peer-to-peer enabled, SYS joins two switches of different
 // sockets of one node through both root complexes and the directed
 // inter-socket link: UP_src, X(socket_src -> socket_dst), DN_dst, at the PCIe
@@ -80,8 +83,9 @@ i64 rate_of(const Topo& t, int cls) {
 }
 
 // Node-local instance table shared by the k = 0 (intra-node) and k != 0
-// (remote) sets: PIX copies, PXB, and NIC for every slot pair.  Resource ids:
-// UP q -> q, DN q -> Q+q, TX q -> 2Q+q, RX q -> 3Q+q.
+// (remote) sets: PIX copies, PXB, and NIC for every slot pair and NIC pair.
+// Resource ids: UP q -> q, DN q -> Q+q, TX of NIC x of slot q -> 2Q+q*m+x,
+// RX of NIC y of slot q -> 2Q+Q*m+q*m+y, socket links after them.
 std::vector<Inst> local_table(const Topo& t) {
   const int Q = t.Q();
   std::vector<Inst> v;
@@ -92,16 +96,19 @@ std::vector<Inst> local_table(const Topo& t) {
     for (int q2 = 0; q2 < Q; ++q2)
       if (q != q2 && q / t.switches == q2 / t.switches)
         v.push_back({0, PXB, q, q2, 0, false, rate_of(t, PXB), {q, Q + q2}});
-  if (t.nics > 0)
-    for (int q = 0; q < Q; ++q)
-      for (int q2 = 0; q2 < Q; ++q2)
-        v.push_back({0, NIC, q, q2, 0, false, rate_of(t, NIC), {2 * Q + q, 3 * Q + q2}});
-  // socket link s -> s2: resource 4Q + s * sockets + s2
+  const int m = t.nics, X = 2 * Q + 2 * Q * m;   // socket links from X on
+  for (int q = 0; q < Q; ++q)
+    for (int q2 = 0; q2 < Q; ++q2)
+      for (int x = 0; x < m; ++x)
+        for (int y = 0; y < m; ++y)
+          v.push_back({0, NIC, q, q2, x * m + y, false, rate_of(t, NIC),
+                       {2 * Q + q * m + x, 2 * Q + Q * m + q2 * m + y}});
+  // socket link s -> s2: resource X + s * sockets + s2
   if (t.sys)
     for (int q = 0; q < Q; ++q)
       for (int q2 = 0; q2 < Q; ++q2) {
         const int s = q / t.switches, s2 = q2 / t.switches;
-        if (s != s2) v.push_back({0, SYS, q, q2, 0, false, rate_of(t, SYS), {q, Q + q2, 4 * Q + s * t.sockets + s2}});
+        if (s != s2) v.push_back({0, SYS, q, q2, 0, false, rate_of(t, SYS), {q, Q + q2, X + s * t.sockets + s2}});
       }
   std::sort(v.begin(), v.end(), [](const Inst& x, const Inst& y) {
     return std::make_tuple(x.cls, x.a, x.d, x.copy) < std::make_tuple(y.cls, y.a, y.d, y.copy);
@@ -112,7 +119,8 @@ std::vector<Inst> local_table(const Topo& t) {
 
 // Cluster-level instance set over all G groups (used for the full, unreduced
 // Alg. 1 catalog of small topologies).  Resource ids: UP a -> a, DN a -> G+a,
-// TX a -> 2G+a, RX a -> 3G+a.
+// TX of NIC x of group a -> 2G+a*m+x, RX of NIC y of group d -> 2G+G*m+d*m+y,
+// socket links after them.
 std::vector<Inst> cluster_table(const Topo& t) {
   const int G = t.G(), Q = t.Q();
   std::vector<Inst> v;
@@ -126,17 +134,20 @@ std::vector<Inst> cluster_table(const Topo& t) {
       if (a != d && same_socket)
         v.push_back({0, PXB, a, d, 0, false, rate_of(t, PXB), {a, G + d}});
     }
-  if (t.nics > 0)
-    for (int a = 0; a < G; ++a)
-      for (int d = 0; d < G; ++d)
-        v.push_back({0, NIC, a, d, 0, false, rate_of(t, NIC), {2 * G + a, 3 * G + d}});
-  // socket link of node n, s -> s2: resource 4G + (n * sockets + s) * sockets + s2
+  const int m = t.nics, X = 2 * G + 2 * G * m;
+  for (int a = 0; a < G; ++a)
+    for (int d = 0; d < G; ++d)
+      for (int x = 0; x < m; ++x)
+        for (int y = 0; y < m; ++y)
+          v.push_back({0, NIC, a, d, x * m + y, false, rate_of(t, NIC),
+                       {2 * G + a * m + x, 2 * G + G * m + d * m + y}});
+  // socket link of node n, s -> s2: resource X + (n * sockets + s) * sockets + s2
   if (t.sys)
     for (int a = 0; a < G; ++a)
       for (int d = 0; d < G; ++d) {
         const int n = a / Q, s = (a % Q) / t.switches, s2 = (d % Q) / t.switches;
         if (n == d / Q && s != s2)
-          v.push_back({0, SYS, a, d, 0, false, rate_of(t, SYS), {a, G + d, 4 * G + (n * t.sockets + s) * t.sockets + s2}});
+          v.push_back({0, SYS, a, d, 0, false, rate_of(t, SYS), {a, G + d, X + (n * t.sockets + s) * t.sockets + s2}});
       }
   std::sort(v.begin(), v.end(), [](const Inst& x, const Inst& y) {
     return std::make_tuple(x.cls, x.a, x.d, x.copy) < std::make_tuple(y.cls, y.a, y.d, y.copy);
@@ -177,56 +188,97 @@ typedef std::vector<int> Fam;
 typedef std::vector<int> ShapeKey;
 
 // Every family of an instance set, from its definition (Sec. 4.1, Eq. (3)
-// and Eq. (4)): a set of instances in which each group is the source of
-// exactly g instances and the destination of exactly g, and no modeled
-// resource is used twice.  The search decides one group at a time which g of
-// the instances leaving it the family takes (every g-subset, in index
-// order); a choice is abandoned as soon as some group would receive more
-// than g lanes or a resource would repeat, and a complete choice is kept
-// when every group receives exactly g.  The set of families found does not
-// depend on the order of the search.
+// and Eq. (4)): a set of instances in which each group is the destination of
+// exactly g instances and the source of exactly g, and no modeled resource
+// is used twice.  The search decides one group at a time which g of the
+// instances arriving at it the family takes (every g-subset, in index
+// order); a choice is abandoned as soon as some group would send more than
+// g lanes or a resource would repeat, and a complete choice is kept when
+// every group sends exactly g.  The set of families found does not depend
+// on the order of the search.
 std::vector<std::vector<int>> all_families(const std::vector<Inst>& R, int n_groups, int g, int n_res) {
-  std::vector<std::vector<int>> leaving(n_groups);
-  for (int i = 0; i < (int)R.size(); ++i) leaving[R[i].a].push_back(i);
+  std::vector<std::vector<int>> arriving(n_groups);
+  for (int i = 0; i < (int)R.size(); ++i) arriving[R[i].d].push_back(i);
   std::vector<std::vector<int>> found;
-  std::vector<int> into(n_groups, 0), res_used(n_res, 0), chosen;
+  std::vector<int> sends(n_groups, 0), res_used(n_res, 0), chosen;
 
-  // try to add instance i; undo with take_back
   auto fits = [&](int i) {
-    if (into[R[i].d] == g) return false;
+    if (sends[R[i].a] == g) return false;
     for (int l : R[i].L)
       if (res_used[l]) return false;
     return true;
   };
   auto take = [&](int i, int sgn) {
-    into[R[i].d] += sgn;
+    sends[R[i].a] += sgn;
     for (int l : R[i].L) res_used[l] += sgn;
   };
-  // group a picks its remaining `need` lanes among leaving[a][from..]
-  std::function<void(int, int, int)> pick = [&](int a, int from, int need) {
+  // group d picks its remaining `need` lanes among arriving[d][from..]
+  std::function<void(int, int, int)> pick = [&](int d, int from, int need) {
     if (need == 0) {
-      if (a + 1 < n_groups) {
-        pick(a + 1, 0, g);
+      if (d + 1 < n_groups) {
+        pick(d + 1, 0, g);
         return;
       }
       for (int x = 0; x < n_groups; ++x)
-        if (into[x] != g) return;
+        if (sends[x] != g) return;
       found.push_back(chosen);
       return;
     }
-    const std::vector<int>& opts = leaving[a];
-    for (int m = from; m + need <= (int)opts.size(); ++m) {
-      const int i = opts[m];
+    const std::vector<int>& opts = arriving[d];
+    for (int k = from; k + need <= (int)opts.size(); ++k) {
+      const int i = opts[k];
       if (!fits(i)) continue;
       take(i, +1);
       chosen.push_back(i);
-      pick(a, m + 1, need - 1);
+      pick(d, k + 1, need - 1);
       chosen.pop_back();
       take(i, -1);
     }
   };
   if (n_groups > 0) pick(0, 0, g);
   return found;
+}
+
+// NIC symmetry (reading: the m NICs of a switch are interchangeable, same
+// rate and same attachment): two families that differ only by a renaming of
+// each group's NICs are one family under two names.  A family is kept only
+// when no renaming (a permutation of the NICs of every group, applied to the
+// source NIC of its lanes out of that group and to the destination NIC of
+// its lanes into it) gives a smaller sorted id list.
+std::vector<Fam> keep_nic_canonical(const std::vector<Fam>& fams, const std::vector<Inst>& table, int n_groups,
+                                    int m) {
+  if (m <= 1) return fams;
+  std::map<std::tuple<int, int, int>, int> nic_id;   // (src group, dst group, copy) -> id
+  for (const Inst& r : table)
+    if (r.cls == NIC) nic_id[std::make_tuple(r.a, r.d, r.copy)] = r.id;
+  std::vector<std::vector<int>> perms;
+  std::vector<int> p(m);
+  for (int x = 0; x < m; ++x) p[x] = x;
+  do perms.push_back(p); while (std::next_permutation(p.begin(), p.end()));
+  std::vector<Fam> out;
+  for (const Fam& f : fams) {
+    bool smallest = true;
+    std::vector<int> pick(n_groups, 0);   // permutation index per group, odometer order
+    while (smallest) {
+      Fam img;
+      for (int id : f) {
+        const Inst& r = table[id];
+        if (r.cls != NIC) {
+          img.push_back(id);
+          continue;
+        }
+        const int x = perms[pick[r.a]][r.copy / m], y = perms[pick[r.d]][r.copy % m];
+        img.push_back(nic_id.at(std::make_tuple(r.a, r.d, x * m + y)));
+      }
+      std::sort(img.begin(), img.end());
+      if (img < f) smallest = false;
+      int gpos = 0;
+      while (gpos < n_groups && ++pick[gpos] == (int)perms.size()) pick[gpos++] = 0;
+      if (gpos == n_groups) break;
+    }
+    if (smallest) out.push_back(f);
+  }
+  return out;
 }
 
 // Family-level pruning (Sec. 4.1): inside one shape bucket, exact duplicates
@@ -283,10 +335,11 @@ std::vector<Fam> drop_duplicate_and_dominated(std::vector<Fam> fams, const std::
 
 // The catalog of one instance set: drop dominated paths, find every family,
 // file each under its shape (lane counts per group pair, remote lanes
-// counted apart), then prune each bucket.
+// counted apart), then prune each bucket and keep one family per NIC
+// renaming.
 std::map<ShapeKey, std::vector<Fam>> catalog_of(const std::vector<Inst>& table,
                                                 const std::vector<Inst>& candidates, int n_groups, int g,
-                                                int n_res) {
+                                                int n_res, int nics) {
   std::vector<Inst> R = drop_dominated_paths(candidates);
   std::sort(R.begin(), R.end(), [](const Inst& x, const Inst& y) { return x.id < y.id; });
   std::map<ShapeKey, std::vector<Fam>> buckets;
@@ -301,7 +354,8 @@ std::map<ShapeKey, std::vector<Fam>> catalog_of(const std::vector<Inst>& table,
     std::sort(f.begin(), f.end());
     buckets[M].push_back(f);
   }
-  for (auto& kv : buckets) kv.second = drop_duplicate_and_dominated(kv.second, table);
+  for (auto& kv : buckets)
+    kv.second = keep_nic_canonical(drop_duplicate_and_dominated(kv.second, table), table, n_groups, nics);
   return buckets;
 }
 
@@ -374,11 +428,11 @@ void build_circulant(Catalog& C, bool nearest) {
   const Topo& t = C.topo;
   const int Q = t.Q(), g = t.g, nn = t.n_nodes;
   C.table = local_table(t);
-  const int n_res = 4 * Q + t.sockets * t.sockets;
+  const int n_res = 2 * Q + 2 * Q * t.nics + t.sockets * t.sockets;
   // k = 0 set: PIX, PXB, NIC between slots of the same node (loopback).
   std::vector<Inst> set0;
   for (Inst r : C.table) { r.remote = false; set0.push_back(r); }
-  auto b0 = catalog_of(C.table, set0, Q, g, n_res);
+  auto b0 = catalog_of(C.table, set0, Q, g, n_res, t.nics);
   if (nearest) keep_nearest(b0, C.table, t, false);
   // k != 0 set: PIX, PXB, and NIC lanes to the same slot pattern on another node.
   std::map<ShapeKey, std::vector<Fam>> b1;
@@ -386,7 +440,7 @@ void build_circulant(Catalog& C, bool nearest) {
     std::vector<Inst> set1;
     for (Inst r : C.table) { r.remote = (r.cls == NIC); set1.push_back(r); }
     std::vector<Inst> table1 = set1;
-    auto all1 = catalog_of(table1, set1, Q, g, n_res);
+    auto all1 = catalog_of(table1, set1, Q, g, n_res, t.nics);
     for (auto& kv : all1) {
       std::vector<Fam> keep;
       for (const Fam& f : kv.second) {
@@ -443,7 +497,7 @@ void build_full(Catalog& C, bool nearest) {
   const Topo& t = C.topo;
   const int G = t.G();
   C.table = cluster_table(t);
-  auto b = catalog_of(C.table, C.table, G, t.g, 4 * G + t.n_nodes * t.sockets * t.sockets);
+  auto b = catalog_of(C.table, C.table, G, t.g, 2 * G + 2 * G * t.nics + t.n_nodes * t.sockets * t.sockets, t.nics);
   if (nearest) keep_nearest(b, C.table, t, false);
   for (const auto& kv : b) {
     CShape s;
@@ -924,8 +978,8 @@ int orc_catalog_build(const orc_topology* tp, int mode, orc_catalog** out) {
   if (!tp || !out) return INVALID_ARGUMENT;
   Topo t{tp->n_nodes, tp->sockets_per_node, tp->switches_per_socket, tp->gpus_per_switch,
          tp->nics_per_switch, tp->pcie_bytes_per_ns, tp->nic_bytes_per_ns, (tp->flags & 1) != 0};
-  // every ordered pair needs a path: one NIC per switch, at least two GPUs per switch
-  if (t.n_nodes < 1 || t.sockets < 1 || t.switches < 1 || t.g < 2 || t.nics != 1 ||
+  // every ordered pair needs a path: 1 to 4 NICs per switch, at least two GPUs per switch
+  if (t.n_nodes < 1 || t.sockets < 1 || t.switches < 1 || t.g < 2 || t.nics < 1 || t.nics > 4 ||
       t.pcie < 1 || t.nic < 1 || (tp->flags & ~1) != 0)
     return INVALID_ARGUMENT;
   Catalog* C = new Catalog();
@@ -1122,6 +1176,7 @@ int orc_rotation_time(const orc_topology* tp, const int64_t* D, int32_t nearest,
                       int64_t* num, int64_t* den) {
   Topo t{tp->n_nodes, tp->sockets_per_node, tp->switches_per_socket, tp->gpus_per_switch,
          tp->nics_per_switch, tp->pcie_bytes_per_ns, tp->nic_bytes_per_ns, (tp->flags & 1) != 0};
+  if (t.nics != 1) return UNSUPPORTED;   // the rotation model has one NIC per switch
   const int N = t.N(), Q = t.Q();
   auto group = [&](int r) { return r / t.g; };
   auto node = [&](int a) { return a / Q; };

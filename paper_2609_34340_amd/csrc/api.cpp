@@ -54,7 +54,18 @@ vp_status check_topology(const vp_topology& t) {
     return set_error(VP_ERR_UNSUPPORTED, "sockets*switches per node must be in [1, 8]");
   if (t.gpus_per_switch < 2 || t.gpus_per_switch > vp::kMaxGpusPerSwitch)
     return set_error(VP_ERR_UNSUPPORTED, "gpus_per_switch must be in [2, 4]");
-  if (t.nics_per_switch != 1) return set_error(VP_ERR_UNSUPPORTED, "nics_per_switch must be 1");
+  if (t.nics_per_switch < 1 || t.nics_per_switch > 4)
+    return set_error(VP_ERR_UNSUPPORTED, "nics_per_switch must be in [1, 4]");
+  {
+    // one bit per directed resource of a node (UP, DN per switch; TX, RX per
+    // NIC; socket links) and node-local instance ids below 256
+    const int64_t S = t.sockets_per_node, W = t.switches_per_socket, Q = S * W, m = t.nics_per_switch;
+    const bool sys = (t.flags & VP_TOPO_SYS_P2P) != 0;
+    if (2 * Q + 2 * Q * m + (sys ? S * S : 0) > 64)
+      return set_error(VP_ERR_UNSUPPORTED, "too many switches and NICs per node (resource bits)");
+    const int64_t n_inst = Q * t.gpus_per_switch + S * W * (W - 1) + Q * Q * m * m + (sys ? Q * Q - S * W * W : 0);
+    if (n_inst > 256) return set_error(VP_ERR_UNSUPPORTED, "more than 256 node-local path instances");
+  }
   if (t.pcie_bytes_per_ns < 1 || t.nic_bytes_per_ns < 1)
     return set_error(VP_ERR_INVALID_ARGUMENT, "rates must be positive");
   int64_t N = (int64_t)t.n_nodes * t.sockets_per_node * t.switches_per_socket * t.gpus_per_switch;

@@ -8,7 +8,10 @@
 // This visits exactly the compatible, complete instance sets that Alg. 1's
 // include/exclude DFS reaches, each once: identical PIX copies are taken in
 // copy order, which is PruneFamilies' exact-duplicate rule applied during the
-// search.  PrunePaths runs before, the dominance half of PruneFamilies after.
+// search.  PrunePaths runs before, the rest of PruneFamilies after.  With
+// several NICs per switch, families that differ only by which of a
+// switch's interchangeable NICs a lane uses are kept once (the smallest of
+// each renaming class).
 //
 // Multi-node topologies use the node-circulant reduction: the same node-local
 // pattern in every node, all NIC lanes of node n landing on node (n+k) mod
@@ -29,7 +32,7 @@ namespace {
 struct Cand {
   int id, cls, src, dst, copy;
   int64_t bw;
-  uint64_t res;   // bit per directed resource: UP q, DN q, TX q, RX q, socket link s -> s2
+  uint64_t res;   // bit per directed resource: UP q, DN q, TX (q, nic), RX (q, nic), socket link s -> s2
   bool remote;    // NIC lane to another node
 };
 
@@ -112,50 +115,110 @@ class SlotSearch {
   std::vector<Found> found_;
 };
 
-// PruneFamilies: drop exact duplicates (same multiset of (pair, footprint,
-// rate)) and families dominated inside their shape.
-std::vector<Found> prune_families(std::vector<Found> fs, const std::vector<Cand>& by_id) {
-  typedef std::tuple<int, int, bool, uint64_t> PairFoot;
-  auto profile = [&](const Found& f) {
-    std::map<PairFoot, std::vector<int64_t>> m;
-    for (int id : f.ids) {
-      const Cand& c = by_id[id];
-      m[PairFoot(c.src, c.dst, c.remote, c.res)].push_back(c.bw);
-    }
-    for (auto& kv : m) std::sort(kv.second.begin(), kv.second.end(), std::greater<int64_t>());
-    return m;
-  };
+typedef std::tuple<int, int, bool, uint64_t> PairFoot;
+typedef std::map<PairFoot, std::vector<int64_t>> Profile;
+
+// Rates of a family's lanes per (pair, footprint), descending.
+Profile profile_of(const Found& f, const std::vector<Cand>& by_id) {
+  Profile m;
+  for (int id : f.ids) {
+    const Cand& c = by_id[id];
+    m[PairFoot(c.src, c.dst, c.remote, c.res)].push_back(c.bw);
+  }
+  for (auto& kv : m) std::sort(kv.second.begin(), kv.second.end(), std::greater<int64_t>());
+  return m;
+}
+
+// PruneFamilies, first half: exact duplicates (same multiset of (pair,
+// footprint, rate)) keep their first family in canonical order; the result
+// is sorted by (L, R, ids), so every shape's families are contiguous.
+std::vector<Found> drop_duplicates(std::vector<Found> fs, const std::vector<Cand>& by_id) {
   std::sort(fs.begin(), fs.end(), [](const Found& a, const Found& b) {
     return std::tie(a.L, a.R, a.ids) < std::tie(b.L, b.R, b.ids);
   });
   std::vector<Found> uniq;
-  std::set<std::map<PairFoot, std::vector<int64_t>>> seen;
-  std::vector<std::map<PairFoot, std::vector<int64_t>>> prof;
-  for (Found& f : fs) {
-    auto p = profile(f);
-    if (seen.insert(p).second) {
-      prof.push_back(p);
-      uniq.push_back(std::move(f));
-    }
-  }
+  std::set<Profile> seen;
+  for (Found& f : fs)
+    if (seen.insert(profile_of(f, by_id)).second) uniq.push_back(std::move(f));
+  return uniq;
+}
+
+// PruneFamilies, second half: a family is dropped when another of its shape
+// pairs with it per (pair, footprint) at no lower rate, one strictly higher.
+// Shapes are contiguous in the input, so only families of one run compare.
+std::vector<Found> drop_dominated(std::vector<Found> fs, const std::vector<Cand>& by_id) {
+  std::vector<Profile> prof;
+  for (const Found& f : fs) prof.push_back(profile_of(f, by_id));
   std::vector<Found> out;
-  for (size_t i = 0; i < uniq.size(); ++i) {
-    bool dominated = false;
-    for (size_t j = 0; j < uniq.size() && !dominated; ++j) {
-      if (i == j || uniq[i].L != uniq[j].L || uniq[i].R != uniq[j].R) continue;
-      if (prof[i].size() != prof[j].size()) continue;
-      bool ok = true, strict = false;
-      for (auto it = prof[j].begin(); it != prof[j].end() && ok; ++it) {
-        auto jt = prof[i].find(it->first);
-        if (jt == prof[i].end() || jt->second.size() != it->second.size()) { ok = false; break; }
-        for (size_t x = 0; x < it->second.size(); ++x) {
-          if (it->second[x] < jt->second[x]) ok = false;
-          if (it->second[x] > jt->second[x]) strict = true;
+  size_t b = 0;
+  while (b < fs.size()) {
+    size_t e = b + 1;
+    while (e < fs.size() && fs[e].L == fs[b].L && fs[e].R == fs[b].R) ++e;
+    for (size_t i = b; i < e; ++i) {
+      bool dominated = false;
+      for (size_t j = b; j < e && !dominated; ++j) {
+        if (i == j || prof[i].size() != prof[j].size()) continue;
+        bool ok = true, strict = false;
+        for (auto it = prof[j].begin(); it != prof[j].end() && ok; ++it) {
+          auto jt = prof[i].find(it->first);
+          if (jt == prof[i].end() || jt->second.size() != it->second.size()) { ok = false; break; }
+          for (size_t x = 0; x < it->second.size(); ++x) {
+            if (it->second[x] < jt->second[x]) ok = false;
+            if (it->second[x] > jt->second[x]) strict = true;
+          }
         }
+        dominated = ok && strict;
       }
-      dominated = ok && strict;
+      if (!dominated) out.push_back(fs[i]);
     }
-    if (!dominated) out.push_back(uniq[i]);
+    b = e;
+  }
+  return out;
+}
+
+}  // namespace
+
+namespace {
+
+// Families that differ only by which of a switch's interchangeable NICs
+// each lane uses are one family: a family is kept when renaming the NICs of
+// the slots (one permutation per slot, on the source NIC of the lanes it
+// sends and the destination NIC of the lanes it receives) never yields a
+// smaller ascending id list.  Every renaming of a slot's NICs is tried.
+std::vector<Found> nic_representatives(std::vector<Found> fs, const std::vector<Cand>& by_id, int Q, int m) {
+  if (m == 1) return fs;
+  // id of each NIC instance by (src, dst, copy)
+  std::map<std::tuple<int, int, int>, int> nic;
+  for (const Cand& c : by_id)
+    if (c.cls == VP_PATH_NIC) nic[std::make_tuple(c.src, c.dst, c.copy)] = c.id;
+  std::vector<std::vector<int>> sym;   // the m! permutations of one slot's NICs
+  std::vector<int> perm(m);
+  for (int x = 0; x < m; ++x) perm[x] = x;
+  do sym.push_back(perm); while (std::next_permutation(perm.begin(), perm.end()));
+  int64_t combos = 1;
+  for (int q = 0; q < Q; ++q) combos *= (int64_t)sym.size();
+  std::vector<Found> out;
+  std::vector<int32_t> renamed;
+  for (Found& f : fs) {
+    bool least = true;
+    for (int64_t code = 1; code < combos && least; ++code) {
+      renamed.clear();
+      for (int32_t id : f.ids) {
+        const Cand& c = by_id[id];
+        if (c.cls != VP_PATH_NIC) {
+          renamed.push_back(id);
+          continue;
+        }
+        int64_t cs = code, cd = code;
+        for (int q = 0; q < c.src; ++q) cs /= (int64_t)sym.size();
+        for (int q = 0; q < c.dst; ++q) cd /= (int64_t)sym.size();
+        const int x = sym[cs % (int64_t)sym.size()][c.copy / m], y = sym[cd % (int64_t)sym.size()][c.copy % m];
+        renamed.push_back(nic.at(std::make_tuple(c.src, c.dst, x * m + y)));
+      }
+      std::sort(renamed.begin(), renamed.end());
+      least = !(renamed < f.ids);
+    }
+    if (least) out.push_back(std::move(f));
   }
   return out;
 }
@@ -165,9 +228,12 @@ std::vector<Found> prune_families(std::vector<Found> fs, const std::vector<Cand>
 namespace {
 
 // Node-local instance table in canonical id order: (class, src, dst, copy).
+// A NIC instance leaves through NIC x of its source switch and arrives
+// through NIC y of its destination switch (copy = x * m + y, m NICs per
+// switch); every GPU of a switch reaches each of the switch's NICs.
 std::vector<Cand> instance_table(const vp_topology& t) {
   const int W = t.switches_per_socket, g = t.gpus_per_switch;
-  const int Q = t.sockets_per_node * W;
+  const int Q = t.sockets_per_node * W, m = t.nics_per_switch;
   const int64_t pcie = t.pcie_bytes_per_ns;
   const int64_t nicbw = std::min(t.pcie_bytes_per_ns, t.nic_bytes_per_ns);
   std::vector<Cand> table;
@@ -182,14 +248,17 @@ std::vector<Cand> instance_table(const vp_topology& t) {
     for (int q2 = 0; q2 < Q; ++q2)
       if (q != q2 && q / W == q2 / W) add(VP_PATH_PXB, q, q2, 0, pcie, bit(q) | bit(Q + q2));
   for (int q = 0; q < Q; ++q)
-    for (int q2 = 0; q2 < Q; ++q2) add(VP_PATH_NIC, q, q2, 0, nicbw, bit(2 * Q + q) | bit(3 * Q + q2));
+    for (int q2 = 0; q2 < Q; ++q2)
+      for (int x = 0; x < m; ++x)
+        for (int y = 0; y < m; ++y)
+          add(VP_PATH_NIC, q, q2, x * m + y, nicbw, bit(2 * Q + q * m + x) | bit(2 * Q + Q * m + q2 * m + y));
   // peer to peer between sockets: both switches' root-complex links and the
   // directed link between the two sockets, at the PCIe rate
   if (t.flags & VP_TOPO_SYS_P2P)
     for (int q = 0; q < Q; ++q)
       for (int q2 = 0; q2 < Q; ++q2)
         if (q / W != q2 / W)
-          add(VP_PATH_SYS, q, q2, 0, pcie, bit(q) | bit(Q + q2) | bit(4 * Q + (q / W) * S + q2 / W));
+          add(VP_PATH_SYS, q, q2, 0, pcie, bit(q) | bit(Q + q2) | bit(2 * Q + 2 * Q * m + (q / W) * S + q2 / W));
   return table;
 }
 
@@ -290,7 +359,10 @@ vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
     SlotSearch search(prune_paths(table, remote_nic), c.Q, c.g);
     std::vector<Cand> cand = table;
     for (Cand& x : cand) x.remote = remote_nic && x.cls == VP_PATH_NIC;
-    std::vector<Found> fs = prune_families(search.run(), cand);
+    // renaming a slot's NICs preserves dominance both ways, so the NIC
+    // classes may be reduced to their representatives before it is checked
+    std::vector<Found> fs = drop_dominated(
+        nic_representatives(drop_duplicates(search.run(), cand), cand, c.Q, t.nics_per_switch), cand);
     if (remote_nic) {
       std::vector<Found> with_nic;
       for (Found& f : fs) {
@@ -360,8 +432,9 @@ std::vector<uint8_t> serialize_catalog(const vp_catalog& c) {
 // Rebuilds a catalog from its serialized form.  Everything Alg. 1 guarantees
 // is checked again: every family is a complete, resource-disjoint set of
 // surviving path instances (Eq. (1), Eq. (4)), identical PIX copies appear in
-// copy order, NIC-carrying families carry a NIC lane, and each list is in
-// strictly increasing canonical order (no duplicates).  A subset of the
+// copy order, NIC-carrying families carry a NIC lane, every family is the
+// representative of its NIC renaming class, and each list is in strictly
+// increasing canonical order (no duplicates).  A subset of the
 // families Alg. 1 would find is accepted (a restricted catalog).
 vp_status deserialize_catalog(const uint8_t* p, size_t n, vp_catalog& c,
                               vp_status (*check_topology)(const vp_topology&)) {
@@ -423,6 +496,12 @@ vp_status deserialize_catalog(const uint8_t* p, size_t n, vp_catalog& c,
         return set_error(VP_ERR_INVALID_ARGUMENT, "serialized families are not in canonical order");
       lists[part].push_back(std::move(fam));
     }
+    // several NICs per switch: every family must be its renaming class's
+    // representative
+    std::vector<Cand> cand = table;
+    for (Cand& x : cand) x.remote = remote && x.cls == VP_PATH_NIC;
+    if (nic_representatives(lists[part], cand, Q, t.nics_per_switch).size() != lists[part].size())
+      return set_error(VP_ERR_INVALID_ARGUMENT, "serialized catalog holds a family under other NIC names");
   }
   fill_catalog(c, lists[0], lists[1]);
   return VP_OK;
@@ -460,9 +539,9 @@ void build_device_image(vp_catalog& c) {
   std::vector<std::vector<int>> sets;
   std::vector<int> psid(c.J1);
   for (int p = c.J0; p < P; ++p) {
-    std::vector<int> e;
+    std::vector<int> e;   // a slot pair appears once per NIC lane on it
     for (int x = 0; x < Q * Q; ++x)
-      if (c.patR[p][x]) e.push_back(x);
+      for (int r = 0; r < c.patR[p][x]; ++r) e.push_back(x);
     auto it = set_id.find(e);
     if (it == set_id.end()) {
       it = set_id.emplace(e, (int)sets.size()).first;

@@ -40,6 +40,8 @@ int64_t gcd64(int64_t a, int64_t b) {
 
 vp_status rotation_time(const vp_catalog& c, const int64_t* D, int rule, int64_t lambda, int64_t* num,
                         int64_t* den) {
+  if (c.topo.nics_per_switch != 1)
+    return set_error(VP_ERR_UNSUPPORTED, "the rotation model takes one NIC per switch");
   const int N = c.N, g = c.g, Q = c.Q, G = c.G;
   const int W = c.topo.switches_per_socket, S = c.topo.sockets_per_node;
   const bool sys = (c.topo.flags & VP_TOPO_SYS_P2P) != 0;

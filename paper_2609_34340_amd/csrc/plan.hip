@@ -1340,11 +1340,8 @@ vp_status launch_plan(const PlanLaunch& a, void* stream) {
     for (int v : c.patL[p]) nl += v != 0;
     if (nl > kMaxLTerms) return set_error(VP_ERR_UNSUPPORTED, "too many intra-node lane classes");
     mlt = std::max(mlt, nl);
-    int nr = 0;
-    for (int v : c.patR[p]) {   // one NIC per switch: at most one cross-node lane per slot pair
-      if (v > 1) return set_error(VP_ERR_UNSUPPORTED, "more than one NIC lane per slot pair");
-      nr += v != 0;
-    }
+    int nr = 0;   // cross-node lanes (a slot pair counts once per lane: several NICs per switch)
+    for (int v : c.patR[p]) nr += v;
     if (nr > kMaxRTerms) return set_error(VP_ERR_UNSUPPORTED, "too many NIC lanes in one pattern");
     mrt = std::max(mrt, nr);
   }

@@ -248,7 +248,11 @@ def random_demand(rng, N, unit, density, scale):
 
 @pytest.mark.parametrize("topo", [vpgen.tiny_topology(), vpgen.config(1).topo, vpgen.config(2).topo,
                                   vpgen.Topology(3, 1, 2, 3), vpgen.Topology(2, 2, 1, 4),
-                                  vpgen.Topology(1, 1, 1, 4), vpgen.Topology(4, 1, 3, 2, 1, 32, 50)])
+                                  vpgen.Topology(1, 1, 1, 4), vpgen.Topology(4, 1, 3, 2, 1, 32, 50),
+                                  # several NICs per switch (two NIC lanes may join one slot pair)
+                                  vpgen.Topology(1, 1, 2, 2, 2), vpgen.Topology(1, 2, 1, 2, 2),
+                                  vpgen.Topology(2, 1, 2, 2, 2), vpgen.Topology(3, 1, 2, 2, 3),
+                                  vpgen.Topology(1, 1, 2, 3, 2)])
 def test_plan_parity_random_demands(vp, topo):
     rng = np.random.default_rng(topo.n_ranks)
     oc = ocat(topo)

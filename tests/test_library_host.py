@@ -43,7 +43,11 @@ def test_library_exports_every_declared_symbol(vp):
 @pytest.mark.parametrize("topo", [vpgen.tiny_topology(), vpgen.config(1).topo, vpgen.config(2).topo,
                                   vpgen.config(3).topo, vpgen.config(5).topo,
                                   vpgen.Topology(3, 1, 2, 3), vpgen.Topology(2, 2, 1, 4),
-                                  vpgen.Topology(1, 1, 1, 4), vpgen.Topology(4, 1, 3, 2, 1, 32, 50)])
+                                  vpgen.Topology(1, 1, 1, 4), vpgen.Topology(4, 1, 3, 2, 1, 32, 50),
+                                  # several NICs per switch
+                                  vpgen.Topology(1, 1, 2, 2, 2), vpgen.Topology(1, 2, 1, 2, 2),
+                                  vpgen.Topology(1, 1, 2, 3, 2), vpgen.Topology(2, 1, 2, 2, 2),
+                                  vpgen.Topology(3, 1, 2, 2, 3), vpgen.Topology(1, nics_per_switch=2)])
 def test_catalog_equals_oracle(vp, topo):
     ours = vp.Catalog(topo)
     ref = oracle.Catalog(topo)
@@ -63,7 +67,10 @@ def test_catalog_equals_oracle(vp, topo):
 def test_unsupported_topologies_are_rejected(vp):
     for topo in [vpgen.Topology(1, gpus_per_switch=1), vpgen.Topology(1, gpus_per_switch=5),
                  vpgen.Topology(1, nics_per_switch=0), vpgen.Topology(300),
-                 vpgen.Topology(1, sockets_per_node=3, switches_per_socket=3)]:
+                 vpgen.Topology(1, sockets_per_node=3, switches_per_socket=3),
+                 vpgen.Topology(1, nics_per_switch=5),
+                 # 2Q + 2Qm resource bits above 64 / more than 256 node-local instances
+                 vpgen.Topology(1, 2, 4, 2, 4), vpgen.Topology(1, 2, 4, 2, 2)]:
         with pytest.raises(vp.VPError):
             vp.Catalog(topo)
 
@@ -122,7 +129,8 @@ def assert_same_catalog(a, b):
 
 
 @pytest.mark.parametrize("topo", [vpgen.tiny_topology(), vpgen.config(1).topo, vpgen.config(2).topo,
-                                  vpgen.config(5).topo, vpgen.Topology(3, 1, 2, 3), vpgen.Topology(2, 2, 1, 4)])
+                                  vpgen.config(5).topo, vpgen.Topology(3, 1, 2, 3), vpgen.Topology(2, 2, 1, 4),
+                                  vpgen.Topology(1, 1, 2, 2, 2), vpgen.Topology(2, 1, 2, 2, 2)])
 def test_catalog_save_load_round_trip(vp, topo):
     c = vp.Catalog(topo)
     p = c.save()
@@ -273,3 +281,39 @@ def test_plan_noalloc_refuses_more_than_256_ranks(vp):
                                   None, None, None)
     assert st == vp.UNSUPPORTED
     assert b"256" in vp.lib().vp_last_error()
+
+
+def test_catalog_load_rejects_a_family_under_other_nic_names(vp):
+    """With two NICs per switch a payload may name each family only by its
+    renaming class's representative: the same family with the two NICs of a
+    switch swapped is refused even though it is feasible and in order."""
+    topo = vpgen.Topology(1, 1, 2, 2, 2)
+    c = vp.Catalog(topo)
+    inst = c.instances()
+    body = bytearray(c.save()[:-8])
+    QG = 4
+    F0 = int.from_bytes(body[HEAD - 12:HEAD - 8], "little")
+    swapped = None
+    for f in range(F0):
+        ids = list(body[HEAD + f * QG:HEAD + (f + 1) * QG])
+        if not any(inst["cls"][i] == vp.PATH_NIC for i in ids):
+            continue
+        # swap the source NICs of switch 0 (copy = x * 2 + y)
+        new = []
+        for i in ids:
+            if inst["cls"][i] == vp.PATH_NIC and inst["src"][i] == 0:
+                cp = int(inst["copy"][i]) ^ 2
+                j = [k for k in range(len(inst["cls"])) if inst["cls"][k] == vp.PATH_NIC and
+                     inst["src"][k] == inst["src"][i] and inst["dst"][k] == inst["dst"][i] and inst["copy"][k] == cp][0]
+                new.append(j)
+            else:
+                new.append(i)
+        if sorted(new) != ids:
+            swapped = sorted(new)
+            break
+    assert swapped is not None
+    # replace the whole catalog by that one renamed family
+    body[HEAD - 12:HEAD - 8] = (1).to_bytes(4, "little")
+    with pytest.raises(vp.VPError) as e:
+        vp.Catalog.load(reseal(bytes(body[:HEAD]) + bytes(swapped)))
+    assert "NIC" in str(e.value)

@@ -337,3 +337,70 @@ def test_sys_circulant_subset_of_full_catalog():
     for f in cluster_families(full):
         inst |= instantiate(tm, f)
     assert inst == brute_force_channels(tm)
+
+
+# ------------------------------------------------ several NICs per switch
+
+def multi_nic(n_nodes=1, sockets=1, switches=2, g=2, m=2):
+    return vpgen.Topology(n_nodes, sockets, switches, g, nics_per_switch=m)
+
+
+def labels_of(cat, f):
+    """Cluster view of family f and the path label of each instance: the
+    source and destination NIC of its NIC lanes (from the instance's copy)."""
+    cf = cat.cluster_family(f)
+    copy = cat.table()["copy"]
+    m = cat.topo.nics_per_switch
+    labs = [(NIC, int(copy[i]) // m, int(copy[i]) % m) if c == NIC else (int(c), -1, -1)
+            for c, i in zip(cf["cls"], cf["id"])]
+    return cf, labs
+
+
+def test_multi_nic_hand_counts():
+    """Two NICs per switch, counted by hand with Burnside's lemma over the
+    renamings of each switch's two NICs.  One socket with two switches of two
+    GPUs: all-PIX (1 family); one lane each way plus a PIX lane per switch
+    (PXB or one of four NIC pairs each way: 25 choices, 7 classes); two lanes
+    each way (PXB plus a NIC pair, or two NIC lanes on disjoint NICs: 6
+    choices each way, 36 in all, 10 classes): 3 shapes, 18 families.  Two
+    sockets of one switch each (NIC paths only across): 1 + 4 + 2 = 7."""
+    a = oracle.Catalog(multi_nic())
+    assert (a.n_shapes, a.n_families) == (3, 18)
+    b = oracle.Catalog(multi_nic(sockets=2, switches=1))
+    assert (b.n_shapes, b.n_families) == (3, 7)
+
+
+@pytest.mark.parametrize("topo", [multi_nic(), multi_nic(sockets=2, switches=1), multi_nic(g=3)],
+                         ids=["one-socket", "two-sockets", "three-gpus"])
+def test_brute_force_multi_nic_equals_catalog_up_to_renaming(topo):
+    """Every channel that brute force finds over derangements and labelled
+    path vectors (Eq. (1)), renamed to its smallest form, is an instantiation
+    of exactly one catalog family renamed the same way."""
+    from oracle.checks import brute_force_labeled, canonical_labeled, instantiate_labeled
+    tm = TopoModel(topo)
+    cat = oracle.Catalog(topo)
+    seen = set()
+    for f in range(cat.n_families):
+        cf, labs = labels_of(cat, f)
+        got = {canonical_labeled(tm, ch) for ch in instantiate_labeled(tm, cf, labs)}
+        assert got, "family with no valid endpoint binding"
+        assert not (got & seen), "two families differ only by NIC names"
+        seen |= got
+    assert seen == {canonical_labeled(tm, ch) for ch in brute_force_labeled(tm)}
+
+
+def test_multi_nic_families_satisfy_eq3_eq4():
+    """The 8-GPU node with two NICs per switch: every family is balanced and
+    uses no labelled resource twice."""
+    from oracle.checks import shared_labeled
+    topo = vpgen.Topology(1, nics_per_switch=2)
+    cat = oracle.Catalog(topo)
+    tm = TopoModel(topo)
+    for f in range(0, cat.n_families, 37):
+        cf, labs = labels_of(cat, f)
+        outd, ind, used = collections.Counter(cf["a"].tolist()), collections.Counter(cf["d"].tolist()), set()
+        assert all(v == tm.g for v in outd.values()) and all(v == tm.g for v in ind.values())
+        for lab, a, d in zip(labs, cf["a"], cf["d"]):
+            for r in shared_labeled(tm, lab, int(a), int(d)):
+                assert r not in used
+                used.add(r)
