@@ -43,7 +43,21 @@ PEAK_HBM_GBS = 8000.0
 HERE = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "pack_gather_traffic.json")
 KERNEL_NAME = {"moe": "scatter_rows_kernel (vp_pack_gather, token rows)",
-               "heads": "gather_kernel (vp_pack_gather, heads)"}
+               "heads": "gather_heads_kernel (vp_pack_gather, head units)"}
+
+
+def host_cpu():
+    """Model name of the host CPU and the threads this process may run on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
 
 
 def pack_source_sha() -> str:
@@ -83,10 +97,37 @@ def cpu_baseline(w, routing_np, tokens_np):
     S, U, rows = rank0_accounting(w, routing_np[0])
     slices = int((s["bytes"][:, 0] > 0).sum())
     pack_bytes = S + U + 4 * rows + 16 * slices
+    model, threads = host_cpu()
     return dict(value=round(pack_bytes / (t3 - t2) / 1e9, 3), unit="GB/s", cores=1, kind="oracle",
+                cpu_model=model, host_threads_visible=threads,
                 sample="one %d x %d matrix of the workload: demand of all %d ranks, one plan (K=%d), "
                        "rank-0 pack of %.1f MB" % (w.n_ranks, w.n_ranks, w.n_ranks, s["K"], send.size / 1e6),
                 demand_s=round(t1 - t0, 3), plan_us_per_matrix=round((t2 - t1) * 1e6, 1),
+                pack_s=round(t3 - t2, 4))
+
+
+def cpu_baseline_heads(w, act_np):
+    """The oracle, single-threaded, on the Ulysses workload: every rank's
+    head-demand row, one plan, and rank 0's head pack."""
+    import oracle
+    import vpgen
+    cat = oracle.Catalog(w.topo)
+    hl = vpgen.head_split(w.heads, w.n_ranks)
+    t0 = time.perf_counter()
+    D = np.stack([oracle.demand_heads(w.tokens, hl, w.row_bytes, i) for i in range(w.n_ranks)])
+    t1 = time.perf_counter()
+    s = cat.plan(D, w.row_bytes)
+    t2 = time.perf_counter()
+    send, _ = oracle.pack_heads(act_np, w.token_stride, hl, w.row_bytes, 0, s)
+    t3 = time.perf_counter()
+    slices = int((s["bytes"][:, 0] > 0).sum())
+    pack_bytes = 2 * send.size + 16 * slices
+    model, threads = host_cpu()
+    return dict(value=round(pack_bytes / (t3 - t2) / 1e9, 3), unit="GB/s", cores=1, kind="oracle",
+                cpu_model=model, host_threads_visible=threads,
+                sample="the %d x %d head-demand matrix: demand of all %d ranks, one plan (K=%d), rank-0 head "
+                       "pack of %.1f MB" % (w.n_ranks, w.n_ranks, w.n_ranks, s["K"], send.size / 1e6),
+                demand_s=round(t1 - t0, 4), plan_us_per_matrix=round((t2 - t1) * 1e6, 1),
                 pack_s=round(t3 - t2, 4))
 
 
@@ -418,7 +459,12 @@ def summary(w, r):
             # byte read and written once; cache-served duplicate rows can make
             # it exceed what HBM carried)
             "pack_us_median": round(float(np.median(r["pack_ms"]) * 1e3), 1),
-            "pack_logical_2S_GBps": round(float(2 * r["send_bytes"].sum() / (r["pack_ms"].sum() * 1e-3) / 1e9), 2)}
+            "pack_logical_2S_GBps": round(float(2 * r["send_bytes"].sum() / (r["pack_ms"].sum() * 1e-3) / 1e9), 2),
+            # the copy kernel alone (its launch, HIP events): algorithmic bytes over its time
+            "copy_kernel": KERNEL_NAME[w.mode],
+            "copy_us": round(float(r["gather_ms"].mean() * 1e3), 2),
+            "copy_frac_of_hbm_peak": round(float(r["gather_bytes"].sum() / (r["gather_ms"].sum() * 1e-3) / 1e9)
+                                           / PEAK_HBM_GBS, 4)}
 
 
 def main():
@@ -534,7 +580,7 @@ def main():
         if w.mode == "moe":
             out["cpu_baseline"] = cpu_baseline(w, r["routing_np"][0], r["tokens_np"])
         else:
-            out["cpu_baseline"] = None
+            out["cpu_baseline"] = cpu_baseline_heads(w, r["tokens_np"])
     print(json.dumps(out), flush=True)
 
 
