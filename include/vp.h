@@ -373,9 +373,14 @@ vp_status vp_pack_rows(const void* tokens, int64_t T, int32_t k, int64_t row_byt
  * owns, [head_lo[j], head_lo[j+1]) (device int64 [N+1]); units are single
  * heads of head_bytes (a multiple of 16); activations are [T, token_stride].
  * Every head a destination owns must lie inside the token row, else
- * VP_ERR_INVALID_ARGUMENT.  T * (token_stride / head_bytes)^2 must stay
- * below 2^47 and token_stride / head_bytes at or below 2^15
- * (VP_ERR_UNSUPPORTED). */
+ * VP_ERR_INVALID_ARGUMENT.  With the planner's layout, k_max <= 512 and
+ * n_ranks <= 1024 the checks and the copy run as one kernel, in which every
+ * workgroup checks the whole schedule before it copies (so an error still
+ * writes nothing to send); otherwise the two halves below run.  Limits
+ * (VP_ERR_UNSUPPORTED): token_stride / head_bytes at most 2^15, head_bytes
+ * below 2^23, token_stride below 2^32, send_capacity below 2^52, and
+ * T * (token_stride / head_bytes)^2 and (send_capacity / 16) * (head_bytes /
+ * 16) below 2^63. */
 vp_status vp_pack_heads(const void* act, int64_t T, int64_t token_stride, const int64_t* head_lo,
                         int64_t head_bytes, int32_t self_rank, int32_t n_ranks, const int32_t* K,
                         const int32_t* dst, const int64_t* bytes, const int64_t* send_off,
@@ -386,15 +391,15 @@ vp_status vp_pack_heads(const void* act, int64_t T, int64_t token_stride, const 
  * or time the copy on its own.  vp_pack_prepare_* take the same arguments
  * minus `send` and run the slice (without the planner's layout) and index
  * kernels: they fill step_off and the workspace (the copy lists of every
- * token or the source offset of every unit) and check every slice and the
- * capacity.  vp_pack_gather then copies the units from `src` (the tokens or
+ * token, or one descriptor per step for heads) and check every slice and
+ * the capacity.  vp_pack_gather then copies the units from `src` (the tokens or
  * activations given to the prepare call) into `send` with 16-byte loads and
  * non-temporal stores; it must get the same unit_bytes, T, k (0 after
  * vp_pack_prepare_heads), k_max, send_capacity and workspace, and no other
  * prepare on that workspace may come between.  It writes nothing when
- * dev_status already holds an error.  Heads: every unit's source address is
- * derived from its step's checked descriptor and checked against the
- * activations again before the load. */
+ * dev_status already holds an error.  Heads: every step's descriptor is
+ * checked against the activations and the send buffer again before its
+ * units are copied, and every unit's source address follows from it. */
 vp_status vp_pack_prepare_rows(const void* tokens, int64_t T, int32_t k, int64_t row_bytes,
                                const int32_t* sorted_tok, const uint8_t* sorted_slot,
                                const int64_t* dest_off, int32_t self_rank, int32_t n_ranks,

@@ -697,11 +697,35 @@ class Pipeline:
                "vp_pack_gather")
         return send
 
+    def pack_stage(self, tokens: torch.Tensor, head_lo: Optional[torch.Tensor] = None,
+                   send: Optional[torch.Tensor] = None, stream=None):
+        """The pack in one call (vp_pack_rows / vp_pack_heads): both halves,
+        or for heads with a short schedule one kernel that does both."""
+        send = self.send if send is None else send
+        if send.numel() < self.send_capacity:
+            raise ValueError("send buffer smaller than the pipeline's capacity")
+        L, s, p = lib(), _stream(stream), self.params
+        if self.mode == "moe":
+            T = tokens.numel() * tokens.element_size() // self.unit
+            _check(L.vp_pack_rows(_ptr(tokens), T, self.k, self.unit, _ptr(self.dem["sorted_tok"]),
+                                  _ptr(self.dem["sorted_slot"]), _ptr(self.dem["dest_off"]), self.self_rank, self.N,
+                                  _ptr(self.sched["K"]), _ptr(self.sched["dst"]), _ptr(self.sched["bytes"]),
+                                  _ptr(self.sched["send_off"]), _ptr(self.sched["stream_off"]), p.k_max, _ptr(send),
+                                  self.send_capacity, _ptr(self.step_off), _ptr(self.status), _ptr(self.pack_ws),
+                                  self.pack_ws.numel(), s), "vp_pack_rows")
+        else:
+            T = tokens.numel() * tokens.element_size() // self.token_stride
+            _check(L.vp_pack_heads(_ptr(tokens), T, self.token_stride, _ptr(head_lo), self.unit, self.self_rank,
+                                   self.N, _ptr(self.sched["K"]), _ptr(self.sched["dst"]), _ptr(self.sched["bytes"]),
+                                   _ptr(self.sched["send_off"]), _ptr(self.sched["stream_off"]), p.k_max, _ptr(send),
+                                   self.send_capacity, _ptr(self.step_off), _ptr(self.status), _ptr(self.pack_ws),
+                                   self.pack_ws.numel(), s), "vp_pack_heads")
+        return send
+
     def step(self, routing: Optional[torch.Tensor] = None, tokens: Optional[torch.Tensor] = None,
              head_lo: Optional[torch.Tensor] = None, send: Optional[torch.Tensor] = None, stream=None):
         """demand (+ control words) -> plan -> pack for one matrix; returns the send buffer."""
         self.demand_stage(routing, head_lo, stream)
         self.words_stage(stream)
         self.plan_stage(stream)
-        self.pack_prepare_stage(tokens, head_lo, stream)
-        return self.pack_gather_stage(tokens, send, stream)
+        return self.pack_stage(tokens, head_lo, send, stream)

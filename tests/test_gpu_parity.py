@@ -524,6 +524,79 @@ def test_pack_heads_parity(vp, self_rank, layout):
     assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off)
 
 
+# (N, self rank, head bytes, heads per rank, tokens, steps, largest slice in
+# units, spare send capacity in units, row padding in bytes)
+HEADS_SHAPES = [
+    (4, 1, 16, [1, 2, 5, 3], 777, 600, 4, 0, 0),
+    (3, 0, 48, [2, 2, 3], 513, 60, 200, 7, 48),
+    (5, 4, 4096, [1, 3, 2, 1, 2], 100, 40, 30, 0, 0),
+    (6, 2, 272, [2, 1, 1, 3, 2, 2], 1000, 120, 500, 1000, 16),
+    (2, 1, 256, [3, 1], 4096, 9, 4096, 20000, 0),
+]
+
+
+def random_heads_schedule(rng, N, self_rank, T, hl, K, max_units, unit):
+    """A schedule whose lane for self_rank sends, step by step, the next
+    slice of a random destination's head stream (a quarter of the steps
+    idle, streams partly covered when the steps run out); the other lanes
+    are a fixed derangement with no bytes, which the pack never reads."""
+    left = T * np.diff(hl)
+    left[self_rank] = 0
+    dst = np.empty((K, N), np.int32)
+    nb = np.zeros((K, N), np.int64)
+    rows = np.arange(N)
+    for k in range(K):
+        dst[k] = (rows + 1 + k % (N - 1)) % N
+        open_ = np.flatnonzero(left > 0)
+        if open_.size == 0 or rng.random() < 0.25:
+            continue
+        j = int(rng.choice(open_))
+        x = int(rng.integers(1, min(left[j], max_units) + 1))
+        dst[k, self_rank] = j
+        nb[k, self_rank] = x * unit
+        left[j] -= x
+    return {"K": K, "dst": dst, "bytes": nb}
+
+
+@pytest.mark.parametrize("layout", [False, True])
+@pytest.mark.parametrize("shape", range(len(HEADS_SHAPES)))
+def test_pack_heads_shapes(vp, shape, layout):
+    """The heads pack on random schedules over other shapes than the
+    Ulysses workload: 16-byte heads with more than 256 steps of a few units
+    each (the gather's two-level step search, ranges that meet many steps),
+    48- and 272-byte heads (unit vectors not a power of two), 4 KiB heads,
+    a destination with one head, padded token rows, send buffers much
+    larger than the total, and a few long steps over a two-rank stream."""
+    N, self_rank, unit, per, T, K, max_units, spare, pad = HEADS_SHAPES[shape]
+    log("pack heads shape %d layout %s" % (shape, layout))
+    rng = np.random.default_rng(100 + shape)
+    hl = np.concatenate([[0], np.cumsum(per)]).astype(np.int64)
+    stride = int(hl[-1]) * unit + pad
+    act = rng.integers(0, 256, T * stride, dtype=np.uint8)
+    s = random_heads_schedule(rng, N, self_rank, T, hl, K, max_units, unit)
+    ref, ref_off = oracle.pack_heads(act, stride, hl, unit, self_rank, s)
+    k_max = K + 3
+    sched = vp.alloc_schedule(N, k_max, layout=layout)
+    sched["K"].fill_(K)
+    sched["dst"][:K] = torch.from_numpy(s["dst"]).cuda()
+    sched["bytes"][:K] = torch.from_numpy(s["bytes"]).cuda()
+    if layout:
+        so, co = layout_np(s["dst"], s["bytes"])
+        sched["send_off"][:K] = torch.from_numpy(so).cuda()
+        sched["stream_off"][:K] = torch.from_numpy(co).cuda()
+    cap = ref.size + spare * unit
+    send = torch.full((cap + 64,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(k_max + 1, dtype=torch.int64, device="cuda")
+    st = vp.new_status()
+    vp.pack_heads(torch.from_numpy(act).cuda(), stride, torch.from_numpy(hl).cuda(), unit, self_rank, sched,
+                  send[:cap], step_off, st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    assert torch.equal(send[:ref.size], torch.from_numpy(ref).cuda())
+    assert (send[ref.size:] == 0xA5).all()
+    assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off)
+
+
 @pytest.mark.parametrize("where", ["first", "middle", "last"])
 def test_pack_rejects_a_layout_that_does_not_tile(vp, where):
     """A send-offset layout that leaves a gap (here one unit) is refused by
@@ -601,6 +674,40 @@ def test_pipeline_matches_oracle(vp, cid):
     assert np.array_equal(pipe.dem["demand"].cpu().numpy(), D)
     assert_schedule_equal(vp.schedule_to_host(pipe.sched), s)
     assert torch.equal(send[:ref.size], torch.from_numpy(ref).cuda())
+
+
+@pytest.mark.parametrize("cid", [1, 4])
+def test_pack_two_halves_match_one_call(vp, cid):
+    """vp_pack_prepare_* followed by vp_pack_gather gives the send buffer and
+    step offsets of the one-call pack on the pipeline's schedule; for heads
+    the two halves are a different kernel pair than the one-kernel pack."""
+    log("pack halves C%d" % cid)
+    if cid == 4:
+        w, hl, D = heads_case()
+        pipe = vp.Pipeline(w.topo, "heads", w.row_bytes, tokens=w.tokens, token_stride=w.token_stride)
+        tok = torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda()
+        head_lo = torch.from_numpy(hl).cuda()
+        one = pipe.step(tokens=tok, head_lo=head_lo).clone()
+    else:
+        w, R, dem, D = moe_case(cid)
+        pipe = vp.Pipeline(w.topo, "moe", w.row_bytes, n_experts=w.experts, tokens=w.tokens, top_k=w.top_k)
+        tok = torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda()
+        head_lo = None
+        one = pipe.step(routing=torch.from_numpy(R).cuda(), tokens=tok).clone()
+    torch.cuda.synchronize()
+    assert vp.read_status(pipe.status) == 0
+    K = int(pipe.sched["K"].item())
+    off_one = pipe.step_off[:K + 1].clone()
+    two = torch.full_like(one, 0x5A)
+    pipe.step_off.fill_(-1)
+    pipe.pack_prepare_stage(tok, head_lo)
+    pipe.pack_gather_stage(tok, two)
+    torch.cuda.synchronize()
+    assert vp.read_status(pipe.status) == 0
+    total = int(off_one[K].item())
+    assert total > 0
+    assert torch.equal(pipe.step_off[:K + 1], off_one)
+    assert torch.equal(two[:total], one[:total])
 
 
 def test_plan_largest_topology_is_a_valid_decomposition(vp):
