@@ -41,7 +41,7 @@ import numpy as np
 METRIC = "pack HBM GB/s (% of peak) + vp_plan µs per N×N demand matrix, N=8..256"
 PEAK_HBM_GBS = 8000.0
 HERE = os.path.dirname(os.path.abspath(__file__))
-TRAFFIC_FILE = os.path.join(HERE, "profiles", "pack_gather_traffic.json")
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "pack_traffic.json")
 KERNEL_NAME = {"moe": "scatter_rows_kernel (vp_pack_gather, token rows)",
                "heads": "pack_heads_kernel (vp_pack_heads: schedule checks and copy in one kernel)"}
 
@@ -131,7 +131,7 @@ def cpu_baseline_heads(w, act_np):
                 pack_s=round(t3 - t2, 4))
 
 
-def measure(w, steps, warmup, M, dev):
+def measure(w, steps, warmup, M, dev, graph=True):
     """Time `steps` demand -> plan -> pack steps of workload `w` on one stream
     (after `warmup` untimed ones), cycling over M matrices and two send
     buffers.  Returns the per-stage event times and the per-matrix facts."""
@@ -172,9 +172,18 @@ def measure(w, steps, warmup, M, dev):
         pipe.plan_stage()
         if ev is not None:
             ev[3].record()
-        pipe.pack_stage(tokens, head_lo, sends[step % 2])
+        # rows: the pack's two halves, so that the copy kernel has events of
+        # its own; heads: the one-kernel pack (no separate prepare)
+        if w.mode == "moe":
+            pipe.pack_prepare_stage(tokens, head_lo)
         if ev is not None:
             ev[4].record()
+        if w.mode == "moe":
+            pipe.pack_gather_stage(tokens, sends[step % 2])
+        else:
+            pipe.pack_stage(tokens, head_lo, sends[step % 2])
+        if ev is not None:
+            ev[5].record()
 
     for s in range(warmup):
         run(s)
@@ -182,7 +191,7 @@ def measure(w, steps, warmup, M, dev):
     if vp.read_status(pipe.status) != 0:
         raise SystemExit("device error during warmup: %d" % vp.read_status(pipe.status))
 
-    evs = [[E() for _ in range(5)] for _ in range(steps)]
+    evs = [[E() for _ in range(6)] for _ in range(steps)]
     start, end = E(), E()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -198,7 +207,9 @@ def measure(w, steps, warmup, M, dev):
              demand_ms=np.array([e[0].elapsed_time(e[1]) for e in evs]),
              words_ms=np.array([e[1].elapsed_time(e[2]) for e in evs]),
              plan_ms=np.array([e[2].elapsed_time(e[3]) for e in evs]),
-             pack_ms=np.array([e[3].elapsed_time(e[4]) for e in evs]))
+             prep_ms=np.array([e[3].elapsed_time(e[4]) for e in evs]),
+             copy_ms=np.array([e[4].elapsed_time(e[5]) for e in evs]))
+    r["pack_ms"] = r["prep_ms"] + r["copy_ms"]
 
     # the copy kernel on its own: 50 launches captured in a HIP graph and
     # replayed between two events, so that neither the host's launch cost nor
@@ -226,20 +237,21 @@ def measure(w, steps, warmup, M, dev):
         del g
         return a.elapsed_time(b) / reps
 
-    sends[0].zero_()
-    pipe.pack_stage(tokens, head_lo, sends[0])
-    torch.cuda.synchronize()
-    eager = sends[0].clone()
-    sends[0].zero_()
-    if w.mode == "moe":
-        r["prep_graph_ms"] = graph_ms(lambda: pipe.pack_prepare_stage(tokens, head_lo))
-        r["copy_graph_ms"] = graph_ms(lambda: pipe.pack_gather_stage(tokens, sends[0]))
-    else:
-        r["copy_graph_ms"] = graph_ms(lambda: pipe.pack_stage(tokens, head_lo, sends[0]))
-    torch.cuda.synchronize()
-    if vp.read_status(pipe.status) != 0 or not torch.equal(sends[0], eager):
-        raise SystemExit("the graph-replayed pack differs from the eager one")
-    del eager
+    if graph:
+        sends[0].zero_()
+        pipe.pack_stage(tokens, head_lo, sends[0])
+        torch.cuda.synchronize()
+        eager = sends[0].clone()
+        sends[0].zero_()
+        if w.mode == "moe":
+            r["prep_graph_ms"] = graph_ms(lambda: pipe.pack_prepare_stage(tokens, head_lo))
+            r["copy_graph_ms"] = graph_ms(lambda: pipe.pack_gather_stage(tokens, sends[0]))
+        else:
+            r["copy_graph_ms"] = graph_ms(lambda: pipe.pack_stage(tokens, head_lo, sends[0]))
+        torch.cuda.synchronize()
+        if vp.read_status(pipe.status) != 0 or not torch.equal(sends[0], eager):
+            raise SystemExit("the graph-replayed pack differs from the eager one")
+        del eager
 
     # one rank's own row (R = 1: its routing, counts, demand row and sort),
     # the unit each rank runs in deployment; mean of 20 calls, HIP events
@@ -500,10 +512,15 @@ def summary(w, r):
             # algorithmic bytes over its time (rows: the scatter half, after
             # a prepare of prepare_us_graph; heads: the one-kernel pack)
             "copy_kernel": KERNEL_NAME[w.mode],
-            "copy_us_graph": round(float(r["copy_graph_ms"] * 1e3), 2),
+            "copy_us_graph": round(float(r["copy_graph_ms"] * 1e3), 2) if "copy_graph_ms" in r else None,
             "copy_frac_of_hbm_peak": round(float(r["gather_bytes"][-1] / (r["copy_graph_ms"] * 1e-3) / 1e9)
-                                           / PEAK_HBM_GBS, 4),
-            "prepare_us_graph": round(float(r["prep_graph_ms"] * 1e3), 2) if "prep_graph_ms" in r else None}
+                                           / PEAK_HBM_GBS, 4) if "copy_graph_ms" in r else None,
+            "prepare_us_graph": round(float(r["prep_graph_ms"] * 1e3), 2) if "prep_graph_ms" in r else None,
+            # the same kernel inside the timed steps (events around it: for
+            # short kernels the events' own cost is a visible share)
+            "copy_us_in_steps": round(float(r["copy_ms"].mean() * 1e3), 2),
+            "copy_frac_in_steps": round(float(r["gather_bytes"].sum() / (r["copy_ms"].sum() * 1e-3) / 1e9)
+                                        / PEAK_HBM_GBS, 4)}
 
 
 def main():
@@ -520,6 +537,8 @@ def main():
     ap.add_argument("--no-receive", action="store_true", help="skip the receive-side and combine timings")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the planner on the extra demands and the nearest-path ablation")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the graph-replayed timing of the copy kernel (counter runs)")
     ap.add_argument("--calibrate-copy", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB")
     args = ap.parse_args()
@@ -538,18 +557,24 @@ def main():
     M = max(1, min(args.matrices, args.steps))
     print("[bench] %s: %d matrices, %d warmup + %d timed steps" % (w.name, M, args.warmup, args.steps),
           file=sys.stderr, flush=True)
-    r = measure(w, args.steps, args.warmup, M, dev)
+    r = measure(w, args.steps, args.warmup, M, dev, graph=not args.no_graph)
     head = summary(w, r)
     # the copy kernel's algorithmic bytes on the last matrix over its
-    # graph-replayed launch time
-    achieved = float(r["gather_bytes"][-1] / (r["copy_graph_ms"] * 1e-3) / 1e9)
+    # graph-replayed launch time (without the graph: over its time in the
+    # timed steps)
+    if "copy_graph_ms" in r:
+        achieved = float(r["gather_bytes"][-1] / (r["copy_graph_ms"] * 1e-3) / 1e9)
+        timing = "50 launches replayed from a HIP graph between two HIP events"
+    else:
+        achieved = float(r["gather_bytes"].sum() / (r["copy_ms"].sum() * 1e-3) / 1e9)
+        timing = "HIP events around the kernel in the timed steps"
 
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
-        if t.get("kernel_source_sha") == pack_source_sha() and t.get("workload") == w.name:
-            traffic = t.get("bytes_per_launch")
+        if t.get("kernel_source_sha") == pack_source_sha() and w.name in t.get("workloads", {}):
+            traffic = t["workloads"][w.name].get("bytes_per_launch")
 
     if args.calibrate_copy:
         n = args.calibrate_copy << 20
@@ -595,8 +620,10 @@ def main():
                      "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": int(r["gather_bytes"][-1]),
-                     "avg_launch_us": head["copy_us_graph"],
-                     "timing": "50 launches replayed from a HIP graph between two HIP events"},
+                     "avg_launch_us": head["copy_us_graph"] if "copy_graph_ms" in r else head["copy_us_in_steps"],
+                     "timing": timing,
+                     "avg_launch_us_in_steps": head["copy_us_in_steps"],
+                     "frac_in_steps": head["copy_frac_in_steps"]},
         "prepare_us_graph": head["prepare_us_graph"],
     }
     if w.mode == "moe" and not args.no_receive:
