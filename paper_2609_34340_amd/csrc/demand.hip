@@ -10,14 +10,18 @@
 //                  the sorted row per 2048-id chunk (expert-major).
 //   sort_scan      only for sorted rows of more than 64 chunks: one
 //                  workgroup turns the chunk counts into offsets.
-//   demand_finish  pass 2: one workgroup per row sums its parts into the
-//                  row's counts and demand row; one workgroup per sort chunk
-//                  derives the chunk's offsets from all chunk counts (expert
-//                  totals, a block scan, the earlier chunks' counts) and
-//                  places its ids: a stable rank inside each wave's ids from
-//                  a match mask built with one ballot per bit of the expert
-//                  id plus a prefix popcount, then the waves' counts scanned
-//                  per expert.
+//   demand_finish  pass 2: one workgroup per row sums its parts (at most
+//                  16 per row for rows up to 131,072 ids: one round of
+//                  loads) into the row's counts and demand row; one
+//                  workgroup per sort chunk places its ids: a stable rank
+//                  inside each wave's ids from a match mask built with one
+//                  ballot per bit of the expert id plus a prefix popcount,
+//                  while the chunk counts it needs are in flight; then the
+//                  chunk's offsets from all chunk counts (expert totals, a
+//                  block scan, the earlier chunks' counts) and the waves'
+//                  counts scanned per expert.  Loads are unconditional
+//                  (clamped indexes, masked results) so that each wait
+//                  covers only the load it needs.
 //   No workgroup waits for another: the kernel boundary publishes pass 1.
 //   control_words / receive_counts  the sparse expert-parallel control word
 //                 of every (source, destination) pair from the counts, and
@@ -228,6 +232,12 @@ __device__ inline int32_t block_excl_scan(int32_t* v, int n, int32_t* wtot) {
 // wave v ranks the ids [v*64*kPerThread, ...) with one ballot per id bit
 // (a match mask) and a prefix popcount; the waves' counts are then scanned
 // per expert.
+// Offsets of a sort chunk: from the scan kernel, or from every chunk's
+// counts (at most kInBlockScan chunks) held in registers (up to 256
+// experts) or reloaded.
+enum { kOffScanned = 0, kOffHeld = 1, kOffReload = 2 };
+
+template <int OFF>
 __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
   extern __shared__ int32_t sh[];   // rows: E; chunks: off [E], tot [E], wc [kWaves][E]
   __shared__ int32_t wtot[kWaves];
@@ -266,45 +276,36 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
   int32_t* tot = sh + E;
   int32_t* wc = sh + 2 * E;
   const int32_t* ids = a.routing + (size_t)a.sort_row * a.Tk;
-  // the chunk's ids first: their loads overlap the offsets' work
+  if (a.Tk <= 0) {   // an empty row: every destination's range is empty
+    if (chunk == 0)
+      for (int j = tid; j <= a.N; j += kThreads) a.dest_off[j] = 0;
+    return;
+  }
+  // the chunk's ids first, then its chunk counts, all loads unconditional
+  // (indexes clamped into range, results masked after) so that the ranking
+  // below waits for the ids only and the counts' latency hides behind it
   const int64_t base = (int64_t)chunk * kChunk + (int64_t)w * 64 * kPerThread;
   int ev[kPerThread];
 #pragma unroll
   for (int m = 0; m < kPerThread; ++m) {
     const int64_t x = base + m * 64 + lane;
-    ev[m] = x < a.Tk ? ids[x] : -1;
+    ev[m] = ids[x < a.Tk ? x : a.Tk - 1];
   }
-  if (a.scanned) {
+  // The chunk counts: the scan kernel's offsets, or every chunk's counts of
+  // the thread's experts (at most kInBlockScan chunks, 16 loads of four)
+  // held in registers through the ranking, which does not depend on them.
+  constexpr int kEPT = 256 / kThreads;   // experts per thread held in registers (E <= 256)
+  int4 cv[kEPT][kInBlockScan / 4];
+  if (OFF == kOffScanned) {
     for (int e = tid; e < E; e += kThreads) off[e] = a.ccount[(size_t)e * a.nch4 + chunk];
-  } else {
-    for (int e = tid; e < E; e += kThreads) {
-      // this expert's counts of every chunk: up to 16 loads of four in
-      // flight (at most kInBlockScan chunks)
-      const int4* q = (const int4*)(a.ccount + (size_t)e * a.nch4);
-      const int n4 = a.nch4 / 4;
-      int4 v[kInBlockScan / 4];
+  } else if (OFF == kOffHeld) {
+    const int n4 = a.nch4 / 4;
 #pragma unroll
-      for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) v[c4] = c4 < n4 ? q[c4] : make_int4(0, 0, 0, 0);
-      int32_t all = 0, before = 0;
+    for (int m = 0; m < kEPT; ++m) {
+      const int e = tid + m * kThreads;
+      const int4* q = (const int4*)(a.ccount + (size_t)(e < E ? e : 0) * a.nch4);
 #pragma unroll
-      for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) {
-        const int32_t x4[4] = {v[c4].x, v[c4].y, v[c4].z, v[c4].w};
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          all += x4[m];
-          before += 4 * c4 + m < chunk ? x4[m] : 0;
-        }
-      }
-      tot[e] = all;
-      off[e] = before;
-    }
-    __syncthreads();
-    const int32_t total = block_excl_scan(tot, E, wtot);
-    for (int e = tid; e < E; e += kThreads) off[e] += tot[e];
-    if (chunk == 0) {
-      const int eloc = E / a.N;
-      for (int j = tid; j < a.N; j += kThreads) a.dest_off[j] = tot[j * eloc];
-      if (tid == 0) a.dest_off[a.N] = total;
+      for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) cv[m][c4] = q[c4 < n4 ? c4 : n4 - 1];
     }
   }
   int32_t* mine = wc + w * E;
@@ -314,6 +315,8 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
   int rk[kPerThread];
 #pragma unroll
   for (int m = 0; m < kPerThread; ++m) {
+    // ids past the row are no ids
+    if (base + m * 64 + lane >= a.Tk) ev[m] = -1;
     const int e = ev[m];
     const bool ok = (unsigned)e < (unsigned)E;
     uint64_t same = __ballot(ok);
@@ -325,6 +328,60 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
     wave_sync();
     if (ok && (same & lt) == 0) mine[e] += __popcll(same);   // lowest lane of the group advances
     wave_sync();
+  }
+  if (OFF != kOffScanned) {
+    if (OFF == kOffHeld) {
+      const int n4 = a.nch4 / 4;
+#pragma unroll
+      for (int m = 0; m < kEPT; ++m) {
+        const int e = tid + m * kThreads;
+        int32_t all = 0, before = 0;
+#pragma unroll
+        for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) {
+          // the clamped loads past the last chunk count nothing
+          const bool in = c4 < n4;
+          const int32_t x4[4] = {in ? cv[m][c4].x : 0, in ? cv[m][c4].y : 0, in ? cv[m][c4].z : 0,
+                                 in ? cv[m][c4].w : 0};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            all += x4[q];
+            before += 4 * c4 + q < chunk ? x4[q] : 0;
+          }
+        }
+        if (e < E) {
+          tot[e] = all;
+          off[e] = before;
+        }
+      }
+    } else {
+      for (int e = tid; e < E; e += kThreads) {
+        const int4* q = (const int4*)(a.ccount + (size_t)e * a.nch4);
+        const int n4 = a.nch4 / 4;
+        int4 v[kInBlockScan / 4];
+#pragma unroll
+        for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) v[c4] = c4 < n4 ? q[c4] : make_int4(0, 0, 0, 0);
+        int32_t all = 0, before = 0;
+#pragma unroll
+        for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) {
+          const int32_t x4[4] = {v[c4].x, v[c4].y, v[c4].z, v[c4].w};
+#pragma unroll
+          for (int q2 = 0; q2 < 4; ++q2) {
+            all += x4[q2];
+            before += 4 * c4 + q2 < chunk ? x4[q2] : 0;
+          }
+        }
+        tot[e] = all;
+        off[e] = before;
+      }
+    }
+    __syncthreads();
+    const int32_t total = block_excl_scan(tot, E, wtot);
+    for (int e = tid; e < E; e += kThreads) off[e] += tot[e];
+    if (chunk == 0) {
+      const int eloc = E / a.N;
+      for (int j = tid; j < a.N; j += kThreads) a.dest_off[j] = tot[j * eloc];
+      if (tid == 0) a.dest_off[a.N] = total;
+    }
   }
   __syncthreads();
   for (int e = tid; e < E; e += kThreads) {
@@ -412,11 +469,15 @@ __global__ void __launch_bounds__(256) receive_counts_kernel(const uint32_t* __r
 
 int n_chunks_of(int64_t Tk) { return (int)((Tk + kChunk - 1) / kChunk); }
 
-// Ids per histogram part: kThreads * 2^s with s in [2, 5], the largest that
-// still gives about 2,048 workgroups for the whole launch.
+// Ids per histogram part: kThreads * 2^s with s in [2, 5].  Parts grow
+// until a row has at most 16 of them (the merge then reads all of a row's
+// parts in one round of loads), and beyond that while the launch still gets
+// about 2,048 workgroups.
 int64_t part_of(int32_t R, int64_t Tk) {
   int64_t part = (int64_t)kThreads * 4;
-  while (part < (int64_t)kThreads * 32 && (int64_t)R * ((Tk + 2 * part - 1) / (2 * part)) >= 2048) part *= 2;
+  while (part < (int64_t)kThreads * 32 &&
+         ((Tk + part - 1) / part > 16 || (int64_t)R * ((Tk + 2 * part - 1) / (2 * part)) >= 2048))
+    part *= 2;
   return part;
 }
 
@@ -464,8 +525,13 @@ vp_status launch_demand(const DemandLaunch& a, void* stream) {
     hipLaunchKernelGGL(sort_scan, dim3(1), dim3(1024), 0, s, d.ccount, (int64_t)a.E * w.nch4, a.E, a.N, w.nch4,
                        a.dest_off);
   const int64_t blocks2 = (int64_t)a.R + (sorting ? w.nch : 0);
-  hipLaunchKernelGGL(demand_finish, dim3((unsigned)blocks2), dim3(kThreads),
-                     (size_t)(2 + kWaves) * a.E * sizeof(int32_t), s, d);
+  const size_t lds2 = (size_t)(2 + kWaves) * a.E * sizeof(int32_t);
+  if (d.scanned)
+    hipLaunchKernelGGL(demand_finish<kOffScanned>, dim3((unsigned)blocks2), dim3(kThreads), lds2, s, d);
+  else if (a.E <= 256)
+    hipLaunchKernelGGL(demand_finish<kOffHeld>, dim3((unsigned)blocks2), dim3(kThreads), lds2, s, d);
+  else
+    hipLaunchKernelGGL(demand_finish<kOffReload>, dim3((unsigned)blocks2), dim3(kThreads), lds2, s, d);
   if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "demand launch failed");
   return VP_OK;
 }
