@@ -1185,25 +1185,39 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         at32(ginst, o) = live ? iid[(size_t)best_c * N + t] : bid[t];
         at32(gbytes, o) = x;
         if (grecv_src) at32(grecv_src, (uint32_t)(K * N + j)) = i;   // pi_k is a permutation
+        // A residual that did not fit its 32-bit copy is reloaded from
+        // D^rem.  Every use of such a reload stays inside its own branch,
+        // whose stores are relaxed atomic ones so that they are not merged
+        // with the common path's: a use after the branches would make the
+        // common path wait for every store issued so far (the wait counter
+        // covers stores as well).
+        const bool sat = rv >= kRawSaturated;
         if (gsend_off) {
           // Sec. 5 buffer layout: where this lane's slice sits in rank i's
           // send buffer and in its stream to j (bytes sent there before:
           // D[i][j] minus the residual before this step; D[i][j] is added by
           // stream_off_kernel after the plan, which keeps its load off this
           // loop's critical path)
-          const int64_t before = rv < kRawSaturated ? (int64_t)rv : at32(gDrem, (uint32_t)(i * N + j));
           at32(gsend_off, o) = sacc[i];
-          at32(gstream_off, o) = -before;
+          if (__builtin_expect(!sat, 1))
+            at32(gstream_off, o) = -(int64_t)rv;
+          else
+            __hip_atomic_store(&at32(gstream_off, o), -at32(gDrem, (uint32_t)(i * N + j)), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
           sacc[i] += x;
         }
         if (xu > 0) {
           int64_t* dp = &at32(gDrem, (uint32_t)(i * N + j));
-          int64_t nv;
-          if (__builtin_expect(rv < kRawSaturated, 1)) nv = (int64_t)rv - x;
-          else nv = *dp - x;   // the residual did not fit the 32-bit copy
-          *dp = nv;
+          if (__builtin_expect(!sat, 1)) {
+            const int64_t nv = (int64_t)rv - x;
+            *dp = nv;
+            lastv[i] = nv;
+          } else {
+            const int64_t nv = *dp - x;
+            __hip_atomic_store(dp, nv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&lastv[i], nv, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          }
           lastj[i] = j;
-          lastv[i] = nv;
           int kk = dn - n;
           if (kk < 0) kk += nn;
           atomicAdd(&agg[(ss * Q + ds) * kS + kk], -xu);
