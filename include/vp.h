@@ -114,7 +114,10 @@ typedef struct vp_catalog vp_catalog; /* opaque, library-owned */
  * every node with all NIC lanes of node n landing on node (n + k) mod n_nodes.
  * Shapes are ordered by (k, diagonal node block, shift node block) and
  * families inside a shape by their sorted node-local instance ids.
- * *out receives a new handle (free with vp_catalog_free). */
+ * *out receives a new handle (free with vp_catalog_free).  A node whose
+ * candidate channel sets exceed 2^22 before pruning (one node of eight
+ * switches of two GPUs already does) returns VP_ERR_UNSUPPORTED after a few
+ * seconds instead of exhausting host memory. */
 vp_status vp_build_catalog(const vp_topology* topo, vp_catalog** out);
 
 /* info[0..7] = N, G (groups), g, Q (switches per node), n_nodes, shapes,

@@ -50,6 +50,11 @@ bool path_dominates(const Cand& a, const Cand& b) {
   return a.res != b.res || a.bw > b.bw;
 }
 
+// Channel sets the search may record before the pruning rules run (a few
+// GB of host memory at most): a node whose sets exceed it is refused rather
+// than left to exhaust memory (eight switches of two GPUs already do).
+constexpr size_t kMaxFound = size_t(1) << 22;
+
 class SlotSearch {
  public:
   SlotSearch(const std::vector<Cand>& cands, int Q, int g) : Q_(Q), g_(g), out_(Q) {
@@ -60,10 +65,12 @@ class SlotSearch {
     slot(0, 0);
     return std::move(found_);
   }
+  bool overflowed() const { return overflow_; }
 
  private:
   // choose g lanes for slot q, then recurse to slot q+1
   void slot(int q, uint64_t used) {
+    if (overflow_) return;
     if (q == Q_) {
       for (int x = 0; x < Q_; ++x)
         if (indeg_[x] != g_) return;
@@ -97,6 +104,10 @@ class SlotSearch {
     }
   }
   void record() {
+    if (found_.size() >= kMaxFound) {
+      overflow_ = true;
+      return;
+    }
     Found f;
     f.L.assign(Q_ * Q_, 0);
     f.R.assign(Q_ * Q_, 0);
@@ -113,6 +124,7 @@ class SlotSearch {
   std::vector<int> indeg_;
   std::vector<const Cand*> chosen_;
   std::vector<Found> found_;
+  bool overflow_ = false;
 };
 
 typedef std::tuple<int, int, bool, uint64_t> PairFoot;
@@ -355,14 +367,20 @@ uint64_t get(const uint8_t* p, int bytes) {
 vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
   set_shape(c, t);
   const std::vector<Cand> table = instance_table(t);
+  bool overflow = false;
   auto enumerate = [&](bool remote_nic) {
     SlotSearch search(prune_paths(table, remote_nic), c.Q, c.g);
+    std::vector<Found> raw = search.run();
+    if (search.overflowed()) {
+      overflow = true;
+      return std::vector<Found>();
+    }
     std::vector<Cand> cand = table;
     for (Cand& x : cand) x.remote = remote_nic && x.cls == VP_PATH_NIC;
     // renaming a slot's NICs preserves dominance both ways, so the NIC
     // classes may be reduced to their representatives before it is checked
     std::vector<Found> fs = drop_dominated(
-        nic_representatives(drop_duplicates(search.run(), cand), cand, c.Q, t.nics_per_switch), cand);
+        nic_representatives(drop_duplicates(std::move(raw), cand), cand, c.Q, t.nics_per_switch), cand);
     if (remote_nic) {
       std::vector<Found> with_nic;
       for (Found& f : fs) {
@@ -375,7 +393,10 @@ vp_status build_catalog_host(const vp_topology& t, vp_catalog& c) {
     return fs;   // sorted by (L, R, ids): canonical
   };
   std::vector<Found> f0 = enumerate(false);
-  std::vector<Found> f1 = c.nn > 1 ? enumerate(true) : std::vector<Found>();
+  std::vector<Found> f1 = c.nn > 1 && !overflow ? enumerate(true) : std::vector<Found>();
+  if (overflow)
+    return set_error(VP_ERR_UNSUPPORTED, "a node with this many switches has more candidate channels than the "
+                                         "catalog search holds (2^22 before pruning)");
   fill_catalog(c, f0, f1);
   return VP_OK;
 }

@@ -317,3 +317,15 @@ def test_catalog_load_rejects_a_family_under_other_nic_names(vp):
     with pytest.raises(vp.VPError) as e:
         vp.Catalog.load(reseal(bytes(body[:HEAD]) + bytes(swapped)))
     assert "NIC" in str(e.value)
+
+
+def test_catalog_of_a_node_too_large_for_the_search_is_refused(vp):
+    """One node of two sockets with four switches of two GPUs each has more
+    candidate channel sets than the catalog search holds before pruning
+    (2^22): the build returns VP_ERR_UNSUPPORTED with a message instead of
+    growing without bound."""
+    import ctypes as C
+    h = C.c_void_p()
+    st = vp.lib().vp_build_catalog(C.byref(vp.topology(vpgen.Topology(1, 2, 4, 2))), C.byref(h))
+    assert st == vp.UNSUPPORTED
+    assert b"2^22" in vp.lib().vp_last_error()
