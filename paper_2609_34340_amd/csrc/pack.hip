@@ -701,10 +701,11 @@ struct FusedHeadsArgs {
 // before it copies anything -- all workgroups read the same schedule, so
 // either every one copies or none does -- and keeps the descriptors in LDS;
 // workgroup 0 writes step_off and the workspace.  The copy is the gather's,
-// over 2048-vector ranges (larger workgroups than the gather's halve the
-// schedule reads, which every workgroup repeats).
+// over ranges of two passes of 2048 vectors (64 KiB): fewer, larger
+// workgroups than the gather's, since every workgroup repeats the schedule
+// reads (measured best against one, four and eight passes).
 constexpr int kFusedThreads = 512;
-constexpr int kFusedPass = kFusedThreads * kGatherUnroll;
+constexpr int kFusedPass = 2 * kFusedThreads * kGatherUnroll;   // vectors per workgroup
 
 __global__ void __launch_bounds__(kFusedThreads) pack_heads_kernel(FusedHeadsArgs a) {
   __shared__ StepDesc sd[kFusedThreads];
@@ -834,7 +835,7 @@ vp_status launch_pack(const PackLaunch& a, void* stream) {
   }
 
   // heads with the planner's layout and a short schedule: prepare and copy
-  // in one kernel (one workgroup per 32 KiB of send capacity, at least one)
+  // in one kernel (one workgroup per 64 KiB of send capacity, at least one)
   if (a.mode == 1 && layout && a.stages == 3 && a.k_max <= kFusedThreads && a.N + 1 <= kHeadLoLds) {
     const int64_t vpu = a.unit / 16;
     const int64_t blocks = std::max<int64_t>(1, (a.send_capacity / 16 + kFusedPass - 1) / kFusedPass);
