@@ -710,6 +710,58 @@ def test_pack_two_halves_match_one_call(vp, cid):
     assert torch.equal(two[:total], one[:total])
 
 
+@pytest.mark.parametrize("cid", [1, 4])
+def test_pack_replayed_from_a_hip_graph(vp, cid):
+    """The pack records no memset, so a caller may capture it in a HIP graph:
+    the one-call pack (rows: prepare and scatter; heads: the one-kernel pack)
+    captured once and replayed three times, with an eager plan of another
+    matrix and a host synchronisation between replays, gives the eager send
+    buffer and step offsets after every replay."""
+    log("pack graph C%d" % cid)
+    if cid == 4:
+        w, hl, D = heads_case()
+        pipe = vp.Pipeline(w.topo, "heads", w.row_bytes, tokens=w.tokens, token_stride=w.token_stride)
+        tok = torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda()
+        head_lo = torch.from_numpy(hl).cuda()
+        pipe.step(tokens=tok, head_lo=head_lo)
+        other = torch.from_numpy(np.ascontiguousarray(D.T)).cuda()
+    else:
+        w, R, dem, D = moe_case(cid)
+        pipe = vp.Pipeline(w.topo, "moe", w.row_bytes, n_experts=w.experts, tokens=w.tokens, top_k=w.top_k)
+        tok = torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda()
+        head_lo = None
+        pipe.step(routing=torch.from_numpy(R).cuda(), tokens=tok)
+        other = torch.from_numpy(np.ascontiguousarray(D.T)).cuda()
+    torch.cuda.synchronize()
+    assert vp.read_status(pipe.status) == 0
+    K = int(pipe.sched["K"].item())
+    total = int(pipe.step_off[K].item())
+    eager = pipe.send[:total].clone()
+    off = pipe.step_off[:K + 1].clone()
+    send = torch.zeros_like(pipe.send)
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        pipe.pack_stage(tok, head_lo, send)
+    torch.cuda.current_stream().wait_stream(side)
+    with torch.cuda.graph(g):
+        pipe.pack_stage(tok, head_lo, send)
+    sched_other = vp.alloc_schedule(pipe.N, pipe.params.k_max, layout=True)
+    for rep in range(3):
+        send.zero_()
+        pipe.step_off.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert vp.read_status(pipe.status) == 0
+        assert torch.equal(send[:total], eager), rep
+        assert torch.equal(pipe.step_off[:K + 1], off), rep
+        # unrelated eager work between replays: a plan of another matrix
+        vp.plan(pipe.cat, other, pipe.params, out=sched_other)
+        torch.cuda.synchronize()
+
+
 def test_plan_largest_topology_is_a_valid_decomposition(vp):
     """1,024 ranks (128 nodes), the planner's largest shape: too big for the
     oracle to plan in test time, so the properties any valid schedule has are
