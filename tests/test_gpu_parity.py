@@ -597,6 +597,48 @@ def test_pack_heads_shapes(vp, shape, layout):
     assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off)
 
 
+@pytest.mark.parametrize("layout", [False, True])
+@pytest.mark.parametrize("case", ["capacity", "k", "heads", "self", "status"])
+def test_pack_heads_errors_write_nothing(vp, case, layout):
+    """Malformed calls of the heads pack set dev_status and write nothing to
+    the send buffer, on the one-kernel path (the planner's layout) and the
+    slice-kernel path: a send buffer one head short (VP_ERR_CAPACITY), K
+    above k_max, a destination whose heads run past the token row, a lane of
+    this rank that sends to itself, and an error already in dev_status
+    (kept, nothing copied)."""
+    w, hl, D = heads_case()
+    log("pack heads error %s layout %s" % (case, layout))
+    s_np = oracle_plan(4, D)
+    ref, _ = oracle.pack_heads(vpgen.tokens_bf16(w, 0), w.token_stride, hl, w.row_bytes, 0, s_np)
+    sched = upload_schedule(vp, w.n_ranks, s_np, layout)
+    K = s_np["K"]
+    cap = ref.size
+    hl_bad = hl.copy()
+    st = vp.new_status()
+    want = vp.INVALID_ARGUMENT
+    if case == "capacity":
+        cap = ref.size - w.row_bytes
+        want = vp.CAPACITY
+    elif case == "k":
+        sched["K"].fill_(8 * w.n_ranks + 1)
+    elif case == "heads":
+        hl_bad[-1] += 1   # the last destination's heads end past the row
+    elif case == "self":
+        k = int(np.flatnonzero(s_np["bytes"][:, 0] > 0)[0])
+        sched["dst"][k, 0] = 0
+    else:
+        st.fill_(vp.NO_PROGRESS)
+        want = vp.NO_PROGRESS
+    send = torch.full((cap + 64,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(8 * w.n_ranks + 1, dtype=torch.int64, device="cuda")
+    vp.pack_heads(torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda(), w.token_stride, torch.from_numpy(hl_bad).cuda(),
+                  w.row_bytes, 0, sched, send[:cap], step_off, st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == want
+    assert (send == 0xA5).all()
+    assert K > 0
+
+
 @pytest.mark.parametrize("where", ["first", "middle", "last"])
 def test_pack_rejects_a_layout_that_does_not_tile(vp, where):
     """A send-offset layout that leaves a gap (here one unit) is refused by
