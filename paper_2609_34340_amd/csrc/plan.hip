@@ -46,7 +46,10 @@ constexpr uint32_t kRawSaturated = 0xFFFFFFFEu;     // residual too large for 32
 
 // Phase timing, compiled only with -DVP_PHASE_STAMPS (phase_stamps.py builds
 // such a copy): thread 0 of workgroup 0 stores the cycle counter at each
-// phase boundary of every iteration, row = iteration (4096 rows of 16).
+// phase boundary of every iteration, row = iteration (4096 rows of 16):
+// columns 0-8 open the phases, 9-14 mark points inside them (thread 0's
+// gather items done, the start draws done, the best start read, the
+// update's reads done, its stores issued, the shared totals written).
 #ifdef VP_PHASE_STAMPS
 __device__ unsigned long long g_phase_stamps[4096 * 16];
 #define VP_STAMP(k)                                                                                  \
@@ -996,6 +999,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
             ++c;
           }
         }
+        VP_STAMP(9);
         // the shuffled starts' permutations (Fisher-Yates on SplitMix64
         // streams keyed by seed, iteration, family, start, group and side):
         // one (family, start) pair and 64 of its groups per wavefront, on the
@@ -1038,6 +1042,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
             }
           }
         }
+        VP_STAMP(10);
       }
       lds_barrier();
       VP_STAMP(4);
@@ -1064,6 +1069,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         int64_t F0 = -1;
         best_start(pr, NS, s0, F0);
         best_valid = true;
+        VP_STAMP(11);
         best_S = F0 * P.unit;
         best_f = cb;
         best_c = 0;
@@ -1180,6 +1186,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         // the unit is below 2^31 (a cap of at least one unit fits 31 bits)
         const int64_t x = (int64_t)((uint64_t)(uint32_t)xu * (uint32_t)P.unit);
         const uint32_t rv = live ? RW[t * kRow + s_ * g + d_] : brw[t];
+        VP_STAMP(12);
         const uint32_t o = (uint32_t)(K * N + i);
         at32(gdst, o) = j;
         at32(ginst, o) = live ? iid[(size_t)best_c * N + t] : bid[t];
@@ -1206,6 +1213,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
                                __HIP_MEMORY_SCOPE_AGENT);
           sacc[i] += x;
         }
+        VP_STAMP(13);
         if (xu > 0) {
           int64_t* dp = &at32(gDrem, (uint32_t)(i * N + j));
           if (__builtin_expect(!sat, 1)) {
@@ -1233,6 +1241,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(PlanArgs P) {
         }
         sh->key = 0;
       }
+      VP_STAMP(14);
       // LDS-only barrier: the global stores above need not land before the
       // next scoring pass (which reads LDS only); the full barrier after it
       // orders them before the next gather reads D^rem.

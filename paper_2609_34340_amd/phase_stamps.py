@@ -21,6 +21,11 @@ import numpy as np
 
 PHASES = ["scoring (wave 0)", "scoring barrier", "argmax", "gather + draws", "AA (wave 0 runs)",
           "AA barrier", "evaluate", "update", "loop top"]
+# (name, from column, to column) of the points stamped inside the phases
+SUB = [("gather: thread 0's items", 3, 9), ("gather: start draws after them", 9, 10),
+       ("gather: barrier", 10, 4), ("evaluate: best start read", 6, 11), ("evaluate: the rest", 11, 7),
+       ("update: reads (lists, binding, credits)", 7, 12), ("update: schedule and layout stores", 12, 13),
+       ("update: residual, aggregates, totals", 13, 14), ("update: barrier", 14, 8)]
 
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -76,6 +81,10 @@ def main(configs):
         cols = [A[:, i + 1] - A[:, i] for i in range(8)] + [nxt - A[:, 8]]
         for name, d in zip(PHASES, cols):
             print("   %-18s %7.0f cycles  %5.1f %%" % (name, np.mean(d), 100 * np.mean(d) / per_iter), flush=True)
+        # points inside the phases (thread 0's view)
+        B = T[1:K - 1]
+        for name, a, b in SUB:
+            print("      %-34s %7.0f cycles" % (name, float(np.mean(B[:, b] - B[:, a]))), flush=True)
 
 
 if __name__ == "__main__":
