@@ -160,7 +160,7 @@ def test_demand_ragged(vp, T, k, E, N, first):
 
 def test_demand_reused_workspace_and_single_rank(vp):
     """One workspace, zero-filled once, serves calls of every shape in turn
-    (its per-row tickets reset themselves): all rows of the 64-rank workload,
+    (nothing in it needs clearing between calls): all rows of the 64-rank workload,
     then one rank's own row (R = 1, the deployed unit) at each end of the
     rank range, then the 8-rank workload, then all 64 rows again; each call
     element-wise against the oracle."""

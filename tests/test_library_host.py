@@ -92,15 +92,17 @@ def test_plan_params_defaults(vp):
 
 
 def test_workspace_queries(vp):
-    # tickets, partial counts of every row, chunk counts of the sorted row
-    assert vp.demand_workspace_bytes(256, 4096, 8, 256) >= 256 * 4 * 32
+    # partial histograms of every row (int32 per part and expert), chunk
+    # counts of the sorted row
+    assert vp.demand_workspace_bytes(256, 4096, 8, 256) >= 256 * 4 * 8 * 4
     assert vp.demand_workspace_bytes(1, 4096, 8, 256) < vp.demand_workspace_bytes(256, 4096, 8, 256)
     assert vp.demand_workspace_bytes(0, 4096, 8, 256) == 0
-    # heads: one descriptor per step, whatever the send buffer's size
-    assert vp.pack_workspace_bytes(2048, 468_729_856, 14336) >= 2048 * 24
+    # heads: a 40-byte descriptor and a 4-byte first unit per step, whatever
+    # the send buffer's size
+    assert vp.pack_workspace_bytes(2048, 468_729_856, 14336) >= 2048 * 44
     assert vp.pack_workspace_bytes(2048, 468_729_856, 14336) == vp.pack_workspace_bytes(2048, 1 << 40, 256)
-    # rows: a copy counter and top-k send-unit slots per token
-    assert vp.pack_workspace_bytes(2048, 468_729_856, 14336, 4096, 8) >= 4096 * 4 * 9
+    # rows: one 8-byte send-unit entry per (token, routing slot)
+    assert vp.pack_workspace_bytes(2048, 468_729_856, 14336, 4096, 8) >= 2048 * 44 + 4096 * 8 * 8
     assert vp.pack_workspace_bytes(2048, 468_729_856, 14336, -1, 8) == 0
 
 
