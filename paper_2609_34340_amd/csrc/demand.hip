@@ -311,24 +311,44 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
   int32_t* mine = wc + w * E;
   for (int e = lane; e < E; e += 64) mine[e] = 0;
   wave_sync();
-  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  int rk[kPerThread];
+  // Match masks of all kPerThread ids at once, bit by bit of the expert id:
+  // the kPerThread ballots of one bit are independent, so their latencies
+  // overlap.  Ids past the row (and bad ids) are no ids.
+  uint64_t same[kPerThread];
 #pragma unroll
   for (int m = 0; m < kPerThread; ++m) {
-    // ids past the row are no ids
     if (base + m * 64 + lane >= a.Tk) ev[m] = -1;
+    same[m] = __ballot((unsigned)ev[m] < (unsigned)E);
+  }
+  for (int bt = 0; bt < a.bits; ++bt) {
+#pragma unroll
+    for (int m = 0; m < kPerThread; ++m) {
+      const bool one = ((uint32_t)ev[m] >> bt) & 1u;
+      const uint64_t ones = __ballot(one);
+      same[m] &= one ? ones : ~ones;
+    }
+  }
+  // The wave's running count of each expert: id m's rank is the count before
+  // it plus its lower lanes with the same expert; the lowest lane of each
+  // group then adds the group's size.  The adds return nothing and the
+  // wave's LDS operations complete in order, so no id waits for the one
+  // before it; the counts read are summed after the last add.
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int rk[kPerThread], cnt_before[kPerThread];
+#pragma unroll
+  for (int m = 0; m < kPerThread; ++m) {
     const int e = ev[m];
     const bool ok = (unsigned)e < (unsigned)E;
-    uint64_t same = __ballot(ok);
-    for (int bt = 0; bt < a.bits; ++bt) {
-      const uint64_t ones = __ballot(ok && ((e >> bt) & 1));
-      same &= ((e >> bt) & 1) ? ones : ~ones;
-    }
-    rk[m] = ok ? mine[e] + __popcll(same & lt) : 0;
+    const uint64_t below = same[m] & lt;
+    rk[m] = __popcll(below);
+    cnt_before[m] = mine[ok ? e : 0];
     wave_sync();
-    if (ok && (same & lt) == 0) mine[e] += __popcll(same);   // lowest lane of the group advances
+    if (ok && below == 0)
+      __hip_atomic_fetch_add(&mine[e], (int32_t)__popcll(same[m]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
     wave_sync();
   }
+#pragma unroll
+  for (int m = 0; m < kPerThread; ++m) rk[m] += cnt_before[m];
   if (OFF != kOffScanned) {
     if (OFF == kOffHeld) {
       const int n4 = a.nch4 / 4;
@@ -393,15 +413,19 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
     }
   }
   __syncthreads();
+  // every id's wave offset read first (clamped index), then the stores
+  int at[kPerThread];
+#pragma unroll
+  for (int m = 0; m < kPerThread; ++m) at[m] = mine[(unsigned)ev[m] < (unsigned)E ? ev[m] : 0] + rk[m];
+  uint8_t* const slot_out = a.sorted_slot;
 #pragma unroll
   for (int m = 0; m < kPerThread; ++m) {
-    const int e = ev[m];
-    if ((unsigned)e < (unsigned)E) {
+    if ((unsigned)ev[m] < (unsigned)E) {
       // x < 2^31 and k < 256: the multiply-high quotient is exact
       const uint32_t x = (uint32_t)(base + m * 64 + lane);
       const uint32_t t = (uint32_t)__umul64hi((uint64_t)x << 24, a.k_magic);
-      a.sorted_tok[mine[e] + rk[m]] = (int32_t)t;
-      if (a.sorted_slot) a.sorted_slot[mine[e] + rk[m]] = (uint8_t)(x - t * (uint32_t)a.k);
+      a.sorted_tok[at[m]] = (int32_t)t;
+      if (slot_out) slot_out[at[m]] = (uint8_t)(x - t * (uint32_t)a.k);
     }
   }
 }
