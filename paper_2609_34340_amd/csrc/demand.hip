@@ -13,7 +13,8 @@
 //   demand_finish  pass 2: one workgroup per row sums its parts (at most
 //                  16 per row for rows up to 131,072 ids: one round of
 //                  loads) into the row's counts and demand row; one
-//                  workgroup per sort chunk places its ids: a stable rank
+//                  workgroup per sort chunk (512 threads, four ids each,
+//                  for up to 256 experts) places its ids: a stable rank
 //                  inside each wave's ids from a match mask built with one
 //                  ballot per bit of the expert id plus a prefix popcount,
 //                  while the chunk counts it needs are in flight; then the
@@ -35,8 +36,7 @@ namespace {
 
 constexpr int kThreads = 256;                    // threads of every demand workgroup
 constexpr int kWaves = kThreads / 64;
-constexpr int kPerThread = 8;                    // ids per thread of a sort chunk
-constexpr int kChunk = kThreads * kPerThread;    // ids per sort chunk (2048)
+constexpr int kChunk = 2048;                     // ids per sort chunk
 constexpr int kInBlockScan = 64;                 // sort chunks up to which each scatter
                                                  // workgroup derives its own offsets
 
@@ -194,11 +194,13 @@ __global__ void __launch_bounds__(1024) sort_scan(int32_t* __restrict__ ccount, 
   if (tid == 0) dest_off[N] = carry;
 }
 
-// Exclusive scan over the block of n values in LDS (n <= 16 * kThreads):
-// each thread a contiguous run; returns the total.
+// Exclusive scan over the block of n values in LDS (n <= 16 * TH): each
+// thread a contiguous run; returns the total.
+template <int TH>
 __device__ inline int32_t block_excl_scan(int32_t* v, int n, int32_t* wtot) {
+  constexpr int W = TH / 64;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int per = (n + kThreads - 1) / kThreads;
+  const int per = (n + TH - 1) / TH;
   const int e0 = min(n, tid * per), e1 = min(n, e0 + per);
   int32_t own = 0;
   for (int e = e0; e < e1; ++e) own += v[e];
@@ -210,7 +212,7 @@ __device__ inline int32_t block_excl_scan(int32_t* v, int n, int32_t* wtot) {
   if (lane == 63) wtot[w] = incl;
   __syncthreads();
   int32_t run = incl - own, all = 0;
-  for (int u = 0; u < kWaves; ++u) {
+  for (int u = 0; u < W; ++u) {
     if (u < w) run += wtot[u];
     all += wtot[u];
   }
@@ -225,22 +227,26 @@ __device__ inline int32_t block_excl_scan(int32_t* v, int n, int32_t* wtot) {
 
 // Pass 2.  Workgroup c < nch places the ids of sort chunk c; the R
 // workgroups after them merge their row's parts into its counts and demand
-// row.  A chunk's
-// offsets: expert e starts at the total of the experts below e plus the
-// counts of e in the chunks before c (each workgroup reads every chunk
-// count, or the scan kernel's offsets for long rows).  Inside the chunk,
-// wave v ranks the ids [v*64*kPerThread, ...) with one ballot per id bit
-// (a match mask) and a prefix popcount; the waves' counts are then scanned
-// per expert.
+// row.  A chunk's offsets: expert e starts at the total of the experts below
+// e plus the counts of e in the chunks before c (each workgroup reads every
+// chunk count, or the scan kernel's offsets for long rows).  Inside the
+// chunk, wave v ranks its ids with one ballot per id bit (a match mask) and
+// a prefix popcount; the waves' counts are then scanned per expert.
 // Offsets of a sort chunk: from the scan kernel, or from every chunk's
 // counts (at most kInBlockScan chunks) held in registers (up to 256
-// experts) or reloaded.
+// experts, TH / 256 threads per expert) or reloaded.  TH threads per
+// workgroup, kChunk / TH ids per thread.
 enum { kOffScanned = 0, kOffHeld = 1, kOffReload = 2 };
 
-template <int OFF>
-__global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
-  extern __shared__ int32_t sh[];   // rows: E; chunks: off [E], tot [E], wc [kWaves][E]
-  __shared__ int32_t wtot[kWaves];
+template <int OFF, int TH>
+__global__ void __launch_bounds__(TH) demand_finish(DemandArgs a) {
+  constexpr int kW = TH / 64;                       // waves
+  constexpr int kPT = kChunk / TH;                  // ids per thread of a sort chunk
+  constexpr int kSplit = TH / 256;                  // threads per expert holding its chunk counts
+  constexpr int kC4 = kInBlockScan / 4 / kSplit;    // chunk counts per thread, in fours
+  static_assert(kPT * TH == kChunk && kSplit >= 1 && kC4 * 4 * kSplit == kInBlockScan, "block shape");
+  extern __shared__ int32_t sh[];   // rows: E; chunks: off [E], tot [E], wc [kW][E]
+  __shared__ int32_t wtot[kW];
   const int tid = threadIdx.x, E = a.E;
   // the sort chunks, whose ranking is the longest work, come first
   const int nsort = a.sort_row >= 0 ? a.nch : 0;
@@ -248,7 +254,7 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
   if (b >= nsort) {
     const int r = b - nsort;
     const int32_t* q = a.partials + (size_t)r * a.P * E;
-    for (int e = tid; e < E; e += kThreads) {
+    for (int e = tid; e < E; e += TH) {
       // loads of 16 parts issued together, then summed
       int32_t c = 0;
       for (int pp = 0; pp < a.P; pp += 16) {
@@ -263,7 +269,7 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
     }
     __syncthreads();
     const int eloc = E / a.N, self = a.first_rank + r;
-    for (int j = tid; j < a.N; j += kThreads) {
+    for (int j = tid; j < a.N; j += TH) {
       int64_t c = 0;
       for (int e = j * eloc; e < (j + 1) * eloc; ++e) c += sh[e];
       a.demand[(size_t)r * a.N + j] = j == self ? 0 : c * a.unit;
@@ -278,51 +284,48 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
   const int32_t* ids = a.routing + (size_t)a.sort_row * a.Tk;
   if (a.Tk <= 0) {   // an empty row: every destination's range is empty
     if (chunk == 0)
-      for (int j = tid; j <= a.N; j += kThreads) a.dest_off[j] = 0;
+      for (int j = tid; j <= a.N; j += TH) a.dest_off[j] = 0;
     return;
   }
   // the chunk's ids first, then its chunk counts, all loads unconditional
   // (indexes clamped into range, results masked after) so that the ranking
   // below waits for the ids only and the counts' latency hides behind it
-  const int64_t base = (int64_t)chunk * kChunk + (int64_t)w * 64 * kPerThread;
-  int ev[kPerThread];
+  const int64_t base = (int64_t)chunk * kChunk + (int64_t)w * 64 * kPT;
+  int ev[kPT];
 #pragma unroll
-  for (int m = 0; m < kPerThread; ++m) {
+  for (int m = 0; m < kPT; ++m) {
     const int64_t x = base + m * 64 + lane;
     ev[m] = ids[x < a.Tk ? x : a.Tk - 1];
   }
-  // The chunk counts: the scan kernel's offsets, or every chunk's counts of
-  // the thread's experts (at most kInBlockScan chunks, 16 loads of four)
-  // held in registers through the ranking, which does not depend on them.
-  constexpr int kEPT = 256 / kThreads;   // experts per thread held in registers (E <= 256)
-  int4 cv[kEPT][kInBlockScan / 4];
+  // The chunk counts: the scan kernel's offsets, or the counts of the
+  // thread's share of every chunk of its expert (at most kInBlockScan
+  // chunks) held in registers through the ranking, which does not depend on
+  // them.
+  const int he = tid / kSplit, c4lo = (tid % kSplit) * kC4;   // held: expert, first four of the share
+  int4 cv[kC4];
   if (OFF == kOffScanned) {
-    for (int e = tid; e < E; e += kThreads) off[e] = a.ccount[(size_t)e * a.nch4 + chunk];
+    for (int e = tid; e < E; e += TH) off[e] = a.ccount[(size_t)e * a.nch4 + chunk];
   } else if (OFF == kOffHeld) {
     const int n4 = a.nch4 / 4;
+    const int4* q = (const int4*)(a.ccount + (size_t)(he < E ? he : 0) * a.nch4);
 #pragma unroll
-    for (int m = 0; m < kEPT; ++m) {
-      const int e = tid + m * kThreads;
-      const int4* q = (const int4*)(a.ccount + (size_t)(e < E ? e : 0) * a.nch4);
-#pragma unroll
-      for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) cv[m][c4] = q[c4 < n4 ? c4 : n4 - 1];
-    }
+    for (int c = 0; c < kC4; ++c) cv[c] = q[c4lo + c < n4 ? c4lo + c : n4 - 1];
   }
   int32_t* mine = wc + w * E;
   for (int e = lane; e < E; e += 64) mine[e] = 0;
   wave_sync();
-  // Match masks of all kPerThread ids at once, bit by bit of the expert id:
-  // the kPerThread ballots of one bit are independent, so their latencies
-  // overlap.  Ids past the row (and bad ids) are no ids.
-  uint64_t same[kPerThread];
+  // Match masks of all kPT ids at once, bit by bit of the expert id: the kPT
+  // ballots of one bit are independent, so their latencies overlap.  Ids
+  // past the row (and bad ids) are no ids.
+  uint64_t same[kPT];
 #pragma unroll
-  for (int m = 0; m < kPerThread; ++m) {
+  for (int m = 0; m < kPT; ++m) {
     if (base + m * 64 + lane >= a.Tk) ev[m] = -1;
     same[m] = __ballot((unsigned)ev[m] < (unsigned)E);
   }
   for (int bt = 0; bt < a.bits; ++bt) {
 #pragma unroll
-    for (int m = 0; m < kPerThread; ++m) {
+    for (int m = 0; m < kPT; ++m) {
       const bool one = ((uint32_t)ev[m] >> bt) & 1u;
       const uint64_t ones = __ballot(one);
       same[m] &= one ? ones : ~ones;
@@ -334,9 +337,9 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
   // wave's LDS operations complete in order, so no id waits for the one
   // before it; the counts read are summed after the last add.
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  int rk[kPerThread], cnt_before[kPerThread];
+  int rk[kPT], cnt_before[kPT];
 #pragma unroll
-  for (int m = 0; m < kPerThread; ++m) {
+  for (int m = 0; m < kPT; ++m) {
     const int e = ev[m];
     const bool ok = (unsigned)e < (unsigned)E;
     const uint64_t below = same[m] & lt;
@@ -348,33 +351,34 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
     wave_sync();
   }
 #pragma unroll
-  for (int m = 0; m < kPerThread; ++m) rk[m] += cnt_before[m];
+  for (int m = 0; m < kPT; ++m) rk[m] += cnt_before[m];
   if (OFF != kOffScanned) {
     if (OFF == kOffHeld) {
       const int n4 = a.nch4 / 4;
+      int32_t all = 0, before = 0;
 #pragma unroll
-      for (int m = 0; m < kEPT; ++m) {
-        const int e = tid + m * kThreads;
-        int32_t all = 0, before = 0;
+      for (int c = 0; c < kC4; ++c) {
+        // the clamped loads past the last chunk count nothing
+        const int c4 = c4lo + c;
+        const bool in = c4 < n4;
+        const int32_t x4[4] = {in ? cv[c].x : 0, in ? cv[c].y : 0, in ? cv[c].z : 0, in ? cv[c].w : 0};
 #pragma unroll
-        for (int c4 = 0; c4 < kInBlockScan / 4; ++c4) {
-          // the clamped loads past the last chunk count nothing
-          const bool in = c4 < n4;
-          const int32_t x4[4] = {in ? cv[m][c4].x : 0, in ? cv[m][c4].y : 0, in ? cv[m][c4].z : 0,
-                                 in ? cv[m][c4].w : 0};
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            all += x4[q];
-            before += 4 * c4 + q < chunk ? x4[q] : 0;
-          }
-        }
-        if (e < E) {
-          tot[e] = all;
-          off[e] = before;
+        for (int q = 0; q < 4; ++q) {
+          all += x4[q];
+          before += 4 * c4 + q < chunk ? x4[q] : 0;
         }
       }
+#pragma unroll
+      for (int o = 1; o < kSplit; o <<= 1) {   // the expert's threads are neighbouring lanes
+        all += __shfl_xor(all, o);
+        before += __shfl_xor(before, o);
+      }
+      if (he < E && tid % kSplit == 0) {
+        tot[he] = all;
+        off[he] = before;
+      }
     } else {
-      for (int e = tid; e < E; e += kThreads) {
+      for (int e = tid; e < E; e += TH) {
         const int4* q = (const int4*)(a.ccount + (size_t)e * a.nch4);
         const int n4 = a.nch4 / 4;
         int4 v[kInBlockScan / 4];
@@ -395,18 +399,18 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
       }
     }
     __syncthreads();
-    const int32_t total = block_excl_scan(tot, E, wtot);
-    for (int e = tid; e < E; e += kThreads) off[e] += tot[e];
+    const int32_t total = block_excl_scan<TH>(tot, E, wtot);
+    for (int e = tid; e < E; e += TH) off[e] += tot[e];
     if (chunk == 0) {
       const int eloc = E / a.N;
-      for (int j = tid; j < a.N; j += kThreads) a.dest_off[j] = tot[j * eloc];
+      for (int j = tid; j < a.N; j += TH) a.dest_off[j] = tot[j * eloc];
       if (tid == 0) a.dest_off[a.N] = total;
     }
   }
   __syncthreads();
-  for (int e = tid; e < E; e += kThreads) {
+  for (int e = tid; e < E; e += TH) {
     int32_t acc = off[e];
-    for (int v = 0; v < kWaves; ++v) {
+    for (int v = 0; v < kW; ++v) {
       const int32_t c = wc[v * E + e];
       wc[v * E + e] = acc;
       acc += c;
@@ -414,12 +418,12 @@ __global__ void __launch_bounds__(kThreads) demand_finish(DemandArgs a) {
   }
   __syncthreads();
   // every id's wave offset read first (clamped index), then the stores
-  int at[kPerThread];
+  int at[kPT];
 #pragma unroll
-  for (int m = 0; m < kPerThread; ++m) at[m] = mine[(unsigned)ev[m] < (unsigned)E ? ev[m] : 0] + rk[m];
+  for (int m = 0; m < kPT; ++m) at[m] = mine[(unsigned)ev[m] < (unsigned)E ? ev[m] : 0] + rk[m];
   uint8_t* const slot_out = a.sorted_slot;
 #pragma unroll
-  for (int m = 0; m < kPerThread; ++m) {
+  for (int m = 0; m < kPT; ++m) {
     if ((unsigned)ev[m] < (unsigned)E) {
       // x < 2^31 and k < 256: the multiply-high quotient is exact
       const uint32_t x = (uint32_t)(base + m * 64 + lane);
@@ -548,14 +552,18 @@ vp_status launch_demand(const DemandLaunch& a, void* stream) {
   if (d.scanned)
     hipLaunchKernelGGL(sort_scan, dim3(1), dim3(1024), 0, s, d.ccount, (int64_t)a.E * w.nch4, a.E, a.N, w.nch4,
                        a.dest_off);
+  // pass 2: 512 threads when the chunk counts are held in registers (up to
+  // 256 experts), else 256 (LDS: the chunk's offsets, totals and one count
+  // row per wave)
   const int64_t blocks2 = (int64_t)a.R + (sorting ? w.nch : 0);
-  const size_t lds2 = (size_t)(2 + kWaves) * a.E * sizeof(int32_t);
+  const size_t lds256 = (size_t)(2 + 256 / 64) * a.E * sizeof(int32_t);
+  const size_t lds512 = (size_t)(2 + 512 / 64) * a.E * sizeof(int32_t);
   if (d.scanned)
-    hipLaunchKernelGGL(demand_finish<kOffScanned>, dim3((unsigned)blocks2), dim3(kThreads), lds2, s, d);
+    hipLaunchKernelGGL((demand_finish<kOffScanned, 256>), dim3((unsigned)blocks2), dim3(256), lds256, s, d);
   else if (a.E <= 256)
-    hipLaunchKernelGGL(demand_finish<kOffHeld>, dim3((unsigned)blocks2), dim3(kThreads), lds2, s, d);
+    hipLaunchKernelGGL((demand_finish<kOffHeld, 512>), dim3((unsigned)blocks2), dim3(512), lds512, s, d);
   else
-    hipLaunchKernelGGL(demand_finish<kOffReload>, dim3((unsigned)blocks2), dim3(kThreads), lds2, s, d);
+    hipLaunchKernelGGL((demand_finish<kOffReload, 256>), dim3((unsigned)blocks2), dim3(256), lds256, s, d);
   if (hipGetLastError() != hipSuccess) return set_error(VP_ERR_HIP, "demand launch failed");
   return VP_OK;
 }
