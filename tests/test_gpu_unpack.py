@@ -143,6 +143,28 @@ def test_unpack_rows_parity_full_size(vp, cid, r):
     assert (out[ref.size:] == 0).all()
 
 
+@pytest.mark.parametrize("cid,r,extra", [(1, 5, 13), (2, 3, 1), (3, 10, 777)])
+def test_unpack_rows_receive_buffer_larger_than_its_rows(vp, cid, r, extra):
+    """A receive buffer with `extra` slots past the rows the schedule delivers
+    (a capacity, not a count): the copy splits the delivered rows, not the
+    capacity, between the XCDs, and the slots past them are never read."""
+    w, rb, R, dem, D, counts = case(cid)
+    N = w.n_ranks
+    sb = oracle.slot_bytes(rb)
+    s = oplan(cid, D, rb, False)
+    U = int(D[:, r].sum()) // rb
+    log("unpack rows C%d rank %d: %d rows in %d slots" % (cid, r, U, U + extra))
+    recv = rand_bytes((U + extra) * sb, 2000 * cid + r)
+    ref = oracle.unpack_rows(recv[:U * sb].cpu().numpy(), r, N, s, rb, counts)
+    out = torch.zeros(ref.size + sb, dtype=torch.uint8, device="cuda")
+    st = vp.new_status()
+    vp.unpack_rows(recv, rb, torch.from_numpy(counts).cuda(), r, upload(vp, N, s), out[:ref.size], st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    assert torch.equal(out[:ref.size], torch.from_numpy(ref).cuda())
+    assert (out[ref.size:] == 0).all()
+
+
 @pytest.mark.parametrize("cid,r", [(1, 3), (2, 0), (5, 0)])
 def test_pack_combine_parity_full_size(vp, cid, r):
     w, rb, R, dem, D, counts = case(cid)
