@@ -22,6 +22,7 @@
 #include <cstring>
 #include <map>
 #include <set>
+#include <thread>
 #include <tuple>
 
 #include "internal.h"
@@ -48,6 +49,24 @@ bool path_dominates(const Cand& a, const Cand& b) {
   bool subset = (a.res & ~b.res) == 0;
   if (!subset || a.bw < b.bw) return false;
   return a.res != b.res || a.bw > b.bw;
+}
+
+// fn(i) for every i in [0, n), on up to 16 host threads in contiguous
+// blocks (the pruning rules judge each family or shape on its own).
+template <class Fn>
+void parallel_for(size_t n, Fn fn) {
+  const unsigned T = std::min<unsigned>(16, std::max(1u, std::thread::hardware_concurrency()));
+  if (n < 4096 || T == 1) {
+    for (size_t i = 0; i < n; ++i) fn(i);
+    return;
+  }
+  const size_t chunk = (n + T - 1) / T;
+  std::vector<std::thread> th;
+  for (unsigned t = 0; t < T; ++t)
+    th.emplace_back([&fn, t, chunk, n] {
+      for (size_t i = t * chunk; i < std::min(n, (t + 1) * chunk); ++i) fn(i);
+    });
+  for (std::thread& x : th) x.join();
 }
 
 // Channel sets the search may record before the pruning rules run (a few
@@ -141,17 +160,91 @@ Profile profile_of(const Found& f, const std::vector<Cand>& by_id) {
   return m;
 }
 
+// A lane's part of a family's profile as one word: the index of its (pair,
+// footprint) among the table's distinct ones, then its rate.  A family's
+// sorted words are its profile: two families have equal profiles exactly
+// when they have the same multiset of (pair, footprint, rate).
+std::vector<uint64_t> lane_words(const std::vector<Cand>& by_id) {
+  std::map<PairFoot, uint64_t> foot;
+  std::vector<uint64_t> w(by_id.size());
+  for (const Cand& c : by_id) {
+    auto it = foot.emplace(PairFoot(c.src, c.dst, c.remote, c.res), (uint64_t)foot.size()).first;
+    w[c.id] = (it->second << 40) | (uint64_t)c.bw;   // rates are below 2^40 bytes/ns
+  }
+  return w;
+}
+
+uint64_t words_hash(const uint64_t* v, size_t n) {
+  uint64_t h = 0x9E3779B97F4A7C15ull;
+  for (size_t i = 0; i < n; ++i) {
+    h ^= v[i] + 0x9E3779B97F4A7C15ull + (h << 6) + (h >> 2);
+    h *= 0xFF51AFD7ED558CCDull;
+  }
+  return h ^ (h >> 32);
+}
+
+// Families sorted into canonical order, (L, R, ids) lexicographic: every
+// family's three lists are written once as one flat big-endian 16-bit key
+// (all values are below 2^16), and an index array is sorted by comparing
+// keys as bytes.
+void sort_canonical(std::vector<Found>& fs) {
+  const size_t n = fs.size();
+  if (n < 2) return;
+  const size_t qq = fs[0].L.size(), w = fs[0].ids.size(), kl = 2 * (2 * qq + w);
+  std::vector<uint8_t> key(n * kl);
+  parallel_for(n, [&](size_t i) {
+    uint8_t* k = key.data() + i * kl;
+    auto put16 = [&](int v) {
+      *k++ = (uint8_t)(v >> 8);
+      *k++ = (uint8_t)v;
+    };
+    for (int v : fs[i].L) put16(v);
+    for (int v : fs[i].R) put16(v);
+    for (int v : fs[i].ids) put16(v);
+  });
+  std::vector<uint32_t> idx(n);
+  for (size_t i = 0; i < n; ++i) idx[i] = (uint32_t)i;
+  std::sort(idx.begin(), idx.end(), [&](uint32_t a, uint32_t b) {
+    return std::memcmp(key.data() + a * kl, key.data() + b * kl, kl) < 0;
+  });
+  std::vector<Found> out(n);
+  for (size_t i = 0; i < n; ++i) out[i] = std::move(fs[idx[i]]);
+  fs.swap(out);
+}
+
 // PruneFamilies, first half: exact duplicates (same multiset of (pair,
 // footprint, rate)) keep their first family in canonical order; the result
 // is sorted by (L, R, ids), so every shape's families are contiguous.
+// Profiles are compared through a 64-bit hash, every hash hit by the full
+// sorted words.
 std::vector<Found> drop_duplicates(std::vector<Found> fs, const std::vector<Cand>& by_id) {
-  std::sort(fs.begin(), fs.end(), [](const Found& a, const Found& b) {
-    return std::tie(a.L, a.R, a.ids) < std::tie(b.L, b.R, b.ids);
+  sort_canonical(fs);
+  const std::vector<uint64_t> lw = lane_words(by_id);
+  const size_t n = fs.size(), w = n ? fs[0].ids.size() : 0;
+  std::vector<uint64_t> prof(n * w);
+  // (hash, index) pairs sorted: equal profiles meet in one run of equal
+  // hashes, where every family but the first of its profile is a duplicate
+  std::vector<std::pair<uint64_t, uint32_t>> hi(n);
+  parallel_for(n, [&](size_t i) {
+    uint64_t* p = prof.data() + i * w;
+    for (size_t x = 0; x < w; ++x) p[x] = lw[fs[i].ids[x]];
+    std::sort(p, p + w);
+    hi[i] = {words_hash(p, w), (uint32_t)i};
   });
+  std::sort(hi.begin(), hi.end());
+  std::vector<uint8_t> dup(n, 0);
+  for (size_t b = 0, e; b < n; b = e) {
+    for (e = b + 1; e < n && hi[e].first == hi[b].first; ++e) {
+    }
+    for (size_t x = b + 1; x < e; ++x)
+      for (size_t y = b; y < x && !dup[hi[x].second]; ++y)
+        if (!dup[hi[y].second] && std::equal(prof.data() + hi[x].second * w, prof.data() + (hi[x].second + 1) * w,
+                                             prof.data() + hi[y].second * w))
+          dup[hi[x].second] = 1;   // the run is in index order: y is the earlier family
+  }
   std::vector<Found> uniq;
-  std::set<Profile> seen;
-  for (Found& f : fs)
-    if (seen.insert(profile_of(f, by_id)).second) uniq.push_back(std::move(f));
+  for (size_t i = 0; i < n; ++i)
+    if (!dup[i]) uniq.push_back(std::move(fs[i]));
   return uniq;
 }
 
@@ -159,13 +252,16 @@ std::vector<Found> drop_duplicates(std::vector<Found> fs, const std::vector<Cand
 // pairs with it per (pair, footprint) at no lower rate, one strictly higher.
 // Shapes are contiguous in the input, so only families of one run compare.
 std::vector<Found> drop_dominated(std::vector<Found> fs, const std::vector<Cand>& by_id) {
-  std::vector<Profile> prof;
-  for (const Found& f : fs) prof.push_back(profile_of(f, by_id));
-  std::vector<Found> out;
-  size_t b = 0;
-  while (b < fs.size()) {
-    size_t e = b + 1;
-    while (e < fs.size() && fs[e].L == fs[b].L && fs[e].R == fs[b].R) ++e;
+  const size_t n = fs.size();
+  std::vector<Profile> prof(n);
+  parallel_for(n, [&](size_t i) { prof[i] = profile_of(fs[i], by_id); });
+  std::vector<size_t> runs;   // first family of every shape, then n
+  for (size_t b = 0; b < n; ++b)
+    if (b == 0 || fs[b].L != fs[b - 1].L || fs[b].R != fs[b - 1].R) runs.push_back(b);
+  runs.push_back(n);
+  std::vector<uint8_t> keep(n, 1);
+  parallel_for(runs.size() - 1, [&](size_t r) {
+    const size_t b = runs[r], e = runs[r + 1];
     for (size_t i = b; i < e; ++i) {
       bool dominated = false;
       for (size_t j = b; j < e && !dominated; ++j) {
@@ -181,10 +277,12 @@ std::vector<Found> drop_dominated(std::vector<Found> fs, const std::vector<Cand>
         }
         dominated = ok && strict;
       }
-      if (!dominated) out.push_back(fs[i]);
+      keep[i] = !dominated;
     }
-    b = e;
-  }
+  });
+  std::vector<Found> out;
+  for (size_t i = 0; i < n; ++i)
+    if (keep[i]) out.push_back(std::move(fs[i]));
   return out;
 }
 
@@ -209,9 +307,10 @@ std::vector<Found> nic_representatives(std::vector<Found> fs, const std::vector<
   do sym.push_back(perm); while (std::next_permutation(perm.begin(), perm.end()));
   int64_t combos = 1;
   for (int q = 0; q < Q; ++q) combos *= (int64_t)sym.size();
-  std::vector<Found> out;
-  std::vector<int32_t> renamed;
-  for (Found& f : fs) {
+  std::vector<uint8_t> keep(fs.size());
+  parallel_for(fs.size(), [&](size_t fi) {
+    const Found& f = fs[fi];
+    std::vector<int32_t> renamed;
     bool least = true;
     for (int64_t code = 1; code < combos && least; ++code) {
       renamed.clear();
@@ -230,8 +329,11 @@ std::vector<Found> nic_representatives(std::vector<Found> fs, const std::vector<
       std::sort(renamed.begin(), renamed.end());
       least = !(renamed < f.ids);
     }
-    if (least) out.push_back(std::move(f));
-  }
+    keep[fi] = least;
+  });
+  std::vector<Found> out;
+  for (size_t fi = 0; fi < fs.size(); ++fi)
+    if (keep[fi]) out.push_back(std::move(fs[fi]));
   return out;
 }
 
