@@ -253,6 +253,41 @@ def measure(w, steps, warmup, M, dev, graph=False):
             raise SystemExit("the graph-replayed pack differs from the eager one")
         del eager
 
+        # the whole step (demand, control words, plan, one-call pack) of the
+        # first matrix captured once and replayed `steps` times between two
+        # events: the step time without the host's launch gaps; the send
+        # buffer after the replays must equal the eager step's
+        def whole():
+            pipe.demand_stage(routing[0], head_lo)
+            pipe.words_stage()
+            pipe.plan_stage()
+            pipe.pack_stage(tokens, head_lo, sends[0])
+
+        sends[0].zero_()
+        whole()
+        torch.cuda.synchronize()
+        eager = sends[0].clone()
+        sends[0].zero_()
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            whole()
+        torch.cuda.current_stream().wait_stream(side)
+        with torch.cuda.graph(g):
+            whole()
+        g.replay()
+        a, b = E(), E()
+        a.record()
+        for _ in range(steps):
+            g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        r["step_graph_ms"] = a.elapsed_time(b) / steps
+        if vp.read_status(pipe.status) != 0 or not torch.equal(sends[0], eager):
+            raise SystemExit("the graph-replayed step differs from the eager one")
+        del g, eager
+
     # one rank's own row (R = 1: its routing, counts, demand row and sort),
     # the unit each rank runs in deployment; mean of 20 calls, HIP events
     if w.mode == "moe":
@@ -516,6 +551,8 @@ def summary(w, r):
             "copy_frac_graph": round(float(r["gather_bytes"][-1] / (r["copy_graph_ms"] * 1e-3) / 1e9)
                                            / PEAK_HBM_GBS, 4) if "copy_graph_ms" in r else None,
             "prepare_us_graph": round(float(r["prep_graph_ms"] * 1e3), 2) if "prep_graph_ms" in r else None,
+            # the whole step replayed from one HIP graph (--graph)
+            "ms_per_step_graph": round(float(r["step_graph_ms"]), 4) if "step_graph_ms" in r else None,
             # the same kernel inside the timed steps (events around it: for
             # short kernels the events' own cost is a visible share)
             "copy_us_in_steps": round(float(r["copy_ms"].mean() * 1e3), 2),
@@ -539,7 +576,8 @@ def main():
                     help="skip the planner on the extra demands and the nearest-path ablation")
     ap.add_argument("--graph", action="store_true",
                     help="also time the copy kernel by 50 launches replayed from a HIP graph (reported beside "
-                         "the timed steps' figure; leave it off for profiler runs of the default command)")
+                         "the timed steps' figure) and the whole step replayed from one graph "
+                         "(ms_per_step_graph); leave it off for profiler runs of the default command")
     ap.add_argument("--calibrate-copy", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB")
     args = ap.parse_args()
@@ -621,6 +659,7 @@ def main():
                      "avg_launch_us_graph": head["copy_us_graph"],
                      "frac_graph": head["copy_frac_graph"]},
         "prepare_us_graph": head["prepare_us_graph"],
+        "ms_per_step_graph": head["ms_per_step_graph"],
     }
     if w.mode == "moe" and not args.no_receive:
         print("[bench] receive side and combine", file=sys.stderr, flush=True)

@@ -804,6 +804,63 @@ def test_pack_replayed_from_a_hip_graph(vp, cid):
         torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("cid", [1, 4])
+def test_whole_step_replayed_from_a_hip_graph(vp, cid):
+    """No call of the hot path records a memset, allocates or synchronises
+    with the host, so a whole step -- demand (and control words), plan, pack
+    -- can be captured in one HIP graph.  Replayed three times, with every
+    output cleared before each replay and an eager plan of another matrix and
+    a host synchronisation after it, each replay gives the eager step's
+    demand matrix, schedule, buffer layout, step offsets and send buffer."""
+    log("whole step graph C%d" % cid)
+    if cid == 4:
+        w, hl, D = heads_case()
+        pipe = vp.Pipeline(w.topo, "heads", w.row_bytes, tokens=w.tokens, token_stride=w.token_stride)
+        kw = dict(tokens=torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda(), head_lo=torch.from_numpy(hl).cuda())
+    else:
+        w, R, dem, D = moe_case(cid)
+        pipe = vp.Pipeline(w.topo, "moe", w.row_bytes, n_experts=w.experts, tokens=w.tokens, top_k=w.top_k)
+        kw = dict(routing=torch.from_numpy(R).cuda(), tokens=torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda())
+    send = torch.zeros_like(pipe.send)
+    pipe.step(send=send, **kw)
+    torch.cuda.synchronize()
+    assert vp.read_status(pipe.status) == 0
+    K = int(pipe.sched["K"].item())
+    total = int(pipe.step_off[K].item())
+    outs = dict(demand=pipe.dem["demand"], K=pipe.sched["K"], family=pipe.sched["family"], dst=pipe.sched["dst"],
+                bytes=pipe.sched["bytes"], send_off=pipe.sched["send_off"], stream_off=pipe.sched["stream_off"],
+                step_off=pipe.step_off)
+    eager = {k: v.clone() for k, v in outs.items()}
+    eager_send = send[:total].clone()
+    assert K > 0 and total > 0
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        pipe.step(send=send, **kw)
+    torch.cuda.current_stream().wait_stream(side)
+    with torch.cuda.graph(g):
+        pipe.step(send=send, **kw)
+    other = torch.from_numpy(np.ascontiguousarray(D.T)).cuda()
+    sched_other = vp.alloc_schedule(pipe.N, pipe.params.k_max, layout=True)
+    for rep in range(3):
+        send.zero_()
+        for v in outs.values():
+            v.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert vp.read_status(pipe.status) == 0, rep
+        for k, v in outs.items():
+            # rows up to K are the schedule; the rest is not written
+            a, b = (v[:K + 1], eager[k][:K + 1]) if k == "step_off" else (
+                (v[:K], eager[k][:K]) if k in ("family", "dst", "bytes", "send_off", "stream_off") else (v, eager[k]))
+            assert torch.equal(a, b), (rep, k)
+        assert torch.equal(send[:total], eager_send), rep
+        vp.plan(pipe.cat, other, pipe.params, out=sched_other)
+        torch.cuda.synchronize()
+
+
 def test_plan_largest_topology_is_a_valid_decomposition(vp):
     """1,024 ranks (128 nodes), the planner's largest shape: too big for the
     oracle to plan in test time, so the properties any valid schedule has are
