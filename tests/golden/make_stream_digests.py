@@ -7,6 +7,7 @@ process per matrix batch (about 3 minutes on 8 cores).
 
     python tests/golden/make_stream_digests.py [--jobs 8]
     python tests/golden/make_stream_digests.py --all-256 [--jobs 8]   # every matrix of the 256-rank stream
+    python tests/golden/make_stream_digests.py --sys-256              # matrix 0 of it on SYS nodes (about a minute)
 """
 from __future__ import annotations
 
@@ -46,15 +47,42 @@ def oracle_job(args):
                 send=sd.send_digest(sd.send_sample(send), send.size), step_off=sd.step_off_digest(off))
 
 
+def sys256():
+    """The oracle's demand and schedule digests for the first matrix of the
+    256-rank workload on nodes with cross-socket peer to peer."""
+    import dataclasses
+    import oracle
+    import vpgen
+    w = vpgen.config(5)
+    topo = dataclasses.replace(w.topo, flags=1)
+    R = vpgen.routing_all(w, 0)
+    D = np.stack([oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes)["row"] for i in range(w.n_ranks)])
+    t0 = time.time()
+    s = oracle.Catalog(topo).plan(D, w.row_bytes)
+    print("SYS 256 ranks: K=%d in %.0f s" % (s["K"], time.time() - t0), flush=True)
+    out = dict(workload=w.name, topology="%s, SYS peer to peer" % (topo.as_tuple(),), matrix=0, K=int(s["K"]),
+               tau=int(s["tau"]), demand=sd.demand_digest(D), schedule=sd.schedule_digest(s))
+    with open(sd.GOLDEN_SYS256, "w") as f:
+        json.dump(out, f, indent=0)
+        f.write("\n")
+    print("wrote", sd.GOLDEN_SYS256)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=8)
     ap.add_argument("--all-256", action="store_true",
                     help="digest all 1000 matrices of the 256-rank stream into %s" % os.path.basename(sd.GOLDEN_ALL5))
+    ap.add_argument("--sys-256", action="store_true",
+                    help="digest matrix 0 of the 256-rank workload on SYS nodes into %s" %
+                         os.path.basename(sd.GOLDEN_SYS256))
     args = ap.parse_args()
     import oracle
     import vpgen
     oracle.build()
+    if args.sys_256:
+        sys256()
+        return
     out = {"sample_stride": sd.SAMPLE_STRIDE, "streams": {}}
     ctx = mp.get_context("spawn")
     streams = {5: list(range(1000))} if args.all_256 else sd.STREAMS

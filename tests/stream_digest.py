@@ -29,8 +29,11 @@ SAMPLE_STRIDE = 4099
 # stream, every 10th of the 256-rank stream
 STREAMS = {3: list(range(100)), 5: list(range(0, 1000, 10))}
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "stream_digests.json")
-# every matrix of the 256-rank stream (an opt-in GPU check)
+# every matrix of the 256-rank stream
 GOLDEN_ALL5 = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "stream_digests_256_all.json")
+# the first matrix of the 256-rank workload planned on nodes with cross-socket
+# peer to peer (SYS paths)
+GOLDEN_SYS256 = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "sys256_digest.json")
 
 
 def _sha(*arrays) -> str:

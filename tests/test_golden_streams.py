@@ -1,7 +1,8 @@
 """The stored stream digests agree with the oracle as it stands: the demand
 and schedule digests of the first and last matrix of the 64-rank stream and of
-the first matrix of the 256-rank stream are recomputed here (the full streams
-and the send-buffer digests are rebuilt by golden/make_stream_digests.py)."""
+the first matrix of the 256-rank stream (also on SYS nodes) are recomputed
+here (the full streams and the send-buffer digests are rebuilt by
+golden/make_stream_digests.py)."""
 import json
 
 import numpy as np
@@ -52,3 +53,20 @@ def test_full_256_stream_digests_agree_with_the_subset(golden):
     assert sorted(full) == list(range(1000))
     for r in golden["streams"]["5"]["matrices"]:
         assert full[r["matrix"]] == r
+
+
+def test_sys256_digest_matches_oracle():
+    """The stored digest of the 256-rank workload on SYS nodes (the GPU
+    parity reference of tests/test_gpu_extra.py) is the oracle's plan as it
+    stands (about a minute on one core)."""
+    import dataclasses
+    with open(sd.GOLDEN_SYS256) as f:
+        ref = json.load(f)
+    w = vpgen.config(5)
+    topo = dataclasses.replace(w.topo, flags=1)
+    R = vpgen.routing_all(w, ref["matrix"])
+    D = np.stack([oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes)["row"] for i in range(w.n_ranks)])
+    assert sd.demand_digest(D) == ref["demand"]
+    s = oracle.Catalog(topo).plan(D, w.row_bytes)
+    assert (s["K"], s["tau"]) == (ref["K"], ref["tau"])
+    assert sd.schedule_digest(s) == ref["schedule"]

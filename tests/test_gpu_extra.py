@@ -3,6 +3,7 @@ s = 0.4 / 0.6 / 0.8, Wan2.1-like head/context layouts) with the full catalog
 and with the nearest-path catalog of the peer/path ablation, against the
 oracle, bit-exact; the head/context demand itself comes from vp_demand_heads
 per all-to-all group."""
+import os
 import sys
 
 import numpy as np
@@ -93,16 +94,24 @@ def test_sys_topology_plan_parity(vp, cid):
     assert (gc.instances()["cls"][g["inst"]] == vp.PATH_SYS).any()
 
 
-def test_sys_topology_256_ranks_plans_validly(vp):
-    """256 ranks with SYS paths (60,104 families): the GPU plan is a valid
+def test_sys_topology_256_ranks_plan_parity(vp):
+    """256 ranks with SYS paths (60,104 families): the GPU schedule equals the
+    oracle's through the digests tests/golden/make_stream_digests.py --sys-256
+    stored (the oracle takes about a minute there), and is a valid
     decomposition (every activation feasible, sums to D, progressing)."""
     import dataclasses
+    import json
     from oracle.checks import TopoModel, schedule_valid
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    import stream_digest as sd
+    with open(sd.GOLDEN_SYS256) as f:
+        ref = json.load(f)
     w = vpgen.config(5)
     topo = dataclasses.replace(w.topo, flags=vp.TOPO_SYS_P2P)
     log("SYS topology 256 ranks")
     R = vpgen.routing_all(w, 0)
     D = np.stack([oracle.demand(R[i], w.n_ranks, w.experts, i, w.row_bytes)["row"] for i in range(w.n_ranks)])
+    assert sd.demand_digest(D) == ref["demand"]
     gc = vp.Catalog(topo)
     gc.upload()
     p = vp.plan_params(gc.N, w.row_bytes)
@@ -111,5 +120,7 @@ def test_sys_topology_256_ranks_plans_validly(vp):
     torch.cuda.synchronize()
     assert vp.read_status(st) == 0
     g = vp.schedule_to_host(s)
+    assert (g["K"], g["tau"]) == (ref["K"], ref["tau"])
+    assert sd.schedule_digest(g) == ref["schedule"]
     schedule_valid(TopoModel(topo), D, g, gc.instances()["cls"])
     assert (g["bytes"].sum(axis=1) > 0).all()
