@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <exception>
 #include <new>
 
 #include "internal.h"
@@ -84,7 +85,13 @@ vp_status vp_build_catalog(const vp_topology* t, vp_catalog** out) {
   if (s != VP_OK) return s;
   vp_catalog* c = new (std::nothrow) vp_catalog();
   if (!c) return set_error(VP_ERR_INVALID_ARGUMENT, "out of host memory");
-  s = vp::build_catalog_host(*t, *c);
+  try {
+    s = vp::build_catalog_host(*t, *c);
+  } catch (const std::bad_alloc&) {
+    s = set_error(VP_ERR_UNSUPPORTED, "out of host memory while building the catalog");
+  } catch (const std::exception& e) {
+    s = set_error(VP_ERR_UNSUPPORTED, std::string("catalog build failed: ") + e.what());
+  }
   if (s != VP_OK) {
     delete c;
     return s;

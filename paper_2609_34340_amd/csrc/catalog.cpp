@@ -22,6 +22,8 @@
 #include <cstring>
 #include <map>
 #include <set>
+#include <exception>
+#include <system_error>
 #include <thread>
 #include <tuple>
 
@@ -52,7 +54,9 @@ bool path_dominates(const Cand& a, const Cand& b) {
 }
 
 // fn(i) for every i in [0, n), on up to 16 host threads in contiguous
-// blocks (the pruning rules judge each family or shape on its own).
+// blocks (the pruning rules judge each family or shape on its own).  A block
+// whose thread cannot be started runs on the calling thread; an exception in
+// any block is rethrown here after every thread has joined.
 template <class Fn>
 void parallel_for(size_t n, Fn fn) {
   const unsigned T = std::min<unsigned>(16, std::max(1u, std::thread::hardware_concurrency()));
@@ -61,12 +65,25 @@ void parallel_for(size_t n, Fn fn) {
     return;
   }
   const size_t chunk = (n + T - 1) / T;
-  std::vector<std::thread> th;
-  for (unsigned t = 0; t < T; ++t)
-    th.emplace_back([&fn, t, chunk, n] {
+  std::vector<std::exception_ptr> err(T);
+  auto block = [&fn, &err, chunk, n](unsigned t) {
+    try {
       for (size_t i = t * chunk; i < std::min(n, (t + 1) * chunk); ++i) fn(i);
-    });
+    } catch (...) {
+      err[t] = std::current_exception();
+    }
+  };
+  std::vector<std::thread> th;
+  for (unsigned t = 0; t < T; ++t) {
+    try {
+      th.emplace_back(block, t);
+    } catch (const std::system_error&) {
+      block(t);
+    }
+  }
   for (std::thread& x : th) x.join();
+  for (const std::exception_ptr& e : err)
+    if (e) std::rethrow_exception(e);
 }
 
 // Channel sets the search may record before the pruning rules run (a few
