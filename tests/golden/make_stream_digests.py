@@ -8,6 +8,7 @@ process per matrix batch (about 3 minutes on 8 cores).
     python tests/golden/make_stream_digests.py [--jobs 8]
     python tests/golden/make_stream_digests.py --all-256 [--jobs 8]   # every matrix of the 256-rank stream
     python tests/golden/make_stream_digests.py --sys-256              # matrix 0 of it on SYS nodes (about a minute)
+    python tests/golden/make_stream_digests.py --ranks-1024           # 1,024 ranks (about 12 minutes)
 """
 from __future__ import annotations
 
@@ -68,6 +69,25 @@ def sys256():
     print("wrote", sd.GOLDEN_SYS256)
 
 
+def ranks1024():
+    """The oracle's schedule digest for the hot-destination demand on 1,024
+    ranks (128 nodes), k_max = 32N."""
+    import oracle
+    import vpgen
+    topo = vpgen.Topology(128)
+    N, unit = topo.n_ranks, 4096
+    D = vpgen.hot_destinations_demand(N, unit, 1024)
+    t0 = time.time()
+    s = oracle.Catalog(topo).plan(D, unit, k_max=32 * N)
+    print("1024 ranks: K=%d in %.0f s" % (s["K"], time.time() - t0), flush=True)
+    out = dict(topology="%s" % (topo.as_tuple(),), unit=unit, k_max=32 * N, K=int(s["K"]), tau=int(s["tau"]),
+               demand=sd.demand_digest(D), schedule=sd.schedule_digest(s))
+    with open(sd.GOLDEN_1024, "w") as f:
+        json.dump(out, f, indent=0)
+        f.write("\n")
+    print("wrote", sd.GOLDEN_1024)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=8)
@@ -76,12 +96,17 @@ def main():
     ap.add_argument("--sys-256", action="store_true",
                     help="digest matrix 0 of the 256-rank workload on SYS nodes into %s" %
                          os.path.basename(sd.GOLDEN_SYS256))
+    ap.add_argument("--ranks-1024", action="store_true",
+                    help="digest the 1,024-rank plan into %s" % os.path.basename(sd.GOLDEN_1024))
     args = ap.parse_args()
     import oracle
     import vpgen
     oracle.build()
     if args.sys_256:
         sys256()
+        return
+    if args.ranks_1024:
+        ranks1024()
         return
     out = {"sample_stride": sd.SAMPLE_STRIDE, "streams": {}}
     ctx = mp.get_context("spawn")

@@ -34,6 +34,9 @@ GOLDEN_ALL5 = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
 # the first matrix of the 256-rank workload planned on nodes with cross-socket
 # peer to peer (SYS paths)
 GOLDEN_SYS256 = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "sys256_digest.json")
+# the planner's largest shape: 1,024 ranks (128 nodes) under the hot-destination
+# demand of vpgen.hot_destinations_demand, k_max = 32N
+GOLDEN_1024 = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "plan1024_digest.json")
 
 
 def _sha(*arrays) -> str:

@@ -70,3 +70,16 @@ def test_sys256_digest_matches_oracle():
     s = oracle.Catalog(topo).plan(D, w.row_bytes)
     assert (s["K"], s["tau"]) == (ref["K"], ref["tau"])
     assert sd.schedule_digest(s) == ref["schedule"]
+
+
+def test_ranks1024_digest_is_for_the_generated_demand():
+    """The stored 1,024-rank digest (the GPU parity reference of
+    tests/test_gpu_parity.py; the oracle's plan takes about ten minutes, so
+    only the script recomputes it) names the demand vpgen generates, and a K
+    any valid schedule of it can have."""
+    with open(sd.GOLDEN_1024) as f:
+        ref = json.load(f)
+    N = 1024
+    D = vpgen.hot_destinations_demand(N, ref["unit"], 1024)
+    assert sd.demand_digest(D) == ref["demand"]
+    assert ref["k_max"] == 32 * N and N - 1 <= ref["K"] <= ref["k_max"]

@@ -114,3 +114,58 @@ def test_bad_matrix_fails_alone(vp):
     for b in (0, 2):
         h = host(s, b)
         assert h["K"] == o["K"] and np.array_equal(h["dst"], o["dst"]) and np.array_equal(h["bytes"], o["bytes"])
+
+
+def test_pipelines_on_concurrent_streams(vp):
+    """The library keeps no state between calls on a device (every call's
+    state is in its own arguments and workspaces): two whole steps of
+    different workloads (the 8-rank and 64-rank MoE dispatches), each on its
+    own stream and enqueued interleaved so that their kernels can overlap,
+    give each workload the demand, schedule and send buffer it gets alone."""
+    cases = []
+    for cid in (1, 3):
+        w = vpgen.config(cid)
+        pipe = vp.Pipeline(w.topo, "moe", w.row_bytes, n_experts=w.experts, tokens=w.tokens, top_k=w.top_k)
+        R = torch.from_numpy(vpgen.routing_all(w, 0)).cuda()
+        tok = torch.from_numpy(vpgen.tokens_bf16(w, 0)).cuda()
+        cases.append((cid, pipe, R, tok))
+    alone = []
+    for cid, pipe, R, tok in cases:
+        log("step alone C%d" % cid)
+        send = pipe.step(routing=R, tokens=tok)
+        torch.cuda.synchronize()
+        assert vp.read_status(pipe.status) == 0
+        K = int(pipe.sched["K"].item())
+        alone.append(dict(K=K, demand=pipe.dem["demand"].clone(), dst=pipe.sched["dst"][:K].clone(),
+                          bytes=pipe.sched["bytes"][:K].clone(), step_off=pipe.step_off[:K + 1].clone(),
+                          send=send[:int(pipe.step_off[K].item())].clone()))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for rep in range(2):
+        log("steps on two streams, round %d" % rep)
+        for (cid, pipe, R, tok), st in zip(cases, streams):
+            pipe.send.zero_()
+            pipe.dem["demand"].fill_(-1)
+            pipe.sched["dst"].fill_(-1)
+        torch.cuda.synchronize()
+        # stage by stage, alternating between the streams
+        for stage in ("demand", "words", "plan", "pack"):
+            for (cid, pipe, R, tok), st in zip(cases, streams):
+                s = st
+                if stage == "demand":
+                    pipe.demand_stage(R, None, stream=s)
+                elif stage == "words":
+                    pipe.words_stage(stream=s)
+                elif stage == "plan":
+                    pipe.plan_stage(stream=s)
+                else:
+                    pipe.pack_stage(tok, None, stream=s)
+        torch.cuda.synchronize()
+        for (cid, pipe, R, tok), ref in zip(cases, alone):
+            assert vp.read_status(pipe.status) == 0, cid
+            K = int(pipe.sched["K"].item())
+            assert K == ref["K"], cid
+            assert torch.equal(pipe.dem["demand"], ref["demand"]), cid
+            assert torch.equal(pipe.sched["dst"][:K], ref["dst"]), cid
+            assert torch.equal(pipe.sched["bytes"][:K], ref["bytes"]), cid
+            assert torch.equal(pipe.step_off[:K + 1], ref["step_off"]), cid
+            assert torch.equal(pipe.send[:ref["send"].numel()], ref["send"]), cid

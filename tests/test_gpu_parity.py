@@ -861,26 +861,22 @@ def test_whole_step_replayed_from_a_hip_graph(vp, cid):
         torch.cuda.synchronize()
 
 
-def test_plan_largest_topology_is_a_valid_decomposition(vp):
-    """1,024 ranks (128 nodes), the planner's largest shape: too big for the
-    oracle to plan in test time, so the properties any valid schedule has are
-    checked instead -- the activations sum to D exactly, every step is a
+def test_plan_largest_topology_parity(vp):
+    """1,024 ranks (128 nodes), the planner's largest shape, under a MoE-like
+    skew (light traffic between every pair plus a global hot tenth of the
+    destinations, vpgen.hot_destinations_demand): the schedule hashes to the
+    oracle's (stored by tests/golden/make_stream_digests.py --ranks-1024; the
+    oracle takes about ten minutes there), and has the properties any valid
+    schedule has -- the activations sum to D exactly, every step is a
     derangement whose lanes use path classes of their group pairs and share
     no modeled resource (Eq. (1)), every step serves bytes, and K stays
     within k_max (raised to 32N)."""
+    import json
+    import stream_digest as sd
     topo = vpgen.Topology(128)
     N = topo.n_ranks
-    rng = np.random.default_rng(1024)
     unit = 4096
-    # MoE-like skew: light traffic between every pair plus a global set of
-    # hot destinations (a tenth of the ranks), as in the 256-rank workload
-    D = rng.integers(0, 8, (N, N)).astype(np.int64)
-    hot = rng.choice(N, N // 10, replace=False)
-    D[:, hot] += rng.integers(20, 60, (N, hot.size))
-    np.fill_diagonal(D, 0)
-    # volumes of tens of thousands of units per rank, so that a quantum
-    # (tau at K_target = 2N) holds tens of units
-    D *= 32 * unit
+    D = vpgen.hot_destinations_demand(N, unit, 1024)
     log("plan on 1024 ranks")
     # every pair carries bytes: the caller gives room beyond the default 8N
     g = gpu_plan(vp, topo, D, unit, k_max=32 * N)
@@ -896,6 +892,11 @@ def test_plan_largest_topology_is_a_valid_decomposition(vp):
     np.add.at(X, (np.broadcast_to(rows, (K, N)), dst), nb)
     assert np.array_equal(X, D)
     assert (nb.sum(axis=1) > 0).all()
+    with open(sd.GOLDEN_1024) as f:
+        ref = json.load(f)
+    assert sd.demand_digest(D) == ref["demand"]
+    assert (K, g["tau"]) == (ref["K"], ref["tau"])
+    assert sd.schedule_digest(g) == ref["schedule"]
     cls = gcat(vp, topo).instances()["cls"][inst]
     # every step's lanes are resource-disjoint (Eq. (1)) on the topology model
     from oracle.checks import TopoModel, schedule_valid_np

@@ -31,7 +31,7 @@ __all__ = [
     "Topology", "Workload", "CONFIGS", "config", "tiny_topology",
     "routing", "routing_all", "tokens_bf16", "head_split", "bf16_from_f32",
     "expert_weights", "DemandCase", "EXTRA", "extra", "uniform_demand", "zipf_pair_demand",
-    "hc_groups", "hc_layout",
+    "hc_groups", "hc_layout", "hot_destinations_demand",
 ]
 
 
@@ -278,6 +278,20 @@ def uniform_demand(case: DemandCase) -> np.ndarray:
     D = np.full((N, N), case.per_pair, dtype=np.int64)
     np.fill_diagonal(D, 0)
     return D
+
+
+def hot_destinations_demand(n_ranks: int = 1024, unit: int = 4096, seed: int = 1024) -> np.ndarray:
+    """int64 [N, N] MoE-like skew at the planner's largest shape: 0-7 units
+    between every pair plus 20-59 more toward a global hot tenth of the
+    destinations, times 32 units (tens of units per quantum at K_target = 2N).
+    numpy PCG64 seeded by `seed`."""
+    rng = np.random.default_rng(seed)
+    N = n_ranks
+    D = rng.integers(0, 8, (N, N)).astype(np.int64)
+    hot = rng.choice(N, N // 10, replace=False)
+    D[:, hot] += rng.integers(20, 60, (N, hot.size))
+    np.fill_diagonal(D, 0)
+    return D * (32 * unit)
 
 
 def zipf_pair_demand(case: DemandCase, matrix: int = 0) -> np.ndarray:
