@@ -184,6 +184,41 @@ def test_demand_reused_workspace_and_single_rank(vp):
         assert np.array_equal(out["dest_off"].cpu().numpy(), ref["dest_off"])
 
 
+@pytest.mark.parametrize("cid,rank,tokens", [(1, 0, None), (1, 7, None), (5, 0, None), (5, 255, None), (5, 100, 1000),
+                                             (5, 3, 4097), (5, 9, 4095)])
+def test_demand_one_rank(vp, cid, rank, tokens):
+    """One rank's own row (R = 1, the deployed unit) with its sort: rows of up
+    to 32,768 ids take the one-launch path, longer ones the two-pass path
+    (4,097 tokens of top-8); ragged lengths; every output element-wise
+    against the oracle."""
+    w = vpgen.config(cid)
+    R = vpgen.routing(w, rank, 0, tokens)
+    log("demand one rank C%d rank %d T=%d" % (cid, rank, R.shape[0]))
+    ref = oracle.demand(R, w.n_ranks, w.experts, rank, w.row_bytes)
+    out = vp.demand(torch.from_numpy(np.ascontiguousarray(R[None])).cuda(), w.n_ranks, w.experts, w.row_bytes,
+                    first_rank=rank, sort_row=0)
+    torch.cuda.synchronize()
+    assert vp.read_status(out["status"]) == 0
+    assert np.array_equal(out["demand"][0].cpu().numpy(), ref["row"])
+    assert np.array_equal(out["counts"][0].cpu().numpy(), ref["counts"])
+    n = R.size
+    assert np.array_equal(out["sorted_tok"][:n].cpu().numpy(), ref["sorted_tok"])
+    assert np.array_equal(out["sorted_slot"][:n].cpu().numpy(), ref["sorted_slot"])
+    assert np.array_equal(out["dest_off"].cpu().numpy(), ref["dest_off"])
+
+
+def test_demand_one_rank_bad_id(vp):
+    """A bad id in a one-launch row is reported; the others are still counted."""
+    w = vpgen.config(1)
+    R = vpgen.routing(w, 0, 0, 100).copy()
+    R[7, 1] = w.experts
+    out = vp.demand(torch.from_numpy(R[None]).cuda(), w.n_ranks, w.experts, w.row_bytes, sort_row=0)
+    torch.cuda.synchronize()
+    assert vp.read_status(out["status"]) == vp.INVALID_ARGUMENT
+    good = R[R < w.experts]
+    assert int(out["counts"][0].sum().item()) == good.size
+
+
 def test_demand_empty_and_bad_ids(vp):
     log("demand empty / bad ids")
     R = torch.zeros((1, 0, 2), dtype=torch.int32, device="cuda")
