@@ -25,8 +25,9 @@ import sys
 import numpy as np
 
 SAMPLE_STRIDE = 4099
-# the matrices of each stream that are checked: every matrix of the 64-rank
-# stream, every 10th of the 256-rank stream
+# the matrices in stream_digests.json: every matrix of the 64-rank stream,
+# every 10th of the 256-rank stream (all 1000 are in stream_digests_256_all.json,
+# which the GPU suite checks)
 STREAMS = {3: list(range(100)), 5: list(range(0, 1000, 10))}
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "stream_digests.json")
 # every matrix of the 256-rank stream
