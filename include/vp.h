@@ -285,8 +285,17 @@ size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
  * bytes or 2^28 units (the planner keeps unit counts in 32 bits: 4 GiB of
  * demand at a 16-byte unit, 64 GiB at a 256-byte unit).  An invalid entry
  * takes precedence over these limits.  The catalog must have been uploaded.  Host
- * errors: VP_ERR_UNSUPPORTED when k_max * N * 8 reaches 2^32 (one matrix's
- * schedule arrays are addressed with 32-bit byte offsets). */
+ * errors, returned before anything is enqueued: VP_ERR_UNSUPPORTED when
+ * k_max * N * 8 reaches 2^32 (one matrix's schedule arrays are addressed with
+ * 32-bit byte offsets), when the catalog exceeds the kernel's index widths
+ * (more than 4095 shapes of either kind, 255 node shifts, 256 node-local
+ * instances, 8 switches per node or 4 GPUs per switch), and when the planner's
+ * per-catalog state (shape terms, family lane maps, node aggregates) plus one
+ * family's working set does not fit in one workgroup's LDS (160 KiB on gfx950):
+ * two-socket nodes of two switches of three GPUs with cross-socket peer to
+ * peer (2,744 families over 2,185 shapes from two nodes on) are the smallest
+ * such catalogs met.  Larger catalogs need a planner that keeps those tables
+ * in HBM. */
 vp_status vp_plan(const vp_catalog* cat, const int64_t* demand, const vp_plan_params* p,
                   int32_t* K, int32_t* family, int32_t* dst, int32_t* inst, int64_t* bytes,
                   int64_t* send_off, int64_t* stream_off, int32_t* recv_src, int64_t* tau,

@@ -124,3 +124,35 @@ def test_sys_topology_256_ranks_plan_parity(vp):
     assert sd.schedule_digest(g) == ref["schedule"]
     schedule_valid(TopoModel(topo), D, g, gc.instances()["cls"])
     assert (g["bytes"].sum(axis=1) > 0).all()
+
+
+def test_plan_state_beyond_lds_is_refused_on_host(vp):
+    """Two nodes of two sockets x two switches x three GPUs with cross-socket
+    peer to peer give 2,185 shapes and 2,744 families, whose planner tables do
+    not fit in one workgroup's LDS: vp_plan refuses the catalog on the host
+    with VP_ERR_UNSUPPORTED and enqueues nothing (the outputs keep their
+    sentinel), and a plan on a catalog that fits still runs afterwards."""
+    topo = vpgen.Topology(2, 2, 2, 3, 1, 32, 12, vp.TOPO_SYS_P2P)
+    gc = vp.Catalog(topo)
+    gc.upload()
+    N = gc.N
+    D = torch.full((N, N), 4096, dtype=torch.int64, device="cuda")
+    D.fill_diagonal_(0)
+    p = vp.plan_params(N, 4096)
+    st = vp.new_status()
+    out = vp.alloc_schedule(N, p.k_max)
+    out["K"].fill_(-7)
+    with pytest.raises(vp.VPError) as e:
+        vp.plan(gc, D, p, status=st, out=out)
+    assert e.value.status == vp.UNSUPPORTED
+    assert "LDS" in str(e.value)
+    torch.cuda.synchronize()
+    assert int(out["K"].item()) == -7 and vp.read_status(st) == 0
+    # a catalog that fits: the same nodes without SYS paths
+    small = vp.Catalog(vpgen.Topology(2, 2, 2, 3, 1, 32, 12, 0))
+    small.upload()
+    s = vp.plan(small, D, vp.plan_params(N, 4096), status=st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    g = vp.schedule_to_host(s)
+    assert g["K"] >= 1 and int(g["bytes"].sum()) == int(D.sum().item())
