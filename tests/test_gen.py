@@ -75,3 +75,19 @@ def test_head_split():
     counts = np.diff(hl)
     assert hl[0] == 0 and hl[-1] == 40
     assert (counts[:8] == 2).all() and (counts[8:] == 3).all()
+
+
+def test_random_routing_shapes_and_law():
+    R = vpgen.random_routing(5, 3, 4000, 24, 4, 1.0)
+    assert R.shape == (3, 4000, 4) and R.dtype == np.int32
+    assert R.min() >= 0 and R.max() < 24
+    assert all(len(set(row)) == 4 for row in R.reshape(-1, 4))          # distinct per token
+    assert np.array_equal(R, vpgen.random_routing(5, 3, 4000, 24, 4, 1.0))
+    assert not np.array_equal(R[0], R[1])                                # ranks draw apart
+    # first draws follow rank^-1 over the shared permutation: the most
+    # popular expert is drawn about 1 / H_24 of the time
+    first = np.bincount(R[:, :, 0].ravel(), minlength=24) / R[:, :, 0].size
+    h = (1.0 / np.arange(1, 25)).sum()
+    assert abs(first.max() - 1.0 / h) < 0.02
+    u = vpgen.random_routing(1, 1, 20000, 8, 1, 0.0)                     # zipf 0: uniform
+    assert np.abs(np.bincount(u.ravel(), minlength=8) / 20000 - 0.125).max() < 0.01

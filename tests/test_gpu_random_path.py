@@ -1,0 +1,120 @@
+"""The whole path on seeded random shapes against the oracle, bit-exact.
+
+Each case draws a topology (2 to 64 ranks, SYS nodes and two NICs per switch
+among them), experts per rank, tokens (ragged around the demand kernels'
+tiles), top-k, routing skew, row size and self rank; then checks the GPU
+demand of every rank (rows, expert counts, the self rank's (expert, token)
+order, routing slots and destination offsets, Sec. 3 model setup), the GPU
+plan with its buffer layout (Alg. 2; K, tau, family, destination, instance
+and bytes of every step) and the self rank's pack (Sec. 5 buffer layout) with
+the planner's layout and with the plain schedule: send bytes, nothing written
+past them, step offsets."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import vpgen
+
+pytestmark = pytest.mark.gpu
+_cat = {}
+
+TOPOS = [vpgen.Topology(1, 2, 2, 2), vpgen.Topology(2, 2, 2, 2), vpgen.Topology(8, 2, 2, 2),
+         vpgen.Topology(1, 1, 2, 3), vpgen.Topology(3, 1, 2, 2), vpgen.Topology(2, 2, 1, 4),
+         vpgen.Topology(1, 1, 1, 2), vpgen.Topology(2, 2, 2, 2, 1, 32, 50), vpgen.Topology(2, 1, 2, 2, 2),
+         vpgen.Topology(3, 2, 2, 2, 1, 32, 25, 1)]
+N_CASES = 40
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def vp():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2609_34340_amd as vp
+    vp.lib()
+    return vp
+
+
+def case_params(i):
+    """Shape of case i (a pure function of i)."""
+    r = np.random.default_rng(1000 + i)
+    topo = TOPOS[i % len(TOPOS)]
+    N = topo.n_ranks
+    L = int(r.choice([1, 2, 3, 4, 8, 16]))
+    while N * L > 4096:
+        L //= 2
+    E = N * L
+    k = int(r.integers(1, min(8, E) + 1))
+    T = int(r.choice([1, 2, 63, 64, 65, 511, 1000, 2048, 3001]))
+    while N * T * k > 2_000_000 and T > 1:
+        T //= 2
+    row = 16 * int(r.choice([1, 2, 7, 65, 256, 900, 1024, 2049]))
+    zipf = float(r.choice([0.0, 0.6, 1.2, 2.0]))
+    self_rank = int(r.integers(N))
+    return topo, E, T, k, row, zipf, self_rank
+
+
+def catalogs(vp, topo):
+    key = topo.as_tuple()
+    if key not in _cat:
+        c = vp.Catalog(topo)
+        c.upload()
+        _cat[key] = (c, oracle.Catalog(topo))
+    return _cat[key]
+
+
+@pytest.mark.parametrize("i", range(N_CASES))
+def test_random_path_parity(vp, i):
+    topo, E, T, k, row, zipf, self_rank = case_params(i)
+    N = topo.n_ranks
+    log("random path case %d: topo %s E=%d T=%d k=%d row=%d zipf=%.1f self=%d" %
+        (i, topo.as_tuple(), E, T, k, row, zipf, self_rank))
+    gc, oc = catalogs(vp, topo)
+    R = vpgen.random_routing(i, N, T, E, k, zipf)
+    dem = [oracle.demand(R[r], N, E, r, row) for r in range(N)]
+    D = np.stack([d["row"] for d in dem])
+    od = dem[self_rank]
+
+    gd = vp.demand(torch.from_numpy(R).cuda(), N, E, row, sort_row=self_rank)
+    torch.cuda.synchronize()
+    assert vp.read_status(gd["status"]) == 0
+    assert np.array_equal(gd["demand"].cpu().numpy(), D)
+    assert np.array_equal(gd["counts"].cpu().numpy(), np.stack([d["counts"] for d in dem]))
+    assert np.array_equal(gd["sorted_tok"][:T * k].cpu().numpy(), od["sorted_tok"])
+    assert np.array_equal(gd["sorted_slot"][:T * k].cpu().numpy(), od["sorted_slot"])
+    assert np.array_equal(gd["dest_off"].cpu().numpy(), od["dest_off"])
+
+    p = vp.plan_params(N, row, k_max=64 * N)   # skewed random routing can need more than 8N steps
+    st = vp.new_status()
+    s = vp.plan(gc, gd["demand"], p, status=st, out=vp.alloc_schedule(N, p.k_max, layout=True))
+    torch.cuda.synchronize()
+    o = oc.plan(D, row, k_max=64 * N)
+    assert vp.read_status(st) == 0 == o["status"]
+    h = vp.schedule_to_host(s)
+    assert (h["K"], h["tau"]) == (o["K"], o["tau"])
+    for key in ("family", "dst", "inst", "bytes"):
+        assert np.array_equal(np.asarray(h[key]), np.asarray(o[key])), key
+
+    tok = np.random.default_rng(i).integers(0, 256, (T, row), dtype=np.uint8)
+    ref, ref_off = oracle.pack_rows(tok, row, od["sorted_tok"], od["dest_off"], self_rank, o)
+    K = o["K"]
+    rows = max(K, 1)
+    plain = {"K": s["K"], "dst": s["dst"][:rows], "bytes": s["bytes"][:rows]}
+    for name, sched in (("layout", s), ("plain", plain)):
+        cap = ref.size + 64
+        send = torch.full((cap,), 0xA5, dtype=torch.uint8, device="cuda")
+        step_off = torch.empty(p.k_max + 1, dtype=torch.int64, device="cuda")
+        pst = vp.new_status()
+        vp.pack_rows(torch.from_numpy(tok).cuda(), row, gd["sorted_tok"], gd["sorted_slot"], gd["dest_off"],
+                     self_rank, sched, send, step_off, pst)
+        torch.cuda.synchronize()
+        assert vp.read_status(pst) == 0, name
+        assert torch.equal(send[:ref.size].cpu(), torch.from_numpy(ref)), name
+        assert (send[ref.size:] == 0xA5).all(), name + ": wrote past the packed bytes"
+        assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off), name

@@ -31,7 +31,7 @@ __all__ = [
     "Topology", "Workload", "CONFIGS", "config", "tiny_topology",
     "routing", "routing_all", "tokens_bf16", "head_split", "bf16_from_f32",
     "expert_weights", "DemandCase", "EXTRA", "extra", "uniform_demand", "zipf_pair_demand",
-    "hc_groups", "hc_layout", "hot_destinations_demand",
+    "hc_groups", "hc_layout", "hot_destinations_demand", "random_routing",
 ]
 
 
@@ -183,6 +183,20 @@ def routing(w: Workload, rank: int, matrix: int = 0, tokens: Optional[int] = Non
 def routing_all(w: Workload, matrix: int = 0, tokens: Optional[int] = None) -> np.ndarray:
     """int32 [N, T, k]: every rank's routing for one matrix."""
     return np.stack([routing(w, rk, matrix, tokens) for rk in range(w.n_ranks)])
+
+
+def random_routing(seed: int, n_ranks: int, tokens: int, experts: int, top_k: int,
+                   zipf_s: float) -> np.ndarray:
+    """int32 [N, T, k]: every rank's top-k distinct experts per token, each
+    draw weighted by popularity rank^-zipf_s over one random permutation of
+    the experts shared by all ranks (zipf_s = 0 is uniform); for randomized
+    shapes outside the named workloads."""
+    r = _rng(7, seed)
+    perm = r.permutation(experts)
+    p = np.empty(experts)
+    p[perm] = (np.arange(1, experts + 1, dtype=np.float64)) ** (-zipf_s)
+    p /= p.sum()
+    return np.stack([_topk_without_replacement(_rng(7, seed, rk), p, tokens, top_k) for rk in range(n_ranks)])
 
 
 def bf16_from_f32(x: np.ndarray) -> np.ndarray:
