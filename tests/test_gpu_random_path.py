@@ -1,5 +1,7 @@
 """The whole path on seeded random shapes against the oracle, bit-exact.
 
+Token rows (MoE dispatch):
+
 Each case draws a topology (2 to 64 ranks, SYS nodes and two NICs per switch
 among them), experts per rank, tokens (ragged around the demand kernels'
 tiles), top-k, routing skew, row size and self rank; then checks the GPU
@@ -8,7 +10,8 @@ order, routing slots and destination offsets, Sec. 3 model setup), the GPU
 plan with its buffer layout (Alg. 2; K, tau, family, destination, instance
 and bytes of every step) and the self rank's pack (Sec. 5 buffer layout) with
 the planner's layout and with the plain schedule: send bytes, nothing written
-past them, step offsets."""
+past them, step offsets.  Head blocks (head/context re-layout): the same for
+random uneven head splits, head sizes, tokens and row padding."""
 import sys
 
 import numpy as np
@@ -113,6 +116,69 @@ def test_random_path_parity(vp, i):
         pst = vp.new_status()
         vp.pack_rows(torch.from_numpy(tok).cuda(), row, gd["sorted_tok"], gd["sorted_slot"], gd["dest_off"],
                      self_rank, sched, send, step_off, pst)
+        torch.cuda.synchronize()
+        assert vp.read_status(pst) == 0, name
+        assert torch.equal(send[:ref.size].cpu(), torch.from_numpy(ref)), name
+        assert (send[ref.size:] == 0xA5).all(), name + ": wrote past the packed bytes"
+        assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off), name
+
+
+N_HEADS_CASES = 20
+
+
+def heads_params(i):
+    """Shape of head/context case i: heads split unevenly (some ranks may own
+    none), head size, tokens, row padding and self rank."""
+    r = np.random.default_rng(5000 + i)
+    topo = TOPOS[(3 * i + 1) % len(TOPOS)]
+    N = topo.n_ranks
+    H = int(r.integers(N, 4 * N + 1))
+    cuts = np.sort(r.integers(0, H + 1, N - 1))
+    hl = np.concatenate([[0], cuts, [H]]).astype(np.int64)
+    head_bytes = 16 * int(r.choice([1, 3, 8, 16, 17, 64]))
+    T = int(r.choice([1, 7, 64, 333, 1024]))
+    pad = 16 * int(r.choice([0, 0, 1, 5]))
+    self_rank = int(r.integers(N))
+    return topo, hl, head_bytes, T, H * head_bytes + pad, self_rank
+
+
+@pytest.mark.parametrize("i", range(N_HEADS_CASES))
+def test_random_heads_path_parity(vp, i):
+    """Sec. 6.2 head/context re-layout on seeded random splits: the GPU demand
+    of every rank, the plan with its layout, and the self rank's head pack
+    (one-kernel pack with the layout, prepare and gather without) against
+    the oracle."""
+    topo, hl, hb, T, stride, self_rank = heads_params(i)
+    N = topo.n_ranks
+    log("random heads case %d: topo %s heads %d bytes %d T=%d stride %d self=%d" %
+        (i, topo.as_tuple(), int(hl[-1]), hb, T, stride, self_rank))
+    gc, oc = catalogs(vp, topo)
+    D = np.stack([oracle.demand_heads(T, hl, hb, r) for r in range(N)])
+    hl_d = torch.from_numpy(hl).cuda()
+    gD = vp.demand_heads(T, hl_d, hb, first_rank=0, R=N)
+    torch.cuda.synchronize()
+    assert np.array_equal(gD.cpu().numpy(), D)
+
+    p = vp.plan_params(N, hb)
+    st = vp.new_status()
+    s = vp.plan(gc, gD, p, status=st, out=vp.alloc_schedule(N, p.k_max, layout=True))
+    torch.cuda.synchronize()
+    o = oc.plan(D, hb)
+    assert vp.read_status(st) == 0 == o["status"]
+    h = vp.schedule_to_host(s)
+    assert (h["K"], h["tau"]) == (o["K"], o["tau"])
+    for key in ("family", "dst", "inst", "bytes"):
+        assert np.array_equal(np.asarray(h[key]), np.asarray(o[key])), key
+
+    act = np.random.default_rng(i).integers(0, 256, (T, stride), dtype=np.uint8)
+    ref, ref_off = oracle.pack_heads(act, stride, hl, hb, self_rank, o)
+    K = o["K"]
+    plain = {"K": s["K"], "dst": s["dst"][:max(K, 1)], "bytes": s["bytes"][:max(K, 1)]}
+    for name, sched in (("layout", s), ("plain", plain)):
+        send = torch.full((ref.size + 64,), 0xA5, dtype=torch.uint8, device="cuda")
+        step_off = torch.empty(p.k_max + 1, dtype=torch.int64, device="cuda")
+        pst = vp.new_status()
+        vp.pack_heads(torch.from_numpy(act).cuda(), stride, hl_d, hb, self_rank, sched, send, step_off, pst)
         torch.cuda.synchronize()
         assert vp.read_status(pst) == 0, name
         assert torch.equal(send[:ref.size].cpu(), torch.from_numpy(ref)), name
