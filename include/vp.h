@@ -289,7 +289,9 @@ size_t vp_plan_workspace(const vp_catalog* cat, const vp_plan_params* p);
  * k_max * N * 8 reaches 2^32 (one matrix's schedule arrays are addressed with
  * 32-bit byte offsets), when the catalog exceeds the kernel's index widths
  * (more than 4095 shapes of either kind, 255 node shifts, 256 node-local
- * instances, 8 switches per node or 4 GPUs per switch), and when the planner's
+ * instances, 512 rank groups, 8 switches per node or 4 GPUs per switch, or a
+ * pattern with more intra-node lane classes or NIC lanes than its term
+ * tables hold), and when the planner's
  * per-catalog state (shape terms, family lane maps, node aggregates) plus one
  * family's working set does not fit in one workgroup's LDS (160 KiB on gfx950):
  * two-socket nodes of two switches of three GPUs with cross-socket peer to
