@@ -583,7 +583,7 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build's hot path is the per-rank demand -> plan -> "
+        print("bench.py measures one GPU only: the hot path is the per-rank demand -> plan -> "
               "pack work, which runs on a single MI355X; run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 

@@ -48,7 +48,7 @@ typedef enum {
   VP_ERR_INVALID_DEMAND = 2,   /* D_ij < 0, D_ii != 0, or D_ij not a multiple of the unit */
   VP_ERR_NO_PROGRESS = 3,      /* an iteration of Alg. 2 could serve no byte */
   VP_ERR_CAPACITY = 4,         /* schedule longer than k_max, or send buffer too small */
-  VP_ERR_UNSUPPORTED = 5,      /* shape outside this build's limits (see each call) */
+  VP_ERR_UNSUPPORTED = 5,      /* shape outside the library's limits (see each call) */
   VP_ERR_HIP = 6               /* a HIP runtime call failed */
 } vp_status;
 
@@ -75,7 +75,7 @@ enum { VP_TOPO_SYS_P2P = 1 };
  * keeps the one with the smallest instance ids).  Rates are in bytes per
  * nanosecond; a NIC path runs at min(pcie, nic), PIX, PXB and SYS paths at
  * the PCIe rate.
- * Limits of this build: gpus_per_switch in [2, 4], sockets*switches <= 8,
+ * Limits of the library: gpus_per_switch in [2, 4], sockets*switches <= 8,
  * nics_per_switch in [1, 4] with 2*Q*(1 + nics) (+ sockets^2 with SYS) <= 64
  * for Q = sockets*switches, at most 256 node-local path instances, n_nodes
  * in [1, 256], N <= 1024.  vp_rotation_time takes one NIC per switch. */
