@@ -184,3 +184,46 @@ def test_random_heads_path_parity(vp, i):
         assert torch.equal(send[:ref.size].cpu(), torch.from_numpy(ref)), name
         assert (send[ref.size:] == 0xA5).all(), name + ": wrote past the packed bytes"
         assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off), name
+
+
+@pytest.mark.parametrize("k", [64, 65, 255])
+def test_many_slots_path_parity(vp, k):
+    """Top-k at and beyond one wavefront's worth of routing slots, up to the
+    largest k the demand takes (255): the sort's slot bytes, and the scatter's
+    path that keeps routing order for more than 64 slots, against the
+    oracle."""
+    topo = vpgen.Topology(1, 2, 2, 2)
+    N, E, T, row = 8, 512, 37, 272
+    self_rank = 3
+    log("many slots k=%d" % k)
+    gc, oc = catalogs(vp, topo)
+    R = vpgen.random_routing(100 + k, N, T, E, k, 0.8)
+    dem = [oracle.demand(R[r], N, E, r, row) for r in range(N)]
+    D = np.stack([d["row"] for d in dem])
+    od = dem[self_rank]
+    gd = vp.demand(torch.from_numpy(R).cuda(), N, E, row, sort_row=self_rank)
+    p = vp.plan_params(N, row)
+    st = vp.new_status()
+    s = vp.plan(gc, gd["demand"], p, status=st, out=vp.alloc_schedule(N, p.k_max, layout=True))
+    torch.cuda.synchronize()
+    assert vp.read_status(gd["status"]) == 0 == vp.read_status(st)
+    assert np.array_equal(gd["demand"].cpu().numpy(), D)
+    assert np.array_equal(gd["sorted_tok"][:T * k].cpu().numpy(), od["sorted_tok"])
+    assert np.array_equal(gd["sorted_slot"][:T * k].cpu().numpy(), od["sorted_slot"])
+    o = oc.plan(D, row)
+    h = vp.schedule_to_host(s)
+    assert (h["K"], h["tau"]) == (o["K"], o["tau"])
+    for key in ("family", "dst", "inst", "bytes"):
+        assert np.array_equal(np.asarray(h[key]), np.asarray(o[key])), key
+    tok = np.random.default_rng(k).integers(0, 256, (T, row), dtype=np.uint8)
+    ref, ref_off = oracle.pack_rows(tok, row, od["sorted_tok"], od["dest_off"], self_rank, o)
+    send = torch.full((ref.size + 64,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(p.k_max + 1, dtype=torch.int64, device="cuda")
+    pst = vp.new_status()
+    vp.pack_rows(torch.from_numpy(tok).cuda(), row, gd["sorted_tok"], gd["sorted_slot"], gd["dest_off"],
+                 self_rank, s, send, step_off, pst)
+    torch.cuda.synchronize()
+    assert vp.read_status(pst) == 0
+    assert torch.equal(send[:ref.size].cpu(), torch.from_numpy(ref))
+    assert (send[ref.size:] == 0xA5).all()
+    assert np.array_equal(step_off[:o["K"] + 1].cpu().numpy(), ref_off)
