@@ -227,3 +227,61 @@ def test_many_slots_path_parity(vp, k):
     assert torch.equal(send[:ref.size].cpu(), torch.from_numpy(ref))
     assert (send[ref.size:] == 0xA5).all()
     assert np.array_equal(step_off[:o["K"] + 1].cpu().numpy(), ref_off)
+
+
+def test_pack_at_1024_ranks(vp):
+    """The largest rank count the library takes: demand of all 1,024 ranks
+    (one expert each, top-8 over 256 tokens) against the oracle, a GPU plan
+    checked for validity (sums to D, every step a derangement sharing no
+    modeled resource, Eq. (1); its exactness at this size is pinned by the
+    1,024-rank digest test), and rank 777's pack with the planner's layout
+    against the oracle's pack of that same schedule."""
+    from oracle.checks import TopoModel, schedule_valid_np
+    topo = vpgen.Topology(128)
+    N, E, T, k, row, self_rank = 1024, 1024, 256, 8, 1024, 777
+    log("pack at 1024 ranks")
+    R = vpgen.random_routing(1024, N, T, E, k, 0.5)
+    dem = [oracle.demand(R[r], N, E, r, row) for r in range(N)]
+    D = np.stack([d["row"] for d in dem])
+    od = dem[self_rank]
+    gc, _ = catalogs_gpu_only(vp, topo)
+    gd = vp.demand(torch.from_numpy(R).cuda(), N, E, row, sort_row=self_rank)
+    p = vp.plan_params(N, row, k_max=16 * N)
+    st = vp.new_status()
+    s = vp.plan(gc, gd["demand"], p, status=st, out=vp.alloc_schedule(N, p.k_max, layout=True))
+    torch.cuda.synchronize()
+    assert vp.read_status(gd["status"]) == 0 == vp.read_status(st)
+    assert np.array_equal(gd["demand"].cpu().numpy(), D)
+    assert np.array_equal(gd["sorted_tok"][:T * k].cpu().numpy(), od["sorted_tok"])
+    assert np.array_equal(gd["dest_off"].cpu().numpy(), od["dest_off"])
+    h = vp.schedule_to_host(s)
+    K = h["K"]
+    log("1024 ranks: K = %d" % K)
+    rows = np.arange(N)
+    X = np.zeros((N, N), np.int64)
+    np.add.at(X, (np.broadcast_to(rows, (K, N)), h["dst"]), h["bytes"])
+    assert np.array_equal(X, D)
+    schedule_valid_np(TopoModel(topo), D, h["dst"], gc.instances()["cls"][h["inst"]], h["bytes"])
+    tok = np.random.default_rng(777).integers(0, 256, (T, row), dtype=np.uint8)
+    ref, ref_off = oracle.pack_rows(tok, row, od["sorted_tok"], od["dest_off"], self_rank, h)
+    send = torch.full((ref.size + 64,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(p.k_max + 1, dtype=torch.int64, device="cuda")
+    pst = vp.new_status()
+    vp.pack_rows(torch.from_numpy(tok).cuda(), row, gd["sorted_tok"], gd["sorted_slot"], gd["dest_off"],
+                 self_rank, s, send, step_off, pst)
+    torch.cuda.synchronize()
+    assert vp.read_status(pst) == 0
+    assert torch.equal(send[:ref.size].cpu(), torch.from_numpy(ref))
+    assert (send[ref.size:] == 0xA5).all()
+    assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off)
+
+
+def catalogs_gpu_only(vp, topo):
+    """The library's catalog alone (the oracle's is not needed, and takes
+    long to enumerate at 128 nodes)."""
+    key = ("gpu",) + topo.as_tuple()
+    if key not in _cat:
+        c = vp.Catalog(topo)
+        c.upload()
+        _cat[key] = (c, None)
+    return _cat[key]
