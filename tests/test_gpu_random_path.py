@@ -285,3 +285,47 @@ def catalogs_gpu_only(vp, topo):
         c.upload()
         _cat[key] = (c, None)
     return _cat[key]
+
+
+def test_heads_pack_at_1024_ranks(vp):
+    """Head/context re-layout on 1,024 ranks (an uneven split of 2,500 heads
+    of 64 B, some ranks owning none): demand against the oracle, a validated
+    GPU plan, and rank 5's head pack (the prepare-and-gather pair: more steps
+    than the one-kernel pack takes) against the oracle's pack of that
+    schedule."""
+    from oracle.checks import TopoModel, schedule_valid_np
+    topo = vpgen.Topology(128)
+    N, H, hb, T, self_rank = 1024, 2500, 64, 48, 5
+    r = np.random.default_rng(2500)
+    hl = np.concatenate([[0], np.sort(r.integers(0, H + 1, N - 1)), [H]]).astype(np.int64)
+    stride = H * hb + 32
+    log("heads pack at 1024 ranks")
+    D = np.stack([oracle.demand_heads(T, hl, hb, i) for i in range(N)])
+    gc, _ = catalogs_gpu_only(vp, topo)
+    hl_d = torch.from_numpy(hl).cuda()
+    gD = vp.demand_heads(T, hl_d, hb, first_rank=0, R=N)
+    p = vp.plan_params(N, hb)
+    st = vp.new_status()
+    s = vp.plan(gc, gD, p, status=st, out=vp.alloc_schedule(N, p.k_max, layout=True))
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    assert np.array_equal(gD.cpu().numpy(), D)
+    h = vp.schedule_to_host(s)
+    K = h["K"]
+    log("1024 ranks heads: K = %d" % K)
+    rows = np.arange(N)
+    X = np.zeros((N, N), np.int64)
+    np.add.at(X, (np.broadcast_to(rows, (K, N)), h["dst"]), h["bytes"])
+    assert np.array_equal(X, D)
+    schedule_valid_np(TopoModel(topo), D, h["dst"], gc.instances()["cls"][h["inst"]], h["bytes"])
+    act = np.random.default_rng(5).integers(0, 256, (T, stride), dtype=np.uint8)
+    ref, ref_off = oracle.pack_heads(act, stride, hl, hb, self_rank, h)
+    send = torch.full((ref.size + 64,), 0xA5, dtype=torch.uint8, device="cuda")
+    step_off = torch.empty(p.k_max + 1, dtype=torch.int64, device="cuda")
+    pst = vp.new_status()
+    vp.pack_heads(torch.from_numpy(act).cuda(), stride, hl_d, hb, self_rank, s, send, step_off, pst)
+    torch.cuda.synchronize()
+    assert vp.read_status(pst) == 0
+    assert torch.equal(send[:ref.size].cpu(), torch.from_numpy(ref))
+    assert (send[ref.size:] == 0xA5).all()
+    assert np.array_equal(step_off[:K + 1].cpu().numpy(), ref_off)
