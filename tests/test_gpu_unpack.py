@@ -4,7 +4,8 @@ vp_unpack_rows, vp_pack_combine and vp_unpack_combine are compared byte for
 byte with the oracle's functions on the same inputs: at full size with the
 oracle's schedule uploaded and random buffer contents, and end to end (GPU
 demand, plan, pack of every rank, a transfer emulated in the test, unpack,
-then the combine back) against the oracle's own pipeline.  Error cases:
+then the combine back) against the oracle's own pipeline, for the named
+workloads and for seeded random shapes.  Error cases:
 an inconsistent receive view, buffers too small, a schedule that leaves a
 stream incomplete, and the empty schedule."""
 import sys
@@ -315,6 +316,99 @@ def test_dispatch_and_combine_round_trip(vp, cid, tokens, row_bytes):
         remote = (R[i] // eloc) != i
         want = np.broadcast_to(tok[i][:, None, :], (T, k, rb))
         assert (c[remote] == want[remote]).all()
+
+
+RANDOM_TRIPS = [  # (topology, experts per rank, tokens, top-k, row bytes, routing skew)
+    (vpgen.Topology(1, 2, 2, 2), 3, 333, 5, 1040, 1.2),
+    (vpgen.Topology(2, 1, 2, 2, 2), 2, 65, 3, 16, 0.0),
+    (vpgen.Topology(1, 1, 2, 3), 4, 1000, 8, 272, 2.0),
+    (vpgen.Topology(2, 2, 2, 2, 1, 32, 25, 1), 1, 129, 1, 4112, 0.6),
+    (vpgen.Topology(1, 1, 1, 2), 8, 7, 8, 48, 1.0),
+]
+
+
+@pytest.mark.parametrize("i", range(len(RANDOM_TRIPS)))
+def test_random_round_trip(vp, i):
+    """Dispatch and combine on seeded random shapes (odd row sizes, top-1 to
+    top-8, SYS nodes, two NICs per switch): GPU demand -> plan -> pack of
+    every rank -> emulated transfer -> unpack, then the transposed plan ->
+    combine pack -> transfer -> combine unpack, against the oracle's
+    pipeline on the oracle's schedules (which the GPU's equal)."""
+    topo, L, T, k, rb, zipf = RANDOM_TRIPS[i]
+    N = topo.n_ranks
+    E = N * L
+    sb = oracle.slot_bytes(rb)
+    log("random round trip %d: topo %s E=%d T=%d k=%d row %d" % (i, topo.as_tuple(), E, T, k, rb))
+    R = vpgen.random_routing(300 + i, N, T, E, k, zipf)
+    dem = [oracle.demand(R[r], N, E, r, rb) for r in range(N)]
+    D = np.stack([d["row"] for d in dem])
+    counts = np.stack([d["counts"] for d in dem])
+    rng = np.random.default_rng(i)
+    tok = [rng.integers(0, 256, (T, rb), dtype=np.uint8) for _ in range(N)]
+    oc = _cache.setdefault(("ocat",) + topo.as_tuple(), oracle.Catalog(topo))
+    s_o, sc_o = oc.plan(D, rb), oc.plan(np.ascontiguousarray(D.T), rb)
+    packs = [oracle.pack_rows(tok[r], rb, dem[r]["sorted_tok"], dem[r]["dest_off"], r, s_o) for r in range(N)]
+    ref_out = [oracle.unpack_rows(oracle.receive(r, N, s_o, rb, [p[0] for p in packs], [p[1] for p in packs]),
+                                  r, N, s_o, rb, counts) for r in range(N)]
+    cpk = [oracle.pack_combine(ref_out[r], r, N, sc_o, rb, counts) for r in range(N)]
+    ref_comb = [oracle.unpack_combine(oracle.receive(j, N, sc_o, rb, [p[0] for p in cpk], [p[1] for p in cpk]),
+                                      j, N, sc_o, rb, T, k, dem[j]["sorted_tok"], dem[j]["sorted_slot"],
+                                      dem[j]["dest_off"]) for j in range(N)]
+
+    cat = gcat(vp, topo)
+    rt = torch.from_numpy(R).cuda()
+    st = vp.new_status()
+    dems = [vp.demand(rt, N, E, rb, sort_row=r, status=st) for r in range(N)]
+    D_dev, counts_dev = dems[0]["demand"], dems[0]["counts"]
+
+    def plan(Dd):
+        p = vp.plan_params(N, rb)
+        s = vp.plan(cat, Dd, p, out=vp.alloc_schedule(N, p.k_max, layout=True))
+        torch.cuda.synchronize()
+        assert vp.read_status(s["status"]) == 0
+        K = int(s["K"].item())
+        return s, s["dst"][:K].cpu().numpy(), s["bytes"][:K].cpu().numpy()
+
+    s, dst, nb = plan(D_dev)
+    assert np.array_equal(dst, s_o["dst"]) and np.array_equal(nb, s_o["bytes"])
+    sends, offs = [], []
+    for r in range(N):
+        total = int(D[r].sum())
+        send = torch.empty(max(total, 16), dtype=torch.uint8, device="cuda")
+        step_off = torch.empty(8 * N + 1, dtype=torch.int64, device="cuda")
+        vp.pack_rows(torch.from_numpy(tok[r]).cuda(), rb, dems[r]["sorted_tok"], dems[r]["sorted_slot"],
+                     dems[r]["dest_off"], r, s, send[:total], step_off, st)
+        sends.append(send)
+        offs.append(step_off.cpu().numpy())
+    outs = []
+    for r in range(N):
+        recv = emulate_transfer(sends, offs, dst, nb, r, rb, sb)
+        out = torch.zeros(max(expert_rows(counts, r, N), 1) * sb, dtype=torch.uint8, device="cuda")
+        vp.unpack_rows(recv, rb, counts_dev, r, s, out, st)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    for r in range(N):
+        assert torch.equal(outs[r], torch.from_numpy(ref_out[r]).cuda()), "unpack rank %d" % r
+
+    sc, cdst, cnb = plan(vp.demand_transpose(D_dev))
+    assert np.array_equal(cdst, sc_o["dst"]) and np.array_equal(cnb, sc_o["bytes"])
+    csends, coffs = [], []
+    for r in range(N):
+        total = int(D[:, r].sum())
+        send = torch.empty(max(total, 16), dtype=torch.uint8, device="cuda")
+        step_off = torch.empty(8 * N + 1, dtype=torch.int64, device="cuda")
+        vp.pack_combine(outs[r], rb, counts_dev, r, sc, send[:total], step_off, st)
+        csends.append(send)
+        coffs.append(step_off.cpu().numpy())
+    for j in range(N):
+        recv = emulate_transfer(csends, coffs, cdst, cnb, j, rb, sb)
+        comb = torch.zeros(T * k * sb, dtype=torch.uint8, device="cuda")
+        vp.unpack_combine(recv, rb, T, k, dems[j]["sorted_tok"], dems[j]["sorted_slot"], dems[j]["dest_off"], j,
+                          sc, comb, st)
+        torch.cuda.synchronize()
+        assert vp.read_status(st) == 0
+        assert torch.equal(comb, torch.from_numpy(ref_comb[j]).cuda()), "combine rank %d" % j
 
 
 # ------------------------------------------------------------ error paths
