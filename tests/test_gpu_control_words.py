@@ -105,3 +105,36 @@ def test_receive_counts_parity(vp, cid):
         torch.cuda.synchronize()
         assert np.array_equal(got1.cpu().numpy(), ref)
     assert vp.read_status(d["status"]) == 0
+
+
+@pytest.mark.parametrize("N,L,seed", [(3, 1, 0), (8, 2, 1), (7, 5, 2), (16, 16, 3), (5, 31, 4), (64, 4, 5)])
+def test_control_words_random(vp, N, L, seed):
+    """Random sparse counts for 1 to 31 local experts per rank, counts up to
+    the largest the 32 - L count bits hold: the words of every source, and
+    every receiver's decode of its column, against the oracle."""
+    rng = np.random.default_rng(seed)
+    E = N * L
+    limit = (1 << (32 - L)) - 1
+    counts = rng.integers(0, min(limit, 1 << 20) + 1, (N, E)).astype(np.int64)
+    counts[rng.random((N, E)) < 0.5] = 0
+    hot = rng.random((N, E)) < 0.05
+    counts[hot] = limit                                # the largest count a word carries
+    counts = counts.astype(np.int32)
+    log("control words random N=%d L=%d" % (N, L))
+    c = torch.from_numpy(counts).cuda()
+    st = vp.new_status()
+    words = vp.control_words(c, N, status=st)
+    torch.cuda.synchronize()
+    assert vp.read_status(st) == 0
+    ref = np.stack([oracle.control_words(counts[i], N, i) for i in range(N)])
+    assert np.array_equal(words_np(words), ref)
+    for r in range(N):
+        block = counts[:, r * L:(r + 1) * L]
+        signal = np.where(block > 0, block, rng.integers(1, 1000, block.shape)).astype(np.int32)
+        want = oracle.receive_counts(ref[:, r], signal, L)
+        got = vp.receive_counts(words, N, torch.from_numpy(signal).cuda(), L, offset=r)
+        torch.cuda.synchronize()
+        assert np.array_equal(got.cpu().numpy(), want), "receiver %d" % r
+        exp = block.copy()
+        exp[r] = 0                                     # no words to itself
+        assert np.array_equal(want, exp)
