@@ -1,7 +1,8 @@
 """vp_plan_batch: several matrices planned side by side, one workgroup
 each, must give every matrix the schedule the oracle gives it (through the
-stored stream digests, and element by element for a dispatch matrix D and
-its combine matrix D^T); a bad matrix fails alone."""
+stored stream digests, element by element for a dispatch matrix D and its
+combine matrix D^T, and for batches of random matrices with their buffer
+layout); a bad matrix fails alone."""
 import json
 import sys
 
@@ -169,3 +170,52 @@ def test_pipelines_on_concurrent_streams(vp):
             assert torch.equal(pipe.sched["bytes"][:K], ref["bytes"]), cid
             assert torch.equal(pipe.step_off[:K + 1], ref["step_off"]), cid
             assert torch.equal(pipe.send[:ref["send"].numel()], ref["send"]), cid
+
+
+@pytest.mark.parametrize("topo", [vpgen.Topology(2, 2, 2, 2), vpgen.Topology(2, 1, 2, 2, 2),
+                                  vpgen.Topology(2, 2, 2, 2, 1, 32, 25, 1), vpgen.Topology(3, 1, 2, 3)])
+def test_batch_of_random_demands(vp, topo):
+    """Twelve random matrices of mixed density and scale (an all-zero one
+    among them) in one launch, with the buffer layout: every matrix's
+    schedule, step offsets and receive view equal what the oracle's
+    schedule gives, element by element."""
+    N, unit, B = topo.n_ranks, 4096, 12
+    rng = np.random.default_rng(N + topo.flags + 7 * topo.nics_per_switch)
+    Ds = []
+    for b in range(B):
+        dens, scale = [(0.05, 3), (0.3, 20), (1.0, 50), (0.6, 1)][b % 4]
+        D = rng.integers(0, scale + 1, (N, N)) * (rng.random((N, N)) < dens)
+        np.fill_diagonal(D, 0)
+        Ds.append((D * unit).astype(np.int64))
+    Ds[5][:] = 0
+    log("batch of random demands topo %s" % (topo.as_tuple(),))
+    cat = vp.Catalog(topo)
+    cat.upload()
+    oc = oracle.Catalog(topo)
+    p = vp.plan_params(N, unit, k_max=64 * N)
+    out = vp.alloc_schedule_batch(B, N, p.k_max, layout=True)
+    s = vp.plan_batch(cat, torch.from_numpy(np.stack(Ds)).cuda(), p, out=out)
+    torch.cuda.synchronize()
+    assert (s["status"].cpu().numpy() == 0).all()
+    for b in range(B):
+        o = oc.plan(Ds[b], unit, k_max=64 * N)
+        g = host(s, b)
+        assert (g["K"], g["tau"]) == (o["K"], o["tau"]), b
+        for key in ("family", "dst", "inst", "bytes"):
+            assert np.array_equal(g[key], o[key]), (b, key)
+        K = o["K"]
+        if K:
+            # send offsets: running sums of each rank's lanes; stream offsets: bytes
+            # of the same pair before the step; receive view: the inverse of dst
+            nb, dst = o["bytes"], o["dst"]
+            want_so = np.cumsum(nb, axis=0) - nb
+            assert np.array_equal(s["send_off"][b, :K].cpu().numpy(), want_so), b
+            co = np.zeros((K, N), np.int64)
+            seen = np.zeros((N, N), np.int64)
+            for k in range(K):
+                co[k] = seen[np.arange(N), dst[k]]
+                seen[np.arange(N), dst[k]] += nb[k]
+            assert np.array_equal(s["stream_off"][b, :K].cpu().numpy(), co), b
+            rs = np.zeros((K, N), np.int32)
+            rs[np.arange(K)[:, None], dst] = np.arange(N, dtype=np.int32)[None, :]
+            assert np.array_equal(s["recv_src"][b, :K].cpu().numpy(), rs), b
